@@ -1,0 +1,334 @@
+/*
+ * ckm_ref.c -- CPU oracle (test infrastructure only; see ckm_ref.h).
+ *
+ * Plain C99, single thread, no blocking, fusion or reordering beyond what the
+ * definitions state. Each function names the passage of the paper it follows.
+ */
+#include "ckm_ref.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* Philox4x32-10 (Salmon et al., "Parallel random numbers: as easy as 1, 2,
+ * 3", SC'11). Round: two 32x32->64 products of counter words 0 and 2 with
+ * the multipliers; the new counter is (hi1 ^ c1 ^ k0, lo1, hi0 ^ c3 ^ k1,
+ * lo0); the key is advanced by the Weyl constants between rounds. */
+#define PHILOX_M0 0xD2511F53u
+#define PHILOX_M1 0xCD9E8D57u
+#define PHILOX_W0 0x9E3779B9u
+#define PHILOX_W1 0xBB67AE85u
+
+void ckm_ref_philox4x32_10(const uint32_t key[2], const uint32_t ctr[4], uint32_t out[4]) {
+  uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+  uint32_t k0 = key[0], k1 = key[1];
+  int r;
+  for (r = 0; r < 10; ++r) {
+    uint64_t p0, p1;
+    uint32_t n0, n1, n2, n3;
+    if (r > 0) {
+      k0 += PHILOX_W0;
+      k1 += PHILOX_W1;
+    }
+    p0 = (uint64_t)PHILOX_M0 * (uint64_t)c0;
+    p1 = (uint64_t)PHILOX_M1 * (uint64_t)c2;
+    n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+    n1 = (uint32_t)p1;
+    n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+    n3 = (uint32_t)p0;
+    c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+  }
+  out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+uint32_t ckm_ref_draw(uint64_t seed, uint32_t k, uint32_t t, uint32_t i) {
+  uint32_t key[2], ctr[4], x[4];
+  uint32_t j = i % 8u;
+  key[0] = (uint32_t)(seed & 0xFFFFFFFFu);
+  key[1] = (uint32_t)(seed >> 32);
+  ctr[0] = i / 8u;
+  ctr[1] = t;
+  ctr[2] = k;
+  ctr[3] = 0u;
+  ckm_ref_philox4x32_10(key, ctr, x);
+  return (x[j / 2u] >> (16u * (j % 2u))) & 0xFFFFu;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Section 4.1: a DAG whose nodes are numbered topologically, with per-node
+ * output size M_v and compute cost C_v. */
+int ckm_ref_validate_graph(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
+                           const int64_t* cost, const int64_t* size,
+                           int64_t m_input, int64_t m_param) {
+  int32_t j, a, b;
+  int64_t total_m, total_c;
+  if (n < 1 || !dep_ptr || !cost || !size) return CKM_REF_E_INVALID_ARG;
+  if (dep_ptr[0] != 0) return CKM_REF_E_GRAPH;
+  for (j = 0; j < n; ++j)
+    if (dep_ptr[j + 1] < dep_ptr[j]) return CKM_REF_E_GRAPH;
+  if (dep_ptr[n] > 0 && !dep_idx) return CKM_REF_E_INVALID_ARG;
+  for (j = 0; j < n; ++j) {
+    for (a = dep_ptr[j]; a < dep_ptr[j + 1]; ++a) {
+      int32_t i = dep_idx[a];
+      if (i < 0 || i >= j) return CKM_REF_E_GRAPH;            /* not topological */
+      for (b = dep_ptr[j]; b < a; ++b)
+        if (dep_idx[b] == i) return CKM_REF_E_GRAPH;          /* duplicate edge */
+    }
+  }
+  if (m_input < 0 || m_param < 0) return CKM_REF_E_INVALID_ARG;
+  for (j = 0; j < n; ++j)
+    if (cost[j] < 0 || size[j] < 0) return CKM_REF_E_INVALID_ARG;
+  /* M_in + 2 M_param + sum M must fit in int64 */
+  total_m = m_input;
+  if (m_param > INT64_MAX - total_m) return CKM_REF_E_OVERFLOW;
+  total_m += m_param;
+  if (m_param > INT64_MAX - total_m) return CKM_REF_E_OVERFLOW;
+  total_m += m_param;
+  for (j = 0; j < n; ++j) {
+    if (size[j] > INT64_MAX - total_m) return CKM_REF_E_OVERFLOW;
+    total_m += size[j];
+  }
+  /* n * sum C must fit in int64 (every stage may compute every node) */
+  total_c = 0;
+  for (j = 0; j < n; ++j) {
+    if (cost[j] > INT64_MAX - total_c) return CKM_REF_E_OVERFLOW;
+    total_c += cost[j];
+  }
+  if (total_c > 0 && (int64_t)n > INT64_MAX / total_c) return CKM_REF_E_OVERFLOW;
+  return CKM_REF_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Section 5.1: randomized rounding takes x_int = 1 with probability x*. The
+ * probability is quantized to 16 bits: q = floor(x* * 2^16), so that
+ * Pr[u < q] = q / 2^16 lies in (x* - 2^-16, x*]. */
+int ckm_ref_quantize(int32_t n, const double* s_frac, int64_t ld, uint32_t* q) {
+  int32_t t, i;
+  for (t = 0; t < n; ++t) {
+    for (i = 0; i < n; ++i) {
+      uint32_t v = 0;
+      if (i < t) {
+        double x = s_frac[(int64_t)t * ld + i];
+        if (isnan(x)) return CKM_REF_E_INVALID_ARG;
+        if (x < 0.0) x = 0.0;
+        if (x > 1.0) x = 1.0;
+        v = (uint32_t)floor(x * 65536.0);
+      }
+      q[(int64_t)t * n + i] = v;
+    }
+  }
+  return CKM_REF_OK;
+}
+
+void ckm_ref_round_random(int32_t n, const uint32_t* q, uint64_t seed, uint32_t k, uint8_t* S) {
+  int32_t t, i;
+  for (t = 0; t < n; ++t)
+    for (i = 0; i < n; ++i) {
+      uint8_t s = 0;
+      if (i < t) s = ckm_ref_draw(seed, k, (uint32_t)t, (uint32_t)i) < q[(int64_t)t * n + i];
+      S[(int64_t)t * n + i] = s;
+    }
+}
+
+/* Algorithm 2, first line: deterministic rounding S_int = 1[S* > 0.5]. */
+void ckm_ref_round_det(int32_t n, const double* s_frac, int64_t ld, uint8_t* S) {
+  int32_t t, i;
+  for (t = 0; t < n; ++t)
+    for (i = 0; i < n; ++i)
+      S[(int64_t)t * n + i] = (i < t) && (s_frac[(int64_t)t * ld + i] > 0.5);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Algorithm 2 (two-phase rounding), given S_int:
+ *   R <- I (constraint 4a: node t is computed in stage t);
+ *   while constraint (1c) S[t][i] <= R[t-1][i] + S[t-1][i] is violated for
+ *     some t >= 1: compute v_i in the previous stage, R[t-1][i] <- 1;
+ *   while constraint (1b) R[t][j] <= R[t][i] + S[t][i] is violated for some
+ *     edge (i, j): compute v_i as a temporary, R[t][i] <- 1.
+ * Section 5.2 scans each stage right to left (reverse topological order);
+ * the loops below repeat full sweeps until no violation remains. */
+void ckm_ref_solve_R(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
+                     const uint8_t* S, uint8_t* R) {
+  int32_t t, i, j, a;
+  int changed;
+  memset(R, 0, (size_t)n * (size_t)n);
+  for (t = 0; t < n; ++t) R[(int64_t)t * n + t] = 1;
+
+  do {  /* constraint (1c) */
+    changed = 0;
+    for (t = 1; t < n; ++t)
+      for (i = 0; i < n; ++i)
+        if (S[(int64_t)t * n + i] > R[(int64_t)(t - 1) * n + i] + S[(int64_t)(t - 1) * n + i]) {
+          R[(int64_t)(t - 1) * n + i] = 1;
+          changed = 1;
+        }
+  } while (changed);
+
+  do {  /* constraint (1b) */
+    changed = 0;
+    for (t = 0; t < n; ++t)
+      for (j = n - 1; j >= 0; --j)
+        for (a = dep_ptr[j]; a < dep_ptr[j + 1]; ++a) {
+          i = dep_idx[a];
+          if (R[(int64_t)t * n + j] > R[(int64_t)t * n + i] + S[(int64_t)t * n + i]) {
+            R[(int64_t)t * n + i] = 1;
+            changed = 1;
+          }
+        }
+  } while (changed);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Section 4.4. Memory in use at the start of stage t (eq. U_init):
+ *   U_{t,0} = M_in + 2 M_param + sum_i M_i S[t][i];
+ * after computing v_k (eq. mem_recurrence): U_{t,k} = U_{t,k-1} - freed(k-1)
+ *   + R[t][k] M_k, where freed(k) = sum over i in Deps[k] u {k} of
+ *   M_i FREE(t,i,k) (eq. GC) and
+ *   FREE(t,i,k) = R[t][k] (1 - S[t+1][i]) prod_{j in Users[i], j > k} (1 - R[t][j])
+ *   (eq. collectable). The i = k term is kept (it is only dropped from the
+ *   ILP as implied by optimality, Section 4.8).
+ * The objective of Section 4.3 gives the cost: sum_t sum_i C_i R[t][i]. */
+void ckm_ref_simulate(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
+                      const int64_t* cost, const int64_t* size, int64_t m_input, int64_t m_param,
+                      const uint8_t* S, const uint8_t* R, int64_t* peak, int64_t* total_cost,
+                      int64_t* stage_peak, int32_t* max_frees, int64_t* U_end) {
+  int32_t t, i, k, a, b, j;
+  int32_t E = dep_ptr[n];
+  int32_t* user_ptr = (int32_t*)calloc((size_t)n + 1, sizeof(int32_t));
+  int32_t* user_idx = (int32_t*)malloc((size_t)(E > 0 ? E : 1) * sizeof(int32_t));
+  int32_t* fill = (int32_t*)calloc((size_t)n, sizeof(int32_t));
+  int32_t* free_count = (int32_t*)calloc((size_t)n, sizeof(int32_t));
+  int64_t best = INT64_MIN, csum = 0;
+  int32_t worst_frees = 0;
+
+  /* Users[i] = { j : (v_i, v_j) in E } (transpose of Deps) */
+  for (j = 0; j < n; ++j)
+    for (a = dep_ptr[j]; a < dep_ptr[j + 1]; ++a) user_ptr[dep_idx[a] + 1]++;
+  for (i = 0; i < n; ++i) user_ptr[i + 1] += user_ptr[i];
+  for (j = 0; j < n; ++j)
+    for (a = dep_ptr[j]; a < dep_ptr[j + 1]; ++a) {
+      i = dep_idx[a];
+      user_idx[user_ptr[i] + fill[i]++] = j;
+    }
+
+  for (t = 0; t < n; ++t) {
+    const uint8_t* St = S + (int64_t)t * n;
+    const uint8_t* Rt = R + (int64_t)t * n;
+    const uint8_t* Snext = (t + 1 < n) ? S + (int64_t)(t + 1) * n : NULL;  /* S[n] = 0 */
+    int64_t U = m_input + 2 * m_param;
+    int64_t speak = INT64_MIN;
+    for (i = 0; i < n; ++i) U += size[i] * (int64_t)St[i];
+    memset(free_count, 0, (size_t)n * sizeof(int32_t));
+    for (k = 0; k < n; ++k) {
+      int64_t freed = 0;
+      int32_t m;
+      U += (int64_t)Rt[k] * size[k];
+      if (U > speak) speak = U;
+      /* i ranges over Deps[k] u {k}; m = 0 .. deg(k)-1 are the deps, m = deg(k) is k */
+      for (m = 0; m <= dep_ptr[k + 1] - dep_ptr[k]; ++m) {
+        int64_t FREE;
+        i = (m < dep_ptr[k + 1] - dep_ptr[k]) ? dep_idx[dep_ptr[k] + m] : k;
+        FREE = (int64_t)Rt[k] * (1 - (int64_t)(Snext ? Snext[i] : 0));
+        for (b = user_ptr[i]; b < user_ptr[i + 1]; ++b) {
+          j = user_idx[b];
+          if (j > k) FREE *= (1 - (int64_t)Rt[j]);
+        }
+        freed += size[i] * FREE;
+        free_count[i] += (int32_t)FREE;
+      }
+      U -= freed;
+    }
+    for (i = 0; i < n; ++i) {
+      csum += cost[i] * (int64_t)Rt[i];
+      if (free_count[i] > worst_frees) worst_frees = free_count[i];
+    }
+    if (stage_peak) stage_peak[t] = speak;
+    if (U_end) U_end[t] = U;
+    if (speak > best) best = speak;
+  }
+  *peak = best;
+  *total_cost = csum;
+  if (max_frees) *max_frees = worst_frees;
+  free(user_ptr);
+  free(user_idx);
+  free(fill);
+  free(free_count);
+}
+
+/* ------------------------------------------------------------------------ */
+int ckm_ref_eval_candidate(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
+                           const int64_t* cost, const int64_t* size, int64_t m_input,
+                           int64_t m_param, const double* s_frac, int64_t ld, const uint32_t* q,
+                           uint64_t seed, uint32_t k, uint32_t flags, int64_t* peak,
+                           int64_t* total_cost, uint8_t* S_out, uint8_t* R_out) {
+  size_t nn = (size_t)n * (size_t)n;
+  uint8_t* S = S_out ? S_out : (uint8_t*)malloc(nn);
+  uint8_t* R = R_out ? R_out : (uint8_t*)malloc(nn);
+  if (!S || !R) return CKM_REF_E_INVALID_ARG;
+  if (k == 0 && (flags & CKM_REF_F_DET0))
+    ckm_ref_round_det(n, s_frac, ld, S);
+  else
+    ckm_ref_round_random(n, q, seed, k, S);
+  ckm_ref_solve_R(n, dep_ptr, dep_idx, S, R);
+  ckm_ref_simulate(n, dep_ptr, dep_idx, cost, size, m_input, m_param, S, R, peak, total_cost,
+                   NULL, NULL, NULL);
+  if (!S_out) free(S);
+  if (!R_out) free(R);
+  return CKM_REF_OK;
+}
+
+static void pack_rows(int32_t n, const uint8_t* X, uint64_t* out) {
+  int32_t W = (n + 63) / 64, t, i;
+  memset(out, 0, (size_t)n * (size_t)W * sizeof(uint64_t));
+  for (t = 0; t < n; ++t)
+    for (i = 0; i < n; ++i)
+      if (X[(int64_t)t * n + i]) out[(int64_t)t * W + i / 64] |= (uint64_t)1 << (i % 64);
+}
+
+int ckm_ref_round_eval(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
+                       const int64_t* cost, const int64_t* size, int64_t m_input, int64_t m_param,
+                       const double* s_frac, int64_t ld, int32_t K, uint64_t seed, int64_t budget,
+                       uint32_t flags, int64_t* peak, int64_t* total_cost, uint8_t* feasible,
+                       int32_t* best_k, uint64_t* best_S, uint64_t* best_R) {
+  int st;
+  int32_t k, bk = -1;
+  uint32_t* q;
+  size_t nn = (size_t)n * (size_t)n;
+  if (K < 1 || !s_frac || ld < n || budget < 0 || !peak || !total_cost || !feasible || !best_k)
+    return CKM_REF_E_INVALID_ARG;
+  st = ckm_ref_validate_graph(n, dep_ptr, dep_idx, cost, size, m_input, m_param);
+  if (st != CKM_REF_OK) return st;
+  q = (uint32_t*)malloc(nn * sizeof(uint32_t));
+  st = ckm_ref_quantize(n, s_frac, ld, q);
+  if (st != CKM_REF_OK) { free(q); return st; }
+  for (k = 0; k < K; ++k) {
+    ckm_ref_eval_candidate(n, dep_ptr, dep_idx, cost, size, m_input, m_param, s_frac, ld, q, seed,
+                           (uint32_t)k, flags, &peak[k], &total_cost[k], NULL, NULL);
+    feasible[k] = peak[k] <= budget;
+    /* best = lexicographic minimum of (cost, peak, k) over feasible k */
+    if (feasible[k] && (bk < 0 || total_cost[k] < total_cost[bk] ||
+                        (total_cost[k] == total_cost[bk] && peak[k] < peak[bk])))
+      bk = k;
+  }
+  *best_k = bk;
+  if (best_S || best_R) {
+    int32_t W = (n + 63) / 64;
+    if (bk >= 0) {
+      uint8_t* S = (uint8_t*)malloc(nn);
+      uint8_t* R = (uint8_t*)malloc(nn);
+      int64_t p, c;
+      ckm_ref_eval_candidate(n, dep_ptr, dep_idx, cost, size, m_input, m_param, s_frac, ld, q,
+                             seed, (uint32_t)bk, flags, &p, &c, S, R);
+      if (best_S) pack_rows(n, S, best_S);
+      if (best_R) pack_rows(n, R, best_R);
+      free(S);
+      free(R);
+    } else {
+      if (best_S) memset(best_S, 0, (size_t)n * (size_t)W * sizeof(uint64_t));
+      if (best_R) memset(best_R, 0, (size_t)n * (size_t)W * sizeof(uint64_t));
+    }
+  }
+  free(q);
+  return CKM_REF_OK;
+}
