@@ -1,0 +1,160 @@
+"""Throughput of batched candidate-schedule evaluation on one MI355X.
+
+A step is one pass of the whole path over the transformer-stack workload
+(n = 1009 nodes, K = 1024 candidates, 25 % budget): thresholds from S*,
+rounding + Algorithm 2 repair + memory/cost simulation of every candidate,
+per-candidate reduction, argmin, and the best candidate's S and R rows.
+The graph and S* are resident in HBM before timing starts.
+
+Prints one JSON line. `value` is candidate schedules evaluated per second.
+`roofline` prices the dominant kernel (the evaluate kernel) against HBM
+bandwidth with the algorithmic bytes of bit-packed S and R rows, each
+written once and read once: 4 * n * ceil(n/64) * 8 bytes per candidate.
+`cpu_baseline` times the CPU oracle on a bounded sample of the same
+workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "candidate schedules evaluated/sec at n=1000,K=1024; % HBM roofline"
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_eval_transformer_n1009_K1024.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_1910_02653_amd", "csrc", "ckm_kernels.hip")
+
+
+def kernel_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per evaluate launch from committed rocprofv3 counters, if they
+    were taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            d = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if d.get("kernel_sha256_16") != kernel_hash():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, sample: int):
+    """The oracle, single thread, on candidates 0 .. sample-1 of the workload."""
+    from oracle import ref
+    q = ref.quantize(w.s_frac)
+    t = time.perf_counter()
+    for k in range(sample):
+        ref.eval_candidate(w, k, q=q)
+    dt = time.perf_counter() - t
+    return {"value": sample / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
+            "sample": "candidates 0-%d of the same %d-candidate transformer workload (n=%d): "
+                      "rounding + Algorithm 2 repair + literal U/FREE simulation per candidate, "
+                      "one thread, %.1f s" % (sample - 1, w.K, w.n, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=4, help="workload 1..5 (4 = transformer stack)")
+    ap.add_argument("--splits", type=int, default=0, help="stage splits per 64 candidates (0 = auto)")
+    ap.add_argument("--cpu-sample", type=int, default=256, help="oracle candidates to time (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(candidates would shard across GPUs with one small all-gather; not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_1910_02653_amd import ckm
+    from paper_1910_02653_amd import workloads as wl
+
+    torch.cuda.set_device(0)
+    w = wl.config(args.config)
+    n, K = w.n, w.K
+    W = (n + 63) // 64
+    g = ckm.Graph.from_workload(w)
+    d_s = torch.from_numpy(w.s_frac).cuda()
+    work = g.alloc_work(K)
+    out = g.alloc_outputs(K)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        g.quantize_async(d_s, work, stream)
+        if ev is not None:
+            ev[0].record(stream)
+        g.evaluate_async(K, w.seed, 0, work, stage_splits=args.splits, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        g.select_async(K, w.seed, w.budget, 0, out, work, stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    assert int(out["status"].item()) == ckm.OK
+
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t0.record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_step = t0.elapsed_time(t1) / args.steps
+    eval_ms = [a.elapsed_time(b) for a, b in evs]
+    eval_avg_ms = float(np.mean(eval_ms))
+
+    b_cand = 4 * n * W * 8
+    achieved = K * b_cand / (eval_avg_ms * 1e-3) / 1e9
+    traffic = measured_traffic()
+    result = {
+        "metric": METRIC,
+        "value": K / (ms_step * 1e-3),
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": "%s n=%d K=%d budget %.0f%% of checkpoint-all (seq 2048, hidden 2048, "
+                               "24 blocks, mirrored backward)" % (w.name, n, K, w.budget_pct)
+                   if args.config == 4 else "%s n=%d K=%d" % (w.name, n, K),
+                   "n": n, "K": K, "budget": int(w.budget), "stage_splits": args.splits},
+        "stage_evals_per_s": K * n / (ms_step * 1e-3),
+        "evaluate_kernel_ms": eval_avg_ms,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic},
+        "wall_s": wall,
+    }
+    if args.cpu_sample > 0:
+        result["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, K))
+    print(json.dumps(result), flush=True)
+    g.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,165 @@
+/*
+ * ckm.h -- batched evaluation of rounded rematerialization schedules on
+ * MI355X (gfx950).
+ *
+ * The method is the approximation path of Checkmate (Jain et al., "Checkmate:
+ * Breaking the Memory Wall with Optimal Tensor Rematerialization", MLSys
+ * 2020): a fractional checkpoint matrix S* (the LP relaxation of Section 5.1)
+ * is rounded into K candidate checkpoint matrices by randomized rounding
+ * (Section 5.1); for each candidate the recomputation matrix R is repaired by
+ * two-phase rounding (Algorithm 2, Section 5.2); each candidate is simulated
+ * for peak memory (the U recurrence with the FREE terms, Section 4.4) and for
+ * cost (the objective of Section 4.3); the cheapest candidate within the
+ * memory budget (constraint U_{t,k} <= M_budget of Section 4.7) is returned.
+ *
+ * Index convention: nodes and stages are 0..n-1 (the paper counts from 1);
+ * node t is computed for the first time in stage t (frontier-advancing
+ * stages, Section 4.6). S[t][i] = 1 means value i is resident at the start of
+ * stage t (only i < t); R[t][i] = 1 means node i is computed in stage t (only
+ * i <= t). Nothing is kept after the last stage.
+ *
+ * Rounding: q[t][i] = floor(clamp(S*[t][i], 0, 1) * 65536) and candidate k
+ * keeps value i into stage t iff u_{k,t,i} < q[t][i], where u is a 16-bit
+ * draw of Philox4x32-10 (Salmon et al., SC'11) with key = seed (low 32 bits,
+ * high 32 bits) and counter = (i / 8, t, k, 0); draw i uses 16-bit half
+ * (i mod 8) of the 128-bit output, low half of word 0 first. With CKM_F_DET0
+ * candidate 0 instead uses Algorithm 2's deterministic rounding S* > 0.5.
+ *
+ * Bit rows: a row of an n x n 0/1 matrix is W = ceil(n/64) uint64 words;
+ * node i is bit (i % 64) of word (i / 64); unused high bits are zero.
+ *
+ * Errors never cross the ABI as exceptions: every call returns a ckm_status;
+ * ckm_last_error() gives a thread-local message for the last non-OK status
+ * of the calling thread. On a non-OK return the outputs are unspecified.
+ *
+ * Exact-arithmetic range: the kernels accumulate sizes and costs in IEEE
+ * binary64, which is exact for integers below 2^53. A graph whose
+ * M_in + 2 M_param + sum(M) or sum(C) reaches 2^53, or whose n * sum(C)
+ * exceeds INT64_MAX, is rejected with CKM_E_OVERFLOW.
+ */
+#ifndef CKM_H
+#define CKM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ckm_graph ckm_graph; /* opaque, immutable after creation */
+
+typedef enum {
+  CKM_OK = 0,
+  CKM_E_INVALID_ARG = 1, /* bad argument: NULL, K < 1, ld < n, negative budget, NaN in S* */
+  CKM_E_GRAPH = 2,       /* not topologically numbered, duplicate edge, users != transpose */
+  CKM_E_OVERFLOW = 3,    /* sizes or costs outside the exact-arithmetic range */
+  CKM_E_UNSUPPORTED = 4, /* n > CKM_MAX_NODES or K > CKM_MAX_CANDIDATES */
+  CKM_E_NOMEM = 5,       /* host or device allocation failed */
+  CKM_E_DEVICE = 6       /* a HIP runtime call failed (message has the HIP error) */
+} ckm_status;
+
+enum { CKM_F_DET0 = 1u }; /* candidate 0 = deterministic rounding S* > 0.5 (Algorithm 2) */
+
+#define CKM_MAX_NODES 4096
+#define CKM_MAX_CANDIDATES (1 << 24)
+
+/* Build a graph (Section 4.1: a DAG numbered in topological order, node v
+ * with output size M_v = bytes[v] and cost C_v = cost[v]) and upload it to
+ * the current HIP device.
+ *   n                  number of nodes, 1..CKM_MAX_NODES
+ *   dep_ptr, dep_idx   CSR of Deps: the deps of node j are
+ *                      dep_idx[dep_ptr[j] .. dep_ptr[j+1]), any order, each
+ *                      i < j, no duplicates; dep_ptr has n+1 entries,
+ *                      dep_ptr[0] = 0
+ *   user_ptr, user_idx CSR of Users (Section 4.4), or both NULL to derive it;
+ *                      if given it must be the transpose of Deps
+ *   cost, bytes        int64 [n], >= 0
+ *   m_input, m_param   M_in and M_param of eq. U_init, >= 0
+ *   out                receives the handle
+ * All arrays are host arrays, copied; the caller keeps ownership. */
+ckm_status ckm_graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
+                            const int32_t* user_ptr, const int32_t* user_idx,
+                            const int64_t* cost, const int64_t* bytes, int64_t m_input,
+                            int64_t m_param, ckm_graph** out);
+
+/* Free a graph and its device memory. NULL is ignored. The graph must not be
+ * in use by work still queued on a stream. */
+void ckm_graph_destroy(ckm_graph* g);
+
+/* Number of nodes, or -1 for NULL. */
+int32_t ckm_graph_num_nodes(const ckm_graph* g);
+
+/* The whole path, synchronous, host arrays.
+ *   s_frac      host float64, n rows of stride ld (ld >= n); only the
+ *               strict lower triangle (i < t) is read; values are clamped
+ *               to [0, 1]; NaN there gives CKM_E_INVALID_ARG
+ *   K           number of candidates, 1..CKM_MAX_CANDIDATES
+ *   seed        Philox key
+ *   budget      M_budget in bytes, >= 0; candidate k is feasible iff its
+ *               peak memory <= budget
+ *   flags       0 or CKM_F_DET0
+ *   peak, cost  int64 [K]: max_{t,k} U_{t,k} and sum_t sum_i C_i R[t][i]
+ *   feasible    uint8 [K]: 1 iff peak <= budget
+ *   best_k      lexicographic minimum of (cost, peak, k) over feasible
+ *               candidates, or -1 when none is feasible
+ *   best_S, best_R  uint64 [n * W] bit rows of the best candidate (zero when
+ *               best_k = -1); either may be NULL
+ * Runs on the current HIP device (the graph's) on an internal stream and
+ * returns when the results are in the caller's arrays. */
+ckm_status ckm_round_eval(const ckm_graph* g, const double* s_frac, int64_t ld, int32_t K,
+                          uint64_t seed, int64_t budget, uint32_t flags, int64_t* peak,
+                          int64_t* cost, uint8_t* feasible, int32_t* best_k, uint64_t* best_S,
+                          uint64_t* best_R);
+
+/* ---- asynchronous, device-pointer form --------------------------------
+ * Every pointer below is device memory on the graph's device; `stream` is a
+ * hipStream_t (NULL = the null stream). Calls only enqueue work; buffers must
+ * stay alive until the stream has executed it. Work buffers are caller-owned
+ * and sized by ckm_workspace_size; one work buffer must not be used by two
+ * calls that may run concurrently. The three stages run in the order
+ * quantize -> evaluate -> select, on one work buffer. */
+
+/* Bytes of work buffer needed for K candidates on graph g. */
+ckm_status ckm_workspace_size(const ckm_graph* g, int32_t K, size_t* bytes);
+
+/* Stage a1: thresholds q (Section 5.1) and the deterministic-rounding bits of
+ * Algorithm 2 from S* (device float64, n rows of stride ld >= n). A NaN in
+ * the strict lower triangle is recorded in the work buffer and reported by
+ * ckm_select_async through d_status. */
+ckm_status ckm_quantize_async(const ckm_graph* g, const double* d_s_frac, int64_t ld,
+                              void* d_work, size_t work_bytes, void* stream);
+
+/* Stages a2-a5 for candidates 0..K-1: rounding, Algorithm 2's R repair,
+ * memory simulation and cost. Writes per-candidate partial results into the
+ * work buffer. stage_splits = number of stage ranges each group of 64
+ * candidates is split into (0 = automatic); results do not depend on it. */
+ckm_status ckm_evaluate_async(const ckm_graph* g, int32_t K, uint64_t seed, uint32_t flags,
+                              int32_t stage_splits, void* d_work, size_t work_bytes, void* stream);
+
+/* Stages a6-a7: per-candidate peak / cost / feasible, the argmin, and the
+ * best candidate's S and R bit rows (d_best_S / d_best_R may be NULL).
+ * d_status (may be NULL) receives CKM_OK, or CKM_E_INVALID_ARG when S*
+ * held a NaN (then every other output is unspecified). K, seed and flags
+ * must be those given to ckm_evaluate_async. */
+ckm_status ckm_select_async(const ckm_graph* g, int32_t K, uint64_t seed, int64_t budget,
+                            uint32_t flags, int64_t* d_peak, int64_t* d_cost,
+                            uint8_t* d_feasible, int32_t* d_best_k, uint64_t* d_best_S,
+                            uint64_t* d_best_R, int32_t* d_status, void* d_work,
+                            size_t work_bytes, void* stream);
+
+/* The three stages in one call (same arguments as ckm_round_eval, all
+ * arrays on the device, plus d_status, the work buffer and the stream). */
+ckm_status ckm_round_eval_async(const ckm_graph* g, const double* d_s_frac, int64_t ld,
+                                int32_t K, uint64_t seed, int64_t budget, uint32_t flags,
+                                int64_t* d_peak, int64_t* d_cost, uint8_t* d_feasible,
+                                int32_t* d_best_k, uint64_t* d_best_S, uint64_t* d_best_R,
+                                int32_t* d_status, void* d_work, size_t work_bytes, void* stream);
+
+/* Thread-local text describing the calling thread's last non-OK status. */
+const char* ckm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,203 @@
+"""Thin ctypes binding of libckm (include/ckm.h): argument marshalling only.
+
+Every step of the path runs in the library's HIP kernels; this module only
+converts numpy / torch arguments to pointers. It never falls back to another
+implementation: if libckm.so is missing, loading raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libckm.so")
+
+OK, E_INVALID_ARG, E_GRAPH, E_OVERFLOW, E_UNSUPPORTED, E_NOMEM, E_DEVICE = range(7)
+F_DET0 = 1
+MAX_NODES = 4096
+MAX_CANDIDATES = 1 << 24
+
+# every extern "C" symbol declared in include/ckm.h
+EXPORTS = (
+    "ckm_graph_create", "ckm_graph_destroy", "ckm_graph_num_nodes", "ckm_round_eval",
+    "ckm_workspace_size", "ckm_quantize_async", "ckm_evaluate_async", "ckm_select_async",
+    "ckm_round_eval_async", "ckm_last_error",
+)
+
+
+class CkmError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__("ckm status %d: %s" % (status, msg))
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load libckm.so (built by __graft_entry__.build() / build.py)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libckm.so is not built (%s); run __graft_entry__.build()" % LIB_PATH)
+        # torch ships its own HIP runtime with the same soname (libamdhip64.so.7).
+        # Loading torch first makes libckm bind to that runtime, so the process
+        # has one HIP runtime and torch's streams and allocations are valid in
+        # libckm's calls. Loaded the other way round, two runtimes would coexist.
+        import torch  # noqa: F401
+        L = C.CDLL(LIB_PATH)
+        p, i32, i64, u32, u64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_uint64, C.c_size_t
+        L.ckm_graph_create.argtypes = [i32, p, p, p, p, p, p, i64, i64, C.POINTER(p)]
+        L.ckm_graph_create.restype = C.c_int
+        L.ckm_graph_destroy.argtypes = [p]
+        L.ckm_graph_destroy.restype = None
+        L.ckm_graph_num_nodes.argtypes = [p]
+        L.ckm_graph_num_nodes.restype = i32
+        L.ckm_round_eval.argtypes = [p, p, i64, i32, u64, i64, u32, p, p, p, p, p, p]
+        L.ckm_round_eval.restype = C.c_int
+        L.ckm_workspace_size.argtypes = [p, i32, C.POINTER(sz)]
+        L.ckm_workspace_size.restype = C.c_int
+        L.ckm_quantize_async.argtypes = [p, p, i64, p, sz, p]
+        L.ckm_quantize_async.restype = C.c_int
+        L.ckm_evaluate_async.argtypes = [p, i32, u64, u32, i32, p, sz, p]
+        L.ckm_evaluate_async.restype = C.c_int
+        L.ckm_select_async.argtypes = [p, i32, u64, i64, u32, p, p, p, p, p, p, p, p, sz, p]
+        L.ckm_select_async.restype = C.c_int
+        L.ckm_round_eval_async.argtypes = [p, p, i64, i32, u64, i64, u32, p, p, p, p, p, p, p, p, sz, p]
+        L.ckm_round_eval_async.restype = C.c_int
+        L.ckm_last_error.argtypes = []
+        L.ckm_last_error.restype = C.c_char_p
+        _lib = L
+    return _lib
+
+
+def last_error() -> str:
+    return lib().ckm_last_error().decode()
+
+
+def _check(status: int):
+    if status != OK:
+        raise CkmError(status, last_error())
+
+
+def _np_ptr(a):
+    return None if a is None else a.ctypes.data_as(C.c_void_p)
+
+
+def _dev_ptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream_ptr(stream):
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+class Graph:
+    """A graph uploaded to the current HIP device (ckm_graph_create)."""
+
+    def __init__(self, n, dep_ptr, dep_idx, cost, size, m_input, m_param, user_ptr=None, user_idx=None):
+        dp = np.ascontiguousarray(dep_ptr, dtype=np.int32)
+        di = np.ascontiguousarray(dep_idx, dtype=np.int32)
+        up = None if user_ptr is None else np.ascontiguousarray(user_ptr, dtype=np.int32)
+        ui = None if user_idx is None else np.ascontiguousarray(user_idx, dtype=np.int32)
+        c = np.ascontiguousarray(cost, dtype=np.int64)
+        s = np.ascontiguousarray(size, dtype=np.int64)
+        h = C.c_void_p()
+        self._h = None
+        _check(lib().ckm_graph_create(int(n), _np_ptr(dp), _np_ptr(di) if di.size else None, _np_ptr(up),
+                                      _np_ptr(ui) if (ui is not None and ui.size) else None, _np_ptr(c),
+                                      _np_ptr(s), int(m_input), int(m_param), C.byref(h)))
+        self._h = h
+        self.n = int(n)
+        self.W = (self.n + 63) // 64
+
+    @classmethod
+    def from_workload(cls, w) -> "Graph":
+        return cls(w.n, w.dep_ptr, w.dep_idx, w.cost, w.size, w.m_input, w.m_param)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self):
+        if self._h is not None and self._h.value:
+            lib().ckm_graph_destroy(self._h)
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def workspace_size(self, K: int) -> int:
+        out = C.c_size_t()
+        _check(lib().ckm_workspace_size(self._h, int(K), C.byref(out)))
+        return int(out.value)
+
+    # -- synchronous, host arrays -----------------------------------------
+    def round_eval(self, s_frac, K: int, seed: int, budget: int, flags: int = 0, want_rows: bool = True):
+        s = np.ascontiguousarray(s_frac, dtype=np.float64)
+        peak = np.zeros(K, np.int64)
+        cost = np.zeros(K, np.int64)
+        feas = np.zeros(K, np.uint8)
+        bk = np.zeros(1, np.int32)
+        bS = np.zeros((self.n, self.W), np.uint64) if want_rows else None
+        bR = np.zeros((self.n, self.W), np.uint64) if want_rows else None
+        _check(lib().ckm_round_eval(self._h, _np_ptr(s), s.shape[1], int(K), int(seed), int(budget), int(flags),
+                                    _np_ptr(peak), _np_ptr(cost), _np_ptr(feas), _np_ptr(bk), _np_ptr(bS),
+                                    _np_ptr(bR)))
+        return dict(peak=peak, cost=cost, feasible=feas, best_k=int(bk[0]), best_S=bS, best_R=bR)
+
+    # -- asynchronous, torch device tensors ---------------------------------
+    def quantize_async(self, d_s_frac, work, stream=None):
+        _check(lib().ckm_quantize_async(self._h, _dev_ptr(d_s_frac), d_s_frac.stride(0), _dev_ptr(work),
+                                        work.numel() * work.element_size(), _stream_ptr(stream)))
+
+    def evaluate_async(self, K, seed, flags, work, stage_splits: int = 0, stream=None):
+        _check(lib().ckm_evaluate_async(self._h, int(K), int(seed), int(flags), int(stage_splits),
+                                        _dev_ptr(work), work.numel() * work.element_size(), _stream_ptr(stream)))
+
+    def select_async(self, K, seed, budget, flags, out: dict, work, stream=None):
+        _check(lib().ckm_select_async(self._h, int(K), int(seed), int(budget), int(flags), _dev_ptr(out["peak"]),
+                                      _dev_ptr(out["cost"]), _dev_ptr(out["feasible"]), _dev_ptr(out["best_k"]),
+                                      _dev_ptr(out.get("best_S")), _dev_ptr(out.get("best_R")),
+                                      _dev_ptr(out.get("status")), _dev_ptr(work),
+                                      work.numel() * work.element_size(), _stream_ptr(stream)))
+
+    def round_eval_async(self, d_s_frac, K, seed, budget, flags, out: dict, work, stream=None):
+        _check(lib().ckm_round_eval_async(self._h, _dev_ptr(d_s_frac), d_s_frac.stride(0), int(K), int(seed),
+                                          int(budget), int(flags), _dev_ptr(out["peak"]), _dev_ptr(out["cost"]),
+                                          _dev_ptr(out["feasible"]), _dev_ptr(out["best_k"]),
+                                          _dev_ptr(out.get("best_S")), _dev_ptr(out.get("best_R")),
+                                          _dev_ptr(out.get("status")), _dev_ptr(work),
+                                          work.numel() * work.element_size(), _stream_ptr(stream)))
+
+    def alloc_outputs(self, K: int, device="cuda", rows: bool = True) -> dict:
+        """Device tensors for the async calls (torch: memory only)."""
+        import torch
+        W = self.W
+        out = dict(peak=torch.empty(K, dtype=torch.int64, device=device),
+                   cost=torch.empty(K, dtype=torch.int64, device=device),
+                   feasible=torch.empty(K, dtype=torch.uint8, device=device),
+                   best_k=torch.empty(1, dtype=torch.int32, device=device),
+                   status=torch.empty(1, dtype=torch.int32, device=device))
+        if rows:
+            out["best_S"] = torch.empty((self.n, W), dtype=torch.int64, device=device)
+            out["best_R"] = torch.empty((self.n, W), dtype=torch.int64, device=device)
+        return out
+
+    def alloc_work(self, K: int, device="cuda"):
+        import torch
+        return torch.empty(self.workspace_size(K), dtype=torch.uint8, device=device)
+
+
+def rows_to_numpy(t) -> np.ndarray:
+    """int64 device rows -> uint64 numpy bit rows."""
+    return t.cpu().numpy().view(np.uint64)

@@ -1,0 +1,426 @@
+// Host side of libckm: argument and graph validation, device upload, the
+// work-buffer layout and the C ABI entry points declared in include/ckm.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "ckm_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+ckm_status fail(ckm_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+ckm_status fail_hip(hipError_t e, const char* what) {
+  return fail(CKM_E_DEVICE, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
+}
+
+constexpr int64_t kExactLimit = int64_t(1) << 53;  // binary64 integers are exact below this
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Restores the caller's current device on scope exit.
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = false;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) return;
+    ok = (prev == dev) || (hipSetDevice(dev) == hipSuccess);
+  }
+  ~DeviceGuard() {
+    if (ok && prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+}  // namespace
+
+namespace ckm {
+
+int32_t max_splits_for(int32_t n, int32_t K) {
+  int64_t cap = std::max<int64_t>(4, (int64_t(1) << 22) / std::max<int32_t>(K, 1));
+  cap = std::min<int64_t>(cap, 512);
+  cap = std::min<int64_t>(cap, n);
+  return (int32_t)std::max<int64_t>(cap, 1);
+}
+
+int32_t auto_splits(int32_t n, int32_t K, int32_t max_splits) {
+  // About 2048 waves over the device, and at least ~8 stages per split so the
+  // extra S row a split regenerates at its start stays a small fraction.
+  const int32_t groups = (K + kWave - 1) / kWave;
+  int32_t s = std::max<int32_t>(1, 2048 / std::max<int32_t>(groups, 1));
+  s = std::min<int32_t>(s, std::max<int32_t>(1, n / 8));
+  return std::min<int32_t>(s, max_splits);
+}
+
+Layout make_layout(int32_t n, int32_t K) {
+  Layout L;
+  L.n = n;
+  L.K = K;
+  L.ldq = ((n + 8 + 63) / 64) * 64;
+  L.det_words = L.ldq / 32;
+  L.row_words = 2 * ((n + 63) / 64);
+  L.max_splits = max_splits_for(n, K);
+  L.reduce_blocks = (K + 255) / 256;
+  size_t off = 0;
+  L.hdr_off = off;       off = align256(off + 256);
+  L.q_off = off;         off = align256(off + (size_t)n * L.ldq * sizeof(uint32_t));
+  L.det_off = off;       off = align256(off + (size_t)n * L.det_words * sizeof(uint32_t));
+  L.nan_off = off;       off = align256(off + (size_t)n * sizeof(int32_t));
+  L.part_peak_off = off; off = align256(off + (size_t)L.max_splits * K * sizeof(int64_t));
+  L.part_cost_off = off; off = align256(off + (size_t)L.max_splits * K * sizeof(int64_t));
+  L.best_off = off;      off = align256(off + (size_t)L.reduce_blocks * 24);
+  L.srows_off = off;     off = align256(off + (size_t)n * L.row_words * sizeof(uint32_t));
+  L.total = off;
+  return L;
+}
+
+}  // namespace ckm
+
+using ckm::Layout;
+
+extern "C" {
+
+const char* ckm_last_error(void) { return g_last_error.c_str(); }
+
+int32_t ckm_graph_num_nodes(const ckm_graph* g) { return g ? g->n : -1; }
+
+ckm_status ckm_graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
+                            const int32_t* user_ptr, const int32_t* user_idx,
+                            const int64_t* cost, const int64_t* bytes, int64_t m_input,
+                            int64_t m_param, ckm_graph** out) {
+  if (!out) return fail(CKM_E_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (n < 1) return fail(CKM_E_INVALID_ARG, "n = %d < 1", n);
+  if (n > CKM_MAX_NODES) return fail(CKM_E_UNSUPPORTED, "n = %d > %d", n, CKM_MAX_NODES);
+  if (!dep_ptr || !cost || !bytes) return fail(CKM_E_INVALID_ARG, "NULL dep_ptr, cost or bytes");
+  if (!user_ptr && user_idx)
+    return fail(CKM_E_INVALID_ARG, "user_idx given without user_ptr");
+  if (dep_ptr[0] != 0) return fail(CKM_E_GRAPH, "dep_ptr[0] = %d, expected 0", dep_ptr[0]);
+  for (int32_t j = 0; j < n; ++j)
+    if (dep_ptr[j + 1] < dep_ptr[j]) return fail(CKM_E_GRAPH, "dep_ptr decreases at %d", j);
+  const int32_t E = dep_ptr[n];
+  if (E > 0 && !dep_idx) return fail(CKM_E_INVALID_ARG, "dep_idx is NULL with %d edges", E);
+  if (m_input < 0 || m_param < 0) return fail(CKM_E_INVALID_ARG, "negative m_input or m_param");
+
+  // Deps rows: in range, topological (i < j), no duplicates; stored sorted.
+  std::vector<int32_t> dp(dep_ptr, dep_ptr + n + 1), di(E);
+  std::vector<int32_t> seen(n, -1);
+  for (int32_t j = 0; j < n; ++j) {
+    for (int32_t a = dep_ptr[j]; a < dep_ptr[j + 1]; ++a) {
+      const int32_t i = dep_idx[a];
+      if (i < 0 || i >= j)
+        return fail(CKM_E_GRAPH, "edge %d -> %d is not in topological order", i, j);
+      if (seen[i] == j) return fail(CKM_E_GRAPH, "duplicate edge %d -> %d", i, j);
+      seen[i] = j;
+      di[a] = i;
+    }
+    std::sort(di.begin() + dp[j], di.begin() + dp[j + 1]);
+  }
+  // Sizes and costs: non-negative, totals inside the exact range.
+  int64_t total_m = m_input, total_c = 0;
+  auto add_checked = [](int64_t& acc, int64_t v) {
+    if (v > kExactLimit - 1 - acc) return false;
+    acc += v;
+    return true;
+  };
+  if (!add_checked(total_m, m_param) || !add_checked(total_m, m_param))
+    return fail(CKM_E_OVERFLOW, "M_in + 2 M_param reaches 2^53");
+  for (int32_t v = 0; v < n; ++v) {
+    if (cost[v] < 0 || bytes[v] < 0)
+      return fail(CKM_E_INVALID_ARG, "negative cost or size at node %d", v);
+    if (!add_checked(total_m, bytes[v]))
+      return fail(CKM_E_OVERFLOW, "M_in + 2 M_param + sum(M) reaches 2^53");
+    if (!add_checked(total_c, cost[v])) return fail(CKM_E_OVERFLOW, "sum(C) reaches 2^53");
+  }
+  if (total_c > 0 && (int64_t)n > INT64_MAX / total_c)
+    return fail(CKM_E_OVERFLOW, "n * sum(C) exceeds INT64_MAX");
+
+  // Users = transpose(Deps), rows ascending.
+  std::vector<int32_t> up(n + 1, 0), ui(E);
+  for (int32_t a = 0; a < E; ++a) up[di[a] + 1]++;
+  for (int32_t i = 0; i < n; ++i) up[i + 1] += up[i];
+  {
+    std::vector<int32_t> fill(up.begin(), up.end() - 1);
+    for (int32_t j = 0; j < n; ++j)
+      for (int32_t a = dp[j]; a < dp[j + 1]; ++a) ui[fill[di[a]]++] = j;  // j ascending
+  }
+  if (user_ptr) {
+    if (E > 0 && !user_idx) return fail(CKM_E_INVALID_ARG, "user_idx is NULL with %d edges", E);
+    if (user_ptr[0] != 0 || user_ptr[n] != E)
+      return fail(CKM_E_GRAPH, "users CSR does not have the edge count of deps");
+    for (int32_t i = 0; i < n; ++i)
+      if (user_ptr[i + 1] < user_ptr[i]) return fail(CKM_E_GRAPH, "user_ptr decreases at %d", i);
+    for (int32_t i = 0; i < n; ++i) {
+      if (user_ptr[i + 1] - user_ptr[i] != up[i + 1] - up[i])
+        return fail(CKM_E_GRAPH, "users of node %d differ from the transpose of deps", i);
+      std::vector<int32_t> got(user_idx + user_ptr[i], user_idx + user_ptr[i + 1]);
+      std::sort(got.begin(), got.end());
+      if (!std::equal(got.begin(), got.end(), ui.begin() + up[i]))
+        return fail(CKM_E_GRAPH, "users of node %d differ from the transpose of deps", i);
+    }
+  }
+  // dep_upos: for entry (i -> j), first position in Users[i] after j.
+  std::vector<int32_t> upos(E);
+  for (int32_t j = 0; j < n; ++j)
+    for (int32_t a = dp[j]; a < dp[j + 1]; ++a) {
+      const int32_t i = di[a];
+      const int32_t* b = ui.data() + up[i];
+      const int32_t* e = ui.data() + up[i + 1];
+      upos[a] = (int32_t)(std::upper_bound(b, e, j) - ui.data());
+    }
+
+  ckm_graph* g = new (std::nothrow) ckm_graph();
+  if (!g) return fail(CKM_E_NOMEM, "host allocation failed");
+  g->n = n;
+  g->num_edges = E;
+  g->base = (double)(m_input + 2 * m_param);
+  hipError_t e = hipGetDevice(&g->device);
+  if (e != hipSuccess) {
+    delete g;
+    return fail_hip(e, "hipGetDevice");
+  }
+  const size_t Ea = (size_t)std::max(E, 1);
+  const size_t off_M = 0;
+  const size_t off_C = align256(off_M + n * sizeof(double));
+  const size_t off_up = align256(off_C + n * sizeof(double));
+  const size_t off_ui = align256(off_up + (n + 1) * sizeof(int32_t));
+  const size_t off_dp = align256(off_ui + Ea * sizeof(int32_t));
+  const size_t off_di = align256(off_dp + (n + 1) * sizeof(int32_t));
+  const size_t off_uo = align256(off_di + Ea * sizeof(int32_t));
+  const size_t total = align256(off_uo + Ea * sizeof(int32_t));
+  std::vector<char> host(total, 0);
+  std::vector<double> Md(n), Cd(n);
+  for (int32_t v = 0; v < n; ++v) {
+    Md[v] = (double)bytes[v];
+    Cd[v] = (double)cost[v];
+  }
+  memcpy(host.data() + off_M, Md.data(), n * sizeof(double));
+  memcpy(host.data() + off_C, Cd.data(), n * sizeof(double));
+  memcpy(host.data() + off_up, up.data(), (n + 1) * sizeof(int32_t));
+  if (E) memcpy(host.data() + off_ui, ui.data(), E * sizeof(int32_t));
+  memcpy(host.data() + off_dp, dp.data(), (n + 1) * sizeof(int32_t));
+  if (E) memcpy(host.data() + off_di, di.data(), E * sizeof(int32_t));
+  if (E) memcpy(host.data() + off_uo, upos.data(), E * sizeof(int32_t));
+  e = hipMalloc(&g->d_mem, total);
+  if (e != hipSuccess) {
+    delete g;
+    return e == hipErrorOutOfMemory ? fail(CKM_E_NOMEM, "hipMalloc of %zu bytes failed", total)
+                                    : fail_hip(e, "hipMalloc");
+  }
+  e = hipMemcpy(g->d_mem, host.data(), total, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(g->d_mem);
+    delete g;
+    return fail_hip(e, "hipMemcpy graph upload");
+  }
+  char* base = static_cast<char*>(g->d_mem);
+  g->d_M = reinterpret_cast<const double*>(base + off_M);
+  g->d_C = reinterpret_cast<const double*>(base + off_C);
+  g->d_user_ptr = reinterpret_cast<const int32_t*>(base + off_up);
+  g->d_user_idx = reinterpret_cast<const int32_t*>(base + off_ui);
+  g->d_dep_ptr = reinterpret_cast<const int32_t*>(base + off_dp);
+  g->d_dep_idx = reinterpret_cast<const int32_t*>(base + off_di);
+  g->d_dep_upos = reinterpret_cast<const int32_t*>(base + off_uo);
+  *out = g;
+  return CKM_OK;
+}
+
+void ckm_graph_destroy(ckm_graph* g) {
+  if (!g) return;
+  if (g->d_mem) {
+    DeviceGuard dg(g->device);
+    (void)hipFree(g->d_mem);
+  }
+  delete g;
+}
+
+ckm_status ckm_workspace_size(const ckm_graph* g, int32_t K, size_t* bytes) {
+  if (!g || !bytes) return fail(CKM_E_INVALID_ARG, "NULL graph or bytes");
+  if (K < 1) return fail(CKM_E_INVALID_ARG, "K = %d < 1", K);
+  if (K > CKM_MAX_CANDIDATES) return fail(CKM_E_UNSUPPORTED, "K = %d > %d", K, CKM_MAX_CANDIDATES);
+  *bytes = ckm::make_layout(g->n, K).total;
+  return CKM_OK;
+}
+
+static ckm_status check_work(const ckm_graph* g, int32_t K, void* d_work, size_t work_bytes,
+                             Layout* L) {
+  if (!g) return fail(CKM_E_INVALID_ARG, "graph is NULL");
+  if (K < 1) return fail(CKM_E_INVALID_ARG, "K = %d < 1", K);
+  if (K > CKM_MAX_CANDIDATES) return fail(CKM_E_UNSUPPORTED, "K = %d > %d", K, CKM_MAX_CANDIDATES);
+  if (!d_work) return fail(CKM_E_INVALID_ARG, "work buffer is NULL");
+  *L = ckm::make_layout(g->n, K);
+  if (work_bytes < L->total)
+    return fail(CKM_E_INVALID_ARG, "work buffer of %zu bytes, %zu needed", work_bytes, L->total);
+  return CKM_OK;
+}
+
+ckm_status ckm_quantize_async(const ckm_graph* g, const double* d_s_frac, int64_t ld, void* d_work,
+                              size_t work_bytes, void* stream) {
+  Layout L;
+  if (!g) return fail(CKM_E_INVALID_ARG, "graph is NULL");
+  // The thresholds do not depend on K; size the check with K = 1.
+  ckm_status st = check_work(g, 1, d_work, work_bytes, &L);
+  if (st != CKM_OK) return st;
+  if (!d_s_frac) return fail(CKM_E_INVALID_ARG, "S* is NULL");
+  if (ld < g->n) return fail(CKM_E_INVALID_ARG, "ld = %lld < n = %d", (long long)ld, g->n);
+  DeviceGuard dg(g->device);
+  hipError_t e = ckm::launch_quantize(*g, L, d_s_frac, ld, static_cast<char*>(d_work),
+                                      static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CKM_OK : fail_hip(e, "quantize launch");
+}
+
+ckm_status ckm_evaluate_async(const ckm_graph* g, int32_t K, uint64_t seed, uint32_t flags,
+                              int32_t stage_splits, void* d_work, size_t work_bytes, void* stream) {
+  Layout L;
+  ckm_status st = check_work(g, K, d_work, work_bytes, &L);
+  if (st != CKM_OK) return st;
+  if (flags & ~(uint32_t)CKM_F_DET0) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
+  if (stage_splits < 0) return fail(CKM_E_INVALID_ARG, "stage_splits = %d < 0", stage_splits);
+  int32_t splits = stage_splits ? std::min(stage_splits, L.max_splits)
+                                : ckm::auto_splits(g->n, K, L.max_splits);
+  DeviceGuard dg(g->device);
+  hipError_t e = ckm::launch_evaluate(*g, L, K, seed, flags, splits, static_cast<char*>(d_work),
+                                      static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CKM_OK : fail_hip(e, "evaluate launch");
+}
+
+ckm_status ckm_select_async(const ckm_graph* g, int32_t K, uint64_t seed, int64_t budget,
+                            uint32_t flags, int64_t* d_peak, int64_t* d_cost, uint8_t* d_feasible,
+                            int32_t* d_best_k, uint64_t* d_best_S, uint64_t* d_best_R,
+                            int32_t* d_status, void* d_work, size_t work_bytes, void* stream) {
+  Layout L;
+  ckm_status st = check_work(g, K, d_work, work_bytes, &L);
+  if (st != CKM_OK) return st;
+  if (budget < 0) return fail(CKM_E_INVALID_ARG, "budget = %lld < 0", (long long)budget);
+  if (flags & ~(uint32_t)CKM_F_DET0) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
+  if (!d_peak || !d_cost || !d_feasible || !d_best_k)
+    return fail(CKM_E_INVALID_ARG, "NULL peak, cost, feasible or best_k");
+  DeviceGuard dg(g->device);
+  hipError_t e = ckm::launch_select(*g, L, K, seed, budget, flags, d_peak, d_cost, d_feasible,
+                                    d_best_k, d_best_S, d_best_R, d_status,
+                                    static_cast<char*>(d_work), static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CKM_OK : fail_hip(e, "select launch");
+}
+
+ckm_status ckm_round_eval_async(const ckm_graph* g, const double* d_s_frac, int64_t ld, int32_t K,
+                                uint64_t seed, int64_t budget, uint32_t flags, int64_t* d_peak,
+                                int64_t* d_cost, uint8_t* d_feasible, int32_t* d_best_k,
+                                uint64_t* d_best_S, uint64_t* d_best_R, int32_t* d_status,
+                                void* d_work, size_t work_bytes, void* stream) {
+  Layout L;
+  ckm_status st = check_work(g, K, d_work, work_bytes, &L);
+  if (st != CKM_OK) return st;
+  if (budget < 0) return fail(CKM_E_INVALID_ARG, "budget = %lld < 0", (long long)budget);
+  if (flags & ~(uint32_t)CKM_F_DET0) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
+  if (!d_peak || !d_cost || !d_feasible || !d_best_k)
+    return fail(CKM_E_INVALID_ARG, "NULL peak, cost, feasible or best_k");
+  st = ckm_quantize_async(g, d_s_frac, ld, d_work, work_bytes, stream);
+  if (st != CKM_OK) return st;
+  st = ckm_evaluate_async(g, K, seed, flags, 0, d_work, work_bytes, stream);
+  if (st != CKM_OK) return st;
+  return ckm_select_async(g, K, seed, budget, flags, d_peak, d_cost, d_feasible, d_best_k,
+                          d_best_S, d_best_R, d_status, d_work, work_bytes, stream);
+}
+
+ckm_status ckm_round_eval(const ckm_graph* g, const double* s_frac, int64_t ld, int32_t K,
+                          uint64_t seed, int64_t budget, uint32_t flags, int64_t* peak,
+                          int64_t* cost, uint8_t* feasible, int32_t* best_k, uint64_t* best_S,
+                          uint64_t* best_R) {
+  if (!g) return fail(CKM_E_INVALID_ARG, "graph is NULL");
+  if (!s_frac || !peak || !cost || !feasible || !best_k)
+    return fail(CKM_E_INVALID_ARG, "NULL S*, peak, cost, feasible or best_k");
+  if (ld < g->n) return fail(CKM_E_INVALID_ARG, "ld = %lld < n = %d", (long long)ld, g->n);
+  if (K < 1) return fail(CKM_E_INVALID_ARG, "K = %d < 1", K);
+  if (K > CKM_MAX_CANDIDATES) return fail(CKM_E_UNSUPPORTED, "K = %d > %d", K, CKM_MAX_CANDIDATES);
+  if (budget < 0) return fail(CKM_E_INVALID_ARG, "budget = %lld < 0", (long long)budget);
+  if (flags & ~(uint32_t)CKM_F_DET0) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
+  // NaN check on the host: only the strict lower triangle is read.
+  const int32_t n = g->n;
+  for (int32_t t = 0; t < n; ++t)
+    for (int32_t i = 0; i < t; ++i)
+      if (std::isnan(s_frac[(int64_t)t * ld + i]))
+        return fail(CKM_E_INVALID_ARG, "S*[%d][%d] is NaN", t, i);
+
+  DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
+  const Layout L = ckm::make_layout(n, K);
+  const int32_t W = (n + 63) / 64;
+  const size_t s_bytes = (size_t)n * n * sizeof(double);
+  const size_t rows_bytes = (size_t)n * W * sizeof(uint64_t);
+  size_t off = 0;
+  const size_t o_s = off;    off = align256(off + s_bytes);
+  const size_t o_peak = off; off = align256(off + (size_t)K * 8);
+  const size_t o_cost = off; off = align256(off + (size_t)K * 8);
+  const size_t o_feas = off; off = align256(off + (size_t)K);
+  const size_t o_bk = off;   off = align256(off + 8);
+  const size_t o_st = off;   off = align256(off + 8);
+  const size_t o_bS = off;   off = align256(off + rows_bytes);
+  const size_t o_bR = off;   off = align256(off + rows_bytes);
+  const size_t o_w = off;    off = align256(off + L.total);
+  char* d = nullptr;
+  hipError_t e = hipMalloc(&d, off);
+  if (e != hipSuccess)
+    return e == hipErrorOutOfMemory ? fail(CKM_E_NOMEM, "hipMalloc of %zu bytes failed", off)
+                                    : fail_hip(e, "hipMalloc");
+  hipStream_t stream = nullptr;
+  ckm_status st = CKM_OK;
+  int32_t status_dev = 0;
+  do {
+    if ((e = hipStreamCreateWithFlags(&stream, hipStreamNonBlocking)) != hipSuccess) {
+      st = fail_hip(e, "hipStreamCreate");
+      break;
+    }
+    if ((e = hipMemcpy2DAsync(d + o_s, (size_t)n * sizeof(double), s_frac, (size_t)ld * sizeof(double),
+                              (size_t)n * sizeof(double), n, hipMemcpyHostToDevice, stream)) != hipSuccess) {
+      st = fail_hip(e, "hipMemcpy2D S*");
+      break;
+    }
+    st = ckm_round_eval_async(g, reinterpret_cast<const double*>(d + o_s), n, K, seed, budget, flags,
+                              reinterpret_cast<int64_t*>(d + o_peak), reinterpret_cast<int64_t*>(d + o_cost),
+                              reinterpret_cast<uint8_t*>(d + o_feas), reinterpret_cast<int32_t*>(d + o_bk),
+                              best_S ? reinterpret_cast<uint64_t*>(d + o_bS) : nullptr,
+                              best_R ? reinterpret_cast<uint64_t*>(d + o_bR) : nullptr,
+                              reinterpret_cast<int32_t*>(d + o_st), d + o_w, L.total, stream);
+    if (st != CKM_OK) break;
+    struct Copy { void* dst; size_t off, bytes; } copies[] = {
+        {peak, o_peak, (size_t)K * 8}, {cost, o_cost, (size_t)K * 8}, {feasible, o_feas, (size_t)K},
+        {best_k, o_bk, 4}, {&status_dev, o_st, 4}, {best_S, o_bS, rows_bytes}, {best_R, o_bR, rows_bytes}};
+    for (const Copy& c : copies) {
+      if (!c.dst) continue;
+      if ((e = hipMemcpyAsync(c.dst, d + c.off, c.bytes, hipMemcpyDeviceToHost, stream)) != hipSuccess) {
+        st = fail_hip(e, "hipMemcpy results");
+        break;
+      }
+    }
+    if (st != CKM_OK) break;
+    if ((e = hipStreamSynchronize(stream)) != hipSuccess) {
+      st = fail_hip(e, "hipStreamSynchronize");
+      break;
+    }
+    if (status_dev != CKM_OK) st = fail((ckm_status)status_dev, "S* holds a NaN");
+  } while (false);
+  if (stream) {
+    (void)hipStreamSynchronize(stream);
+    (void)hipStreamDestroy(stream);
+  }
+  (void)hipFree(d);
+  return st;
+}
+
+}  // extern "C"

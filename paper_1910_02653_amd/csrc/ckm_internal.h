@@ -1,0 +1,62 @@
+// Internal declarations shared by the host glue and the HIP kernels of libckm.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "ckm.h"
+
+// Graph on the device. Node arrays hold sizes and costs as binary64 (exact:
+// the host rejects totals >= 2^53). Users rows are sorted ascending; for the
+// dep entry e = (i -> v) in v's deps row, dep_upos[e] is the index in
+// user_idx of the first user of i that is greater than v.
+struct ckm_graph {
+  int32_t n = 0;
+  int32_t num_edges = 0;
+  int device = 0;
+  double base = 0.0;          // M_in + 2 M_param (eq. U_init constant overhead)
+  void* d_mem = nullptr;      // one allocation holding every array below
+  const double* d_M = nullptr;
+  const double* d_C = nullptr;
+  const int32_t* d_user_ptr = nullptr;
+  const int32_t* d_user_idx = nullptr;
+  const int32_t* d_dep_ptr = nullptr;
+  const int32_t* d_dep_idx = nullptr;
+  const int32_t* d_dep_upos = nullptr;
+};
+
+namespace ckm {
+
+constexpr int kWave = 64;
+
+// Work-buffer layout for (n, K). Offsets are bytes from the buffer start,
+// each 256-byte aligned.
+struct Layout {
+  int32_t n = 0, K = 0;
+  int32_t ldq = 0;        // q / det row stride in elements: round_up(n + 8, 64)
+  int32_t det_words = 0;  // ldq / 32
+  int32_t row_words = 0;  // 32-bit words per output bit row: 2 * ceil(n / 64)
+  int32_t max_splits = 0; // capacity of the partial-result arrays
+  int32_t reduce_blocks = 0;
+  // hdr: int32 number of stage splits used by the last evaluate
+  size_t hdr_off = 0, q_off = 0, det_off = 0, nan_off = 0, part_peak_off = 0, part_cost_off = 0,
+         best_off = 0, srows_off = 0, total = 0;
+};
+
+Layout make_layout(int32_t n, int32_t K);
+int32_t auto_splits(int32_t n, int32_t K, int32_t max_splits);
+
+// Kernel launchers (defined in ckm_kernels.hip). They only enqueue work.
+hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,
+                           char* work, hipStream_t stream);
+hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
+                           uint32_t flags, int32_t splits, char* work, hipStream_t stream);
+hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
+                         int64_t budget, uint32_t flags, int64_t* d_peak,
+                         int64_t* d_cost, uint8_t* d_feasible, int32_t* d_best_k,
+                         uint64_t* d_best_S, uint64_t* d_best_R, int32_t* d_status, char* work,
+                         hipStream_t stream);
+
+}  // namespace ckm

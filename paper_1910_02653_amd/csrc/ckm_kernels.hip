@@ -1,0 +1,482 @@
+// HIP kernels for gfx950: batched rounding, Algorithm 2 repair, memory
+// simulation, reduction and argmin of Checkmate candidate schedules.
+//
+// Work decomposition of the dominant kernel (ckm_eval_kernel): one wave of 64
+// lanes owns 64 candidates (lane = candidate) and a contiguous range of
+// stages. All lanes walk the same nodes in the same order, so graph metadata,
+// thresholds and loop bounds are wave-uniform (scalar loads) and only the
+// candidate's bits and running sums live in vector registers. Each lane keeps
+// two bit rows (32-bit words, bit i%32 of word i/32) in LDS, laid out
+// [word][lane] so that a wave-uniform word index touches 64 consecutive
+// dwords: no bank conflicts.
+//
+// Sums of sizes and costs run in binary64. The host admits only graphs whose
+// totals stay below 2^53, so every partial sum is an exactly represented
+// integer and the result is identical to int64 arithmetic in any order.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "ckm_internal.h"
+
+namespace ckm {
+namespace {
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): multipliers for counter
+// words 0 and 2, key advanced by the Weyl constants between rounds.
+constexpr uint32_t kPhiloxM0 = 0xD2511F53u;
+constexpr uint32_t kPhiloxM1 = 0xCD9E8D57u;
+constexpr uint32_t kPhiloxW0 = 0x9E3779B9u;
+constexpr uint32_t kPhiloxW1 = 0xBB67AE85u;
+
+__device__ __forceinline__ void philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                              uint32_t k0, uint32_t k1, uint32_t x[4]) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t p0 = (uint64_t)kPhiloxM0 * c0;
+    const uint64_t p1 = (uint64_t)kPhiloxM1 * c2;
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+    c0 = n0;
+    c1 = (uint32_t)p1;
+    c2 = n2;
+    c3 = (uint32_t)p0;
+    k0 += kPhiloxW0;
+    k1 += kPhiloxW1;
+  }
+  x[0] = c0; x[1] = c1; x[2] = c2; x[3] = c3;
+}
+
+// 32 rounding decisions of row r, candidate k: bits i = 32w .. 32w+31 of
+// S_k[r] (Section 5.1 randomized rounding, thresholds q). Entries i >= r
+// have q = 0 and round to 0.
+__device__ __forceinline__ uint32_t round_word(const uint32_t* __restrict__ qrow, int w, int r,
+                                               uint32_t k, uint32_t key0, uint32_t key1) {
+  uint32_t word = 0;
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const int m = 4 * w + b;        // draws 8m .. 8m+7 share one Philox output
+    if (8 * m >= r) break;          // wave-uniform: the rest of the word is beyond the row
+    uint32_t x[4];
+    philox4x32_10((uint32_t)m, (uint32_t)r, k, 0u, key0, key1, x);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t u = (x[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+      word |= (uint32_t)(u < qrow[8 * m + j]) << (8 * b + j);
+    }
+  }
+  return word;
+}
+
+struct EvalArgs {
+  int32_t n, K, splits, ldq, det_words;
+  uint32_t key0, key1;
+  uint32_t det0;                 // CKM_F_DET0 given
+  double base;                   // M_in + 2 M_param
+  const uint32_t* __restrict__ q;
+  const uint32_t* __restrict__ det;
+  const double* __restrict__ M;
+  const double* __restrict__ C;
+  const int32_t* __restrict__ user_ptr;
+  const int32_t* __restrict__ user_idx;
+  const int32_t* __restrict__ dep_ptr;
+  const int32_t* __restrict__ dep_idx;
+  const int32_t* __restrict__ dep_upos;
+  int64_t* __restrict__ part_peak;   // [splits][K]
+  int64_t* __restrict__ part_cost;   // [splits][K]
+  int32_t* __restrict__ hdr;
+};
+
+// First stage of split s: splits cover equal shares of the sum of stage
+// lengths (stage t touches t + 1 nodes), t_s = floor(sqrt(n^2 s / splits)).
+__device__ __forceinline__ int split_begin(int n, int splits, int s) {
+  if (s <= 0) return 0;
+  if (s >= splits) return n;
+  const uint64_t x = (uint64_t)n * (uint64_t)n * (uint64_t)s / (uint64_t)splits;
+  uint64_t r = (uint64_t)sqrt((double)x);
+  while (r * r > x) --r;
+  while ((r + 1) * (r + 1) <= x) ++r;
+  return (int)r;
+}
+
+// Row r of the candidate into LDS words 0 .. r/32 (dst[w * 64]).
+__device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bool det_lane,
+                                        uint32_t* dst) {
+  const int nw = (r >> 5) + 1;
+  if (r >= a.n) {  // S after the last stage: nothing is kept
+    for (int w = 0; w < nw; ++w) dst[w * kWave] = 0u;
+    return;
+  }
+  const uint32_t* qrow = a.q + (size_t)r * a.ldq;
+  const uint32_t* drow = a.det + (size_t)r * a.det_words;
+  for (int w = 0; w < nw; ++w) {
+    uint32_t word = round_word(qrow, w, r, k, a.key0, a.key1);
+    if (det_lane) word = drow[w];
+    dst[w * kWave] = word;
+  }
+}
+
+__device__ __forceinline__ uint32_t bit(uint32_t word, int pos) { return (word >> pos) & 1u; }
+
+// One stage t of one candidate (per lane). On entry A holds S_t and B holds
+// S_{t+1} (words 0 .. t/32). Algorithm 2's repair of R runs right to left
+// (reverse topological order); in the same pass the U recurrence of Section
+// 4.4 is evaluated in suffix form:
+//   val_k = sum_{j>=k} freed_j - sum_{j>k} alloc_j,   U_{t,k} = U_end + val_k,
+// so the stage peak is U_end + max_k val_k with U_end = U_{t,0} - Y, Y being
+// the suffix value after node 0. R_t overwrites S_t in A, chunk by chunk.
+__device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, uint32_t* A, const uint32_t* B,
+                                           double& stage_peak, double& stage_cost) {
+  double U0 = a.base, Y = 0.0, maxv = -INFINITY, cost = 0.0;
+  for (int c = t >> 5; c >= 0; --c) {
+    const uint32_t w0 = A[c * kWave];
+    const uint32_t w1 = B[c * kWave];
+    uint32_t rw = 0;
+    const int jtop = min(31, t - 32 * c);
+    for (int jj = jtop; jj >= 0; --jj) {
+      const int v = 32 * c + jj;
+      const uint32_t s0 = bit(w0, jj);
+      const uint32_t s1 = bit(w1, jj);
+      // does any user of v computed in this stage need it?
+      uint32_t anyU = 0;
+      const int ue = a.user_ptr[v + 1];
+      for (int e = a.user_ptr[v]; e < ue; ++e) {
+        const int u = a.user_idx[e];
+        if (u > t) break;
+        const uint32_t word = ((u >> 5) == c) ? rw : A[(u >> 5) * kWave];
+        anyU |= bit(word, u & 31);
+      }
+      // (4a) R_tt = 1; (1c) keep-for-next-stage needs v in memory; (1b) a
+      // computed user needs v unless it is checkpointed.
+      const uint32_t r = (v == t) ? 1u : ((s1 | anyU) & ~s0 & 1u);
+      rw |= r << jj;
+      const double Mv = a.M[v];
+      // FREE(t, v, v): computed, not kept, no computed user
+      double freed = (r & ~s1 & ~anyU & 1u) ? Mv : 0.0;
+      // FREE(t, i, v) for deps i: v is the last computed user and i not kept
+      const int de = a.dep_ptr[v + 1];
+      for (int e = a.dep_ptr[v]; e < de; ++e) {
+        const int i = a.dep_idx[e];
+        const uint32_t wi = ((i >> 5) == c) ? w1 : B[(i >> 5) * kWave];
+        const uint32_t si1 = bit(wi, i & 31);
+        uint32_t later = 0;
+        const int le = a.user_ptr[i + 1];
+        for (int e2 = a.dep_upos[e]; e2 < le; ++e2) {
+          const int u = a.user_idx[e2];
+          if (u > t) break;
+          const uint32_t word = ((u >> 5) == c) ? rw : A[(u >> 5) * kWave];
+          later |= bit(word, u & 31);
+        }
+        if (r & ~si1 & ~later & 1u) freed += a.M[i];
+      }
+      cost += r ? a.C[v] : 0.0;
+      U0 += s0 ? Mv : 0.0;
+      const double val = Y + freed;
+      maxv = fmax(maxv, val);
+      Y = val - (r ? Mv : 0.0);
+    }
+    A[c * kWave] = rw;
+  }
+  stage_peak = U0 - Y + maxv;
+  stage_cost = cost;
+}
+
+__global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
+  extern __shared__ uint32_t lds[];
+  const int lane = threadIdx.x;
+  const int group = blockIdx.x;
+  const int split = blockIdx.y;
+  const uint32_t k = (uint32_t)(group * kWave + lane);
+  const bool det_lane = a.det0 && k == 0;
+  const int words = (a.n >> 5) + 1;
+  uint32_t* A = lds + lane;
+  uint32_t* B = lds + (size_t)words * kWave + lane;
+
+  if (group == 0 && split == 0 && lane == 0) a.hdr[0] = a.splits;
+
+  const int t0 = split_begin(a.n, a.splits, split);
+  const int t1 = split_begin(a.n, a.splits, split + 1);
+  double seg_peak = -INFINITY;
+  int64_t seg_cost = 0;
+  if (t0 < t1) {
+    gen_row(a, t0, k, det_lane, A);
+    for (int t = t0; t < t1; ++t) {
+      gen_row(a, t + 1, k, det_lane, B);
+      double sp, sc;
+      eval_stage(a, t, A, B, sp, sc);
+      seg_peak = fmax(seg_peak, sp);
+      seg_cost += (int64_t)sc;
+      uint32_t* tmp = A; A = B; B = tmp;
+    }
+  }
+  if ((int)k < a.K) {
+    const size_t o = (size_t)split * a.K + k;
+    a.part_peak[o] = (t0 < t1) ? (int64_t)seg_peak : INT64_MIN;
+    a.part_cost[o] = seg_cost;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Thresholds: one block per row r; q[r][i] = floor(clamp(S*, 0, 1) * 2^16) for
+// i < r (Section 5.1), the deterministic bits 1[S* > 0.5] of Algorithm 2, and
+// a per-row NaN flag.
+__global__ void __launch_bounds__(256) ckm_quantize_kernel(const double* __restrict__ s, int64_t ld,
+                                                           int32_t n, int32_t ldq, int32_t det_words,
+                                                           uint32_t* __restrict__ q,
+                                                           uint32_t* __restrict__ det,
+                                                           int32_t* __restrict__ nan_row) {
+  __shared__ int any_nan;
+  const int r = blockIdx.x;
+  if (threadIdx.x == 0) any_nan = 0;
+  __syncthreads();
+  int my_nan = 0;
+  for (int i0 = 0; i0 < ldq; i0 += blockDim.x) {
+    const int i = i0 + threadIdx.x;   // ldq is a multiple of 64: whole waves stay in the row
+    double x = 0.0;
+    const bool in = i < r;
+    if (in) x = s[(int64_t)r * ld + i];
+    const bool isnan_x = in && (x != x);
+    my_nan |= isnan_x;
+    uint32_t qv = 0;
+    if (in && !isnan_x) qv = (uint32_t)floor(fmin(fmax(x, 0.0), 1.0) * 65536.0);
+    if (i < ldq) q[(size_t)r * ldq + i] = qv;
+    const uint64_t bits = __ballot(in && x > 0.5);
+    const int lane = threadIdx.x & 63;
+    if (i < ldq && (lane == 0 || lane == 32))
+      det[(size_t)r * det_words + (i >> 5)] = (uint32_t)(bits >> lane);
+  }
+  if (my_nan) atomicOr(&any_nan, 1);
+  __syncthreads();
+  if (threadIdx.x == 0) nan_row[r] = any_nan;
+}
+
+// ---------------------------------------------------------------------------
+// Per-candidate reduction over stage splits, feasibility, and the block's
+// lexicographic minimum of (cost, peak, k) over feasible candidates.
+struct Best {
+  int64_t cost, peak;
+  int32_t k, pad;
+};
+
+__device__ __forceinline__ bool better(const Best& x, const Best& y) {
+  if (x.k < 0) return false;
+  if (y.k < 0) return true;
+  if (x.cost != y.cost) return x.cost < y.cost;
+  if (x.peak != y.peak) return x.peak < y.peak;
+  return x.k < y.k;
+}
+
+__global__ void __launch_bounds__(256) ckm_reduce_kernel(int32_t K, const int32_t* __restrict__ hdr,
+                                                         const int64_t* __restrict__ part_peak,
+                                                         const int64_t* __restrict__ part_cost,
+                                                         int64_t budget, int64_t* __restrict__ peak,
+                                                         int64_t* __restrict__ cost,
+                                                         uint8_t* __restrict__ feasible,
+                                                         Best* __restrict__ block_best) {
+  __shared__ Best sb[256];
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  const int splits = hdr[0];
+  Best b{0, 0, -1, 0};
+  if (k < K) {
+    int64_t p = INT64_MIN, c = 0;
+    for (int s = 0; s < splits; ++s) {
+      const int64_t v = part_peak[(size_t)s * K + k];
+      p = v > p ? v : p;
+      c += part_cost[(size_t)s * K + k];
+    }
+    peak[k] = p;
+    cost[k] = c;
+    const bool f = p <= budget;
+    feasible[k] = f ? 1 : 0;
+    if (f) b = Best{c, p, k, 0};
+  }
+  sb[threadIdx.x] = b;
+  __syncthreads();
+  for (int off = blockDim.x / 2; off > 0; off >>= 1) {
+    if (threadIdx.x < off && better(sb[threadIdx.x + off], sb[threadIdx.x]))
+      sb[threadIdx.x] = sb[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) block_best[blockIdx.x] = sb[0];
+}
+
+__global__ void __launch_bounds__(256) ckm_argmin_kernel(int32_t nblocks, const Best* __restrict__ block_best,
+                                                         int32_t n, const int32_t* __restrict__ nan_row,
+                                                         int32_t* __restrict__ best_k,
+                                                         int32_t* __restrict__ status) {
+  __shared__ Best sb[256];
+  __shared__ int any_nan;
+  if (threadIdx.x == 0) any_nan = 0;
+  Best b{0, 0, -1, 0};
+  for (int i = threadIdx.x; i < nblocks; i += blockDim.x)
+    if (better(block_best[i], b)) b = block_best[i];
+  int nan = 0;
+  for (int r = threadIdx.x; r < n; r += blockDim.x) nan |= nan_row[r];
+  sb[threadIdx.x] = b;
+  __syncthreads();
+  if (nan) atomicOr(&any_nan, 1);
+  for (int off = blockDim.x / 2; off > 0; off >>= 1) {
+    if (threadIdx.x < off && better(sb[threadIdx.x + off], sb[threadIdx.x]))
+      sb[threadIdx.x] = sb[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    best_k[0] = sb[0].k;
+    if (status) status[0] = any_nan ? (int32_t)CKM_E_INVALID_ARG : (int32_t)CKM_OK;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Best candidate's S rows: thread per (row r, 32-bit word w). Output rows
+// have row_words words; words with no node (32w >= n) are zero.
+__global__ void __launch_bounds__(256) ckm_best_rows_kernel(const uint32_t* __restrict__ q,
+                                                            const uint32_t* __restrict__ det,
+                                                            int32_t n, int32_t ldq, int32_t det_words,
+                                                            int32_t row_words, uint32_t key0,
+                                                            uint32_t key1, uint32_t det0,
+                                                            const int32_t* __restrict__ best_k,
+                                                            uint32_t* __restrict__ S_rows) {
+  const int r = blockIdx.y;
+  const int w = blockIdx.x * blockDim.x + threadIdx.x;
+  if (w >= row_words) return;
+  const int bk = best_k[0];
+  uint32_t word = 0;
+  if (bk >= 0 && 32 * w < n) {
+    if (det0 && bk == 0)
+      word = det[(size_t)r * det_words + w];
+    else
+      word = round_word(q + (size_t)r * ldq, w, r, (uint32_t)bk, key0, key1);
+  }
+  S_rows[(size_t)r * row_words + w] = word;
+}
+
+// Best candidate's R rows: lane per stage t, Algorithm 2's right-to-left
+// repair reading the S rows written above; bits of higher chunks come back
+// from the lane's own output row.
+__global__ void __launch_bounds__(kWave) ckm_best_closure_kernel(int32_t n, int32_t row_words,
+                                                                 const int32_t* __restrict__ user_ptr,
+                                                                 const int32_t* __restrict__ user_idx,
+                                                                 const int32_t* __restrict__ best_k,
+                                                                 const uint32_t* __restrict__ S_rows,
+                                                                 uint32_t* __restrict__ R_rows) {
+  const int t = blockIdx.x * kWave + threadIdx.x;
+  const bool active = t < n;
+  const int tmax = min(n - 1, (int)blockIdx.x * kWave + kWave - 1);
+  const int bk = best_k[0];
+  uint32_t* Rrow = R_rows + (size_t)(active ? t : 0) * row_words;
+  const uint32_t* S0 = S_rows + (size_t)(active ? t : 0) * row_words;
+  const uint32_t* S1 = S_rows + (size_t)((active && t + 1 < n) ? t + 1 : 0) * row_words;
+  if (bk < 0) {
+    if (active)
+      for (int w = 0; w < row_words; ++w) Rrow[w] = 0u;
+    return;
+  }
+  for (int c = tmax >> 5; c >= 0; --c) {
+    const bool lane_chunk = active && c <= (t >> 5);
+    const uint32_t w0 = lane_chunk ? S0[c] : 0u;
+    const uint32_t w1 = (lane_chunk && t + 1 < n) ? S1[c] : 0u;
+    uint32_t rw = 0;
+    for (int jj = 31; jj >= 0; --jj) {
+      const int v = 32 * c + jj;
+      if (v > tmax) continue;
+      uint32_t anyU = 0;
+      const int ue = user_ptr[v + 1];
+      for (int e = user_ptr[v]; e < ue; ++e) {
+        const int u = user_idx[e];
+        if (u > tmax) break;
+        if (lane_chunk && u <= t) {
+          const uint32_t word = ((u >> 5) == c) ? rw : Rrow[u >> 5];
+          anyU |= bit(word, u & 31);
+        }
+      }
+      uint32_t r = 0;
+      if (lane_chunk && v <= t)
+        r = (v == t) ? 1u : ((bit(w1, jj) | anyU) & ~bit(w0, jj) & 1u);
+      rw |= r << jj;
+    }
+    if (lane_chunk) Rrow[c] = rw;
+  }
+  if (active)
+    for (int w = (t >> 5) + 1; w < row_words; ++w) Rrow[w] = 0u;
+}
+
+template <typename T>
+T* at(char* work, size_t off) { return reinterpret_cast<T*>(work + off); }
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,
+                           char* work, hipStream_t stream) {
+  hipLaunchKernelGGL(ckm_quantize_kernel, dim3(g.n), dim3(256), 0, stream, d_s, ld, g.n, L.ldq,
+                     L.det_words, at<uint32_t>(work, L.q_off), at<uint32_t>(work, L.det_off),
+                     at<int32_t>(work, L.nan_off));
+  return hipGetLastError();
+}
+
+hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
+                           uint32_t flags, int32_t splits, char* work, hipStream_t stream) {
+  EvalArgs a;
+  a.n = g.n;
+  a.K = K;
+  a.splits = splits;
+  a.ldq = L.ldq;
+  a.det_words = L.det_words;
+  a.key0 = (uint32_t)(seed & 0xFFFFFFFFu);
+  a.key1 = (uint32_t)(seed >> 32);
+  a.det0 = (flags & CKM_F_DET0) ? 1u : 0u;
+  a.base = g.base;
+  a.q = at<uint32_t>(work, L.q_off);
+  a.det = at<uint32_t>(work, L.det_off);
+  a.M = g.d_M;
+  a.C = g.d_C;
+  a.user_ptr = g.d_user_ptr;
+  a.user_idx = g.d_user_idx;
+  a.dep_ptr = g.d_dep_ptr;
+  a.dep_idx = g.d_dep_idx;
+  a.dep_upos = g.d_dep_upos;
+  a.part_peak = at<int64_t>(work, L.part_peak_off);
+  a.part_cost = at<int64_t>(work, L.part_cost_off);
+  a.hdr = at<int32_t>(work, L.hdr_off);
+  const int groups = (K + kWave - 1) / kWave;
+  const size_t lds_bytes = 2u * (size_t)((g.n >> 5) + 1) * kWave * sizeof(uint32_t);
+  if (lds_bytes > 65536) {
+    hipError_t e = hipFuncSetAttribute((const void*)ckm_eval_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(ckm_eval_kernel, dim3(groups, splits), dim3(kWave), lds_bytes, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
+                         int64_t budget, uint32_t flags, int64_t* d_peak, int64_t* d_cost,
+                         uint8_t* d_feasible, int32_t* d_best_k, uint64_t* d_best_S,
+                         uint64_t* d_best_R, int32_t* d_status, char* work, hipStream_t stream) {
+  const int rb = (K + 255) / 256;
+  hipLaunchKernelGGL(ckm_reduce_kernel, dim3(rb), dim3(256), 0, stream, K,
+                     at<const int32_t>(work, L.hdr_off), at<const int64_t>(work, L.part_peak_off),
+                     at<const int64_t>(work, L.part_cost_off), budget, d_peak, d_cost, d_feasible,
+                     at<Best>(work, L.best_off));
+  hipLaunchKernelGGL(ckm_argmin_kernel, dim3(1), dim3(256), 0, stream, rb,
+                     at<const Best>(work, L.best_off), g.n, at<const int32_t>(work, L.nan_off),
+                     d_best_k, d_status);
+  if (d_best_S || d_best_R) {
+    uint32_t* srows = d_best_S ? reinterpret_cast<uint32_t*>(d_best_S) : at<uint32_t>(work, L.srows_off);
+    dim3 grid((L.row_words + 255) / 256, g.n);
+    hipLaunchKernelGGL(ckm_best_rows_kernel, grid, dim3(256), 0, stream,
+                       at<const uint32_t>(work, L.q_off), at<const uint32_t>(work, L.det_off), g.n,
+                       L.ldq, L.det_words, L.row_words, (uint32_t)(seed & 0xFFFFFFFFu),
+                       (uint32_t)(seed >> 32), (flags & CKM_F_DET0) ? 1u : 0u, d_best_k, srows);
+    if (d_best_R) {
+      hipLaunchKernelGGL(ckm_best_closure_kernel, dim3((g.n + kWave - 1) / kWave), dim3(kWave), 0,
+                         stream, g.n, L.row_words, g.d_user_ptr, g.d_user_idx, d_best_k, srows,
+                         reinterpret_cast<uint32_t*>(d_best_R));
+    }
+  }
+  return hipGetLastError();
+}
+
+}  // namespace ckm

@@ -1,0 +1,101 @@
+"""Host-side checks of libckm that need no GPU: the library loads, exports
+every function include/ckm.h declares, and rejects malformed graphs and
+arguments before touching the device."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from conftest import ROOT
+from paper_1910_02653_amd import ckm
+
+HEADER = os.path.join(ROOT, "include", "ckm.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ckm_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert set(names) == set(ckm.EXPORTS)
+    L = ckm.lib()
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_no_torch_types_in_header():
+    text = open(HEADER).read()
+    assert "torch" not in re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+
+
+def create(n, deps, cost=None, size=None, m_input=0, m_param=0, users=None):
+    ptr = np.zeros(n + 1, np.int32)
+    flat = []
+    for j, d in enumerate(deps):
+        flat.extend(d)
+        ptr[j + 1] = len(flat)
+    idx = np.asarray(flat if flat else [0], np.int32)
+    cost = np.ones(n, np.int64) if cost is None else np.asarray(cost, np.int64)
+    size = np.ones(n, np.int64) if size is None else np.asarray(size, np.int64)
+    h = C.c_void_p()
+    up = ui = None
+    if users is not None:
+        up = np.zeros(n + 1, np.int32)
+        uf = []
+        for i, u in enumerate(users):
+            uf.extend(u)
+            up[i + 1] = len(uf)
+        ui = np.asarray(uf if uf else [0], np.int32)
+    st = ckm.lib().ckm_graph_create(n, ptr.ctypes.data_as(C.c_void_p), idx.ctypes.data_as(C.c_void_p),
+                                    None if up is None else up.ctypes.data_as(C.c_void_p),
+                                    None if ui is None else ui.ctypes.data_as(C.c_void_p),
+                                    cost.ctypes.data_as(C.c_void_p), size.ctypes.data_as(C.c_void_p),
+                                    m_input, m_param, C.byref(h))
+    return st, h
+
+
+@pytest.mark.parametrize("case,status", [
+    (dict(n=0, deps=[]), ckm.E_INVALID_ARG),
+    (dict(n=4097, deps=[[]] * 4097), ckm.E_UNSUPPORTED),
+    (dict(n=3, deps=[[], [1], []]), ckm.E_GRAPH),             # self edge
+    (dict(n=3, deps=[[], [2], []]), ckm.E_GRAPH),             # forward in numbering
+    (dict(n=3, deps=[[], [0], [1, 1]]), ckm.E_GRAPH),         # duplicate
+    (dict(n=3, deps=[[], [0], [-1]]), ckm.E_GRAPH),           # out of range
+    (dict(n=3, deps=[[], [0], [1]], users=[[1], [], [2]]), ckm.E_GRAPH),   # users != transpose
+    (dict(n=3, deps=[[], [0], [1]], users=[[2], [1], []]), ckm.E_GRAPH),
+    (dict(n=2, deps=[[], [0]], cost=[1, -1]), ckm.E_INVALID_ARG),
+    (dict(n=2, deps=[[], [0]], size=[-5, 1]), ckm.E_INVALID_ARG),
+    (dict(n=2, deps=[[], [0]], m_param=-1), ckm.E_INVALID_ARG),
+    (dict(n=2, deps=[[], [0]], size=[2 ** 52, 2 ** 52]), ckm.E_OVERFLOW),      # sum M reaches 2^53
+    (dict(n=2, deps=[[], [0]], size=[1, 1], m_param=2 ** 52), ckm.E_OVERFLOW),
+    (dict(n=2, deps=[[], [0]], cost=[2 ** 53 - 1, 1]), ckm.E_OVERFLOW),
+    (dict(n=4096, deps=[[]] * 4096, cost=[2 ** 52] + [0] * 4095), ckm.E_OVERFLOW),  # n * sum C
+])
+def test_graph_validation_errors(case, status):
+    st, h = create(**case)
+    assert st == status, ckm.last_error()
+    assert not h.value
+    assert ckm.last_error()
+
+
+def test_null_arguments_rejected():
+    L = ckm.lib()
+    h = C.c_void_p()
+    assert L.ckm_graph_create(2, None, None, None, None, None, None, 0, 0, C.byref(h)) == ckm.E_INVALID_ARG
+    assert L.ckm_graph_create(2, None, None, None, None, None, None, 0, 0, None) == ckm.E_INVALID_ARG
+    sz = C.c_size_t()
+    assert L.ckm_workspace_size(None, 4, C.byref(sz)) == ckm.E_INVALID_ARG
+    assert L.ckm_round_eval(None, None, 0, 4, 0, 0, 0, None, None, None, None, None, None) == ckm.E_INVALID_ARG
+    assert L.ckm_evaluate_async(None, 4, 0, 0, 0, None, 0, None) == ckm.E_INVALID_ARG
+    assert L.ckm_select_async(None, 4, 0, 0, 0, None, None, None, None, None, None, None, None, 0,
+                              None) == ckm.E_INVALID_ARG
+    assert L.ckm_quantize_async(None, None, 0, None, 0, None) == ckm.E_INVALID_ARG
+    assert L.ckm_round_eval_async(None, None, 0, 4, 0, 0, 0, None, None, None, None, None, None, None, None,
+                                  0, None) == ckm.E_INVALID_ARG
+    assert L.ckm_graph_num_nodes(None) == -1
+    L.ckm_graph_destroy(None)

@@ -1,0 +1,288 @@
+"""Bit-exact parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Every result is integer (peak bytes, cost, feasible flags, best index, S and
+R bit rows), so the bar is equality. Inputs are the seeded synthetic
+workloads (paper_1910_02653_amd.workloads); expected values come from the
+oracle only.
+"""
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+import pytest
+
+from oracle import ref
+from paper_1910_02653_amd import ckm
+from paper_1910_02653_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+THREADS = min(16, os.cpu_count() or 4)
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def oracle_candidates(w, ks, flags=0, seed=None):
+    """{k: (peak, cost)} from the oracle, candidates evaluated on a thread pool."""
+    ww = w if seed is None else w.replace(seed=seed)
+    q = ref.quantize(ww.s_frac)
+    with ThreadPoolExecutor(THREADS) as ex:
+        res = list(ex.map(lambda k: ref.eval_candidate(ww, int(k), flags=flags, q=q), ks))
+    return dict(zip([int(k) for k in ks], res))
+
+
+def lexi_best(peak, cost, budget):
+    cands = [(int(cost[k]), int(peak[k]), k) for k in range(len(peak)) if peak[k] <= budget]
+    return min(cands)[2] if cands else -1
+
+
+def check_full(w, got, flags=0, budget=None, seed=None):
+    """Compare a GPU result over all K candidates with the oracle."""
+    budget = w.budget if budget is None else budget
+    orc = oracle_candidates(w, range(w.K), flags=flags, seed=seed)
+    peak = np.array([orc[k][0] for k in range(w.K)], np.int64)
+    cost = np.array([orc[k][1] for k in range(w.K)], np.int64)
+    bad = np.nonzero((got["peak"] != peak) | (got["cost"] != cost))[0]
+    assert bad.size == 0, "mismatch at k=%s gpu=%s oracle=%s" % (
+        bad[:5], [(int(got["peak"][k]), int(got["cost"][k])) for k in bad[:5]],
+        [orc[int(k)] for k in bad[:5]])
+    assert np.array_equal(got["feasible"], (peak <= budget).astype(np.uint8))
+    bk = lexi_best(peak, cost, budget)
+    assert got["best_k"] == bk
+    check_rows(w, got, bk, flags, seed)
+    return peak, cost
+
+
+def check_rows(w, got, bk, flags=0, seed=None):
+    if got.get("best_S") is None:
+        return
+    if bk < 0:
+        assert not got["best_S"].any() and not got["best_R"].any()
+        return
+    ww = w if seed is None else w.replace(seed=seed)
+    _, _, S, R = ref.eval_candidate(ww, bk, flags=flags, want_rows=True)
+    assert np.array_equal(got["best_S"], ref.pack_rows(S)), "best_S differs"
+    assert np.array_equal(got["best_R"], ref.pack_rows(R)), "best_R differs"
+
+
+def gpu_round_eval(w, K=None, seed=None, budget=None, flags=0):
+    g = ckm.Graph.from_workload(w)
+    try:
+        return g.round_eval(w.s_frac, w.K if K is None else K, w.seed if seed is None else seed,
+                            w.budget if budget is None else budget, flags)
+    finally:
+        g.close()
+
+
+def test_single_hip_runtime_in_process():
+    """libckm and torch share one HIP runtime (no second libamdhip64 mapped)."""
+    import torch
+    ckm.lib()
+    torch.zeros(1, device="cuda")
+    paths = set()
+    with open("/proc/self/maps") as f:
+        for line in f:
+            if "libamdhip64" in line:
+                paths.add(line.split()[-1])
+    assert len(paths) == 1, paths
+
+
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_small_configs_full_parity(cfg):
+    w = wl.config(cfg)
+    log("config %d n=%d K=%d" % (cfg, w.n, w.K))
+    got = gpu_round_eval(w)
+    peak, _ = check_full(w, got)
+    # feasible-rich: budget at the median candidate peak exercises the argmin
+    med = int(np.median(peak))
+    log("config %d median budget %d" % (cfg, med))
+    got2 = gpu_round_eval(w, budget=med)
+    check_full(w, got2, budget=med)
+    assert got2["best_k"] >= 0
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_small_configs_sparse_checkpoints(cfg):
+    """S* scaled by 0.2: few checkpoints, long recomputation closures."""
+    w = wl.config(cfg)
+    w = w.replace(s_frac=0.2 * w.s_frac, K=min(w.K, 128))
+    log("config %d sparse K=%d" % (cfg, w.K))
+    got = gpu_round_eval(w)
+    peak, _ = check_full(w, got)
+    med = int(np.median(peak))
+    check_full(w, gpu_round_eval(w, budget=med), budget=med)
+
+
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_det0_candidate(cfg):
+    w = wl.config(cfg)
+    log("config %d DET0" % cfg)
+    got = gpu_round_eval(w, flags=ckm.F_DET0)
+    check_full(w, got, flags=ckm.F_DET0)
+    big = int(got["peak"].max())
+    got2 = gpu_round_eval(w, flags=ckm.F_DET0, budget=big)
+    check_full(w, got2, flags=ckm.F_DET0, budget=big)
+
+
+def test_config4_transformer_full_parity():
+    w = wl.config(4)
+    log("config 4 n=%d K=%d" % (w.n, w.K))
+    got = gpu_round_eval(w)
+    peak, _ = check_full(w, got)
+    med = int(np.median(peak))
+    log("config 4 median budget")
+    check_full(w, gpu_round_eval(w, budget=med), budget=med)
+
+
+def test_config4_sparse_sampled():
+    w = wl.config(4)
+    w = w.replace(s_frac=0.2 * w.s_frac, K=96)
+    log("config 4 sparse K=96")
+    got = gpu_round_eval(w)
+    check_full(w, got)
+
+
+def test_config5_random_dag_sampled():
+    """n = 4001, K = 4096: the GPU evaluates every candidate; the oracle checks
+    a spread of candidates (each is independent of the others)."""
+    w = wl.config(5)
+    log("config 5 n=%d K=%d" % (w.n, w.K))
+    got = gpu_round_eval(w)
+    rng = np.random.default_rng(5)
+    ks = sorted(set([0, 1, 63, 64, 65, 127, 2047, 4031, 4095] + list(rng.integers(0, w.K, 23))))
+    orc = oracle_candidates(w, ks)
+    for k in ks:
+        assert (int(got["peak"][k]), int(got["cost"][k])) == orc[k], k
+    assert np.array_equal(got["feasible"], (got["peak"] <= w.budget).astype(np.uint8))
+    assert got["best_k"] == lexi_best(got["peak"], got["cost"], w.budget)
+    # a budget that admits some candidates: argmin and its rows
+    budget = int(np.quantile(got["peak"], 0.3))
+    got2 = gpu_round_eval(w, budget=budget)
+    assert np.array_equal(got2["peak"], got["peak"]) and np.array_equal(got2["cost"], got["cost"])
+    bk = lexi_best(got2["peak"], got2["cost"], budget)
+    assert got2["best_k"] == bk >= 0
+    orc_bk = oracle_candidates(w, [bk])[bk]
+    assert (int(got2["peak"][bk]), int(got2["cost"][bk])) == orc_bk
+    check_rows(w, got2, bk)
+
+
+SWEEP = [(1, 3, "uniform"), (2, 5, "uniform"), (3, 4, "beta"), (5, 9, "binary"), (17, 64, "sparse"),
+         (31, 63, "uniform"), (32, 65, "beta"), (33, 1, "sparse"), (63, 64, "uniform"), (64, 130, "beta"),
+         (65, 7, "sparse"), (100, 33, "binary"), (127, 64, "uniform"), (128, 65, "sparse"), (129, 40, "beta"),
+         (200, 70, "uniform"), (257, 20, "sparse"), (300, 64, "beta")]
+
+
+@pytest.mark.parametrize("n,K,kind", SWEEP)
+def test_random_dag_sweep(n, K, kind):
+    w = wl.random_dag(n, seed=n * 7 + K, K=K, s_kind=kind, window=min(n, 24), max_deg=3,
+                      max_size=1000, max_cost=1000, budget_pct=55.0)
+    log("random dag n=%d K=%d %s" % (n, K, kind))
+    got = gpu_round_eval(w)
+    peak, _ = check_full(w, got)
+    med = int(np.median(peak))
+    check_full(w, gpu_round_eval(w, budget=med), budget=med)
+
+
+def test_dense_wide_graph():
+    """Many deps and users per node (fan-in / fan-out up to 40)."""
+    w = wl.random_dag(150, seed=11, K=70, max_deg=40, window=150, s_kind="uniform", budget_pct=60.0)
+    log("dense wide graph")
+    got = gpu_round_eval(w)
+    peak, _ = check_full(w, got)
+
+
+def test_max_nodes_chain():
+    """n = 4096 (the largest graph): a chain with a mirrored backward pass."""
+    F = 2047
+    fwd = [[]] + [[v - 1] for v in range(1, F)]
+    deps, size, cost, _ = wl.mirror_training_graph(fwd, np.full(F, 3 << 20), np.full(F, 50), 4, 7)
+    deps.append([len(deps) - 1])           # one extra node: n = 4096
+    size = np.append(size, 1 << 20)
+    cost = np.append(cost, 9)
+    ptr, idx = wl.csr_from_deps(deps)
+    n = len(deps)
+    assert n == 4096
+    w = wl.Workload("chain4096", n, ptr, idx, cost, size, 1 << 20, 1 << 20, wl.s_frac_uniform(n, 9), 64, 9,
+                    1 << 40)
+    log("max nodes chain")
+    got = gpu_round_eval(w)
+    orc = oracle_candidates(w, [0, 37, 63])
+    for k, v in orc.items():
+        assert (int(got["peak"][k]), int(got["cost"][k])) == v
+    assert got["best_k"] == lexi_best(got["peak"], got["cost"], w.budget)
+    check_rows(w, got, got["best_k"])
+
+
+def test_async_stages_and_split_invariance():
+    """The staged async calls give the same bits for any stage split (a race
+    or a split-boundary error would change them)."""
+    import torch
+    w = wl.config(3)
+    w = w.replace(K=200)
+    g = ckm.Graph.from_workload(w)
+    d_s = torch.from_numpy(w.s_frac).cuda()
+    work = g.alloc_work(w.K)
+    ref_out = None
+    budget = w.budget * 3
+    for splits in (1, 2, 7, 64, 10 ** 6, 0):
+        log("splits %d" % splits)
+        out = g.alloc_outputs(w.K)
+        g.quantize_async(d_s, work)
+        g.evaluate_async(w.K, w.seed, 0, work, stage_splits=splits)
+        g.select_async(w.K, w.seed, budget, 0, out, work)
+        torch.cuda.synchronize()
+        res = dict(peak=out["peak"].cpu().numpy(), cost=out["cost"].cpu().numpy(),
+                   feasible=out["feasible"].cpu().numpy(), best_k=int(out["best_k"].item()),
+                   best_S=ckm.rows_to_numpy(out["best_S"]), best_R=ckm.rows_to_numpy(out["best_R"]))
+        assert int(out["status"].item()) == ckm.OK
+        if ref_out is None:
+            check_full(w, res, budget=budget)
+            ref_out = res
+        else:
+            for key in ("peak", "cost", "feasible", "best_S", "best_R"):
+                assert np.array_equal(res[key], ref_out[key]), (splits, key)
+            assert res["best_k"] == ref_out["best_k"]
+    # the one-call async form agrees too, on a strided S*
+    big = torch.zeros((w.n, w.n + 5), dtype=torch.float64, device="cuda")
+    big[:, :w.n] = d_s
+    out = g.alloc_outputs(w.K)
+    g.round_eval_async(big, w.K, w.seed, budget, 0, out, work)
+    torch.cuda.synchronize()
+    assert np.array_equal(out["peak"].cpu().numpy(), ref_out["peak"])
+    assert int(out["best_k"].item()) == ref_out["best_k"]
+    g.close()
+
+
+def test_nan_reported():
+    import torch
+    w = wl.config(2).replace(K=8)
+    s = w.s_frac.copy()
+    s[50, 3] = np.nan
+    with pytest.raises(ckm.CkmError) as e:
+        gpu_round_eval(w.replace(s_frac=s))
+    assert e.value.status == ckm.E_INVALID_ARG
+    g = ckm.Graph.from_workload(w)
+    work = g.alloc_work(w.K)
+    out = g.alloc_outputs(w.K)
+    g.round_eval_async(torch.from_numpy(s).cuda(), w.K, w.seed, w.budget, 0, out, work)
+    torch.cuda.synchronize()
+    assert int(out["status"].item()) == ckm.E_INVALID_ARG
+    s2 = w.s_frac.copy()
+    s2[3, 50] = np.nan                      # above the diagonal: never read
+    g.round_eval_async(torch.from_numpy(s2).cuda(), w.K, w.seed, w.budget, 0, out, work)
+    torch.cuda.synchronize()
+    assert int(out["status"].item()) == ckm.OK
+    g.close()
+
+
+def test_out_of_range_s_values_clamped():
+    w = wl.config(2).replace(K=64)
+    s = w.s_frac * 3.0 - 1.0               # values in [-1, 2], clamped to [0, 1]
+    s = np.tril(s, -1)
+    w2 = w.replace(s_frac=s)
+    got = gpu_round_eval(w2)
+    check_full(w2, got)
