@@ -203,7 +203,8 @@ ckm_status ckm_graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* de
   const size_t off_dp = align256(off_ui + Ea * sizeof(int32_t));
   const size_t off_di = align256(off_dp + (n + 1) * sizeof(int32_t));
   const size_t off_uo = align256(off_di + Ea * sizeof(int32_t));
-  const size_t total = align256(off_uo + Ea * sizeof(int32_t));
+  const size_t off_rec = align256(off_uo + Ea * sizeof(int32_t));
+  const size_t total = align256(off_rec + (size_t)n * ckm::kNodeRecBytes);
   std::vector<char> host(total, 0);
   std::vector<double> Md(n), Cd(n);
   for (int32_t v = 0; v < n; ++v) {
@@ -217,6 +218,8 @@ ckm_status ckm_graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* de
   memcpy(host.data() + off_dp, dp.data(), (n + 1) * sizeof(int32_t));
   if (E) memcpy(host.data() + off_di, di.data(), E * sizeof(int32_t));
   if (E) memcpy(host.data() + off_uo, upos.data(), E * sizeof(int32_t));
+  ckm::build_node_records(n, Md.data(), Cd.data(), dp.data(), di.data(), up.data(), ui.data(),
+                          host.data() + off_rec);
   e = hipMalloc(&g->d_mem, total);
   if (e != hipSuccess) {
     delete g;
@@ -237,6 +240,7 @@ ckm_status ckm_graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* de
   g->d_dep_ptr = reinterpret_cast<const int32_t*>(base + off_dp);
   g->d_dep_idx = reinterpret_cast<const int32_t*>(base + off_di);
   g->d_dep_upos = reinterpret_cast<const int32_t*>(base + off_uo);
+  g->d_recs = base + off_rec;
   *out = g;
   return CKM_OK;
 }

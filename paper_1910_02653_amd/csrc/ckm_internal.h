@@ -25,11 +25,19 @@ struct ckm_graph {
   const int32_t* d_dep_ptr = nullptr;
   const int32_t* d_dep_idx = nullptr;
   const int32_t* d_dep_upos = nullptr;
+  const void* d_recs = nullptr;  // n node records of ckm::kNodeRecBytes (see ckm_kernels.hip)
 };
 
 namespace ckm {
 
 constexpr int kWave = 64;
+constexpr int kNodeRecBytes = 128;
+
+// Host-side builder of the per-node records the evaluate kernel reads
+// (layout documented with NodeRec in ckm_kernels.hip). Writes n records.
+void build_node_records(int32_t n, const double* M, const double* C, const int32_t* dep_ptr,
+                        const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx,
+                        void* out);
 
 // Work-buffer layout for (n, K). Offsets are bytes from the buffer start,
 // each 256-byte aligned.

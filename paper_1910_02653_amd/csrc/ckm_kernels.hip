@@ -15,8 +15,10 @@
 // integer and the result is identical to int64 arithmetic in any order.
 #include <hip/hip_runtime.h>
 
+#include <climits>
 #include <cmath>
 #include <cstdint>
+#include <cstring>
 
 #include "ckm_internal.h"
 
@@ -30,6 +32,17 @@ constexpr uint32_t kPhiloxM0 = 0xD2511F53u;
 constexpr uint32_t kPhiloxM1 = 0xCD9E8D57u;
 constexpr uint32_t kPhiloxW0 = 0x9E3779B9u;
 constexpr uint32_t kPhiloxW1 = 0xBB67AE85u;
+
+// Read-only data that every lane of a wave reads at the same address (graph
+// CSR, sizes, costs, thresholds): load it through the constant address space
+// so that uniform reads become scalar loads through the scalar cache.
+template <typename T>
+using cptr = const __attribute__((address_space(4))) T*;
+
+template <typename T>
+__host__ __device__ __forceinline__ cptr<T> as_const(const T* p) {
+  return (cptr<T>)(p);
+}
 
 __device__ __forceinline__ void philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
                                               uint32_t k0, uint32_t k1, uint32_t x[4]) {
@@ -52,7 +65,8 @@ __device__ __forceinline__ void philox4x32_10(uint32_t c0, uint32_t c1, uint32_t
 // 32 rounding decisions of row r, candidate k: bits i = 32w .. 32w+31 of
 // S_k[r] (Section 5.1 randomized rounding, thresholds q). Entries i >= r
 // have q = 0 and round to 0.
-__device__ __forceinline__ uint32_t round_word(const uint32_t* __restrict__ qrow, int w, int r,
+template <typename QPtr>
+__device__ __forceinline__ uint32_t round_word(QPtr qrow, int w, int r,
                                                uint32_t k, uint32_t key0, uint32_t key1) {
   uint32_t word = 0;
 #pragma unroll
@@ -70,20 +84,90 @@ __device__ __forceinline__ uint32_t round_word(const uint32_t* __restrict__ qrow
   return word;
 }
 
+// Per-node record read once per node visit (one 128-byte scalar load).
+// Masks are relative to the node v: bit d <-> node v + 1 + d, d < 64.
+struct DepSlot {
+  int32_t i;              // a dep of v
+  uint32_t lmask_lo;      // users u of i with v < u <= v + 32
+  uint32_t lmask_hi;      //                  v + 32 < u <= v + 64
+  int32_t far_later;      // the user of i beyond v + 64, or INT32_MAX
+  double M;               // M_i
+};
+constexpr int kRecDeps = 4;
+constexpr uint32_t kRecSlow = 1u << 31;   // node does not fit: use the CSR lists
+struct NodeRec {
+  double M, C;            // M_v, C_v
+  uint32_t umask_lo;      // users u of v with u <= v + 32
+  uint32_t umask_hi;      //                  v + 32 < u <= v + 64
+  int32_t far_user;       // the user of v beyond v + 64, or INT32_MAX
+  uint32_t info;          // number of deps (bits 0-2) | kRecSlow
+  DepSlot dep[kRecDeps];
+};
+static_assert(sizeof(NodeRec) == kNodeRecBytes, "node record layout");
+
+__device__ __forceinline__ double dbl(uint32_t lo, uint32_t hi) {
+  return __hiloint2double((int)hi, (int)lo);
+}
+
+struct DepRegs {
+  int i;
+  uint32_t lmask_lo, lmask_hi;
+  int far_later;
+  double M;
+};
+
+// The 32 dwords of a node record in vector registers (every lane holds the
+// same values).
+struct RecRegs {
+  uint32_t w[kNodeRecBytes / 4];
+  __device__ double M() const { return dbl(w[0], w[1]); }
+  __device__ double C() const { return dbl(w[2], w[3]); }
+  __device__ uint32_t umask_lo() const { return w[4]; }
+  __device__ uint32_t umask_hi() const { return w[5]; }
+  __device__ int far_user() const { return (int)w[6]; }
+  __device__ uint32_t info() const { return w[7]; }
+  __device__ DepRegs dep(int sl) const {
+    const uint32_t* d = w + 8 + 6 * sl;
+    return DepRegs{(int)d[0], d[1], d[2], (int)d[3], dbl(d[4], d[5])};
+  }
+};
+
+// A zero the compiler cannot see through: added to an address, it makes a
+// wave-uniform load a vector load, whose completion counter is in order and
+// so can run one node ahead of its use.
+__device__ __forceinline__ int opaque_zero() {
+  int z;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+  return z;
+}
+
+__device__ __forceinline__ void load_rec(RecRegs& r, const uint4* __restrict__ recs, int v, int lane_off) {
+  const uint4* p = recs + (size_t)v * (kNodeRecBytes / 16) + lane_off;
+#pragma unroll
+  for (int q = 0; q < kNodeRecBytes / 16; ++q) {
+    const uint4 x = p[q];
+    r.w[4 * q + 0] = x.x;
+    r.w[4 * q + 1] = x.y;
+    r.w[4 * q + 2] = x.z;
+    r.w[4 * q + 3] = x.w;
+  }
+}
+
 struct EvalArgs {
   int32_t n, K, splits, ldq, det_words;
   uint32_t key0, key1;
   uint32_t det0;                 // CKM_F_DET0 given
   double base;                   // M_in + 2 M_param
-  const uint32_t* __restrict__ q;
-  const uint32_t* __restrict__ det;
-  const double* __restrict__ M;
-  const double* __restrict__ C;
-  const int32_t* __restrict__ user_ptr;
-  const int32_t* __restrict__ user_idx;
-  const int32_t* __restrict__ dep_ptr;
-  const int32_t* __restrict__ dep_idx;
-  const int32_t* __restrict__ dep_upos;
+  cptr<uint32_t> q;
+  cptr<uint32_t> det;
+  cptr<double> M;
+  cptr<double> C;
+  cptr<int32_t> user_ptr;
+  cptr<int32_t> user_idx;
+  cptr<int32_t> dep_ptr;
+  cptr<int32_t> dep_idx;
+  cptr<int32_t> dep_upos;
+  const uint4* __restrict__ recs;
   int64_t* __restrict__ part_peak;   // [splits][K]
   int64_t* __restrict__ part_cost;   // [splits][K]
   int32_t* __restrict__ hdr;
@@ -109,8 +193,8 @@ __device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bo
     for (int w = 0; w < nw; ++w) dst[w * kWave] = 0u;
     return;
   }
-  const uint32_t* qrow = a.q + (size_t)r * a.ldq;
-  const uint32_t* drow = a.det + (size_t)r * a.det_words;
+  cptr<uint32_t> qrow = a.q + (size_t)r * a.ldq;
+  cptr<uint32_t> drow = a.det + (size_t)r * a.det_words;
   for (int w = 0; w < nw; ++w) {
     uint32_t word = round_word(qrow, w, r, k, a.key0, a.key1);
     if (det_lane) word = drow[w];
@@ -120,64 +204,115 @@ __device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bo
 
 __device__ __forceinline__ uint32_t bit(uint32_t word, int pos) { return (word >> pos) & 1u; }
 
+// R bit of node u for a lane at node v of the right-to-left scan (v < u <= t):
+// nodes v+1 .. v+64 are in the window (Rlo: v+1 .. v+32, Rhi: v+33 .. v+64);
+// farther nodes lie in chunks already finished, whose R words are in A.
+__device__ __forceinline__ uint32_t r_bit(int u, int v, uint32_t Rlo, uint32_t Rhi, const uint32_t* A) {
+  const int d = u - v - 1;
+  if (d < 32) return bit(Rlo, d);
+  if (d < 64) return bit(Rhi, d - 32);
+  return bit(A[(u >> 5) * kWave], u & 31);
+}
+
+// R bit of a far node u (more than 64 above the current node, so its chunk is
+// finished and stored in A), or 0 when u > t (including "none" = INT32_MAX).
+// The read address is clamped so that it always stays inside the row.
+__device__ __forceinline__ uint32_t far_bit(int u, int t, const uint32_t* A) {
+  const int uc = min(u, t);
+  const uint32_t b = bit(A[(uc >> 5) * kWave], uc & 31);
+  return (u <= t) ? b : 0u;
+}
+
 // One stage t of one candidate (per lane). On entry A holds S_t and B holds
 // S_{t+1} (words 0 .. t/32). Algorithm 2's repair of R runs right to left
-// (reverse topological order); in the same pass the U recurrence of Section
-// 4.4 is evaluated in suffix form:
+// (reverse topological order), so every user of node v is decided before v:
+// v is computed iff it is node t (constraint 4a), or it is not checkpointed
+// and is kept for the next stage (1c) or needed by a computed user (1b).
+// In the same pass the U recurrence of Section 4.4 is evaluated in suffix
+// form:
 //   val_k = sum_{j>=k} freed_j - sum_{j>k} alloc_j,   U_{t,k} = U_end + val_k,
 // so the stage peak is U_end + max_k val_k with U_end = U_{t,0} - Y, Y being
-// the suffix value after node 0. R_t overwrites S_t in A, chunk by chunk.
+// the suffix value after node 0. freed_v collects FREE(t,i,v) M_i over
+// i in Deps[v] u {v}: v computed, i not kept, and no computed user of i
+// after v. The R bits of the 64 nodes above v live in two registers; R_t
+// overwrites S_t in A chunk by chunk. Node records are read with vector
+// loads one node ahead (the scan order is v = t, t-1, ..., 0).
 __device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, uint32_t* A, const uint32_t* B,
                                            double& stage_peak, double& stage_cost) {
   double U0 = a.base, Y = 0.0, maxv = -INFINITY, cost = 0.0;
+  uint32_t Rlo = 0, Rhi = 0;
+  const int lane_off = opaque_zero();
+  RecRegs nxt;
+  load_rec(nxt, a.recs, t, lane_off);
   for (int c = t >> 5; c >= 0; --c) {
     const uint32_t w0 = A[c * kWave];
     const uint32_t w1 = B[c * kWave];
-    uint32_t rw = 0;
     const int jtop = min(31, t - 32 * c);
     for (int jj = jtop; jj >= 0; --jj) {
       const int v = 32 * c + jj;
+      const RecRegs rec = nxt;
+      load_rec(nxt, a.recs, max(v - 1, 0), lane_off);
       const uint32_t s0 = bit(w0, jj);
       const uint32_t s1 = bit(w1, jj);
-      // does any user of v computed in this stage need it?
-      uint32_t anyU = 0;
-      const int ue = a.user_ptr[v + 1];
-      for (int e = a.user_ptr[v]; e < ue; ++e) {
-        const int u = a.user_idx[e];
-        if (u > t) break;
-        const uint32_t word = ((u >> 5) == c) ? rw : A[(u >> 5) * kWave];
-        anyU |= bit(word, u & 31);
-      }
-      // (4a) R_tt = 1; (1c) keep-for-next-stage needs v in memory; (1b) a
-      // computed user needs v unless it is checkpointed.
-      const uint32_t r = (v == t) ? 1u : ((s1 | anyU) & ~s0 & 1u);
-      rw |= r << jj;
-      const double Mv = a.M[v];
-      // FREE(t, v, v): computed, not kept, no computed user
-      double freed = (r & ~s1 & ~anyU & 1u) ? Mv : 0.0;
-      // FREE(t, i, v) for deps i: v is the last computed user and i not kept
-      const int de = a.dep_ptr[v + 1];
-      for (int e = a.dep_ptr[v]; e < de; ++e) {
-        const int i = a.dep_idx[e];
-        const uint32_t wi = ((i >> 5) == c) ? w1 : B[(i >> 5) * kWave];
-        const uint32_t si1 = bit(wi, i & 31);
-        uint32_t later = 0;
-        const int le = a.user_ptr[i + 1];
-        for (int e2 = a.dep_upos[e]; e2 < le; ++e2) {
-          const int u = a.user_idx[e2];
-          if (u > t) break;
-          const uint32_t word = ((u >> 5) == c) ? rw : A[(u >> 5) * kWave];
-          later |= bit(word, u & 31);
+      const double Mv = rec.M();
+      const uint32_t info = __builtin_amdgcn_readfirstlane(rec.info());
+      uint32_t anyU, r;
+      double freed;
+      if (!(info & kRecSlow)) {
+        anyU = (Rlo & rec.umask_lo()) | (Rhi & rec.umask_hi());
+        anyU |= far_bit(rec.far_user(), t, A);
+        anyU = min(anyU, 1u);
+        r = (v == t) ? 1u : ((s1 | anyU) & ~s0 & 1u);
+        freed = (double)(r & ~s1 & ~anyU & 1u) * Mv;
+        const int nd = (int)(info & 7u);
+#pragma unroll
+        for (int sl = 0; sl < kRecDeps; ++sl) {
+          if (sl < nd) {
+            const DepRegs ds = rec.dep(sl);
+            const uint32_t wi = B[(ds.i >> 5) * kWave];
+            uint32_t later = (Rlo & ds.lmask_lo) | (Rhi & ds.lmask_hi);
+            later |= far_bit(ds.far_later, t, A);
+            const uint32_t fr = r & ~bit(wi, ds.i & 31) & ~min(later, 1u) & 1u;
+            freed = fma((double)fr, ds.M, freed);
+          }
         }
-        if (r & ~si1 & ~later & 1u) freed += a.M[i];
+      } else {
+        // nodes outside the record format: walk the CSR lists
+        anyU = 0;
+        const int ue = a.user_ptr[v + 1];
+        for (int e = a.user_ptr[v]; e < ue; ++e) {
+          const int u = a.user_idx[e];
+          if (u > t) break;
+          anyU |= r_bit(u, v, Rlo, Rhi, A);
+        }
+        r = (v == t) ? 1u : ((s1 | anyU) & ~s0 & 1u);
+        freed = (double)(r & ~s1 & ~anyU & 1u) * Mv;
+        const int de = a.dep_ptr[v + 1];
+        for (int e = a.dep_ptr[v]; e < de; ++e) {
+          const int i = a.dep_idx[e];
+          const uint32_t wi = B[(i >> 5) * kWave];
+          uint32_t later = 0;
+          const int le = a.user_ptr[i + 1];
+          for (int e2 = a.dep_upos[e]; e2 < le; ++e2) {
+            const int u = a.user_idx[e2];
+            if (u > t) break;
+            later |= r_bit(u, v, Rlo, Rhi, A);
+          }
+          const uint32_t fr = r & ~bit(wi, i & 31) & ~later & 1u;
+          freed = fma((double)fr, a.M[i], freed);
+        }
       }
-      cost += r ? a.C[v] : 0.0;
-      U0 += s0 ? Mv : 0.0;
+      const double rd = (double)r;
+      cost = fma(rd, rec.C(), cost);
+      U0 = fma((double)s0, Mv, U0);
       const double val = Y + freed;
       maxv = fmax(maxv, val);
-      Y = val - (r ? Mv : 0.0);
+      Y = fma(-rd, Mv, val);
+      // slide the window down by one node: bit 0 becomes node v
+      Rhi = (Rhi << 1) | (Rlo >> 31);
+      Rlo = (Rlo << 1) | r;
     }
-    A[c * kWave] = rw;
+    A[c * kWave] = Rlo;   // R bits of nodes 32c .. 32c+31
   }
   stage_peak = U0 - Y + maxv;
   stage_cost = cost;
@@ -193,8 +328,6 @@ __global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
   const int words = (a.n >> 5) + 1;
   uint32_t* A = lds + lane;
   uint32_t* B = lds + (size_t)words * kWave + lane;
-
-  if (group == 0 && split == 0 && lane == 0) a.hdr[0] = a.splits;
 
   const int t0 = split_begin(a.n, a.splits, split);
   const int t1 = split_begin(a.n, a.splits, split + 1);
@@ -216,6 +349,7 @@ __global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
     a.part_peak[o] = (t0 < t1) ? (int64_t)seg_peak : INT64_MIN;
     a.part_cost[o] = seg_cost;
   }
+  if (group == 0 && split == 0 && lane == 0) a.hdr[0] = a.splits;
 }
 
 // ---------------------------------------------------------------------------
@@ -428,15 +562,16 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   a.key1 = (uint32_t)(seed >> 32);
   a.det0 = (flags & CKM_F_DET0) ? 1u : 0u;
   a.base = g.base;
-  a.q = at<uint32_t>(work, L.q_off);
-  a.det = at<uint32_t>(work, L.det_off);
-  a.M = g.d_M;
-  a.C = g.d_C;
-  a.user_ptr = g.d_user_ptr;
-  a.user_idx = g.d_user_idx;
-  a.dep_ptr = g.d_dep_ptr;
-  a.dep_idx = g.d_dep_idx;
-  a.dep_upos = g.d_dep_upos;
+  a.q = as_const(at<const uint32_t>(work, L.q_off));
+  a.det = as_const(at<const uint32_t>(work, L.det_off));
+  a.M = as_const(g.d_M);
+  a.C = as_const(g.d_C);
+  a.user_ptr = as_const(g.d_user_ptr);
+  a.user_idx = as_const(g.d_user_idx);
+  a.dep_ptr = as_const(g.d_dep_ptr);
+  a.dep_idx = as_const(g.d_dep_idx);
+  a.dep_upos = as_const(g.d_dep_upos);
+  a.recs = reinterpret_cast<const uint4*>(g.d_recs);
   a.part_peak = at<int64_t>(work, L.part_peak_off);
   a.part_cost = at<int64_t>(work, L.part_cost_off);
   a.hdr = at<int32_t>(work, L.hdr_off);
@@ -477,6 +612,49 @@ hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_
     }
   }
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+void build_node_records(int32_t n, const double* M, const double* C, const int32_t* dep_ptr,
+                        const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx,
+                        void* out) {
+  NodeRec* recs = static_cast<NodeRec*>(out);
+  for (int32_t v = 0; v < n; ++v) {
+    NodeRec r;
+    memset(&r, 0, sizeof(r));
+    r.M = M[v];
+    r.C = C[v];
+    r.far_user = INT32_MAX;
+    bool slow = false;
+    int nfar = 0;
+    for (int32_t e = user_ptr[v]; e < user_ptr[v + 1]; ++e) {
+      const int d = user_idx[e] - v - 1;
+      if (d < 32) r.umask_lo |= 1u << d;
+      else if (d < 64) r.umask_hi |= 1u << (d - 32);
+      else if (nfar++ == 0) r.far_user = user_idx[e];
+    }
+    if (nfar > 1) slow = true;
+    const int nd = dep_ptr[v + 1] - dep_ptr[v];
+    if (nd > kRecDeps) slow = true;
+    for (int sl = 0; sl < nd && !slow; ++sl) {
+      DepSlot& ds = r.dep[sl];
+      ds.i = dep_idx[dep_ptr[v] + sl];
+      ds.M = M[ds.i];
+      ds.far_later = INT32_MAX;
+      int nlate = 0;
+      for (int32_t e = user_ptr[ds.i]; e < user_ptr[ds.i + 1]; ++e) {
+        const int u = user_idx[e];
+        if (u <= v) continue;
+        const int d = u - v - 1;
+        if (d < 32) ds.lmask_lo |= 1u << d;
+        else if (d < 64) ds.lmask_hi |= 1u << (d - 32);
+        else if (nlate++ == 0) ds.far_later = u;
+      }
+      if (nlate > 1) slow = true;
+    }
+    r.info = (uint32_t)(slow ? 0 : nd) | (slow ? kRecSlow : 0u);
+    recs[v] = r;
+  }
 }
 
 }  // namespace ckm
