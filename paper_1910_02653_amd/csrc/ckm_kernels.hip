@@ -3,12 +3,11 @@
 //
 // Work decomposition of the dominant kernel (ckm_eval_kernel): one wave of 64
 // lanes owns 64 candidates (lane = candidate) and a contiguous range of
-// stages. All lanes walk the same nodes in the same order, so graph metadata,
-// thresholds and loop bounds are wave-uniform (scalar loads) and only the
-// candidate's bits and running sums live in vector registers. Each lane keeps
-// two bit rows (32-bit words, bit i%32 of word i/32) in LDS, laid out
-// [word][lane] so that a wave-uniform word index touches 64 consecutive
-// dwords: no bank conflicts.
+// stages. All lanes walk the same nodes in the same order, so graph data,
+// thresholds and loop bounds are wave-uniform and only the candidate's bits
+// and running sums differ per lane. Each lane keeps two bit rows (32-bit
+// words, bit i%32 of word i/32) in LDS, laid out [word][lane] so that a
+// wave-uniform word index touches 64 consecutive dwords: no bank conflicts.
 //
 // Sums of sizes and costs run in binary64. The host admits only graphs whose
 // totals stay below 2^53, so every partial sum is an exactly represented
@@ -25,17 +24,9 @@
 namespace ckm {
 namespace {
 
-// ---------------------------------------------------------------------------
-// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): multipliers for counter
-// words 0 and 2, key advanced by the Weyl constants between rounds.
-constexpr uint32_t kPhiloxM0 = 0xD2511F53u;
-constexpr uint32_t kPhiloxM1 = 0xCD9E8D57u;
-constexpr uint32_t kPhiloxW0 = 0x9E3779B9u;
-constexpr uint32_t kPhiloxW1 = 0xBB67AE85u;
-
 // Read-only data that every lane of a wave reads at the same address (graph
-// CSR, sizes, costs, thresholds): load it through the constant address space
-// so that uniform reads become scalar loads through the scalar cache.
+// CSR, sizes, thresholds): load it through the constant address space so
+// that uniform reads become scalar loads through the scalar cache.
 template <typename T>
 using cptr = const __attribute__((address_space(4))) T*;
 
@@ -43,6 +34,14 @@ template <typename T>
 __host__ __device__ __forceinline__ cptr<T> as_const(const T* p) {
   return (cptr<T>)(p);
 }
+
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): multipliers for counter
+// words 0 and 2, key advanced by the Weyl constants between rounds.
+constexpr uint32_t kPhiloxM0 = 0xD2511F53u;
+constexpr uint32_t kPhiloxM1 = 0xCD9E8D57u;
+constexpr uint32_t kPhiloxW0 = 0x9E3779B9u;
+constexpr uint32_t kPhiloxW1 = 0xBB67AE85u;
 
 __device__ __forceinline__ void philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
                                               uint32_t k0, uint32_t k1, uint32_t x[4]) {
@@ -64,33 +63,40 @@ __device__ __forceinline__ void philox4x32_10(uint32_t c0, uint32_t c1, uint32_t
 
 // 32 rounding decisions of row r, candidate k: bits i = 32w .. 32w+31 of
 // S_k[r] (Section 5.1 randomized rounding, thresholds q). Entries i >= r
-// have q = 0 and round to 0.
+// have q = 0 and round to 0. The word is assembled high bit first:
+// word = 2 word + [u < q].
 template <typename QPtr>
-__device__ __forceinline__ uint32_t round_word(QPtr qrow, int w, int r,
-                                               uint32_t k, uint32_t key0, uint32_t key1) {
+__device__ __forceinline__ uint32_t round_word(QPtr qrow, int w, int r, uint32_t k, uint32_t key0,
+                                               uint32_t key1) {
   uint32_t word = 0;
 #pragma unroll
-  for (int b = 0; b < 4; ++b) {
+  for (int b = 3; b >= 0; --b) {
     const int m = 4 * w + b;        // draws 8m .. 8m+7 share one Philox output
-    if (8 * m >= r) break;          // wave-uniform: the rest of the word is beyond the row
+    if (8 * m >= r) {               // wave-uniform: this part of the word is beyond the row
+      word <<= 8;
+      continue;
+    }
     uint32_t x[4];
     philox4x32_10((uint32_t)m, (uint32_t)r, k, 0u, key0, key1, x);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int j = 7; j >= 0; --j) {
       const uint32_t u = (x[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-      word |= (uint32_t)(u < qrow[8 * m + j]) << (8 * b + j);
+      word = word + word + (uint32_t)(u < qrow[8 * m + j]);
     }
   }
   return word;
 }
 
-// Per-node record read once per node visit (one 128-byte scalar load).
-// Masks are relative to the node v: bit d <-> node v + 1 + d, d < 64.
+// ---------------------------------------------------------------------------
+// Per-node record, read once per node visit. Masks are relative to the node
+// v: bit d <-> node v + 1 + d, d < 64. A "ref" locates one bit of a row in
+// LDS: (word * 256) << 16 | bit, i.e. the byte offset of the word within a
+// row buffer (lane 0) in the high half and the bit position in the low half.
 struct DepSlot {
-  int32_t i;              // a dep of v
+  uint32_t s1_ref;        // the dep i in the next-stage checkpoint row
+  uint32_t fl_ref;        // the user of i beyond v + 64 in the R row, or the zero word
   uint32_t lmask_lo;      // users u of i with v < u <= v + 32
   uint32_t lmask_hi;      //                  v + 32 < u <= v + 64
-  int32_t far_later;      // the user of i beyond v + 64, or INT32_MAX
   double M;               // M_i
 };
 constexpr int kRecDeps = 4;
@@ -99,22 +105,22 @@ struct NodeRec {
   double M, C;            // M_v, C_v
   uint32_t umask_lo;      // users u of v with u <= v + 32
   uint32_t umask_hi;      //                  v + 32 < u <= v + 64
-  int32_t far_user;       // the user of v beyond v + 64, or INT32_MAX
+  uint32_t fu_ref;        // the user of v beyond v + 64 in the R row, or the zero word
   uint32_t info;          // number of deps (bits 0-2) | kRecSlow
   DepSlot dep[kRecDeps];
 };
 static_assert(sizeof(NodeRec) == kNodeRecBytes, "node record layout");
 
+__host__ __device__ __forceinline__ uint32_t make_ref(int node) {
+  return ((uint32_t)(node >> 5) * 256u) << 16 | (uint32_t)(node & 31);
+}
+__host__ __device__ __forceinline__ uint32_t zero_ref(int n) {
+  return ((uint32_t)((n >> 5) + 1) * 256u) << 16;
+}
+
 __device__ __forceinline__ double dbl(uint32_t lo, uint32_t hi) {
   return __hiloint2double((int)hi, (int)lo);
 }
-
-struct DepRegs {
-  int i;
-  uint32_t lmask_lo, lmask_hi;
-  int far_later;
-  double M;
-};
 
 // The 32 dwords of a node record in vector registers (every lane holds the
 // same values).
@@ -124,12 +130,13 @@ struct RecRegs {
   __device__ double C() const { return dbl(w[2], w[3]); }
   __device__ uint32_t umask_lo() const { return w[4]; }
   __device__ uint32_t umask_hi() const { return w[5]; }
-  __device__ int far_user() const { return (int)w[6]; }
+  __device__ uint32_t fu_ref() const { return w[6]; }
   __device__ uint32_t info() const { return w[7]; }
-  __device__ DepRegs dep(int sl) const {
-    const uint32_t* d = w + 8 + 6 * sl;
-    return DepRegs{(int)d[0], d[1], d[2], (int)d[3], dbl(d[4], d[5])};
-  }
+  __device__ uint32_t s1_ref(int s) const { return w[8 + 6 * s]; }
+  __device__ uint32_t fl_ref(int s) const { return w[9 + 6 * s]; }
+  __device__ uint32_t lm_lo(int s) const { return w[10 + 6 * s]; }
+  __device__ uint32_t lm_hi(int s) const { return w[11 + 6 * s]; }
+  __device__ double dM(int s) const { return dbl(w[12 + 6 * s], w[13 + 6 * s]); }
 };
 
 // A zero the compiler cannot see through: added to an address, it makes a
@@ -154,14 +161,13 @@ __device__ __forceinline__ void load_rec(RecRegs& r, const uint4* __restrict__ r
 }
 
 struct EvalArgs {
-  int32_t n, K, splits, ldq, det_words;
+  int32_t n, K, splits, ldq, det_words, row_words;
   uint32_t key0, key1;
   uint32_t det0;                 // CKM_F_DET0 given
   double base;                   // M_in + 2 M_param
   cptr<uint32_t> q;
   cptr<uint32_t> det;
   cptr<double> M;
-  cptr<double> C;
   cptr<int32_t> user_ptr;
   cptr<int32_t> user_idx;
   cptr<int32_t> dep_ptr;
@@ -185,12 +191,25 @@ __device__ __forceinline__ int split_begin(int n, int splits, int s) {
   return (int)r;
 }
 
-// Row r of the candidate into LDS words 0 .. r/32 (dst[w * 64]).
-__device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bool det_lane,
-                                        uint32_t* dst) {
+// A lane's view of one LDS row buffer: word w at byte (w * 256) of `base`.
+struct Row {
+  char* base;  // buffer start + 4 * lane
+  __device__ uint32_t& word(int w) const { return *reinterpret_cast<uint32_t*>(base + w * 256); }
+  __device__ uint32_t at_ref(uint32_t ref) const {
+    return *reinterpret_cast<const uint32_t*>(base + (ref >> 16));
+  }
+  __device__ uint32_t bit_ref(uint32_t ref) const {  // bit position: low 5 bits of ref
+    return __builtin_amdgcn_ubfe(at_ref(ref), ref, 1);
+  }
+};
+
+__device__ __forceinline__ uint32_t bit(uint32_t word, int pos) { return (word >> pos) & 1u; }
+
+// Row r of the candidate into words 0 .. r/32.
+__device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bool det_lane, Row dst) {
   const int nw = (r >> 5) + 1;
   if (r >= a.n) {  // S after the last stage: nothing is kept
-    for (int w = 0; w < nw; ++w) dst[w * kWave] = 0u;
+    for (int w = 0; w < nw; ++w) dst.word(w) = 0u;
     return;
   }
   cptr<uint32_t> qrow = a.q + (size_t)r * a.ldq;
@@ -198,124 +217,136 @@ __device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bo
   for (int w = 0; w < nw; ++w) {
     uint32_t word = round_word(qrow, w, r, k, a.key0, a.key1);
     if (det_lane) word = drow[w];
-    dst[w * kWave] = word;
+    dst.word(w) = word;
   }
 }
-
-__device__ __forceinline__ uint32_t bit(uint32_t word, int pos) { return (word >> pos) & 1u; }
 
 // R bit of node u for a lane at node v of the right-to-left scan (v < u <= t):
 // nodes v+1 .. v+64 are in the window (Rlo: v+1 .. v+32, Rhi: v+33 .. v+64);
 // farther nodes lie in chunks already finished, whose R words are in A.
-__device__ __forceinline__ uint32_t r_bit(int u, int v, uint32_t Rlo, uint32_t Rhi, const uint32_t* A) {
+__device__ __forceinline__ uint32_t r_bit(int u, int v, uint32_t Rlo, uint32_t Rhi, Row A) {
   const int d = u - v - 1;
   if (d < 32) return bit(Rlo, d);
   if (d < 64) return bit(Rhi, d - 32);
-  return bit(A[(u >> 5) * kWave], u & 31);
+  return bit(A.word(u >> 5), u & 31);
 }
 
-// R bit of a far node u (more than 64 above the current node, so its chunk is
-// finished and stored in A), or 0 when u > t (including "none" = INT32_MAX).
-// The read address is clamped so that it always stays inside the row.
-__device__ __forceinline__ uint32_t far_bit(int u, int t, const uint32_t* A) {
-  const int uc = min(u, t);
-  const uint32_t b = bit(A[(uc >> 5) * kWave], uc & 31);
-  return (u <= t) ? b : 0u;
-}
+// Running state of the right-to-left scan of one stage (per lane).
+struct Scan {
+  double U0, Y, maxv, cost;
+  uint32_t Rlo, Rhi;   // R bits of the 64 nodes above the current node
+  uint32_t w0, w1;     // S_t and S_{t+1} words of the current chunk
+};
 
-// One stage t of one candidate (per lane). On entry A holds S_t and B holds
-// S_{t+1} (words 0 .. t/32). Algorithm 2's repair of R runs right to left
-// (reverse topological order), so every user of node v is decided before v:
-// v is computed iff it is node t (constraint 4a), or it is not checkpointed
-// and is kept for the next stage (1c) or needed by a computed user (1b).
-// In the same pass the U recurrence of Section 4.4 is evaluated in suffix
-// form:
+// One node v of stage t. Algorithm 2's repair runs right to left (reverse
+// topological order), so every user of v is decided before v: v is computed
+// iff it is node t (constraint 4a), or it is not checkpointed and is kept
+// for the next stage (1c) or needed by a computed user (1b). The U
+// recurrence of Section 4.4 runs in suffix form in the same pass:
 //   val_k = sum_{j>=k} freed_j - sum_{j>k} alloc_j,   U_{t,k} = U_end + val_k,
 // so the stage peak is U_end + max_k val_k with U_end = U_{t,0} - Y, Y being
 // the suffix value after node 0. freed_v collects FREE(t,i,v) M_i over
 // i in Deps[v] u {v}: v computed, i not kept, and no computed user of i
-// after v. The R bits of the 64 nodes above v live in two registers; R_t
-// overwrites S_t in A chunk by chunk. Node records are read with vector
-// loads one node ahead (the scan order is v = t, t-1, ..., 0).
-__device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, uint32_t* A, const uint32_t* B,
-                                           double& stage_peak, double& stage_cost) {
-  double U0 = a.base, Y = 0.0, maxv = -INFINITY, cost = 0.0;
-  uint32_t Rlo = 0, Rhi = 0;
-  const int lane_off = opaque_zero();
-  RecRegs nxt;
-  load_rec(nxt, a.recs, t, lane_off);
-  for (int c = t >> 5; c >= 0; --c) {
-    const uint32_t w0 = A[c * kWave];
-    const uint32_t w1 = B[c * kWave];
-    const int jtop = min(31, t - 32 * c);
-    for (int jj = jtop; jj >= 0; --jj) {
-      const int v = 32 * c + jj;
-      const RecRegs rec = nxt;
-      load_rec(nxt, a.recs, max(v - 1, 0), lane_off);
-      const uint32_t s0 = bit(w0, jj);
-      const uint32_t s1 = bit(w1, jj);
-      const double Mv = rec.M();
-      const uint32_t info = __builtin_amdgcn_readfirstlane(rec.info());
-      uint32_t anyU, r;
-      double freed;
-      if (!(info & kRecSlow)) {
-        anyU = (Rlo & rec.umask_lo()) | (Rhi & rec.umask_hi());
-        anyU |= far_bit(rec.far_user(), t, A);
-        anyU = min(anyU, 1u);
-        r = (v == t) ? 1u : ((s1 | anyU) & ~s0 & 1u);
-        freed = (double)(r & ~s1 & ~anyU & 1u) * Mv;
-        const int nd = (int)(info & 7u);
+// after v. A holds S_t below the current chunk and R_t above it; B holds
+// S_{t+1}. Rows are zero beyond their last word, so a reference to a node
+// above t (or to the zero word) reads 0.
+__device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const RecRegs& rec, Scan& sc,
+                                          Row A, Row B) {
+  const int jj = v & 31;
+  const uint32_t s0 = bit(sc.w0, jj);
+  const uint32_t s1 = bit(sc.w1, jj);
+  const double Mv = rec.M();
+  const uint32_t info = __builtin_amdgcn_readfirstlane(rec.info());
+  uint32_t anyU, r;
+  double freed;
+  if (!(info & kRecSlow)) {
+    anyU = (sc.Rlo & rec.umask_lo()) | (sc.Rhi & rec.umask_hi()) | A.bit_ref(rec.fu_ref());
+    anyU = min(anyU, 1u);
+    r = ((s1 | anyU) & ~s0 & 1u) | (uint32_t)(v == t);
+    freed = (double)(r & ~s1 & ~anyU & 1u) * Mv;
+    const int nd = (int)(info & 7u);
 #pragma unroll
-        for (int sl = 0; sl < kRecDeps; ++sl) {
-          if (sl < nd) {
-            const DepRegs ds = rec.dep(sl);
-            const uint32_t wi = B[(ds.i >> 5) * kWave];
-            uint32_t later = (Rlo & ds.lmask_lo) | (Rhi & ds.lmask_hi);
-            later |= far_bit(ds.far_later, t, A);
-            const uint32_t fr = r & ~bit(wi, ds.i & 31) & ~min(later, 1u) & 1u;
-            freed = fma((double)fr, ds.M, freed);
-          }
-        }
-      } else {
-        // nodes outside the record format: walk the CSR lists
-        anyU = 0;
-        const int ue = a.user_ptr[v + 1];
-        for (int e = a.user_ptr[v]; e < ue; ++e) {
-          const int u = a.user_idx[e];
-          if (u > t) break;
-          anyU |= r_bit(u, v, Rlo, Rhi, A);
-        }
-        r = (v == t) ? 1u : ((s1 | anyU) & ~s0 & 1u);
-        freed = (double)(r & ~s1 & ~anyU & 1u) * Mv;
-        const int de = a.dep_ptr[v + 1];
-        for (int e = a.dep_ptr[v]; e < de; ++e) {
-          const int i = a.dep_idx[e];
-          const uint32_t wi = B[(i >> 5) * kWave];
-          uint32_t later = 0;
-          const int le = a.user_ptr[i + 1];
-          for (int e2 = a.dep_upos[e]; e2 < le; ++e2) {
-            const int u = a.user_idx[e2];
-            if (u > t) break;
-            later |= r_bit(u, v, Rlo, Rhi, A);
-          }
-          const uint32_t fr = r & ~bit(wi, i & 31) & ~later & 1u;
-          freed = fma((double)fr, a.M[i], freed);
-        }
+    for (int sl = 0; sl < kRecDeps; ++sl) {
+      if (sl < nd) {
+        uint32_t later = (sc.Rlo & rec.lm_lo(sl)) | (sc.Rhi & rec.lm_hi(sl)) | A.bit_ref(rec.fl_ref(sl));
+        later = min(later, 1u);
+        const uint32_t fr = r & ~B.bit_ref(rec.s1_ref(sl)) & ~later & 1u;
+        freed = fma((double)fr, rec.dM(sl), freed);
       }
-      const double rd = (double)r;
-      cost = fma(rd, rec.C(), cost);
-      U0 = fma((double)s0, Mv, U0);
-      const double val = Y + freed;
-      maxv = fmax(maxv, val);
-      Y = fma(-rd, Mv, val);
-      // slide the window down by one node: bit 0 becomes node v
-      Rhi = (Rhi << 1) | (Rlo >> 31);
-      Rlo = (Rlo << 1) | r;
     }
-    A[c * kWave] = Rlo;   // R bits of nodes 32c .. 32c+31
+  } else {
+    // nodes outside the record format: walk the CSR lists
+    anyU = 0;
+    const int ue = a.user_ptr[v + 1];
+    for (int e = a.user_ptr[v]; e < ue; ++e) {
+      const int u = a.user_idx[e];
+      if (u > t) break;
+      anyU |= r_bit(u, v, sc.Rlo, sc.Rhi, A);
+    }
+    r = ((s1 | anyU) & ~s0 & 1u) | (uint32_t)(v == t);
+    freed = (double)(r & ~s1 & ~anyU & 1u) * Mv;
+    const int de = a.dep_ptr[v + 1];
+    for (int e = a.dep_ptr[v]; e < de; ++e) {
+      const int i = a.dep_idx[e];
+      uint32_t later = 0;
+      const int le = a.user_ptr[i + 1];
+      for (int e2 = a.dep_upos[e]; e2 < le; ++e2) {
+        const int u = a.user_idx[e2];
+        if (u > t) break;
+        later |= r_bit(u, v, sc.Rlo, sc.Rhi, A);
+      }
+      const uint32_t fr = r & ~bit(B.word(i >> 5), i & 31) & ~later & 1u;
+      freed = fma((double)fr, a.M[i], freed);
+    }
   }
-  stage_peak = U0 - Y + maxv;
-  stage_cost = cost;
+  const double rd = (double)r;
+  sc.cost = fma(rd, rec.C(), sc.cost);
+  sc.U0 = fma((double)s0, Mv, sc.U0);
+  const double val = sc.Y + freed;
+  sc.maxv = fmax(sc.maxv, val);
+  sc.Y = fma(-rd, Mv, val);
+  // slide the window down by one node: bit 0 becomes node v
+  sc.Rhi = (sc.Rhi << 1) | (sc.Rlo >> 31);
+  sc.Rlo = (sc.Rlo << 1) | r;
+  if (jj == 0) {               // chunk finished: R_t replaces S_t, move to the next chunk
+    const int c = v >> 5;
+    A.word(c) = sc.Rlo;
+    if (c > 0) {
+      sc.w0 = A.word(c - 1);
+      sc.w1 = B.word(c - 1);
+    }
+  }
+}
+
+// One stage t of one candidate (per lane): S_t in A, S_{t+1} in B on entry,
+// R_t in A on exit. Node records are read one node ahead into two register
+// buffers used alternately.
+__device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, Row B, double& stage_peak,
+                                           double& stage_cost) {
+  Scan sc;
+  sc.U0 = a.base;
+  sc.Y = 0.0;
+  sc.maxv = -INFINITY;
+  sc.cost = 0.0;
+  sc.Rlo = sc.Rhi = 0;
+  sc.w0 = A.word(t >> 5);
+  sc.w1 = B.word(t >> 5);
+  const int lane_off = opaque_zero();
+  RecRegs r0, r1;
+  load_rec(r0, a.recs, t, lane_off);
+  int v = t;
+  while (true) {
+    load_rec(r1, a.recs, max(v - 1, 0), lane_off);
+    scan_node(a, t, v, r0, sc, A, B);
+    if (v == 0) break;
+    --v;
+    load_rec(r0, a.recs, max(v - 1, 0), lane_off);
+    scan_node(a, t, v, r1, sc, A, B);
+    if (v == 0) break;
+    --v;
+  }
+  stage_peak = sc.U0 - sc.Y + sc.maxv;
+  stage_cost = sc.cost;
 }
 
 __global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
@@ -325,9 +356,13 @@ __global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
   const int split = blockIdx.y;
   const uint32_t k = (uint32_t)(group * kWave + lane);
   const bool det_lane = a.det0 && k == 0;
-  const int words = (a.n >> 5) + 1;
-  uint32_t* A = lds + lane;
-  uint32_t* B = lds + (size_t)words * kWave + lane;
+  Row A{reinterpret_cast<char*>(lds) + 4 * lane};
+  Row B{reinterpret_cast<char*>(lds) + (size_t)a.row_words * 256 + 4 * lane};
+  // Rows start zeroed: words beyond a row's end (and the zero word) read 0.
+  for (int w = 0; w < a.row_words; ++w) {
+    A.word(w) = 0u;
+    B.word(w) = 0u;
+  }
 
   const int t0 = split_begin(a.n, a.splits, split);
   const int t1 = split_begin(a.n, a.splits, split + 1);
@@ -341,7 +376,9 @@ __global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
       eval_stage(a, t, A, B, sp, sc);
       seg_peak = fmax(seg_peak, sp);
       seg_cost += (int64_t)sc;
-      uint32_t* tmp = A; A = B; B = tmp;
+      const Row tmp = A;
+      A = B;
+      B = tmp;
     }
   }
   if ((int)k < a.K) {
@@ -558,6 +595,7 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   a.splits = splits;
   a.ldq = L.ldq;
   a.det_words = L.det_words;
+  a.row_words = (g.n >> 5) + 2;   // words of a row plus one word that stays zero
   a.key0 = (uint32_t)(seed & 0xFFFFFFFFu);
   a.key1 = (uint32_t)(seed >> 32);
   a.det0 = (flags & CKM_F_DET0) ? 1u : 0u;
@@ -565,7 +603,6 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   a.q = as_const(at<const uint32_t>(work, L.q_off));
   a.det = as_const(at<const uint32_t>(work, L.det_off));
   a.M = as_const(g.d_M);
-  a.C = as_const(g.d_C);
   a.user_ptr = as_const(g.d_user_ptr);
   a.user_idx = as_const(g.d_user_idx);
   a.dep_ptr = as_const(g.d_dep_ptr);
@@ -576,7 +613,7 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   a.part_cost = at<int64_t>(work, L.part_cost_off);
   a.hdr = at<int32_t>(work, L.hdr_off);
   const int groups = (K + kWave - 1) / kWave;
-  const size_t lds_bytes = 2u * (size_t)((g.n >> 5) + 1) * kWave * sizeof(uint32_t);
+  const size_t lds_bytes = 2u * (size_t)a.row_words * kWave * sizeof(uint32_t);
   if (lds_bytes > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)ckm_eval_kernel,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
@@ -619,36 +656,39 @@ void build_node_records(int32_t n, const double* M, const double* C, const int32
                         const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx,
                         void* out) {
   NodeRec* recs = static_cast<NodeRec*>(out);
+  const uint32_t zref = zero_ref(n);
   for (int32_t v = 0; v < n; ++v) {
     NodeRec r;
     memset(&r, 0, sizeof(r));
     r.M = M[v];
     r.C = C[v];
-    r.far_user = INT32_MAX;
+    r.fu_ref = zref;
     bool slow = false;
     int nfar = 0;
     for (int32_t e = user_ptr[v]; e < user_ptr[v + 1]; ++e) {
-      const int d = user_idx[e] - v - 1;
+      const int u = user_idx[e];
+      const int d = u - v - 1;
       if (d < 32) r.umask_lo |= 1u << d;
       else if (d < 64) r.umask_hi |= 1u << (d - 32);
-      else if (nfar++ == 0) r.far_user = user_idx[e];
+      else if (nfar++ == 0) r.fu_ref = make_ref(u);
     }
     if (nfar > 1) slow = true;
     const int nd = dep_ptr[v + 1] - dep_ptr[v];
     if (nd > kRecDeps) slow = true;
     for (int sl = 0; sl < nd && !slow; ++sl) {
       DepSlot& ds = r.dep[sl];
-      ds.i = dep_idx[dep_ptr[v] + sl];
-      ds.M = M[ds.i];
-      ds.far_later = INT32_MAX;
+      const int i = dep_idx[dep_ptr[v] + sl];
+      ds.s1_ref = make_ref(i);
+      ds.fl_ref = zref;
+      ds.M = M[i];
       int nlate = 0;
-      for (int32_t e = user_ptr[ds.i]; e < user_ptr[ds.i + 1]; ++e) {
+      for (int32_t e = user_ptr[i]; e < user_ptr[i + 1]; ++e) {
         const int u = user_idx[e];
         if (u <= v) continue;
         const int d = u - v - 1;
         if (d < 32) ds.lmask_lo |= 1u << d;
         else if (d < 64) ds.lmask_hi |= 1u << (d - 32);
-        else if (nlate++ == 0) ds.far_later = u;
+        else if (nlate++ == 0) ds.fl_ref = make_ref(u);
       }
       if (nlate > 1) slow = true;
     }
