@@ -205,6 +205,13 @@ struct Row {
 
 __device__ __forceinline__ uint32_t bit(uint32_t word, int pos) { return (word >> pos) & 1u; }
 
+// min(x, 1): 1 iff x != 0, as one VALU instruction.
+__device__ __forceinline__ uint32_t umin1(uint32_t x) {
+  uint32_t y;
+  asm("v_min_u32 %0, %1, 1" : "=v"(y) : "v"(x));
+  return y;
+}
+
 // Row r of the candidate into words 0 .. r/32.
 __device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bool det_lane, Row dst) {
   const int nw = (r >> 5) + 1;
@@ -260,17 +267,29 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
   uint32_t anyU, r;
   double freed;
   if (!(info & kRecSlow)) {
-    anyU = (sc.Rlo & rec.umask_lo()) | (sc.Rhi & rec.umask_hi()) | A.bit_ref(rec.fu_ref());
-    anyU = min(anyU, 1u);
+    // all LDS words this node needs, read together (unused slots read the zero word)
+    const uint32_t lfu = A.at_ref(rec.fu_ref());
+    uint32_t lfl[kRecDeps], ls1[kRecDeps];
+#pragma unroll
+    for (int sl = 0; sl < kRecDeps; ++sl) {
+      lfl[sl] = A.at_ref(rec.fl_ref(sl));
+      ls1[sl] = B.at_ref(rec.s1_ref(sl));
+    }
+    // keep the nine reads together (one wait) instead of sunk into the slots' branches
+    asm volatile("" ::"v"(lfu), "v"(lfl[0]), "v"(lfl[1]), "v"(lfl[2]), "v"(lfl[3]), "v"(ls1[0]),
+                 "v"(ls1[1]), "v"(ls1[2]), "v"(ls1[3]));
+    anyU = (sc.Rlo & rec.umask_lo()) | (sc.Rhi & rec.umask_hi()) | __builtin_amdgcn_ubfe(lfu, rec.fu_ref(), 1);
+    anyU = umin1(anyU);
     r = ((s1 | anyU) & ~s0 & 1u) | (uint32_t)(v == t);
     freed = (double)(r & ~s1 & ~anyU & 1u) * Mv;
     const int nd = (int)(info & 7u);
 #pragma unroll
     for (int sl = 0; sl < kRecDeps; ++sl) {
       if (sl < nd) {
-        uint32_t later = (sc.Rlo & rec.lm_lo(sl)) | (sc.Rhi & rec.lm_hi(sl)) | A.bit_ref(rec.fl_ref(sl));
-        later = min(later, 1u);
-        const uint32_t fr = r & ~B.bit_ref(rec.s1_ref(sl)) & ~later & 1u;
+        uint32_t later = (sc.Rlo & rec.lm_lo(sl)) | (sc.Rhi & rec.lm_hi(sl)) |
+                         __builtin_amdgcn_ubfe(lfl[sl], rec.fl_ref(sl), 1);
+        later = umin1(later);
+        const uint32_t fr = r & ~__builtin_amdgcn_ubfe(ls1[sl], rec.s1_ref(sl), 1) & ~later & 1u;
         freed = fma((double)fr, rec.dM(sl), freed);
       }
     }
