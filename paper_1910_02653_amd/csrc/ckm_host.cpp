@@ -60,12 +60,16 @@ int32_t max_splits_for(int32_t n, int32_t K) {
 }
 
 int32_t auto_splits(int32_t n, int32_t K, int32_t max_splits) {
-  // About 2048 waves over the device, and at least ~8 stages per split so the
-  // extra S row a split regenerates at its start stays a small fraction.
+  // About two waves per resident slot: 256 CUs, as many waves per CU as the
+  // two LDS rows of a wave allow (at most 20, the register limit). Each extra
+  // split regenerates one S row, a small cost next to idle slots.
   const int32_t groups = (K + kWave - 1) / kWave;
-  int32_t s = std::max<int32_t>(1, 2048 / std::max<int32_t>(groups, 1));
-  s = std::min<int32_t>(s, std::max<int32_t>(1, n / 8));
-  return std::min<int32_t>(s, max_splits);
+  const int64_t wave_lds = 2 * (int64_t)((n >> 5) + 2) * kWave * 4;
+  const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(20, (160 * 1024) / wave_lds));
+  const int64_t slots = 2 * 256 * per_cu;
+  int64_t s = (slots + groups - 1) / groups;
+  s = std::min<int64_t>(s, n);
+  return (int32_t)std::max<int64_t>(1, std::min<int64_t>(s, max_splits));
 }
 
 Layout make_layout(int32_t n, int32_t K) {
@@ -76,7 +80,7 @@ Layout make_layout(int32_t n, int32_t K) {
   L.det_words = L.ldq / 32;
   L.row_words = 2 * ((n + 63) / 64);
   L.max_splits = max_splits_for(n, K);
-  L.reduce_blocks = (K + 255) / 256;
+  L.reduce_blocks = (K + kWave - 1) / kWave;
   size_t off = 0;
   L.hdr_off = off;       off = align256(off + 256);
   L.q_off = off;         off = align256(off + (size_t)n * L.ldq * sizeof(uint32_t));

@@ -21,6 +21,13 @@
 
 #include "ckm_internal.h"
 
+#ifndef CKM_MAX_EVAL_WAVES
+#define CKM_MAX_EVAL_WAVES 4
+#endif
+#ifndef CKM_CU_LDS
+#define CKM_CU_LDS (160 * 1024)
+#endif
+
 namespace ckm {
 namespace {
 
@@ -100,6 +107,7 @@ struct DepSlot {
   double M;               // M_i
 };
 constexpr int kRecDeps = 4;
+constexpr int kMaxEvalWaves = CKM_MAX_EVAL_WAVES;
 constexpr uint32_t kRecSlow = 1u << 31;   // node does not fit: use the CSR lists
 struct NodeRec {
   double M, C;            // M_v, C_v
@@ -368,15 +376,20 @@ __device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, Row 
   stage_cost = sc.cost;
 }
 
-__global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
+// A workgroup holds several waves (several groups of 64 candidates) on the
+// same stage range, so they read the same node records and thresholds at
+// about the same time and share them through the caches.
+__global__ void __launch_bounds__(kMaxEvalWaves * kWave) ckm_eval_kernel(EvalArgs a) {
   extern __shared__ uint32_t lds[];
-  const int lane = threadIdx.x;
-  const int group = blockIdx.x;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int group = blockIdx.x * (blockDim.x / kWave) + wave;
   const int split = blockIdx.y;
   const uint32_t k = (uint32_t)(group * kWave + lane);
   const bool det_lane = a.det0 && k == 0;
-  Row A{reinterpret_cast<char*>(lds) + 4 * lane};
-  Row B{reinterpret_cast<char*>(lds) + (size_t)a.row_words * 256 + 4 * lane};
+  char* wave_lds = reinterpret_cast<char*>(lds) + (size_t)wave * 2 * a.row_words * 256;
+  Row A{wave_lds + 4 * lane};
+  Row B{wave_lds + (size_t)a.row_words * 256 + 4 * lane};
   // Rows start zeroed: words beyond a row's end (and the zero word) read 0.
   for (int w = 0; w < a.row_words; ++w) {
     A.word(w) = 0u;
@@ -458,6 +471,9 @@ __device__ __forceinline__ bool better(const Best& x, const Best& y) {
   return x.k < y.k;
 }
 
+// One block per 64 candidates: the four waves reduce interleaved stage
+// splits (coalesced over candidates), then combine; feasibility and the
+// block's lexicographic minimum follow.
 __global__ void __launch_bounds__(256) ckm_reduce_kernel(int32_t K, const int32_t* __restrict__ hdr,
                                                          const int64_t* __restrict__ part_peak,
                                                          const int64_t* __restrict__ part_cost,
@@ -465,26 +481,42 @@ __global__ void __launch_bounds__(256) ckm_reduce_kernel(int32_t K, const int32_
                                                          int64_t* __restrict__ cost,
                                                          uint8_t* __restrict__ feasible,
                                                          Best* __restrict__ block_best) {
-  __shared__ Best sb[256];
-  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  __shared__ int64_t sp[4][kWave];
+  __shared__ int64_t sc[4][kWave];
+  __shared__ Best sb[kWave];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int stripe = threadIdx.x / kWave;
+  const int k = blockIdx.x * kWave + lane;
   const int splits = hdr[0];
-  Best b{0, 0, -1, 0};
+  int64_t p = INT64_MIN, c = 0;
   if (k < K) {
-    int64_t p = INT64_MIN, c = 0;
-    for (int s = 0; s < splits; ++s) {
+    for (int s = stripe; s < splits; s += 4) {
       const int64_t v = part_peak[(size_t)s * K + k];
       p = v > p ? v : p;
       c += part_cost[(size_t)s * K + k];
     }
-    peak[k] = p;
-    cost[k] = c;
-    const bool f = p <= budget;
-    feasible[k] = f ? 1 : 0;
-    if (f) b = Best{c, p, k, 0};
   }
-  sb[threadIdx.x] = b;
+  sp[stripe][lane] = p;
+  sc[stripe][lane] = c;
   __syncthreads();
-  for (int off = blockDim.x / 2; off > 0; off >>= 1) {
+  if (stripe == 0) {
+    Best b{0, 0, -1, 0};
+    if (k < K) {
+#pragma unroll
+      for (int q = 1; q < 4; ++q) {
+        p = sp[q][lane] > p ? sp[q][lane] : p;
+        c += sc[q][lane];
+      }
+      peak[k] = p;
+      cost[k] = c;
+      const bool f = p <= budget;
+      feasible[k] = f ? 1 : 0;
+      if (f) b = Best{c, p, k, 0};
+    }
+    sb[lane] = b;
+  }
+  __syncthreads();
+  for (int off = kWave / 2; off > 0; off >>= 1) {
     if (threadIdx.x < off && better(sb[threadIdx.x + off], sb[threadIdx.x]))
       sb[threadIdx.x] = sb[threadIdx.x + off];
     __syncthreads();
@@ -632,13 +664,19 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   a.part_cost = at<int64_t>(work, L.part_cost_off);
   a.hdr = at<int32_t>(work, L.hdr_off);
   const int groups = (K + kWave - 1) / kWave;
-  const size_t lds_bytes = 2u * (size_t)a.row_words * kWave * sizeof(uint32_t);
+  const size_t wave_lds = 2u * (size_t)a.row_words * kWave * sizeof(uint32_t);
+  // waves per workgroup: up to kMaxEvalWaves while two workgroups still fit a CU's LDS
+  int waves = 1;
+  while (waves * 2 <= kMaxEvalWaves && waves * 2 <= groups && 2 * (size_t)(waves * 2) * wave_lds <= CKM_CU_LDS)
+    waves *= 2;
+  const size_t lds_bytes = (size_t)waves * wave_lds;
   if (lds_bytes > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)ckm_eval_kernel,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(ckm_eval_kernel, dim3(groups, splits), dim3(kWave), lds_bytes, stream, a);
+  hipLaunchKernelGGL(ckm_eval_kernel, dim3((groups + waves - 1) / waves, splits), dim3(waves * kWave),
+                     lds_bytes, stream, a);
   return hipGetLastError();
 }
 
@@ -646,7 +684,7 @@ hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_
                          int64_t budget, uint32_t flags, int64_t* d_peak, int64_t* d_cost,
                          uint8_t* d_feasible, int32_t* d_best_k, uint64_t* d_best_S,
                          uint64_t* d_best_R, int32_t* d_status, char* work, hipStream_t stream) {
-  const int rb = (K + 255) / 256;
+  const int rb = (K + kWave - 1) / kWave;
   hipLaunchKernelGGL(ckm_reduce_kernel, dim3(rb), dim3(256), 0, stream, K,
                      at<const int32_t>(work, L.hdr_off), at<const int64_t>(work, L.part_peak_off),
                      at<const int64_t>(work, L.part_cost_off), budget, d_peak, d_cost, d_feasible,
