@@ -22,7 +22,7 @@
 #include "ckm_internal.h"
 
 #ifndef CKM_MAX_EVAL_WAVES
-#define CKM_MAX_EVAL_WAVES 4
+#define CKM_MAX_EVAL_WAVES 1
 #endif
 #ifndef CKM_CU_LDS
 #define CKM_CU_LDS (160 * 1024)
@@ -50,14 +50,19 @@ constexpr uint32_t kPhiloxM1 = 0xCD9E8D57u;
 constexpr uint32_t kPhiloxW0 = 0x9E3779B9u;
 constexpr uint32_t kPhiloxW1 = 0xBB67AE85u;
 
+// a ^ b ^ c in one VALU instruction (c is wave-uniform: the round key).
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+  return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);  // truth table of a ^ b ^ c
+}
+
 __device__ __forceinline__ void philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
                                               uint32_t k0, uint32_t k1, uint32_t x[4]) {
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
     const uint64_t p0 = (uint64_t)kPhiloxM0 * c0;
     const uint64_t p1 = (uint64_t)kPhiloxM1 * c2;
-    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
-    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+    const uint32_t n0 = xor3((uint32_t)(p1 >> 32), c1, k0);
+    const uint32_t n2 = xor3((uint32_t)(p0 >> 32), c3, k1);
     c0 = n0;
     c1 = (uint32_t)p1;
     c2 = n2;
@@ -68,28 +73,67 @@ __device__ __forceinline__ void philox4x32_10(uint32_t c0, uint32_t c1, uint32_t
   x[0] = c0; x[1] = c1; x[2] = c2; x[3] = c3;
 }
 
+// word = 2^8 word + (8 rounding bits), high draw first: bit j of the new
+// byte is [u_j < q_j], where u_j is 16-bit half (j mod 2) of x[j / 2] and
+// q_j is wave-uniform. Each compare writes a lane mask that a carry-in add
+// folds into the word; three masks rotate so that every add reads a mask
+// written at least two instructions earlier (the VALU-written SGPR to VALU
+// lane-mask read distance).
+__device__ __forceinline__ uint32_t append8_uniform(uint32_t word, const uint32_t x[4], const uint32_t q[8]) {
+  uint64_t m0, m1, m2;
+  asm("v_cmp_lt_u32_sdwa %[m0], %[x3], %[q7] src0_sel:WORD_1 src1_sel:DWORD\n\t"
+      "v_cmp_lt_u32_sdwa %[m1], %[x3], %[q6] src0_sel:WORD_0 src1_sel:DWORD\n\t"
+      "v_cmp_lt_u32_sdwa %[m2], %[x2], %[q5] src0_sel:WORD_1 src1_sel:DWORD\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m0]\n\t"
+      "v_cmp_lt_u32_sdwa %[m0], %[x2], %[q4] src0_sel:WORD_0 src1_sel:DWORD\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m1]\n\t"
+      "v_cmp_lt_u32_sdwa %[m1], %[x1], %[q3] src0_sel:WORD_1 src1_sel:DWORD\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m2]\n\t"
+      "v_cmp_lt_u32_sdwa %[m2], %[x1], %[q2] src0_sel:WORD_0 src1_sel:DWORD\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m0]\n\t"
+      "v_cmp_lt_u32_sdwa %[m0], %[x0], %[q1] src0_sel:WORD_1 src1_sel:DWORD\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m1]\n\t"
+      "v_cmp_lt_u32_sdwa %[m1], %[x0], %[q0] src0_sel:WORD_0 src1_sel:DWORD\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m2]\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m0]\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m1]"
+      : [w] "+v"(word), [m0] "=&s"(m0), [m1] "=&s"(m1), [m2] "=&s"(m2)
+      : [x0] "v"(x[0]), [x1] "v"(x[1]), [x2] "v"(x[2]), [x3] "v"(x[3]), [q0] "s"(q[0]), [q1] "s"(q[1]),
+        [q2] "s"(q[2]), [q3] "s"(q[3]), [q4] "s"(q[4]), [q5] "s"(q[5]), [q6] "s"(q[6]), [q7] "s"(q[7])
+      : "vcc");
+  return word;
+}
+
+// Same bits, thresholds in any register class.
+__device__ __forceinline__ uint32_t append8(uint32_t word, const uint32_t x[4], const uint32_t q[8]) {
+#pragma unroll
+  for (int j = 7; j >= 0; --j) {
+    const uint32_t u = (x[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+    word = word + word + (u < q[j] ? 1u : 0u);
+  }
+  return word;
+}
+
 // 32 rounding decisions of row r, candidate k: bits i = 32w .. 32w+31 of
 // S_k[r] (Section 5.1 randomized rounding, thresholds q). Entries i >= r
-// have q = 0 and round to 0. The word is assembled high bit first:
-// word = 2 word + [u < q].
-template <typename QPtr>
+// have q = 0 and round to 0. The word is assembled high bit first.
+// kUniformQ: the row pointer and w are the same for the whole wave.
+template <bool kUniformQ, typename QPtr>
 __device__ __forceinline__ uint32_t round_word(QPtr qrow, int w, int r, uint32_t k, uint32_t key0,
                                                uint32_t key1) {
   uint32_t word = 0;
 #pragma unroll
   for (int b = 3; b >= 0; --b) {
     const int m = 4 * w + b;        // draws 8m .. 8m+7 share one Philox output
-    if (8 * m >= r) {               // wave-uniform: this part of the word is beyond the row
+    if (8 * m >= r) {               // this part of the word is beyond the row
       word <<= 8;
       continue;
     }
-    uint32_t x[4];
+    uint32_t x[4], q[8];
     philox4x32_10((uint32_t)m, (uint32_t)r, k, 0u, key0, key1, x);
 #pragma unroll
-    for (int j = 7; j >= 0; --j) {
-      const uint32_t u = (x[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-      word = word + word + (uint32_t)(u < qrow[8 * m + j]);
-    }
+    for (int j = 0; j < 8; ++j) q[j] = qrow[8 * m + j];
+    word = kUniformQ ? append8_uniform(word, x, q) : append8(word, x, q);
   }
   return word;
 }
@@ -230,7 +274,7 @@ __device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bo
   cptr<uint32_t> qrow = a.q + (size_t)r * a.ldq;
   cptr<uint32_t> drow = a.det + (size_t)r * a.det_words;
   for (int w = 0; w < nw; ++w) {
-    uint32_t word = round_word(qrow, w, r, k, a.key0, a.key1);
+    uint32_t word = round_word<true>(qrow, w, r, k, a.key0, a.key1);
     if (det_lane) word = drow[w];
     dst.word(w) = word;
   }
@@ -569,7 +613,7 @@ __global__ void __launch_bounds__(256) ckm_best_rows_kernel(const uint32_t* __re
     if (det0 && bk == 0)
       word = det[(size_t)r * det_words + w];
     else
-      word = round_word(q + (size_t)r * ldq, w, r, (uint32_t)bk, key0, key1);
+      word = round_word<false>(q + (size_t)r * ldq, w, r, (uint32_t)bk, key0, key1);
   }
   S_rows[(size_t)r * row_words + w] = word;
 }
