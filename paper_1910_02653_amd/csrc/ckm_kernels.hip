@@ -193,18 +193,22 @@ struct RecRegs {
 
 // A zero the compiler cannot see through: added to an address, it makes a
 // wave-uniform load a vector load, whose completion counter is in order and
-// so can run one node ahead of its use.
-__device__ __forceinline__ int opaque_zero() {
-  int z;
+// so can run nodes ahead of its use.
+__device__ __forceinline__ uint32_t opaque_zero() {
+  uint32_t z;
   asm volatile("v_mov_b32 %0, 0" : "=v"(z));
   return z;
 }
 
-__device__ __forceinline__ void load_rec(RecRegs& r, const uint4* __restrict__ recs, int v, int lane_off) {
-  const uint4* p = recs + (size_t)v * (kNodeRecBytes / 16) + lane_off;
+__device__ __forceinline__ void load_rec(RecRegs& r, const uint4* __restrict__ recs, int v) {
+  // wave-uniform base in scalar registers plus a vector offset of zero made
+  // here, so the base is not folded into a loop-invariant vector pointer
+  const int vu = __builtin_amdgcn_readfirstlane(v);
+  const char* base = reinterpret_cast<const char*>(recs) + (size_t)vu * kNodeRecBytes;
+  const size_t off = opaque_zero();
 #pragma unroll
   for (int q = 0; q < kNodeRecBytes / 16; ++q) {
-    const uint4 x = p[q];
+    const uint4 x = *reinterpret_cast<const uint4*>(base + off + 16 * q);
     r.w[4 * q + 0] = x.x;
     r.w[4 * q + 1] = x.y;
     r.w[4 * q + 2] = x.z;
@@ -297,6 +301,36 @@ struct Scan {
   uint32_t w0, w1;     // S_t and S_{t+1} words of the current chunk
 };
 
+// LDS words one node reads: the R word of v's user beyond the window, and
+// per dependency slot the R word of its user beyond the window and its
+// S_{t+1} word. Unused slots reference the zero word.
+struct LdsVals {
+  uint32_t fu;
+  uint32_t fl[kRecDeps];
+  uint32_t s1[kRecDeps];
+};
+
+// Issues the reads for the node whose record is `rec`. They are issued one
+// node ahead of their use: the words they read are final by then (users
+// beyond the window lie in chunks already finished, S_{t+1} is not written
+// during the stage).
+__device__ __forceinline__ void issue_reads(const RecRegs& rec, Row A, Row B, LdsVals& L) {
+  L.fu = A.at_ref(rec.fu_ref());
+#pragma unroll
+  for (int sl = 0; sl < kRecDeps; ++sl) {
+    L.fl[sl] = A.at_ref(rec.fl_ref(sl));
+    L.s1[sl] = B.at_ref(rec.s1_ref(sl));
+  }
+}
+
+// max(a, b) for values that are never NaN, without the quieting step that
+// fmax adds on a loop-carried operand.
+__device__ __forceinline__ double max_f64(double a, double b) {
+  double d;
+  asm("v_max_f64 %0, %1, %2" : "=v"(d) : "v"(a), "v"(b));
+  return d;
+}
+
 // One node v of stage t. Algorithm 2's repair runs right to left (reverse
 // topological order), so every user of v is decided before v: v is computed
 // iff it is node t (constraint 4a), or it is not checkpointed and is kept
@@ -308,9 +342,11 @@ struct Scan {
 // i in Deps[v] u {v}: v computed, i not kept, and no computed user of i
 // after v. A holds S_t below the current chunk and R_t above it; B holds
 // S_{t+1}. Rows are zero beyond their last word, so a reference to a node
-// above t (or to the zero word) reads 0.
-__device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const RecRegs& rec, Scan& sc,
-                                          Row A, Row B) {
+// above t (or to the zero word) reads 0. kFirst: v == t, which is always
+// computed and has no computed user in the stage.
+template <bool kFirst>
+__device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const RecRegs& rec, const LdsVals& L,
+                                          Scan& sc, Row A, Row B) {
   const int jj = v & 31;
   const uint32_t s0 = bit(sc.w0, jj);
   const uint32_t s1 = bit(sc.w1, jj);
@@ -318,32 +354,33 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
   const uint32_t info = __builtin_amdgcn_readfirstlane(rec.info());
   uint32_t anyU, r;
   double freed;
-  if (!(info & kRecSlow)) {
-    // all LDS words this node needs, read together (unused slots read the zero word)
-    const uint32_t lfu = A.at_ref(rec.fu_ref());
-    uint32_t lfl[kRecDeps], ls1[kRecDeps];
-#pragma unroll
-    for (int sl = 0; sl < kRecDeps; ++sl) {
-      lfl[sl] = A.at_ref(rec.fl_ref(sl));
-      ls1[sl] = B.at_ref(rec.s1_ref(sl));
+  if (__builtin_expect(!(info & kRecSlow), 1)) {
+    if (kFirst) {
+      anyU = 0;
+      r = 1;
+    } else {
+      anyU = (sc.Rlo & rec.umask_lo()) | (sc.Rhi & rec.umask_hi()) | __builtin_amdgcn_ubfe(L.fu, rec.fu_ref(), 1);
+      anyU = umin1(anyU);
+      r = (s1 | anyU) & ~s0 & 1u;
     }
-    // keep the nine reads together (one wait) instead of sunk into the slots' branches
-    asm volatile("" ::"v"(lfu), "v"(lfl[0]), "v"(lfl[1]), "v"(lfl[2]), "v"(lfl[3]), "v"(ls1[0]),
-                 "v"(ls1[1]), "v"(ls1[2]), "v"(ls1[3]));
-    anyU = (sc.Rlo & rec.umask_lo()) | (sc.Rhi & rec.umask_hi()) | __builtin_amdgcn_ubfe(lfu, rec.fu_ref(), 1);
-    anyU = umin1(anyU);
-    r = ((s1 | anyU) & ~s0 & 1u) | (uint32_t)(v == t);
-    freed = (double)(r & ~s1 & ~anyU & 1u) * Mv;
+    // FREE(t,v,v): v computed, not kept, no computed user after it. A node
+    // other than t is computed only because it is kept (s1) or used (anyU),
+    // so only node t can be freed right after it is computed.
+    freed = kFirst ? (double)(~s1 & 1u) * Mv : 0.0;
     const int nd = (int)(info & 7u);
-#pragma unroll
-    for (int sl = 0; sl < kRecDeps; ++sl) {
-      if (sl < nd) {
-        uint32_t later = (sc.Rlo & rec.lm_lo(sl)) | (sc.Rhi & rec.lm_hi(sl)) |
-                         __builtin_amdgcn_ubfe(lfl[sl], rec.fl_ref(sl), 1);
-        later = umin1(later);
-        const uint32_t fr = r & ~__builtin_amdgcn_ubfe(ls1[sl], rec.s1_ref(sl), 1) & ~later & 1u;
-        freed = fma((double)fr, rec.dM(sl), freed);
-      }
+    auto slot = [&](int sl) {
+      uint32_t later = (sc.Rlo & rec.lm_lo(sl)) | (sc.Rhi & rec.lm_hi(sl)) |
+                       __builtin_amdgcn_ubfe(L.fl[sl], rec.fl_ref(sl), 1);
+      later = umin1(later);
+      const uint32_t fr = r & ~__builtin_amdgcn_ubfe(L.s1[sl], rec.s1_ref(sl), 1) & ~later & 1u;
+      freed = fma((double)fr, rec.dM(sl), freed);
+    };
+    // most nodes have one or two dependencies
+    if (__builtin_expect(nd >= 1, 1)) slot(0);
+    if (__builtin_expect(nd >= 2, 1)) slot(1);
+    if (__builtin_expect(nd >= 3, 0)) {
+      slot(2);
+      if (nd >= 4) slot(3);
     }
   } else {
     // nodes outside the record format: walk the CSR lists
@@ -354,7 +391,7 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
       if (u > t) break;
       anyU |= r_bit(u, v, sc.Rlo, sc.Rhi, A);
     }
-    r = ((s1 | anyU) & ~s0 & 1u) | (uint32_t)(v == t);
+    r = ((s1 | anyU) & ~s0 & 1u) | (uint32_t)kFirst;
     freed = (double)(r & ~s1 & ~anyU & 1u) * Mv;
     const int de = a.dep_ptr[v + 1];
     for (int e = a.dep_ptr[v]; e < de; ++e) {
@@ -374,12 +411,12 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
   sc.cost = fma(rd, rec.C(), sc.cost);
   sc.U0 = fma((double)s0, Mv, sc.U0);
   const double val = sc.Y + freed;
-  sc.maxv = fmax(sc.maxv, val);
+  sc.maxv = max_f64(sc.maxv, val);
   sc.Y = fma(-rd, Mv, val);
   // slide the window down by one node: bit 0 becomes node v
   sc.Rhi = (sc.Rhi << 1) | (sc.Rlo >> 31);
   sc.Rlo = (sc.Rlo << 1) | r;
-  if (jj == 0) {               // chunk finished: R_t replaces S_t, move to the next chunk
+  if (__builtin_expect(jj == 0, 0)) {  // chunk finished: R_t replaces S_t, move to the next chunk
     const int c = v >> 5;
     A.word(c) = sc.Rlo;
     if (c > 0) {
@@ -389,9 +426,29 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
   }
 }
 
+// Waits for every load of a record buffer.
+__device__ __forceinline__ void settle(const RecRegs& r) {
+#pragma unroll
+  for (int q = 0; q < kNodeRecBytes / 4; q += 8)
+    asm volatile("" ::"v"(r.w[q]), "v"(r.w[q + 1]), "v"(r.w[q + 2]), "v"(r.w[q + 3]), "v"(r.w[q + 4]),
+                 "v"(r.w[q + 5]), "v"(r.w[q + 6]), "v"(r.w[q + 7]));
+}
+
+// One node of the scan, software-pipelined: the record of node v - 2 is
+// requested, the LDS words of node v - 1 are requested, then node v is
+// evaluated with the record and words requested one and two nodes earlier.
+// Record buffers rotate through (C, N, NN) so registers never move.
+template <int C, int N, int NN, bool kFirst>
+__device__ __forceinline__ void pipe_step(const EvalArgs& a, int t, int v, RecRegs (&rb)[3], LdsVals (&lb)[3],
+                                          Scan& sc, Row A, Row B) {
+  load_rec(rb[NN], a.recs, max(v - 2, 0));
+  issue_reads(rb[N], A, B, lb[N]);
+  asm volatile("" ::: "memory");  // keep the requests ahead of this node's work
+  scan_node<kFirst>(a, t, v, rb[C], lb[C], sc, A, B);
+}
+
 // One stage t of one candidate (per lane): S_t in A, S_{t+1} in B on entry,
-// R_t in A on exit. Node records are read one node ahead into two register
-// buffers used alternately.
+// R_t in A on exit.
 __device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, Row B, double& stage_peak,
                                            double& stage_cost) {
   Scan sc;
@@ -402,20 +459,30 @@ __device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, Row 
   sc.Rlo = sc.Rhi = 0;
   sc.w0 = A.word(t >> 5);
   sc.w1 = B.word(t >> 5);
-  const int lane_off = opaque_zero();
-  RecRegs r0, r1;
-  load_rec(r0, a.recs, t, lane_off);
+  RecRegs rb[3];
+  LdsVals lb[3];
+  load_rec(rb[0], a.recs, t);
+  load_rec(rb[1], a.recs, max(t - 1, 0));
+  issue_reads(rb[0], A, B, lb[0]);
   int v = t;
-  while (true) {
-    load_rec(r1, a.recs, max(v - 1, 0), lane_off);
-    scan_node(a, t, v, r0, sc, A, B);
-    if (v == 0) break;
-    --v;
-    load_rec(r0, a.recs, max(v - 1, 0), lane_off);
-    scan_node(a, t, v, r1, sc, A, B);
-    if (v == 0) break;
-    --v;
+  pipe_step<0, 1, 2, true>(a, t, v, rb, lb, sc, A, B);
+  // node t leaves part of its record unread; retire those loads here, once
+  // per stage, so the loop never waits for loads older than two nodes
+  settle(rb[0]);
+  // nodes t-1 .. 0 in groups of three (one turn of the buffer rotation),
+  // then the remainder
+  const int groups = __builtin_amdgcn_readfirstlane(t / 3);
+  for (int g = 0; g < groups; ++g) {
+    pipe_step<1, 2, 0, false>(a, t, --v, rb, lb, sc, A, B);
+    pipe_step<2, 0, 1, false>(a, t, --v, rb, lb, sc, A, B);
+    pipe_step<0, 1, 2, false>(a, t, --v, rb, lb, sc, A, B);
   }
+  if (v >= 1) pipe_step<1, 2, 0, false>(a, t, --v, rb, lb, sc, A, B);
+  if (v >= 1) pipe_step<2, 0, 1, false>(a, t, --v, rb, lb, sc, A, B);
+  // prefetches past node 0 are never read: retire them inside the stage
+  settle(rb[0]);
+  settle(rb[1]);
+  settle(rb[2]);
   stage_peak = sc.U0 - sc.Y + sc.maxv;
   stage_cost = sc.cost;
 }
