@@ -53,23 +53,50 @@ struct DeviceGuard {
 namespace ckm {
 
 int32_t max_splits_for(int32_t n, int32_t K) {
+  // partial arrays of at most 2^22 entries each (64 MiB), at most n rows
   int64_t cap = std::max<int64_t>(4, (int64_t(1) << 22) / std::max<int32_t>(K, 1));
-  cap = std::min<int64_t>(cap, 512);
+  cap = std::min<int64_t>(cap, 1024);
   cap = std::min<int64_t>(cap, n);
   return (int32_t)std::max<int64_t>(cap, 1);
 }
 
-int32_t auto_splits(int32_t n, int32_t K, int32_t max_splits) {
-  // About two waves per resident slot: 256 CUs, as many waves per CU as the
-  // two LDS rows of a wave allow (at most 20, the register limit). Each extra
-  // split regenerates one S row, a small cost next to idle slots.
-  const int32_t groups = (K + kWave - 1) / kWave;
+// Resident evaluate waves on the device: 256 CUs, as many waves per CU as
+// the two LDS rows of a wave allow (at most 20).
+static int64_t eval_slots(int32_t n) {
   const int64_t wave_lds = 2 * (int64_t)((n >> 5) + 2) * kWave * 4;
-  const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(20, (160 * 1024) / wave_lds));
-  const int64_t slots = 2 * 256 * per_cu;
-  int64_t s = (slots + groups - 1) / groups;
-  s = std::min<int64_t>(s, n);
-  return (int32_t)std::max<int64_t>(1, std::min<int64_t>(s, max_splits));
+  return 256 * std::max<int64_t>(1, std::min<int64_t>(20, (160 * 1024) / wave_lds));
+}
+
+Plan plan_splits(int32_t n, int32_t splits) {
+  Plan p;
+  p.kind = 0;
+  p.items = std::max(1, std::min(splits, n));
+  return p;
+}
+
+Plan plan_auto(int32_t n, int32_t K, int32_t max_items) {
+  // About eight items per resident wave slot. The upper half of the stages
+  // goes in items of P stages, the lower half (a quarter of the work) in as
+  // many ranges, each about a third of an upper item, so the launch ends on
+  // small items. Each item regenerates one S row; the finer balance is worth
+  // more than that on this workload range.
+  const int64_t groups = (K + kWave - 1) / kWave;
+  const int64_t target = std::max<int64_t>(1, (8 * eval_slots(n) + groups - 1) / groups);
+  if (n < 8 || target < 4) return plan_splits(n, (int32_t)std::min<int64_t>(target, max_items));
+  Plan p;
+  p.kind = 1;
+  p.T0 = n / 2;
+  const int64_t half = std::max<int64_t>(1, target / 2);
+  p.P = (int32_t)std::max<int64_t>(1, (n - p.T0 + half - 1) / half);
+  for (;;) {
+    p.R1 = (n - p.T0 + p.P - 1) / p.P;
+    p.R2 = std::max(1, std::min(p.T0, p.R1));
+    p.items = p.R1 + p.R2;
+    if (p.items <= max_items || p.P >= n) break;
+    p.P *= 2;
+  }
+  if (p.items > max_items) return plan_splits(n, max_items);
+  return p;
 }
 
 Layout make_layout(int32_t n, int32_t K) {
@@ -300,10 +327,10 @@ ckm_status ckm_evaluate_async(const ckm_graph* g, int32_t K, uint64_t seed, uint
   if (st != CKM_OK) return st;
   if (flags & ~(uint32_t)CKM_F_DET0) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
   if (stage_splits < 0) return fail(CKM_E_INVALID_ARG, "stage_splits = %d < 0", stage_splits);
-  int32_t splits = stage_splits ? std::min(stage_splits, L.max_splits)
-                                : ckm::auto_splits(g->n, K, L.max_splits);
+  const ckm::Plan plan = stage_splits ? ckm::plan_splits(g->n, std::min(stage_splits, L.max_splits))
+                                      : ckm::plan_auto(g->n, K, L.max_splits);
   DeviceGuard dg(g->device);
-  hipError_t e = ckm::launch_evaluate(*g, L, K, seed, flags, splits, static_cast<char*>(d_work),
+  hipError_t e = ckm::launch_evaluate(*g, L, K, seed, flags, plan, static_cast<char*>(d_work),
                                       static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CKM_OK : fail_hip(e, "evaluate launch");
 }

@@ -31,7 +31,7 @@ struct ckm_graph {
 namespace ckm {
 
 constexpr int kWave = 64;
-constexpr int kNodeRecBytes = 128;
+constexpr int kNodeRecBytes = 256;
 
 // Host-side builder of the per-node records the evaluate kernel reads
 // (layout documented with NodeRec in ckm_kernels.hip). Writes n records.
@@ -48,19 +48,31 @@ struct Layout {
   int32_t row_words = 0;  // 32-bit words per output bit row: 2 * ceil(n / 64)
   int32_t max_splits = 0; // capacity of the partial-result arrays
   int32_t reduce_blocks = 0;
-  // hdr: int32 number of stage splits used by the last evaluate
+  // hdr: int32 number of work items (rows of the partial arrays) of the last evaluate
   size_t hdr_off = 0, q_off = 0, det_off = 0, nan_off = 0, part_peak_off = 0, part_cost_off = 0,
          best_off = 0, srows_off = 0, total = 0;
 };
 
 Layout make_layout(int32_t n, int32_t K);
-int32_t auto_splits(int32_t n, int32_t K, int32_t max_splits);
+
+// How the stages of one group of 64 candidates are cut into work items (one
+// wave each). Items are numbered in dispatch order, most expensive first, so
+// the cheap ones fill the end of the launch.
+//   kind 0: `items` ranges of about equal sum of stage lengths, top first.
+//   kind 1: stages T0 .. n-1 in R1 items of P consecutive stages (top
+//           first), then stages 0 .. T0-1 in R2 ranges of about equal sum of
+//           stage lengths (top first).
+struct Plan {
+  int32_t items = 1, kind = 0, P = 0, T0 = 0, R1 = 0, R2 = 0;
+};
+Plan plan_auto(int32_t n, int32_t K, int32_t max_items);
+Plan plan_splits(int32_t n, int32_t splits);
 
 // Kernel launchers (defined in ckm_kernels.hip). They only enqueue work.
 hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,
                            char* work, hipStream_t stream);
 hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
-                           uint32_t flags, int32_t splits, char* work, hipStream_t stream);
+                           uint32_t flags, const Plan& plan, char* work, hipStream_t stream);
 hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
                          int64_t budget, uint32_t flags, int64_t* d_peak,
                          int64_t* d_cost, uint8_t* d_feasible, int32_t* d_best_k,

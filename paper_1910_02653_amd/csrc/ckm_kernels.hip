@@ -160,6 +160,10 @@ struct NodeRec {
   uint32_t fu_ref;        // the user of v beyond v + 64 in the R row, or the zero word
   uint32_t info;          // number of deps (bits 0-2) | kRecSlow
   DepSlot dep[kRecDeps];
+  // the bit positions of the references, five bits each: fu, then per slot
+  // s1 and fl (slots 0-1 and s1 of slot 2 in bits0, the rest in bits1)
+  uint32_t bits0, bits1;
+  uint32_t pad[30];       // one dword per lane of a 64-lane load
 };
 static_assert(sizeof(NodeRec) == kNodeRecBytes, "node record layout");
 
@@ -174,50 +178,46 @@ __device__ __forceinline__ double dbl(uint32_t lo, uint32_t hi) {
   return __hiloint2double((int)hi, (int)lo);
 }
 
-// The 32 dwords of a node record in vector registers (every lane holds the
-// same values).
+// A node record spread over the lanes of one vector register: lane L holds
+// dword L. Fields are moved to scalar registers when used
+// (v_readlane), so a record costs 256 bytes of vector-memory return per
+// wave instead of 128 bytes for each of the 64 lanes.
 struct RecRegs {
-  uint32_t w[kNodeRecBytes / 4];
-  __device__ double M() const { return dbl(w[0], w[1]); }
-  __device__ double C() const { return dbl(w[2], w[3]); }
-  __device__ uint32_t umask_lo() const { return w[4]; }
-  __device__ uint32_t umask_hi() const { return w[5]; }
-  __device__ uint32_t fu_ref() const { return w[6]; }
-  __device__ uint32_t info() const { return w[7]; }
-  __device__ uint32_t s1_ref(int s) const { return w[8 + 6 * s]; }
-  __device__ uint32_t fl_ref(int s) const { return w[9 + 6 * s]; }
-  __device__ uint32_t lm_lo(int s) const { return w[10 + 6 * s]; }
-  __device__ uint32_t lm_hi(int s) const { return w[11 + 6 * s]; }
-  __device__ double dM(int s) const { return dbl(w[12 + 6 * s], w[13 + 6 * s]); }
+  uint32_t w;
+  __device__ uint32_t get(int i) const { return __builtin_amdgcn_readlane(w, i); }
+  __device__ double M() const { return dbl(get(0), get(1)); }
+  __device__ double C() const { return dbl(get(2), get(3)); }
+  __device__ uint32_t umask_lo() const { return get(4); }
+  __device__ uint32_t umask_hi() const { return get(5); }
+  __device__ uint32_t fu_ref() const { return get(6); }
+  __device__ uint32_t info() const { return get(7); }
+  __device__ uint32_t s1_ref(int s) const { return get(8 + 6 * s); }
+  __device__ uint32_t fl_ref(int s) const { return get(9 + 6 * s); }
+  __device__ uint32_t lm_lo(int s) const { return get(10 + 6 * s); }
+  __device__ uint32_t lm_hi(int s) const { return get(11 + 6 * s); }
+  __device__ double dM(int s) const { return dbl(get(12 + 6 * s), get(13 + 6 * s)); }
+  __device__ uint32_t bits0() const { return get(32); }
+  __device__ uint32_t bits1() const { return get(33); }
 };
 
-// A zero the compiler cannot see through: added to an address, it makes a
-// wave-uniform load a vector load, whose completion counter is in order and
-// so can run nodes ahead of its use.
-__device__ __forceinline__ uint32_t opaque_zero() {
-  uint32_t z;
-  asm volatile("v_mov_b32 %0, 0" : "=v"(z));
-  return z;
+// Bit position k of a record (0: fu; 1 + 2s: s1 of slot s; 2 + 2s: fl of
+// slot s) from its two packed dwords; only the low five bits of the result
+// matter to the bit-field extracts that use it.
+__device__ __forceinline__ uint32_t bitpos(uint32_t b0, uint32_t b1, int k) {
+  return k < 6 ? (b0 >> (5 * k)) : (b1 >> (5 * (k - 6)));
 }
 
 __device__ __forceinline__ void load_rec(RecRegs& r, const uint4* __restrict__ recs, int v) {
-  // wave-uniform base in scalar registers plus a vector offset of zero made
-  // here, so the base is not folded into a loop-invariant vector pointer
+  // wave-uniform record base in scalar registers, one dword per lane
   const int vu = __builtin_amdgcn_readfirstlane(v);
   const char* base = reinterpret_cast<const char*>(recs) + (size_t)vu * kNodeRecBytes;
-  const size_t off = opaque_zero();
-#pragma unroll
-  for (int q = 0; q < kNodeRecBytes / 16; ++q) {
-    const uint4 x = *reinterpret_cast<const uint4*>(base + off + 16 * q);
-    r.w[4 * q + 0] = x.x;
-    r.w[4 * q + 1] = x.y;
-    r.w[4 * q + 2] = x.z;
-    r.w[4 * q + 3] = x.w;
-  }
+  const size_t off = (size_t)((threadIdx.x & 63u) * 4u);
+  r.w = *reinterpret_cast<const uint32_t*>(base + off);
 }
 
 struct EvalArgs {
-  int32_t n, K, splits, ldq, det_words, row_words;
+  int32_t n, K, ldq, det_words, row_words;
+  int32_t items, kind, P, T0, R1, R2;   // work plan (see Plan)
   uint32_t key0, key1;
   uint32_t det0;                 // CKM_F_DET0 given
   double base;                   // M_in + 2 M_param
@@ -230,21 +230,38 @@ struct EvalArgs {
   cptr<int32_t> dep_idx;
   cptr<int32_t> dep_upos;
   const uint4* __restrict__ recs;
-  int64_t* __restrict__ part_peak;   // [splits][K]
-  int64_t* __restrict__ part_cost;   // [splits][K]
+  int64_t* __restrict__ part_peak;   // [items][K]
+  int64_t* __restrict__ part_cost;   // [items][K]
   int32_t* __restrict__ hdr;
 };
 
-// First stage of split s: splits cover equal shares of the sum of stage
-// lengths (stage t touches t + 1 nodes), t_s = floor(sqrt(n^2 s / splits)).
-__device__ __forceinline__ int split_begin(int n, int splits, int s) {
+// First stage of range s of `parts` ranges over stages 0 .. m-1 with about
+// equal sums of stage lengths (stage t touches t + 1 nodes):
+// floor(sqrt(m^2 s / parts)).
+__device__ __forceinline__ int split_begin(int m, int parts, int s) {
   if (s <= 0) return 0;
-  if (s >= splits) return n;
-  const uint64_t x = (uint64_t)n * (uint64_t)n * (uint64_t)s / (uint64_t)splits;
+  if (s >= parts) return m;
+  const uint64_t x = (uint64_t)m * (uint64_t)m * (uint64_t)s / (uint64_t)parts;
   uint64_t r = (uint64_t)sqrt((double)x);
   while (r * r > x) --r;
   while ((r + 1) * (r + 1) <= x) ++r;
   return (int)r;
+}
+
+// Stages [t0, t1) of work item `item` (numbered most expensive first).
+__device__ __forceinline__ void item_range(const EvalArgs& a, int item, int& t0, int& t1) {
+  if (a.kind == 0) {
+    const int s = a.items - 1 - item;
+    t0 = split_begin(a.n, a.items, s);
+    t1 = split_begin(a.n, a.items, s + 1);
+  } else if (item < a.R1) {
+    t1 = a.n - a.P * item;
+    t0 = max(a.T0, t1 - a.P);
+  } else {
+    const int s = a.R2 - 1 - (item - a.R1);
+    t0 = split_begin(a.T0, a.R2, s);
+    t1 = split_begin(a.T0, a.R2, s + 1);
+  }
 }
 
 // A lane's view of one LDS row buffer: word w at byte (w * 256) of `base`.
@@ -277,8 +294,11 @@ __device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bo
   }
   cptr<uint32_t> qrow = a.q + (size_t)r * a.ldq;
   cptr<uint32_t> drow = a.det + (size_t)r * a.det_words;
+  // the round keys are rebuilt per row instead of held for the whole kernel
+  uint32_t key0 = a.key0, key1 = a.key1;
+  asm volatile("" : "+s"(key0), "+s"(key1));
   for (int w = 0; w < nw; ++w) {
-    uint32_t word = round_word<true>(qrow, w, r, k, a.key0, a.key1);
+    uint32_t word = round_word<true>(qrow, w, r, k, key0, key1);
     if (det_lane) word = drow[w];
     dst.word(w) = word;
   }
@@ -304,22 +324,41 @@ struct Scan {
 // LDS words one node reads: the R word of v's user beyond the window, and
 // per dependency slot the R word of its user beyond the window and its
 // S_{t+1} word. Unused slots reference the zero word.
+// LDS words one node reads: the R word of v's user beyond the window, and
+// per dependency slot the R word of its user beyond the window and its
+// S_{t+1} word. Unused slots reference the zero word. The references stay
+// in scalar registers until the node is evaluated (their low five bits are
+// the bit positions).
 struct LdsVals {
   uint32_t fu;
   uint32_t fl[kRecDeps];
   uint32_t s1[kRecDeps];
 };
 
+// Keeps a group of scalar values together: all of them are computed before
+// any use that follows (the v_readlane results then need no wait states).
+__device__ __forceinline__ void pin_s(uint32_t a, uint32_t b, uint32_t c) { asm volatile("" ::"s"(a), "s"(b), "s"(c)); }
+
 // Issues the reads for the node whose record is `rec`. They are issued one
 // node ahead of their use: the words they read are final by then (users
 // beyond the window lie in chunks already finished, S_{t+1} is not written
 // during the stage).
 __device__ __forceinline__ void issue_reads(const RecRegs& rec, Row A, Row B, LdsVals& L) {
-  L.fu = A.at_ref(rec.fu_ref());
+  const uint32_t fu = rec.fu_ref();
+  uint32_t fl[kRecDeps], s1[kRecDeps];
 #pragma unroll
   for (int sl = 0; sl < kRecDeps; ++sl) {
-    L.fl[sl] = A.at_ref(rec.fl_ref(sl));
-    L.s1[sl] = B.at_ref(rec.s1_ref(sl));
+    fl[sl] = rec.fl_ref(sl);
+    s1[sl] = rec.s1_ref(sl);
+  }
+  pin_s(fu, fl[0], s1[0]);
+  pin_s(fl[1], s1[1], fl[2]);
+  pin_s(s1[2], fl[3], s1[3]);
+  L.fu = A.at_ref(fu);
+#pragma unroll
+  for (int sl = 0; sl < kRecDeps; ++sl) {
+    L.fl[sl] = A.at_ref(fl[sl]);
+    L.s1[sl] = B.at_ref(s1[sl]);
   }
 }
 
@@ -350,8 +389,15 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
   const int jj = v & 31;
   const uint32_t s0 = bit(sc.w0, jj);
   const uint32_t s1 = bit(sc.w1, jj);
-  const double Mv = rec.M();
-  const uint32_t info = __builtin_amdgcn_readfirstlane(rec.info());
+  // the node's scalar fields, read together
+  const uint32_t m_lo = rec.get(0), m_hi = rec.get(1), c_lo = rec.get(2), c_hi = rec.get(3);
+  const uint32_t um_lo = rec.umask_lo(), um_hi = rec.umask_hi(), info = rec.info();
+  const uint32_t b0 = rec.bits0(), b1 = rec.bits1();
+  pin_s(m_lo, m_hi, c_lo);
+  pin_s(c_hi, um_lo, um_hi);
+  pin_s(info, b0, b1);
+  const double Mv = dbl(m_lo, m_hi);
+  const double Cv = dbl(c_lo, c_hi);
   uint32_t anyU, r;
   double freed;
   if (__builtin_expect(!(info & kRecSlow), 1)) {
@@ -359,7 +405,7 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
       anyU = 0;
       r = 1;
     } else {
-      anyU = (sc.Rlo & rec.umask_lo()) | (sc.Rhi & rec.umask_hi()) | __builtin_amdgcn_ubfe(L.fu, rec.fu_ref(), 1);
+      anyU = (sc.Rlo & um_lo) | (sc.Rhi & um_hi) | __builtin_amdgcn_ubfe(L.fu, b0, 1);
       anyU = umin1(anyU);
       r = (s1 | anyU) & ~s0 & 1u;
     }
@@ -369,11 +415,14 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
     freed = kFirst ? (double)(~s1 & 1u) * Mv : 0.0;
     const int nd = (int)(info & 7u);
     auto slot = [&](int sl) {
-      uint32_t later = (sc.Rlo & rec.lm_lo(sl)) | (sc.Rhi & rec.lm_hi(sl)) |
-                       __builtin_amdgcn_ubfe(L.fl[sl], rec.fl_ref(sl), 1);
+      const uint32_t lm_lo = rec.lm_lo(sl), lm_hi = rec.lm_hi(sl);
+      const uint32_t d_lo = rec.get(12 + 6 * sl), d_hi = rec.get(13 + 6 * sl);
+      pin_s(lm_lo, lm_hi, d_lo);
+      pin_s(d_hi, d_hi, d_hi);
+      uint32_t later = (sc.Rlo & lm_lo) | (sc.Rhi & lm_hi) | __builtin_amdgcn_ubfe(L.fl[sl], bitpos(b0, b1, 2 + 2 * sl), 1);
       later = umin1(later);
-      const uint32_t fr = r & ~__builtin_amdgcn_ubfe(L.s1[sl], rec.s1_ref(sl), 1) & ~later & 1u;
-      freed = fma((double)fr, rec.dM(sl), freed);
+      const uint32_t fr = r & ~__builtin_amdgcn_ubfe(L.s1[sl], bitpos(b0, b1, 1 + 2 * sl), 1) & ~later & 1u;
+      freed = fma((double)fr, dbl(d_lo, d_hi), freed);
     };
     // most nodes have one or two dependencies
     if (__builtin_expect(nd >= 1, 1)) slot(0);
@@ -408,7 +457,7 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
     }
   }
   const double rd = (double)r;
-  sc.cost = fma(rd, rec.C(), sc.cost);
+  sc.cost = fma(rd, Cv, sc.cost);
   sc.U0 = fma((double)s0, Mv, sc.U0);
   const double val = sc.Y + freed;
   sc.maxv = max_f64(sc.maxv, val);
@@ -427,12 +476,7 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
 }
 
 // Waits for every load of a record buffer.
-__device__ __forceinline__ void settle(const RecRegs& r) {
-#pragma unroll
-  for (int q = 0; q < kNodeRecBytes / 4; q += 8)
-    asm volatile("" ::"v"(r.w[q]), "v"(r.w[q + 1]), "v"(r.w[q + 2]), "v"(r.w[q + 3]), "v"(r.w[q + 4]),
-                 "v"(r.w[q + 5]), "v"(r.w[q + 6]), "v"(r.w[q + 7]));
-}
+__device__ __forceinline__ void settle(const RecRegs& r) { asm volatile("" ::"v"(r.w)); }
 
 // One node of the scan, software-pipelined: the record of node v - 2 is
 // requested, the LDS words of node v - 1 are requested, then node v is
@@ -495,7 +539,7 @@ __global__ void __launch_bounds__(kMaxEvalWaves * kWave) ckm_eval_kernel(EvalArg
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int group = blockIdx.x * (blockDim.x / kWave) + wave;
-  const int split = blockIdx.y;
+  const int item = blockIdx.y;
   const uint32_t k = (uint32_t)(group * kWave + lane);
   const bool det_lane = a.det0 && k == 0;
   char* wave_lds = reinterpret_cast<char*>(lds) + (size_t)wave * 2 * a.row_words * 256;
@@ -507,8 +551,8 @@ __global__ void __launch_bounds__(kMaxEvalWaves * kWave) ckm_eval_kernel(EvalArg
     B.word(w) = 0u;
   }
 
-  const int t0 = split_begin(a.n, a.splits, split);
-  const int t1 = split_begin(a.n, a.splits, split + 1);
+  int t0, t1;
+  item_range(a, item, t0, t1);
   double seg_peak = -INFINITY;
   int64_t seg_cost = 0;
   if (t0 < t1) {
@@ -525,11 +569,11 @@ __global__ void __launch_bounds__(kMaxEvalWaves * kWave) ckm_eval_kernel(EvalArg
     }
   }
   if ((int)k < a.K) {
-    const size_t o = (size_t)split * a.K + k;
+    const size_t o = (size_t)item * a.K + k;
     a.part_peak[o] = (t0 < t1) ? (int64_t)seg_peak : INT64_MIN;
     a.part_cost[o] = seg_cost;
   }
-  if (group == 0 && split == 0 && lane == 0) a.hdr[0] = a.splits;
+  if (group == 0 && item == 0 && lane == 0) a.hdr[0] = a.items;
 }
 
 // ---------------------------------------------------------------------------
@@ -750,11 +794,16 @@ hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_
 }
 
 hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
-                           uint32_t flags, int32_t splits, char* work, hipStream_t stream) {
+                           uint32_t flags, const Plan& plan, char* work, hipStream_t stream) {
   EvalArgs a;
   a.n = g.n;
   a.K = K;
-  a.splits = splits;
+  a.items = plan.items;
+  a.kind = plan.kind;
+  a.P = plan.P;
+  a.T0 = plan.T0;
+  a.R1 = plan.R1;
+  a.R2 = plan.R2;
   a.ldq = L.ldq;
   a.det_words = L.det_words;
   a.row_words = (g.n >> 5) + 2;   // words of a row plus one word that stays zero
@@ -786,7 +835,7 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(ckm_eval_kernel, dim3((groups + waves - 1) / waves, splits), dim3(waves * kWave),
+  hipLaunchKernelGGL(ckm_eval_kernel, dim3((groups + waves - 1) / waves, plan.items), dim3(waves * kWave),
                      lds_bytes, stream, a);
   return hipGetLastError();
 }
@@ -861,6 +910,14 @@ void build_node_records(int32_t n, const double* M, const double* C, const int32
       if (nlate > 1) slow = true;
     }
     r.info = (uint32_t)(slow ? 0 : nd) | (slow ? kRecSlow : 0u);
+    uint32_t pos[1 + 2 * kRecDeps];
+    pos[0] = r.fu_ref & 31u;
+    for (int sl = 0; sl < kRecDeps; ++sl) {
+      pos[1 + 2 * sl] = r.dep[sl].s1_ref & 31u;
+      pos[2 + 2 * sl] = r.dep[sl].fl_ref & 31u;
+    }
+    for (int k = 0; k < 6; ++k) r.bits0 |= pos[k] << (5 * k);
+    for (int k = 6; k < 1 + 2 * kRecDeps; ++k) r.bits1 |= pos[k] << (5 * (k - 6));
     recs[v] = r;
   }
 }
