@@ -278,6 +278,13 @@ struct Row {
 
 __device__ __forceinline__ uint32_t bit(uint32_t word, int pos) { return (word >> pos) & 1u; }
 
+// (a & b) | c as one VALU instruction (b wave-uniform).
+__device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t d;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(d) : "v"(a), "s"(b), "v"(c));
+  return d;
+}
+
 // min(x, 1): 1 iff x != 0, as one VALU instruction.
 __device__ __forceinline__ uint32_t umin1(uint32_t x) {
   uint32_t y;
@@ -344,21 +351,25 @@ __device__ __forceinline__ void pin_s(uint32_t a, uint32_t b, uint32_t c) { asm 
 // beyond the window lie in chunks already finished, S_{t+1} is not written
 // during the stage).
 __device__ __forceinline__ void issue_reads(const RecRegs& rec, Row A, Row B, LdsVals& L) {
-  const uint32_t fu = rec.fu_ref();
-  uint32_t fl[kRecDeps], s1[kRecDeps];
-#pragma unroll
-  for (int sl = 0; sl < kRecDeps; ++sl) {
-    fl[sl] = rec.fl_ref(sl);
-    s1[sl] = rec.s1_ref(sl);
-  }
-  pin_s(fu, fl[0], s1[0]);
-  pin_s(fl[1], s1[1], fl[2]);
-  pin_s(s1[2], fl[3], s1[3]);
+  const uint32_t info = rec.info();
+  const uint32_t fu = rec.fu_ref(), fl0 = rec.fl_ref(0), s10 = rec.s1_ref(0);
+  const uint32_t fl1 = rec.fl_ref(1), s11 = rec.s1_ref(1);
+  pin_s(fu, fl0, s10);
+  pin_s(fl1, s11, info);
   L.fu = A.at_ref(fu);
-#pragma unroll
-  for (int sl = 0; sl < kRecDeps; ++sl) {
-    L.fl[sl] = A.at_ref(fl[sl]);
-    L.s1[sl] = B.at_ref(s1[sl]);
+  L.fl[0] = A.at_ref(fl0);
+  L.s1[0] = B.at_ref(s10);
+  L.fl[1] = A.at_ref(fl1);
+  L.s1[1] = B.at_ref(s11);
+  // slots 2 and 3 only for the few nodes that use them
+  if (__builtin_expect((info & 7u) > 2u, 0)) {
+    const uint32_t fl2 = rec.fl_ref(2), s12 = rec.s1_ref(2), fl3 = rec.fl_ref(3), s13 = rec.s1_ref(3);
+    pin_s(fl2, s12, fl3);
+    pin_s(s13, s13, s13);
+    L.fl[2] = A.at_ref(fl2);
+    L.s1[2] = B.at_ref(s12);
+    L.fl[3] = A.at_ref(fl3);
+    L.s1[3] = B.at_ref(s13);
   }
 }
 
@@ -405,7 +416,8 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
       anyU = 0;
       r = 1;
     } else {
-      anyU = (sc.Rlo & um_lo) | (sc.Rhi & um_hi) | __builtin_amdgcn_ubfe(L.fu, b0, 1);
+      const uint32_t far = __builtin_amdgcn_ubfe(L.fu, b0, 1);
+      anyU = and_or(sc.Rlo, um_lo, and_or(sc.Rhi, um_hi, far));
       anyU = umin1(anyU);
       r = (s1 | anyU) & ~s0 & 1u;
     }
@@ -419,7 +431,8 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
       const uint32_t d_lo = rec.get(12 + 6 * sl), d_hi = rec.get(13 + 6 * sl);
       pin_s(lm_lo, lm_hi, d_lo);
       pin_s(d_hi, d_hi, d_hi);
-      uint32_t later = (sc.Rlo & lm_lo) | (sc.Rhi & lm_hi) | __builtin_amdgcn_ubfe(L.fl[sl], bitpos(b0, b1, 2 + 2 * sl), 1);
+      const uint32_t far = __builtin_amdgcn_ubfe(L.fl[sl], bitpos(b0, b1, 2 + 2 * sl), 1);
+      uint32_t later = and_or(sc.Rlo, lm_lo, and_or(sc.Rhi, lm_hi, far));
       later = umin1(later);
       const uint32_t fr = r & ~__builtin_amdgcn_ubfe(L.s1[sl], bitpos(b0, b1, 1 + 2 * sl), 1) & ~later & 1u;
       freed = fma((double)fr, dbl(d_lo, d_hi), freed);
