@@ -15,6 +15,7 @@
 #include <hip/hip_runtime.h>
 
 #include <climits>
+#include <cstddef>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -163,7 +164,10 @@ struct NodeRec {
   // the bit positions of the references, five bits each: fu, then per slot
   // s1 and fl (slots 0-1 and s1 of slot 2 in bits0, the rest in bits1)
   uint32_t bits0, bits1;
-  uint32_t pad[30];       // one dword per lane of a 64-lane load
+  // fp64 operands again, read by two wave-uniform 16-byte loads: M_v, C_v,
+  // and the M of dependency slots 0 and 1
+  double mc[2], dm01[2];
+  uint32_t pad[22];       // one dword per lane of a 64-lane load
 };
 static_assert(sizeof(NodeRec) == kNodeRecBytes, "node record layout");
 
@@ -178,15 +182,26 @@ __device__ __forceinline__ double dbl(uint32_t lo, uint32_t hi) {
   return __hiloint2double((int)hi, (int)lo);
 }
 
+// A zero the compiler cannot see through: added to an address, it keeps a
+// wave-uniform load a vector load (whose completion counter is in order, so
+// it can run nodes ahead of its use) instead of a scalar one.
+__device__ __forceinline__ uint32_t opaque_zero() {
+  uint32_t z;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+  return z;
+}
+
 // A node record spread over the lanes of one vector register: lane L holds
 // dword L. Fields are moved to scalar registers when used
 // (v_readlane), so a record costs 256 bytes of vector-memory return per
 // wave instead of 128 bytes for each of the 64 lanes.
 struct RecRegs {
   uint32_t w;
+  uint4 mc, dm;  // M_v, C_v and the M of slots 0-1, in every lane
   __device__ uint32_t get(int i) const { return __builtin_amdgcn_readlane(w, i); }
-  __device__ double M() const { return dbl(get(0), get(1)); }
-  __device__ double C() const { return dbl(get(2), get(3)); }
+  __device__ double M() const { return dbl(mc.x, mc.y); }
+  __device__ double C() const { return dbl(mc.z, mc.w); }
+  __device__ double dM01(int s) const { return s == 0 ? dbl(dm.x, dm.y) : dbl(dm.z, dm.w); }
   __device__ uint32_t umask_lo() const { return get(4); }
   __device__ uint32_t umask_hi() const { return get(5); }
   __device__ uint32_t fu_ref() const { return get(6); }
@@ -212,6 +227,8 @@ __device__ __forceinline__ void load_rec(RecRegs& r, const uint4* __restrict__ r
   const int vu = __builtin_amdgcn_readfirstlane(v);
   const char* base = reinterpret_cast<const char*>(recs) + (size_t)vu * kNodeRecBytes;
   const size_t off = (size_t)((threadIdx.x & 63u) * 4u);
+  r.mc = *reinterpret_cast<const uint4*>(base + offsetof(NodeRec, mc) + (size_t)opaque_zero());
+  r.dm = *reinterpret_cast<const uint4*>(base + offsetof(NodeRec, dm01) + (size_t)opaque_zero());
   r.w = *reinterpret_cast<const uint32_t*>(base + off);
 }
 
@@ -401,14 +418,12 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
   const uint32_t s0 = bit(sc.w0, jj);
   const uint32_t s1 = bit(sc.w1, jj);
   // the node's scalar fields, read together
-  const uint32_t m_lo = rec.get(0), m_hi = rec.get(1), c_lo = rec.get(2), c_hi = rec.get(3);
   const uint32_t um_lo = rec.umask_lo(), um_hi = rec.umask_hi(), info = rec.info();
   const uint32_t b0 = rec.bits0(), b1 = rec.bits1();
-  pin_s(m_lo, m_hi, c_lo);
-  pin_s(c_hi, um_lo, um_hi);
-  pin_s(info, b0, b1);
-  const double Mv = dbl(m_lo, m_hi);
-  const double Cv = dbl(c_lo, c_hi);
+  pin_s(um_lo, um_hi, info);
+  pin_s(b0, b1, b1);
+  const double Mv = rec.M();
+  const double Cv = rec.C();
   uint32_t anyU, r;
   double freed;
   if (__builtin_expect(!(info & kRecSlow), 1)) {
@@ -428,14 +443,20 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
     const int nd = (int)(info & 7u);
     auto slot = [&](int sl) {
       const uint32_t lm_lo = rec.lm_lo(sl), lm_hi = rec.lm_hi(sl);
-      const uint32_t d_lo = rec.get(12 + 6 * sl), d_hi = rec.get(13 + 6 * sl);
-      pin_s(lm_lo, lm_hi, d_lo);
-      pin_s(d_hi, d_hi, d_hi);
+      pin_s(lm_lo, lm_hi, lm_hi);
+      double dMs;
+      if (sl < 2) {
+        dMs = rec.dM01(sl);
+      } else {
+        const uint32_t d_lo = rec.get(12 + 6 * sl), d_hi = rec.get(13 + 6 * sl);
+        pin_s(d_lo, d_hi, d_hi);
+        dMs = dbl(d_lo, d_hi);
+      }
       const uint32_t far = __builtin_amdgcn_ubfe(L.fl[sl], bitpos(b0, b1, 2 + 2 * sl), 1);
       uint32_t later = and_or(sc.Rlo, lm_lo, and_or(sc.Rhi, lm_hi, far));
       later = umin1(later);
       const uint32_t fr = r & ~__builtin_amdgcn_ubfe(L.s1[sl], bitpos(b0, b1, 1 + 2 * sl), 1) & ~later & 1u;
-      freed = fma((double)fr, dbl(d_lo, d_hi), freed);
+      freed = fma((double)fr, dMs, freed);
     };
     // most nodes have one or two dependencies
     if (__builtin_expect(nd >= 1, 1)) slot(0);
@@ -489,7 +510,10 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
 }
 
 // Waits for every load of a record buffer.
-__device__ __forceinline__ void settle(const RecRegs& r) { asm volatile("" ::"v"(r.w)); }
+__device__ __forceinline__ void settle(const RecRegs& r) {
+  asm volatile("" ::"v"(r.w), "v"(r.mc.x), "v"(r.mc.y), "v"(r.mc.z), "v"(r.mc.w), "v"(r.dm.x), "v"(r.dm.y),
+               "v"(r.dm.z), "v"(r.dm.w));
+}
 
 // One node of the scan, software-pipelined: the record of node v - 2 is
 // requested, the LDS words of node v - 1 are requested, then node v is
@@ -931,6 +955,10 @@ void build_node_records(int32_t n, const double* M, const double* C, const int32
     }
     for (int k = 0; k < 6; ++k) r.bits0 |= pos[k] << (5 * k);
     for (int k = 6; k < 1 + 2 * kRecDeps; ++k) r.bits1 |= pos[k] << (5 * (k - 6));
+    r.mc[0] = r.M;
+    r.mc[1] = r.C;
+    r.dm01[0] = r.dep[0].M;
+    r.dm01[1] = r.dep[1].M;
     recs[v] = r;
   }
 }
