@@ -131,9 +131,11 @@ ckm_status ckm_quantize_async(const ckm_graph* g, const double* d_s_frac, int64_
                               void* d_work, size_t work_bytes, void* stream);
 
 /* Stages a2-a5 for candidates 0..K-1: rounding, Algorithm 2's R repair,
- * memory simulation and cost. Writes per-candidate partial results into the
- * work buffer. stage_splits = number of stage ranges each group of 64
- * candidates is split into (0 = automatic); results do not depend on it. */
+ * memory simulation and cost. Leaves each candidate's peak and cost in the
+ * work buffer (reset at the start of every call). stage_splits = number of
+ * stage ranges each group of 64 candidates is split into, 1..n (0 =
+ * automatic: ranges cut and ordered for load balance); results do not depend
+ * on it. */
 ckm_status ckm_evaluate_async(const ckm_graph* g, int32_t K, uint64_t seed, uint32_t flags,
                               int32_t stage_splits, void* d_work, size_t work_bytes, void* stream);
 

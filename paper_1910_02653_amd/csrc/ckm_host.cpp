@@ -52,12 +52,9 @@ struct DeviceGuard {
 
 namespace ckm {
 
-int32_t max_splits_for(int32_t n, int32_t K) {
-  // partial arrays of at most 2^22 entries each (64 MiB), at most n rows
-  int64_t cap = std::max<int64_t>(4, (int64_t(1) << 22) / std::max<int32_t>(K, 1));
-  cap = std::min<int64_t>(cap, 1024);
-  cap = std::min<int64_t>(cap, n);
-  return (int32_t)std::max<int64_t>(cap, 1);
+int32_t max_splits_for(int32_t n, int32_t /*K*/) {
+  // work items per group of 64 candidates: at most one per stage
+  return std::max<int32_t>(n, 1);
 }
 
 // Resident evaluate waves on the device: 256 CUs, as many waves per CU as
@@ -107,14 +104,14 @@ Layout make_layout(int32_t n, int32_t K) {
   L.det_words = L.ldq / 32;
   L.row_words = 2 * ((n + 63) / 64);
   L.max_splits = max_splits_for(n, K);
-  L.reduce_blocks = (K + kWave - 1) / kWave;
+  L.reduce_blocks = (K + 255) / 256;
   size_t off = 0;
   L.hdr_off = off;       off = align256(off + 256);
   L.q_off = off;         off = align256(off + (size_t)n * L.ldq * sizeof(uint32_t));
   L.det_off = off;       off = align256(off + (size_t)n * L.det_words * sizeof(uint32_t));
   L.nan_off = off;       off = align256(off + (size_t)n * sizeof(int32_t));
-  L.part_peak_off = off; off = align256(off + (size_t)L.max_splits * K * sizeof(int64_t));
-  L.part_cost_off = off; off = align256(off + (size_t)L.max_splits * K * sizeof(int64_t));
+  L.part_peak_off = off; off = align256(off + (size_t)K * sizeof(int64_t));
+  L.part_cost_off = off; off = align256(off + (size_t)K * sizeof(int64_t));
   L.best_off = off;      off = align256(off + (size_t)L.reduce_blocks * 24);
   L.srows_off = off;     off = align256(off + (size_t)n * L.row_words * sizeof(uint32_t));
   L.total = off;

@@ -46,7 +46,7 @@ struct Layout {
   int32_t ldq = 0;        // q / det row stride in elements: round_up(n + 8, 64)
   int32_t det_words = 0;  // ldq / 32
   int32_t row_words = 0;  // 32-bit words per output bit row: 2 * ceil(n / 64)
-  int32_t max_splits = 0; // capacity of the partial-result arrays
+  int32_t max_splits = 0; // most work items per group of 64 candidates
   int32_t reduce_blocks = 0;
   // hdr: int32 number of work items (rows of the partial arrays) of the last evaluate
   size_t hdr_off = 0, q_off = 0, det_off = 0, nan_off = 0, part_peak_off = 0, part_cost_off = 0,

@@ -247,8 +247,8 @@ struct EvalArgs {
   cptr<int32_t> dep_idx;
   cptr<int32_t> dep_upos;
   const uint4* __restrict__ recs;
-  int64_t* __restrict__ part_peak;   // [items][K]
-  int64_t* __restrict__ part_cost;   // [items][K]
+  int64_t* __restrict__ part_peak;   // [K] running max over work items
+  int64_t* __restrict__ part_cost;   // [K] running sum over work items
   int32_t* __restrict__ hdr;
 };
 
@@ -605,12 +605,23 @@ __global__ void __launch_bounds__(kMaxEvalWaves * kWave) ckm_eval_kernel(EvalArg
       B = tmp;
     }
   }
-  if ((int)k < a.K) {
-    const size_t o = (size_t)item * a.K + k;
-    a.part_peak[o] = (t0 < t1) ? (int64_t)seg_peak : INT64_MIN;
-    a.part_cost[o] = seg_cost;
+  // fold the item's result into the candidate's totals: max of the stage
+  // peaks, sum of the stage costs (exact integers, any order)
+  if ((int)k < a.K && t0 < t1) {
+    atomicMax(reinterpret_cast<long long*>(a.part_peak) + k, (long long)seg_peak);
+    atomicAdd(reinterpret_cast<unsigned long long*>(a.part_cost) + k, (unsigned long long)seg_cost);
   }
   if (group == 0 && item == 0 && lane == 0) a.hdr[0] = a.items;
+}
+
+// Empty totals before an evaluate launch: peak = INT64_MIN, cost = 0.
+__global__ void __launch_bounds__(256) ckm_eval_init_kernel(int32_t K, int64_t* __restrict__ peak,
+                                                            int64_t* __restrict__ cost) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k < K) {
+    peak[k] = INT64_MIN;
+    cost[k] = 0;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -648,8 +659,8 @@ __global__ void __launch_bounds__(256) ckm_quantize_kernel(const double* __restr
 }
 
 // ---------------------------------------------------------------------------
-// Per-candidate reduction over stage splits, feasibility, and the block's
-// lexicographic minimum of (cost, peak, k) over feasible candidates.
+// Per-candidate feasibility and the block's lexicographic minimum of
+// (cost, peak, k) over feasible candidates.
 struct Best {
   int64_t cost, peak;
   int32_t k, pad;
@@ -663,52 +674,28 @@ __device__ __forceinline__ bool better(const Best& x, const Best& y) {
   return x.k < y.k;
 }
 
-// One block per 64 candidates: the four waves reduce interleaved stage
-// splits (coalesced over candidates), then combine; feasibility and the
-// block's lexicographic minimum follow.
-__global__ void __launch_bounds__(256) ckm_reduce_kernel(int32_t K, const int32_t* __restrict__ hdr,
-                                                         const int64_t* __restrict__ part_peak,
-                                                         const int64_t* __restrict__ part_cost,
+// One thread per candidate: copy out its totals, test the budget, then the
+// block's minimum.
+__global__ void __launch_bounds__(256) ckm_reduce_kernel(int32_t K, const int64_t* __restrict__ tot_peak,
+                                                         const int64_t* __restrict__ tot_cost,
                                                          int64_t budget, int64_t* __restrict__ peak,
                                                          int64_t* __restrict__ cost,
                                                          uint8_t* __restrict__ feasible,
                                                          Best* __restrict__ block_best) {
-  __shared__ int64_t sp[4][kWave];
-  __shared__ int64_t sc[4][kWave];
-  __shared__ Best sb[kWave];
-  const int lane = threadIdx.x & (kWave - 1);
-  const int stripe = threadIdx.x / kWave;
-  const int k = blockIdx.x * kWave + lane;
-  const int splits = hdr[0];
-  int64_t p = INT64_MIN, c = 0;
+  __shared__ Best sb[256];
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  Best b{0, 0, -1, 0};
   if (k < K) {
-    for (int s = stripe; s < splits; s += 4) {
-      const int64_t v = part_peak[(size_t)s * K + k];
-      p = v > p ? v : p;
-      c += part_cost[(size_t)s * K + k];
-    }
+    const int64_t p = tot_peak[k], c = tot_cost[k];
+    peak[k] = p;
+    cost[k] = c;
+    const bool f = p <= budget;
+    feasible[k] = f ? 1 : 0;
+    if (f) b = Best{c, p, k, 0};
   }
-  sp[stripe][lane] = p;
-  sc[stripe][lane] = c;
+  sb[threadIdx.x] = b;
   __syncthreads();
-  if (stripe == 0) {
-    Best b{0, 0, -1, 0};
-    if (k < K) {
-#pragma unroll
-      for (int q = 1; q < 4; ++q) {
-        p = sp[q][lane] > p ? sp[q][lane] : p;
-        c += sc[q][lane];
-      }
-      peak[k] = p;
-      cost[k] = c;
-      const bool f = p <= budget;
-      feasible[k] = f ? 1 : 0;
-      if (f) b = Best{c, p, k, 0};
-    }
-    sb[lane] = b;
-  }
-  __syncthreads();
-  for (int off = kWave / 2; off > 0; off >>= 1) {
+  for (int off = blockDim.x / 2; off > 0; off >>= 1) {
     if (threadIdx.x < off && better(sb[threadIdx.x + off], sb[threadIdx.x]))
       sb[threadIdx.x] = sb[threadIdx.x + off];
     __syncthreads();
@@ -872,6 +859,8 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     if (e != hipSuccess) return e;
   }
+  hipLaunchKernelGGL(ckm_eval_init_kernel, dim3((K + 255) / 256), dim3(256), 0, stream, K, a.part_peak,
+                     a.part_cost);
   hipLaunchKernelGGL(ckm_eval_kernel, dim3((groups + waves - 1) / waves, plan.items), dim3(waves * kWave),
                      lds_bytes, stream, a);
   return hipGetLastError();
@@ -881,11 +870,10 @@ hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_
                          int64_t budget, uint32_t flags, int64_t* d_peak, int64_t* d_cost,
                          uint8_t* d_feasible, int32_t* d_best_k, uint64_t* d_best_S,
                          uint64_t* d_best_R, int32_t* d_status, char* work, hipStream_t stream) {
-  const int rb = (K + kWave - 1) / kWave;
+  const int rb = L.reduce_blocks;
   hipLaunchKernelGGL(ckm_reduce_kernel, dim3(rb), dim3(256), 0, stream, K,
-                     at<const int32_t>(work, L.hdr_off), at<const int64_t>(work, L.part_peak_off),
-                     at<const int64_t>(work, L.part_cost_off), budget, d_peak, d_cost, d_feasible,
-                     at<Best>(work, L.best_off));
+                     at<const int64_t>(work, L.part_peak_off), at<const int64_t>(work, L.part_cost_off),
+                     budget, d_peak, d_cost, d_feasible, at<Best>(work, L.best_off));
   hipLaunchKernelGGL(ckm_argmin_kernel, dim3(1), dim3(256), 0, stream, rb,
                      at<const Best>(work, L.best_off), g.n, at<const int32_t>(work, L.nan_off),
                      d_best_k, d_status);
