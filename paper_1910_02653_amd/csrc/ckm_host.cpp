@@ -60,7 +60,7 @@ int32_t max_splits_for(int32_t n, int32_t /*K*/) {
 // Resident evaluate waves on the device: 256 CUs, as many waves per CU as
 // the two LDS rows of a wave allow (at most 20).
 static int64_t eval_slots(int32_t n) {
-  const int64_t wave_lds = 2 * (int64_t)((n >> 5) + 2) * kWave * 4;
+  const int64_t wave_lds = 2 * (int64_t)((n >> 5) + 1) * kWave * 4;
   return 256 * std::max<int64_t>(1, std::min<int64_t>(20, (160 * 1024) / wave_lds));
 }
 

@@ -146,7 +146,7 @@ __device__ __forceinline__ uint32_t round_word(QPtr qrow, int w, int r, uint32_t
 // row buffer (lane 0) in the high half and the bit position in the low half.
 struct DepSlot {
   uint32_t s1_ref;        // the dep i in the next-stage checkpoint row
-  uint32_t fl_ref;        // the user of i beyond v + 64 in the R row, or the zero word
+  uint32_t fl_ref;        // the user of i beyond v + 64 in the R row, or none (node n)
   uint32_t lmask_lo;      // users u of i with v < u <= v + 32
   uint32_t lmask_hi;      //                  v + 32 < u <= v + 64
   double M;               // M_i
@@ -158,7 +158,7 @@ struct NodeRec {
   double M, C;            // M_v, C_v
   uint32_t umask_lo;      // users u of v with u <= v + 32
   uint32_t umask_hi;      //                  v + 32 < u <= v + 64
-  uint32_t fu_ref;        // the user of v beyond v + 64 in the R row, or the zero word
+  uint32_t fu_ref;        // the user of v beyond v + 64 in the R row, or none (node n)
   uint32_t info;          // number of deps (bits 0-2) | kRecSlow
   DepSlot dep[kRecDeps];
   // the bit positions of the references, five bits each: fu, then per slot
@@ -174,9 +174,9 @@ static_assert(sizeof(NodeRec) == kNodeRecBytes, "node record layout");
 __host__ __device__ __forceinline__ uint32_t make_ref(int node) {
   return ((uint32_t)(node >> 5) * 256u) << 16 | (uint32_t)(node & 31);
 }
-__host__ __device__ __forceinline__ uint32_t zero_ref(int n) {
-  return ((uint32_t)((n >> 5) + 1) * 256u) << 16;
-}
+// "No node": the bit of node n, which no row ever sets (rows hold bits of
+// nodes below their stage, and stages are < n).
+__host__ __device__ __forceinline__ uint32_t zero_ref(int n) { return make_ref(n); }
 
 __device__ __forceinline__ double dbl(uint32_t lo, uint32_t hi) {
   return __hiloint2double((int)hi, (int)lo);
@@ -347,12 +347,7 @@ struct Scan {
 
 // LDS words one node reads: the R word of v's user beyond the window, and
 // per dependency slot the R word of its user beyond the window and its
-// S_{t+1} word. Unused slots reference the zero word.
-// LDS words one node reads: the R word of v's user beyond the window, and
-// per dependency slot the R word of its user beyond the window and its
-// S_{t+1} word. Unused slots reference the zero word. The references stay
-// in scalar registers until the node is evaluated (their low five bits are
-// the bit positions).
+// S_{t+1} word. Unused slots reference the "none" bit (node n).
 struct LdsVals {
   uint32_t fu;
   uint32_t fl[kRecDeps];
@@ -409,7 +404,7 @@ __device__ __forceinline__ double max_f64(double a, double b) {
 // i in Deps[v] u {v}: v computed, i not kept, and no computed user of i
 // after v. A holds S_t below the current chunk and R_t above it; B holds
 // S_{t+1}. Rows are zero beyond their last word, so a reference to a node
-// above t (or to the zero word) reads 0. kFirst: v == t, which is always
+// above t (or to node n, "none") reads 0. kFirst: v == t, which is always
 // computed and has no computed user in the stage.
 template <bool kFirst>
 __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const RecRegs& rec, const LdsVals& L,
@@ -582,7 +577,7 @@ __global__ void __launch_bounds__(kMaxEvalWaves * kWave) ckm_eval_kernel(EvalArg
   char* wave_lds = reinterpret_cast<char*>(lds) + (size_t)wave * 2 * a.row_words * 256;
   Row A{wave_lds + 4 * lane};
   Row B{wave_lds + (size_t)a.row_words * 256 + 4 * lane};
-  // Rows start zeroed: words beyond a row's end (and the zero word) read 0.
+  // Rows start zeroed: words beyond a row's end (and node n's bit) read 0.
   for (int w = 0; w < a.row_words; ++w) {
     A.word(w) = 0u;
     B.word(w) = 0u;
@@ -830,7 +825,7 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   a.R2 = plan.R2;
   a.ldq = L.ldq;
   a.det_words = L.det_words;
-  a.row_words = (g.n >> 5) + 2;   // words of a row plus one word that stays zero
+  a.row_words = (g.n >> 5) + 1;   // words for nodes 0 .. n (node n's bit is the "none" bit)
   a.key0 = (uint32_t)(seed & 0xFFFFFFFFu);
   a.key1 = (uint32_t)(seed >> 32);
   a.det0 = (flags & CKM_F_DET0) ? 1u : 0u;
