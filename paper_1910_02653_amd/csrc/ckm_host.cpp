@@ -57,11 +57,14 @@ int32_t max_splits_for(int32_t n, int32_t /*K*/) {
   return std::max<int32_t>(n, 1);
 }
 
-// Resident evaluate waves on the device: 256 CUs, as many waves per CU as
-// the two LDS rows of a wave allow (at most 20).
+// Resident evaluate waves on the device: 256 CUs times the waves per CU.
+// With n < 1024 one row is in registers and the register file allows 16
+// waves per CU; otherwise the two LDS rows of a wave set the count.
 static int64_t eval_slots(int32_t n) {
-  const int64_t wave_lds = 2 * (int64_t)((n >> 5) + 1) * kWave * 4;
-  return 256 * std::max<int64_t>(1, std::min<int64_t>(20, (160 * 1024) / wave_lds));
+  const int64_t words = (n >> 5) + 1;
+  if (words <= 32) return 256 * 16;
+  const int64_t wave_lds = 2 * words * kWave * 4;
+  return 256 * std::max<int64_t>(1, std::min<int64_t>(16, (160 * 1024) / wave_lds));
 }
 
 Plan plan_splits(int32_t n, int32_t splits) {

@@ -22,12 +22,6 @@
 
 #include "ckm_internal.h"
 
-#ifndef CKM_MAX_EVAL_WAVES
-#define CKM_MAX_EVAL_WAVES 1
-#endif
-#ifndef CKM_CU_LDS
-#define CKM_CU_LDS (160 * 1024)
-#endif
 
 namespace ckm {
 namespace {
@@ -152,7 +146,6 @@ struct DepSlot {
   double M;               // M_i
 };
 constexpr int kRecDeps = 4;
-constexpr int kMaxEvalWaves = CKM_MAX_EVAL_WAVES;
 constexpr uint32_t kRecSlow = 1u << 31;   // node does not fit: use the CSR lists
 struct NodeRec {
   double M, C;            // M_v, C_v
@@ -293,6 +286,26 @@ struct Row {
   }
 };
 
+// A row held in the lane's vector registers instead of LDS (n < 1024): word
+// w is register w of the array; a wave-uniform index selects it with
+// s_set_gpr_idx. Same interface as Row.
+constexpr int kRegRowWords = 32;
+typedef uint32_t u32x32 __attribute__((ext_vector_type(kRegRowWords)));
+struct RowReg {
+  u32x32 w;
+  struct WordRef {  // assignable element of the vector
+    u32x32& v;
+    int i;
+    __device__ WordRef& operator=(uint32_t x) {
+      v[i] = x;
+      return *this;
+    }
+    __device__ operator uint32_t() const { return v[i]; }
+  };
+  __device__ WordRef word(int i) { return WordRef{w, i}; }
+  __device__ uint32_t at_ref(uint32_t ref) const { return w[ref >> 24]; }  // word index of the ref
+};
+
 __device__ __forceinline__ uint32_t bit(uint32_t word, int pos) { return (word >> pos) & 1u; }
 
 // (a & b) | c as one VALU instruction (b wave-uniform).
@@ -310,7 +323,8 @@ __device__ __forceinline__ uint32_t umin1(uint32_t x) {
 }
 
 // Row r of the candidate into words 0 .. r/32.
-__device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bool det_lane, Row dst) {
+template <typename RowT>
+__device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bool det_lane, RowT& dst) {
   const int nw = (r >> 5) + 1;
   if (r >= a.n) {  // S after the last stage: nothing is kept
     for (int w = 0; w < nw; ++w) dst.word(w) = 0u;
@@ -362,7 +376,8 @@ __device__ __forceinline__ void pin_s(uint32_t a, uint32_t b, uint32_t c) { asm 
 // node ahead of their use: the words they read are final by then (users
 // beyond the window lie in chunks already finished, S_{t+1} is not written
 // during the stage).
-__device__ __forceinline__ void issue_reads(const RecRegs& rec, Row A, Row B, LdsVals& L) {
+template <typename RowB>
+__device__ __forceinline__ void issue_reads(const RecRegs& rec, Row A, RowB& B, LdsVals& L) {
   const uint32_t info = rec.info();
   const uint32_t fu = rec.fu_ref(), fl0 = rec.fl_ref(0), s10 = rec.s1_ref(0);
   const uint32_t fl1 = rec.fl_ref(1), s11 = rec.s1_ref(1);
@@ -406,9 +421,9 @@ __device__ __forceinline__ double max_f64(double a, double b) {
 // S_{t+1}. Rows are zero beyond their last word, so a reference to a node
 // above t (or to node n, "none") reads 0. kFirst: v == t, which is always
 // computed and has no computed user in the stage.
-template <bool kFirst>
+template <bool kFirst, typename RowB>
 __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const RecRegs& rec, const LdsVals& L,
-                                          Scan& sc, Row A, Row B) {
+                                          Scan& sc, Row A, RowB& B) {
   const int jj = v & 31;
   const uint32_t s0 = bit(sc.w0, jj);
   const uint32_t s1 = bit(sc.w1, jj);
@@ -514,18 +529,19 @@ __device__ __forceinline__ void settle(const RecRegs& r) {
 // requested, the LDS words of node v - 1 are requested, then node v is
 // evaluated with the record and words requested one and two nodes earlier.
 // Record buffers rotate through (C, N, NN) so registers never move.
-template <int C, int N, int NN, bool kFirst>
+template <int C, int N, int NN, bool kFirst, typename RowB>
 __device__ __forceinline__ void pipe_step(const EvalArgs& a, int t, int v, RecRegs (&rb)[3], LdsVals (&lb)[3],
-                                          Scan& sc, Row A, Row B) {
+                                          Scan& sc, Row A, RowB& B) {
   load_rec(rb[NN], a.recs, max(v - 2, 0));
   issue_reads(rb[N], A, B, lb[N]);
   asm volatile("" ::: "memory");  // keep the requests ahead of this node's work
-  scan_node<kFirst>(a, t, v, rb[C], lb[C], sc, A, B);
+  scan_node<kFirst, RowB>(a, t, v, rb[C], lb[C], sc, A, B);
 }
 
 // One stage t of one candidate (per lane): S_t in A, S_{t+1} in B on entry,
 // R_t in A on exit.
-__device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, Row B, double& stage_peak,
+template <typename RowB>
+__device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, RowB& B, double& stage_peak,
                                            double& stage_cost) {
   Scan sc;
   sc.U0 = a.base;
@@ -563,41 +579,61 @@ __device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, Row 
   stage_cost = sc.cost;
 }
 
-// A workgroup holds several waves (several groups of 64 candidates) on the
-// same stage range, so they read the same node records and thresholds at
-// about the same time and share them through the caches.
-__global__ void __launch_bounds__(kMaxEvalWaves * kWave) ckm_eval_kernel(EvalArgs a) {
+// One wave per workgroup: 64 candidates over one work item (a range of
+// stages). kBReg: the S_{t+1} row lives in vector registers and is copied to
+// the LDS row at the end of each stage (n < 1024), halving the LDS a wave
+// needs; otherwise both rows are in LDS and swap roles.
+template <bool kBReg>
+__global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
   extern __shared__ uint32_t lds[];
-  const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x / kWave;
-  const int group = blockIdx.x * (blockDim.x / kWave) + wave;
+  const int lane = threadIdx.x;
+  const int group = blockIdx.x;
   const int item = blockIdx.y;
   const uint32_t k = (uint32_t)(group * kWave + lane);
   const bool det_lane = a.det0 && k == 0;
-  char* wave_lds = reinterpret_cast<char*>(lds) + (size_t)wave * 2 * a.row_words * 256;
+  char* wave_lds = reinterpret_cast<char*>(lds);
   Row A{wave_lds + 4 * lane};
-  Row B{wave_lds + (size_t)a.row_words * 256 + 4 * lane};
   // Rows start zeroed: words beyond a row's end (and node n's bit) read 0.
-  for (int w = 0; w < a.row_words; ++w) {
-    A.word(w) = 0u;
-    B.word(w) = 0u;
-  }
+  for (int w = 0; w < a.row_words; ++w) A.word(w) = 0u;
 
   int t0, t1;
   item_range(a, item, t0, t1);
   double seg_peak = -INFINITY;
   int64_t seg_cost = 0;
-  if (t0 < t1) {
-    gen_row(a, t0, k, det_lane, A);
-    for (int t = t0; t < t1; ++t) {
-      gen_row(a, t + 1, k, det_lane, B);
-      double sp, sc;
-      eval_stage(a, t, A, B, sp, sc);
-      seg_peak = fmax(seg_peak, sp);
-      seg_cost += (int64_t)sc;
-      const Row tmp = A;
-      A = B;
-      B = tmp;
+  if (kBReg) {
+    RowReg B;
+    B.w = (u32x32)0u;
+    if (t0 < t1) {
+      gen_row(a, t0, k, det_lane, A);
+      for (int t = t0; t < t1; ++t) {
+        gen_row(a, t + 1, k, det_lane, B);
+        double sp, sc;
+        eval_stage(a, t, A, B, sp, sc);
+        seg_peak = fmax(seg_peak, sp);
+        seg_cost += (int64_t)sc;
+        // S_{t+1} becomes the next stage's S_t (its words end at (t+1)/32;
+        // the LDS row is zero above that)
+        const int last = (t + 1) >> 5;
+#pragma unroll
+        for (int w = 0; w < kRegRowWords; ++w)
+          if (w <= last) A.word(w) = B.w[w];
+      }
+    }
+  } else {
+    Row B{wave_lds + (size_t)a.row_words * 256 + 4 * lane};
+    for (int w = 0; w < a.row_words; ++w) B.word(w) = 0u;
+    if (t0 < t1) {
+      gen_row(a, t0, k, det_lane, A);
+      for (int t = t0; t < t1; ++t) {
+        gen_row(a, t + 1, k, det_lane, B);
+        double sp, sc;
+        eval_stage(a, t, A, B, sp, sc);
+        seg_peak = fmax(seg_peak, sp);
+        seg_cost += (int64_t)sc;
+        const Row tmp = A;
+        A = B;
+        B = tmp;
+      }
     }
   }
   // fold the item's result into the candidate's totals: max of the stage
@@ -843,21 +879,19 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   a.part_cost = at<int64_t>(work, L.part_cost_off);
   a.hdr = at<int32_t>(work, L.hdr_off);
   const int groups = (K + kWave - 1) / kWave;
-  const size_t wave_lds = 2u * (size_t)a.row_words * kWave * sizeof(uint32_t);
-  // waves per workgroup: up to kMaxEvalWaves while two workgroups still fit a CU's LDS
-  int waves = 1;
-  while (waves * 2 <= kMaxEvalWaves && waves * 2 <= groups && 2 * (size_t)(waves * 2) * wave_lds <= CKM_CU_LDS)
-    waves *= 2;
-  const size_t lds_bytes = (size_t)waves * wave_lds;
+  const bool breg = a.row_words <= kRegRowWords;
+  const size_t lds_bytes = (breg ? 1u : 2u) * (size_t)a.row_words * kWave * sizeof(uint32_t);
+  const void* fn = breg ? (const void*)ckm_eval_kernel<true> : (const void*)ckm_eval_kernel<false>;
   if (lds_bytes > 65536) {
-    hipError_t e = hipFuncSetAttribute((const void*)ckm_eval_kernel,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(ckm_eval_init_kernel, dim3((K + 255) / 256), dim3(256), 0, stream, K, a.part_peak,
                      a.part_cost);
-  hipLaunchKernelGGL(ckm_eval_kernel, dim3((groups + waves - 1) / waves, plan.items), dim3(waves * kWave),
-                     lds_bytes, stream, a);
+  if (breg)
+    hipLaunchKernelGGL(ckm_eval_kernel<true>, dim3(groups, plan.items), dim3(kWave), lds_bytes, stream, a);
+  else
+    hipLaunchKernelGGL(ckm_eval_kernel<false>, dim3(groups, plan.items), dim3(kWave), lds_bytes, stream, a);
   return hipGetLastError();
 }
 
