@@ -11,7 +11,9 @@ Prints one JSON line. `value` is candidate schedules evaluated per second.
 bandwidth with the algorithmic bytes of bit-packed S and R rows, each
 written once and read once: 4 * n * ceil(n/64) * 8 bytes per candidate.
 `cpu_baseline` times the CPU oracle on a bounded sample of the same
-workload.
+workload. `supplied_schedules` times the batch evaluation of K given integral
+checkpoint matrices (banded, 30 % of values kept) on the same graph: Algorithm
+2 repair, simulation, argmin and the best R, with the matrices resident in HBM.
 """
 from __future__ import annotations
 
@@ -63,6 +65,35 @@ def cpu_baseline(w, sample: int):
                       "one thread, %.1f s" % (sample - 1, w.K, w.n, dt)}
 
 
+def time_schedules(g, w, K, steps, stream):
+    """Throughput of ckm_eval_schedules_async on K banded integral S matrices."""
+    import numpy as np
+    import torch
+
+    from paper_1910_02653_amd import ckm
+    from paper_1910_02653_amd import workloads as wl
+
+    rows = wl.random_schedules(w.n, K, seed=w.seed + 1, density=0.3, kind="intervals", junk=False)
+    d_S = torch.from_numpy(rows.view(np.int64)).cuda()
+    work = g.alloc_work(K)
+    out = g.alloc_outputs(K)
+    for _ in range(3):
+        g.eval_schedules_async(d_S, K, w.budget, out, work, stream)
+    torch.cuda.synchronize()
+    assert int(out["status"].item()) == ckm.OK
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(steps):
+        g.eval_schedules_async(d_S, K, w.budget, out, work, stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    return {"value": K / (ms * 1e-3), "unit": "candidates/s", "ms_per_call": ms, "steps": steps,
+            "input": "K=%d banded S matrices (each value kept with p=0.3 over a random stage range), "
+                     "%.1f MB of bit rows in HBM" % (K, rows.nbytes / 1e6)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -71,6 +102,8 @@ def main():
     ap.add_argument("--config", type=int, default=4, help="workload 1..5 (4 = transformer stack)")
     ap.add_argument("--splits", type=int, default=0, help="stage splits per 64 candidates (0 = auto)")
     ap.add_argument("--cpu-sample", type=int, default=256, help="oracle candidates to time (0 = skip)")
+    ap.add_argument("--sched-steps", type=int, default=20,
+                    help="timed calls of the supplied-schedule evaluation (0 = skip)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -150,6 +183,8 @@ def main():
                      "traffic": traffic},
         "wall_s": wall,
     }
+    if args.sched_steps > 0:
+        result["supplied_schedules"] = time_schedules(g, w, K, args.sched_steps, stream)
     if args.cpu_sample > 0:
         result["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, K))
     print(json.dumps(result), flush=True)

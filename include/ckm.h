@@ -158,6 +158,30 @@ ckm_status ckm_round_eval_async(const ckm_graph* g, const double* d_s_frac, int6
                                 int32_t* d_best_k, uint64_t* d_best_S, uint64_t* d_best_R,
                                 int32_t* d_status, void* d_work, size_t work_bytes, void* stream);
 
+/* ---- caller-supplied schedules -----------------------------------------
+ * Evaluates K given integral checkpoint matrices S_0 .. S_{K-1} the way the
+ * rounded candidates are evaluated: R by Algorithm 2's repair (Section 5.2),
+ * memory by the U recurrence with the FREE terms (Section 4.4), cost by the
+ * objective of Section 4.3, feasibility by peak <= budget (the U <= M_budget
+ * constraint of the complete MILP, Section 4.7), and the lexicographic
+ * minimum of (cost, peak, k) over feasible k (-1 if none).
+ *
+ * S: K matrices of n bit rows; a row is ceil(n/64) uint64 words, least
+ * significant bit first: S_k[t][i] is bit i % 64 of word i / 64 of row t of
+ * matrix k (the layout of best_S). Bits on or above the diagonal (i >= t)
+ * are ignored. peak, cost, feasible: [K]. best_R (may be NULL): the chosen
+ * matrix's R rows in the same layout, zero when best_k = -1. The
+ * synchronous form takes host arrays; the asynchronous form device arrays, a
+ * work buffer sized by ckm_workspace_size(g, K) and a stream, and writes
+ * CKM_OK to d_status (may be NULL). */
+ckm_status ckm_eval_schedules(const ckm_graph* g, const uint64_t* S, int32_t K, int64_t budget,
+                              int64_t* peak, int64_t* cost, uint8_t* feasible, int32_t* best_k,
+                              uint64_t* best_R);
+ckm_status ckm_eval_schedules_async(const ckm_graph* g, const uint64_t* d_S, int32_t K, int64_t budget,
+                                    int64_t* d_peak, int64_t* d_cost, uint8_t* d_feasible,
+                                    int32_t* d_best_k, uint64_t* d_best_R, int32_t* d_status,
+                                    void* d_work, size_t work_bytes, void* stream);
+
 /* Thread-local text describing the calling thread's last non-OK status. */
 const char* ckm_last_error(void);
 

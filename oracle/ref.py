@@ -188,6 +188,31 @@ def round_eval(w, K=None, seed=None, budget=None, flags: int = 0, want_rows: boo
     return dict(peak=peak, cost=tc, feasible=feas, best_k=int(bk[0]), best_S=bS, best_R=bR)
 
 
+def eval_schedules(w, S_mats, budget: int):
+    """Given checkpoint matrices (each n x n 0/1; only the strict lower
+    triangle is used): Algorithm 2's R (Section 5.2), the U/FREE simulation
+    (Section 4.4) and cost (Section 4.3) of each, feasibility peak <= budget,
+    and the lexicographic minimum of (cost, peak, k) over feasible k (-1 if
+    none) with its R rows."""
+    peaks, costs, Rs = [], [], []
+    for S in S_mats:
+        S = np.tril(np.asarray(S, dtype=np.uint8), -1)
+        R = solve_R(w, S)
+        sim = simulate(w, S, R)
+        peaks.append(sim["peak"])
+        costs.append(sim["cost"])
+        Rs.append(R)
+    feas = [p <= budget for p in peaks]
+    best = -1
+    for k in range(len(peaks)):
+        if feas[k] and (best < 0 or (costs[k], peaks[k], k) < (costs[best], peaks[best], best)):
+            best = k
+    W = (w.n + 63) // 64
+    best_R = pack_rows(Rs[best]) if best >= 0 else np.zeros((w.n, W), np.uint64)
+    return dict(peak=np.array(peaks, np.int64), cost=np.array(costs, np.int64),
+                feasible=np.array(feas, np.uint8), best_k=best, best_R=best_R)
+
+
 def pack_rows(X) -> np.ndarray:
     """n x n 0/1 matrix -> n x W uint64 bit rows (bit i%64 of word i/64)."""
     X = np.asarray(X, dtype=np.uint8)

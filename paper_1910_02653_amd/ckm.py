@@ -24,7 +24,7 @@ MAX_CANDIDATES = 1 << 24
 EXPORTS = (
     "ckm_graph_create", "ckm_graph_destroy", "ckm_graph_num_nodes", "ckm_round_eval",
     "ckm_workspace_size", "ckm_quantize_async", "ckm_evaluate_async", "ckm_select_async",
-    "ckm_round_eval_async", "ckm_last_error",
+    "ckm_round_eval_async", "ckm_eval_schedules", "ckm_eval_schedules_async", "ckm_last_error",
 )
 
 
@@ -68,6 +68,10 @@ def lib():
         L.ckm_select_async.restype = C.c_int
         L.ckm_round_eval_async.argtypes = [p, p, i64, i32, u64, i64, u32, p, p, p, p, p, p, p, p, sz, p]
         L.ckm_round_eval_async.restype = C.c_int
+        L.ckm_eval_schedules.argtypes = [p, p, i32, i64, p, p, p, p, p]
+        L.ckm_eval_schedules.restype = C.c_int
+        L.ckm_eval_schedules_async.argtypes = [p, p, i32, i64, p, p, p, p, p, p, p, sz, p]
+        L.ckm_eval_schedules_async.restype = C.c_int
         L.ckm_last_error.argtypes = []
         L.ckm_last_error.restype = C.c_char_p
         _lib = L
@@ -155,6 +159,21 @@ class Graph:
                                     _np_ptr(bR)))
         return dict(peak=peak, cost=cost, feasible=feas, best_k=int(bk[0]), best_S=bS, best_R=bR)
 
+    def eval_schedules(self, S_rows, budget: int, want_rows: bool = True):
+        """K given checkpoint matrices as uint64 bit rows [K][n][W] (ckm_eval_schedules)."""
+        S = np.ascontiguousarray(S_rows, dtype=np.uint64)
+        if S.ndim != 3 or S.shape[1:] != (self.n, self.W):
+            raise ValueError("S_rows must have shape [K][%d][%d]" % (self.n, self.W))
+        K = S.shape[0]
+        peak = np.zeros(K, np.int64)
+        cost = np.zeros(K, np.int64)
+        feas = np.zeros(K, np.uint8)
+        bk = np.zeros(1, np.int32)
+        bR = np.zeros((self.n, self.W), np.uint64) if want_rows else None
+        _check(lib().ckm_eval_schedules(self._h, _np_ptr(S), int(K), int(budget), _np_ptr(peak), _np_ptr(cost),
+                                        _np_ptr(feas), _np_ptr(bk), _np_ptr(bR)))
+        return dict(peak=peak, cost=cost, feasible=feas, best_k=int(bk[0]), best_R=bR)
+
     # -- asynchronous, torch device tensors ---------------------------------
     def quantize_async(self, d_s_frac, work, stream=None):
         _check(lib().ckm_quantize_async(self._h, _dev_ptr(d_s_frac), d_s_frac.stride(0), _dev_ptr(work),
@@ -178,6 +197,14 @@ class Graph:
                                           _dev_ptr(out.get("best_S")), _dev_ptr(out.get("best_R")),
                                           _dev_ptr(out.get("status")), _dev_ptr(work),
                                           work.numel() * work.element_size(), _stream_ptr(stream)))
+
+    def eval_schedules_async(self, d_S, K, budget, out: dict, work, stream=None):
+        """d_S: int64 device tensor holding K x n x W bit-row words."""
+        _check(lib().ckm_eval_schedules_async(self._h, _dev_ptr(d_S), int(K), int(budget), _dev_ptr(out["peak"]),
+                                              _dev_ptr(out["cost"]), _dev_ptr(out["feasible"]),
+                                              _dev_ptr(out["best_k"]), _dev_ptr(out.get("best_R")),
+                                              _dev_ptr(out.get("status")), _dev_ptr(work),
+                                              work.numel() * work.element_size(), _stream_ptr(stream)))
 
     def alloc_outputs(self, K: int, device="cuda", rows: bool = True) -> dict:
         """Device tensors for the async calls (torch: memory only)."""

@@ -71,12 +71,15 @@ Plan plan_splits(int32_t n, int32_t splits);
 // Kernel launchers (defined in ckm_kernels.hip). They only enqueue work.
 hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,
                            char* work, hipStream_t stream);
+// s_user: K caller-supplied S matrices ([K][n][row_words] 32-bit words) to
+// evaluate instead of rounding S*; null for the rounding path.
 hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
-                           uint32_t flags, const Plan& plan, char* work, hipStream_t stream);
+                           uint32_t flags, const Plan& plan, const uint64_t* s_user, char* work,
+                           hipStream_t stream);
 hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
                          int64_t budget, uint32_t flags, int64_t* d_peak,
                          int64_t* d_cost, uint8_t* d_feasible, int32_t* d_best_k,
-                         uint64_t* d_best_S, uint64_t* d_best_R, int32_t* d_status, char* work,
-                         hipStream_t stream);
+                         uint64_t* d_best_S, uint64_t* d_best_R, int32_t* d_status,
+                         const uint64_t* s_user, char* work, hipStream_t stream);
 
 }  // namespace ckm

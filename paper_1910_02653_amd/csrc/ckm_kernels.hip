@@ -240,6 +240,8 @@ struct EvalArgs {
   cptr<int32_t> dep_idx;
   cptr<int32_t> dep_upos;
   const uint4* __restrict__ recs;
+  const uint32_t* __restrict__ s_user;  // caller-supplied S rows ([K][n][s_words]), or null: round S*
+  int32_t s_words;                      // 32-bit words per supplied row
   int64_t* __restrict__ part_peak;   // [K] running max over work items
   int64_t* __restrict__ part_cost;   // [K] running sum over work items
   int32_t* __restrict__ hdr;
@@ -322,12 +324,25 @@ __device__ __forceinline__ uint32_t umin1(uint32_t x) {
   return y;
 }
 
-// Row r of the candidate into words 0 .. r/32.
-template <typename RowT>
+// Row r of the candidate into words 0 .. r/32. kUser: the rows are the
+// caller's (a.s_user) instead of rounded from S*.
+template <bool kUser, typename RowT>
 __device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bool det_lane, RowT& dst) {
   const int nw = (r >> 5) + 1;
   if (r >= a.n) {  // S after the last stage: nothing is kept
     for (int w = 0; w < nw; ++w) dst.word(w) = 0u;
+    return;
+  }
+  if (kUser) {
+    // caller-supplied S: row r of candidate k; bits on or above the diagonal
+    // (i >= r) are cleared. Lanes past K read candidate K-1 (results unused).
+    const uint32_t kk = k < (uint32_t)a.K ? k : (uint32_t)a.K - 1u;
+    const uint32_t* src = a.s_user + ((size_t)kk * a.n + r) * a.s_words;
+    for (int w = 0; w < nw; ++w) {
+      uint32_t word = src[w];
+      if (w == nw - 1) word &= (1u << (r & 31)) - 1u;   // the diagonal's word: keep bits < r
+      dst.word(w) = word;
+    }
     return;
   }
   cptr<uint32_t> qrow = a.q + (size_t)r * a.ldq;
@@ -582,8 +597,9 @@ __device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, RowB
 // One wave per workgroup: 64 candidates over one work item (a range of
 // stages). kBReg: the S_{t+1} row lives in vector registers and is copied to
 // the LDS row at the end of each stage (n < 1024), halving the LDS a wave
-// needs; otherwise both rows are in LDS and swap roles.
-template <bool kBReg>
+// needs; otherwise both rows are in LDS and swap roles. kUser: evaluate the
+// caller's S rows instead of rounding S*.
+template <bool kBReg, bool kUser>
 __global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
   extern __shared__ uint32_t lds[];
   const int lane = threadIdx.x;
@@ -604,9 +620,9 @@ __global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
     RowReg B;
     B.w = (u32x32)0u;
     if (t0 < t1) {
-      gen_row(a, t0, k, det_lane, A);
+      gen_row<kUser>(a, t0, k, det_lane, A);
       for (int t = t0; t < t1; ++t) {
-        gen_row(a, t + 1, k, det_lane, B);
+        gen_row<kUser>(a, t + 1, k, det_lane, B);
         double sp, sc;
         eval_stage(a, t, A, B, sp, sc);
         seg_peak = fmax(seg_peak, sp);
@@ -623,9 +639,9 @@ __global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
     Row B{wave_lds + (size_t)a.row_words * 256 + 4 * lane};
     for (int w = 0; w < a.row_words; ++w) B.word(w) = 0u;
     if (t0 < t1) {
-      gen_row(a, t0, k, det_lane, A);
+      gen_row<kUser>(a, t0, k, det_lane, A);
       for (int t = t0; t < t1; ++t) {
-        gen_row(a, t + 1, k, det_lane, B);
+        gen_row<kUser>(a, t + 1, k, det_lane, B);
         double sp, sc;
         eval_stage(a, t, A, B, sp, sc);
         seg_peak = fmax(seg_peak, sp);
@@ -791,12 +807,17 @@ __global__ void __launch_bounds__(kWave) ckm_best_closure_kernel(int32_t n, int3
                                                                  const int32_t* __restrict__ user_ptr,
                                                                  const int32_t* __restrict__ user_idx,
                                                                  const int32_t* __restrict__ best_k,
-                                                                 const uint32_t* __restrict__ S_rows,
+                                                                 const uint32_t* __restrict__ S_base,
+                                                                 size_t cand_stride,
                                                                  uint32_t* __restrict__ R_rows) {
   const int t = blockIdx.x * kWave + threadIdx.x;
   const bool active = t < n;
   const int tmax = min(n - 1, (int)blockIdx.x * kWave + kWave - 1);
   const int bk = best_k[0];
+  // the best candidate's S rows: cand_stride = 0 for rows regenerated into
+  // S_base, n * row_words for caller-supplied rows (bits on or above the
+  // diagonal are never read below)
+  const uint32_t* S_rows = S_base + (bk >= 0 ? (size_t)bk * cand_stride : 0);
   uint32_t* Rrow = R_rows + (size_t)(active ? t : 0) * row_words;
   const uint32_t* S0 = S_rows + (size_t)(active ? t : 0) * row_words;
   const uint32_t* S1 = S_rows + (size_t)((active && t + 1 < n) ? t + 1 : 0) * row_words;
@@ -849,10 +870,13 @@ hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_
 }
 
 hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
-                           uint32_t flags, const Plan& plan, char* work, hipStream_t stream) {
+                           uint32_t flags, const Plan& plan, const uint64_t* s_user, char* work,
+                           hipStream_t stream) {
   EvalArgs a;
   a.n = g.n;
   a.K = K;
+  a.s_user = reinterpret_cast<const uint32_t*>(s_user);
+  a.s_words = L.row_words;
   a.items = plan.items;
   a.kind = plan.kind;
   a.P = plan.P;
@@ -881,32 +905,41 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   const int groups = (K + kWave - 1) / kWave;
   const bool breg = a.row_words <= kRegRowWords;
   const size_t lds_bytes = (breg ? 1u : 2u) * (size_t)a.row_words * kWave * sizeof(uint32_t);
-  const void* fn = breg ? (const void*)ckm_eval_kernel<true> : (const void*)ckm_eval_kernel<false>;
+  void (*fn)(EvalArgs);
+  if (s_user)
+    fn = breg ? ckm_eval_kernel<true, true> : ckm_eval_kernel<false, true>;
+  else
+    fn = breg ? ckm_eval_kernel<true, false> : ckm_eval_kernel<false, false>;
   if (lds_bytes > 65536) {
-    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+    hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(ckm_eval_init_kernel, dim3((K + 255) / 256), dim3(256), 0, stream, K, a.part_peak,
                      a.part_cost);
-  if (breg)
-    hipLaunchKernelGGL(ckm_eval_kernel<true>, dim3(groups, plan.items), dim3(kWave), lds_bytes, stream, a);
-  else
-    hipLaunchKernelGGL(ckm_eval_kernel<false>, dim3(groups, plan.items), dim3(kWave), lds_bytes, stream, a);
+  hipLaunchKernelGGL(fn, dim3(groups, plan.items), dim3(kWave), lds_bytes, stream, a);
   return hipGetLastError();
 }
 
 hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
                          int64_t budget, uint32_t flags, int64_t* d_peak, int64_t* d_cost,
                          uint8_t* d_feasible, int32_t* d_best_k, uint64_t* d_best_S,
-                         uint64_t* d_best_R, int32_t* d_status, char* work, hipStream_t stream) {
+                         uint64_t* d_best_R, int32_t* d_status, const uint64_t* s_user, char* work,
+                         hipStream_t stream) {
   const int rb = L.reduce_blocks;
   hipLaunchKernelGGL(ckm_reduce_kernel, dim3(rb), dim3(256), 0, stream, K,
                      at<const int64_t>(work, L.part_peak_off), at<const int64_t>(work, L.part_cost_off),
                      budget, d_peak, d_cost, d_feasible, at<Best>(work, L.best_off));
+  // rounded candidates: S* NaN flags from the quantize stage; supplied S: none
   hipLaunchKernelGGL(ckm_argmin_kernel, dim3(1), dim3(256), 0, stream, rb,
-                     at<const Best>(work, L.best_off), g.n, at<const int32_t>(work, L.nan_off),
+                     at<const Best>(work, L.best_off), s_user ? 0 : g.n, at<const int32_t>(work, L.nan_off),
                      d_best_k, d_status);
-  if (d_best_S || d_best_R) {
+  if (s_user) {
+    if (d_best_R)
+      hipLaunchKernelGGL(ckm_best_closure_kernel, dim3((g.n + kWave - 1) / kWave), dim3(kWave), 0, stream,
+                         g.n, L.row_words, g.d_user_ptr, g.d_user_idx, d_best_k,
+                         reinterpret_cast<const uint32_t*>(s_user), (size_t)g.n * L.row_words,
+                         reinterpret_cast<uint32_t*>(d_best_R));
+  } else if (d_best_S || d_best_R) {
     uint32_t* srows = d_best_S ? reinterpret_cast<uint32_t*>(d_best_S) : at<uint32_t>(work, L.srows_off);
     dim3 grid((L.row_words + 255) / 256, g.n);
     hipLaunchKernelGGL(ckm_best_rows_kernel, grid, dim3(256), 0, stream,
@@ -915,8 +948,8 @@ hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_
                        (uint32_t)(seed >> 32), (flags & CKM_F_DET0) ? 1u : 0u, d_best_k, srows);
     if (d_best_R) {
       hipLaunchKernelGGL(ckm_best_closure_kernel, dim3((g.n + kWave - 1) / kWave), dim3(kWave), 0,
-                         stream, g.n, L.row_words, g.d_user_ptr, g.d_user_idx, d_best_k, srows,
-                         reinterpret_cast<uint32_t*>(d_best_R));
+                         stream, g.n, L.row_words, g.d_user_ptr, g.d_user_idx, d_best_k,
+                         static_cast<const uint32_t*>(srows), (size_t)0, reinterpret_cast<uint32_t*>(d_best_R));
     }
   }
   return hipGetLastError();

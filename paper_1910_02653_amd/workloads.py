@@ -362,3 +362,51 @@ def random_dag(n: int, seed: int, max_deg: int = 3, window: int = 8, max_size: i
                     K=K, seed=seed,
                     budget=checkpoint_all_budget(size, m_input, m_param, budget_pct),
                     budget_pct=budget_pct)
+
+
+# ---------------------------------------------------------------------------
+# supplied checkpoint matrices (integral S) for batch evaluation
+# ---------------------------------------------------------------------------
+
+def random_schedules(n: int, K: int, seed: int, density: float = 0.3, kind: str = "bernoulli",
+                     junk: bool = True) -> np.ndarray:
+    """K checkpoint matrices as bit rows [K][n][ceil(n/64)] uint64 (bit i % 64
+    of word i / 64 of row t is S[t][i]).
+
+    kind "bernoulli": each strict-lower entry is 1 with probability density.
+    kind "intervals": each value i is kept with probability density, from
+    stage i + 1 up to a uniformly drawn last stage (the banded shape of
+    checkpoint schedules, where a stored value stays resident for a while).
+    junk: also set random bits on and above the diagonal and in the padding
+    past node n - 1; the evaluation must ignore them."""
+    rng = np.random.default_rng(seed)
+    W = (n + 63) // 64
+    out = np.zeros((K, n, W), np.uint64)
+    tri = np.tri(n, W * 64, -1, dtype=bool)
+    for k in range(K):
+        if kind == "bernoulli":
+            bits = rng.random((n, W * 64)) < density
+        elif kind == "intervals":
+            keep = rng.random(n) < density
+            first = np.arange(1, n + 1)
+            end = first + np.floor(rng.random(n) * (n + 1 - first)).astype(np.int64)
+            t = np.arange(n)[:, None]
+            i = np.arange(W * 64)[None, :]
+            i_c = np.minimum(i, n - 1)
+            bits = (i < n) & keep[i_c] & (t > i) & (t < end[i_c])
+        else:
+            raise ValueError(kind)
+        bits = bits & tri
+        if junk:
+            bits = bits | ((rng.random((n, W * 64)) < 0.5) & ~tri)
+        packed = np.packbits(bits.astype(np.uint8).reshape(n, W, 64), axis=2, bitorder="little")
+        out[k] = packed.view(np.uint64).reshape(n, W)
+    return out
+
+
+def unpack_schedules(rows: np.ndarray, n: int) -> np.ndarray:
+    """[K][n][W] uint64 bit rows -> [K][n][n] uint8 0/1 (the inverse layout)."""
+    rows = np.ascontiguousarray(rows, np.uint64)
+    K = rows.shape[0]
+    bits = np.unpackbits(rows.view(np.uint8).reshape(K, n, -1), axis=2, bitorder="little")
+    return bits[:, :, :n].copy()

@@ -399,6 +399,44 @@ def test_round_eval_none_feasible_and_det0():
     assert np.array_equal(r2["peak"][1:], r3["peak"][1:])
 
 
+def test_eval_schedules_closed_forms_and_argmin():
+    """Supplied schedules: checkpoint-all gives cost sum C and peak
+    M_in + 2 M_param + sum M (R = I, Section 5.2); the all-zero S of a chain
+    gives the quadratic recompute cost of Section 4.2; anything on or above
+    the diagonal is ignored; the argmin is over feasible (cost, peak, k)."""
+    w = wl.random_dag(23, 2, m_input=5, m_param=3)
+    n = w.n
+    full = np.tril(np.ones((n, n), np.uint8), -1)
+    junk = np.triu(np.ones((n, n), np.uint8))
+    zero = np.zeros((n, n), np.uint8)
+    r = ref.eval_schedules(w, [zero, full | junk, full], budget=2 ** 62)
+    assert int(r["cost"][1]) == int(w.cost.sum()) == int(r["cost"][2])
+    assert int(r["peak"][1]) == 5 + 2 * 3 + int(w.size.sum()) == int(r["peak"][2])
+    assert r["cost"][0] >= r["cost"][1]
+    # equal (cost, peak): the lower index wins; the zero schedule wins on
+    # peak only if it also has the least cost
+    cands = sorted((int(r["cost"][k]), int(r["peak"][k]), k) for k in range(3))
+    assert r["best_k"] == cands[0][2]
+    assert r["best_k"] in (0, 1)
+    assert np.array_equal(r["best_R"], ref.pack_rows(ref.solve_R(w, [zero, full, full][r["best_k"]])))
+    # a budget below every peak: nothing feasible, R rows all zero
+    low = int(r["peak"].min()) - 1
+    r2 = ref.eval_schedules(w, [zero, full], budget=low)
+    assert r2["best_k"] == -1 and not r2["feasible"].any() and not r2["best_R"].any()
+
+
+def test_eval_schedules_agrees_with_rounding_path():
+    """The rounded S of each candidate, fed back as a supplied schedule, must
+    give that candidate's peak and cost, and the same argmin."""
+    w = wl.random_dag(30, 5, K=12, budget_pct=70.0)
+    Ss = [ref.eval_candidate(w, k, want_rows=True)[2] for k in range(w.K)]
+    r = ref.eval_schedules(w, Ss, w.budget)
+    e = ref.round_eval(w)
+    assert np.array_equal(r["peak"], e["peak"]) and np.array_equal(r["cost"], e["cost"])
+    assert np.array_equal(r["feasible"], e["feasible"]) and r["best_k"] == e["best_k"]
+    assert np.array_equal(r["best_R"], e["best_R"])
+
+
 def test_validate_graph_errors():
     n = 3
     ok = ref.validate_graph(n, [0, 0, 1, 3], [0, 0, 1], [1, 1, 1], [1, 1, 1], 0, 0)
