@@ -139,6 +139,29 @@ void ckm_ref_round_det(int32_t n, const double* s_frac, int64_t ld, uint8_t* S) 
       S[(int64_t)t * n + i] = (i < t) && (s_frac[(int64_t)t * ld + i] > 0.5);
 }
 
+/* Deterministic rounding at a chosen threshold p (Section 5.1 rounds
+ * x_int = 1[x* >= p]; Algorithm 2 takes p = 0.5 with a strict comparison, the
+ * form used here): S[t][i] = [clamp(S*[t][i], 0, 1) > p] for i < t, compared
+ * in double. A NaN entry of the strict lower triangle, or a NaN p, is an
+ * argument error. */
+int ckm_ref_round_threshold(int32_t n, const double* s_frac, int64_t ld, double p, uint8_t* S) {
+  int32_t t, i;
+  if (isnan(p)) return CKM_REF_E_INVALID_ARG;
+  for (t = 0; t < n; ++t)
+    for (i = 0; i < n; ++i) {
+      uint8_t v = 0;
+      if (i < t) {
+        double x = s_frac[(int64_t)t * ld + i];
+        if (isnan(x)) return CKM_REF_E_INVALID_ARG;
+        if (x < 0.0) x = 0.0;
+        if (x > 1.0) x = 1.0;
+        v = x > p;
+      }
+      S[(int64_t)t * n + i] = v;
+    }
+  return CKM_REF_OK;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Algorithm 2 (two-phase rounding), given S_int:
  *   R <- I (constraint 4a: node t is computed in stage t);

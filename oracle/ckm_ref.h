@@ -66,6 +66,11 @@ void ckm_ref_round_random(int32_t n, const uint32_t* q, uint64_t seed, uint32_t 
 /* Deterministic rounding of Algorithm 2: S[t][i] = [S*[t][i] > 0.5]. */
 void ckm_ref_round_det(int32_t n, const double* s_frac, int64_t ld, uint8_t* S);
 
+/* Deterministic rounding at threshold p: S[t][i] = [clamp(S*[t][i], 0, 1) > p]
+ * for i < t (Section 5.1 with the strict comparison of Algorithm 2). Returns
+ * CKM_REF_E_INVALID_ARG for a NaN p or a NaN S* entry with i < t. */
+int ckm_ref_round_threshold(int32_t n, const double* s_frac, int64_t ld, double p, uint8_t* S);
+
 /* Algorithm 2, phase two: R = I, then repair constraint (1c) and then (1b)
  * until neither is violated. */
 void ckm_ref_solve_R(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,

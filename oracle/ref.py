@@ -51,6 +51,8 @@ def lib():
         L.ckm_ref_round_random.restype = None
         L.ckm_ref_round_det.argtypes = [C.c_int32, p, C.c_int64, p]
         L.ckm_ref_round_det.restype = None
+        L.ckm_ref_round_threshold.argtypes = [C.c_int32, p, C.c_int64, C.c_double, p]
+        L.ckm_ref_round_threshold.restype = C.c_int
         L.ckm_ref_solve_R.argtypes = [C.c_int32, p, p, p, p]
         L.ckm_ref_solve_R.restype = None
         L.ckm_ref_simulate.argtypes = [C.c_int32, p, p, p, p, C.c_int64, C.c_int64, p, p, p, p, p, p, p]
@@ -164,6 +166,29 @@ def eval_candidate(w, k: int, flags: int = 0, q=None, want_rows: bool = False):
     if want_rows:
         return int(peak[0]), int(tc[0]), S, R
     return int(peak[0]), int(tc[0])
+
+
+def round_threshold(s_frac, p: float):
+    """S[t][i] = [clamp(S*[t][i], 0, 1) > p] for i < t (Section 5.1 at threshold p)."""
+    s = np.ascontiguousarray(s_frac, dtype=np.float64)
+    n = s.shape[0]
+    S = np.zeros((n, n), dtype=np.uint8)
+    st = lib().ckm_ref_round_threshold(n, _ptr(s), s.shape[1], float(p), _ptr(S))
+    if st != OK:
+        raise ValueError("round_threshold: status %d" % st)
+    return S
+
+
+def threshold_eval(w, p, budget=None):
+    """One candidate per threshold p_k: deterministic rounding at p_k, then
+    Algorithm 2, the simulation and the feasible argmin, as for supplied
+    schedules. Adds the best candidate's S rows."""
+    budget = w.budget if budget is None else budget
+    Ss = [round_threshold(w.s_frac, pk) for pk in np.asarray(p, np.float64)]
+    r = eval_schedules(w, Ss, budget)
+    W = (w.n + 63) // 64
+    r["best_S"] = pack_rows(Ss[r["best_k"]]) if r["best_k"] >= 0 else np.zeros((w.n, W), np.uint64)
+    return r
 
 
 def round_eval(w, K=None, seed=None, budget=None, flags: int = 0, want_rows: bool = True):

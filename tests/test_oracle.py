@@ -437,6 +437,62 @@ def test_eval_schedules_agrees_with_rounding_path():
     assert np.array_equal(r["best_R"], e["best_R"])
 
 
+def test_threshold_rounding_values():
+    """S = [clamp(S*, 0, 1) > p] below the diagonal, worked by hand: the
+    comparison is strict, values are clamped to [0, 1] first, and nothing on
+    or above the diagonal is read."""
+    s = np.array([[9.0, 9.0, 9.0, 9.0],
+                  [0.5, 9.0, 9.0, 9.0],
+                  [1.5, -0.3, 9.0, 9.0],
+                  [0.25, 0.75, 1.0, np.nan]])
+    assert ref.round_threshold(s, 0.5).tolist() == [[0, 0, 0, 0], [0, 0, 0, 0], [1, 0, 0, 0], [0, 1, 1, 0]]
+    assert ref.round_threshold(s, 0.25).tolist() == [[0, 0, 0, 0], [1, 0, 0, 0], [1, 0, 0, 0], [0, 1, 1, 0]]
+    assert ref.round_threshold(s, -0.5).tolist() == [[0, 0, 0, 0], [1, 0, 0, 0], [1, 1, 0, 0], [1, 1, 1, 0]]
+    assert not ref.round_threshold(s, 1.0).any()          # clamped 1.5 and 1.0 are not > 1
+    assert ref.round_threshold(s, 0.9999).tolist()[2][0] == 1
+    with pytest.raises(ValueError):
+        ref.round_threshold(s, float("nan"))
+    bad = s.copy()
+    bad[3, 1] = np.nan
+    with pytest.raises(ValueError):
+        ref.round_threshold(bad, 0.5)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_threshold_rounding_half_is_algorithm2_and_monotone(seed):
+    """p = 0.5 is Algorithm 2's deterministic rounding; S shrinks as p grows."""
+    rng = np.random.default_rng(seed)
+    n = 40
+    s = wl.lower_triangle(n, rng.random(n * (n - 1) // 2))
+    assert np.array_equal(ref.round_threshold(s, 0.5), ref.round_det(s))
+    prev = None
+    for p in np.sort(rng.random(12)):
+        S = ref.round_threshold(s, p)
+        if prev is not None:
+            assert np.all(S <= prev)
+        prev = S
+
+
+def test_threshold_eval_closed_forms():
+    """p < 0 keeps every value (the checkpoint-all closed form); p >= 1 keeps
+    none, which on a pure chain gives the quadratic recompute cost."""
+    w = wl.random_dag(23, 4, m_input=5, m_param=3)
+    r = ref.threshold_eval(w, [-1.0, 0.5, 1.0], budget=2 ** 62)
+    assert int(r["cost"][0]) == int(w.cost.sum())
+    assert int(r["peak"][0]) == 5 + 2 * 3 + int(w.size.sum())
+    assert r["best_k"] == 0
+    assert np.array_equal(r["best_S"], ref.pack_rows(np.tri(w.n, w.n, -1, dtype=np.uint8)))
+    assert np.array_equal(r["best_R"], ref.pack_rows(np.eye(w.n, dtype=np.uint8)))
+    n = 12
+    ptr, idx = wl.csr_from_deps([[]] + [[v - 1] for v in range(1, n)])
+    cost = np.arange(1, n + 1, dtype=np.int64)
+    chain = wl.Workload("chain", n, ptr, idx, cost, np.ones(n, np.int64), 1, 1,
+                        wl.s_frac_uniform(n, 3), 1, 0, 0)
+    r = ref.threshold_eval(chain, [1.0, 2.0], budget=0)
+    assert r["best_k"] == -1 and not r["best_S"].any()
+    assert int(r["cost"][0]) == sum(int(cost[: t + 1].sum()) for t in range(n)) == int(r["cost"][1])
+
+
 def test_validate_graph_errors():
     n = 3
     ok = ref.validate_graph(n, [0, 0, 1, 3], [0, 0, 1], [1, 1, 1], [1, 1, 1], 0, 0)
