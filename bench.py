@@ -14,6 +14,9 @@ written once and read once: 4 * n * ceil(n/64) * 8 bytes per candidate.
 workload. `supplied_schedules` times the batch evaluation of K given integral
 checkpoint matrices (banded, 30 % of values kept) on the same graph: Algorithm
 2 repair, simulation, argmin and the best R, with the matrices resident in HBM.
+`threshold_family` times K deterministic candidates [clamp(S*) > p_k] on an
+even threshold grid over [0, 1] for the same graph and S*: keys, evaluation,
+argmin and the best S and R.
 """
 from __future__ import annotations
 
@@ -94,6 +97,32 @@ def time_schedules(g, w, K, steps, stream):
                      "%.1f MB of bit rows in HBM" % (K, rows.nbytes / 1e6)}
 
 
+def time_thresholds(g, w, K, steps, stream, d_s):
+    """Throughput of ckm_threshold_eval_async on an even grid of K thresholds."""
+    import numpy as np
+    import torch
+
+    from paper_1910_02653_amd import ckm
+
+    d_p = torch.from_numpy(np.linspace(0.0, 1.0, K)).cuda()
+    work = g.alloc_work(K)
+    out = g.alloc_outputs(K)
+    for _ in range(3):
+        g.threshold_eval_async(d_s, d_p, w.budget, out, work, stream)
+    torch.cuda.synchronize()
+    assert int(out["status"].item()) == ckm.OK
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(steps):
+        g.threshold_eval_async(d_s, d_p, w.budget, out, work, stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    return {"value": K / (ms * 1e-3), "unit": "candidates/s", "ms_per_call": ms, "steps": steps,
+            "input": "K=%d thresholds evenly spaced over [0, 1] on the workload's S*" % K}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -104,6 +133,8 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=256, help="oracle candidates to time (0 = skip)")
     ap.add_argument("--sched-steps", type=int, default=20,
                     help="timed calls of the supplied-schedule evaluation (0 = skip)")
+    ap.add_argument("--thr-steps", type=int, default=20,
+                    help="timed calls of the threshold-family evaluation (0 = skip)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -185,6 +216,8 @@ def main():
     }
     if args.sched_steps > 0:
         result["supplied_schedules"] = time_schedules(g, w, K, args.sched_steps, stream)
+    if args.thr_steps > 0:
+        result["threshold_family"] = time_thresholds(g, w, K, args.thr_steps, stream, d_s)
     if args.cpu_sample > 0:
         result["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, K))
     print(json.dumps(result), flush=True)

@@ -54,7 +54,7 @@ typedef enum {
   CKM_E_INVALID_ARG = 1, /* bad argument: NULL, K < 1, ld < n, negative budget, NaN in S* */
   CKM_E_GRAPH = 2,       /* not topologically numbered, duplicate edge, users != transpose */
   CKM_E_OVERFLOW = 3,    /* sizes or costs outside the exact-arithmetic range */
-  CKM_E_UNSUPPORTED = 4, /* n > CKM_MAX_NODES or K > CKM_MAX_CANDIDATES */
+  CKM_E_UNSUPPORTED = 4, /* n > CKM_MAX_NODES, K > CKM_MAX_CANDIDATES (CKM_MAX_THRESHOLDS) */
   CKM_E_NOMEM = 5,       /* host or device allocation failed */
   CKM_E_DEVICE = 6       /* a HIP runtime call failed (message has the HIP error) */
 } ckm_status;
@@ -63,6 +63,7 @@ enum { CKM_F_DET0 = 1u }; /* candidate 0 = deterministic rounding S* > 0.5 (Algo
 
 #define CKM_MAX_NODES 4096
 #define CKM_MAX_CANDIDATES (1 << 24)
+#define CKM_MAX_THRESHOLDS (1 << 16) /* candidates of the threshold family */
 
 /* Build a graph (Section 4.1: a DAG numbered in topological order, node v
  * with output size M_v = bytes[v] and cost C_v = cost[v]) and upload it to
@@ -181,6 +182,30 @@ ckm_status ckm_eval_schedules_async(const ckm_graph* g, const uint64_t* d_S, int
                                     int64_t* d_peak, int64_t* d_cost, uint8_t* d_feasible,
                                     int32_t* d_best_k, uint64_t* d_best_R, int32_t* d_status,
                                     void* d_work, size_t work_bytes, void* stream);
+
+/* ---- threshold family --------------------------------------------------
+ * One deterministic candidate per threshold: S_k[t][i] = [clamp(S*[t][i], 0,
+ * 1) > p_k] for i < t, compared in double (Section 5.1's deterministic
+ * rounding at a chosen threshold; Algorithm 2's is p = 0.5 with the strict
+ * comparison used here). The candidates are then evaluated as the rounded
+ * ones: Algorithm 2's R repair (Section 5.2), memory and cost (Sections 4.4
+ * and 4.3), feasibility and the lexicographic argmin of (cost, peak, k).
+ *
+ * s_frac, ld: as for ckm_round_eval. p: float64 [K] thresholds, any order,
+ * duplicates allowed (each is its own candidate). K: 1..CKM_MAX_THRESHOLDS.
+ * A NaN threshold or a NaN in the strict lower triangle of S* gives
+ * CKM_E_INVALID_ARG (the asynchronous form reports it through d_status).
+ * Outputs as for ckm_round_eval; best_S and best_R may be NULL. The
+ * asynchronous form takes device arrays, a work buffer sized by
+ * ckm_workspace_size(g, K) and a stream. */
+ckm_status ckm_threshold_eval(const ckm_graph* g, const double* s_frac, int64_t ld, const double* p,
+                              int32_t K, int64_t budget, int64_t* peak, int64_t* cost, uint8_t* feasible,
+                              int32_t* best_k, uint64_t* best_S, uint64_t* best_R);
+ckm_status ckm_threshold_eval_async(const ckm_graph* g, const double* d_s_frac, int64_t ld, const double* d_p,
+                                   int32_t K, int64_t budget, int64_t* d_peak, int64_t* d_cost,
+                                   uint8_t* d_feasible, int32_t* d_best_k, uint64_t* d_best_S,
+                                   uint64_t* d_best_R, int32_t* d_status, void* d_work, size_t work_bytes,
+                                   void* stream);
 
 /* Thread-local text describing the calling thread's last non-OK status. */
 const char* ckm_last_error(void);

@@ -19,12 +19,14 @@ OK, E_INVALID_ARG, E_GRAPH, E_OVERFLOW, E_UNSUPPORTED, E_NOMEM, E_DEVICE = range
 F_DET0 = 1
 MAX_NODES = 4096
 MAX_CANDIDATES = 1 << 24
+MAX_THRESHOLDS = 1 << 16
 
 # every extern "C" symbol declared in include/ckm.h
 EXPORTS = (
     "ckm_graph_create", "ckm_graph_destroy", "ckm_graph_num_nodes", "ckm_round_eval",
     "ckm_workspace_size", "ckm_quantize_async", "ckm_evaluate_async", "ckm_select_async",
-    "ckm_round_eval_async", "ckm_eval_schedules", "ckm_eval_schedules_async", "ckm_last_error",
+    "ckm_round_eval_async", "ckm_eval_schedules", "ckm_eval_schedules_async", "ckm_threshold_eval",
+    "ckm_threshold_eval_async", "ckm_last_error",
 )
 
 
@@ -72,6 +74,10 @@ def lib():
         L.ckm_eval_schedules.restype = C.c_int
         L.ckm_eval_schedules_async.argtypes = [p, p, i32, i64, p, p, p, p, p, p, p, sz, p]
         L.ckm_eval_schedules_async.restype = C.c_int
+        L.ckm_threshold_eval.argtypes = [p, p, i64, p, i32, i64, p, p, p, p, p, p]
+        L.ckm_threshold_eval.restype = C.c_int
+        L.ckm_threshold_eval_async.argtypes = [p, p, i64, p, i32, i64, p, p, p, p, p, p, p, p, sz, p]
+        L.ckm_threshold_eval_async.restype = C.c_int
         L.ckm_last_error.argtypes = []
         L.ckm_last_error.restype = C.c_char_p
         _lib = L
@@ -159,6 +165,22 @@ class Graph:
                                     _np_ptr(bR)))
         return dict(peak=peak, cost=cost, feasible=feas, best_k=int(bk[0]), best_S=bS, best_R=bR)
 
+    def threshold_eval(self, s_frac, p, budget: int, want_rows: bool = True):
+        """One deterministic candidate per threshold p_k (ckm_threshold_eval)."""
+        s = np.ascontiguousarray(s_frac, dtype=np.float64)
+        pk = np.ascontiguousarray(p, dtype=np.float64).reshape(-1)
+        K = pk.size
+        peak = np.zeros(K, np.int64)
+        cost = np.zeros(K, np.int64)
+        feas = np.zeros(K, np.uint8)
+        bk = np.zeros(1, np.int32)
+        bS = np.zeros((self.n, self.W), np.uint64) if want_rows else None
+        bR = np.zeros((self.n, self.W), np.uint64) if want_rows else None
+        _check(lib().ckm_threshold_eval(self._h, _np_ptr(s), s.shape[1], _np_ptr(pk), int(K), int(budget),
+                                        _np_ptr(peak), _np_ptr(cost), _np_ptr(feas), _np_ptr(bk), _np_ptr(bS),
+                                        _np_ptr(bR)))
+        return dict(peak=peak, cost=cost, feasible=feas, best_k=int(bk[0]), best_S=bS, best_R=bR)
+
     def eval_schedules(self, S_rows, budget: int, want_rows: bool = True):
         """K given checkpoint matrices as uint64 bit rows [K][n][W] (ckm_eval_schedules)."""
         S = np.ascontiguousarray(S_rows, dtype=np.uint64)
@@ -205,6 +227,16 @@ class Graph:
                                               _dev_ptr(out["best_k"]), _dev_ptr(out.get("best_R")),
                                               _dev_ptr(out.get("status")), _dev_ptr(work),
                                               work.numel() * work.element_size(), _stream_ptr(stream)))
+
+    def threshold_eval_async(self, d_s_frac, d_p, budget, out: dict, work, stream=None):
+        """d_p: float64 device tensor of K thresholds."""
+        _check(lib().ckm_threshold_eval_async(self._h, _dev_ptr(d_s_frac), d_s_frac.stride(0), _dev_ptr(d_p),
+                                              int(d_p.numel()), int(budget), _dev_ptr(out["peak"]),
+                                              _dev_ptr(out["cost"]), _dev_ptr(out["feasible"]),
+                                              _dev_ptr(out["best_k"]), _dev_ptr(out.get("best_S")),
+                                              _dev_ptr(out.get("best_R")), _dev_ptr(out.get("status")),
+                                              _dev_ptr(work), work.numel() * work.element_size(),
+                                              _stream_ptr(stream)))
 
     def alloc_outputs(self, K: int, device="cuda", rows: bool = True) -> dict:
         """Device tensors for the async calls (torch: memory only)."""

@@ -117,6 +117,10 @@ Layout make_layout(int32_t n, int32_t K) {
   L.part_cost_off = off; off = align256(off + (size_t)K * sizeof(int64_t));
   L.best_off = off;      off = align256(off + (size_t)L.reduce_blocks * 24);
   L.srows_off = off;     off = align256(off + (size_t)n * L.row_words * sizeof(uint32_t));
+  // threshold family: sorted thresholds and per-candidate ranks
+  const size_t kt = (size_t)std::min<int32_t>(K, CKM_MAX_THRESHOLDS);
+  L.thr_sorted_off = off; off = align256(off + kt * sizeof(double));
+  L.thr_rank_off = off;   off = align256(off + kt * sizeof(uint32_t));
   L.total = off;
   return L;
 }
@@ -330,8 +334,8 @@ ckm_status ckm_evaluate_async(const ckm_graph* g, int32_t K, uint64_t seed, uint
   const ckm::Plan plan = stage_splits ? ckm::plan_splits(g->n, std::min(stage_splits, L.max_splits))
                                       : ckm::plan_auto(g->n, K, L.max_splits);
   DeviceGuard dg(g->device);
-  hipError_t e = ckm::launch_evaluate(*g, L, K, seed, flags, plan, nullptr, static_cast<char*>(d_work),
-                                      static_cast<hipStream_t>(stream));
+  hipError_t e = ckm::launch_evaluate(*g, L, K, seed, flags, plan, ckm::kSrcRound, nullptr,
+                                      static_cast<char*>(d_work), static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CKM_OK : fail_hip(e, "evaluate launch");
 }
 
@@ -348,7 +352,7 @@ ckm_status ckm_select_async(const ckm_graph* g, int32_t K, uint64_t seed, int64_
     return fail(CKM_E_INVALID_ARG, "NULL peak, cost, feasible or best_k");
   DeviceGuard dg(g->device);
   hipError_t e = ckm::launch_select(*g, L, K, seed, budget, flags, d_peak, d_cost, d_feasible,
-                                    d_best_k, d_best_S, d_best_R, d_status, nullptr,
+                                    d_best_k, d_best_S, d_best_R, d_status, ckm::kSrcRound, nullptr,
                                     static_cast<char*>(d_work), static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CKM_OK : fail_hip(e, "select launch");
 }
@@ -386,11 +390,12 @@ ckm_status ckm_eval_schedules_async(const ckm_graph* g, const uint64_t* d_S, int
     return fail(CKM_E_INVALID_ARG, "NULL peak, cost, feasible or best_k");
   const ckm::Plan plan = ckm::plan_auto(g->n, K, L.max_splits);
   DeviceGuard dg(g->device);
-  hipError_t e = ckm::launch_evaluate(*g, L, K, 0, 0, plan, d_S, static_cast<char*>(d_work),
+  hipError_t e = ckm::launch_evaluate(*g, L, K, 0, 0, plan, ckm::kSrcUser, d_S, static_cast<char*>(d_work),
                                       static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail_hip(e, "evaluate launch");
   e = ckm::launch_select(*g, L, K, 0, budget, 0, d_peak, d_cost, d_feasible, d_best_k, nullptr, d_best_R,
-                         d_status, d_S, static_cast<char*>(d_work), static_cast<hipStream_t>(stream));
+                         d_status, ckm::kSrcUser, d_S, static_cast<char*>(d_work),
+                         static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CKM_OK : fail_hip(e, "select launch");
 }
 
@@ -442,6 +447,114 @@ ckm_status ckm_eval_schedules(const ckm_graph* g, const uint64_t* S, int32_t K, 
     struct Copy { void* dst; size_t off, bytes; } copies[] = {
         {peak, o_peak, (size_t)K * 8}, {cost, o_cost, (size_t)K * 8}, {feasible, o_feas, (size_t)K},
         {best_k, o_bk, 4}, {best_R, o_bR, rows_bytes}};
+    for (const Copy& c : copies) {
+      if (!c.dst) continue;
+      if ((e = hipMemcpyAsync(c.dst, d + c.off, c.bytes, hipMemcpyDeviceToHost, stream)) != hipSuccess) {
+        st = fail_hip(e, "hipMemcpy results");
+        break;
+      }
+    }
+    if (st != CKM_OK) break;
+    if ((e = hipStreamSynchronize(stream)) != hipSuccess) st = fail_hip(e, "hipStreamSynchronize");
+  } while (false);
+  if (stream) {
+    (void)hipStreamSynchronize(stream);
+    (void)hipStreamDestroy(stream);
+  }
+  (void)hipFree(d);
+  return st;
+}
+
+ckm_status ckm_threshold_eval_async(const ckm_graph* g, const double* d_s_frac, int64_t ld, const double* d_p,
+                                   int32_t K, int64_t budget, int64_t* d_peak, int64_t* d_cost,
+                                   uint8_t* d_feasible, int32_t* d_best_k, uint64_t* d_best_S,
+                                   uint64_t* d_best_R, int32_t* d_status, void* d_work, size_t work_bytes,
+                                   void* stream) {
+  Layout L;
+  ckm_status st = check_work(g, K, d_work, work_bytes, &L);
+  if (st != CKM_OK) return st;
+  if (K > CKM_MAX_THRESHOLDS) return fail(CKM_E_UNSUPPORTED, "K = %d > %d thresholds", K, CKM_MAX_THRESHOLDS);
+  if (!d_s_frac || !d_p) return fail(CKM_E_INVALID_ARG, "NULL S* or thresholds");
+  if (ld < g->n) return fail(CKM_E_INVALID_ARG, "ld = %lld < n = %d", (long long)ld, g->n);
+  if (budget < 0) return fail(CKM_E_INVALID_ARG, "budget = %lld < 0", (long long)budget);
+  if (!d_peak || !d_cost || !d_feasible || !d_best_k)
+    return fail(CKM_E_INVALID_ARG, "NULL peak, cost, feasible or best_k");
+  const ckm::Plan plan = ckm::plan_auto(g->n, K, L.max_splits);
+  DeviceGuard dg(g->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* work = static_cast<char*>(d_work);
+  hipError_t e = ckm::launch_threshold_keys(*g, L, d_s_frac, ld, d_p, K, work, s);
+  if (e != hipSuccess) return fail_hip(e, "threshold key launch");
+  e = ckm::launch_evaluate(*g, L, K, 0, 0, plan, ckm::kSrcThreshold, nullptr, work, s);
+  if (e != hipSuccess) return fail_hip(e, "evaluate launch");
+  e = ckm::launch_select(*g, L, K, 0, budget, 0, d_peak, d_cost, d_feasible, d_best_k, d_best_S, d_best_R,
+                         d_status, ckm::kSrcThreshold, nullptr, work, s);
+  return e == hipSuccess ? CKM_OK : fail_hip(e, "select launch");
+}
+
+ckm_status ckm_threshold_eval(const ckm_graph* g, const double* s_frac, int64_t ld, const double* p,
+                              int32_t K, int64_t budget, int64_t* peak, int64_t* cost, uint8_t* feasible,
+                              int32_t* best_k, uint64_t* best_S, uint64_t* best_R) {
+  if (!g) return fail(CKM_E_INVALID_ARG, "graph is NULL");
+  if (!s_frac || !p || !peak || !cost || !feasible || !best_k)
+    return fail(CKM_E_INVALID_ARG, "NULL S*, thresholds, peak, cost, feasible or best_k");
+  if (ld < g->n) return fail(CKM_E_INVALID_ARG, "ld = %lld < n = %d", (long long)ld, g->n);
+  if (K < 1) return fail(CKM_E_INVALID_ARG, "K = %d < 1", K);
+  if (K > CKM_MAX_THRESHOLDS) return fail(CKM_E_UNSUPPORTED, "K = %d > %d thresholds", K, CKM_MAX_THRESHOLDS);
+  if (budget < 0) return fail(CKM_E_INVALID_ARG, "budget = %lld < 0", (long long)budget);
+  const int32_t n = g->n;
+  for (int32_t k = 0; k < K; ++k)
+    if (std::isnan(p[k])) return fail(CKM_E_INVALID_ARG, "threshold %d is NaN", k);
+  for (int32_t t = 0; t < n; ++t)
+    for (int32_t i = 0; i < t; ++i)
+      if (std::isnan(s_frac[(int64_t)t * ld + i]))
+        return fail(CKM_E_INVALID_ARG, "S*[%d][%d] is NaN", t, i);
+
+  DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
+  const Layout L = ckm::make_layout(n, K);
+  const int32_t W = (n + 63) / 64;
+  const size_t rows_bytes = (size_t)n * W * sizeof(uint64_t);
+  size_t off = 0;
+  const size_t o_s = off;    off = align256(off + (size_t)n * n * sizeof(double));
+  const size_t o_p = off;    off = align256(off + (size_t)K * sizeof(double));
+  const size_t o_peak = off; off = align256(off + (size_t)K * 8);
+  const size_t o_cost = off; off = align256(off + (size_t)K * 8);
+  const size_t o_feas = off; off = align256(off + (size_t)K);
+  const size_t o_bk = off;   off = align256(off + 8);
+  const size_t o_bS = off;   off = align256(off + rows_bytes);
+  const size_t o_bR = off;   off = align256(off + rows_bytes);
+  const size_t o_w = off;    off = align256(off + L.total);
+  char* d = nullptr;
+  hipError_t e = hipMalloc(&d, off);
+  if (e != hipSuccess)
+    return e == hipErrorOutOfMemory ? fail(CKM_E_NOMEM, "hipMalloc of %zu bytes failed", off)
+                                    : fail_hip(e, "hipMalloc");
+  hipStream_t stream = nullptr;
+  ckm_status st = CKM_OK;
+  do {
+    if ((e = hipStreamCreateWithFlags(&stream, hipStreamNonBlocking)) != hipSuccess) {
+      st = fail_hip(e, "hipStreamCreate");
+      break;
+    }
+    if ((e = hipMemcpy2DAsync(d + o_s, (size_t)n * sizeof(double), s_frac, (size_t)ld * sizeof(double),
+                              (size_t)n * sizeof(double), n, hipMemcpyHostToDevice, stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(d + o_p, p, (size_t)K * sizeof(double), hipMemcpyHostToDevice, stream)) !=
+            hipSuccess) {
+      st = fail_hip(e, "hipMemcpy S* or thresholds");
+      break;
+    }
+    st = ckm_threshold_eval_async(g, reinterpret_cast<const double*>(d + o_s), n,
+                                  reinterpret_cast<const double*>(d + o_p), K, budget,
+                                  reinterpret_cast<int64_t*>(d + o_peak), reinterpret_cast<int64_t*>(d + o_cost),
+                                  reinterpret_cast<uint8_t*>(d + o_feas), reinterpret_cast<int32_t*>(d + o_bk),
+                                  best_S ? reinterpret_cast<uint64_t*>(d + o_bS) : nullptr,
+                                  best_R ? reinterpret_cast<uint64_t*>(d + o_bR) : nullptr, nullptr, d + o_w,
+                                  L.total, stream);
+    if (st != CKM_OK) break;
+    struct Copy { void* dst; size_t off, bytes; } copies[] = {
+        {peak, o_peak, (size_t)K * 8}, {cost, o_cost, (size_t)K * 8}, {feasible, o_feas, (size_t)K},
+        {best_k, o_bk, 4}, {best_S, o_bS, rows_bytes}, {best_R, o_bR, rows_bytes}};
     for (const Copy& c : copies) {
       if (!c.dst) continue;
       if ((e = hipMemcpyAsync(c.dst, d + c.off, c.bytes, hipMemcpyDeviceToHost, stream)) != hipSuccess) {

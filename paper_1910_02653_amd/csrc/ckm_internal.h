@@ -33,6 +33,13 @@ namespace ckm {
 constexpr int kWave = 64;
 constexpr int kNodeRecBytes = 256;
 
+// Where the evaluate kernel's S rows come from.
+enum : int {
+  kSrcRound = 0,      // randomized rounding of S* (deterministic candidate 0 under CKM_F_DET0)
+  kSrcUser = 1,       // the caller's integral S matrices
+  kSrcThreshold = 2,  // threshold rounding [clamp(S*) > p_k], one threshold per candidate
+};
+
 // Host-side builder of the per-node records the evaluate kernel reads
 // (layout documented with NodeRec in ckm_kernels.hip). Writes n records.
 void build_node_records(int32_t n, const double* M, const double* C, const int32_t* dep_ptr,
@@ -50,7 +57,7 @@ struct Layout {
   int32_t reduce_blocks = 0;
   // hdr: int32 number of work items (rows of the partial arrays) of the last evaluate
   size_t hdr_off = 0, q_off = 0, det_off = 0, nan_off = 0, part_peak_off = 0, part_cost_off = 0,
-         best_off = 0, srows_off = 0, total = 0;
+         best_off = 0, srows_off = 0, thr_sorted_off = 0, thr_rank_off = 0, total = 0;
 };
 
 Layout make_layout(int32_t n, int32_t K);
@@ -71,15 +78,19 @@ Plan plan_splits(int32_t n, int32_t splits);
 // Kernel launchers (defined in ckm_kernels.hip). They only enqueue work.
 hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,
                            char* work, hipStream_t stream);
-// s_user: K caller-supplied S matrices ([K][n][row_words] 32-bit words) to
-// evaluate instead of rounding S*; null for the rounding path.
+// Threshold family: ranks of the K thresholds, their sorted copy, and the
+// keys of S* in place of the quantized thresholds q.
+hipError_t launch_threshold_keys(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,
+                                 const double* d_p, int32_t K, char* work, hipStream_t stream);
+// src: one of kSrcRound, kSrcUser, kSrcThreshold. s_user: for kSrcUser, K
+// caller-supplied S matrices ([K][n][row_words] 32-bit words).
 hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
-                           uint32_t flags, const Plan& plan, const uint64_t* s_user, char* work,
+                           uint32_t flags, const Plan& plan, int src, const uint64_t* s_user, char* work,
                            hipStream_t stream);
 hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
                          int64_t budget, uint32_t flags, int64_t* d_peak,
                          int64_t* d_cost, uint8_t* d_feasible, int32_t* d_best_k,
-                         uint64_t* d_best_S, uint64_t* d_best_R, int32_t* d_status,
+                         uint64_t* d_best_S, uint64_t* d_best_R, int32_t* d_status, int src,
                          const uint64_t* s_user, char* work, hipStream_t stream);
 
 }  // namespace ckm

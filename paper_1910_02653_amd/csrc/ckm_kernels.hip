@@ -133,6 +133,61 @@ __device__ __forceinline__ uint32_t round_word(QPtr qrow, int w, int r, uint32_t
   return word;
 }
 
+// word = 2^8 word + (8 threshold bits), high bit first: bit j of the new byte
+// is [rk < q_j] with rk the lane's threshold rank and q_j wave-uniform keys
+// (same carry-in fold as append8_uniform).
+__device__ __forceinline__ uint32_t append8_rank(uint32_t word, uint32_t rk, const uint32_t q[8]) {
+  uint64_t m0, m1, m2;
+  asm("v_cmp_lt_u32_e64 %[m0], %[rk], %[q7]\n\t"
+      "v_cmp_lt_u32_e64 %[m1], %[rk], %[q6]\n\t"
+      "v_cmp_lt_u32_e64 %[m2], %[rk], %[q5]\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m0]\n\t"
+      "v_cmp_lt_u32_e64 %[m0], %[rk], %[q4]\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m1]\n\t"
+      "v_cmp_lt_u32_e64 %[m1], %[rk], %[q3]\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m2]\n\t"
+      "v_cmp_lt_u32_e64 %[m2], %[rk], %[q2]\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m0]\n\t"
+      "v_cmp_lt_u32_e64 %[m0], %[rk], %[q1]\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m1]\n\t"
+      "v_cmp_lt_u32_e64 %[m1], %[rk], %[q0]\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m2]\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m0]\n\t"
+      "v_addc_co_u32 %[w], vcc, %[w], %[w], %[m1]"
+      : [w] "+v"(word), [m0] "=&s"(m0), [m1] "=&s"(m1), [m2] "=&s"(m2)
+      : [rk] "v"(rk), [q0] "s"(q[0]), [q1] "s"(q[1]), [q2] "s"(q[2]), [q3] "s"(q[3]), [q4] "s"(q[4]),
+        [q5] "s"(q[5]), [q6] "s"(q[6]), [q7] "s"(q[7])
+      : "vcc");
+  return word;
+}
+
+// 32 threshold-rounding decisions of row r: bits i = 32w .. 32w+31 of
+// S[r][i] = [clamp(S*[r][i], 0, 1) > p_k], computed exactly as [rk < key[r][i]]
+// with key = #{j : p_j < clamp(S*)} and rk = #{j : p_j < p_k}. Keys of
+// entries i >= r are 0. kUniformQ: the row pointer and w are wave-uniform.
+template <bool kUniformQ, typename QPtr>
+__device__ __forceinline__ uint32_t threshold_word(QPtr qrow, int w, int r, uint32_t rk) {
+  uint32_t word = 0;
+#pragma unroll
+  for (int b = 3; b >= 0; --b) {
+    const int m = 4 * w + b;
+    if (8 * m >= r) {
+      word <<= 8;
+      continue;
+    }
+    uint32_t q[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) q[j] = qrow[8 * m + j];
+    if (kUniformQ) {
+      word = append8_rank(word, rk, q);
+    } else {
+#pragma unroll
+      for (int j = 7; j >= 0; --j) word = word + word + (rk < q[j] ? 1u : 0u);
+    }
+  }
+  return word;
+}
+
 // ---------------------------------------------------------------------------
 // Per-node record, read once per node visit. Masks are relative to the node
 // v: bit d <-> node v + 1 + d, d < 64. A "ref" locates one bit of a row in
@@ -240,8 +295,9 @@ struct EvalArgs {
   cptr<int32_t> dep_idx;
   cptr<int32_t> dep_upos;
   const uint4* __restrict__ recs;
-  const uint32_t* __restrict__ s_user;  // caller-supplied S rows ([K][n][s_words]), or null: round S*
+  const uint32_t* __restrict__ s_user;  // kSrcUser: caller-supplied S rows ([K][n][s_words])
   int32_t s_words;                      // 32-bit words per supplied row
+  const uint32_t* __restrict__ rank;    // kSrcThreshold: [K] threshold ranks (q holds the keys)
   int64_t* __restrict__ part_peak;   // [K] running max over work items
   int64_t* __restrict__ part_cost;   // [K] running sum over work items
   int32_t* __restrict__ hdr;
@@ -324,16 +380,18 @@ __device__ __forceinline__ uint32_t umin1(uint32_t x) {
   return y;
 }
 
-// Row r of the candidate into words 0 .. r/32. kUser: the rows are the
-// caller's (a.s_user) instead of rounded from S*.
-template <bool kUser, typename RowT>
-__device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bool det_lane, RowT& dst) {
+// Row r of the candidate into words 0 .. r/32, from the source kSrc:
+// randomized rounding of S*, the caller's rows (a.s_user), or threshold
+// rounding (lane threshold rank rk against the keys in q).
+template <int kSrc, typename RowT>
+__device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bool det_lane, uint32_t rk,
+                                        RowT& dst) {
   const int nw = (r >> 5) + 1;
   if (r >= a.n) {  // S after the last stage: nothing is kept
     for (int w = 0; w < nw; ++w) dst.word(w) = 0u;
     return;
   }
-  if (kUser) {
+  if (kSrc == kSrcUser) {
     // caller-supplied S: row r of candidate k; bits on or above the diagonal
     // (i >= r) are cleared. Lanes past K read candidate K-1 (results unused).
     const uint32_t kk = k < (uint32_t)a.K ? k : (uint32_t)a.K - 1u;
@@ -346,6 +404,10 @@ __device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bo
     return;
   }
   cptr<uint32_t> qrow = a.q + (size_t)r * a.ldq;
+  if (kSrc == kSrcThreshold) {
+    for (int w = 0; w < nw; ++w) dst.word(w) = threshold_word<true>(qrow, w, r, rk);
+    return;
+  }
   cptr<uint32_t> drow = a.det + (size_t)r * a.det_words;
   // the round keys are rebuilt per row instead of held for the whole kernel
   uint32_t key0 = a.key0, key1 = a.key1;
@@ -597,9 +659,9 @@ __device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, RowB
 // One wave per workgroup: 64 candidates over one work item (a range of
 // stages). kBReg: the S_{t+1} row lives in vector registers and is copied to
 // the LDS row at the end of each stage (n < 1024), halving the LDS a wave
-// needs; otherwise both rows are in LDS and swap roles. kUser: evaluate the
-// caller's S rows instead of rounding S*.
-template <bool kBReg, bool kUser>
+// needs; otherwise both rows are in LDS and swap roles. kSrc: where the S
+// rows come from (kSrcRound, kSrcUser, kSrcThreshold).
+template <bool kBReg, int kSrc>
 __global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
   extern __shared__ uint32_t lds[];
   const int lane = threadIdx.x;
@@ -607,6 +669,8 @@ __global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
   const int item = blockIdx.y;
   const uint32_t k = (uint32_t)(group * kWave + lane);
   const bool det_lane = a.det0 && k == 0;
+  // threshold rank of the lane's candidate (lanes past K take K-1's)
+  const uint32_t rk = kSrc == kSrcThreshold ? a.rank[k < (uint32_t)a.K ? k : (uint32_t)a.K - 1u] : 0u;
   char* wave_lds = reinterpret_cast<char*>(lds);
   Row A{wave_lds + 4 * lane};
   // Rows start zeroed: words beyond a row's end (and node n's bit) read 0.
@@ -620,9 +684,9 @@ __global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
     RowReg B;
     B.w = (u32x32)0u;
     if (t0 < t1) {
-      gen_row<kUser>(a, t0, k, det_lane, A);
+      gen_row<kSrc>(a, t0, k, det_lane, rk, A);
       for (int t = t0; t < t1; ++t) {
-        gen_row<kUser>(a, t + 1, k, det_lane, B);
+        gen_row<kSrc>(a, t + 1, k, det_lane, rk, B);
         double sp, sc;
         eval_stage(a, t, A, B, sp, sc);
         seg_peak = fmax(seg_peak, sp);
@@ -639,9 +703,9 @@ __global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
     Row B{wave_lds + (size_t)a.row_words * 256 + 4 * lane};
     for (int w = 0; w < a.row_words; ++w) B.word(w) = 0u;
     if (t0 < t1) {
-      gen_row<kUser>(a, t0, k, det_lane, A);
+      gen_row<kSrc>(a, t0, k, det_lane, rk, A);
       for (int t = t0; t < t1; ++t) {
-        gen_row<kUser>(a, t + 1, k, det_lane, B);
+        gen_row<kSrc>(a, t + 1, k, det_lane, rk, B);
         double sp, sc;
         eval_stage(a, t, A, B, sp, sc);
         seg_peak = fmax(seg_peak, sp);
@@ -699,6 +763,81 @@ __global__ void __launch_bounds__(256) ckm_quantize_kernel(const double* __restr
     const int lane = threadIdx.x & 63;
     if (i < ldq && (lane == 0 || lane == 32))
       det[(size_t)r * det_words + (i >> 5)] = (uint32_t)(bits >> lane);
+  }
+  if (my_nan) atomicOr(&any_nan, 1);
+  __syncthreads();
+  if (threadIdx.x == 0) nan_row[r] = any_nan;
+}
+
+// ---------------------------------------------------------------------------
+// Threshold family, ranks: thread per candidate k; rank[k] = #{j : p_j < p_k}
+// and p_k stored at position rank[k] + #{j < k : p_j == p_k} of the sorted
+// copy (a stable counting sort; K is at most CKM_MAX_THRESHOLDS). The
+// thresholds are staged through LDS in tiles of the block size.
+__global__ void __launch_bounds__(256) ckm_threshold_rank_kernel(int32_t K, const double* __restrict__ p,
+                                                                 double* __restrict__ sorted,
+                                                                 uint32_t* __restrict__ rank) {
+  __shared__ double tile[256];
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  const double pk = k < K ? p[k] : 0.0;
+  uint32_t lt = 0, eq = 0;
+  for (int j0 = 0; j0 < K; j0 += 256) {
+    __syncthreads();
+    if (j0 + (int)threadIdx.x < K) tile[threadIdx.x] = p[j0 + threadIdx.x];
+    __syncthreads();
+    const int m = min(256, K - j0);
+    for (int jj = 0; jj < m; ++jj) {
+      const double pj = tile[jj];
+      lt += pj < pk ? 1u : 0u;
+      eq += (pj == pk && j0 + jj < k) ? 1u : 0u;
+    }
+  }
+  if (k < K) {
+    rank[k] = lt;
+    sorted[lt + eq] = pk;   // lt + eq <= K - 1: both count distinct j != k
+  }
+}
+
+// Threshold family, keys: one block per row r; q[r][i] = #{j : p_j <
+// clamp(S*[r][i], 0, 1)} for i < r (a lower-bound search of the sorted
+// thresholds), 0 elsewhere. The row's NaN flag covers S*; row 0, which has
+// no entries, carries the flag for NaN thresholds.
+__global__ void __launch_bounds__(256) ckm_threshold_key_kernel(const double* __restrict__ s, int64_t ld,
+                                                                int32_t n, int32_t ldq, int32_t K,
+                                                                const double* __restrict__ p,
+                                                                const double* __restrict__ sorted,
+                                                                uint32_t* __restrict__ q,
+                                                                int32_t* __restrict__ nan_row) {
+  __shared__ int any_nan;
+  const int r = blockIdx.x;
+  if (threadIdx.x == 0) any_nan = 0;
+  __syncthreads();
+  int my_nan = 0;
+  if (r == 0)
+    for (int k = threadIdx.x; k < K; k += blockDim.x) my_nan |= p[k] != p[k];
+  for (int i0 = 0; i0 < ldq; i0 += blockDim.x) {
+    const int i = i0 + threadIdx.x;
+    const bool in = i < r;
+    double x = in ? s[(int64_t)r * ld + i] : 0.0;
+    const bool isnan_x = in && (x != x);
+    my_nan |= isnan_x;
+    uint32_t key = 0;
+    if (in && !isnan_x) {
+      x = fmin(fmax(x, 0.0), 1.0);
+      // first position whose threshold is not below x
+      uint32_t lo = 0, len = (uint32_t)K;
+      while (len > 0) {
+        const uint32_t half = len >> 1;
+        if (sorted[lo + half] < x) {
+          lo += half + 1;
+          len -= half + 1;
+        } else {
+          len = half;
+        }
+      }
+      key = lo;
+    }
+    if (i < ldq) q[(size_t)r * ldq + i] = key;
   }
   if (my_nan) atomicOr(&any_nan, 1);
   __syncthreads();
@@ -778,12 +917,14 @@ __global__ void __launch_bounds__(256) ckm_argmin_kernel(int32_t nblocks, const 
 
 // ---------------------------------------------------------------------------
 // Best candidate's S rows: thread per (row r, 32-bit word w). Output rows
-// have row_words words; words with no node (32w >= n) are zero.
+// have row_words words; words with no node (32w >= n) are zero. rank: the
+// threshold family (q holds keys), else randomized or deterministic rounding.
 __global__ void __launch_bounds__(256) ckm_best_rows_kernel(const uint32_t* __restrict__ q,
                                                             const uint32_t* __restrict__ det,
                                                             int32_t n, int32_t ldq, int32_t det_words,
                                                             int32_t row_words, uint32_t key0,
                                                             uint32_t key1, uint32_t det0,
+                                                            const uint32_t* __restrict__ rank,
                                                             const int32_t* __restrict__ best_k,
                                                             uint32_t* __restrict__ S_rows) {
   const int r = blockIdx.y;
@@ -792,7 +933,9 @@ __global__ void __launch_bounds__(256) ckm_best_rows_kernel(const uint32_t* __re
   const int bk = best_k[0];
   uint32_t word = 0;
   if (bk >= 0 && 32 * w < n) {
-    if (det0 && bk == 0)
+    if (rank)
+      word = threshold_word<false>(q + (size_t)r * ldq, w, r, rank[bk]);
+    else if (det0 && bk == 0)
       word = det[(size_t)r * det_words + w];
     else
       word = round_word<false>(q + (size_t)r * ldq, w, r, (uint32_t)bk, key0, key1);
@@ -869,14 +1012,26 @@ hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_
   return hipGetLastError();
 }
 
+hipError_t launch_threshold_keys(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,
+                                 const double* d_p, int32_t K, char* work, hipStream_t stream) {
+  double* sorted = at<double>(work, L.thr_sorted_off);
+  hipLaunchKernelGGL(ckm_threshold_rank_kernel, dim3((K + 255) / 256), dim3(256), 0, stream, K, d_p, sorted,
+                     at<uint32_t>(work, L.thr_rank_off));
+  hipLaunchKernelGGL(ckm_threshold_key_kernel, dim3(g.n), dim3(256), 0, stream, d_s, ld, g.n, L.ldq, K, d_p,
+                     static_cast<const double*>(sorted), at<uint32_t>(work, L.q_off),
+                     at<int32_t>(work, L.nan_off));
+  return hipGetLastError();
+}
+
 hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
-                           uint32_t flags, const Plan& plan, const uint64_t* s_user, char* work,
+                           uint32_t flags, const Plan& plan, int src, const uint64_t* s_user, char* work,
                            hipStream_t stream) {
   EvalArgs a;
   a.n = g.n;
   a.K = K;
   a.s_user = reinterpret_cast<const uint32_t*>(s_user);
   a.s_words = L.row_words;
+  a.rank = at<const uint32_t>(work, L.thr_rank_off);
   a.items = plan.items;
   a.kind = plan.kind;
   a.P = plan.P;
@@ -906,10 +1061,12 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   const bool breg = a.row_words <= kRegRowWords;
   const size_t lds_bytes = (breg ? 1u : 2u) * (size_t)a.row_words * kWave * sizeof(uint32_t);
   void (*fn)(EvalArgs);
-  if (s_user)
-    fn = breg ? ckm_eval_kernel<true, true> : ckm_eval_kernel<false, true>;
+  if (src == kSrcUser)
+    fn = breg ? ckm_eval_kernel<true, kSrcUser> : ckm_eval_kernel<false, kSrcUser>;
+  else if (src == kSrcThreshold)
+    fn = breg ? ckm_eval_kernel<true, kSrcThreshold> : ckm_eval_kernel<false, kSrcThreshold>;
   else
-    fn = breg ? ckm_eval_kernel<true, false> : ckm_eval_kernel<false, false>;
+    fn = breg ? ckm_eval_kernel<true, kSrcRound> : ckm_eval_kernel<false, kSrcRound>;
   if (lds_bytes > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     if (e != hipSuccess) return e;
@@ -923,17 +1080,17 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
 hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
                          int64_t budget, uint32_t flags, int64_t* d_peak, int64_t* d_cost,
                          uint8_t* d_feasible, int32_t* d_best_k, uint64_t* d_best_S,
-                         uint64_t* d_best_R, int32_t* d_status, const uint64_t* s_user, char* work,
-                         hipStream_t stream) {
+                         uint64_t* d_best_R, int32_t* d_status, int src, const uint64_t* s_user,
+                         char* work, hipStream_t stream) {
   const int rb = L.reduce_blocks;
   hipLaunchKernelGGL(ckm_reduce_kernel, dim3(rb), dim3(256), 0, stream, K,
                      at<const int64_t>(work, L.part_peak_off), at<const int64_t>(work, L.part_cost_off),
                      budget, d_peak, d_cost, d_feasible, at<Best>(work, L.best_off));
-  // rounded candidates: S* NaN flags from the quantize stage; supplied S: none
+  // rounded candidates: NaN flags from the quantize or key stage; supplied S: none
   hipLaunchKernelGGL(ckm_argmin_kernel, dim3(1), dim3(256), 0, stream, rb,
-                     at<const Best>(work, L.best_off), s_user ? 0 : g.n, at<const int32_t>(work, L.nan_off),
-                     d_best_k, d_status);
-  if (s_user) {
+                     at<const Best>(work, L.best_off), src == kSrcUser ? 0 : g.n,
+                     at<const int32_t>(work, L.nan_off), d_best_k, d_status);
+  if (src == kSrcUser) {
     if (d_best_R)
       hipLaunchKernelGGL(ckm_best_closure_kernel, dim3((g.n + kWave - 1) / kWave), dim3(kWave), 0, stream,
                          g.n, L.row_words, g.d_user_ptr, g.d_user_idx, d_best_k,
@@ -945,7 +1102,9 @@ hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_
     hipLaunchKernelGGL(ckm_best_rows_kernel, grid, dim3(256), 0, stream,
                        at<const uint32_t>(work, L.q_off), at<const uint32_t>(work, L.det_off), g.n,
                        L.ldq, L.det_words, L.row_words, (uint32_t)(seed & 0xFFFFFFFFu),
-                       (uint32_t)(seed >> 32), (flags & CKM_F_DET0) ? 1u : 0u, d_best_k, srows);
+                       (uint32_t)(seed >> 32), (flags & CKM_F_DET0) ? 1u : 0u,
+                       src == kSrcThreshold ? at<const uint32_t>(work, L.thr_rank_off) : nullptr, d_best_k,
+                       srows);
     if (d_best_R) {
       hipLaunchKernelGGL(ckm_best_closure_kernel, dim3((g.n + kWave - 1) / kWave), dim3(kWave), 0,
                          stream, g.n, L.row_words, g.d_user_ptr, g.d_user_idx, d_best_k,
