@@ -355,3 +355,135 @@ int ckm_ref_round_eval(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx
   free(q);
   return CKM_REF_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Conditions the plan generator needs of (S, R), strict lower S and lower R
+ * (entries of S with i >= t and of R with i > t are not read):
+ *   R[t][t] = 1 (constraint 4a); no value both kept and recomputed in one
+ *   stage (R[t][i] S[t][i] = 0, which Algorithm 2's output satisfies);
+ *   (1b) R[t][j] <= R[t][i] + S[t][i] for every edge (i, j);
+ *   (1c) S[t+1][i] <= R[t][i] + S[t][i].
+ * Returns CKM_REF_OK or CKM_REF_E_INVALID_ARG. */
+int ckm_ref_check_schedule(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
+                           const uint8_t* S, const uint8_t* R) {
+  int32_t t, i, j, a;
+#define SB(t, i) ((i) < (t) ? S[(int64_t)(t) * n + (i)] : 0)
+#define RB(t, i) ((i) <= (t) ? R[(int64_t)(t) * n + (i)] : 0)
+  for (t = 0; t < n; ++t) {
+    if (!RB(t, t)) return CKM_REF_E_INVALID_ARG;
+    for (i = 0; i < t; ++i)
+      if (SB(t, i) && RB(t, i)) return CKM_REF_E_INVALID_ARG;
+    for (j = 0; j <= t; ++j)
+      if (RB(t, j))
+        for (a = dep_ptr[j]; a < dep_ptr[j + 1]; ++a) {
+          i = dep_idx[a];
+          if (!RB(t, i) && !SB(t, i)) return CKM_REF_E_INVALID_ARG;
+        }
+    if (t + 1 < n)
+      for (i = 0; i <= t; ++i)
+        if (SB(t + 1, i) && !RB(t, i) && !SB(t, i)) return CKM_REF_E_INVALID_ARG;
+  }
+#undef SB
+#undef RB
+  return CKM_REF_OK;
+}
+
+/* Section 4.9, Algorithm 1: a row-major scan of R; stage t, node k:
+ *   if R[t][k]: "%r = compute v_k", Regs[k] = r, r = r + 1;
+ *   for i in Deps[k] u {k} (ascending; k is the largest): if FREE(t,i,k):
+ *   "deallocate %Regs[i]", with FREE(t,i,k) = R[t][k] (1 - S[t+1][i])
+ *   prod_{j in Users[i], j > k} (1 - R[t][j]) (eq. collectable).
+ * A checkpoint of stage t with no computed user in the stage and not kept
+ * into stage t+1 gets no FREE term; it is deallocated at the end of the stage
+ * (where the U recurrence stops counting it), or with early != 0 at the
+ * start of the stage (the code motion of Section 4.9).
+ * Statement s is stmts[4s .. 4s+3] = (op, node, register, stage) with op 0 =
+ * compute, 1 = deallocate. mem[s] (may be NULL) = M_in + 2 M_param + the
+ * sizes of the registers live after statement s. At most `capacity`
+ * statements are written; *count receives the number the plan has. Returns
+ * CKM_REF_E_INVALID_ARG when (S, R) fails ckm_ref_check_schedule. */
+int ckm_ref_plan(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx, const int64_t* size,
+                 int64_t m_input, int64_t m_param, const uint8_t* S, const uint8_t* R, int early,
+                 int32_t* stmts, int64_t* mem, int64_t capacity, int64_t* count) {
+  int32_t t, k, i, j, a, m, pass;
+  int64_t s = 0, r = 0, live_bytes = 0;
+  int32_t* Regs;
+  int32_t* user_ptr;
+  int32_t* user_idx;
+  int32_t* fill;
+  int32_t E = dep_ptr[n];
+  int st = ckm_ref_check_schedule(n, dep_ptr, dep_idx, S, R);
+  if (st != CKM_REF_OK) return st;
+  Regs = (int32_t*)malloc((size_t)n * sizeof(int32_t));
+  user_ptr = (int32_t*)calloc((size_t)n + 1, sizeof(int32_t));
+  user_idx = (int32_t*)malloc((size_t)(E > 0 ? E : 1) * sizeof(int32_t));
+  fill = (int32_t*)calloc((size_t)n, sizeof(int32_t));
+  for (i = 0; i < n; ++i) Regs[i] = -1;
+  for (j = 0; j < n; ++j)
+    for (a = dep_ptr[j]; a < dep_ptr[j + 1]; ++a) user_ptr[dep_idx[a] + 1]++;
+  for (i = 0; i < n; ++i) user_ptr[i + 1] += user_ptr[i];
+  for (j = 0; j < n; ++j)
+    for (a = dep_ptr[j]; a < dep_ptr[j + 1]; ++a) {
+      i = dep_idx[a];
+      user_idx[user_ptr[i] + fill[i]++] = j;
+    }
+
+#define EMIT(op_, node_, reg_)                                                  \
+  do {                                                                          \
+    live_bytes += (op_) == 0 ? size[node_] : -size[node_];                      \
+    if (s < capacity) {                                                         \
+      stmts[4 * s] = (op_);                                                     \
+      stmts[4 * s + 1] = (node_);                                               \
+      stmts[4 * s + 2] = (int32_t)(reg_);                                       \
+      stmts[4 * s + 3] = t;                                                     \
+      if (mem) mem[s] = m_input + 2 * m_param + live_bytes;                     \
+    }                                                                           \
+    ++s;                                                                        \
+  } while (0)
+
+  for (t = 0; t < n; ++t) {
+    const uint8_t* St = S + (int64_t)t * n;
+    const uint8_t* Rt = R + (int64_t)t * n;
+    for (pass = 0; pass < 3; ++pass) {
+      if (pass == 1) {
+        /* the scan of Algorithm 1 */
+        for (k = 0; k <= t; ++k) {
+          if (Rt[k]) {
+            Regs[k] = (int32_t)r;
+            EMIT(0, k, r);
+            ++r;
+          }
+          for (m = 0; m <= dep_ptr[k + 1] - dep_ptr[k]; ++m) {
+            int64_t FREE;
+            int32_t b;
+            i = (m < dep_ptr[k + 1] - dep_ptr[k]) ? dep_idx[dep_ptr[k] + m] : k;
+            FREE = (int64_t)Rt[k] * (1 - (int64_t)((t + 1 < n && i < t + 1) ? S[(int64_t)(t + 1) * n + i] : 0));
+            for (b = user_ptr[i]; b < user_ptr[i + 1]; ++b) {
+              j = user_idx[b];
+              if (j > k) FREE *= (1 - (int64_t)(j <= t ? Rt[j] : 0));
+            }
+            if (FREE) EMIT(1, i, Regs[i]);
+          }
+        }
+      } else if ((pass == 0) == (early != 0)) {
+        /* unused checkpoints not kept into stage t+1 */
+        for (i = 0; i < t; ++i) {
+          int32_t b, used = 0;
+          if (!St[i] || (t + 1 < n && S[(int64_t)(t + 1) * n + i])) continue;
+          for (b = user_ptr[i]; b < user_ptr[i + 1]; ++b) {
+            j = user_idx[b];
+            if (j <= t && Rt[j]) used = 1;
+          }
+          if (!used) EMIT(1, i, Regs[i]);
+        }
+      }
+    }
+  }
+#undef EMIT
+  *count = s;
+  free(Regs);
+  free(user_ptr);
+  free(user_idx);
+  free(fill);
+  return CKM_REF_OK;
+}

@@ -106,6 +106,22 @@ int ckm_ref_round_eval(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx
                        uint32_t flags, int64_t* peak, int64_t* total_cost, uint8_t* feasible,
                        int32_t* best_k, uint64_t* best_S, uint64_t* best_R);
 
+/* Whether (S, R) meets what the plan generator needs: R[t][t] = 1 (4a), no
+ * value both kept and recomputed in a stage, constraints (1b) and (1c).
+ * Entries of S with i >= t and of R with i > t are not read. */
+int ckm_ref_check_schedule(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
+                           const uint8_t* S, const uint8_t* R);
+
+/* Algorithm 1 (Section 4.9): the execution plan of (S, R) as statements
+ * (op, node, register, stage), op 0 = compute, 1 = deallocate, with the
+ * memory in use after each statement (mem may be NULL). Unused checkpoints
+ * that are not kept are deallocated at the end of their stage, or at its
+ * start when early != 0. Writes at most capacity statements; *count = the
+ * plan's length. CKM_REF_E_INVALID_ARG if (S, R) fails the check above. */
+int ckm_ref_plan(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx, const int64_t* size,
+                 int64_t m_input, int64_t m_param, const uint8_t* S, const uint8_t* R, int early,
+                 int32_t* stmts, int64_t* mem, int64_t capacity, int64_t* count);
+
 #ifdef __cplusplus
 }
 #endif

@@ -53,6 +53,10 @@ def lib():
         L.ckm_ref_round_det.restype = None
         L.ckm_ref_round_threshold.argtypes = [C.c_int32, p, C.c_int64, C.c_double, p]
         L.ckm_ref_round_threshold.restype = C.c_int
+        L.ckm_ref_check_schedule.argtypes = [C.c_int32, p, p, p, p]
+        L.ckm_ref_check_schedule.restype = C.c_int
+        L.ckm_ref_plan.argtypes = [C.c_int32, p, p, p, C.c_int64, C.c_int64, p, p, C.c_int, p, p, C.c_int64, p]
+        L.ckm_ref_plan.restype = C.c_int
         L.ckm_ref_solve_R.argtypes = [C.c_int32, p, p, p, p]
         L.ckm_ref_solve_R.restype = None
         L.ckm_ref_simulate.argtypes = [C.c_int32, p, p, p, p, C.c_int64, C.c_int64, p, p, p, p, p, p, p]
@@ -236,6 +240,32 @@ def eval_schedules(w, S_mats, budget: int):
     best_R = pack_rows(Rs[best]) if best >= 0 else np.zeros((w.n, W), np.uint64)
     return dict(peak=np.array(peaks, np.int64), cost=np.array(costs, np.int64),
                 feasible=np.array(feas, np.uint8), best_k=best, best_R=best_R)
+
+
+def check_schedule(w, S, R) -> int:
+    ptr, idx, _, _ = _graph(w)
+    S = np.ascontiguousarray(S, dtype=np.uint8)
+    R = np.ascontiguousarray(R, dtype=np.uint8)
+    return lib().ckm_ref_check_schedule(w.n, _ptr(ptr), _ptr(idx), _ptr(S), _ptr(R))
+
+
+def plan(w, S, R, early: bool = False):
+    """Algorithm 1's execution plan of (S, R): (stmts [count][4] int32 as
+    (op, node, register, stage), mem [count] int64)."""
+    ptr, idx, _, size = _graph(w)
+    S = np.ascontiguousarray(S, dtype=np.uint8)
+    R = np.ascontiguousarray(R, dtype=np.uint8)
+    cap = int(2 * R.astype(np.int64).sum()) + 1
+    stmts = np.zeros((cap, 4), np.int32)
+    mem = np.zeros(cap, np.int64)
+    cnt = np.zeros(1, np.int64)
+    st = lib().ckm_ref_plan(w.n, _ptr(ptr), _ptr(idx), _ptr(size), w.m_input, w.m_param, _ptr(S), _ptr(R),
+                            1 if early else 0, _ptr(stmts), _ptr(mem), cap, _ptr(cnt))
+    if st != OK:
+        raise ValueError("plan: status %d" % st)
+    c = int(cnt[0])
+    assert c <= cap
+    return stmts[:c].copy(), mem[:c].copy()
 
 
 def pack_rows(X) -> np.ndarray:
