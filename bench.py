@@ -17,6 +17,9 @@ checkpoint matrices (banded, 30 % of values kept) on the same graph: Algorithm
 `threshold_family` times K deterministic candidates [clamp(S*) > p_k] on an
 even threshold grid over [0, 1] for the same graph and S*: keys, evaluation,
 argmin and the best S and R.
+`execution_plan` times Algorithm 1's plan (with the memory after each
+statement) for the step's best candidate, or candidate 0's rows when none
+is feasible, read from HBM where the step left them.
 """
 from __future__ import annotations
 
@@ -123,6 +126,46 @@ def time_thresholds(g, w, K, steps, stream, d_s):
             "input": "K=%d thresholds evenly spaced over [0, 1] on the workload's S*" % K}
 
 
+def time_plan(g, w, steps, stream, d_s):
+    """Throughput of ckm_plan_async on one schedule of the workload: the best
+    candidate at the median-peak budget (a budget some candidates meet)."""
+    import numpy as np
+    import torch
+
+    from paper_1910_02653_amd import ckm
+
+    K = w.K
+    work = g.alloc_work(K)
+    out = g.alloc_outputs(K)
+    g.round_eval_async(d_s, K, w.seed, 2 ** 62, 0, out, work, stream)
+    torch.cuda.synchronize()
+    budget = int(np.median(out["peak"].cpu().numpy()))
+    g.round_eval_async(d_s, K, w.seed, budget, 0, out, work, stream)
+    torch.cuda.synchronize()
+    assert int(out["status"].item()) == ckm.OK and int(out["best_k"].item()) >= 0
+    cap = w.n * (w.n + 1)
+    d_P = torch.empty((cap, 4), dtype=torch.int32, device="cuda")
+    d_mem = torch.empty(cap, dtype=torch.int64, device="cuda")
+    d_cnt = torch.empty(1, dtype=torch.int64, device="cuda")
+    d_st = torch.empty(1, dtype=torch.int32, device="cuda")
+    for _ in range(3):
+        g.plan_async(out["best_S"], out["best_R"], False, d_P, cap, d_cnt, d_mem, d_st, work, stream)
+    torch.cuda.synchronize()
+    assert int(d_st.item()) == ckm.OK
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(steps):
+        g.plan_async(out["best_S"], out["best_R"], False, d_P, cap, d_cnt, d_mem, d_st, work, stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    cnt = int(d_cnt.item())
+    return {"ms_per_call": ms, "statements": cnt, "statements_per_s": cnt / (ms * 1e-3), "steps": steps,
+            "input": "candidate %d of %d (best at the median-peak budget %d B), n=%d"
+                     % (int(out["best_k"].item()), K, budget, w.n)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -135,6 +178,8 @@ def main():
                     help="timed calls of the supplied-schedule evaluation (0 = skip)")
     ap.add_argument("--thr-steps", type=int, default=20,
                     help="timed calls of the threshold-family evaluation (0 = skip)")
+    ap.add_argument("--plan-steps", type=int, default=20,
+                    help="timed calls of the execution-plan generation (0 = skip)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -216,6 +261,8 @@ def main():
     }
     if args.sched_steps > 0:
         result["supplied_schedules"] = time_schedules(g, w, K, args.sched_steps, stream)
+    if args.plan_steps > 0:
+        result["execution_plan"] = time_plan(g, w, args.plan_steps, stream, d_s)
     if args.thr_steps > 0:
         result["threshold_family"] = time_thresholds(g, w, K, args.thr_steps, stream, d_s)
     if args.cpu_sample > 0:

@@ -207,6 +207,50 @@ ckm_status ckm_threshold_eval_async(const ckm_graph* g, const double* d_s_frac, 
                                    uint64_t* d_best_R, int32_t* d_status, void* d_work, size_t work_bytes,
                                    void* stream);
 
+/* ---- execution plans ---------------------------------------------------
+ * Algorithm 1 (Section 4.9): the program that carries out a schedule (S, R).
+ * R is scanned row by row. In stage t, node k is computed into a new virtual
+ * register when R[t][k] = 1 ("%r = compute v_k"; registers are numbered
+ * 0, 1, ... in compute order). Then every i in Deps[k] u {k}, ascending, is
+ * deallocated when FREE(t,i,k) = R[t][k] (1 - S[t+1][i]) prod over users
+ * j > k of i of (1 - R[t][j]) holds (eq. collectable, S[n] = 0): each value
+ * that is not kept goes right after its last computed use. A checkpoint with
+ * no computed user in the stage that is not kept gets no FREE term. It is
+ * deallocated at the end of the stage, where the U recurrence of Section 4.4
+ * stops counting it. With CKM_PLAN_EARLY_FREE it is deallocated at the start
+ * of the stage instead, the code motion Section 4.9 describes. Without that
+ * flag, the memory after each compute equals U_{t,k} of the recurrence.
+ *
+ * S, R: n bit rows each, ceil(n/64) uint64 words per row, least significant
+ * bit first (the layout of best_S / best_R). Entries of S with i >= t and of
+ * R with i > t are ignored. (S, R) must satisfy R[t][t] = 1 (constraint 4a),
+ * (1b), (1c), and S[t][i] R[t][i] = 0 (Algorithm 2's output does). Otherwise
+ * the status is CKM_E_INVALID_ARG.
+ * P: capacity statements (op, node, reg, stage). mem (may be NULL): capacity
+ * int64 entries, the bytes in use after each statement, M_in + 2 M_param
+ * included. count receives the plan's length, which is at most
+ * CKM_PLAN_MAX_STMTS(n). With P NULL only the count is computed. If P is
+ * given and capacity < count, the result is CKM_E_INVALID_ARG and nothing is
+ * written to P. The synchronous form takes host arrays. The asynchronous
+ * form takes device arrays, a work buffer from ckm_workspace_size(g, K) for
+ * any K >= 1, and a stream. It writes the count and the status to d_count
+ * and d_status (the latter may be NULL). */
+typedef struct ckm_stmt {
+  int32_t op;    /* CKM_OP_COMPUTE or CKM_OP_DEALLOCATE */
+  int32_t node;  /* v_k computed, or the node whose value is deallocated */
+  int32_t reg;   /* virtual register defined or released */
+  int32_t stage; /* t */
+} ckm_stmt;
+enum { CKM_OP_COMPUTE = 0, CKM_OP_DEALLOCATE = 1 };
+enum { CKM_PLAN_EARLY_FREE = 1u };
+#define CKM_PLAN_MAX_STMTS(n) ((int64_t)(n) * ((int64_t)(n) + 1))
+
+ckm_status ckm_plan(const ckm_graph* g, const uint64_t* S, const uint64_t* R, uint32_t flags, ckm_stmt* P,
+                    int64_t capacity, int64_t* count, int64_t* mem);
+ckm_status ckm_plan_async(const ckm_graph* g, const uint64_t* d_S, const uint64_t* d_R, uint32_t flags,
+                          ckm_stmt* d_P, int64_t capacity, int64_t* d_count, int64_t* d_mem, int32_t* d_status,
+                          void* d_work, size_t work_bytes, void* stream);
+
 /* Thread-local text describing the calling thread's last non-OK status. */
 const char* ckm_last_error(void);
 

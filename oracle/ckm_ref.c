@@ -411,6 +411,8 @@ int ckm_ref_plan(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx, cons
   int32_t* user_ptr;
   int32_t* user_idx;
   int32_t* fill;
+  int32_t* order;
+  int32_t deg;
   int32_t E = dep_ptr[n];
   int st = ckm_ref_check_schedule(n, dep_ptr, dep_idx, S, R);
   if (st != CKM_REF_OK) return st;
@@ -418,6 +420,7 @@ int ckm_ref_plan(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx, cons
   user_ptr = (int32_t*)calloc((size_t)n + 1, sizeof(int32_t));
   user_idx = (int32_t*)malloc((size_t)(E > 0 ? E : 1) * sizeof(int32_t));
   fill = (int32_t*)calloc((size_t)n, sizeof(int32_t));
+  order = (int32_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
   for (i = 0; i < n; ++i) Regs[i] = -1;
   for (j = 0; j < n; ++j)
     for (a = dep_ptr[j]; a < dep_ptr[j + 1]; ++a) user_ptr[dep_idx[a] + 1]++;
@@ -453,10 +456,20 @@ int ckm_ref_plan(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx, cons
             EMIT(0, k, r);
             ++r;
           }
-          for (m = 0; m <= dep_ptr[k + 1] - dep_ptr[k]; ++m) {
+          /* Deps[k] in ascending order, then k */
+          deg = dep_ptr[k + 1] - dep_ptr[k];
+          for (m = 0; m < deg; ++m) {
+            int32_t x = dep_idx[dep_ptr[k] + m], y = m;
+            while (y > 0 && order[y - 1] > x) {
+              order[y] = order[y - 1];
+              --y;
+            }
+            order[y] = x;
+          }
+          for (m = 0; m <= deg; ++m) {
             int64_t FREE;
             int32_t b;
-            i = (m < dep_ptr[k + 1] - dep_ptr[k]) ? dep_idx[dep_ptr[k] + m] : k;
+            i = (m < deg) ? order[m] : k;
             FREE = (int64_t)Rt[k] * (1 - (int64_t)((t + 1 < n && i < t + 1) ? S[(int64_t)(t + 1) * n + i] : 0));
             for (b = user_ptr[i]; b < user_ptr[i + 1]; ++b) {
               j = user_idx[b];
@@ -485,5 +498,6 @@ int ckm_ref_plan(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx, cons
   free(user_ptr);
   free(user_idx);
   free(fill);
+  free(order);
   return CKM_REF_OK;
 }

@@ -26,8 +26,10 @@ EXPORTS = (
     "ckm_graph_create", "ckm_graph_destroy", "ckm_graph_num_nodes", "ckm_round_eval",
     "ckm_workspace_size", "ckm_quantize_async", "ckm_evaluate_async", "ckm_select_async",
     "ckm_round_eval_async", "ckm_eval_schedules", "ckm_eval_schedules_async", "ckm_threshold_eval",
-    "ckm_threshold_eval_async", "ckm_last_error",
+    "ckm_threshold_eval_async", "ckm_plan", "ckm_plan_async", "ckm_last_error",
 )
+PLAN_EARLY_FREE = 1
+OP_COMPUTE, OP_DEALLOCATE = 0, 1
 
 
 class CkmError(RuntimeError):
@@ -78,6 +80,10 @@ def lib():
         L.ckm_threshold_eval.restype = C.c_int
         L.ckm_threshold_eval_async.argtypes = [p, p, i64, p, i32, i64, p, p, p, p, p, p, p, p, sz, p]
         L.ckm_threshold_eval_async.restype = C.c_int
+        L.ckm_plan.argtypes = [p, p, p, u32, p, i64, p, p]
+        L.ckm_plan.restype = C.c_int
+        L.ckm_plan_async.argtypes = [p, p, p, u32, p, i64, p, p, p, p, sz, p]
+        L.ckm_plan_async.restype = C.c_int
         L.ckm_last_error.argtypes = []
         L.ckm_last_error.restype = C.c_char_p
         _lib = L
@@ -180,6 +186,33 @@ class Graph:
                                         _np_ptr(peak), _np_ptr(cost), _np_ptr(feas), _np_ptr(bk), _np_ptr(bS),
                                         _np_ptr(bR)))
         return dict(peak=peak, cost=cost, feasible=feas, best_k=int(bk[0]), best_S=bS, best_R=bR)
+
+    def plan(self, S_rows, R_rows, early: bool = False, capacity=None, want_mem: bool = True):
+        """Algorithm 1's execution plan of (S, R) bit rows (ckm_plan): statements
+        [count][4] int32 (op, node, register, stage) and the memory after each.
+        capacity None: ask for the count first."""
+        S = np.ascontiguousarray(S_rows, dtype=np.uint64)
+        R = np.ascontiguousarray(R_rows, dtype=np.uint64)
+        if S.shape != (self.n, self.W) or R.shape != (self.n, self.W):
+            raise ValueError("S and R must have shape [%d][%d]" % (self.n, self.W))
+        flags = PLAN_EARLY_FREE if early else 0
+        cnt = np.zeros(1, np.int64)
+        if capacity is None:
+            _check(lib().ckm_plan(self._h, _np_ptr(S), _np_ptr(R), flags, None, 0, _np_ptr(cnt), None))
+            capacity = int(cnt[0])
+        P = np.zeros((max(int(capacity), 1), 4), np.int32)
+        mem = np.zeros(max(int(capacity), 1), np.int64) if want_mem else None
+        _check(lib().ckm_plan(self._h, _np_ptr(S), _np_ptr(R), flags, _np_ptr(P), int(capacity), _np_ptr(cnt),
+                              _np_ptr(mem)))
+        c = int(cnt[0])
+        return P[:c].copy(), (mem[:c].copy() if want_mem else None)
+
+    def plan_async(self, d_S, d_R, early, d_P, capacity, d_count, d_mem, d_status, work, stream=None):
+        """Device tensors: d_S, d_R int64 [n][W]; d_P int32 [capacity][4] or None."""
+        _check(lib().ckm_plan_async(self._h, _dev_ptr(d_S), _dev_ptr(d_R), PLAN_EARLY_FREE if early else 0,
+                                    _dev_ptr(d_P), int(capacity), _dev_ptr(d_count), _dev_ptr(d_mem),
+                                    _dev_ptr(d_status), _dev_ptr(work), work.numel() * work.element_size(),
+                                    _stream_ptr(stream)))
 
     def eval_schedules(self, S_rows, budget: int, want_rows: bool = True):
         """K given checkpoint matrices as uint64 bit rows [K][n][W] (ckm_eval_schedules)."""

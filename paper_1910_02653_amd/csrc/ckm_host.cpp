@@ -121,6 +121,12 @@ Layout make_layout(int32_t n, int32_t K) {
   const size_t kt = (size_t)std::min<int32_t>(K, CKM_MAX_THRESHOLDS);
   L.thr_sorted_off = off; off = align256(off + kt * sizeof(double));
   L.thr_rank_off = off;   off = align256(off + kt * sizeof(uint32_t));
+  L.plan_cnt_off = off;   off = align256(off + (size_t)n * sizeof(int64_t));
+  L.plan_comp_off = off;  off = align256(off + (size_t)n * sizeof(int64_t));
+  L.plan_err_off = off;   off = align256(off + (size_t)n * sizeof(int32_t));
+  L.plan_pos_off = off;   off = align256(off + (size_t)n * sizeof(int64_t));
+  L.plan_rbase_off = off; off = align256(off + (size_t)n * sizeof(int64_t));
+  L.plan_go_off = off;    off = align256(off + sizeof(int32_t));
   L.total = off;
   return L;
 }
@@ -564,6 +570,98 @@ ckm_status ckm_threshold_eval(const ckm_graph* g, const double* s_frac, int64_t 
     }
     if (st != CKM_OK) break;
     if ((e = hipStreamSynchronize(stream)) != hipSuccess) st = fail_hip(e, "hipStreamSynchronize");
+  } while (false);
+  if (stream) {
+    (void)hipStreamSynchronize(stream);
+    (void)hipStreamDestroy(stream);
+  }
+  (void)hipFree(d);
+  return st;
+}
+
+ckm_status ckm_plan_async(const ckm_graph* g, const uint64_t* d_S, const uint64_t* d_R, uint32_t flags,
+                          ckm_stmt* d_P, int64_t capacity, int64_t* d_count, int64_t* d_mem, int32_t* d_status,
+                          void* d_work, size_t work_bytes, void* stream) {
+  Layout L;
+  ckm_status st = check_work(g, 1, d_work, work_bytes, &L);
+  if (st != CKM_OK) return st;
+  if (!d_S || !d_R || !d_count) return fail(CKM_E_INVALID_ARG, "NULL S, R or count");
+  if (flags & ~(uint32_t)CKM_PLAN_EARLY_FREE) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
+  if (capacity < 0) return fail(CKM_E_INVALID_ARG, "capacity = %lld < 0", (long long)capacity);
+  DeviceGuard dg(g->device);
+  hipError_t e = ckm::launch_plan(*g, L, d_S, d_R, flags, reinterpret_cast<int32_t*>(d_P), capacity, d_count,
+                                  d_P ? d_mem : nullptr, d_status, static_cast<char*>(d_work),
+                                  static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CKM_OK : fail_hip(e, "plan launch");
+}
+
+ckm_status ckm_plan(const ckm_graph* g, const uint64_t* S, const uint64_t* R, uint32_t flags, ckm_stmt* P,
+                    int64_t capacity, int64_t* count, int64_t* mem) {
+  if (!g) return fail(CKM_E_INVALID_ARG, "graph is NULL");
+  if (!S || !R || !count) return fail(CKM_E_INVALID_ARG, "NULL S, R or count");
+  if (flags & ~(uint32_t)CKM_PLAN_EARLY_FREE) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
+  if (P && capacity < 0) return fail(CKM_E_INVALID_ARG, "capacity = %lld < 0", (long long)capacity);
+  if (!P) capacity = 0;
+  const int32_t n = g->n;
+  DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
+  const Layout L = ckm::make_layout(n, 1);
+  const size_t rows_bytes = (size_t)n * ((n + 63) / 64) * sizeof(uint64_t);
+  size_t off = 0;
+  const size_t o_s = off;   off = align256(off + rows_bytes);
+  const size_t o_r = off;   off = align256(off + rows_bytes);
+  const size_t o_cnt = off; off = align256(off + 8);
+  const size_t o_st = off;  off = align256(off + 8);
+  const size_t o_w = off;   off = align256(off + L.total);
+  const size_t o_p = off;   off = align256(off + (size_t)capacity * sizeof(ckm_stmt));
+  const size_t o_m = off;   off = align256(off + (mem ? (size_t)capacity * sizeof(int64_t) : 0));
+  char* d = nullptr;
+  hipError_t e = hipMalloc(&d, off);
+  if (e != hipSuccess)
+    return e == hipErrorOutOfMemory ? fail(CKM_E_NOMEM, "hipMalloc of %zu bytes failed", off)
+                                    : fail_hip(e, "hipMalloc");
+  hipStream_t stream = nullptr;
+  ckm_status st = CKM_OK;
+  int32_t status_dev = 0;
+  int64_t total = 0;
+  do {
+    if ((e = hipStreamCreateWithFlags(&stream, hipStreamNonBlocking)) != hipSuccess) {
+      st = fail_hip(e, "hipStreamCreate");
+      break;
+    }
+    if ((e = hipMemcpyAsync(d + o_s, S, rows_bytes, hipMemcpyHostToDevice, stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(d + o_r, R, rows_bytes, hipMemcpyHostToDevice, stream)) != hipSuccess) {
+      st = fail_hip(e, "hipMemcpy S or R");
+      break;
+    }
+    st = ckm_plan_async(g, reinterpret_cast<const uint64_t*>(d + o_s), reinterpret_cast<const uint64_t*>(d + o_r),
+                        flags, P ? reinterpret_cast<ckm_stmt*>(d + o_p) : nullptr, capacity,
+                        reinterpret_cast<int64_t*>(d + o_cnt), mem ? reinterpret_cast<int64_t*>(d + o_m) : nullptr,
+                        reinterpret_cast<int32_t*>(d + o_st), d + o_w, L.total, stream);
+    if (st != CKM_OK) break;
+    if ((e = hipMemcpyAsync(&total, d + o_cnt, 8, hipMemcpyDeviceToHost, stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(&status_dev, d + o_st, 4, hipMemcpyDeviceToHost, stream)) != hipSuccess ||
+        (e = hipStreamSynchronize(stream)) != hipSuccess) {
+      st = fail_hip(e, "hipMemcpy count");
+      break;
+    }
+    *count = total;
+    if (status_dev != CKM_OK) {
+      st = (P && total > capacity) ? fail(CKM_E_INVALID_ARG, "plan has %lld statements, capacity %lld",
+                                          (long long)total, (long long)capacity)
+                                   : fail(CKM_E_INVALID_ARG, "(S, R) violates (4a), (1b), (1c) or S & R = 0");
+      break;
+    }
+    if (P && total > 0) {
+      if ((e = hipMemcpyAsync(P, d + o_p, (size_t)total * sizeof(ckm_stmt), hipMemcpyDeviceToHost, stream)) !=
+              hipSuccess ||
+          (mem && (e = hipMemcpyAsync(mem, d + o_m, (size_t)total * sizeof(int64_t), hipMemcpyDeviceToHost,
+                                      stream)) != hipSuccess) ||
+          (e = hipStreamSynchronize(stream)) != hipSuccess) {
+        st = fail_hip(e, "hipMemcpy plan");
+        break;
+      }
+    }
   } while (false);
   if (stream) {
     (void)hipStreamSynchronize(stream);

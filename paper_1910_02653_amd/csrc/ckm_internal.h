@@ -32,6 +32,7 @@ namespace ckm {
 
 constexpr int kWave = 64;
 constexpr int kNodeRecBytes = 256;
+constexpr int kMaxNodesWords = CKM_MAX_NODES / 32;
 
 // Where the evaluate kernel's S rows come from.
 enum : int {
@@ -57,7 +58,11 @@ struct Layout {
   int32_t reduce_blocks = 0;
   // hdr: int32 number of work items (rows of the partial arrays) of the last evaluate
   size_t hdr_off = 0, q_off = 0, det_off = 0, nan_off = 0, part_peak_off = 0, part_cost_off = 0,
-         best_off = 0, srows_off = 0, thr_sorted_off = 0, thr_rank_off = 0, total = 0;
+         best_off = 0, srows_off = 0, thr_sorted_off = 0, thr_rank_off = 0,
+         // execution plans: per-stage statement and compute counts, check
+         // flags, first statement and first register, and the go flag
+         plan_cnt_off = 0, plan_comp_off = 0, plan_err_off = 0, plan_pos_off = 0, plan_rbase_off = 0,
+         plan_go_off = 0, total = 0;
 };
 
 Layout make_layout(int32_t n, int32_t K);
@@ -82,6 +87,11 @@ hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_
 // keys of S* in place of the quantized thresholds q.
 hipError_t launch_threshold_keys(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,
                                  const double* d_p, int32_t K, char* work, hipStream_t stream);
+// Execution plan of (S, R) (bit rows of row_words 32-bit words): counts,
+// checks and prefix sums, then the statements when d_P is not null.
+hipError_t launch_plan(const ckm_graph& g, const Layout& L, const uint64_t* d_S, const uint64_t* d_R,
+                       uint32_t flags, int32_t* d_P, int64_t capacity, int64_t* d_count, int64_t* d_mem,
+                       int32_t* d_status, char* work, hipStream_t stream);
 // src: one of kSrcRound, kSrcUser, kSrcThreshold. s_user: for kSrcUser, K
 // caller-supplied S matrices ([K][n][row_words] 32-bit words).
 hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,

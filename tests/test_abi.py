@@ -103,5 +103,7 @@ def test_null_arguments_rejected():
     assert L.ckm_threshold_eval(None, None, 4, None, 4, 0, None, None, None, None, None, None) == ckm.E_INVALID_ARG
     assert L.ckm_threshold_eval_async(None, None, 4, None, 4, 0, None, None, None, None, None, None, None, None, 0,
                                       None) == ckm.E_INVALID_ARG
+    assert L.ckm_plan(None, None, None, 0, None, 0, None, None) == ckm.E_INVALID_ARG
+    assert L.ckm_plan_async(None, None, None, 0, None, 0, None, None, None, None, 0, None) == ckm.E_INVALID_ARG
     assert L.ckm_graph_num_nodes(None) == -1
     L.ckm_graph_destroy(None)
