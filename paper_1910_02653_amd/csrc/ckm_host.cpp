@@ -127,6 +127,8 @@ Layout make_layout(int32_t n, int32_t K) {
   L.plan_pos_off = off;   off = align256(off + (size_t)n * sizeof(int64_t));
   L.plan_rbase_off = off; off = align256(off + (size_t)n * sizeof(int64_t));
   L.plan_go_off = off;    off = align256(off + sizeof(int32_t));
+  L.plan_rt_off = off;    off = align256(off + (size_t)n * ((n + 31) / 32) * sizeof(uint32_t));
+  L.plan_rpre_off = off;  off = align256(off + (size_t)n * ckm::kMaxNodesWords * sizeof(int32_t));
   L.total = off;
   return L;
 }

@@ -62,7 +62,9 @@ struct Layout {
          // execution plans: per-stage statement and compute counts, check
          // flags, first statement and first register, and the go flag
          plan_cnt_off = 0, plan_comp_off = 0, plan_err_off = 0, plan_pos_off = 0, plan_rbase_off = 0,
-         plan_go_off = 0, total = 0;
+         plan_go_off = 0,
+         // R transposed (n columns of ceil(n/32) words) and per-row word ranks
+         plan_rt_off = 0, plan_rpre_off = 0, total = 0;
 };
 
 Layout make_layout(int32_t n, int32_t K);

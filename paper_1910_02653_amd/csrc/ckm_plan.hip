@@ -87,7 +87,8 @@ __global__ void __launch_bounds__(kPlanWave) ckm_plan_count_kernel(int32_t n, in
                                                                    const int32_t* __restrict__ dep_idx,
                                                                    int64_t* __restrict__ cnt,
                                                                    int64_t* __restrict__ comp,
-                                                                   int32_t* __restrict__ err) {
+                                                                   int32_t* __restrict__ err,
+                                                                   int32_t* __restrict__ rpre) {
   const int t = blockIdx.x;
   const int lane = threadIdx.x;
   const int nwt = (t >> 5) + 1;
@@ -112,6 +113,17 @@ __global__ void __launch_bounds__(kPlanWave) ckm_plan_count_kernel(int32_t n, in
         const uint32_t have = s_word(S, rw, t, i >> 5) | r_word(R, rw, t, i >> 5);
         bad |= bit_of(have, i) ^ 1u;
       }
+    }
+  }
+  // computes of R_t before each word, for the registers of later stages
+  {
+    int64_t carry = 0;
+    for (int w0 = 0; w0 < nwt; w0 += kPlanWave) {
+      const int w = w0 + lane;
+      const int64_t pc = w < nwt ? __popc(r_word(R, rw, t, w)) : 0;
+      const int64_t inc = wave_scan_i64(pc, lane);
+      if (w < nwt) rpre[(size_t)t * kMaxNodesWords + w] = (int32_t)(carry + inc - pc);
+      carry += __shfl(inc, kPlanWave - 1);
     }
   }
   c = wave_sum_i64(c);
@@ -178,9 +190,12 @@ __global__ void __launch_bounds__(kScanThreads) ckm_plan_scan_kernel(
 struct PlanArgs {
   int32_t n, rw;
   int32_t early;
+  int32_t rtw;                       // words per column of RT: ceil(n / 32)
   double base;                       // M_in + 2 M_param
   const uint32_t* S;
   const uint32_t* R;
+  const uint32_t* RT;                // R transposed: bit s of RT[i] = R[s][i]
+  const int32_t* rpre;               // [n][kMaxNodesWords]: computes in row s before word w
   const int32_t* dep_ptr;
   const int32_t* dep_idx;
   const int32_t* user_ptr;
@@ -207,39 +222,78 @@ __device__ __forceinline__ void put_stmt(const PlanArgs& a, int64_t s, int op, i
   if (a.mem) a.mem[s] = (int64_t)mem_after;
 }
 
-// Register of value i live in stage t: computed in this stage, or the
-// register of the stage s < t that computed the checkpoint: the last stage
-// s <= t with S[s][i] = 0 (constraint (1c) then has R[s][i] = 1).
-__device__ int64_t reg_of(const PlanArgs& a, int t, int i, const uint32_t* rt_lds, const int32_t* wpre) {
+// Register of value i live in stage t: computed in this stage, or else kept
+// from the last stage s < t that computed it (R[s][i] = 1; no value is both
+// kept and recomputed, so the kept copy is that one). s is the highest set
+// bit below t of column i of R.
+__device__ int64_t reg_of(const PlanArgs& a, int t, int i, const uint32_t* rt_l, const int32_t* wpre) {
   const int w = i >> 5;
   const uint32_t below = (1u << (i & 31)) - 1u;
-  if (bit_of(rt_lds[w], i)) return (int64_t)wpre[w] + __popc(rt_lds[w] & below) + a.rbase[t];
-  int s = t - 1;
-  while (s > i && bit_of(s_word(a.S, a.rw, s, w), i)) --s;
-  int64_t rank = 0;
-  for (int v = 0; v < w; ++v) rank += __popc(r_word(a.R, a.rw, s, v));
-  rank += __popc(r_word(a.R, a.rw, s, w) & below);
-  return a.rbase[s] + rank;
+  if (bit_of(rt_l[w], i)) return a.rbase[t] + wpre[w] + __popc(rt_l[w] & below);
+  const uint32_t* col = a.RT + (size_t)i * a.rtw;
+  int sw = (t - 1) >> 5;
+  const int top = (t - 1) & 31;
+  uint32_t m = col[sw] & (top == 31 ? ~0u : ((2u << top) - 1u));
+  while (m == 0u && sw > 0) m = col[--sw];
+  if (m == 0u) return -1;   // unreachable for a checked schedule
+  const int s = 32 * sw + 31 - __clz(m);
+  return a.rbase[s] + a.rpre[(size_t)s * kMaxNodesWords + w] + __popc(r_word(a.R, a.rw, s, w) & below);
 }
 
-// Stage t: one wave. LDS holds the stage's rows, the per-word compute counts
-// of R_t and each node's free point.
-__global__ void __launch_bounds__(kPlanWave) ckm_plan_emit_kernel(PlanArgs a) {
+// Column words of RT: block (node group of 64, stage word); lane = node.
+__global__ void __launch_bounds__(kPlanWave) ckm_plan_transpose_kernel(int32_t n, int32_t rw,
+                                                                       const uint32_t* __restrict__ R,
+                                                                       int32_t rtw, uint32_t* __restrict__ RT) {
+  const int i = blockIdx.x * kPlanWave + threadIdx.x;
+  const int sw = blockIdx.y;
+  uint32_t word = 0;
+  for (int q = 0; q < 32; ++q) {
+    const int s = 32 * sw + q;
+    if (s < n && i < n) word |= bit_of(r_word(R, rw, s, i >> 5), i) << q;
+  }
+  if (i < n) RT[(size_t)i * rtw + sw] = word;
+}
+
+constexpr int kMaxChunks = CKM_MAX_NODES / kPlanWave;
+
+// Stage t = n - 1 - blockIdx.x (longest first): kEmitWaves waves (4, or 16
+// for large graphs, whose LDS allows only a few blocks per CU). Node k's
+// statements are its compute and the deallocations whose free point is k;
+// an unused checkpoint's deallocation sits at the stage start or end.
+//   1. free point of every node (LDS), unused checkpoints per 64 nodes, the
+//      stage's starting memory U_{t,0};
+//   2. per node: statement count and memory change (LDS), per 64 nodes the
+//      totals;
+//   3. one wave: offsets of every 64-node group (positions and memory);
+//   4. every wave writes the statements of its groups.
+// Dynamic LDS: n doubles (memory change), then n + n int32 (free point,
+// statement count).
+template <int kEmitWaves>
+__global__ void __launch_bounds__(kEmitWaves * kPlanWave) ckm_plan_emit_kernel(PlanArgs a) {
+  constexpr int kEmitThreads = kEmitWaves * kPlanWave;
+  extern __shared__ double dyn[];
   __shared__ uint32_t st_l[kMaxNodesWords], rt_l[kMaxNodesWords], sn_l[kMaxNodesWords];
   __shared__ int32_t wpre[kMaxNodesWords];
-  __shared__ int32_t fpt[CKM_MAX_NODES];
-  const int t = blockIdx.x;
-  const int lane = threadIdx.x;
+  __shared__ int64_t ch_cnt[kMaxChunks], uc_cnt[kMaxChunks];
+  __shared__ double ch_mem[kMaxChunks], uc_mem[kMaxChunks];
+  __shared__ double kept_part[kEmitWaves];
+  double* cmem = dyn;
+  int32_t* fpt = reinterpret_cast<int32_t*>(dyn + a.n);
+  int32_t* ccnt = fpt + a.n;
+  const int t = a.n - 1 - (int)blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kPlanWave - 1);
+  const int wave = tid / kPlanWave;
   if (a.go[0] == 0) return;
   const int nwt = (t >> 5) + 1;
-  for (int w = lane; w < nwt; w += kPlanWave) {
+  const int nc = (t >> 6) + 1;
+  for (int w = tid; w < nwt; w += kEmitThreads) {
     st_l[w] = s_word(a.S, a.rw, t, w);
     rt_l[w] = r_word(a.R, a.rw, t, w);
     sn_l[w] = (t + 1 < a.n) ? s_word(a.S, a.rw, t + 1, w) : 0u;
   }
   __syncthreads();
-  // computes in the words before w (nwt <= 128: two rounds of 64 lanes)
-  {
+  if (wave == 0) {   // computes in R_t before each word (<= 128 words)
     int64_t carry = 0;
     for (int w0 = 0; w0 < nwt; w0 += kPlanWave) {
       const int w = w0 + lane;
@@ -249,75 +303,111 @@ __global__ void __launch_bounds__(kPlanWave) ckm_plan_emit_kernel(PlanArgs a) {
       carry += __shfl(inc, kPlanWave - 1);
     }
   }
-  // free point of each node and the stage's starting memory
+  // 1. free points; wave w owns the 64-node groups w, w + 4, ...
   double kept_bytes = 0.0;
-  for (int i = lane; i <= t; i += kPlanWave) {
-    const uint32_t si = bit_of(st_l[i >> 5], i), ri = bit_of(rt_l[i >> 5], i);
+  for (int c = wave; c < nc; c += kEmitWaves) {
+    const int i = 64 * c + lane;
     int f = kFreeNone;
-    if ((si | ri) && !bit_of(sn_l[i >> 5], i)) {
-      f = ri ? i : kFreeUnused;
-      for (int e = a.user_ptr[i + 1] - 1; e >= a.user_ptr[i]; --e) {
-        const int j = a.user_idx[e];
-        if (j <= t && bit_of(rt_l[j >> 5], j)) {
-          f = j;
-          break;
+    double mi = 0.0;
+    if (i <= t) {
+      const uint32_t si = bit_of(st_l[i >> 5], i), ri = bit_of(rt_l[i >> 5], i);
+      mi = a.M[i];
+      if ((si | ri) && !bit_of(sn_l[i >> 5], i)) {
+        f = ri ? i : kFreeUnused;
+        for (int e = a.user_ptr[i + 1] - 1; e >= a.user_ptr[i]; --e) {
+          const int j = a.user_idx[e];
+          if (j <= t && bit_of(rt_l[j >> 5], j)) {
+            f = j;
+            break;
+          }
         }
       }
+      fpt[i] = f;
+      if (si) kept_bytes += mi;
     }
-    fpt[i] = f;
-    if (si) kept_bytes += a.M[i];
+    const bool un = f == kFreeUnused;
+    const double su = wave_sum_f64(un ? -mi : 0.0);
+    const uint64_t um = __ballot(un);
+    if (lane == 0) {
+      uc_cnt[c] = __popcll(um);
+      uc_mem[c] = su;
+    }
   }
+  kept_bytes = wave_sum_f64(kept_bytes);
+  if (lane == 0) kept_part[wave] = kept_bytes;
   __syncthreads();
-  double u = a.base + wave_sum_f64(kept_bytes);   // U_{t,0}: exact integer
-  int64_t pos = a.off[t];
-
-  // unused checkpoints, ascending; at the start (early) or at the end
-  auto unused_pass = [&]() {
-    for (int i0 = 0; i0 <= t; i0 += kPlanWave) {
-      const int i = i0 + lane;
-      const bool fl = i <= t && fpt[i] == kFreeUnused;
-      const uint64_t mask = __ballot(fl);
-      if (!mask) continue;
-      const int idx = __popcll(mask & ((1ull << lane) - 1ull));
-      const double d = fl ? -a.M[i] : 0.0;
-      const double incl = wave_scan_f64(d, lane);
-      if (fl) put_stmt(a, pos + idx, 1, i, reg_of(a, t, i, rt_l, wpre), t, u + incl);
-      pos += __popcll(mask);
-      u += __shfl(incl, kPlanWave - 1);
-    }
-  };
-  if (a.early) unused_pass();
-
-  // the scan of Algorithm 1, 64 nodes at a time
-  for (int k0 = 0; k0 <= t; k0 += kPlanWave) {
-    const int k = k0 + lane;
-    int64_t c = 0;
+  // 2. per node: statements and memory change
+  for (int c = wave; c < nc; c += kEmitWaves) {
+    const int k = 64 * c + lane;
+    int64_t cn = 0;
     double d = 0.0;
-    const bool in = k <= t;
-    const bool rk = in && bit_of(rt_l[k >> 5], k);
-    if (in) {
-      if (rk) {
-        c = 1;
+    if (k <= t) {
+      if (bit_of(rt_l[k >> 5], k)) {
+        cn = 1;
         d = a.M[k];
       }
       for (int e = a.dep_ptr[k]; e < a.dep_ptr[k + 1]; ++e) {
         const int i = a.dep_idx[e];
         if (fpt[i] == k) {
-          ++c;
+          ++cn;
           d -= a.M[i];
         }
       }
       if (fpt[k] == k) {
-        ++c;
+        ++cn;
         d -= a.M[k];
       }
+      ccnt[k] = (int32_t)cn;
+      cmem[k] = d;
     }
-    const int64_t cinc = wave_scan_i64(c, lane);
+    cn = wave_sum_i64(cn);
+    d = wave_sum_f64(d);
+    if (lane == 0) {
+      ch_cnt[c] = cn;
+      ch_mem[c] = d;
+    }
+  }
+  __syncthreads();
+  // 3. offsets of the groups (nc <= 64: one wave)
+  if (wave == 0) {
+    double u0 = a.base;
+    for (int w = 0; w < kEmitWaves; ++w) u0 += kept_part[w];
+    const bool in = lane < nc;
+    const int64_t cn = in ? ch_cnt[lane] : 0, un = in ? uc_cnt[lane] : 0;
+    const double dm = in ? ch_mem[lane] : 0.0, um = in ? uc_mem[lane] : 0.0;
+    const int64_t cn_inc = wave_scan_i64(cn, lane), un_inc = wave_scan_i64(un, lane);
+    const double dm_inc = wave_scan_f64(dm, lane), um_inc = wave_scan_f64(um, lane);
+    const int64_t node_total = __shfl(cn_inc, kPlanWave - 1), un_total = __shfl(un_inc, kPlanWave - 1);
+    const double node_mem = __shfl(dm_inc, kPlanWave - 1), un_mem = __shfl(um_inc, kPlanWave - 1);
+    const int64_t o = a.off[t];
+    int64_t node_pos = o, un_pos = o + node_total;
+    double node_mb = u0, un_mb = u0 + node_mem;
+    if (a.early) {
+      un_pos = o;
+      un_mb = u0;
+      node_pos = o + un_total;
+      node_mb = u0 + un_mem;
+    }
+    if (in) {
+      ch_cnt[lane] = node_pos + cn_inc - cn;
+      ch_mem[lane] = node_mb + dm_inc - dm;
+      uc_cnt[lane] = un_pos + un_inc - un;
+      uc_mem[lane] = un_mb + um_inc - um;
+    }
+  }
+  __syncthreads();
+  // 4. statements
+  for (int c = wave; c < nc; c += kEmitWaves) {
+    const int k = 64 * c + lane;
+    const bool in = k <= t;
+    const int64_t cn = in ? ccnt[k] : 0;
+    const double d = in ? cmem[k] : 0.0;
+    const int64_t cinc = wave_scan_i64(cn, lane);
     const double dinc = wave_scan_f64(d, lane);
-    int64_t s = pos + cinc - c;
-    double mu = u + dinc - d;      // memory before this node's statements
-    if (c) {
-      if (rk) {
+    int64_t s = ch_cnt[c] + cinc - cn;
+    double mu = ch_mem[c] + dinc - d;   // memory before node k's statements
+    if (cn) {
+      if (bit_of(rt_l[k >> 5], k)) {
         mu += a.M[k];
         const int64_t reg = a.rbase[t] + wpre[k >> 5] + __popc(rt_l[k >> 5] & ((1u << (k & 31)) - 1u));
         put_stmt(a, s++, 0, k, reg, t, mu);
@@ -334,10 +424,17 @@ __global__ void __launch_bounds__(kPlanWave) ckm_plan_emit_kernel(PlanArgs a) {
         put_stmt(a, s++, 1, k, reg_of(a, t, k, rt_l, wpre), t, mu);
       }
     }
-    pos += __shfl(cinc, kPlanWave - 1);
-    u += __shfl(dinc, kPlanWave - 1);
+    // unused checkpoints of this group, ascending
+    const bool un = in && fpt[k] == kFreeUnused;
+    const uint64_t um = __ballot(un);
+    if (um) {
+      const double du = un ? -a.M[k] : 0.0;
+      const double uinc = wave_scan_f64(du, lane);
+      if (un)
+        put_stmt(a, uc_cnt[c] + __popcll(um & ((1ull << lane) - 1ull)), 1, k, reg_of(a, t, k, rt_l, wpre), t,
+                 uc_mem[c] + uinc);
+    }
   }
-  if (!a.early) unused_pass();
 }
 
 template <typename T>
@@ -356,19 +453,27 @@ hipError_t launch_plan(const ckm_graph& g, const Layout& L, const uint64_t* d_S,
   int64_t* off = at<int64_t>(work, L.plan_pos_off);
   int64_t* rbase = at<int64_t>(work, L.plan_rbase_off);
   int32_t* go = at<int32_t>(work, L.plan_go_off);
+  int32_t* rpre = at<int32_t>(work, L.plan_rpre_off);
+  uint32_t* RT = at<uint32_t>(work, L.plan_rt_off);
+  const int32_t rtw = (g.n + 31) / 32;
   hipLaunchKernelGGL(ckm_plan_count_kernel, dim3(g.n), dim3(kPlanWave), 0, stream, g.n, L.row_words, S, R,
-                     g.d_dep_ptr, g.d_dep_idx, cnt, comp, err);
+                     g.d_dep_ptr, g.d_dep_idx, cnt, comp, err, rpre);
   hipLaunchKernelGGL(ckm_plan_scan_kernel, dim3(1), dim3(kScanThreads), 0, stream, g.n,
                      static_cast<const int64_t*>(cnt), static_cast<const int64_t*>(comp),
                      static_cast<const int32_t*>(err), off, rbase, capacity, d_P ? 1 : 0, d_count, d_status, go);
   if (d_P) {
+    hipLaunchKernelGGL(ckm_plan_transpose_kernel, dim3((g.n + kPlanWave - 1) / kPlanWave, rtw), dim3(kPlanWave),
+                       0, stream, g.n, L.row_words, R, rtw, RT);
     PlanArgs a;
     a.n = g.n;
     a.rw = L.row_words;
     a.early = (flags & CKM_PLAN_EARLY_FREE) ? 1 : 0;
+    a.rtw = rtw;
     a.base = g.base;
     a.S = S;
     a.R = R;
+    a.RT = RT;
+    a.rpre = rpre;
     a.dep_ptr = g.d_dep_ptr;
     a.dep_idx = g.d_dep_idx;
     a.user_ptr = g.d_user_ptr;
@@ -380,7 +485,12 @@ hipError_t launch_plan(const ckm_graph& g, const Layout& L, const uint64_t* d_S,
     a.P = d_P;
     a.mem = d_mem;
     a.capacity = capacity;
-    hipLaunchKernelGGL(ckm_plan_emit_kernel, dim3(g.n), dim3(kPlanWave), 0, stream, a);
+    const size_t lds = (size_t)g.n * (sizeof(double) + 2 * sizeof(int32_t));
+    const bool wide = g.n > 1024;
+    void (*fn)(PlanArgs) = wide ? ckm_plan_emit_kernel<16> : ckm_plan_emit_kernel<4>;
+    hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fn, dim3(g.n), dim3((wide ? 16 : 4) * kPlanWave), lds, stream, a);
   }
   return hipGetLastError();
 }
