@@ -14,6 +14,7 @@
 // integer and the result is identical to int64 arithmetic in any order.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <climits>
 #include <cstddef>
 #include <cmath>
@@ -190,41 +191,33 @@ __device__ __forceinline__ uint32_t threshold_word(QPtr qrow, int w, int r, uint
 
 // ---------------------------------------------------------------------------
 // Per-node record, read once per node visit. Masks are relative to the node
-// v: bit d <-> node v + 1 + d, d < 64. A "ref" locates one bit of a row in
-// LDS: (word * 256) << 16 | bit, i.e. the byte offset of the word within a
-// row buffer (lane 0) in the high half and the bit position in the low half.
-struct DepSlot {
-  uint32_t s1_ref;        // the dep i in the next-stage checkpoint row
-  uint32_t fl_ref;        // the user of i beyond v + 64 in the R row, or none (node n)
-  uint32_t lmask_lo;      // users u of i with v < u <= v + 32
-  uint32_t lmask_hi;      //                  v + 32 < u <= v + 64
-  double M;               // M_i
-};
+// v: bit d <-> node v + 1 + d, d < 64. A reference locates one bit of a row:
+// its word index (8 bits, packed four to a dword) and its bit position (5
+// bits, packed six to a dword). The references are: the user of v beyond
+// v + 64 in the R row (fu), and per dependency slot the user of the dep
+// beyond v + 64 in the R row (fl) and the dep in the next-stage checkpoint
+// row (s1); absent ones point at node n, whose bit no row ever sets.
 constexpr int kRecDeps = 4;
-constexpr uint32_t kRecSlow = 1u << 31;   // node does not fit: use the CSR lists
 struct NodeRec {
-  double M, C;            // M_v, C_v
-  uint32_t umask_lo;      // users u of v with u <= v + 32
-  uint32_t umask_hi;      //                  v + 32 < u <= v + 64
-  uint32_t fu_ref;        // the user of v beyond v + 64 in the R row, or none (node n)
-  uint32_t info;          // number of deps (bits 0-2) | kRecSlow
-  DepSlot dep[kRecDeps];
-  // the bit positions of the references, five bits each: fu, then per slot
-  // s1 and fl (slots 0-1 and s1 of slot 2 in bits0, the rest in bits1)
-  uint32_t bits0, bits1;
+  double M, C;              // M_v, C_v
+  uint32_t umask_lo;        // users u of v with u <= v + 32
+  uint32_t umask_hi;        //                  v + 32 < u <= v + 64
+  uint32_t refs0;           // word indices: fu | fl0 << 8 | s1_0 << 16 | fl1 << 24
+  uint32_t refs1;           // s1_1 word | deps << 8 | slow << 11 | bit positions 6-8 at 12, 17, 22
+  uint32_t bits0;           // bit positions 0-5 (fu, s1_0, fl0, s1_1, fl1, s1_2) | min(deps, 3) << 30,
+                            // or 3 << 30 for a node outside the format
+  uint32_t lm[2 * kRecDeps];  // per slot: users u of the dep with v < u <= v + 32, then v + 32 < u <= v + 64
+  uint32_t refs2;           // word indices: fl2 | s1_2 << 8 | fl3 << 16 | s1_3 << 24
+  double dM[kRecDeps];      // M of each dependency slot
+  uint32_t pad0[2];
   // fp64 operands again, read by two wave-uniform 16-byte loads: M_v, C_v,
   // and the M of dependency slots 0 and 1
   double mc[2], dm01[2];
-  uint32_t pad[22];       // one dword per lane of a 64-lane load
+  uint32_t pad[28];         // one dword per lane of a 64-lane load
 };
 static_assert(sizeof(NodeRec) == kNodeRecBytes, "node record layout");
-
-__host__ __device__ __forceinline__ uint32_t make_ref(int node) {
-  return ((uint32_t)(node >> 5) * 256u) << 16 | (uint32_t)(node & 31);
-}
-// "No node": the bit of node n, which no row ever sets (rows hold bits of
-// nodes below their stage, and stages are < n).
-__host__ __device__ __forceinline__ uint32_t zero_ref(int n) { return make_ref(n); }
+static_assert(offsetof(NodeRec, mc) % 16 == 0 && offsetof(NodeRec, dm01) % 16 == 0, "16-byte loads");
+constexpr uint32_t kRefsSlow = 1u << 11;   // refs1: node does not fit, use the CSR lists
 
 __device__ __forceinline__ double dbl(uint32_t lo, uint32_t hi) {
   return __hiloint2double((int)hi, (int)lo);
@@ -252,23 +245,24 @@ struct RecRegs {
   __device__ double dM01(int s) const { return s == 0 ? dbl(dm.x, dm.y) : dbl(dm.z, dm.w); }
   __device__ uint32_t umask_lo() const { return get(4); }
   __device__ uint32_t umask_hi() const { return get(5); }
-  __device__ uint32_t fu_ref() const { return get(6); }
-  __device__ uint32_t info() const { return get(7); }
-  __device__ uint32_t s1_ref(int s) const { return get(8 + 6 * s); }
-  __device__ uint32_t fl_ref(int s) const { return get(9 + 6 * s); }
-  __device__ uint32_t lm_lo(int s) const { return get(10 + 6 * s); }
-  __device__ uint32_t lm_hi(int s) const { return get(11 + 6 * s); }
-  __device__ double dM(int s) const { return dbl(get(12 + 6 * s), get(13 + 6 * s)); }
-  __device__ uint32_t bits0() const { return get(32); }
-  __device__ uint32_t bits1() const { return get(33); }
+  __device__ uint32_t refs0() const { return get(6); }
+  __device__ uint32_t refs1() const { return get(7); }
+  __device__ uint32_t bits0() const { return get(8); }
+  __device__ uint32_t lm_lo(int s) const { return get(9 + 2 * s); }
+  __device__ uint32_t lm_hi(int s) const { return get(10 + 2 * s); }
+  __device__ uint32_t refs2() const { return get(17); }
+  __device__ double dM(int s) const { return dbl(get(18 + 2 * s), get(19 + 2 * s)); }
 };
 
 // Bit position k of a record (0: fu; 1 + 2s: s1 of slot s; 2 + 2s: fl of
-// slot s) from its two packed dwords; only the low five bits of the result
-// matter to the bit-field extracts that use it.
-__device__ __forceinline__ uint32_t bitpos(uint32_t b0, uint32_t b1, int k) {
-  return k < 6 ? (b0 >> (5 * k)) : (b1 >> (5 * (k - 6)));
+// slot s) from bits0 and refs1; only the low five bits of the result matter
+// to the bit-field extracts that use it.
+__device__ __forceinline__ uint32_t bitpos(uint32_t b0, uint32_t refs1, int k) {
+  return k < 6 ? (b0 >> (5 * k)) : (refs1 >> (12 + 5 * (k - 6)));
 }
+
+// Word index of byte j of a packed dword of word indices.
+__device__ __forceinline__ uint32_t word_at(uint32_t refs, int j) { return (refs >> (8 * j)) & 0xFFu; }
 
 __device__ __forceinline__ void load_rec(RecRegs& r, const uint4* __restrict__ recs, int v) {
   // wave-uniform record base in scalar registers, one dword per lane
@@ -336,11 +330,8 @@ __device__ __forceinline__ void item_range(const EvalArgs& a, int item, int& t0,
 struct Row {
   char* base;  // buffer start + 4 * lane
   __device__ uint32_t& word(int w) const { return *reinterpret_cast<uint32_t*>(base + w * 256); }
-  __device__ uint32_t at_ref(uint32_t ref) const {
-    return *reinterpret_cast<const uint32_t*>(base + (ref >> 16));
-  }
-  __device__ uint32_t bit_ref(uint32_t ref) const {  // bit position: low 5 bits of ref
-    return __builtin_amdgcn_ubfe(at_ref(ref), ref, 1);
+  __device__ uint32_t at_word(uint32_t w) const {  // wave-uniform word index
+    return *reinterpret_cast<const uint32_t*>(base + (w << 8));
   }
 };
 
@@ -361,7 +352,7 @@ struct RowReg {
     __device__ operator uint32_t() const { return v[i]; }
   };
   __device__ WordRef word(int i) { return WordRef{w, i}; }
-  __device__ uint32_t at_ref(uint32_t ref) const { return w[ref >> 24]; }  // word index of the ref
+  __device__ uint32_t at_word(uint32_t i) const { return w[i]; }  // wave-uniform word index
 };
 
 __device__ __forceinline__ uint32_t bit(uint32_t word, int pos) { return (word >> pos) & 1u; }
@@ -455,25 +446,26 @@ __device__ __forceinline__ void pin_s(uint32_t a, uint32_t b, uint32_t c) { asm 
 // during the stage).
 template <typename RowB>
 __device__ __forceinline__ void issue_reads(const RecRegs& rec, Row A, RowB& B, LdsVals& L) {
-  const uint32_t info = rec.info();
-  const uint32_t fu = rec.fu_ref(), fl0 = rec.fl_ref(0), s10 = rec.s1_ref(0);
-  const uint32_t fl1 = rec.fl_ref(1), s11 = rec.s1_ref(1);
+  const uint32_t r0 = rec.refs0(), r1 = rec.refs1();
+  const uint32_t fu = word_at(r0, 0), fl0 = word_at(r0, 1), s10 = word_at(r0, 2);
+  const uint32_t fl1 = word_at(r0, 3), s11 = word_at(r1, 0);
   pin_s(fu, fl0, s10);
-  pin_s(fl1, s11, info);
-  L.fu = A.at_ref(fu);
-  L.fl[0] = A.at_ref(fl0);
-  L.s1[0] = B.at_ref(s10);
-  L.fl[1] = A.at_ref(fl1);
-  L.s1[1] = B.at_ref(s11);
+  pin_s(fl1, s11, r1);
+  L.fu = A.at_word(fu);
+  L.fl[0] = A.at_word(fl0);
+  L.s1[0] = B.at_word(s10);
+  L.fl[1] = A.at_word(fl1);
+  L.s1[1] = B.at_word(s11);
   // slots 2 and 3 only for the few nodes that use them
-  if (__builtin_expect((info & 7u) > 2u, 0)) {
-    const uint32_t fl2 = rec.fl_ref(2), s12 = rec.s1_ref(2), fl3 = rec.fl_ref(3), s13 = rec.s1_ref(3);
+  if (__builtin_expect(((r1 >> 8) & 7u) > 2u, 0)) {
+    const uint32_t r2 = rec.refs2();
+    const uint32_t fl2 = word_at(r2, 0), s12 = word_at(r2, 1), fl3 = word_at(r2, 2), s13 = word_at(r2, 3);
     pin_s(fl2, s12, fl3);
     pin_s(s13, s13, s13);
-    L.fl[2] = A.at_ref(fl2);
-    L.s1[2] = B.at_ref(s12);
-    L.fl[3] = A.at_ref(fl3);
-    L.s1[3] = B.at_ref(s13);
+    L.fl[2] = A.at_word(fl2);
+    L.s1[2] = B.at_word(s12);
+    L.fl[3] = A.at_word(fl3);
+    L.s1[3] = B.at_word(s13);
   }
 }
 
@@ -505,15 +497,20 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
   const uint32_t s0 = bit(sc.w0, jj);
   const uint32_t s1 = bit(sc.w1, jj);
   // the node's scalar fields, read together
-  const uint32_t um_lo = rec.umask_lo(), um_hi = rec.umask_hi(), info = rec.info();
-  const uint32_t b0 = rec.bits0(), b1 = rec.bits1();
-  pin_s(um_lo, um_hi, info);
-  pin_s(b0, b1, b1);
+  const uint32_t um_lo = rec.umask_lo(), um_hi = rec.umask_hi(), b0 = rec.bits0();
+  pin_s(um_lo, um_hi, b0);
   const double Mv = rec.M();
   const double Cv = rec.C();
   uint32_t anyU, r;
-  double freed;
-  if (__builtin_expect(!(info & kRecSlow), 1)) {
+  // val = Y + freed_v, accumulated in place (exact integers: any order)
+  double val = sc.Y;
+  // deps 0-2 from bits0; 3 means "read refs1" (3 or 4 deps, or a slow node)
+  uint32_t nd = b0 >> 30, r1 = 0;
+  if (__builtin_expect(nd == 3u, 0)) {
+    r1 = rec.refs1();
+    nd = (r1 & kRefsSlow) ? 15u : ((r1 >> 8) & 7u);
+  }
+  if (__builtin_expect(nd != 15u, 1)) {
     if (kFirst) {
       anyU = 0;
       r = 1;
@@ -526,8 +523,7 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
     // FREE(t,v,v): v computed, not kept, no computed user after it. A node
     // other than t is computed only because it is kept (s1) or used (anyU),
     // so only node t can be freed right after it is computed.
-    freed = kFirst ? (double)(~s1 & 1u) * Mv : 0.0;
-    const int nd = (int)(info & 7u);
+    if (kFirst) val = fma((double)(~s1 & 1u), Mv, val);
     auto slot = [&](int sl) {
       const uint32_t lm_lo = rec.lm_lo(sl), lm_hi = rec.lm_hi(sl);
       pin_s(lm_lo, lm_hi, lm_hi);
@@ -535,15 +531,15 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
       if (sl < 2) {
         dMs = rec.dM01(sl);
       } else {
-        const uint32_t d_lo = rec.get(12 + 6 * sl), d_hi = rec.get(13 + 6 * sl);
+        const uint32_t d_lo = rec.get(18 + 2 * sl), d_hi = rec.get(19 + 2 * sl);
         pin_s(d_lo, d_hi, d_hi);
         dMs = dbl(d_lo, d_hi);
       }
-      const uint32_t far = __builtin_amdgcn_ubfe(L.fl[sl], bitpos(b0, b1, 2 + 2 * sl), 1);
+      const uint32_t far = __builtin_amdgcn_ubfe(L.fl[sl], bitpos(b0, r1, 2 + 2 * sl), 1);
       uint32_t later = and_or(sc.Rlo, lm_lo, and_or(sc.Rhi, lm_hi, far));
       later = umin1(later);
-      const uint32_t fr = r & ~__builtin_amdgcn_ubfe(L.s1[sl], bitpos(b0, b1, 1 + 2 * sl), 1) & ~later & 1u;
-      freed = fma((double)fr, dMs, freed);
+      const uint32_t fr = r & ~__builtin_amdgcn_ubfe(L.s1[sl], bitpos(b0, r1, 1 + 2 * sl), 1) & ~later & 1u;
+      val = fma((double)fr, dMs, val);
     };
     // most nodes have one or two dependencies
     if (__builtin_expect(nd >= 1, 1)) slot(0);
@@ -562,7 +558,7 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
       anyU |= r_bit(u, v, sc.Rlo, sc.Rhi, A);
     }
     r = ((s1 | anyU) & ~s0 & 1u) | (uint32_t)kFirst;
-    freed = (double)(r & ~s1 & ~anyU & 1u) * Mv;
+    val = fma((double)(r & ~s1 & ~anyU & 1u), Mv, val);
     const int de = a.dep_ptr[v + 1];
     for (int e = a.dep_ptr[v]; e < de; ++e) {
       const int i = a.dep_idx[e];
@@ -574,13 +570,12 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
         later |= r_bit(u, v, sc.Rlo, sc.Rhi, A);
       }
       const uint32_t fr = r & ~bit(B.word(i >> 5), i & 31) & ~later & 1u;
-      freed = fma((double)fr, a.M[i], freed);
+      val = fma((double)fr, a.M[i], val);
     }
   }
   const double rd = (double)r;
   sc.cost = fma(rd, Cv, sc.cost);
   sc.U0 = fma((double)s0, Mv, sc.U0);
-  const double val = sc.Y + freed;
   sc.maxv = max_f64(sc.maxv, val);
   sc.Y = fma(-rd, Mv, val);
   // slide the window down by one node: bit 0 becomes node v
@@ -1119,13 +1114,14 @@ void build_node_records(int32_t n, const double* M, const double* C, const int32
                         const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx,
                         void* out) {
   NodeRec* recs = static_cast<NodeRec*>(out);
-  const uint32_t zref = zero_ref(n);
   for (int32_t v = 0; v < n; ++v) {
     NodeRec r;
     memset(&r, 0, sizeof(r));
     r.M = M[v];
     r.C = C[v];
-    r.fu_ref = zref;
+    // references, node n for "none": fu, then per slot s1 and fl
+    int ref[1 + 2 * kRecDeps];
+    for (int k = 0; k < 1 + 2 * kRecDeps; ++k) ref[k] = n;
     bool slow = false;
     int nfar = 0;
     for (int32_t e = user_ptr[v]; e < user_ptr[v + 1]; ++e) {
@@ -1133,41 +1129,39 @@ void build_node_records(int32_t n, const double* M, const double* C, const int32
       const int d = u - v - 1;
       if (d < 32) r.umask_lo |= 1u << d;
       else if (d < 64) r.umask_hi |= 1u << (d - 32);
-      else if (nfar++ == 0) r.fu_ref = make_ref(u);
+      else if (nfar++ == 0) ref[0] = u;
     }
     if (nfar > 1) slow = true;
     const int nd = dep_ptr[v + 1] - dep_ptr[v];
     if (nd > kRecDeps) slow = true;
     for (int sl = 0; sl < nd && !slow; ++sl) {
-      DepSlot& ds = r.dep[sl];
       const int i = dep_idx[dep_ptr[v] + sl];
-      ds.s1_ref = make_ref(i);
-      ds.fl_ref = zref;
-      ds.M = M[i];
+      ref[1 + 2 * sl] = i;
+      r.dM[sl] = M[i];
       int nlate = 0;
       for (int32_t e = user_ptr[i]; e < user_ptr[i + 1]; ++e) {
         const int u = user_idx[e];
         if (u <= v) continue;
         const int d = u - v - 1;
-        if (d < 32) ds.lmask_lo |= 1u << d;
-        else if (d < 64) ds.lmask_hi |= 1u << (d - 32);
-        else if (nlate++ == 0) ds.fl_ref = make_ref(u);
+        if (d < 32) r.lm[2 * sl] |= 1u << d;
+        else if (d < 64) r.lm[2 * sl + 1] |= 1u << (d - 32);
+        else if (nlate++ == 0) ref[2 + 2 * sl] = u;
       }
       if (nlate > 1) slow = true;
     }
-    r.info = (uint32_t)(slow ? 0 : nd) | (slow ? kRecSlow : 0u);
-    uint32_t pos[1 + 2 * kRecDeps];
-    pos[0] = r.fu_ref & 31u;
-    for (int sl = 0; sl < kRecDeps; ++sl) {
-      pos[1 + 2 * sl] = r.dep[sl].s1_ref & 31u;
-      pos[2 + 2 * sl] = r.dep[sl].fl_ref & 31u;
-    }
-    for (int k = 0; k < 6; ++k) r.bits0 |= pos[k] << (5 * k);
-    for (int k = 6; k < 1 + 2 * kRecDeps; ++k) r.bits1 |= pos[k] << (5 * (k - 6));
+    const int ndeps = slow ? 0 : nd;
+    // word indices (node >> 5 <= 128 fits 8 bits) and bit positions
+    auto wd = [&](int k) { return (uint32_t)(ref[k] >> 5); };
+    auto bp = [&](int k) { return (uint32_t)(ref[k] & 31); };
+    r.refs0 = wd(0) | wd(2) << 8 | wd(1) << 16 | wd(4) << 24;
+    r.refs1 = wd(3) | (uint32_t)ndeps << 8 | (slow ? kRefsSlow : 0u) | bp(6) << 12 | bp(7) << 17 | bp(8) << 22;
+    r.refs2 = wd(6) | wd(5) << 8 | wd(8) << 16 | wd(7) << 24;
+    for (int k = 0; k < 6; ++k) r.bits0 |= bp(k) << (5 * k);
+    r.bits0 |= (slow ? 3u : (uint32_t)std::min(ndeps, 3)) << 30;
     r.mc[0] = r.M;
     r.mc[1] = r.C;
-    r.dm01[0] = r.dep[0].M;
-    r.dm01[1] = r.dep[1].M;
+    r.dm01[0] = r.dM[0];
+    r.dm01[1] = r.dM[1];
     recs[v] = r;
   }
 }
