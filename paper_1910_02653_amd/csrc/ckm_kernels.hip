@@ -938,59 +938,124 @@ __global__ void __launch_bounds__(256) ckm_best_rows_kernel(const uint32_t* __re
   S_rows[(size_t)r * row_words + w] = word;
 }
 
-// Best candidate's R rows: lane per stage t, Algorithm 2's right-to-left
-// repair reading the S rows written above; bits of higher chunks come back
-// from the lane's own output row.
-__global__ void __launch_bounds__(kWave) ckm_best_closure_kernel(int32_t n, int32_t row_words,
-                                                                 const int32_t* __restrict__ user_ptr,
-                                                                 const int32_t* __restrict__ user_idx,
-                                                                 const int32_t* __restrict__ best_k,
-                                                                 const uint32_t* __restrict__ S_base,
-                                                                 size_t cand_stride,
-                                                                 uint32_t* __restrict__ R_rows) {
-  const int t = blockIdx.x * kWave + threadIdx.x;
-  const bool active = t < n;
-  const int tmax = min(n - 1, (int)blockIdx.x * kWave + kWave - 1);
-  const int bk = best_k[0];
-  // the best candidate's S rows: cand_stride = 0 for rows regenerated into
-  // S_base, n * row_words for caller-supplied rows (bits on or above the
-  // diagonal are never read below)
-  const uint32_t* S_rows = S_base + (bk >= 0 ? (size_t)bk * cand_stride : 0);
-  uint32_t* Rrow = R_rows + (size_t)(active ? t : 0) * row_words;
-  const uint32_t* S0 = S_rows + (size_t)(active ? t : 0) * row_words;
-  const uint32_t* S1 = S_rows + (size_t)((active && t + 1 < n) ? t + 1 : 0) * row_words;
-  if (bk < 0) {
-    if (active)
-      for (int w = 0; w < row_words; ++w) Rrow[w] = 0u;
-    return;
+// Best candidate's R rows: lane = stage t (64 stages per wave), Algorithm
+// 2's right-to-left repair over nodes v = (last stage of the wave) .. 0, all
+// lanes at the same node. As in the evaluate kernel, the R bits of the 64
+// nodes above v sit in a two-register window and R words of finished chunks
+// sit in an LDS row per lane ([word][lane]) for users beyond the window. With
+// one wave per SIMD nothing hides latency, so node records come 32 at a time
+// (a chunk, one register each, lane L holding dword L) one chunk ahead, and
+// the lane's S_t and S_{t+1} rows are copied to LDS first. A lane whose stage
+// is below v computes nothing there. Bits of the S rows on or above the
+// diagonal are never decisive: node t is computed whatever S_t[t] holds.
+// Dynamic LDS: three rows (R, S_t, S_{t+1}) of n / 32 + 1 words per lane.
+struct ClosureArgs {
+  int32_t n, row_words;
+  const int32_t* user_ptr;
+  const int32_t* user_idx;
+  const uint4* recs;
+  const int32_t* best_k;
+  const uint32_t* S_base;
+  size_t cand_stride;
+  uint32_t* R_rows;
+};
+
+constexpr int kChunk = 32;
+
+// Records of nodes 32c .. 32c + 31 (clamped to node n - 1), lane L holding
+// dword L of each.
+__device__ __forceinline__ void load_chunk(uint32_t (&rec)[kChunk], const uint4* recs, int c, int n) {
+  const size_t lane_off = (size_t)((threadIdx.x & 63u) * 4u);
+#pragma unroll
+  for (int j = 0; j < kChunk; ++j) {
+    const int v = __builtin_amdgcn_readfirstlane(min(kChunk * c + j, n - 1));
+    rec[j] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(recs) + (size_t)v * kNodeRecBytes +
+                                                 lane_off);
   }
-  for (int c = tmax >> 5; c >= 0; --c) {
-    const bool lane_chunk = active && c <= (t >> 5);
-    const uint32_t w0 = lane_chunk ? S0[c] : 0u;
-    const uint32_t w1 = (lane_chunk && t + 1 < n) ? S1[c] : 0u;
-    uint32_t rw = 0;
-    for (int jj = 31; jj >= 0; --jj) {
-      const int v = 32 * c + jj;
-      if (v > tmax) continue;
-      uint32_t anyU = 0;
-      const int ue = user_ptr[v + 1];
-      for (int e = user_ptr[v]; e < ue; ++e) {
-        const int u = user_idx[e];
-        if (u > tmax) break;
-        if (lane_chunk && u <= t) {
-          const uint32_t word = ((u >> 5) == c) ? rw : Rrow[u >> 5];
-          anyU |= bit(word, u & 31);
+}
+
+__device__ __forceinline__ uint32_t rl(uint32_t w, int i) { return __builtin_amdgcn_readlane(w, i); }
+
+// Nodes 32c + 31 .. 32c of the scan for the lane's stage t.
+__device__ __forceinline__ void closure_chunk(const ClosureArgs& a, int c, int t, int tmax, const uint32_t (&rec)[kChunk],
+                                              Row A, Row S0, Row S1, uint32_t& Rlo, uint32_t& Rhi) {
+  const uint32_t w0 = S0.word(c), w1 = S1.word(c);
+  uint32_t far_next = A.at_word(word_at(rl(rec[kChunk - 1], 6), 0));
+#pragma unroll
+  for (int jj = kChunk - 1; jj >= 0; --jj) {
+    const int v = kChunk * c + jj;
+    const uint32_t far_w = far_next;
+    if (jj > 0) far_next = A.at_word(word_at(rl(rec[jj - 1], 6), 0));
+    uint32_t r = 0;
+    if (v <= tmax) {
+      const uint32_t um_lo = rl(rec[jj], 4), um_hi = rl(rec[jj], 5), b0 = rl(rec[jj], 8);
+      pin_s(um_lo, um_hi, b0);
+      bool slow = false;
+      if (__builtin_expect((b0 >> 30) == 3u, 0)) slow = (rl(rec[jj], 7) & kRefsSlow) != 0u;
+      uint32_t anyU;
+      if (__builtin_expect(!slow, 1)) {
+        anyU = umin1(and_or(Rlo, um_lo, and_or(Rhi, um_hi, __builtin_amdgcn_ubfe(far_w, b0, 1))));
+      } else {
+        // more than one user beyond the window: walk the users
+        anyU = 0;
+        const int ue = a.user_ptr[v + 1];
+        for (int e = a.user_ptr[v]; e < ue; ++e) {
+          const int u = a.user_idx[e];
+          const int d = u - v - 1;
+          anyU |= d < 32 ? bit(Rlo, d) : (d < 64 ? bit(Rhi, d - 32) : bit(A.word(u >> 5), u & 31));
         }
       }
-      uint32_t r = 0;
-      if (lane_chunk && v <= t)
-        r = (v == t) ? 1u : ((bit(w1, jj) | anyU) & ~bit(w0, jj) & 1u);
-      rw |= r << jj;
+      r = ((bit(w1, jj) | anyU) & ~bit(w0, jj)) & 1u;
+      if (v == t) r = 1u;
+      if (v > t) r = 0u;
     }
-    if (lane_chunk) Rrow[c] = rw;
+    Rhi = (Rhi << 1) | (Rlo >> 31);
+    Rlo = (Rlo << 1) | r;
+  }
+  A.word(c) = Rlo;
+}
+
+__global__ void __launch_bounds__(kWave) ckm_best_closure_kernel(ClosureArgs a) {
+  extern __shared__ uint32_t lds_c[];
+  const int lane = threadIdx.x;
+  const int t = blockIdx.x * kWave + lane;
+  const bool active = t < a.n;
+  const int tmax = min(a.n - 1, (int)blockIdx.x * kWave + kWave - 1);
+  const int bk = a.best_k[0];
+  uint32_t* Rout = a.R_rows + (size_t)(active ? t : 0) * a.row_words;
+  if (bk < 0) {
+    if (active)
+      for (int w = 0; w < a.row_words; ++w) Rout[w] = 0u;
+    return;
+  }
+  const int lwords = (a.n >> 5) + 1;
+  char* base = reinterpret_cast<char*>(lds_c) + 4 * lane;
+  Row A{base}, S0{base + (size_t)lwords * 256}, S1{base + (size_t)2 * lwords * 256};
+  // the lane's rows; words past its stage read as zero (never decisive)
+  const int ts = active ? t : tmax;
+  const uint32_t* src0 = a.S_base + (size_t)bk * a.cand_stride + (size_t)ts * a.row_words;
+  const uint32_t* src1 = src0 + a.row_words;
+  const bool has1 = ts + 1 < a.n;
+  for (int w = 0; w < lwords; ++w) {
+    const bool in = w <= (ts >> 5);
+    A.word(w) = 0u;
+    S0.word(w) = in ? src0[w] : 0u;
+    S1.word(w) = (in && has1) ? src1[w] : 0u;
+  }
+  uint32_t Rlo = 0, Rhi = 0;
+  uint32_t ra[kChunk], rb[kChunk];
+  int c = tmax >> 5;
+  load_chunk(ra, a.recs, c, a.n);
+  for (;;) {
+    if (c >= 1) load_chunk(rb, a.recs, c - 1, a.n);
+    closure_chunk(a, c, t, tmax, ra, A, S0, S1, Rlo, Rhi);
+    if (--c < 0) break;
+    if (c >= 1) load_chunk(ra, a.recs, c - 1, a.n);
+    closure_chunk(a, c, t, tmax, rb, A, S0, S1, Rlo, Rhi);
+    if (--c < 0) break;
   }
   if (active)
-    for (int w = (t >> 5) + 1; w < row_words; ++w) Rrow[w] = 0u;
+    for (int w = 0; w < a.row_words; ++w) Rout[w] = w <= (t >> 5) ? A.word(w) : 0u;
 }
 
 template <typename T>
@@ -1072,6 +1137,28 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   return hipGetLastError();
 }
 
+static hipError_t launch_closure(const ckm_graph& g, const Layout& L, const int32_t* d_best_k,
+                                 const uint32_t* S_base, size_t cand_stride, uint32_t* R_rows, hipStream_t stream) {
+  ClosureArgs c;
+  c.n = g.n;
+  c.row_words = L.row_words;
+  c.user_ptr = g.d_user_ptr;
+  c.user_idx = g.d_user_idx;
+  c.recs = reinterpret_cast<const uint4*>(g.d_recs);
+  c.best_k = d_best_k;
+  c.S_base = S_base;
+  c.cand_stride = cand_stride;
+  c.R_rows = R_rows;
+  const size_t lds = (size_t)3 * ((g.n >> 5) + 1) * kWave * sizeof(uint32_t);
+  if (lds > 65536) {
+    hipError_t e = hipFuncSetAttribute((const void*)ckm_best_closure_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(ckm_best_closure_kernel, dim3((g.n + kWave - 1) / kWave), dim3(kWave), lds, stream, c);
+  return hipGetLastError();
+}
+
 hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
                          int64_t budget, uint32_t flags, int64_t* d_peak, int64_t* d_cost,
                          uint8_t* d_feasible, int32_t* d_best_k, uint64_t* d_best_S,
@@ -1086,11 +1173,11 @@ hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_
                      at<const Best>(work, L.best_off), src == kSrcUser ? 0 : g.n,
                      at<const int32_t>(work, L.nan_off), d_best_k, d_status);
   if (src == kSrcUser) {
-    if (d_best_R)
-      hipLaunchKernelGGL(ckm_best_closure_kernel, dim3((g.n + kWave - 1) / kWave), dim3(kWave), 0, stream,
-                         g.n, L.row_words, g.d_user_ptr, g.d_user_idx, d_best_k,
-                         reinterpret_cast<const uint32_t*>(s_user), (size_t)g.n * L.row_words,
-                         reinterpret_cast<uint32_t*>(d_best_R));
+    if (d_best_R) {
+      hipError_t e = launch_closure(g, L, d_best_k, reinterpret_cast<const uint32_t*>(s_user),
+                                    (size_t)g.n * L.row_words, reinterpret_cast<uint32_t*>(d_best_R), stream);
+      if (e != hipSuccess) return e;
+    }
   } else if (d_best_S || d_best_R) {
     uint32_t* srows = d_best_S ? reinterpret_cast<uint32_t*>(d_best_S) : at<uint32_t>(work, L.srows_off);
     dim3 grid((L.row_words + 255) / 256, g.n);
@@ -1101,9 +1188,9 @@ hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_
                        src == kSrcThreshold ? at<const uint32_t>(work, L.thr_rank_off) : nullptr, d_best_k,
                        srows);
     if (d_best_R) {
-      hipLaunchKernelGGL(ckm_best_closure_kernel, dim3((g.n + kWave - 1) / kWave), dim3(kWave), 0,
-                         stream, g.n, L.row_words, g.d_user_ptr, g.d_user_idx, d_best_k,
-                         static_cast<const uint32_t*>(srows), (size_t)0, reinterpret_cast<uint32_t*>(d_best_R));
+      hipError_t e = launch_closure(g, L, d_best_k, static_cast<const uint32_t*>(srows), (size_t)0,
+                                    reinterpret_cast<uint32_t*>(d_best_R), stream);
+      if (e != hipSuccess) return e;
     }
   }
   return hipGetLastError();
