@@ -501,3 +501,61 @@ int ckm_ref_plan(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx, cons
   free(order);
   return CKM_REF_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Largest batch multiplier of one schedule (the maximum-batch experiment of
+ * the evaluation): node sizes become B * M_i (M_input and M_param stay), and
+ * B is the largest integer with peak memory <= budget, subject to the cost
+ * cap of eq. (cost_constr) (costs do not scale with B). Found by search over
+ * the simulator: doubling, then bisection. 0 when B = 1 already fails or the
+ * cost exceeds the cap; limit when B = limit still fits. */
+int64_t ckm_ref_max_batch(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx, const int64_t* cost,
+                          const int64_t* size, int64_t m_input, int64_t m_param, const uint8_t* S,
+                          const uint8_t* R, int64_t budget, int64_t cost_cap, int64_t limit) {
+  int64_t* scaled = (int64_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int64_t));
+  int64_t lo = 0, hi, peak, c;
+  int32_t i;
+#define FITS(B_, out_)                                                                     \
+  do {                                                                                     \
+    for (i = 0; i < n; ++i) scaled[i] = (B_) * size[i];                                    \
+    ckm_ref_simulate(n, dep_ptr, dep_idx, cost, scaled, m_input, m_param, S, R, &peak, &c, \
+                     NULL, NULL, NULL);                                                    \
+    (out_) = peak <= budget;                                                               \
+  } while (0)
+  {
+    int ok;
+    FITS((int64_t)1, ok);
+    if (!ok || c > cost_cap) {
+      free(scaled);
+      return 0;
+    }
+  }
+  lo = 1;
+  hi = 2;
+  for (;;) {   /* doubling: lo fits, find hi that does not (or reach the limit) */
+    int ok;
+    if (hi >= limit) {
+      FITS(limit, ok);
+      if (ok) {
+        free(scaled);
+        return limit;
+      }
+      hi = limit;
+      break;
+    }
+    FITS(hi, ok);
+    if (!ok) break;
+    lo = hi;
+    hi *= 2;
+  }
+  while (hi - lo > 1) {   /* lo fits, hi does not */
+    int64_t mid = lo + (hi - lo) / 2;
+    int ok;
+    FITS(mid, ok);
+    if (ok) lo = mid;
+    else hi = mid;
+  }
+#undef FITS
+  free(scaled);
+  return lo;
+}

@@ -122,6 +122,14 @@ int ckm_ref_plan(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx, cons
                  int64_t m_input, int64_t m_param, const uint8_t* S, const uint8_t* R, int early,
                  int32_t* stmts, int64_t* mem, int64_t capacity, int64_t* count);
 
+/* Largest batch multiplier B of a schedule: sizes B * M_i (M_input, M_param
+ * unscaled), peak <= budget, and the schedule's cost <= cost_cap (eq.
+ * cost_constr). Searched over the simulator (doubling, then bisection); 0 if
+ * B = 1 fails, `limit` if B = limit fits. */
+int64_t ckm_ref_max_batch(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx, const int64_t* cost,
+                          const int64_t* size, int64_t m_input, int64_t m_param, const uint8_t* S,
+                          const uint8_t* R, int64_t budget, int64_t cost_cap, int64_t limit);
+
 #ifdef __cplusplus
 }
 #endif

@@ -57,6 +57,9 @@ def lib():
         L.ckm_ref_check_schedule.restype = C.c_int
         L.ckm_ref_plan.argtypes = [C.c_int32, p, p, p, C.c_int64, C.c_int64, p, p, C.c_int, p, p, C.c_int64, p]
         L.ckm_ref_plan.restype = C.c_int
+        L.ckm_ref_max_batch.argtypes = [C.c_int32, p, p, p, p, C.c_int64, C.c_int64, p, p, C.c_int64, C.c_int64,
+                                        C.c_int64]
+        L.ckm_ref_max_batch.restype = C.c_int64
         L.ckm_ref_solve_R.argtypes = [C.c_int32, p, p, p, p]
         L.ckm_ref_solve_R.restype = None
         L.ckm_ref_simulate.argtypes = [C.c_int32, p, p, p, p, C.c_int64, C.c_int64, p, p, p, p, p, p, p]
@@ -266,6 +269,16 @@ def plan(w, S, R, early: bool = False):
     c = int(cnt[0])
     assert c <= cap
     return stmts[:c].copy(), mem[:c].copy()
+
+
+def max_batch(w, S, R, budget: int, cost_cap: int, limit: int = 1 << 40) -> int:
+    """Largest B with peak(B * M) <= budget and cost <= cost_cap, by search
+    over the simulator (sizes scaled, M_input and M_param not)."""
+    ptr, idx, cost, size = _graph(w)
+    S = np.ascontiguousarray(S, dtype=np.uint8)
+    R = np.ascontiguousarray(R, dtype=np.uint8)
+    return int(lib().ckm_ref_max_batch(w.n, _ptr(ptr), _ptr(idx), _ptr(cost), _ptr(size), w.m_input, w.m_param,
+                                       _ptr(S), _ptr(R), int(budget), int(cost_cap), int(limit)))
 
 
 def pack_rows(X) -> np.ndarray:

@@ -493,6 +493,43 @@ def test_threshold_eval_closed_forms():
     assert int(r["cost"][0]) == sum(int(cost[: t + 1].sum()) for t in range(n)) == int(r["cost"][1])
 
 
+def test_max_batch_hand_worked():
+    """Chain 0 -> 1 -> 2, M = [1, 2, 4], M_in = M_param = 0. Keeping every
+    value peaks at 1 + 2 + 4 = 7 bytes per unit of batch; keeping none peaks
+    at the largest adjacent pair, 2 + 4 = 6. A 70-byte budget then admits a
+    batch of 10 and 11; a cost cap below the schedule's cost admits none."""
+    ptr, idx = wl.csr_from_deps([[], [0], [1]])
+    w = wl.Workload("chain3", 3, ptr, idx, np.array([1, 1, 1], np.int64), np.array([1, 2, 4], np.int64), 0, 0,
+                    np.zeros((3, 3)), 1, 0, 0)
+    full = np.tri(3, 3, -1, dtype=np.uint8)
+    none = np.zeros((3, 3), np.uint8)
+    assert ref.max_batch(w, full, ref.solve_R(w, full), 70, 10 ** 6) == 10
+    assert ref.max_batch(w, none, ref.solve_R(w, none), 70, 10 ** 6) == 11
+    assert ref.max_batch(w, none, ref.solve_R(w, none), 5, 10 ** 6) == 0
+    # S = 0 recomputes: cost 1 + 2 + 3 = 6
+    assert ref.max_batch(w, none, ref.solve_R(w, none), 70, 5) == 0
+    assert ref.max_batch(w, none, ref.solve_R(w, none), 70, 6) == 11
+    assert ref.max_batch(w, none, ref.solve_R(w, none), 10 ** 9, 6, limit=1000) == 1000
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_max_batch_search_matches_linear_form(seed):
+    """Every U term but M_in + 2 M_param scales with B, so the search over the
+    simulator must give floor((budget - base) / (peak - base)) for any budget."""
+    w = wl.random_dag(25, seed, max_size=60, m_input=7, m_param=4)
+    base = 7 + 2 * 4
+    q = ref.quantize(w.s_frac)
+    rng = np.random.default_rng(seed)
+    for k in range(3):
+        S = ref.round_random(q, seed, k)
+        R = ref.solve_R(w, S)
+        sim = ref.simulate(w, S, R)
+        act = sim["peak"] - base
+        for budget in [base - 1, sim["peak"] - 1, sim["peak"]] + [int(x) for x in rng.integers(base, 50 * sim["peak"], 5)]:
+            want = (budget - base) // act if budget >= sim["peak"] else 0
+            assert ref.max_batch(w, S, R, budget, sim["cost"]) == want, (k, budget)
+
+
 def test_validate_graph_errors():
     n = 3
     ok = ref.validate_graph(n, [0, 0, 1, 3], [0, 0, 1], [1, 1, 1], [1, 1, 1], 0, 0)
