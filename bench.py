@@ -17,6 +17,9 @@ checkpoint matrices (banded, 30 % of values kept) on the same graph: Algorithm
 `threshold_family` times K deterministic candidates [clamp(S*) > p_k] on an
 even threshold grid over [0, 1] for the same graph and S*: keys, evaluation,
 argmin and the best S and R.
+`max_batch` times quantize + evaluate + the largest batch multiplier of
+every candidate (budget 3x the median activation peak, cost cap at the
+median cost) on the same workload.
 `execution_plan` times Algorithm 1's plan (with the memory after each
 statement) for the step's best candidate, or candidate 0's rows when none
 is feasible, read from HBM where the step left them.
@@ -126,6 +129,50 @@ def time_thresholds(g, w, K, steps, stream, d_s):
             "input": "K=%d thresholds evenly spaced over [0, 1] on the workload's S*" % K}
 
 
+def time_max_batch(g, w, steps, stream, d_s):
+    """Throughput of quantize + evaluate + ckm_max_batch_async."""
+    import numpy as np
+    import torch
+
+    from paper_1910_02653_amd import ckm
+
+    K = w.K
+    work = g.alloc_work(K)
+    out = g.alloc_outputs(K, rows=False)
+    g.round_eval_async(d_s, K, w.seed, 2 ** 62, 0, out, work, stream)
+    torch.cuda.synchronize()
+    peak, cost = out["peak"].cpu().numpy(), out["cost"].cpu().numpy()
+    base = w.m_input + 2 * w.m_param
+    budget = int(base + 3 * (np.median(peak) - base))
+    cap = int(np.median(cost))
+    d_b = torch.empty(K, dtype=torch.int64, device="cuda")
+    d_bk = torch.empty(1, dtype=torch.int32, device="cuda")
+    d_bb = torch.empty(1, dtype=torch.int64, device="cuda")
+    d_st = torch.empty(1, dtype=torch.int32, device="cuda")
+
+    def call():
+        g.quantize_async(d_s, work, stream)
+        g.evaluate_async(K, w.seed, 0, work, stream=stream)
+        g.max_batch_async(K, budget, cap, d_b, d_bk, d_bb, d_st, work, stream)
+
+    for _ in range(3):
+        call()
+    torch.cuda.synchronize()
+    assert int(d_st.item()) == ckm.OK
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(steps):
+        call()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    return {"value": K / (ms * 1e-3), "unit": "candidates/s", "ms_per_call": ms, "steps": steps,
+            "best_k": int(d_bk.item()), "best_batch": int(d_bb.item()),
+            "input": "K=%d rounded candidates, budget %d B (3x the median activation peak), cost cap %d "
+                     "(median cost)" % (K, budget, cap)}
+
+
 def time_plan(g, w, steps, stream, d_s):
     """Throughput of ckm_plan_async on one schedule of the workload: the best
     candidate at the median-peak budget (a budget some candidates meet)."""
@@ -180,6 +227,8 @@ def main():
                     help="timed calls of the threshold-family evaluation (0 = skip)")
     ap.add_argument("--plan-steps", type=int, default=20,
                     help="timed calls of the execution-plan generation (0 = skip)")
+    ap.add_argument("--batch-steps", type=int, default=20,
+                    help="timed calls of the largest-batch search (0 = skip)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -261,6 +310,8 @@ def main():
     }
     if args.sched_steps > 0:
         result["supplied_schedules"] = time_schedules(g, w, K, args.sched_steps, stream)
+    if args.batch_steps > 0:
+        result["max_batch"] = time_max_batch(g, w, args.batch_steps, stream, d_s)
     if args.plan_steps > 0:
         result["execution_plan"] = time_plan(g, w, args.plan_steps, stream, d_s)
     if args.thr_steps > 0:

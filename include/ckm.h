@@ -207,6 +207,30 @@ ckm_status ckm_threshold_eval_async(const ckm_graph* g, const double* d_s_frac, 
                                    uint64_t* d_best_R, int32_t* d_status, void* d_work, size_t work_bytes,
                                    void* stream);
 
+/* ---- largest batch ------------------------------------------------------
+ * The maximum-batch experiment of the evaluation: a batch multiplier B
+ * scales every node size to B * M_i (M_in and M_param stay). Costs do not
+ * scale. For each rounded candidate k (randomized rounding of S*, Section
+ * 5.1, repaired by Algorithm 2 and simulated as in ckm_round_eval), batch[k]
+ * is the largest B with peak memory <= budget. That is
+ * floor((budget - base) / (peak_k - base)), base = M_in + 2 M_param, since
+ * every other U term scales with B. The candidate's cost must also be
+ * <= cost_cap (eq. cost_constr: at most one extra forward pass; the caller
+ * computes it, 2 sum_fwd C_i + sum_bwd C_i). Otherwise batch[k] = 0. A
+ * candidate with no activation bytes gets INT64_MAX. best_k: the largest B,
+ * then the lexicographic minimum of (cost, peak, k); -1 when every B is 0.
+ * best_batch (may be NULL) receives its B. The synchronous form takes S*
+ * like ckm_round_eval. The asynchronous form reads the per-candidate totals
+ * that the last ckm_evaluate_async left in the work buffer (after
+ * ckm_quantize_async; K must match), so it can run beside ckm_select_async.
+ * It writes the S* NaN status to d_status (may be NULL). */
+ckm_status ckm_max_batch(const ckm_graph* g, const double* s_frac, int64_t ld, int32_t K, uint64_t seed,
+                         uint32_t flags, int64_t budget, int64_t cost_cap, int64_t* batch, int32_t* best_k,
+                         int64_t* best_batch);
+ckm_status ckm_max_batch_async(const ckm_graph* g, int32_t K, int64_t budget, int64_t cost_cap, int64_t* d_batch,
+                               int32_t* d_best_k, int64_t* d_best_batch, int32_t* d_status, void* d_work,
+                               size_t work_bytes, void* stream);
+
 /* ---- execution plans ---------------------------------------------------
  * Algorithm 1 (Section 4.9): the program that carries out a schedule (S, R).
  * R is scanned row by row. In stage t, node k is computed into a new virtual

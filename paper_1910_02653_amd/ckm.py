@@ -26,7 +26,8 @@ EXPORTS = (
     "ckm_graph_create", "ckm_graph_destroy", "ckm_graph_num_nodes", "ckm_round_eval",
     "ckm_workspace_size", "ckm_quantize_async", "ckm_evaluate_async", "ckm_select_async",
     "ckm_round_eval_async", "ckm_eval_schedules", "ckm_eval_schedules_async", "ckm_threshold_eval",
-    "ckm_threshold_eval_async", "ckm_plan", "ckm_plan_async", "ckm_last_error",
+    "ckm_threshold_eval_async", "ckm_plan", "ckm_plan_async", "ckm_max_batch",
+    "ckm_max_batch_async", "ckm_last_error",
 )
 PLAN_EARLY_FREE = 1
 OP_COMPUTE, OP_DEALLOCATE = 0, 1
@@ -84,6 +85,10 @@ def lib():
         L.ckm_plan.restype = C.c_int
         L.ckm_plan_async.argtypes = [p, p, p, u32, p, i64, p, p, p, p, sz, p]
         L.ckm_plan_async.restype = C.c_int
+        L.ckm_max_batch.argtypes = [p, p, i64, i32, u64, u32, i64, i64, p, p, p]
+        L.ckm_max_batch.restype = C.c_int
+        L.ckm_max_batch_async.argtypes = [p, i32, i64, i64, p, p, p, p, p, sz, p]
+        L.ckm_max_batch_async.restype = C.c_int
         L.ckm_last_error.argtypes = []
         L.ckm_last_error.restype = C.c_char_p
         _lib = L
@@ -186,6 +191,21 @@ class Graph:
                                         _np_ptr(peak), _np_ptr(cost), _np_ptr(feas), _np_ptr(bk), _np_ptr(bS),
                                         _np_ptr(bR)))
         return dict(peak=peak, cost=cost, feasible=feas, best_k=int(bk[0]), best_S=bS, best_R=bR)
+
+    def max_batch(self, s_frac, K: int, seed: int, budget: int, cost_cap: int, flags: int = 0):
+        """Largest batch multiplier of each rounded candidate (ckm_max_batch)."""
+        s = np.ascontiguousarray(s_frac, dtype=np.float64)
+        batch = np.zeros(K, np.int64)
+        bk = np.zeros(1, np.int32)
+        bb = np.zeros(1, np.int64)
+        _check(lib().ckm_max_batch(self._h, _np_ptr(s), s.shape[1], int(K), int(seed), int(flags), int(budget),
+                                   int(cost_cap), _np_ptr(batch), _np_ptr(bk), _np_ptr(bb)))
+        return dict(batch=batch, best_k=int(bk[0]), best_batch=int(bb[0]))
+
+    def max_batch_async(self, K, budget, cost_cap, d_batch, d_best_k, d_best_batch, d_status, work, stream=None):
+        _check(lib().ckm_max_batch_async(self._h, int(K), int(budget), int(cost_cap), _dev_ptr(d_batch),
+                                         _dev_ptr(d_best_k), _dev_ptr(d_best_batch), _dev_ptr(d_status),
+                                         _dev_ptr(work), work.numel() * work.element_size(), _stream_ptr(stream)))
 
     def plan(self, S_rows, R_rows, early: bool = False, capacity=None, want_mem: bool = True):
         """Algorithm 1's execution plan of (S, R) bit rows (ckm_plan): statements

@@ -129,6 +129,7 @@ Layout make_layout(int32_t n, int32_t K) {
   L.plan_go_off = off;    off = align256(off + sizeof(int32_t));
   L.plan_rt_off = off;    off = align256(off + (size_t)n * ((n + 31) / 32) * sizeof(uint32_t));
   L.plan_rpre_off = off;  off = align256(off + (size_t)n * ckm::kMaxNodesWords * sizeof(int32_t));
+  L.bbest_off = off;      off = align256(off + (size_t)L.reduce_blocks * 32);
   L.total = off;
   return L;
 }
@@ -663,6 +664,84 @@ ckm_status ckm_plan(const ckm_graph* g, const uint64_t* S, const uint64_t* R, ui
         st = fail_hip(e, "hipMemcpy plan");
         break;
       }
+    }
+  } while (false);
+  if (stream) {
+    (void)hipStreamSynchronize(stream);
+    (void)hipStreamDestroy(stream);
+  }
+  (void)hipFree(d);
+  return st;
+}
+
+ckm_status ckm_max_batch_async(const ckm_graph* g, int32_t K, int64_t budget, int64_t cost_cap, int64_t* d_batch,
+                               int32_t* d_best_k, int64_t* d_best_batch, int32_t* d_status, void* d_work,
+                               size_t work_bytes, void* stream) {
+  Layout L;
+  ckm_status st = check_work(g, K, d_work, work_bytes, &L);
+  if (st != CKM_OK) return st;
+  if (budget < 0) return fail(CKM_E_INVALID_ARG, "budget = %lld < 0", (long long)budget);
+  if (cost_cap < 0) return fail(CKM_E_INVALID_ARG, "cost_cap = %lld < 0", (long long)cost_cap);
+  if (!d_batch || !d_best_k) return fail(CKM_E_INVALID_ARG, "NULL batch or best_k");
+  DeviceGuard dg(g->device);
+  hipError_t e = ckm::launch_max_batch(*g, L, K, budget, cost_cap, d_batch, d_best_k, d_best_batch, d_status,
+                                       static_cast<char*>(d_work), static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CKM_OK : fail_hip(e, "max batch launch");
+}
+
+ckm_status ckm_max_batch(const ckm_graph* g, const double* s_frac, int64_t ld, int32_t K, uint64_t seed,
+                         uint32_t flags, int64_t budget, int64_t cost_cap, int64_t* batch, int32_t* best_k,
+                         int64_t* best_batch) {
+  if (!g) return fail(CKM_E_INVALID_ARG, "graph is NULL");
+  if (!s_frac || !batch || !best_k) return fail(CKM_E_INVALID_ARG, "NULL S*, batch or best_k");
+  if (ld < g->n) return fail(CKM_E_INVALID_ARG, "ld = %lld < n = %d", (long long)ld, g->n);
+  if (K < 1) return fail(CKM_E_INVALID_ARG, "K = %d < 1", K);
+  if (K > CKM_MAX_CANDIDATES) return fail(CKM_E_UNSUPPORTED, "K = %d > %d", K, CKM_MAX_CANDIDATES);
+  if (budget < 0) return fail(CKM_E_INVALID_ARG, "budget = %lld < 0", (long long)budget);
+  if (cost_cap < 0) return fail(CKM_E_INVALID_ARG, "cost_cap = %lld < 0", (long long)cost_cap);
+  if (flags & ~(uint32_t)CKM_F_DET0) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
+  const int32_t n = g->n;
+  for (int32_t t = 0; t < n; ++t)
+    for (int32_t i = 0; i < t; ++i)
+      if (std::isnan(s_frac[(int64_t)t * ld + i])) return fail(CKM_E_INVALID_ARG, "S*[%d][%d] is NaN", t, i);
+  DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
+  const Layout L = ckm::make_layout(n, K);
+  size_t off = 0;
+  const size_t o_s = off;  off = align256(off + (size_t)n * n * sizeof(double));
+  const size_t o_b = off;  off = align256(off + (size_t)K * 8);
+  const size_t o_bk = off; off = align256(off + 8);
+  const size_t o_bb = off; off = align256(off + 8);
+  const size_t o_w = off;  off = align256(off + L.total);
+  char* d = nullptr;
+  hipError_t e = hipMalloc(&d, off);
+  if (e != hipSuccess)
+    return e == hipErrorOutOfMemory ? fail(CKM_E_NOMEM, "hipMalloc of %zu bytes failed", off)
+                                    : fail_hip(e, "hipMalloc");
+  hipStream_t stream = nullptr;
+  ckm_status st = CKM_OK;
+  do {
+    if ((e = hipStreamCreateWithFlags(&stream, hipStreamNonBlocking)) != hipSuccess) {
+      st = fail_hip(e, "hipStreamCreate");
+      break;
+    }
+    if ((e = hipMemcpy2DAsync(d + o_s, (size_t)n * sizeof(double), s_frac, (size_t)ld * sizeof(double),
+                              (size_t)n * sizeof(double), n, hipMemcpyHostToDevice, stream)) != hipSuccess) {
+      st = fail_hip(e, "hipMemcpy2D S*");
+      break;
+    }
+    if ((st = ckm_quantize_async(g, reinterpret_cast<const double*>(d + o_s), n, d + o_w, L.total, stream)) != CKM_OK ||
+        (st = ckm_evaluate_async(g, K, seed, flags, 0, d + o_w, L.total, stream)) != CKM_OK ||
+        (st = ckm_max_batch_async(g, K, budget, cost_cap, reinterpret_cast<int64_t*>(d + o_b),
+                                  reinterpret_cast<int32_t*>(d + o_bk), reinterpret_cast<int64_t*>(d + o_bb), nullptr,
+                                  d + o_w, L.total, stream)) != CKM_OK)
+      break;
+    if ((e = hipMemcpyAsync(batch, d + o_b, (size_t)K * 8, hipMemcpyDeviceToHost, stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(best_k, d + o_bk, 4, hipMemcpyDeviceToHost, stream)) != hipSuccess ||
+        (best_batch && (e = hipMemcpyAsync(best_batch, d + o_bb, 8, hipMemcpyDeviceToHost, stream)) != hipSuccess) ||
+        (e = hipStreamSynchronize(stream)) != hipSuccess) {
+      st = fail_hip(e, "hipMemcpy results");
+      break;
     }
   } while (false);
   if (stream) {

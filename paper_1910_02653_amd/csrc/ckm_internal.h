@@ -64,7 +64,9 @@ struct Layout {
          plan_cnt_off = 0, plan_comp_off = 0, plan_err_off = 0, plan_pos_off = 0, plan_rbase_off = 0,
          plan_go_off = 0,
          // R transposed (n columns of ceil(n/32) words) and per-row word ranks
-         plan_rt_off = 0, plan_rpre_off = 0, total = 0;
+         plan_rt_off = 0, plan_rpre_off = 0,
+         bbest_off = 0,  // per-block best of the batch multipliers
+         total = 0;
 };
 
 Layout make_layout(int32_t n, int32_t K);
@@ -94,6 +96,11 @@ hipError_t launch_threshold_keys(const ckm_graph& g, const Layout& L, const doub
 hipError_t launch_plan(const ckm_graph& g, const Layout& L, const uint64_t* d_S, const uint64_t* d_R,
                        uint32_t flags, int32_t* d_P, int64_t capacity, int64_t* d_count, int64_t* d_mem,
                        int32_t* d_status, char* work, hipStream_t stream);
+// Largest batch multiplier per candidate from the totals of the last
+// evaluate, and the best one.
+hipError_t launch_max_batch(const ckm_graph& g, const Layout& L, int32_t K, int64_t budget, int64_t cost_cap,
+                            int64_t* d_batch, int32_t* d_best_k, int64_t* d_best_batch, int32_t* d_status,
+                            char* work, hipStream_t stream);
 // src: one of kSrcRound, kSrcUser, kSrcThreshold. s_user: for kSrcUser, K
 // caller-supplied S matrices ([K][n][row_words] 32-bit words).
 hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,

@@ -911,6 +911,79 @@ __global__ void __launch_bounds__(256) ckm_argmin_kernel(int32_t nblocks, const 
 }
 
 // ---------------------------------------------------------------------------
+// Largest batch multiplier per candidate (the maximum-batch experiment of
+// the evaluation): with node sizes B * M_i (M_in, M_param fixed) every U term
+// but the constant base = M_in + 2 M_param scales with B, so the peak at B is
+// base + B (peak - base) and the largest B within the budget is
+// floor((budget - base) / (peak - base)). Candidates over the cost cap (eq.
+// cost_constr) or over the budget at B = 1 get 0; a candidate with no
+// activation bytes gets INT64_MAX. The best: largest B, then the
+// lexicographic minimum of (cost, peak, k); k = -1 when every B is 0.
+struct BestB {
+  int64_t B, cost, peak;
+  int32_t k, pad;
+};
+
+__device__ __forceinline__ bool better_b(const BestB& x, const BestB& y) {
+  if (x.k < 0) return false;
+  if (y.k < 0) return true;
+  if (x.B != y.B) return x.B > y.B;
+  if (x.cost != y.cost) return x.cost < y.cost;
+  if (x.peak != y.peak) return x.peak < y.peak;
+  return x.k < y.k;
+}
+
+__global__ void __launch_bounds__(256) ckm_batch_kernel(int32_t K, const int64_t* __restrict__ tot_peak,
+                                                        const int64_t* __restrict__ tot_cost, int64_t base,
+                                                        int64_t budget, int64_t cost_cap,
+                                                        int64_t* __restrict__ batch, BestB* __restrict__ block_best) {
+  __shared__ BestB sb[256];
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  BestB b{0, 0, 0, -1, 0};
+  if (k < K) {
+    const int64_t p = tot_peak[k], c = tot_cost[k];
+    int64_t B = 0;
+    if (c <= cost_cap && p <= budget) B = p > base ? (budget - base) / (p - base) : INT64_MAX;
+    batch[k] = B;
+    if (B > 0) b = BestB{B, c, p, k, 0};
+  }
+  sb[threadIdx.x] = b;
+  __syncthreads();
+  for (int off = blockDim.x / 2; off > 0; off >>= 1) {
+    if (threadIdx.x < off && better_b(sb[threadIdx.x + off], sb[threadIdx.x])) sb[threadIdx.x] = sb[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) block_best[blockIdx.x] = sb[0];
+}
+
+__global__ void __launch_bounds__(256) ckm_batch_argmax_kernel(int32_t nblocks, const BestB* __restrict__ block_best,
+                                                               int32_t n, const int32_t* __restrict__ nan_row,
+                                                               int32_t* __restrict__ best_k,
+                                                               int64_t* __restrict__ best_batch,
+                                                               int32_t* __restrict__ status) {
+  __shared__ BestB sb[256];
+  __shared__ int any_nan;
+  if (threadIdx.x == 0) any_nan = 0;
+  BestB b{0, 0, 0, -1, 0};
+  for (int i = threadIdx.x; i < nblocks; i += blockDim.x)
+    if (better_b(block_best[i], b)) b = block_best[i];
+  int nan = 0;
+  for (int r = threadIdx.x; r < n; r += blockDim.x) nan |= nan_row[r];
+  sb[threadIdx.x] = b;
+  __syncthreads();
+  if (nan) atomicOr(&any_nan, 1);
+  for (int off = blockDim.x / 2; off > 0; off >>= 1) {
+    if (threadIdx.x < off && better_b(sb[threadIdx.x + off], sb[threadIdx.x])) sb[threadIdx.x] = sb[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    best_k[0] = sb[0].k;
+    if (best_batch) best_batch[0] = sb[0].k >= 0 ? sb[0].B : 0;
+    if (status) status[0] = any_nan ? (int32_t)CKM_E_INVALID_ARG : (int32_t)CKM_OK;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Best candidate's S rows: thread per (row r, 32-bit word w). Output rows
 // have row_words words; words with no node (32w >= n) are zero. rank: the
 // threshold family (q holds keys), else randomized or deterministic rounding.
@@ -1156,6 +1229,18 @@ static hipError_t launch_closure(const ckm_graph& g, const Layout& L, const int3
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(ckm_best_closure_kernel, dim3((g.n + kWave - 1) / kWave), dim3(kWave), lds, stream, c);
+  return hipGetLastError();
+}
+
+hipError_t launch_max_batch(const ckm_graph& g, const Layout& L, int32_t K, int64_t budget, int64_t cost_cap,
+                            int64_t* d_batch, int32_t* d_best_k, int64_t* d_best_batch, int32_t* d_status,
+                            char* work, hipStream_t stream) {
+  const int rb = L.reduce_blocks;
+  hipLaunchKernelGGL(ckm_batch_kernel, dim3(rb), dim3(256), 0, stream, K, at<const int64_t>(work, L.part_peak_off),
+                     at<const int64_t>(work, L.part_cost_off), (int64_t)g.base, budget, cost_cap, d_batch,
+                     at<BestB>(work, L.bbest_off));
+  hipLaunchKernelGGL(ckm_batch_argmax_kernel, dim3(1), dim3(256), 0, stream, rb, at<const BestB>(work, L.bbest_off),
+                     g.n, at<const int32_t>(work, L.nan_off), d_best_k, d_best_batch, d_status);
   return hipGetLastError();
 }
 
