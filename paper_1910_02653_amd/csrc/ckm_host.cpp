@@ -60,12 +60,6 @@ int32_t max_splits_for(int32_t n, int32_t /*K*/) {
 // Resident evaluate waves on the device: 256 CUs times the waves per CU.
 // With n < 1024 one row is in registers and the register file allows 16
 // waves per CU; otherwise the two LDS rows of a wave set the count.
-static int64_t eval_slots(int32_t n) {
-  const int64_t words = (n >> 5) + 1;
-  if (words <= 32) return 256 * 16;
-  const int64_t wave_lds = 2 * words * kWave * 4;
-  return 256 * std::max<int64_t>(1, std::min<int64_t>(16, (160 * 1024) / wave_lds));
-}
 
 Plan plan_splits(int32_t n, int32_t splits) {
   Plan p;
@@ -74,14 +68,16 @@ Plan plan_splits(int32_t n, int32_t splits) {
   return p;
 }
 
-Plan plan_auto(int32_t n, int32_t K, int32_t max_items) {
+Plan plan_auto(int32_t n, int32_t K, int32_t max_items, int32_t waves_per_cu) {
   // About eight items per resident wave slot. The upper half of the stages
   // goes in items of P stages, the lower half (a quarter of the work) in as
   // many ranges, each about a third of an upper item, so the launch ends on
   // small items. Each item regenerates one S row; the finer balance is worth
   // more than that on this workload range.
   const int64_t groups = (K + kWave - 1) / kWave;
-  const int64_t target = std::max<int64_t>(1, (8 * eval_slots(n) + groups - 1) / groups);
+  // resident evaluate waves on the chip's 256 CUs
+  const int64_t slots = 256 * (int64_t)std::max(1, waves_per_cu);
+  const int64_t target = std::max<int64_t>(1, (8 * slots + groups - 1) / groups);
   if (n < 8 || target < 4) return plan_splits(n, (int32_t)std::min<int64_t>(target, max_items));
   Plan p;
   p.kind = 1;
@@ -239,6 +235,7 @@ ckm_status ckm_graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* de
     delete g;
     return fail_hip(e, "hipGetDevice");
   }
+  g->eval_waves = ckm::eval_waves_per_cu(n);
   const size_t Ea = (size_t)std::max(E, 1);
   const size_t off_M = 0;
   const size_t off_C = align256(off_M + n * sizeof(double));
@@ -341,7 +338,7 @@ ckm_status ckm_evaluate_async(const ckm_graph* g, int32_t K, uint64_t seed, uint
   if (flags & ~(uint32_t)CKM_F_DET0) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
   if (stage_splits < 0) return fail(CKM_E_INVALID_ARG, "stage_splits = %d < 0", stage_splits);
   const ckm::Plan plan = stage_splits ? ckm::plan_splits(g->n, std::min(stage_splits, L.max_splits))
-                                      : ckm::plan_auto(g->n, K, L.max_splits);
+                                      : ckm::plan_auto(g->n, K, L.max_splits, g->eval_waves);
   DeviceGuard dg(g->device);
   hipError_t e = ckm::launch_evaluate(*g, L, K, seed, flags, plan, ckm::kSrcRound, nullptr,
                                       static_cast<char*>(d_work), static_cast<hipStream_t>(stream));
@@ -397,7 +394,7 @@ ckm_status ckm_eval_schedules_async(const ckm_graph* g, const uint64_t* d_S, int
   if (budget < 0) return fail(CKM_E_INVALID_ARG, "budget = %lld < 0", (long long)budget);
   if (!d_peak || !d_cost || !d_feasible || !d_best_k)
     return fail(CKM_E_INVALID_ARG, "NULL peak, cost, feasible or best_k");
-  const ckm::Plan plan = ckm::plan_auto(g->n, K, L.max_splits);
+  const ckm::Plan plan = ckm::plan_auto(g->n, K, L.max_splits, g->eval_waves);
   DeviceGuard dg(g->device);
   hipError_t e = ckm::launch_evaluate(*g, L, K, 0, 0, plan, ckm::kSrcUser, d_S, static_cast<char*>(d_work),
                                       static_cast<hipStream_t>(stream));
@@ -488,7 +485,7 @@ ckm_status ckm_threshold_eval_async(const ckm_graph* g, const double* d_s_frac, 
   if (budget < 0) return fail(CKM_E_INVALID_ARG, "budget = %lld < 0", (long long)budget);
   if (!d_peak || !d_cost || !d_feasible || !d_best_k)
     return fail(CKM_E_INVALID_ARG, "NULL peak, cost, feasible or best_k");
-  const ckm::Plan plan = ckm::plan_auto(g->n, K, L.max_splits);
+  const ckm::Plan plan = ckm::plan_auto(g->n, K, L.max_splits, g->eval_waves);
   DeviceGuard dg(g->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* work = static_cast<char*>(d_work);

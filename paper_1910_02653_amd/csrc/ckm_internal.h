@@ -17,6 +17,7 @@ struct ckm_graph {
   int32_t num_edges = 0;
   int device = 0;
   double base = 0.0;          // M_in + 2 M_param (eq. U_init constant overhead)
+  int32_t eval_waves = 1;     // resident evaluate waves per CU for this n (work plan sizing)
   void* d_mem = nullptr;      // one allocation holding every array below
   const double* d_M = nullptr;
   const double* d_C = nullptr;
@@ -81,8 +82,12 @@ Layout make_layout(int32_t n, int32_t K);
 struct Plan {
   int32_t items = 1, kind = 0, P = 0, T0 = 0, R1 = 0, R2 = 0;
 };
-Plan plan_auto(int32_t n, int32_t K, int32_t max_items);
+Plan plan_auto(int32_t n, int32_t K, int32_t max_items, int32_t waves_per_cu);
 Plan plan_splits(int32_t n, int32_t splits);
+
+// Resident evaluate waves per CU for a graph of n nodes (the runtime's
+// occupancy figure for the kernel variant and LDS size n selects).
+int32_t eval_waves_per_cu(int32_t n);
 
 // Kernel launchers (defined in ckm_kernels.hip). They only enqueue work.
 hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,

@@ -355,6 +355,61 @@ struct RowReg {
   __device__ uint32_t at_word(uint32_t i) const { return w[i]; }  // wave-uniform word index
 };
 
+// A row of up to 32 * kVecs words (kVecs = 2 or 4) in the lane's vector
+// registers: kVecs 32-word vectors, locals of the kernel held here by
+// reference. Word w is element w % 32 of vector w / 32: a wave-uniform branch
+// picks the vector, s_set_gpr_idx the element. The asm statements keep the
+// branches distinct; merged, they would become one access through a phi of
+// pointers, and the vectors would move to scratch memory.
+template <int kVecs>
+struct RowRegV {
+  u32x32 &v0, &v1, &v2, &v3;
+  __device__ uint32_t at_word(uint32_t i) const {
+    const uint32_t q = i >> 5, r = i & 31u;
+    uint32_t x;
+    if (q == 0) {
+      x = v0[r];
+      asm("; row word 0" : "+v"(x));
+    } else if (kVecs == 2 || q == 1) {
+      x = v1[r];
+      asm("; row word 1" : "+v"(x));
+    } else if (q == 2) {
+      x = v2[r];
+      asm("; row word 2" : "+v"(x));
+    } else {
+      x = v3[r];
+      asm("; row word 3" : "+v"(x));
+    }
+    return x;
+  }
+  __device__ void set(uint32_t i, uint32_t x) const {
+    const uint32_t q = i >> 5, r = i & 31u;
+    if (q == 0) {
+      v0[r] = x;
+      asm volatile("; row set 0");
+    } else if (kVecs == 2 || q == 1) {
+      v1[r] = x;
+      asm volatile("; row set 1");
+    } else if (q == 2) {
+      v2[r] = x;
+      asm volatile("; row set 2");
+    } else {
+      v3[r] = x;
+      asm volatile("; row set 3");
+    }
+  }
+  struct WordRef {
+    const RowRegV& row;
+    uint32_t i;
+    __device__ WordRef& operator=(uint32_t x) {
+      row.set(i, x);
+      return *this;
+    }
+    __device__ operator uint32_t() const { return row.at_word(i); }
+  };
+  __device__ WordRef word(int i) const { return WordRef{*this, (uint32_t)i}; }
+};
+
 __device__ __forceinline__ uint32_t bit(uint32_t word, int pos) { return (word >> pos) & 1u; }
 
 // (a & b) | c as one VALU instruction (b wave-uniform).
@@ -651,12 +706,57 @@ __device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, RowB
   stage_cost = sc.cost;
 }
 
+// After stage t: S_{t+1} becomes the next stage's S_t. With S_{t+1} in
+// registers it is copied into the LDS row (its words end at (t+1)/32; the LDS
+// row is zero above that); with both rows in LDS they swap roles.
+__device__ __forceinline__ void next_stage(Row& A, Row& B, int) {
+  const Row tmp = A;
+  A = B;
+  B = tmp;
+}
+__device__ __forceinline__ void next_stage(Row& A, RowReg& B, int t) {
+  const int last = (t + 1) >> 5;
+#pragma unroll
+  for (int w = 0; w < kRegRowWords; ++w)
+    if (w <= last) A.word(w) = B.w[w];
+}
+template <int kVecs>
+__device__ __forceinline__ void next_stage(Row& A, RowRegV<kVecs>& B, int t) {
+  const int last = (t + 1) >> 5;
+#pragma unroll
+  for (int r = 0; r < 32; ++r) {
+    if (r <= last) A.word(r) = B.v0[r];
+    if (32 + r <= last) A.word(32 + r) = B.v1[r];
+    if (kVecs == 4) {
+      if (64 + r <= last) A.word(64 + r) = B.v2[r];
+      if (96 + r <= last) A.word(96 + r) = B.v3[r];
+    }
+  }
+}
+
+// The stages t0 .. t1-1 of one work item: fold each stage's peak and cost.
+template <int kSrc, typename RowB>
+__device__ __forceinline__ void run_item(const EvalArgs& a, int t0, int t1, uint32_t k, bool det_lane, uint32_t rk,
+                                         Row& A, RowB& B, double& seg_peak, int64_t& seg_cost) {
+  if (t0 >= t1) return;
+  gen_row<kSrc>(a, t0, k, det_lane, rk, A);
+  for (int t = t0; t < t1; ++t) {
+    gen_row<kSrc>(a, t + 1, k, det_lane, rk, B);
+    double sp, sc;
+    eval_stage(a, t, A, B, sp, sc);
+    seg_peak = fmax(seg_peak, sp);
+    seg_cost += (int64_t)sc;
+    next_stage(A, B, t);
+  }
+}
+
 // One wave per workgroup: 64 candidates over one work item (a range of
-// stages). kBReg: the S_{t+1} row lives in vector registers and is copied to
-// the LDS row at the end of each stage (n < 1024), halving the LDS a wave
-// needs; otherwise both rows are in LDS and swap roles. kSrc: where the S
-// rows come from (kSrcRound, kSrcUser, kSrcThreshold).
-template <bool kBReg, int kSrc>
+// stages). kRegW: 32, 64 or 128 when the S_{t+1} row lives in vector
+// registers (rows of up to that many words) and is copied to the LDS row at
+// the end of each stage, which halves the LDS a wave needs; 0 when both rows
+// are in LDS and swap roles. kSrc: where the S rows come from (kSrcRound,
+// kSrcUser, kSrcThreshold).
+template <int kRegW, int kSrc>
 __global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
   extern __shared__ uint32_t lds[];
   const int lane = threadIdx.x;
@@ -675,41 +775,18 @@ __global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
   item_range(a, item, t0, t1);
   double seg_peak = -INFINITY;
   int64_t seg_cost = 0;
-  if (kBReg) {
-    RowReg B;
-    B.w = (u32x32)0u;
-    if (t0 < t1) {
-      gen_row<kSrc>(a, t0, k, det_lane, rk, A);
-      for (int t = t0; t < t1; ++t) {
-        gen_row<kSrc>(a, t + 1, k, det_lane, rk, B);
-        double sp, sc;
-        eval_stage(a, t, A, B, sp, sc);
-        seg_peak = fmax(seg_peak, sp);
-        seg_cost += (int64_t)sc;
-        // S_{t+1} becomes the next stage's S_t (its words end at (t+1)/32;
-        // the LDS row is zero above that)
-        const int last = (t + 1) >> 5;
-#pragma unroll
-        for (int w = 0; w < kRegRowWords; ++w)
-          if (w <= last) A.word(w) = B.w[w];
-      }
-    }
-  } else {
+  if constexpr (kRegW == 0) {
     Row B{wave_lds + (size_t)a.row_words * 256 + 4 * lane};
     for (int w = 0; w < a.row_words; ++w) B.word(w) = 0u;
-    if (t0 < t1) {
-      gen_row<kSrc>(a, t0, k, det_lane, rk, A);
-      for (int t = t0; t < t1; ++t) {
-        gen_row<kSrc>(a, t + 1, k, det_lane, rk, B);
-        double sp, sc;
-        eval_stage(a, t, A, B, sp, sc);
-        seg_peak = fmax(seg_peak, sp);
-        seg_cost += (int64_t)sc;
-        const Row tmp = A;
-        A = B;
-        B = tmp;
-      }
-    }
+    run_item<kSrc>(a, t0, t1, k, det_lane, rk, A, B, seg_peak, seg_cost);
+  } else if constexpr (kRegW == kRegRowWords) {
+    RowReg B;
+    B.w = (u32x32)0u;
+    run_item<kSrc>(a, t0, t1, k, det_lane, rk, A, B, seg_peak, seg_cost);
+  } else {
+    u32x32 b0 = (u32x32)0u, b1 = (u32x32)0u, b2 = (u32x32)0u, b3 = (u32x32)0u;
+    RowRegV<kRegW / 32> B{b0, b1, b2, b3};
+    run_item<kSrc>(a, t0, t1, k, det_lane, rk, A, B, seg_peak, seg_cost);
   }
   // fold the item's result into the candidate's totals: max of the stage
   // peaks, sum of the stage costs (exact integers, any order)
@@ -1156,6 +1233,42 @@ hipError_t launch_threshold_keys(const ckm_graph& g, const Layout& L, const doub
   return hipGetLastError();
 }
 
+// Width of the register row for rows of `words` 32-bit words (0: LDS rows).
+static int reg_row_width(int32_t words) {
+  return words <= 32 ? 32 : words <= 64 ? 64 : words <= 128 ? 128 : 0;
+}
+
+template <int kSrc>
+static void (*eval_kernel_w(int w))(EvalArgs) {
+  switch (w) {
+    case 32: return ckm_eval_kernel<32, kSrc>;
+    case 64: return ckm_eval_kernel<64, kSrc>;
+    case 128: return ckm_eval_kernel<128, kSrc>;
+    default: return ckm_eval_kernel<0, kSrc>;
+  }
+}
+
+static void (*eval_kernel_for(int32_t words, int src))(EvalArgs) {
+  const int w = reg_row_width(words);
+  if (src == kSrcUser) return eval_kernel_w<kSrcUser>(w);
+  if (src == kSrcThreshold) return eval_kernel_w<kSrcThreshold>(w);
+  return eval_kernel_w<kSrcRound>(w);
+}
+
+static size_t eval_lds_bytes(int32_t words) {
+  return (reg_row_width(words) ? 1u : 2u) * (size_t)words * kWave * sizeof(uint32_t);
+}
+
+int32_t eval_waves_per_cu(int32_t n) {
+  const int32_t words = (n >> 5) + 1;
+  const void* fn = (const void*)eval_kernel_for(words, kSrcRound);
+  const size_t lds = eval_lds_bytes(words);
+  if (lds > 65536) (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  int blocks = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, kWave, lds) != hipSuccess || blocks < 1) blocks = 1;
+  return blocks;
+}
+
 hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
                            uint32_t flags, const Plan& plan, int src, const uint64_t* s_user, char* work,
                            hipStream_t stream) {
@@ -1191,15 +1304,8 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   a.part_cost = at<int64_t>(work, L.part_cost_off);
   a.hdr = at<int32_t>(work, L.hdr_off);
   const int groups = (K + kWave - 1) / kWave;
-  const bool breg = a.row_words <= kRegRowWords;
-  const size_t lds_bytes = (breg ? 1u : 2u) * (size_t)a.row_words * kWave * sizeof(uint32_t);
-  void (*fn)(EvalArgs);
-  if (src == kSrcUser)
-    fn = breg ? ckm_eval_kernel<true, kSrcUser> : ckm_eval_kernel<false, kSrcUser>;
-  else if (src == kSrcThreshold)
-    fn = breg ? ckm_eval_kernel<true, kSrcThreshold> : ckm_eval_kernel<false, kSrcThreshold>;
-  else
-    fn = breg ? ckm_eval_kernel<true, kSrcRound> : ckm_eval_kernel<false, kSrcRound>;
+  void (*fn)(EvalArgs) = eval_kernel_for(a.row_words, src);
+  const size_t lds_bytes = eval_lds_bytes(a.row_words);
   if (lds_bytes > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     if (e != hipSuccess) return e;

@@ -187,6 +187,28 @@ def test_random_dag_sweep(n, K, kind):
     check_full(w, gpu_round_eval(w, budget=med), budget=med)
 
 
+@pytest.mark.parametrize("n", [1023, 1024, 1500, 2047, 2048, 3000])
+def test_register_row_widths(n):
+    """Rows of 32, 64 and 128 words in registers (n < 1024, < 2048, < 4096):
+    graphs on both sides of each boundary, sampled candidates against the
+    oracle, the rest through the argmin and the best rows."""
+    w = wl.random_dag(n, seed=n, K=70, window=40, max_deg=3, max_size=1000, max_cost=1000, s_kind="uniform",
+                      budget_pct=55.0)
+    log("register rows n=%d" % n)
+    got = gpu_round_eval(w)
+    ks = [0, 1, 63, 64, 69]
+    orc = oracle_candidates(w, ks)
+    for k in ks:
+        assert (int(got["peak"][k]), int(got["cost"][k])) == orc[k], k
+    budget = int(np.median(got["peak"]))
+    got2 = gpu_round_eval(w, budget=budget)
+    assert np.array_equal(got2["peak"], got["peak"]) and np.array_equal(got2["cost"], got["cost"])
+    bk = lexi_best(got2["peak"], got2["cost"], budget)
+    assert got2["best_k"] == bk >= 0
+    assert (int(got2["peak"][bk]), int(got2["cost"][bk])) == oracle_candidates(w, [bk])[bk]
+    check_rows(w, got2, bk)
+
+
 def test_dense_wide_graph():
     """Many deps and users per node (fan-in / fan-out up to 40)."""
     w = wl.random_dag(150, seed=11, K=70, max_deg=40, window=150, s_kind="uniform", budget_pct=60.0)
