@@ -220,7 +220,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=4, help="workload 1..5 (4 = transformer stack)")
     ap.add_argument("--splits", type=int, default=0, help="stage splits per 64 candidates (0 = auto)")
-    ap.add_argument("--cpu-sample", type=int, default=256, help="oracle candidates to time (0 = skip)")
+    ap.add_argument("--cpu-sample", type=int, default=1024, help="oracle candidates to time (0 = skip)")
     ap.add_argument("--sched-steps", type=int, default=20,
                     help="timed calls of the supplied-schedule evaluation (0 = skip)")
     ap.add_argument("--thr-steps", type=int, default=20,
