@@ -69,11 +69,12 @@ Plan plan_splits(int32_t n, int32_t splits) {
 }
 
 Plan plan_auto(int32_t n, int32_t K, int32_t max_items, int32_t waves_per_cu) {
-  // About eight items per resident wave slot. The upper half of the stages
-  // goes in items of P stages, the lower half (a quarter of the work) in as
-  // many ranges, each about a third of an upper item, so the launch ends on
-  // small items. Each item regenerates one S row; the finer balance is worth
-  // more than that on this workload range.
+  // About eight items per resident wave slot. Stages from T0 = n/16 up go in
+  // items of P stages (one stage when there are enough items), the first
+  // n/16 stages in as many small ranges, so the launch, which dispatches
+  // the most expensive items first, ends on very short ones. Each item
+  // regenerates one S row; the shorter tail is worth more than that (at
+  // n = 1009, K = 1024: 0.94 ms against 1.00 with T0 = n/2).
   const int64_t groups = (K + kWave - 1) / kWave;
   // resident evaluate waves on the chip's 256 CUs
   const int64_t slots = 256 * (int64_t)std::max(1, waves_per_cu);
@@ -81,7 +82,7 @@ Plan plan_auto(int32_t n, int32_t K, int32_t max_items, int32_t waves_per_cu) {
   if (n < 8 || target < 4) return plan_splits(n, (int32_t)std::min<int64_t>(target, max_items));
   Plan p;
   p.kind = 1;
-  p.T0 = n / 2;
+  p.T0 = std::max(1, n / 16);
   const int64_t half = std::max<int64_t>(1, target / 2);
   p.P = (int32_t)std::max<int64_t>(1, (n - p.T0 + half - 1) / half);
   for (;;) {
