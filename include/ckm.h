@@ -121,7 +121,11 @@ ckm_status ckm_round_eval(const ckm_graph* g, const double* s_frac, int64_t ld, 
  * calls that may run concurrently. The three stages run in the order
  * quantize -> evaluate -> select, on one work buffer. */
 
-/* Bytes of work buffer needed for K candidates on graph g. */
+/* Bytes of work buffer for K candidates on graph g. This includes, when the
+ * rounded S rows of all K candidates fit in 1 GiB, room for them; with it the
+ * randomized path rounds each row once instead of twice. A smaller buffer
+ * that still holds everything else is accepted, and the rows are then
+ * rounded inside the evaluate stage (same results). */
 ckm_status ckm_workspace_size(const ckm_graph* g, int32_t K, size_t* bytes);
 
 /* Stage a1: thresholds q (Section 5.1) and the deterministic-rounding bits of

@@ -127,7 +127,16 @@ Layout make_layout(int32_t n, int32_t K) {
   L.plan_rt_off = off;    off = align256(off + (size_t)n * ((n + 31) / 32) * sizeof(uint32_t));
   L.plan_rpre_off = off;  off = align256(off + (size_t)n * ckm::kMaxNodesWords * sizeof(int32_t));
   L.bbest_off = off;      off = align256(off + (size_t)L.reduce_blocks * 32);
+
   L.total = off;
+  // rounded rows of every candidate, word w of row t at (base(t) + w) * kpad
+  // + k: last, and optional (evaluate rounds in the kernel without them)
+  const size_t kpad = (size_t)((K + kWave - 1) / kWave) * kWave;
+  const size_t full = (size_t)(n >> 5), rem = (size_t)(n & 31);
+  const size_t rows_bytes = kpad * (32 * full * (full + 1) / 2 + rem * (full + 1)) * sizeof(uint32_t);
+  L.rows_on = rows_bytes <= ckm::kRowsMaxBytes;
+  L.rows_off = off;
+  L.total_rows = L.rows_on ? align256(off + rows_bytes) : off;
   return L;
 }
 
@@ -300,7 +309,7 @@ ckm_status ckm_workspace_size(const ckm_graph* g, int32_t K, size_t* bytes) {
   if (!g || !bytes) return fail(CKM_E_INVALID_ARG, "NULL graph or bytes");
   if (K < 1) return fail(CKM_E_INVALID_ARG, "K = %d < 1", K);
   if (K > CKM_MAX_CANDIDATES) return fail(CKM_E_UNSUPPORTED, "K = %d > %d", K, CKM_MAX_CANDIDATES);
-  *bytes = ckm::make_layout(g->n, K).total;
+  *bytes = ckm::make_layout(g->n, K).total_rows;
   return CKM_OK;
 }
 
@@ -313,6 +322,7 @@ static ckm_status check_work(const ckm_graph* g, int32_t K, void* d_work, size_t
   *L = ckm::make_layout(g->n, K);
   if (work_bytes < L->total)
     return fail(CKM_E_INVALID_ARG, "work buffer of %zu bytes, %zu needed", work_bytes, L->total);
+  L->rows_on = L->rows_on && work_bytes >= L->total_rows;
   return CKM_OK;
 }
 
@@ -710,7 +720,7 @@ ckm_status ckm_max_batch(const ckm_graph* g, const double* s_frac, int64_t ld, i
   const size_t o_b = off;  off = align256(off + (size_t)K * 8);
   const size_t o_bk = off; off = align256(off + 8);
   const size_t o_bb = off; off = align256(off + 8);
-  const size_t o_w = off;  off = align256(off + L.total);
+  const size_t o_w = off;  off = align256(off + L.total_rows);
   char* d = nullptr;
   hipError_t e = hipMalloc(&d, off);
   if (e != hipSuccess)
@@ -728,11 +738,11 @@ ckm_status ckm_max_batch(const ckm_graph* g, const double* s_frac, int64_t ld, i
       st = fail_hip(e, "hipMemcpy2D S*");
       break;
     }
-    if ((st = ckm_quantize_async(g, reinterpret_cast<const double*>(d + o_s), n, d + o_w, L.total, stream)) != CKM_OK ||
-        (st = ckm_evaluate_async(g, K, seed, flags, 0, d + o_w, L.total, stream)) != CKM_OK ||
+    if ((st = ckm_quantize_async(g, reinterpret_cast<const double*>(d + o_s), n, d + o_w, L.total_rows, stream)) != CKM_OK ||
+        (st = ckm_evaluate_async(g, K, seed, flags, 0, d + o_w, L.total_rows, stream)) != CKM_OK ||
         (st = ckm_max_batch_async(g, K, budget, cost_cap, reinterpret_cast<int64_t*>(d + o_b),
                                   reinterpret_cast<int32_t*>(d + o_bk), reinterpret_cast<int64_t*>(d + o_bb), nullptr,
-                                  d + o_w, L.total, stream)) != CKM_OK)
+                                  d + o_w, L.total_rows, stream)) != CKM_OK)
       break;
     if ((e = hipMemcpyAsync(batch, d + o_b, (size_t)K * 8, hipMemcpyDeviceToHost, stream)) != hipSuccess ||
         (e = hipMemcpyAsync(best_k, d + o_bk, 4, hipMemcpyDeviceToHost, stream)) != hipSuccess ||
@@ -784,7 +794,7 @@ ckm_status ckm_round_eval(const ckm_graph* g, const double* s_frac, int64_t ld, 
   const size_t o_st = off;   off = align256(off + 8);
   const size_t o_bS = off;   off = align256(off + rows_bytes);
   const size_t o_bR = off;   off = align256(off + rows_bytes);
-  const size_t o_w = off;    off = align256(off + L.total);
+  const size_t o_w = off;    off = align256(off + L.total_rows);
   char* d = nullptr;
   hipError_t e = hipMalloc(&d, off);
   if (e != hipSuccess)
@@ -808,7 +818,7 @@ ckm_status ckm_round_eval(const ckm_graph* g, const double* s_frac, int64_t ld, 
                               reinterpret_cast<uint8_t*>(d + o_feas), reinterpret_cast<int32_t*>(d + o_bk),
                               best_S ? reinterpret_cast<uint64_t*>(d + o_bS) : nullptr,
                               best_R ? reinterpret_cast<uint64_t*>(d + o_bR) : nullptr,
-                              reinterpret_cast<int32_t*>(d + o_st), d + o_w, L.total, stream);
+                              reinterpret_cast<int32_t*>(d + o_st), d + o_w, L.total_rows, stream);
     if (st != CKM_OK) break;
     struct Copy { void* dst; size_t off, bytes; } copies[] = {
         {peak, o_peak, (size_t)K * 8}, {cost, o_cost, (size_t)K * 8}, {feasible, o_feas, (size_t)K},

@@ -40,7 +40,13 @@ enum : int {
   kSrcRound = 0,      // randomized rounding of S* (deterministic candidate 0 under CKM_F_DET0)
   kSrcUser = 1,       // the caller's integral S matrices
   kSrcThreshold = 2,  // threshold rounding [clamp(S*) > p_k], one threshold per candidate
+  kSrcRows = 3,       // randomized rounding done beforehand into the work buffer's row array
 };
+
+// The rounded-row array of the randomized path is used when it fits in this
+// many bytes (it holds K * n^2 / 64 words); larger problems round in the
+// evaluate kernel.
+constexpr size_t kRowsMaxBytes = (size_t)1 << 30;
 
 // Host-side builder of the per-node records the evaluate kernel reads
 // (layout documented with NodeRec in ckm_kernels.hip). Writes n records.
@@ -67,7 +73,11 @@ struct Layout {
          // R transposed (n columns of ceil(n/32) words) and per-row word ranks
          plan_rt_off = 0, plan_rpre_off = 0,
          bbest_off = 0,  // per-block best of the batch multipliers
-         total = 0;
+         total = 0,        // bytes every call needs
+         rows_off = 0,     // rounded rows (kSrcRows), past `total`
+         total_rows = 0;   // total plus the rounded rows when they are used
+  bool rows_on = false;    // the rounded rows fit kRowsMaxBytes (and, after
+                           // check_work, the caller's buffer holds them)
 };
 
 Layout make_layout(int32_t n, int32_t K);

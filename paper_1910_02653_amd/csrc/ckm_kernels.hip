@@ -292,6 +292,8 @@ struct EvalArgs {
   const uint32_t* __restrict__ s_user;  // kSrcUser: caller-supplied S rows ([K][n][s_words])
   int32_t s_words;                      // 32-bit words per supplied row
   const uint32_t* __restrict__ rank;    // kSrcThreshold: [K] threshold ranks (q holds the keys)
+  const uint32_t* __restrict__ rows;    // kSrcRows: rounded rows, word w of row t at rows_at(t, w)
+  int32_t kpad;                         // kSrcRows: candidates per row word (64 * groups)
   int64_t* __restrict__ part_peak;   // [K] running max over work items
   int64_t* __restrict__ part_cost;   // [K] running sum over work items
   int32_t* __restrict__ hdr;
@@ -426,6 +428,36 @@ __device__ __forceinline__ uint32_t umin1(uint32_t x) {
   return y;
 }
 
+// Words before row r in the rounded-row array: sum over r' < r of r'/32 + 1
+// (row r' has words 0 .. r'/32).
+__host__ __device__ __forceinline__ size_t row_base(int r) {
+  const size_t full = (size_t)(r >> 5), rem = (size_t)(r & 31);
+  return 32 * full * (full + 1) / 2 + rem * (full + 1);
+}
+
+// Rounds every row once for the evaluate kernel's kSrcRows source: block
+// (candidate group, row r), lane = candidate. The same bits gen_row would
+// produce: randomized rounding (Section 5.1), or the deterministic row for
+// candidate 0 under CKM_F_DET0.
+__global__ void __launch_bounds__(kWave) ckm_round_rows_kernel(const uint32_t* __restrict__ q,
+                                                               const uint32_t* __restrict__ det, int32_t ldq,
+                                                               int32_t det_words, uint32_t key0, uint32_t key1,
+                                                               uint32_t det0, int32_t kpad,
+                                                               uint32_t* __restrict__ rows) {
+  const int r = blockIdx.y;
+  const uint32_t k = blockIdx.x * kWave + threadIdx.x;
+  const bool det_lane = det0 && k == 0;
+  cptr<uint32_t> qrow = as_const(q) + (size_t)r * ldq;
+  const uint32_t* drow = det + (size_t)r * det_words;
+  uint32_t* dst = rows + row_base(r) * (size_t)kpad + k;
+  const int nw = (r >> 5) + 1;
+  for (int w = 0; w < nw; ++w) {
+    uint32_t word = round_word<true>(qrow, w, r, k, key0, key1);
+    if (det_lane) word = drow[w];
+    dst[(size_t)w * kpad] = word;
+  }
+}
+
 // Row r of the candidate into words 0 .. r/32, from the source kSrc:
 // randomized rounding of S*, the caller's rows (a.s_user), or threshold
 // rounding (lane threshold rank rk against the keys in q).
@@ -435,6 +467,13 @@ __device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bo
   const int nw = (r >> 5) + 1;
   if (r >= a.n) {  // S after the last stage: nothing is kept
     for (int w = 0; w < nw; ++w) dst.word(w) = 0u;
+    return;
+  }
+  if (kSrc == kSrcRows) {
+    // rows rounded beforehand: word w of row r for candidate k is at
+    // (row_base(r) + w) * kpad + k, contiguous across the wave
+    const uint32_t* src = a.rows + row_base(r) * (size_t)a.kpad + k;
+    for (int w = 0; w < nw; ++w) dst.word(w) = src[(size_t)w * a.kpad];
     return;
   }
   if (kSrc == kSrcUser) {
@@ -1250,6 +1289,7 @@ static void (*eval_kernel_w(int w))(EvalArgs) {
 
 static void (*eval_kernel_for(int32_t words, int src))(EvalArgs) {
   const int w = reg_row_width(words);
+  if (src == kSrcRows) return eval_kernel_w<kSrcRows>(w);
   if (src == kSrcUser) return eval_kernel_w<kSrcUser>(w);
   if (src == kSrcThreshold) return eval_kernel_w<kSrcThreshold>(w);
   return eval_kernel_w<kSrcRound>(w);
@@ -1278,6 +1318,16 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   a.s_user = reinterpret_cast<const uint32_t*>(s_user);
   a.s_words = L.row_words;
   a.rank = at<const uint32_t>(work, L.thr_rank_off);
+  a.rows = at<const uint32_t>(work, L.rows_off);
+  a.kpad = ((K + kWave - 1) / kWave) * kWave;
+  if (src == kSrcRound && L.rows_on) {
+    // round every row once; the evaluate kernel then streams them
+    hipLaunchKernelGGL(ckm_round_rows_kernel, dim3((K + kWave - 1) / kWave, g.n), dim3(kWave), 0, stream,
+                       at<const uint32_t>(work, L.q_off), at<const uint32_t>(work, L.det_off), L.ldq, L.det_words,
+                       (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32), (flags & CKM_F_DET0) ? 1u : 0u,
+                       a.kpad, at<uint32_t>(work, L.rows_off));
+    src = kSrcRows;
+  }
   a.items = plan.items;
   a.kind = plan.kind;
   a.P = plan.P;
