@@ -2,8 +2,10 @@
 
 A step is one pass of the whole path over the transformer-stack workload
 (n = 1009 nodes, K = 1024 candidates, 25 % budget): thresholds from S*,
-rounding + Algorithm 2 repair + memory/cost simulation of every candidate,
-per-candidate reduction, argmin, and the best candidate's S and R rows.
+rounding of every candidate's S rows (ckm_round_async), Algorithm 2 repair +
+memory/cost simulation of every candidate (ckm_evaluate_async, the
+dominant kernel, bracketed by HIP events on its stream), per-candidate
+reduction, argmin, and the best candidate's S and R rows.
 The graph and S* are resident in HBM before timing starts.
 
 Prints one JSON line. `value` is candidate schedules evaluated per second.
@@ -253,9 +255,10 @@ def main():
 
     def step(ev=None):
         g.quantize_async(d_s, work, stream)
+        g.round_async(K, w.seed, 0, work, stream)
         if ev is not None:
             ev[0].record(stream)
-        g.evaluate_async(K, w.seed, 0, work, stage_splits=args.splits, stream=stream)
+        g.evaluate_async(K, w.seed, ckm.F_ROUNDED, work, stage_splits=args.splits, stream=stream)
         if ev is not None:
             ev[1].record(stream)
         g.select_async(K, w.seed, w.budget, 0, out, work, stream)

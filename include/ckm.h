@@ -59,7 +59,11 @@ typedef enum {
   CKM_E_DEVICE = 6       /* a HIP runtime call failed (message has the HIP error) */
 } ckm_status;
 
-enum { CKM_F_DET0 = 1u }; /* candidate 0 = deterministic rounding S* > 0.5 (Algorithm 2) */
+enum {
+  CKM_F_DET0 = 1u,    /* candidate 0 = deterministic rounding S* > 0.5 (Algorithm 2) */
+  CKM_F_ROUNDED = 2u  /* ckm_evaluate_async / ckm_select_async only: ckm_round_async has
+                         rounded the rows (same K, seed, CKM_F_DET0) on this work buffer */
+};
 
 #define CKM_MAX_NODES 4096
 #define CKM_MAX_CANDIDATES (1 << 24)
@@ -135,12 +139,24 @@ ckm_status ckm_workspace_size(const ckm_graph* g, int32_t K, size_t* bytes);
 ckm_status ckm_quantize_async(const ckm_graph* g, const double* d_s_frac, int64_t ld,
                               void* d_work, size_t work_bytes, void* stream);
 
+/* Stage a2 on its own: rounds every candidate's S rows (Section 5.1) once
+ * into the work buffer's row array, after ckm_quantize_async. It does
+ * nothing when the buffer or the problem has no room for them (see
+ * ckm_workspace_size); ckm_evaluate_async then rounds inside. flags: 0 or
+ * CKM_F_DET0. Call ckm_evaluate_async with CKM_F_ROUNDED and the same K,
+ * seed and CKM_F_DET0 to use the rows; without CKM_F_ROUNDED it rounds them
+ * again itself. */
+ckm_status ckm_round_async(const ckm_graph* g, int32_t K, uint64_t seed, uint32_t flags, void* d_work,
+                           size_t work_bytes, void* stream);
+
 /* Stages a2-a5 for candidates 0..K-1: rounding, Algorithm 2's R repair,
  * memory simulation and cost. Leaves each candidate's peak and cost in the
  * work buffer (reset at the start of every call). stage_splits = number of
  * stage ranges each group of 64 candidates is split into, 1..n (0 =
  * automatic: ranges cut and ordered for load balance); results do not depend
- * on it. */
+ * on it. flags: CKM_F_DET0, and CKM_F_ROUNDED when ckm_round_async has
+ * rounded the rows (with the same K, seed and CKM_F_DET0) since the last
+ * ckm_quantize_async on this buffer; the rows are then not rounded again. */
 ckm_status ckm_evaluate_async(const ckm_graph* g, int32_t K, uint64_t seed, uint32_t flags,
                               int32_t stage_splits, void* d_work, size_t work_bytes, void* stream);
 

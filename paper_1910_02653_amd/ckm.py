@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(HERE, "libckm.so")
 
 OK, E_INVALID_ARG, E_GRAPH, E_OVERFLOW, E_UNSUPPORTED, E_NOMEM, E_DEVICE = range(7)
 F_DET0 = 1
+F_ROUNDED = 2
 MAX_NODES = 4096
 MAX_CANDIDATES = 1 << 24
 MAX_THRESHOLDS = 1 << 16
@@ -24,7 +25,7 @@ MAX_THRESHOLDS = 1 << 16
 # every extern "C" symbol declared in include/ckm.h
 EXPORTS = (
     "ckm_graph_create", "ckm_graph_destroy", "ckm_graph_num_nodes", "ckm_round_eval",
-    "ckm_workspace_size", "ckm_quantize_async", "ckm_evaluate_async", "ckm_select_async",
+    "ckm_workspace_size", "ckm_quantize_async", "ckm_round_async", "ckm_evaluate_async", "ckm_select_async",
     "ckm_round_eval_async", "ckm_eval_schedules", "ckm_eval_schedules_async", "ckm_threshold_eval",
     "ckm_threshold_eval_async", "ckm_plan", "ckm_plan_async", "ckm_max_batch",
     "ckm_max_batch_async", "ckm_last_error",
@@ -67,6 +68,8 @@ def lib():
         L.ckm_workspace_size.restype = C.c_int
         L.ckm_quantize_async.argtypes = [p, p, i64, p, sz, p]
         L.ckm_quantize_async.restype = C.c_int
+        L.ckm_round_async.argtypes = [p, i32, u64, u32, p, sz, p]
+        L.ckm_round_async.restype = C.c_int
         L.ckm_evaluate_async.argtypes = [p, i32, u64, u32, i32, p, sz, p]
         L.ckm_evaluate_async.restype = C.c_int
         L.ckm_select_async.argtypes = [p, i32, u64, i64, u32, p, p, p, p, p, p, p, p, sz, p]
@@ -253,6 +256,10 @@ class Graph:
     def quantize_async(self, d_s_frac, work, stream=None):
         _check(lib().ckm_quantize_async(self._h, _dev_ptr(d_s_frac), d_s_frac.stride(0), _dev_ptr(work),
                                         work.numel() * work.element_size(), _stream_ptr(stream)))
+
+    def round_async(self, K, seed, flags, work, stream=None):
+        _check(lib().ckm_round_async(self._h, int(K), int(seed), int(flags), _dev_ptr(work),
+                                     work.numel() * work.element_size(), _stream_ptr(stream)))
 
     def evaluate_async(self, K, seed, flags, work, stage_splits: int = 0, stream=None):
         _check(lib().ckm_evaluate_async(self._h, int(K), int(seed), int(flags), int(stage_splits),

@@ -341,12 +341,25 @@ ckm_status ckm_quantize_async(const ckm_graph* g, const double* d_s_frac, int64_
   return e == hipSuccess ? CKM_OK : fail_hip(e, "quantize launch");
 }
 
+ckm_status ckm_round_async(const ckm_graph* g, int32_t K, uint64_t seed, uint32_t flags, void* d_work,
+                           size_t work_bytes, void* stream) {
+  Layout L;
+  ckm_status st = check_work(g, K, d_work, work_bytes, &L);
+  if (st != CKM_OK) return st;
+  if (flags & ~(uint32_t)CKM_F_DET0) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
+  DeviceGuard dg(g->device);
+  hipError_t e = ckm::launch_round_rows(*g, L, K, seed, flags, static_cast<char*>(d_work),
+                                        static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? CKM_OK : fail_hip(e, "round launch");
+}
+
 ckm_status ckm_evaluate_async(const ckm_graph* g, int32_t K, uint64_t seed, uint32_t flags,
                               int32_t stage_splits, void* d_work, size_t work_bytes, void* stream) {
   Layout L;
   ckm_status st = check_work(g, K, d_work, work_bytes, &L);
   if (st != CKM_OK) return st;
-  if (flags & ~(uint32_t)CKM_F_DET0) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
+  if (flags & ~(uint32_t)(CKM_F_DET0 | CKM_F_ROUNDED))
+    return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
   if (stage_splits < 0) return fail(CKM_E_INVALID_ARG, "stage_splits = %d < 0", stage_splits);
   const ckm::Plan plan = stage_splits ? ckm::plan_splits(g->n, std::min(stage_splits, L.max_splits))
                                       : ckm::plan_auto(g->n, K, L.max_splits, g->eval_waves);
@@ -364,7 +377,8 @@ ckm_status ckm_select_async(const ckm_graph* g, int32_t K, uint64_t seed, int64_
   ckm_status st = check_work(g, K, d_work, work_bytes, &L);
   if (st != CKM_OK) return st;
   if (budget < 0) return fail(CKM_E_INVALID_ARG, "budget = %lld < 0", (long long)budget);
-  if (flags & ~(uint32_t)CKM_F_DET0) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
+  if (flags & ~(uint32_t)(CKM_F_DET0 | CKM_F_ROUNDED))
+    return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
   if (!d_peak || !d_cost || !d_feasible || !d_best_k)
     return fail(CKM_E_INVALID_ARG, "NULL peak, cost, feasible or best_k");
   DeviceGuard dg(g->device);

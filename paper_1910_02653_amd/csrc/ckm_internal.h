@@ -102,6 +102,10 @@ int32_t eval_waves_per_cu(int32_t n);
 // Kernel launchers (defined in ckm_kernels.hip). They only enqueue work.
 hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,
                            char* work, hipStream_t stream);
+// Randomized path: every candidate's S rows rounded once into the work
+// buffer's row array (nothing when L.rows_on is false).
+hipError_t launch_round_rows(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed, uint32_t flags,
+                             char* work, hipStream_t stream);
 // Threshold family: ranks of the K thresholds, their sorted copy, and the
 // keys of S* in place of the quantized thresholds q.
 hipError_t launch_threshold_keys(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,
@@ -116,7 +120,9 @@ hipError_t launch_plan(const ckm_graph& g, const Layout& L, const uint64_t* d_S,
 hipError_t launch_max_batch(const ckm_graph& g, const Layout& L, int32_t K, int64_t budget, int64_t cost_cap,
                             int64_t* d_batch, int32_t* d_best_k, int64_t* d_best_batch, int32_t* d_status,
                             char* work, hipStream_t stream);
-// src: one of kSrcRound, kSrcUser, kSrcThreshold. s_user: for kSrcUser, K
+// src: one of kSrcRound, kSrcUser, kSrcThreshold (kSrcRound streams the row
+// array when L.rows_on, rounding it first unless flags has CKM_F_ROUNDED).
+// s_user: for kSrcUser, K
 // caller-supplied S matrices ([K][n][row_words] 32-bit words).
 hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
                            uint32_t flags, const Plan& plan, int src, const uint64_t* s_user, char* work,

@@ -1309,6 +1309,17 @@ int32_t eval_waves_per_cu(int32_t n) {
   return blocks;
 }
 
+hipError_t launch_round_rows(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed, uint32_t flags,
+                             char* work, hipStream_t stream) {
+  if (!L.rows_on) return hipSuccess;
+  const int32_t kpad = ((K + kWave - 1) / kWave) * kWave;
+  hipLaunchKernelGGL(ckm_round_rows_kernel, dim3((K + kWave - 1) / kWave, g.n), dim3(kWave), 0, stream,
+                     at<const uint32_t>(work, L.q_off), at<const uint32_t>(work, L.det_off), L.ldq, L.det_words,
+                     (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32), (flags & CKM_F_DET0) ? 1u : 0u, kpad,
+                     at<uint32_t>(work, L.rows_off));
+  return hipGetLastError();
+}
+
 hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
                            uint32_t flags, const Plan& plan, int src, const uint64_t* s_user, char* work,
                            hipStream_t stream) {
@@ -1321,11 +1332,11 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   a.rows = at<const uint32_t>(work, L.rows_off);
   a.kpad = ((K + kWave - 1) / kWave) * kWave;
   if (src == kSrcRound && L.rows_on) {
-    // round every row once; the evaluate kernel then streams them
-    hipLaunchKernelGGL(ckm_round_rows_kernel, dim3((K + kWave - 1) / kWave, g.n), dim3(kWave), 0, stream,
-                       at<const uint32_t>(work, L.q_off), at<const uint32_t>(work, L.det_off), L.ldq, L.det_words,
-                       (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32), (flags & CKM_F_DET0) ? 1u : 0u,
-                       a.kpad, at<uint32_t>(work, L.rows_off));
+    // every row rounded once (here, or by an earlier launch_round_rows), then streamed
+    if (!(flags & CKM_F_ROUNDED)) {
+      hipError_t e = launch_round_rows(g, L, K, seed, flags, work, stream);
+      if (e != hipSuccess) return e;
+    }
     src = kSrcRows;
   }
   a.items = plan.items;

@@ -107,5 +107,6 @@ def test_null_arguments_rejected():
     assert L.ckm_plan_async(None, None, None, 0, None, 0, None, None, None, None, 0, None) == ckm.E_INVALID_ARG
     assert L.ckm_max_batch(None, None, 4, 4, 0, 0, 0, 0, None, None, None) == ckm.E_INVALID_ARG
     assert L.ckm_max_batch_async(None, 4, 0, 0, None, None, None, None, None, 0, None) == ckm.E_INVALID_ARG
+    assert L.ckm_round_async(None, 4, 0, 0, None, 0, None) == ckm.E_INVALID_ARG
     assert L.ckm_graph_num_nodes(None) == -1
     L.ckm_graph_destroy(None)

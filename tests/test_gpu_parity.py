@@ -268,6 +268,16 @@ def test_async_stages_and_split_invariance():
             for key in ("peak", "cost", "feasible", "best_S", "best_R"):
                 assert np.array_equal(res[key], ref_out[key]), (splits, key)
             assert res["best_k"] == ref_out["best_k"]
+    # the staged form with rounding on its own (ckm_round_async + CKM_F_ROUNDED)
+    out = g.alloc_outputs(w.K)
+    g.quantize_async(d_s, work)
+    g.round_async(w.K, w.seed, 0, work)
+    g.evaluate_async(w.K, w.seed, ckm.F_ROUNDED, work)
+    g.select_async(w.K, w.seed, budget, ckm.F_ROUNDED, out, work)
+    torch.cuda.synchronize()
+    assert int(out["status"].item()) == ckm.OK
+    assert np.array_equal(out["peak"].cpu().numpy(), ref_out["peak"])
+    assert np.array_equal(ckm.rows_to_numpy(out["best_R"]), ref_out["best_R"])
     # the one-call async form agrees too, on a strided S*
     big = torch.zeros((w.n, w.n + 5), dtype=torch.float64, device="cuda")
     big[:, :w.n] = d_s
@@ -277,6 +287,32 @@ def test_async_stages_and_split_invariance():
     assert np.array_equal(out["peak"].cpu().numpy(), ref_out["peak"])
     assert int(out["best_k"].item()) == ref_out["best_k"]
     g.close()
+
+
+def test_rounded_flag_without_row_array():
+    """n = 4001, K = 4096: the rounded rows would take 4.1 GB, so there is no
+    row array; ckm_round_async does nothing and evaluate with CKM_F_ROUNDED
+    rounds inside, with the same results as the one-call form."""
+    import torch
+    w = wl.config(5)
+    g = ckm.Graph.from_workload(w)
+    try:
+        work = g.alloc_work(w.K)
+        d_s = torch.from_numpy(w.s_frac).cuda()
+        budget = int(w.budget * 2)
+        a = g.alloc_outputs(w.K)
+        g.round_eval_async(d_s, w.K, w.seed, budget, 0, a, work)
+        b = g.alloc_outputs(w.K)
+        g.quantize_async(d_s, work)
+        g.round_async(w.K, w.seed, 0, work)
+        g.evaluate_async(w.K, w.seed, ckm.F_ROUNDED, work)
+        g.select_async(w.K, w.seed, budget, 0, b, work)
+        torch.cuda.synchronize()
+        log("config 5 rounded flag")
+        for key in ("peak", "cost", "feasible", "best_k"):
+            assert torch.equal(a[key], b[key]), key
+    finally:
+        g.close()
 
 
 def test_nan_reported():
