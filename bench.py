@@ -13,7 +13,11 @@ Prints one JSON line. `value` is candidate schedules evaluated per second.
 bandwidth with the algorithmic bytes of bit-packed S and R rows, each
 written once and read once: 4 * n * ceil(n/64) * 8 bytes per candidate.
 `cpu_baseline` times the CPU oracle on a bounded sample of the same
-workload. `supplied_schedules` times the batch evaluation of K given integral
+workload, on every host thread (candidates split across them) and on one.
+`hbm_copy` is the bandwidth a plain device copy reaches on the same GPU, the
+achievable line beside the 8 TB/s peak. `host_round_trip` times the
+synchronous call that takes S* from host memory and returns host results
+(PCIe transfers and the call's own work-buffer allocation included). `supplied_schedules` times the batch evaluation of K given integral
 checkpoint matrices (banded, 30 % of values kept) on the same graph: Algorithm
 2 repair, simulation, argmin and the best R, with the matrices resident in HBM.
 `threshold_family` times K deterministic candidates [clamp(S*) > p_k] on an
@@ -62,18 +66,83 @@ def measured_traffic():
     return d.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, sample: int):
-    """The oracle, single thread, on candidates 0 .. sample-1 of the workload."""
+def host_threads() -> int:
+    """CPU threads for the oracle: this process's CPU set, at most 16."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def cpu_baseline(w, sample: int, single: int):
+    """The oracle on candidates 0 .. sample-1 of the workload, split by
+    candidate over every host thread (each thread runs the unmodified oracle
+    on its own candidates; candidates are independent), and on candidates
+    0 .. single-1 in one thread."""
+    from concurrent.futures import ThreadPoolExecutor
+
     from oracle import ref
     q = ref.quantize(w.s_frac)
+    threads = host_threads()
+
+    def run(ks):
+        for k in ks:
+            ref.eval_candidate(w, k, q=q)
+
     t = time.perf_counter()
-    for k in range(sample):
-        ref.eval_candidate(w, k, q=q)
+    run(range(single))
+    dt1 = time.perf_counter() - t
+    chunks = [range(i, sample, threads) for i in range(threads)]
+    t = time.perf_counter()
+    with ThreadPoolExecutor(threads) as ex:
+        list(ex.map(run, chunks))
     dt = time.perf_counter() - t
-    return {"value": sample / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
+    return {"value": sample / dt, "unit": "candidates/s", "cores": threads, "kind": "oracle",
             "sample": "candidates 0-%d of the same %d-candidate transformer workload (n=%d): "
                       "rounding + Algorithm 2 repair + literal U/FREE simulation per candidate, "
-                      "one thread, %.1f s" % (sample - 1, w.K, w.n, dt)}
+                      "%d threads (candidates split across them), %.1f s wall"
+                      % (sample - 1, w.K, w.n, threads, dt),
+            "single_thread": {"value": single / dt1, "unit": "candidates/s", "cores": 1,
+                              "sample": "candidates 0-%d, %.1f s" % (single - 1, dt1)}}
+
+
+def copy_bandwidth(stream, nbytes: int = 1 << 30, reps: int = 10):
+    """Achievable HBM bandwidth of a plain device copy (read + write bytes per
+    second), timed with events on the bench stream."""
+    import torch
+    a = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    with torch.cuda.stream(stream):
+        for _ in range(2):
+            b.copy_(a)
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(reps):
+            b.copy_(a)
+        t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / reps
+    del a, b
+    torch.cuda.empty_cache()
+    return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def time_host_round_trip(g, w, K, steps):
+    """The synchronous ckm_round_eval: S* from host memory, results back to
+    host memory, work buffer allocated inside the call (PCIe included)."""
+    for _ in range(2):
+        g.round_eval(w.s_frac, K, w.seed, w.budget)
+    ts = []
+    for _ in range(steps):
+        t = time.perf_counter()
+        g.round_eval(w.s_frac, K, w.seed, w.budget)
+        ts.append(time.perf_counter() - t)
+    ms = 1e3 * sorted(ts)[len(ts) // 2]
+    return {"value": K / (ms * 1e-3), "unit": "candidates/s", "ms_per_call_median": ms, "steps": steps,
+            "input": "host S* (%.1f MB fp64) in, host peak/cost/feasible and best S/R out, "
+                     "synchronous C-ABI call" % (w.s_frac.nbytes / 1e6)}
 
 
 def time_schedules(g, w, K, steps, stream):
@@ -222,7 +291,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=4, help="workload 1..5 (4 = transformer stack)")
     ap.add_argument("--splits", type=int, default=0, help="stage splits per 64 candidates (0 = auto)")
-    ap.add_argument("--cpu-sample", type=int, default=1024, help="oracle candidates to time (0 = skip)")
+    ap.add_argument("--cpu-sample", type=int, default=1024,
+                    help="oracle candidates to time on all host threads (0 = skip)")
+    ap.add_argument("--cpu-single", type=int, default=128, help="oracle candidates to time on one thread")
+    ap.add_argument("--host-steps", type=int, default=10,
+                    help="timed synchronous calls with host buffers (0 = skip)")
     ap.add_argument("--sched-steps", type=int, default=20,
                     help="timed calls of the supplied-schedule evaluation (0 = skip)")
     ap.add_argument("--thr-steps", type=int, default=20,
@@ -254,22 +327,25 @@ def main():
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
         g.quantize_async(d_s, work, stream)
         g.round_async(K, w.seed, 0, work, stream)
         if ev is not None:
-            ev[0].record(stream)
+            ev[1].record(stream)
         g.evaluate_async(K, w.seed, ckm.F_ROUNDED, work, stage_splits=args.splits, stream=stream)
         if ev is not None:
-            ev[1].record(stream)
+            ev[2].record(stream)
         g.select_async(K, w.seed, w.budget, 0, out, work, stream)
+        if ev is not None:
+            ev[3].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     assert int(out["status"].item()) == ckm.OK
 
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(args.steps)]
+    evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(4)) for _ in range(args.steps)]
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -281,8 +357,10 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     ms_step = t0.elapsed_time(t1) / args.steps
-    eval_ms = [a.elapsed_time(b) for a, b in evs]
+    eval_ms = [e[1].elapsed_time(e[2]) for e in evs]
     eval_avg_ms = float(np.mean(eval_ms))
+    step_ms = [e[0].elapsed_time(e[3]) for e in evs]
+    copy_gbs = copy_bandwidth(stream)
 
     b_cand = 4 * n * W * 8
     achieved = K * b_cand / (eval_avg_ms * 1e-3) / 1e9
@@ -304,13 +382,19 @@ def main():
                                "24 blocks, mirrored backward)" % (w.name, n, K, w.budget_pct)
                    if args.config == 4 else "%s n=%d K=%d" % (w.name, n, K),
                    "n": n, "K": K, "budget": int(w.budget), "stage_splits": args.splits},
+        "ms_per_step_median": float(np.median(step_ms)),
         "stage_evals_per_s": K * n / (ms_step * 1e-3),
         "evaluate_kernel_ms": eval_avg_ms,
+        "evaluate_kernel_ms_median": float(np.median(eval_ms)),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic},
+        "hbm_copy": {"achieved": copy_gbs, "unit": "GB/s", "kernel": "device copy of 1 GiB (read + write)",
+                     "evaluate_frac": achieved / copy_gbs},
         "wall_s": wall,
     }
+    if args.host_steps > 0:
+        result["host_round_trip"] = time_host_round_trip(g, w, K, args.host_steps)
     if args.sched_steps > 0:
         result["supplied_schedules"] = time_schedules(g, w, K, args.sched_steps, stream)
     if args.batch_steps > 0:
@@ -320,7 +404,7 @@ def main():
     if args.thr_steps > 0:
         result["threshold_family"] = time_thresholds(g, w, K, args.thr_steps, stream, d_s)
     if args.cpu_sample > 0:
-        result["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, K))
+        result["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, K), min(args.cpu_single, K))
     print(json.dumps(result), flush=True)
     g.close()
 

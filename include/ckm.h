@@ -89,7 +89,14 @@ ckm_status ckm_graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* de
                             int64_t m_param, ckm_graph** out);
 
 /* Free a graph and its device memory. NULL is ignored. The graph must not be
- * in use by work still queued on a stream. */
+ * in use by work still queued on a stream, or by a synchronous call.
+ *
+ * Synchronous calls (ckm_round_eval, ckm_eval_schedules, ckm_threshold_eval,
+ * ckm_plan, ckm_max_batch) keep a stream, device memory and pinned host
+ * memory on the graph, sized by the largest call so far, and reuse them, so
+ * that repeated calls allocate nothing; ckm_graph_destroy frees them. They
+ * may run concurrently on one graph: a call that finds them in use by
+ * another thread allocates its own for its duration. */
 void ckm_graph_destroy(ckm_graph* g);
 
 /* Number of nodes, or -1 for NULL. */

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -47,6 +48,165 @@ struct DeviceGuard {
     if (ok && prev >= 0) (void)hipSetDevice(prev);
   }
 };
+
+}  // namespace
+
+namespace ckm {
+
+// Device memory, pinned host memory and a stream for the synchronous entry
+// points, kept on the graph so that repeated calls allocate nothing after the
+// first. The buffers grow to the largest call seen and are released with the
+// graph.
+struct SyncCache {
+  std::mutex mu;
+  hipStream_t stream = nullptr;
+  char* d = nullptr;
+  size_t d_bytes = 0;
+  char* h = nullptr;
+  size_t h_bytes = 0;
+
+  // Waits for queued work, then frees everything (the graph's device is current).
+  void release() {
+    if (stream) {
+      (void)hipStreamSynchronize(stream);
+      (void)hipStreamDestroy(stream);
+      stream = nullptr;
+    }
+    if (d) (void)hipFree(d);
+    if (h) (void)hipHostFree(h);
+    d = h = nullptr;
+    d_bytes = h_bytes = 0;
+  }
+};
+
+}  // namespace ckm
+
+namespace {
+
+// One synchronous call's hold on the graph's SyncCache. When another thread
+// holds the cache, the call uses private buffers freed at its end, so
+// synchronous calls on a shared graph remain safe to run concurrently. The
+// destructor waits for the stream; construct after the DeviceGuard.
+class SyncCall {
+ public:
+  explicit SyncCall(const ckm_graph* g) : lk_(g->sync->mu, std::try_to_lock) {
+    c_ = lk_.owns_lock() ? g->sync : &own_;
+  }
+  ~SyncCall() {
+    if (c_ == &own_) {
+      own_.release();
+    } else if (c_->stream) {
+      (void)hipStreamSynchronize(c_->stream);
+    }
+  }
+  SyncCall(const SyncCall&) = delete;
+  SyncCall& operator=(const SyncCall&) = delete;
+
+  // At least d_bytes of device memory and h_bytes of pinned host memory.
+  ckm_status reserve(size_t d_bytes, size_t h_bytes) {
+    hipError_t e;
+    if (!c_->stream && (e = hipStreamCreateWithFlags(&c_->stream, hipStreamNonBlocking)) != hipSuccess) {
+      c_->stream = nullptr;
+      return fail_hip(e, "hipStreamCreate");
+    }
+    // the shared buffers are rounded up to 2 MiB, so that slightly larger
+    // calls reuse them
+    constexpr size_t kStep = (size_t)2 << 20;
+    const bool shared = c_ != &own_;
+    auto grow = [&](size_t need) { return shared ? (need + kStep - 1) / kStep * kStep : need; };
+    if (d_bytes > c_->d_bytes) {
+      (void)hipStreamSynchronize(c_->stream);
+      if (c_->d) (void)hipFree(c_->d);
+      c_->d = nullptr;
+      c_->d_bytes = 0;
+      const size_t sz = grow(d_bytes);
+      if ((e = hipMalloc(&c_->d, sz)) != hipSuccess) {
+        c_->d = nullptr;
+        return e == hipErrorOutOfMemory ? fail(CKM_E_NOMEM, "hipMalloc of %zu bytes failed", sz)
+                                        : fail_hip(e, "hipMalloc");
+      }
+      c_->d_bytes = sz;
+    }
+    if (h_bytes > c_->h_bytes) {
+      (void)hipStreamSynchronize(c_->stream);
+      if (c_->h) (void)hipHostFree(c_->h);
+      c_->h = nullptr;
+      c_->h_bytes = 0;
+      const size_t sz = grow(h_bytes);
+      if ((e = hipHostMalloc(reinterpret_cast<void**>(&c_->h), sz, hipHostMallocDefault)) != hipSuccess) {
+        c_->h = nullptr;
+        return e == hipErrorOutOfMemory ? fail(CKM_E_NOMEM, "hipHostMalloc of %zu bytes failed", sz)
+                                        : fail_hip(e, "hipHostMalloc");
+      }
+      c_->h_bytes = sz;
+    }
+    return CKM_OK;
+  }
+
+  hipStream_t stream() const { return c_->stream; }
+  char* dev() const { return c_->d; }
+  char* host() const { return c_->h; }
+
+  // Waits for the stream; maps a failure to CKM_E_DEVICE.
+  ckm_status wait() {
+    const hipError_t e = hipStreamSynchronize(c_->stream);
+    return e == hipSuccess ? CKM_OK : fail_hip(e, "hipStreamSynchronize");
+  }
+
+ private:
+  std::unique_lock<std::mutex> lk_;
+  ckm::SyncCache own_;
+  ckm::SyncCache* c_ = nullptr;
+};
+
+// Copies the strict lower triangle of S* (n rows of stride ld) into the
+// pinned buffer h as an n x n row-major matrix and uploads it to d in blocks
+// of rows, each block's upload overlapping the copy of the next. Entries on
+// and above the diagonal are neither read nor copied (the kernels never read
+// them). A NaN in the lower triangle is an error.
+ckm_status stage_s_frac(const double* s, int64_t ld, int32_t n, double* h, char* d, hipStream_t stream) {
+  const int32_t block = std::max<int32_t>(1, (1 << 17) / std::max(n, 1));  // about 1 MiB of rows
+  for (int32_t t0 = 0; t0 < n; t0 += block) {
+    const int32_t t1 = std::min(n, t0 + block);
+    for (int32_t t = t0; t < t1; ++t) {
+      const double* src = s + (int64_t)t * ld;
+      double* dst = h + (int64_t)t * n;
+      bool bad = false;
+      for (int32_t i = 0; i < t; ++i) {
+        const double x = src[i];
+        bad |= std::isnan(x);
+        dst[i] = x;
+      }
+      if (bad) {
+        for (int32_t i = 0; i < t; ++i)
+          if (std::isnan(src[i])) return fail(CKM_E_INVALID_ARG, "S*[%d][%d] is NaN", t, i);
+      }
+    }
+    const size_t off = (size_t)t0 * n * sizeof(double);
+    const hipError_t e = hipMemcpyAsync(d + off, reinterpret_cast<char*>(h) + off,
+                                        (size_t)(t1 - t0) * n * sizeof(double), hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return fail_hip(e, "hipMemcpy S*");
+  }
+  return CKM_OK;
+}
+
+// A result array copied from the device buffer (at off) to the caller.
+struct Result {
+  void* dst;
+  size_t off, bytes;
+};
+
+// Downloads the device range [lo, hi) that holds every result in one copy
+// into the pinned buffer at h_off, waits, and hands each result on.
+ckm_status fetch_results(SyncCall& sc, size_t lo, size_t hi, size_t h_off, const Result* r, int count) {
+  hipError_t e = hipMemcpyAsync(sc.host() + h_off, sc.dev() + lo, hi - lo, hipMemcpyDeviceToHost, sc.stream());
+  if (e != hipSuccess) return fail_hip(e, "hipMemcpy results");
+  const ckm_status st = sc.wait();
+  if (st != CKM_OK) return st;
+  for (int i = 0; i < count; ++i)
+    if (r[i].dst) memcpy(r[i].dst, sc.host() + h_off + (r[i].off - lo), r[i].bytes);
+  return CKM_OK;
+}
 
 }  // namespace
 
@@ -292,16 +452,24 @@ ckm_status ckm_graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* de
   g->d_dep_idx = reinterpret_cast<const int32_t*>(base + off_di);
   g->d_dep_upos = reinterpret_cast<const int32_t*>(base + off_uo);
   g->d_recs = base + off_rec;
+  g->sync = new (std::nothrow) ckm::SyncCache;
+  if (!g->sync) {
+    (void)hipFree(g->d_mem);
+    delete g;
+    return fail(CKM_E_NOMEM, "out of host memory");
+  }
   *out = g;
   return CKM_OK;
 }
 
 void ckm_graph_destroy(ckm_graph* g) {
   if (!g) return;
-  if (g->d_mem) {
-    DeviceGuard dg(g->device);
-    (void)hipFree(g->d_mem);
+  DeviceGuard dg(g->device);
+  if (g->sync) {
+    g->sync->release();
+    delete g->sync;
   }
+  if (g->d_mem) (void)hipFree(g->d_mem);
   delete g;
 }
 
@@ -446,54 +614,30 @@ ckm_status ckm_eval_schedules(const ckm_graph* g, const uint64_t* S, int32_t K, 
   const int32_t W = (n + 63) / 64;
   const size_t rows_bytes = (size_t)n * W * sizeof(uint64_t);
   size_t off = 0;
+  const size_t o_w = off;    off = align256(off + L.total);
   const size_t o_s = off;    off = align256(off + (size_t)K * rows_bytes);
   const size_t o_peak = off; off = align256(off + (size_t)K * 8);
   const size_t o_cost = off; off = align256(off + (size_t)K * 8);
   const size_t o_feas = off; off = align256(off + (size_t)K);
   const size_t o_bk = off;   off = align256(off + 8);
   const size_t o_bR = off;   off = align256(off + rows_bytes);
-  const size_t o_w = off;    off = align256(off + L.total);
-  char* d = nullptr;
-  hipError_t e = hipMalloc(&d, off);
-  if (e != hipSuccess)
-    return e == hipErrorOutOfMemory ? fail(CKM_E_NOMEM, "hipMalloc of %zu bytes failed", off)
-                                    : fail_hip(e, "hipMalloc");
-  hipStream_t stream = nullptr;
-  ckm_status st = CKM_OK;
-  do {
-    if ((e = hipStreamCreateWithFlags(&stream, hipStreamNonBlocking)) != hipSuccess) {
-      st = fail_hip(e, "hipStreamCreate");
-      break;
-    }
-    if ((e = hipMemcpyAsync(d + o_s, S, (size_t)K * rows_bytes, hipMemcpyHostToDevice, stream)) != hipSuccess) {
-      st = fail_hip(e, "hipMemcpy S");
-      break;
-    }
-    st = ckm_eval_schedules_async(g, reinterpret_cast<const uint64_t*>(d + o_s), K, budget,
-                                  reinterpret_cast<int64_t*>(d + o_peak), reinterpret_cast<int64_t*>(d + o_cost),
-                                  reinterpret_cast<uint8_t*>(d + o_feas), reinterpret_cast<int32_t*>(d + o_bk),
-                                  best_R ? reinterpret_cast<uint64_t*>(d + o_bR) : nullptr, nullptr, d + o_w,
-                                  L.total, stream);
-    if (st != CKM_OK) break;
-    struct Copy { void* dst; size_t off, bytes; } copies[] = {
-        {peak, o_peak, (size_t)K * 8}, {cost, o_cost, (size_t)K * 8}, {feasible, o_feas, (size_t)K},
-        {best_k, o_bk, 4}, {best_R, o_bR, rows_bytes}};
-    for (const Copy& c : copies) {
-      if (!c.dst) continue;
-      if ((e = hipMemcpyAsync(c.dst, d + c.off, c.bytes, hipMemcpyDeviceToHost, stream)) != hipSuccess) {
-        st = fail_hip(e, "hipMemcpy results");
-        break;
-      }
-    }
-    if (st != CKM_OK) break;
-    if ((e = hipStreamSynchronize(stream)) != hipSuccess) st = fail_hip(e, "hipStreamSynchronize");
-  } while (false);
-  if (stream) {
-    (void)hipStreamSynchronize(stream);
-    (void)hipStreamDestroy(stream);
-  }
-  (void)hipFree(d);
-  return st;
+  const size_t o_end = off;
+  SyncCall sc(g);
+  ckm_status st = sc.reserve(o_end, o_end - o_peak);
+  if (st != CKM_OK) return st;
+  char* d = sc.dev();
+  // the matrices go straight from the caller's memory (staged by the runtime)
+  const hipError_t e = hipMemcpyAsync(d + o_s, S, (size_t)K * rows_bytes, hipMemcpyHostToDevice, sc.stream());
+  if (e != hipSuccess) return fail_hip(e, "hipMemcpy S");
+  st = ckm_eval_schedules_async(g, reinterpret_cast<const uint64_t*>(d + o_s), K, budget,
+                                reinterpret_cast<int64_t*>(d + o_peak), reinterpret_cast<int64_t*>(d + o_cost),
+                                reinterpret_cast<uint8_t*>(d + o_feas), reinterpret_cast<int32_t*>(d + o_bk),
+                                best_R ? reinterpret_cast<uint64_t*>(d + o_bR) : nullptr, nullptr, d + o_w, L.total,
+                                sc.stream());
+  if (st != CKM_OK) return st;
+  const Result r[] = {{peak, o_peak, (size_t)K * 8}, {cost, o_cost, (size_t)K * 8}, {feasible, o_feas, (size_t)K},
+                      {best_k, o_bk, 4}, {best_R, o_bR, rows_bytes}};
+  return fetch_results(sc, o_peak, o_end, 0, r, 5);
 }
 
 ckm_status ckm_threshold_eval_async(const ckm_graph* g, const double* d_s_frac, int64_t ld, const double* d_p,
@@ -536,72 +680,47 @@ ckm_status ckm_threshold_eval(const ckm_graph* g, const double* s_frac, int64_t 
   const int32_t n = g->n;
   for (int32_t k = 0; k < K; ++k)
     if (std::isnan(p[k])) return fail(CKM_E_INVALID_ARG, "threshold %d is NaN", k);
-  for (int32_t t = 0; t < n; ++t)
-    for (int32_t i = 0; i < t; ++i)
-      if (std::isnan(s_frac[(int64_t)t * ld + i]))
-        return fail(CKM_E_INVALID_ARG, "S*[%d][%d] is NaN", t, i);
 
   DeviceGuard dg(g->device);
   if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
   const Layout L = ckm::make_layout(n, K);
   const int32_t W = (n + 63) / 64;
   const size_t rows_bytes = (size_t)n * W * sizeof(uint64_t);
+  const size_t s_bytes = align256((size_t)n * n * sizeof(double));
+  const size_t p_bytes = align256((size_t)K * sizeof(double));
   size_t off = 0;
-  const size_t o_s = off;    off = align256(off + (size_t)n * n * sizeof(double));
-  const size_t o_p = off;    off = align256(off + (size_t)K * sizeof(double));
+  const size_t o_w = off;    off = align256(off + L.total);
+  const size_t o_s = off;    off = align256(off + s_bytes);
+  const size_t o_p = off;    off = align256(off + p_bytes);
   const size_t o_peak = off; off = align256(off + (size_t)K * 8);
   const size_t o_cost = off; off = align256(off + (size_t)K * 8);
   const size_t o_feas = off; off = align256(off + (size_t)K);
   const size_t o_bk = off;   off = align256(off + 8);
   const size_t o_bS = off;   off = align256(off + rows_bytes);
   const size_t o_bR = off;   off = align256(off + rows_bytes);
-  const size_t o_w = off;    off = align256(off + L.total);
-  char* d = nullptr;
-  hipError_t e = hipMalloc(&d, off);
-  if (e != hipSuccess)
-    return e == hipErrorOutOfMemory ? fail(CKM_E_NOMEM, "hipMalloc of %zu bytes failed", off)
-                                    : fail_hip(e, "hipMalloc");
-  hipStream_t stream = nullptr;
-  ckm_status st = CKM_OK;
-  do {
-    if ((e = hipStreamCreateWithFlags(&stream, hipStreamNonBlocking)) != hipSuccess) {
-      st = fail_hip(e, "hipStreamCreate");
-      break;
-    }
-    if ((e = hipMemcpy2DAsync(d + o_s, (size_t)n * sizeof(double), s_frac, (size_t)ld * sizeof(double),
-                              (size_t)n * sizeof(double), n, hipMemcpyHostToDevice, stream)) != hipSuccess ||
-        (e = hipMemcpyAsync(d + o_p, p, (size_t)K * sizeof(double), hipMemcpyHostToDevice, stream)) !=
-            hipSuccess) {
-      st = fail_hip(e, "hipMemcpy S* or thresholds");
-      break;
-    }
-    st = ckm_threshold_eval_async(g, reinterpret_cast<const double*>(d + o_s), n,
-                                  reinterpret_cast<const double*>(d + o_p), K, budget,
-                                  reinterpret_cast<int64_t*>(d + o_peak), reinterpret_cast<int64_t*>(d + o_cost),
-                                  reinterpret_cast<uint8_t*>(d + o_feas), reinterpret_cast<int32_t*>(d + o_bk),
-                                  best_S ? reinterpret_cast<uint64_t*>(d + o_bS) : nullptr,
-                                  best_R ? reinterpret_cast<uint64_t*>(d + o_bR) : nullptr, nullptr, d + o_w,
-                                  L.total, stream);
-    if (st != CKM_OK) break;
-    struct Copy { void* dst; size_t off, bytes; } copies[] = {
-        {peak, o_peak, (size_t)K * 8}, {cost, o_cost, (size_t)K * 8}, {feasible, o_feas, (size_t)K},
-        {best_k, o_bk, 4}, {best_S, o_bS, rows_bytes}, {best_R, o_bR, rows_bytes}};
-    for (const Copy& c : copies) {
-      if (!c.dst) continue;
-      if ((e = hipMemcpyAsync(c.dst, d + c.off, c.bytes, hipMemcpyDeviceToHost, stream)) != hipSuccess) {
-        st = fail_hip(e, "hipMemcpy results");
-        break;
-      }
-    }
-    if (st != CKM_OK) break;
-    if ((e = hipStreamSynchronize(stream)) != hipSuccess) st = fail_hip(e, "hipStreamSynchronize");
-  } while (false);
-  if (stream) {
-    (void)hipStreamSynchronize(stream);
-    (void)hipStreamDestroy(stream);
-  }
-  (void)hipFree(d);
-  return st;
+  const size_t o_end = off;
+  // pinned: S*, thresholds, then the results
+  SyncCall sc(g);
+  ckm_status st = sc.reserve(o_end, s_bytes + p_bytes + (o_end - o_peak));
+  if (st != CKM_OK) return st;
+  char* d = sc.dev();
+  char* h = sc.host();
+  if ((st = stage_s_frac(s_frac, ld, n, reinterpret_cast<double*>(h), d + o_s, sc.stream())) != CKM_OK) return st;
+  memcpy(h + s_bytes, p, (size_t)K * sizeof(double));
+  const hipError_t e = hipMemcpyAsync(d + o_p, h + s_bytes, (size_t)K * sizeof(double), hipMemcpyHostToDevice,
+                                      sc.stream());
+  if (e != hipSuccess) return fail_hip(e, "hipMemcpy thresholds");
+  st = ckm_threshold_eval_async(g, reinterpret_cast<const double*>(d + o_s), n,
+                                reinterpret_cast<const double*>(d + o_p), K, budget,
+                                reinterpret_cast<int64_t*>(d + o_peak), reinterpret_cast<int64_t*>(d + o_cost),
+                                reinterpret_cast<uint8_t*>(d + o_feas), reinterpret_cast<int32_t*>(d + o_bk),
+                                best_S ? reinterpret_cast<uint64_t*>(d + o_bS) : nullptr,
+                                best_R ? reinterpret_cast<uint64_t*>(d + o_bR) : nullptr, nullptr, d + o_w, L.total,
+                                sc.stream());
+  if (st != CKM_OK) return st;
+  const Result r[] = {{peak, o_peak, (size_t)K * 8}, {cost, o_cost, (size_t)K * 8}, {feasible, o_feas, (size_t)K},
+                      {best_k, o_bk, 4}, {best_S, o_bS, rows_bytes}, {best_R, o_bR, rows_bytes}};
+  return fetch_results(sc, o_peak, o_end, s_bytes + p_bytes, r, 6);
 }
 
 ckm_status ckm_plan_async(const ckm_graph* g, const uint64_t* d_S, const uint64_t* d_R, uint32_t flags,
@@ -632,68 +751,51 @@ ckm_status ckm_plan(const ckm_graph* g, const uint64_t* S, const uint64_t* R, ui
   if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
   const Layout L = ckm::make_layout(n, 1);
   const size_t rows_bytes = (size_t)n * ((n + 63) / 64) * sizeof(uint64_t);
+  const size_t rows_al = align256(rows_bytes);
   size_t off = 0;
+  const size_t o_w = off;   off = align256(off + L.total);
   const size_t o_s = off;   off = align256(off + rows_bytes);
   const size_t o_r = off;   off = align256(off + rows_bytes);
   const size_t o_cnt = off; off = align256(off + 8);
   const size_t o_st = off;  off = align256(off + 8);
-  const size_t o_w = off;   off = align256(off + L.total);
   const size_t o_p = off;   off = align256(off + (size_t)capacity * sizeof(ckm_stmt));
   const size_t o_m = off;   off = align256(off + (mem ? (size_t)capacity * sizeof(int64_t) : 0));
-  char* d = nullptr;
-  hipError_t e = hipMalloc(&d, off);
-  if (e != hipSuccess)
-    return e == hipErrorOutOfMemory ? fail(CKM_E_NOMEM, "hipMalloc of %zu bytes failed", off)
-                                    : fail_hip(e, "hipMalloc");
-  hipStream_t stream = nullptr;
-  ckm_status st = CKM_OK;
-  int32_t status_dev = 0;
+  // pinned: S and R, then the count and status
+  SyncCall sc(g);
+  ckm_status st = sc.reserve(off, 2 * rows_al + (o_p - o_cnt));
+  if (st != CKM_OK) return st;
+  char* d = sc.dev();
+  char* h = sc.host();
+  memcpy(h, S, rows_bytes);
+  memcpy(h + rows_al, R, rows_bytes);
+  hipError_t e;
+  if ((e = hipMemcpyAsync(d + o_s, h, rows_bytes, hipMemcpyHostToDevice, sc.stream())) != hipSuccess ||
+      (e = hipMemcpyAsync(d + o_r, h + rows_al, rows_bytes, hipMemcpyHostToDevice, sc.stream())) != hipSuccess)
+    return fail_hip(e, "hipMemcpy S or R");
+  st = ckm_plan_async(g, reinterpret_cast<const uint64_t*>(d + o_s), reinterpret_cast<const uint64_t*>(d + o_r),
+                      flags, P ? reinterpret_cast<ckm_stmt*>(d + o_p) : nullptr, capacity,
+                      reinterpret_cast<int64_t*>(d + o_cnt), mem ? reinterpret_cast<int64_t*>(d + o_m) : nullptr,
+                      reinterpret_cast<int32_t*>(d + o_st), d + o_w, L.total, sc.stream());
+  if (st != CKM_OK) return st;
   int64_t total = 0;
-  do {
-    if ((e = hipStreamCreateWithFlags(&stream, hipStreamNonBlocking)) != hipSuccess) {
-      st = fail_hip(e, "hipStreamCreate");
-      break;
-    }
-    if ((e = hipMemcpyAsync(d + o_s, S, rows_bytes, hipMemcpyHostToDevice, stream)) != hipSuccess ||
-        (e = hipMemcpyAsync(d + o_r, R, rows_bytes, hipMemcpyHostToDevice, stream)) != hipSuccess) {
-      st = fail_hip(e, "hipMemcpy S or R");
-      break;
-    }
-    st = ckm_plan_async(g, reinterpret_cast<const uint64_t*>(d + o_s), reinterpret_cast<const uint64_t*>(d + o_r),
-                        flags, P ? reinterpret_cast<ckm_stmt*>(d + o_p) : nullptr, capacity,
-                        reinterpret_cast<int64_t*>(d + o_cnt), mem ? reinterpret_cast<int64_t*>(d + o_m) : nullptr,
-                        reinterpret_cast<int32_t*>(d + o_st), d + o_w, L.total, stream);
-    if (st != CKM_OK) break;
-    if ((e = hipMemcpyAsync(&total, d + o_cnt, 8, hipMemcpyDeviceToHost, stream)) != hipSuccess ||
-        (e = hipMemcpyAsync(&status_dev, d + o_st, 4, hipMemcpyDeviceToHost, stream)) != hipSuccess ||
-        (e = hipStreamSynchronize(stream)) != hipSuccess) {
-      st = fail_hip(e, "hipMemcpy count");
-      break;
-    }
-    *count = total;
-    if (status_dev != CKM_OK) {
-      st = (P && total > capacity) ? fail(CKM_E_INVALID_ARG, "plan has %lld statements, capacity %lld",
+  int32_t status_dev = 0;
+  const Result r[] = {{&total, o_cnt, 8}, {&status_dev, o_st, 4}};
+  if ((st = fetch_results(sc, o_cnt, o_p, 2 * rows_al, r, 2)) != CKM_OK) return st;
+  *count = total;
+  if (status_dev != CKM_OK)
+    return (P && total > capacity) ? fail(CKM_E_INVALID_ARG, "plan has %lld statements, capacity %lld",
                                           (long long)total, (long long)capacity)
                                    : fail(CKM_E_INVALID_ARG, "(S, R) violates (4a), (1b), (1c) or S & R = 0");
-      break;
-    }
-    if (P && total > 0) {
-      if ((e = hipMemcpyAsync(P, d + o_p, (size_t)total * sizeof(ckm_stmt), hipMemcpyDeviceToHost, stream)) !=
-              hipSuccess ||
-          (mem && (e = hipMemcpyAsync(mem, d + o_m, (size_t)total * sizeof(int64_t), hipMemcpyDeviceToHost,
-                                      stream)) != hipSuccess) ||
-          (e = hipStreamSynchronize(stream)) != hipSuccess) {
-        st = fail_hip(e, "hipMemcpy plan");
-        break;
-      }
-    }
-  } while (false);
-  if (stream) {
-    (void)hipStreamSynchronize(stream);
-    (void)hipStreamDestroy(stream);
+  if (P && total > 0) {
+    // the statements go straight into the caller's memory
+    if ((e = hipMemcpyAsync(P, d + o_p, (size_t)total * sizeof(ckm_stmt), hipMemcpyDeviceToHost, sc.stream())) !=
+            hipSuccess ||
+        (mem && (e = hipMemcpyAsync(mem, d + o_m, (size_t)total * sizeof(int64_t), hipMemcpyDeviceToHost,
+                                    sc.stream())) != hipSuccess))
+      return fail_hip(e, "hipMemcpy plan");
+    return sc.wait();
   }
-  (void)hipFree(d);
-  return st;
+  return CKM_OK;
 }
 
 ckm_status ckm_max_batch_async(const ckm_graph* g, int32_t K, int64_t budget, int64_t cost_cap, int64_t* d_batch,
@@ -723,55 +825,32 @@ ckm_status ckm_max_batch(const ckm_graph* g, const double* s_frac, int64_t ld, i
   if (cost_cap < 0) return fail(CKM_E_INVALID_ARG, "cost_cap = %lld < 0", (long long)cost_cap);
   if (flags & ~(uint32_t)CKM_F_DET0) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
   const int32_t n = g->n;
-  for (int32_t t = 0; t < n; ++t)
-    for (int32_t i = 0; i < t; ++i)
-      if (std::isnan(s_frac[(int64_t)t * ld + i])) return fail(CKM_E_INVALID_ARG, "S*[%d][%d] is NaN", t, i);
   DeviceGuard dg(g->device);
   if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
   const Layout L = ckm::make_layout(n, K);
+  const size_t s_bytes = align256((size_t)n * n * sizeof(double));
   size_t off = 0;
-  const size_t o_s = off;  off = align256(off + (size_t)n * n * sizeof(double));
+  const size_t o_w = off;  off = align256(off + L.total_rows);
+  const size_t o_s = off;  off = align256(off + s_bytes);
   const size_t o_b = off;  off = align256(off + (size_t)K * 8);
   const size_t o_bk = off; off = align256(off + 8);
   const size_t o_bb = off; off = align256(off + 8);
-  const size_t o_w = off;  off = align256(off + L.total_rows);
-  char* d = nullptr;
-  hipError_t e = hipMalloc(&d, off);
-  if (e != hipSuccess)
-    return e == hipErrorOutOfMemory ? fail(CKM_E_NOMEM, "hipMalloc of %zu bytes failed", off)
-                                    : fail_hip(e, "hipMalloc");
-  hipStream_t stream = nullptr;
-  ckm_status st = CKM_OK;
-  do {
-    if ((e = hipStreamCreateWithFlags(&stream, hipStreamNonBlocking)) != hipSuccess) {
-      st = fail_hip(e, "hipStreamCreate");
-      break;
-    }
-    if ((e = hipMemcpy2DAsync(d + o_s, (size_t)n * sizeof(double), s_frac, (size_t)ld * sizeof(double),
-                              (size_t)n * sizeof(double), n, hipMemcpyHostToDevice, stream)) != hipSuccess) {
-      st = fail_hip(e, "hipMemcpy2D S*");
-      break;
-    }
-    if ((st = ckm_quantize_async(g, reinterpret_cast<const double*>(d + o_s), n, d + o_w, L.total_rows, stream)) != CKM_OK ||
-        (st = ckm_evaluate_async(g, K, seed, flags, 0, d + o_w, L.total_rows, stream)) != CKM_OK ||
-        (st = ckm_max_batch_async(g, K, budget, cost_cap, reinterpret_cast<int64_t*>(d + o_b),
-                                  reinterpret_cast<int32_t*>(d + o_bk), reinterpret_cast<int64_t*>(d + o_bb), nullptr,
-                                  d + o_w, L.total_rows, stream)) != CKM_OK)
-      break;
-    if ((e = hipMemcpyAsync(batch, d + o_b, (size_t)K * 8, hipMemcpyDeviceToHost, stream)) != hipSuccess ||
-        (e = hipMemcpyAsync(best_k, d + o_bk, 4, hipMemcpyDeviceToHost, stream)) != hipSuccess ||
-        (best_batch && (e = hipMemcpyAsync(best_batch, d + o_bb, 8, hipMemcpyDeviceToHost, stream)) != hipSuccess) ||
-        (e = hipStreamSynchronize(stream)) != hipSuccess) {
-      st = fail_hip(e, "hipMemcpy results");
-      break;
-    }
-  } while (false);
-  if (stream) {
-    (void)hipStreamSynchronize(stream);
-    (void)hipStreamDestroy(stream);
-  }
-  (void)hipFree(d);
-  return st;
+  const size_t o_end = off;
+  SyncCall sc(g);
+  ckm_status st = sc.reserve(o_end, s_bytes + (o_end - o_b));
+  if (st != CKM_OK) return st;
+  char* d = sc.dev();
+  const hipStream_t stream = sc.stream();
+  if ((st = stage_s_frac(s_frac, ld, n, reinterpret_cast<double*>(sc.host()), d + o_s, stream)) != CKM_OK ||
+      (st = ckm_quantize_async(g, reinterpret_cast<const double*>(d + o_s), n, d + o_w, L.total_rows, stream)) !=
+          CKM_OK ||
+      (st = ckm_evaluate_async(g, K, seed, flags, 0, d + o_w, L.total_rows, stream)) != CKM_OK ||
+      (st = ckm_max_batch_async(g, K, budget, cost_cap, reinterpret_cast<int64_t*>(d + o_b),
+                                reinterpret_cast<int32_t*>(d + o_bk), reinterpret_cast<int64_t*>(d + o_bb), nullptr,
+                                d + o_w, L.total_rows, stream)) != CKM_OK)
+    return st;
+  const Result r[] = {{batch, o_b, (size_t)K * 8}, {best_k, o_bk, 4}, {best_batch, o_bb, 8}};
+  return fetch_results(sc, o_b, o_end, s_bytes, r, 3);
 }
 
 ckm_status ckm_round_eval(const ckm_graph* g, const double* s_frac, int64_t ld, int32_t K,
@@ -786,20 +865,15 @@ ckm_status ckm_round_eval(const ckm_graph* g, const double* s_frac, int64_t ld, 
   if (K > CKM_MAX_CANDIDATES) return fail(CKM_E_UNSUPPORTED, "K = %d > %d", K, CKM_MAX_CANDIDATES);
   if (budget < 0) return fail(CKM_E_INVALID_ARG, "budget = %lld < 0", (long long)budget);
   if (flags & ~(uint32_t)CKM_F_DET0) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
-  // NaN check on the host: only the strict lower triangle is read.
   const int32_t n = g->n;
-  for (int32_t t = 0; t < n; ++t)
-    for (int32_t i = 0; i < t; ++i)
-      if (std::isnan(s_frac[(int64_t)t * ld + i]))
-        return fail(CKM_E_INVALID_ARG, "S*[%d][%d] is NaN", t, i);
-
   DeviceGuard dg(g->device);
   if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
   const Layout L = ckm::make_layout(n, K);
   const int32_t W = (n + 63) / 64;
-  const size_t s_bytes = (size_t)n * n * sizeof(double);
+  const size_t s_bytes = align256((size_t)n * n * sizeof(double));
   const size_t rows_bytes = (size_t)n * W * sizeof(uint64_t);
   size_t off = 0;
+  const size_t o_w = off;    off = align256(off + L.total_rows);
   const size_t o_s = off;    off = align256(off + s_bytes);
   const size_t o_peak = off; off = align256(off + (size_t)K * 8);
   const size_t o_cost = off; off = align256(off + (size_t)K * 8);
@@ -808,55 +882,27 @@ ckm_status ckm_round_eval(const ckm_graph* g, const double* s_frac, int64_t ld, 
   const size_t o_st = off;   off = align256(off + 8);
   const size_t o_bS = off;   off = align256(off + rows_bytes);
   const size_t o_bR = off;   off = align256(off + rows_bytes);
-  const size_t o_w = off;    off = align256(off + L.total_rows);
-  char* d = nullptr;
-  hipError_t e = hipMalloc(&d, off);
-  if (e != hipSuccess)
-    return e == hipErrorOutOfMemory ? fail(CKM_E_NOMEM, "hipMalloc of %zu bytes failed", off)
-                                    : fail_hip(e, "hipMalloc");
-  hipStream_t stream = nullptr;
-  ckm_status st = CKM_OK;
+  const size_t o_end = off;
+  // pinned: S*, then the results
+  SyncCall sc(g);
+  ckm_status st = sc.reserve(o_end, s_bytes + (o_end - o_peak));
+  if (st != CKM_OK) return st;
+  char* d = sc.dev();
+  if ((st = stage_s_frac(s_frac, ld, n, reinterpret_cast<double*>(sc.host()), d + o_s, sc.stream())) != CKM_OK)
+    return st;
+  st = ckm_round_eval_async(g, reinterpret_cast<const double*>(d + o_s), n, K, seed, budget, flags,
+                            reinterpret_cast<int64_t*>(d + o_peak), reinterpret_cast<int64_t*>(d + o_cost),
+                            reinterpret_cast<uint8_t*>(d + o_feas), reinterpret_cast<int32_t*>(d + o_bk),
+                            best_S ? reinterpret_cast<uint64_t*>(d + o_bS) : nullptr,
+                            best_R ? reinterpret_cast<uint64_t*>(d + o_bR) : nullptr,
+                            reinterpret_cast<int32_t*>(d + o_st), d + o_w, L.total_rows, sc.stream());
+  if (st != CKM_OK) return st;
   int32_t status_dev = 0;
-  do {
-    if ((e = hipStreamCreateWithFlags(&stream, hipStreamNonBlocking)) != hipSuccess) {
-      st = fail_hip(e, "hipStreamCreate");
-      break;
-    }
-    if ((e = hipMemcpy2DAsync(d + o_s, (size_t)n * sizeof(double), s_frac, (size_t)ld * sizeof(double),
-                              (size_t)n * sizeof(double), n, hipMemcpyHostToDevice, stream)) != hipSuccess) {
-      st = fail_hip(e, "hipMemcpy2D S*");
-      break;
-    }
-    st = ckm_round_eval_async(g, reinterpret_cast<const double*>(d + o_s), n, K, seed, budget, flags,
-                              reinterpret_cast<int64_t*>(d + o_peak), reinterpret_cast<int64_t*>(d + o_cost),
-                              reinterpret_cast<uint8_t*>(d + o_feas), reinterpret_cast<int32_t*>(d + o_bk),
-                              best_S ? reinterpret_cast<uint64_t*>(d + o_bS) : nullptr,
-                              best_R ? reinterpret_cast<uint64_t*>(d + o_bR) : nullptr,
-                              reinterpret_cast<int32_t*>(d + o_st), d + o_w, L.total_rows, stream);
-    if (st != CKM_OK) break;
-    struct Copy { void* dst; size_t off, bytes; } copies[] = {
-        {peak, o_peak, (size_t)K * 8}, {cost, o_cost, (size_t)K * 8}, {feasible, o_feas, (size_t)K},
-        {best_k, o_bk, 4}, {&status_dev, o_st, 4}, {best_S, o_bS, rows_bytes}, {best_R, o_bR, rows_bytes}};
-    for (const Copy& c : copies) {
-      if (!c.dst) continue;
-      if ((e = hipMemcpyAsync(c.dst, d + c.off, c.bytes, hipMemcpyDeviceToHost, stream)) != hipSuccess) {
-        st = fail_hip(e, "hipMemcpy results");
-        break;
-      }
-    }
-    if (st != CKM_OK) break;
-    if ((e = hipStreamSynchronize(stream)) != hipSuccess) {
-      st = fail_hip(e, "hipStreamSynchronize");
-      break;
-    }
-    if (status_dev != CKM_OK) st = fail((ckm_status)status_dev, "S* holds a NaN");
-  } while (false);
-  if (stream) {
-    (void)hipStreamSynchronize(stream);
-    (void)hipStreamDestroy(stream);
-  }
-  (void)hipFree(d);
-  return st;
+  const Result r[] = {{peak, o_peak, (size_t)K * 8}, {cost, o_cost, (size_t)K * 8}, {feasible, o_feas, (size_t)K},
+                      {best_k, o_bk, 4}, {&status_dev, o_st, 4}, {best_S, o_bS, rows_bytes},
+                      {best_R, o_bR, rows_bytes}};
+  if ((st = fetch_results(sc, o_peak, o_end, s_bytes, r, 7)) != CKM_OK) return st;
+  return status_dev == CKM_OK ? CKM_OK : fail((ckm_status)status_dev, "S* holds a NaN");
 }
 
 }  // extern "C"

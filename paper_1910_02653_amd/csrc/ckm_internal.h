@@ -8,6 +8,10 @@
 
 #include "ckm.h"
 
+namespace ckm {
+struct SyncCache;  // buffers and stream of the synchronous entry points (ckm_host.cpp)
+}
+
 // Graph on the device. Node arrays hold sizes and costs as binary64 (exact:
 // the host rejects totals >= 2^53). Users rows are sorted ascending; for the
 // dep entry e = (i -> v) in v's deps row, dep_upos[e] is the index in
@@ -27,6 +31,7 @@ struct ckm_graph {
   const int32_t* d_dep_idx = nullptr;
   const int32_t* d_dep_upos = nullptr;
   const void* d_recs = nullptr;  // n node records of ckm::kNodeRecBytes (see ckm_kernels.hip)
+  ckm::SyncCache* sync = nullptr;  // reused by the synchronous calls; freed with the graph
 };
 
 namespace ckm {

@@ -1,0 +1,114 @@
+"""The synchronous entry points reuse a stream and device / pinned buffers
+kept on the graph. These tests check that reuse changes no result: calls of
+growing and shrinking size, different entry points in turn on one graph, a
+failed call followed by a good one, and concurrent calls from several
+threads (some of which then run on private buffers). Each result is compared
+with the same call on a graph of its own (nothing reused), whose results the
+parity tests check against the oracle; a few are checked against the oracle
+here as well.
+"""
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+import pytest
+
+from oracle import ref
+from paper_1910_02653_amd import ckm
+from paper_1910_02653_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def same(a, b):
+    assert a.keys() == b.keys()
+    for key in a:
+        if isinstance(a[key], np.ndarray) or a[key] is None:
+            assert (a[key] is None and b[key] is None) or np.array_equal(a[key], b[key]), key
+        else:
+            assert a[key] == b[key], key
+
+
+def fresh(w, fn):
+    g = ckm.Graph.from_workload(w)
+    try:
+        return fn(g)
+    finally:
+        g.close()
+
+
+def test_grow_shrink_and_mixed_calls():
+    w = wl.config(3)
+    big = int(w.budget * 2.5)
+    p = np.linspace(0.0, 1.0, 40)
+    sched = wl.random_schedules(w.n, 24, seed=3, density=0.3, kind="intervals", junk=False)
+    S0, R0 = ref.eval_candidate(w, 0, want_rows=True)[2:]
+    calls = [
+        ("round K=64", lambda g: g.round_eval(w.s_frac, 64, w.seed, big)),
+        ("round K=600", lambda g: g.round_eval(w.s_frac, 600, w.seed + 1, big)),
+        ("threshold K=40", lambda g: g.threshold_eval(w.s_frac, p, big)),
+        ("round K=3", lambda g: g.round_eval(w.s_frac, 3, w.seed, big, want_rows=False)),
+        ("schedules K=24", lambda g: g.eval_schedules(sched, big)),
+        ("plan", lambda g: dict(zip(("st", "mem"), g.plan(ref.pack_rows(S0), ref.pack_rows(R0))))),
+        ("max batch K=100", lambda g: g.max_batch(w.s_frac, 100, w.seed, big, 2 ** 62)),
+        ("round K=64 again", lambda g: g.round_eval(w.s_frac, 64, w.seed, big)),
+    ]
+    g = ckm.Graph.from_workload(w)
+    try:
+        for name, fn in calls:
+            log(name)
+            same(fn(g), fresh(w, fn))
+    finally:
+        g.close()
+    # the first call against the oracle
+    got = fresh(w, calls[0][1])
+    for k in (0, 17, 63):
+        assert (int(got["peak"][k]), int(got["cost"][k])) == ref.eval_candidate(w, k)
+
+
+def test_error_then_good_call():
+    w = wl.config(2)
+    g = ckm.Graph.from_workload(w)
+    try:
+        want = g.round_eval(w.s_frac, 50, w.seed, w.budget)
+        s = w.s_frac.copy()
+        s[100, 7] = np.nan
+        with pytest.raises(ckm.CkmError) as e:
+            g.round_eval(s, 50, w.seed, w.budget)
+        assert e.value.status == ckm.E_INVALID_ARG and "NaN" in str(e.value)
+        with pytest.raises(ckm.CkmError):
+            g.max_batch(s, 50, w.seed, w.budget, 2 ** 62)
+        s[7, 100] = np.nan                  # above the diagonal: never read
+        s[100, 7] = 0.5
+        got = g.round_eval(s, 50, w.seed, w.budget)
+        ref_s = w.s_frac.copy()
+        ref_s[100, 7] = 0.5
+        same(got, fresh(w, lambda h: h.round_eval(ref_s, 50, w.seed, w.budget)))
+        same(g.round_eval(w.s_frac, 50, w.seed, w.budget), want)
+        # a strided S* (ld > n) through the staging copy
+        wide = np.zeros((w.n, w.n + 5))
+        wide[:, :w.n] = w.s_frac
+        wide[:, w.n:] = np.nan
+        same(g.round_eval(wide, 50, w.seed, w.budget), want)
+    finally:
+        g.close()
+
+
+def test_concurrent_threads_one_graph():
+    w = wl.config(3)
+    big = int(w.budget * 2.5)
+    jobs = [(K, seed) for K in (32, 200, 64, 129) for seed in (1, 2, 3)]
+    want = {job: fresh(w, lambda g, job=job: g.round_eval(w.s_frac, job[0], job[1], big)) for job in jobs}
+    g = ckm.Graph.from_workload(w)
+    try:
+        log("%d calls on 6 threads" % len(jobs))
+        with ThreadPoolExecutor(6) as ex:
+            for _ in range(2):
+                res = list(ex.map(lambda job: g.round_eval(w.s_frac, job[0], job[1], big), jobs))
+                for job, r in zip(jobs, res):
+                    same(r, want[job])
+    finally:
+        g.close()
