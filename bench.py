@@ -26,6 +26,8 @@ argmin and the best S and R.
 `max_batch` times quantize + evaluate + the largest batch multiplier of
 every candidate (budget 3x the median activation peak, cost cap at the
 median cost) on the same workload.
+`feasible_budget` times the same step at the median-peak budget, where
+select also writes the best candidate's S and R rows.
 `execution_plan` times Algorithm 1's plan (with the memory after each
 statement) for the step's best candidate, or candidate 0's rows when none
 is feasible, read from HBM where the step left them.
@@ -244,6 +246,44 @@ def time_max_batch(g, w, steps, stream, d_s):
                      "(median cost)" % (K, budget, cap)}
 
 
+def time_feasible(g, w, steps, stream, d_s):
+    """The bench step at a budget half the candidates meet (the median
+    peak), so select also writes the best candidate's S and R rows."""
+    import numpy as np
+    import torch
+
+    from paper_1910_02653_amd import ckm
+
+    K = w.K
+    work = g.alloc_work(K)
+    out = g.alloc_outputs(K)
+    g.round_eval_async(d_s, K, w.seed, 2 ** 62, 0, out, work, stream)
+    torch.cuda.synchronize()
+    budget = int(np.median(out["peak"].cpu().numpy()))
+
+    def call():
+        g.quantize_async(d_s, work, stream)
+        g.round_async(K, w.seed, 0, work, stream)
+        g.evaluate_async(K, w.seed, ckm.F_ROUNDED, work, stream=stream)
+        g.select_async(K, w.seed, budget, ckm.F_ROUNDED, out, work, stream)
+
+    for _ in range(3):
+        call()
+    torch.cuda.synchronize()
+    assert int(out["status"].item()) == ckm.OK and int(out["best_k"].item()) >= 0
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(steps):
+        call()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    return {"value": K / (ms * 1e-3), "unit": "candidates/s", "ms_per_step": ms, "steps": steps,
+            "best_k": int(out["best_k"].item()),
+            "input": "the bench step at the median-peak budget %d B (best S and R rows written)" % budget}
+
+
 def time_plan(g, w, steps, stream, d_s):
     """Throughput of ckm_plan_async on one schedule of the workload: the best
     candidate at the median-peak budget (a budget some candidates meet)."""
@@ -302,6 +342,8 @@ def main():
                     help="timed calls of the threshold-family evaluation (0 = skip)")
     ap.add_argument("--plan-steps", type=int, default=20,
                     help="timed calls of the execution-plan generation (0 = skip)")
+    ap.add_argument("--feasible-steps", type=int, default=20,
+                    help="timed steps at the median-peak budget (0 = skip)")
     ap.add_argument("--batch-steps", type=int, default=20,
                     help="timed calls of the largest-batch search (0 = skip)")
     args = ap.parse_args()
@@ -395,6 +437,8 @@ def main():
     }
     if args.host_steps > 0:
         result["host_round_trip"] = time_host_round_trip(g, w, K, args.host_steps)
+    if args.feasible_steps > 0:
+        result["feasible_budget"] = time_feasible(g, w, args.feasible_steps, stream, d_s)
     if args.sched_steps > 0:
         result["supplied_schedules"] = time_schedules(g, w, K, args.sched_steps, stream)
     if args.batch_steps > 0:

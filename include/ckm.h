@@ -133,11 +133,16 @@ ckm_status ckm_round_eval(const ckm_graph* g, const double* s_frac, int64_t ld, 
  * quantize -> evaluate -> select, on one work buffer. */
 
 /* Bytes of work buffer for K candidates on graph g. This includes, when the
- * rounded S rows of all K candidates fit in 1 GiB, room for them; with it the
- * randomized path rounds each row once instead of twice. A smaller buffer
- * that still holds everything else is accepted, and the rows are then
- * rounded inside the evaluate stage (same results). */
+ * S rows of all K candidates fit in 1 GiB, room for them (the row array):
+ * the evaluate stage then streams each row from there instead of making it
+ * twice (randomized rounding, threshold rounding) or reading it from each
+ * candidate's own matrix (supplied schedules). A smaller buffer of at least
+ * ckm_workspace_size_min bytes is accepted, and the rows are then made
+ * inside the evaluate stage (same results). */
 ckm_status ckm_workspace_size(const ckm_graph* g, int32_t K, size_t* bytes);
+
+/* The smallest work buffer accepted for K candidates: without the row array. */
+ckm_status ckm_workspace_size_min(const ckm_graph* g, int32_t K, size_t* bytes);
 
 /* Stage a1: thresholds q (Section 5.1) and the deterministic-rounding bits of
  * Algorithm 2 from S* (device float64, n rows of stride ld >= n). A NaN in

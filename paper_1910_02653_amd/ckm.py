@@ -25,8 +25,8 @@ MAX_THRESHOLDS = 1 << 16
 # every extern "C" symbol declared in include/ckm.h
 EXPORTS = (
     "ckm_graph_create", "ckm_graph_destroy", "ckm_graph_num_nodes", "ckm_round_eval",
-    "ckm_workspace_size", "ckm_quantize_async", "ckm_round_async", "ckm_evaluate_async", "ckm_select_async",
-    "ckm_round_eval_async", "ckm_eval_schedules", "ckm_eval_schedules_async", "ckm_threshold_eval",
+    "ckm_workspace_size", "ckm_workspace_size_min", "ckm_quantize_async", "ckm_round_async",
+    "ckm_evaluate_async", "ckm_select_async", "ckm_round_eval_async", "ckm_eval_schedules", "ckm_eval_schedules_async", "ckm_threshold_eval",
     "ckm_threshold_eval_async", "ckm_plan", "ckm_plan_async", "ckm_max_batch",
     "ckm_max_batch_async", "ckm_last_error",
 )
@@ -66,6 +66,8 @@ def lib():
         L.ckm_round_eval.restype = C.c_int
         L.ckm_workspace_size.argtypes = [p, i32, C.POINTER(sz)]
         L.ckm_workspace_size.restype = C.c_int
+        L.ckm_workspace_size_min.argtypes = [p, i32, C.POINTER(sz)]
+        L.ckm_workspace_size_min.restype = C.c_int
         L.ckm_quantize_async.argtypes = [p, p, i64, p, sz, p]
         L.ckm_quantize_async.restype = C.c_int
         L.ckm_round_async.argtypes = [p, i32, u64, u32, p, sz, p]
@@ -160,9 +162,12 @@ class Graph:
         except Exception:
             pass
 
-    def workspace_size(self, K: int) -> int:
+    def workspace_size(self, K: int, rows: bool = True) -> int:
+        """Work-buffer bytes for K candidates; rows=False: the smallest
+        accepted size, without the row array."""
         out = C.c_size_t()
-        _check(lib().ckm_workspace_size(self._h, int(K), C.byref(out)))
+        fn = lib().ckm_workspace_size if rows else lib().ckm_workspace_size_min
+        _check(fn(self._h, int(K), C.byref(out)))
         return int(out.value)
 
     # -- synchronous, host arrays -----------------------------------------
@@ -312,9 +317,9 @@ class Graph:
             out["best_R"] = torch.empty((self.n, W), dtype=torch.int64, device=device)
         return out
 
-    def alloc_work(self, K: int, device="cuda"):
+    def alloc_work(self, K: int, device="cuda", rows: bool = True):
         import torch
-        return torch.empty(self.workspace_size(K), dtype=torch.uint8, device=device)
+        return torch.empty(self.workspace_size(K, rows), dtype=torch.uint8, device=device)
 
 
 def rows_to_numpy(t) -> np.ndarray:

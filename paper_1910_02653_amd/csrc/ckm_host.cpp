@@ -289,14 +289,16 @@ Layout make_layout(int32_t n, int32_t K) {
   L.bbest_off = off;      off = align256(off + (size_t)L.reduce_blocks * 32);
 
   L.total = off;
-  // rounded rows of every candidate, word w of row t at (base(t) + w) * kpad
-  // + k: last, and optional (evaluate rounds in the kernel without them)
+  // S rows, then R rows, of every candidate, word w of row t at
+  // (base(t) + w) * kpad + k: last, and optional (without them the evaluate
+  // stage makes its S rows itself and select recomputes the best R)
   const size_t kpad = (size_t)((K + kWave - 1) / kWave) * kWave;
   const size_t full = (size_t)(n >> 5), rem = (size_t)(n & 31);
   const size_t rows_bytes = kpad * (32 * full * (full + 1) / 2 + rem * (full + 1)) * sizeof(uint32_t);
   L.rows_on = rows_bytes <= ckm::kRowsMaxBytes;
   L.rows_off = off;
-  L.total_rows = L.rows_on ? align256(off + rows_bytes) : off;
+  L.rrows_off = align256(off + rows_bytes);
+  L.total_rows = L.rows_on ? align256(L.rrows_off + rows_bytes) : off;
   return L;
 }
 
@@ -481,6 +483,14 @@ ckm_status ckm_workspace_size(const ckm_graph* g, int32_t K, size_t* bytes) {
   return CKM_OK;
 }
 
+ckm_status ckm_workspace_size_min(const ckm_graph* g, int32_t K, size_t* bytes) {
+  if (!g || !bytes) return fail(CKM_E_INVALID_ARG, "NULL graph or bytes");
+  if (K < 1) return fail(CKM_E_INVALID_ARG, "K = %d < 1", K);
+  if (K > CKM_MAX_CANDIDATES) return fail(CKM_E_UNSUPPORTED, "K = %d > %d", K, CKM_MAX_CANDIDATES);
+  *bytes = ckm::make_layout(g->n, K).total;
+  return CKM_OK;
+}
+
 static ckm_status check_work(const ckm_graph* g, int32_t K, void* d_work, size_t work_bytes,
                              Layout* L) {
   if (!g) return fail(CKM_E_INVALID_ARG, "graph is NULL");
@@ -614,7 +624,7 @@ ckm_status ckm_eval_schedules(const ckm_graph* g, const uint64_t* S, int32_t K, 
   const int32_t W = (n + 63) / 64;
   const size_t rows_bytes = (size_t)n * W * sizeof(uint64_t);
   size_t off = 0;
-  const size_t o_w = off;    off = align256(off + L.total);
+  const size_t o_w = off;    off = align256(off + L.total_rows);
   const size_t o_s = off;    off = align256(off + (size_t)K * rows_bytes);
   const size_t o_peak = off; off = align256(off + (size_t)K * 8);
   const size_t o_cost = off; off = align256(off + (size_t)K * 8);
@@ -632,7 +642,7 @@ ckm_status ckm_eval_schedules(const ckm_graph* g, const uint64_t* S, int32_t K, 
   st = ckm_eval_schedules_async(g, reinterpret_cast<const uint64_t*>(d + o_s), K, budget,
                                 reinterpret_cast<int64_t*>(d + o_peak), reinterpret_cast<int64_t*>(d + o_cost),
                                 reinterpret_cast<uint8_t*>(d + o_feas), reinterpret_cast<int32_t*>(d + o_bk),
-                                best_R ? reinterpret_cast<uint64_t*>(d + o_bR) : nullptr, nullptr, d + o_w, L.total,
+                                best_R ? reinterpret_cast<uint64_t*>(d + o_bR) : nullptr, nullptr, d + o_w, L.total_rows,
                                 sc.stream());
   if (st != CKM_OK) return st;
   const Result r[] = {{peak, o_peak, (size_t)K * 8}, {cost, o_cost, (size_t)K * 8}, {feasible, o_feas, (size_t)K},
@@ -689,7 +699,7 @@ ckm_status ckm_threshold_eval(const ckm_graph* g, const double* s_frac, int64_t 
   const size_t s_bytes = align256((size_t)n * n * sizeof(double));
   const size_t p_bytes = align256((size_t)K * sizeof(double));
   size_t off = 0;
-  const size_t o_w = off;    off = align256(off + L.total);
+  const size_t o_w = off;    off = align256(off + L.total_rows);
   const size_t o_s = off;    off = align256(off + s_bytes);
   const size_t o_p = off;    off = align256(off + p_bytes);
   const size_t o_peak = off; off = align256(off + (size_t)K * 8);
@@ -715,7 +725,7 @@ ckm_status ckm_threshold_eval(const ckm_graph* g, const double* s_frac, int64_t 
                                 reinterpret_cast<int64_t*>(d + o_peak), reinterpret_cast<int64_t*>(d + o_cost),
                                 reinterpret_cast<uint8_t*>(d + o_feas), reinterpret_cast<int32_t*>(d + o_bk),
                                 best_S ? reinterpret_cast<uint64_t*>(d + o_bS) : nullptr,
-                                best_R ? reinterpret_cast<uint64_t*>(d + o_bR) : nullptr, nullptr, d + o_w, L.total,
+                                best_R ? reinterpret_cast<uint64_t*>(d + o_bR) : nullptr, nullptr, d + o_w, L.total_rows,
                                 sc.stream());
   if (st != CKM_OK) return st;
   const Result r[] = {{peak, o_peak, (size_t)K * 8}, {cost, o_cost, (size_t)K * 8}, {feasible, o_feas, (size_t)K},

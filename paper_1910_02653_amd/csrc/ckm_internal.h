@@ -79,10 +79,11 @@ struct Layout {
          plan_rt_off = 0, plan_rpre_off = 0,
          bbest_off = 0,  // per-block best of the batch multipliers
          total = 0,        // bytes every call needs
-         rows_off = 0,     // rounded rows (kSrcRows), past `total`
-         total_rows = 0;   // total plus the rounded rows when they are used
-  bool rows_on = false;    // the rounded rows fit kRowsMaxBytes (and, after
-                           // check_work, the caller's buffer holds them)
+         rows_off = 0,     // S rows of every candidate (kSrcRows), past `total`
+         rrows_off = 0,    // R rows of every candidate, written by the evaluate stage
+         total_rows = 0;   // total plus the two row arrays when they are used
+  bool rows_on = false;    // the S rows fit kRowsMaxBytes (and, after
+                           // check_work, the caller's buffer holds both arrays)
 };
 
 Layout make_layout(int32_t n, int32_t K);

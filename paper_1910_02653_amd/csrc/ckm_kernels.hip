@@ -292,8 +292,9 @@ struct EvalArgs {
   const uint32_t* __restrict__ s_user;  // kSrcUser: caller-supplied S rows ([K][n][s_words])
   int32_t s_words;                      // 32-bit words per supplied row
   const uint32_t* __restrict__ rank;    // kSrcThreshold: [K] threshold ranks (q holds the keys)
-  const uint32_t* __restrict__ rows;    // kSrcRows: rounded rows, word w of row t at rows_at(t, w)
-  int32_t kpad;                         // kSrcRows: candidates per row word (64 * groups)
+  const uint32_t* __restrict__ rows;    // kSrcRows: S rows, word w of row t at (row_base(t) + w) * kpad + k
+  uint32_t* __restrict__ rrows;         // R rows out, same layout, or NULL
+  int32_t kpad;                         // row arrays: candidates per row word (64 * groups)
   int64_t* __restrict__ part_peak;   // [K] running max over work items
   int64_t* __restrict__ part_cost;   // [K] running sum over work items
   int32_t* __restrict__ hdr;
@@ -455,6 +456,51 @@ __global__ void __launch_bounds__(kWave) ckm_round_rows_kernel(const uint32_t* _
     uint32_t word = round_word<true>(qrow, w, r, k, key0, key1);
     if (det_lane) word = drow[w];
     dst[(size_t)w * kpad] = word;
+  }
+}
+
+// Threshold rows for the kSrcRows source: block (candidate group, row r),
+// lane = candidate with threshold rank rank[k]; the same words gen_row makes
+// for kSrcThreshold. Lanes past K take candidate K-1's rank (results unused).
+__global__ void __launch_bounds__(kWave) ckm_threshold_rows_kernel(const uint32_t* __restrict__ q, int32_t ldq,
+                                                                   const uint32_t* __restrict__ rank, int32_t K,
+                                                                   int32_t kpad, uint32_t* __restrict__ rows) {
+  const int r = blockIdx.y;
+  const uint32_t k = blockIdx.x * kWave + threadIdx.x;
+  const uint32_t rk = rank[k < (uint32_t)K ? k : (uint32_t)K - 1u];
+  cptr<uint32_t> qrow = as_const(q) + (size_t)r * ldq;
+  uint32_t* dst = rows + row_base(r) * (size_t)kpad + k;
+  const int nw = (r >> 5) + 1;
+  for (int w = 0; w < nw; ++w) dst[(size_t)w * kpad] = threshold_word<true>(qrow, w, r, rk);
+}
+
+// The caller's S matrices ([K][n][s_words] 32-bit words) into the kSrcRows
+// layout, bits on and above the diagonal cleared: block (candidate group,
+// row r) of 256 threads. Reads run along each candidate's row, writes along
+// the candidates; an LDS tile [word][candidate] (stride kWave + 1, no bank
+// conflicts either way) turns one into the other. Lanes past K copy
+// candidate K-1 (results unused).
+__global__ void __launch_bounds__(256) ckm_user_rows_kernel(const uint32_t* __restrict__ s_user, int32_t n,
+                                                            int32_t K, int32_t s_words, int32_t kpad,
+                                                            uint32_t* __restrict__ rows) {
+  extern __shared__ uint32_t tile[];
+  const int r = blockIdx.y;
+  const int nw = (r >> 5) + 1;
+  const int k0 = blockIdx.x * kWave;
+  const int cells = nw * kWave;
+  const uint32_t diag = (1u << (r & 31)) - 1u;  // the diagonal's word keeps bits < r
+  for (int j = threadIdx.x; j < cells; j += blockDim.x) {
+    const int c = j / nw, w = j - c * nw;
+    const int k = min(k0 + c, K - 1);
+    uint32_t word = s_user[((size_t)k * n + r) * s_words + w];
+    if (w == nw - 1) word &= diag;
+    tile[w * (kWave + 1) + c] = word;
+  }
+  __syncthreads();
+  uint32_t* dst = rows + row_base(r) * (size_t)kpad + k0;
+  for (int j = threadIdx.x; j < cells; j += blockDim.x) {
+    const int w = j / kWave, c = j % kWave;
+    dst[(size_t)w * kpad + c] = tile[w * (kWave + 1) + c];
   }
 }
 
@@ -785,6 +831,10 @@ __device__ __forceinline__ void run_item(const EvalArgs& a, int t0, int t1, uint
     eval_stage(a, t, A, B, sp, sc);
     seg_peak = fmax(seg_peak, sp);
     seg_cost += (int64_t)sc;
+    if (a.rrows) {  // R_t, now in A, kept for the best-candidate output
+      uint32_t* dst = a.rrows + row_base(t) * (size_t)a.kpad + k;
+      for (int w = 0; w <= (t >> 5); ++w) dst[(size_t)w * a.kpad] = A.word(w);
+    }
     next_stage(A, B, t);
   }
 }
@@ -1127,6 +1177,22 @@ __global__ void __launch_bounds__(256) ckm_best_rows_kernel(const uint32_t* __re
   S_rows[(size_t)r * row_words + w] = word;
 }
 
+// Best candidate's R rows from the R rows the evaluate stage kept for every
+// candidate: thread per (row t, 32-bit word w). Words above t/32 (no node
+// at or below t), and every word when nothing is feasible, are zero.
+__global__ void __launch_bounds__(256) ckm_best_rrows_kernel(const uint32_t* __restrict__ rrows, int32_t kpad,
+                                                             int32_t row_words,
+                                                             const int32_t* __restrict__ best_k,
+                                                             uint32_t* __restrict__ R_rows) {
+  const int t = blockIdx.y;
+  const int w = blockIdx.x * blockDim.x + threadIdx.x;
+  if (w >= row_words) return;
+  const int bk = best_k[0];
+  uint32_t word = 0;
+  if (bk >= 0 && w <= (t >> 5)) word = rrows[(row_base(t) + w) * (size_t)kpad + bk];
+  R_rows[(size_t)t * row_words + w] = word;
+}
+
 // Best candidate's R rows: lane = stage t (64 stages per wave), Algorithm
 // 2's right-to-left repair over nodes v = (last stage of the wave) .. 0, all
 // lanes at the same node. As in the evaluate kernel, the R bits of the 64
@@ -1309,6 +1375,8 @@ int32_t eval_waves_per_cu(int32_t n) {
   return blocks;
 }
 
+static unsigned groups_of(int32_t K) { return (unsigned)((K + kWave - 1) / kWave); }
+
 hipError_t launch_round_rows(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed, uint32_t flags,
                              char* work, hipStream_t stream) {
   if (!L.rows_on) return hipSuccess;
@@ -1330,6 +1398,7 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   a.s_words = L.row_words;
   a.rank = at<const uint32_t>(work, L.thr_rank_off);
   a.rows = at<const uint32_t>(work, L.rows_off);
+  a.rrows = L.rows_on ? at<uint32_t>(work, L.rrows_off) : nullptr;
   a.kpad = ((K + kWave - 1) / kWave) * kWave;
   if (src == kSrcRound && L.rows_on) {
     // every row rounded once (here, or by an earlier launch_round_rows), then streamed
@@ -1337,6 +1406,19 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
       hipError_t e = launch_round_rows(g, L, K, seed, flags, work, stream);
       if (e != hipSuccess) return e;
     }
+    src = kSrcRows;
+  } else if (src == kSrcThreshold && L.rows_on) {
+    // threshold rows made once, then streamed
+    hipLaunchKernelGGL(ckm_threshold_rows_kernel, dim3(groups_of(K), g.n), dim3(kWave), 0, stream,
+                       at<const uint32_t>(work, L.q_off), L.ldq, at<const uint32_t>(work, L.thr_rank_off), K,
+                       a.kpad, at<uint32_t>(work, L.rows_off));
+    src = kSrcRows;
+  } else if (src == kSrcUser && L.rows_on) {
+    // the caller's rows transposed once into the streamed layout (reading
+    // them in place puts each lane of a load in another candidate's matrix)
+    const size_t tile = (size_t)(((g.n - 1) >> 5) + 1) * (kWave + 1) * sizeof(uint32_t);
+    hipLaunchKernelGGL(ckm_user_rows_kernel, dim3(groups_of(K), g.n), dim3(256), tile, stream, a.s_user, g.n, K,
+                       a.s_words, a.kpad, at<uint32_t>(work, L.rows_off));
     src = kSrcRows;
   }
   a.items = plan.items;
@@ -1424,6 +1506,14 @@ hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_
   hipLaunchKernelGGL(ckm_argmin_kernel, dim3(1), dim3(256), 0, stream, rb,
                      at<const Best>(work, L.best_off), src == kSrcUser ? 0 : g.n,
                      at<const int32_t>(work, L.nan_off), d_best_k, d_status);
+  // with the row arrays, the evaluate stage kept every candidate's R rows
+  const bool gather_R = d_best_R && L.rows_on;
+  if (gather_R) {
+    hipLaunchKernelGGL(ckm_best_rrows_kernel, dim3((L.row_words + 255) / 256, g.n), dim3(256), 0, stream,
+                       at<const uint32_t>(work, L.rrows_off), (int32_t)(groups_of(K) * kWave), L.row_words,
+                       d_best_k, reinterpret_cast<uint32_t*>(d_best_R));
+    d_best_R = nullptr;
+  }
   if (src == kSrcUser) {
     if (d_best_R) {
       hipError_t e = launch_closure(g, L, d_best_k, reinterpret_cast<const uint32_t*>(s_user),

@@ -90,6 +90,7 @@ def test_null_arguments_rejected():
     assert L.ckm_graph_create(2, None, None, None, None, None, None, 0, 0, None) == ckm.E_INVALID_ARG
     sz = C.c_size_t()
     assert L.ckm_workspace_size(None, 4, C.byref(sz)) == ckm.E_INVALID_ARG
+    assert L.ckm_workspace_size_min(None, 4, C.byref(sz)) == ckm.E_INVALID_ARG
     assert L.ckm_round_eval(None, None, 0, 4, 0, 0, 0, None, None, None, None, None, None) == ckm.E_INVALID_ARG
     assert L.ckm_evaluate_async(None, 4, 0, 0, 0, None, 0, None) == ckm.E_INVALID_ARG
     assert L.ckm_select_async(None, 4, 0, 0, 0, None, None, None, None, None, None, None, None, 0,

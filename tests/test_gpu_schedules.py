@@ -218,3 +218,37 @@ def test_nothing_feasible_and_bad_args():
             g.eval_schedules(rows[:, :-1], 0)
     finally:
         g.close()
+
+
+@pytest.mark.parametrize("cfg,K", [(2, 100), (3, 130), (4, 200)])
+def test_row_array_and_in_kernel_rows_agree(cfg, K):
+    """With the row array (the caller's matrices transposed into it once) and
+    without it (each lane reads its own matrix in the evaluate kernel): the
+    same results as the synchronous call, checked against the oracle."""
+    import torch
+    w = wl.config(cfg)
+    rows = wl.random_schedules(w.n, K, seed=10 + cfg, density=0.3, kind="bernoulli", junk=True)
+    g = ckm.Graph.from_workload(w)
+    try:
+        assert g.workspace_size(K, rows=False) < g.workspace_size(K)
+        budget = int(np.median(g.eval_schedules(rows, 2 ** 62)["peak"]))
+        sync = g.eval_schedules(rows, budget)
+        d_S = torch.from_numpy(rows.view(np.int64)).cuda()
+        for with_rows in (True, False):
+            log("config %d K=%d row array %s" % (cfg, K, with_rows))
+            work = g.alloc_work(K, rows=with_rows)
+            out = g.alloc_outputs(K)
+            g.eval_schedules_async(d_S, K, budget, out, work)
+            torch.cuda.synchronize()
+            for key in ("peak", "cost", "feasible"):
+                assert np.array_equal(out[key].cpu().numpy(), sync[key]), key
+            assert int(out["best_k"].item()) == sync["best_k"] >= 0
+            assert np.array_equal(ckm.rows_to_numpy(out["best_R"]), sync["best_R"])
+    finally:
+        g.close()
+    if cfg < 4:
+        check(w, rows, sync, budget)
+    else:
+        orc = oracle_schedules(w, rows, [0, 63, 64, 199, sync["best_k"]])
+        for k, pc in orc.items():
+            assert (int(sync["peak"][k]), int(sync["cost"][k])) == pc, k

@@ -240,3 +240,40 @@ def test_async_matches_sync_strided_and_nan():
         assert e.value.status == ckm.E_UNSUPPORTED
     finally:
         g.close()
+
+
+@pytest.mark.parametrize("cfg,K", [(2, 100), (3, 130), (4, 200)])
+def test_row_array_and_in_kernel_rows_agree(cfg, K):
+    """With the row array (threshold rows made once) and without it (made in
+    the evaluate kernel): the same results as the synchronous call, checked
+    against the oracle."""
+    import torch
+    w = wl.config(cfg)
+    p = grid(K, 20 + cfg)
+    g = ckm.Graph.from_workload(w)
+    try:
+        assert g.workspace_size(K, rows=False) < g.workspace_size(K)
+        budget = int(np.median(g.threshold_eval(w.s_frac, p, 2 ** 62)["peak"]))
+        sync = g.threshold_eval(w.s_frac, p, budget)
+        d_s = torch.from_numpy(w.s_frac).cuda()
+        d_p = torch.from_numpy(p).cuda()
+        for with_rows in (True, False):
+            log("config %d K=%d row array %s" % (cfg, K, with_rows))
+            work = g.alloc_work(K, rows=with_rows)
+            out = g.alloc_outputs(K)
+            g.threshold_eval_async(d_s, d_p, budget, out, work)
+            torch.cuda.synchronize()
+            assert int(out["status"].item()) == ckm.OK
+            for key in ("peak", "cost", "feasible"):
+                assert np.array_equal(out[key].cpu().numpy(), sync[key]), key
+            assert int(out["best_k"].item()) == sync["best_k"] >= 0
+            assert np.array_equal(ckm.rows_to_numpy(out["best_S"]), sync["best_S"])
+            assert np.array_equal(ckm.rows_to_numpy(out["best_R"]), sync["best_R"])
+    finally:
+        g.close()
+    if cfg < 4:
+        check(w, p, sync, budget)
+    else:
+        orc = oracle_thresholds(w, p, [0, 63, 64, 199, sync["best_k"]])
+        for k, pc in orc.items():
+            assert (int(sync["peak"][k]), int(sync["cost"][k])) == pc, k
