@@ -12,6 +12,10 @@ Prints one JSON line. `value` is candidate schedules evaluated per second.
 `roofline` prices the dominant kernel (the evaluate kernel) against HBM
 bandwidth with the algorithmic bytes of bit-packed S and R rows, each
 written once and read once: 4 * n * ceil(n/64) * 8 bytes per candidate.
+`roofline_alu` prices the same launch against the vector ALU issue rate that
+actually bounds it: VALU instructions per launch (committed rocprofv3
+counters of the current kernel source, else null) x 64 lanes / the launch
+time, against 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz.
 `cpu_baseline` times the CPU oracle on a bounded sample of the same
 workload, on every host thread (candidates split across them) and on one.
 `hbm_copy` is the bandwidth a plain device copy reaches on the same GPU, the
@@ -46,6 +50,8 @@ sys.path.insert(0, ROOT)
 
 METRIC = "candidate schedules evaluated/sec at n=1000,K=1024; % HBM roofline"
 HBM_PEAK_GBS = 8000.0
+# int32 VALU lane-operations per second: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+ALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_eval_transformer_n1009_K1024.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_1910_02653_amd", "csrc", "ckm_kernels.hip")
 
@@ -55,17 +61,18 @@ def kernel_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic():
-    """HBM bytes per evaluate launch from committed rocprofv3 counters, if they
-    were taken on the current kernel source."""
+def measured_counters():
+    """Counters of one evaluate launch from committed rocprofv3 runs (HBM
+    bytes, VALU instructions), if they were taken on the current kernel
+    source; else {}."""
     try:
         with open(TRAFFIC_FILE) as f:
             d = json.load(f)
     except (OSError, ValueError):
-        return None
+        return {}
     if d.get("kernel_sha256_16") != kernel_hash():
-        return None
-    return d.get("hbm_bytes_per_launch")
+        return {}
+    return d
 
 
 def host_threads() -> int:
@@ -406,7 +413,9 @@ def main():
 
     b_cand = 4 * n * W * 8
     achieved = K * b_cand / (eval_avg_ms * 1e-3) / 1e9
-    traffic = measured_traffic()
+    counters = measured_counters()
+    traffic = counters.get("hbm_bytes_per_launch")
+    valu = counters.get("valu_insts_per_launch")
     result = {
         "metric": METRIC,
         "value": K / (ms_step * 1e-3),
@@ -431,6 +440,10 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic},
+        "roofline_alu": ({"bound": "alu", "achieved": valu * 64 / (eval_avg_ms * 1e-3) / 1e12,
+                          "peak": ALU_PEAK_TOPS, "unit": "T lane-ops/s",
+                          "frac": valu * 64 / (eval_avg_ms * 1e-3) / 1e12 / ALU_PEAK_TOPS,
+                          "valu_insts_per_launch": valu} if valu else None),
         "hbm_copy": {"achieved": copy_gbs, "unit": "GB/s", "kernel": "device copy of 1 GiB (read + write)",
                      "evaluate_frac": achieved / copy_gbs},
         "wall_s": wall,
