@@ -223,14 +223,6 @@ __device__ __forceinline__ double dbl(uint32_t lo, uint32_t hi) {
   return __hiloint2double((int)hi, (int)lo);
 }
 
-// A zero the compiler cannot see through: added to an address, it keeps a
-// wave-uniform load a vector load (whose completion counter is in order, so
-// it can run nodes ahead of its use) instead of a scalar one.
-__device__ __forceinline__ uint32_t opaque_zero() {
-  uint32_t z;
-  asm volatile("v_mov_b32 %0, 0" : "=v"(z));
-  return z;
-}
 
 // A node record spread over the lanes of one vector register: lane L holds
 // dword L. Fields are moved to scalar registers when used
@@ -264,14 +256,25 @@ __device__ __forceinline__ uint32_t bitpos(uint32_t b0, uint32_t refs1, int k) {
 // Word index of byte j of a packed dword of word indices.
 __device__ __forceinline__ uint32_t word_at(uint32_t refs, int j) { return (refs >> (8 * j)) & 0xFFu; }
 
-__device__ __forceinline__ void load_rec(RecRegs& r, const uint4* __restrict__ recs, int v) {
-  // wave-uniform record base in scalar registers, one dword per lane
-  const int vu = __builtin_amdgcn_readfirstlane(v);
-  const char* base = reinterpret_cast<const char*>(recs) + (size_t)vu * kNodeRecBytes;
-  const size_t off = (size_t)((threadIdx.x & 63u) * 4u);
-  r.mc = *reinterpret_cast<const uint4*>(base + offsetof(NodeRec, mc) + (size_t)opaque_zero());
-  r.dm = *reinterpret_cast<const uint4*>(base + offsetof(NodeRec, dm01) + (size_t)opaque_zero());
-  r.w = *reinterpret_cast<const uint32_t*>(base + off);
+// Buffer descriptor word 3 for raw byte-addressed buffers on gfx9-family
+// GPUs (32-bit data format); the hardware returns 0 for reads past the
+// record count instead of faulting.
+constexpr int kBufWord3 = 0x00020000;
+
+// Loads node v's record into r: one dword per lane, plus the two fp64
+// groups in every lane. These are vector-memory loads, whose completion
+// counter is in order, so they can run nodes ahead of their use (a scalar
+// load would share its counter with LDS reads). As buffer loads with the
+// node's offset in a scalar register they need no per-node address
+// arithmetic in vector registers, which a global load of a uniform address
+// would (a zero or 64-bit address register rebuilt for each node).
+__device__ __forceinline__ void load_rec(RecRegs& r, __amdgpu_buffer_rsrc_t rs, int v) {
+  const int so = __builtin_amdgcn_readfirstlane(v) * kNodeRecBytes;
+  const auto mc = __builtin_amdgcn_raw_buffer_load_b128(rs, 0, so + (int)offsetof(NodeRec, mc), 0);
+  const auto dm = __builtin_amdgcn_raw_buffer_load_b128(rs, 0, so + (int)offsetof(NodeRec, dm01), 0);
+  r.mc = make_uint4(mc[0], mc[1], mc[2], mc[3]);
+  r.dm = make_uint4(dm[0], dm[1], dm[2], dm[3]);
+  r.w = __builtin_amdgcn_raw_buffer_load_b32(rs, (threadIdx.x & 63u) * 4u, so, 0);
 }
 
 struct EvalArgs {
@@ -716,6 +719,10 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
   const double rd = (double)r;
   sc.cost = fma(rd, Cv, sc.cost);
   sc.U0 = fma((double)s0, Mv, sc.U0);
+  // Keep both sums here: left free, the compiler sinks them to the end of
+  // the unrolled loop, which keeps a fourth record buffer alive and adds
+  // register copies to every iteration.
+  asm volatile("" : "+v"(sc.cost), "+v"(sc.U0));
   sc.maxv = max_f64(sc.maxv, val);
   sc.Y = fma(-rd, Mv, val);
   // slide the window down by one node: bit 0 becomes node v
@@ -731,6 +738,11 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
   }
 }
 
+// Descriptor of the node-record array.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rec_rsrc(const EvalArgs& a) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(a.recs), 0, a.n * kNodeRecBytes, kBufWord3);
+}
+
 // Waits for every load of a record buffer.
 __device__ __forceinline__ void settle(const RecRegs& r) {
   asm volatile("" ::"v"(r.w), "v"(r.mc.x), "v"(r.mc.y), "v"(r.mc.z), "v"(r.mc.w), "v"(r.dm.x), "v"(r.dm.y),
@@ -744,7 +756,7 @@ __device__ __forceinline__ void settle(const RecRegs& r) {
 template <int C, int N, int NN, bool kFirst, typename RowB>
 __device__ __forceinline__ void pipe_step(const EvalArgs& a, int t, int v, RecRegs (&rb)[3], LdsVals (&lb)[3],
                                           Scan& sc, Row A, RowB& B) {
-  load_rec(rb[NN], a.recs, max(v - 2, 0));
+  load_rec(rb[NN], rec_rsrc(a), max(v - 2, 0));
   issue_reads(rb[N], A, B, lb[N]);
   asm volatile("" ::: "memory");  // keep the requests ahead of this node's work
   scan_node<kFirst, RowB>(a, t, v, rb[C], lb[C], sc, A, B);
@@ -765,8 +777,8 @@ __device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, RowB
   sc.w1 = B.word(t >> 5);
   RecRegs rb[3];
   LdsVals lb[3];
-  load_rec(rb[0], a.recs, t);
-  load_rec(rb[1], a.recs, max(t - 1, 0));
+  load_rec(rb[0], rec_rsrc(a), t);
+  load_rec(rb[1], rec_rsrc(a), max(t - 1, 0));
   issue_reads(rb[0], A, B, lb[0]);
   int v = t;
   pipe_step<0, 1, 2, true>(a, t, v, rb, lb, sc, A, B);
