@@ -191,32 +191,37 @@ __device__ __forceinline__ uint32_t threshold_word(QPtr qrow, int w, int r, uint
 
 // ---------------------------------------------------------------------------
 // Per-node record, read once per node visit. Masks are relative to the node
-// v: bit d <-> node v + 1 + d, d < 64. A reference locates one bit of a row:
-// its word index (8 bits, packed four to a dword) and its bit position (5
-// bits, packed six to a dword). The references are: the user of v beyond
-// v + 64 in the R row (fu), and per dependency slot the user of the dep
-// beyond v + 64 in the R row (fl) and the dep in the next-stage checkpoint
-// row (s1); absent ones point at node n, whose bit no row ever sets.
+// v: bit d <-> node v + 1 + d, d < 32 (the scan's window of R bits). A
+// reference locates one bit of a row: its word index (8 bits, packed four to
+// a dword) and its bit position (5 bits, packed six to a dword). The
+// references are: the user of v beyond v + 32 in the R row (fu), and per
+// dependency slot the user of the dep beyond v + 32 in the R row (fl) and
+// the dep in the next-stage checkpoint row (s1); absent ones point at node
+// n, whose bit no row ever sets.
 constexpr int kRecDeps = 4;
 struct NodeRec {
   double M, C;              // M_v, C_v
-  uint32_t umask_lo;        // users u of v with u <= v + 32
-  uint32_t umask_hi;        //                  v + 32 < u <= v + 64
+  uint32_t umask;           // users u of v with u <= v + 32
   uint32_t refs0;           // word indices: fu | fl0 << 8 | s1_0 << 16 | fl1 << 24
   uint32_t refs1;           // s1_1 word | deps << 8 | slow << 11 | bit positions 6-8 at 12, 17, 22
   uint32_t bits0;           // bit positions 0-5 (fu, s1_0, fl0, s1_1, fl1, s1_2) | min(deps, 3) << 30,
                             // or 3 << 30 for a node outside the format
-  uint32_t lm[2 * kRecDeps];  // per slot: users u of the dep with v < u <= v + 32, then v + 32 < u <= v + 64
+  uint32_t lm[kRecDeps];    // per slot: users u of the dep with v < u <= v + 32
   uint32_t refs2;           // word indices: fl2 | s1_2 << 8 | fl3 << 16 | s1_3 << 24
+  uint32_t pad0;
   double dM[kRecDeps];      // M of each dependency slot
-  uint32_t pad0[2];
+  uint32_t pad1[2];
   // fp64 operands again, read by two wave-uniform 16-byte loads: M_v, C_v,
   // and the M of dependency slots 0 and 1
   double mc[2], dm01[2];
-  uint32_t pad[28];         // one dword per lane of a 64-lane load
+  uint32_t pad[32];         // one dword per lane of a 64-lane load
 };
 static_assert(sizeof(NodeRec) == kNodeRecBytes, "node record layout");
 static_assert(offsetof(NodeRec, mc) % 16 == 0 && offsetof(NodeRec, dm01) % 16 == 0, "16-byte loads");
+static_assert(offsetof(NodeRec, umask) == 16 && offsetof(NodeRec, refs0) == 20 && offsetof(NodeRec, refs1) == 24 &&
+                  offsetof(NodeRec, bits0) == 28 && offsetof(NodeRec, lm) == 32 && offsetof(NodeRec, refs2) == 48 &&
+                  offsetof(NodeRec, dM) == 56,
+              "dword indices used by RecRegs and the closure kernel");
 constexpr uint32_t kRefsSlow = 1u << 11;   // refs1: node does not fit, use the CSR lists
 
 __device__ __forceinline__ double dbl(uint32_t lo, uint32_t hi) {
@@ -235,15 +240,13 @@ struct RecRegs {
   __device__ double M() const { return dbl(mc.x, mc.y); }
   __device__ double C() const { return dbl(mc.z, mc.w); }
   __device__ double dM01(int s) const { return s == 0 ? dbl(dm.x, dm.y) : dbl(dm.z, dm.w); }
-  __device__ uint32_t umask_lo() const { return get(4); }
-  __device__ uint32_t umask_hi() const { return get(5); }
-  __device__ uint32_t refs0() const { return get(6); }
-  __device__ uint32_t refs1() const { return get(7); }
-  __device__ uint32_t bits0() const { return get(8); }
-  __device__ uint32_t lm_lo(int s) const { return get(9 + 2 * s); }
-  __device__ uint32_t lm_hi(int s) const { return get(10 + 2 * s); }
-  __device__ uint32_t refs2() const { return get(17); }
-  __device__ double dM(int s) const { return dbl(get(18 + 2 * s), get(19 + 2 * s)); }
+  __device__ uint32_t umask() const { return get(4); }
+  __device__ uint32_t refs0() const { return get(5); }
+  __device__ uint32_t refs1() const { return get(6); }
+  __device__ uint32_t bits0() const { return get(7); }
+  __device__ uint32_t lm(int s) const { return get(8 + s); }
+  __device__ uint32_t refs2() const { return get(12); }
+  __device__ double dM(int s) const { return dbl(get(14 + 2 * s), get(15 + 2 * s)); }
 };
 
 // Bit position k of a record (0: fu; 1 + 2s: s1 of slot s; 2 + 2s: fl of
@@ -554,19 +557,18 @@ __device__ __forceinline__ void gen_row(const EvalArgs& a, int r, uint32_t k, bo
 }
 
 // R bit of node u for a lane at node v of the right-to-left scan (v < u <= t):
-// nodes v+1 .. v+64 are in the window (Rlo: v+1 .. v+32, Rhi: v+33 .. v+64);
-// farther nodes lie in chunks already finished, whose R words are in A.
-__device__ __forceinline__ uint32_t r_bit(int u, int v, uint32_t Rlo, uint32_t Rhi, Row A) {
+// nodes v+1 .. v+32 are in the window Rwin (bit d <-> node v + 1 + d); a
+// farther node lies in a chunk already finished, whose R word is in A.
+__device__ __forceinline__ uint32_t r_bit(int u, int v, uint32_t Rwin, Row A) {
   const int d = u - v - 1;
-  if (d < 32) return bit(Rlo, d);
-  if (d < 64) return bit(Rhi, d - 32);
+  if (d < 32) return bit(Rwin, d);
   return bit(A.word(u >> 5), u & 31);
 }
 
 // Running state of the right-to-left scan of one stage (per lane).
 struct Scan {
   double U0, Y, maxv, cost;
-  uint32_t Rlo, Rhi;   // R bits of the 64 nodes above the current node
+  uint32_t Rwin;       // R bits of the 32 nodes above the current node
   uint32_t w0, w1;     // S_t and S_{t+1} words of the current chunk
 };
 
@@ -584,9 +586,9 @@ struct LdsVals {
 __device__ __forceinline__ void pin_s(uint32_t a, uint32_t b, uint32_t c) { asm volatile("" ::"s"(a), "s"(b), "s"(c)); }
 
 // Issues the reads for the node whose record is `rec`. They are issued one
-// node ahead of their use: the words they read are final by then (users
-// beyond the window lie in chunks already finished, S_{t+1} is not written
-// during the stage).
+// node ahead of their use: the words they read are final by then (a user
+// more than 32 nodes above the node lies in a chunk above the current one,
+// already finished; S_{t+1} is not written during the stage).
 template <typename RowB>
 __device__ __forceinline__ void issue_reads(const RecRegs& rec, Row A, RowB& B, LdsVals& L) {
   const uint32_t r0 = rec.refs0(), r1 = rec.refs1();
@@ -640,8 +642,8 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
   const uint32_t s0 = bit(sc.w0, jj);
   const uint32_t s1 = bit(sc.w1, jj);
   // the node's scalar fields, read together
-  const uint32_t um_lo = rec.umask_lo(), um_hi = rec.umask_hi(), b0 = rec.bits0();
-  pin_s(um_lo, um_hi, b0);
+  const uint32_t um = rec.umask(), b0 = rec.bits0();
+  pin_s(um, b0, b0);
   const double Mv = rec.M();
   const double Cv = rec.C();
   uint32_t anyU, r;
@@ -659,7 +661,7 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
       r = 1;
     } else {
       const uint32_t far = __builtin_amdgcn_ubfe(L.fu, b0, 1);
-      anyU = and_or(sc.Rlo, um_lo, and_or(sc.Rhi, um_hi, far));
+      anyU = and_or(sc.Rwin, um, far);
       anyU = umin1(anyU);
       r = (s1 | anyU) & ~s0 & 1u;
     }
@@ -668,18 +670,17 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
     // so only node t can be freed right after it is computed.
     if (kFirst) val = fma((double)(~s1 & 1u), Mv, val);
     auto slot = [&](int sl) {
-      const uint32_t lm_lo = rec.lm_lo(sl), lm_hi = rec.lm_hi(sl);
-      pin_s(lm_lo, lm_hi, lm_hi);
+      const uint32_t lm = rec.lm(sl);
       double dMs;
       if (sl < 2) {
         dMs = rec.dM01(sl);
       } else {
-        const uint32_t d_lo = rec.get(18 + 2 * sl), d_hi = rec.get(19 + 2 * sl);
+        const uint32_t d_lo = rec.get(14 + 2 * sl), d_hi = rec.get(15 + 2 * sl);
         pin_s(d_lo, d_hi, d_hi);
         dMs = dbl(d_lo, d_hi);
       }
       const uint32_t far = __builtin_amdgcn_ubfe(L.fl[sl], bitpos(b0, r1, 2 + 2 * sl), 1);
-      uint32_t later = and_or(sc.Rlo, lm_lo, and_or(sc.Rhi, lm_hi, far));
+      uint32_t later = and_or(sc.Rwin, lm, far);
       later = umin1(later);
       const uint32_t fr = r & ~__builtin_amdgcn_ubfe(L.s1[sl], bitpos(b0, r1, 1 + 2 * sl), 1) & ~later & 1u;
       val = fma((double)fr, dMs, val);
@@ -698,7 +699,7 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
     for (int e = a.user_ptr[v]; e < ue; ++e) {
       const int u = a.user_idx[e];
       if (u > t) break;
-      anyU |= r_bit(u, v, sc.Rlo, sc.Rhi, A);
+      anyU |= r_bit(u, v, sc.Rwin, A);
     }
     r = ((s1 | anyU) & ~s0 & 1u) | (uint32_t)kFirst;
     val = fma((double)(r & ~s1 & ~anyU & 1u), Mv, val);
@@ -710,7 +711,7 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
       for (int e2 = a.dep_upos[e]; e2 < le; ++e2) {
         const int u = a.user_idx[e2];
         if (u > t) break;
-        later |= r_bit(u, v, sc.Rlo, sc.Rhi, A);
+        later |= r_bit(u, v, sc.Rwin, A);
       }
       const uint32_t fr = r & ~bit(B.word(i >> 5), i & 31) & ~later & 1u;
       val = fma((double)fr, a.M[i], val);
@@ -726,11 +727,10 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
   sc.maxv = max_f64(sc.maxv, val);
   sc.Y = fma(-rd, Mv, val);
   // slide the window down by one node: bit 0 becomes node v
-  sc.Rhi = (sc.Rhi << 1) | (sc.Rlo >> 31);
-  sc.Rlo = (sc.Rlo << 1) | r;
+  sc.Rwin = (sc.Rwin << 1) | r;
   if (__builtin_expect(jj == 0, 0)) {  // chunk finished: R_t replaces S_t, move to the next chunk
     const int c = v >> 5;
-    A.word(c) = sc.Rlo;
+    A.word(c) = sc.Rwin;
     if (c > 0) {
       sc.w0 = A.word(c - 1);
       sc.w1 = B.word(c - 1);
@@ -772,7 +772,7 @@ __device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, RowB
   sc.Y = 0.0;
   sc.maxv = -INFINITY;
   sc.cost = 0.0;
-  sc.Rlo = sc.Rhi = 0;
+  sc.Rwin = 0;
   sc.w0 = A.word(t >> 5);
   sc.w1 = B.word(t >> 5);
   RecRegs rb[3];
@@ -1207,8 +1207,8 @@ __global__ void __launch_bounds__(256) ckm_best_rrows_kernel(const uint32_t* __r
 
 // Best candidate's R rows: lane = stage t (64 stages per wave), Algorithm
 // 2's right-to-left repair over nodes v = (last stage of the wave) .. 0, all
-// lanes at the same node. As in the evaluate kernel, the R bits of the 64
-// nodes above v sit in a two-register window and R words of finished chunks
+// lanes at the same node. As in the evaluate kernel, the R bits of the 32
+// nodes above v sit in a one-register window and R words of finished chunks
 // sit in an LDS row per lane ([word][lane]) for users beyond the window. With
 // one wave per SIMD nothing hides latency, so node records come 32 at a time
 // (a chunk, one register each, lane L holding dword L) one chunk ahead, and
@@ -1245,23 +1245,23 @@ __device__ __forceinline__ uint32_t rl(uint32_t w, int i) { return __builtin_amd
 
 // Nodes 32c + 31 .. 32c of the scan for the lane's stage t.
 __device__ __forceinline__ void closure_chunk(const ClosureArgs& a, int c, int t, int tmax, const uint32_t (&rec)[kChunk],
-                                              Row A, Row S0, Row S1, uint32_t& Rlo, uint32_t& Rhi) {
+                                              Row A, Row S0, Row S1, uint32_t& Rwin) {
   const uint32_t w0 = S0.word(c), w1 = S1.word(c);
-  uint32_t far_next = A.at_word(word_at(rl(rec[kChunk - 1], 6), 0));
+  uint32_t far_next = A.at_word(word_at(rl(rec[kChunk - 1], 5), 0));
 #pragma unroll
   for (int jj = kChunk - 1; jj >= 0; --jj) {
     const int v = kChunk * c + jj;
     const uint32_t far_w = far_next;
-    if (jj > 0) far_next = A.at_word(word_at(rl(rec[jj - 1], 6), 0));
+    if (jj > 0) far_next = A.at_word(word_at(rl(rec[jj - 1], 5), 0));
     uint32_t r = 0;
     if (v <= tmax) {
-      const uint32_t um_lo = rl(rec[jj], 4), um_hi = rl(rec[jj], 5), b0 = rl(rec[jj], 8);
-      pin_s(um_lo, um_hi, b0);
+      const uint32_t um = rl(rec[jj], 4), b0 = rl(rec[jj], 7);
+      pin_s(um, b0, b0);
       bool slow = false;
-      if (__builtin_expect((b0 >> 30) == 3u, 0)) slow = (rl(rec[jj], 7) & kRefsSlow) != 0u;
+      if (__builtin_expect((b0 >> 30) == 3u, 0)) slow = (rl(rec[jj], 6) & kRefsSlow) != 0u;
       uint32_t anyU;
       if (__builtin_expect(!slow, 1)) {
-        anyU = umin1(and_or(Rlo, um_lo, and_or(Rhi, um_hi, __builtin_amdgcn_ubfe(far_w, b0, 1))));
+        anyU = umin1(and_or(Rwin, um, __builtin_amdgcn_ubfe(far_w, b0, 1)));
       } else {
         // more than one user beyond the window: walk the users
         anyU = 0;
@@ -1269,17 +1269,16 @@ __device__ __forceinline__ void closure_chunk(const ClosureArgs& a, int c, int t
         for (int e = a.user_ptr[v]; e < ue; ++e) {
           const int u = a.user_idx[e];
           const int d = u - v - 1;
-          anyU |= d < 32 ? bit(Rlo, d) : (d < 64 ? bit(Rhi, d - 32) : bit(A.word(u >> 5), u & 31));
+          anyU |= d < 32 ? bit(Rwin, d) : bit(A.word(u >> 5), u & 31);
         }
       }
       r = ((bit(w1, jj) | anyU) & ~bit(w0, jj)) & 1u;
       if (v == t) r = 1u;
       if (v > t) r = 0u;
     }
-    Rhi = (Rhi << 1) | (Rlo >> 31);
-    Rlo = (Rlo << 1) | r;
+    Rwin = (Rwin << 1) | r;
   }
-  A.word(c) = Rlo;
+  A.word(c) = Rwin;
 }
 
 __global__ void __launch_bounds__(kWave) ckm_best_closure_kernel(ClosureArgs a) {
@@ -1309,16 +1308,16 @@ __global__ void __launch_bounds__(kWave) ckm_best_closure_kernel(ClosureArgs a) 
     S0.word(w) = in ? src0[w] : 0u;
     S1.word(w) = (in && has1) ? src1[w] : 0u;
   }
-  uint32_t Rlo = 0, Rhi = 0;
+  uint32_t Rwin = 0;
   uint32_t ra[kChunk], rb[kChunk];
   int c = tmax >> 5;
   load_chunk(ra, a.recs, c, a.n);
   for (;;) {
     if (c >= 1) load_chunk(rb, a.recs, c - 1, a.n);
-    closure_chunk(a, c, t, tmax, ra, A, S0, S1, Rlo, Rhi);
+    closure_chunk(a, c, t, tmax, ra, A, S0, S1, Rwin);
     if (--c < 0) break;
     if (c >= 1) load_chunk(ra, a.recs, c - 1, a.n);
-    closure_chunk(a, c, t, tmax, rb, A, S0, S1, Rlo, Rhi);
+    closure_chunk(a, c, t, tmax, rb, A, S0, S1, Rwin);
     if (--c < 0) break;
   }
   if (active)
@@ -1568,8 +1567,7 @@ void build_node_records(int32_t n, const double* M, const double* C, const int32
     for (int32_t e = user_ptr[v]; e < user_ptr[v + 1]; ++e) {
       const int u = user_idx[e];
       const int d = u - v - 1;
-      if (d < 32) r.umask_lo |= 1u << d;
-      else if (d < 64) r.umask_hi |= 1u << (d - 32);
+      if (d < 32) r.umask |= 1u << d;
       else if (nfar++ == 0) ref[0] = u;
     }
     if (nfar > 1) slow = true;
@@ -1584,8 +1582,7 @@ void build_node_records(int32_t n, const double* M, const double* C, const int32
         const int u = user_idx[e];
         if (u <= v) continue;
         const int d = u - v - 1;
-        if (d < 32) r.lm[2 * sl] |= 1u << d;
-        else if (d < 64) r.lm[2 * sl + 1] |= 1u << (d - 32);
+        if (d < 32) r.lm[sl] |= 1u << d;
         else if (nlate++ == 0) ref[2 + 2 * sl] = u;
       }
       if (nlate > 1) slow = true;
