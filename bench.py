@@ -334,8 +334,8 @@ def time_plan(g, w, steps, stream, d_s):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", type=int, default=4, help="workload 1..5 (4 = transformer stack)")
     ap.add_argument("--splits", type=int, default=0, help="stage splits per 64 candidates (0 = auto)")
     ap.add_argument("--cpu-sample", type=int, default=1024,
