@@ -663,7 +663,8 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
       const uint32_t far = __builtin_amdgcn_ubfe(L.fu, b0, 1);
       anyU = and_or(sc.Rwin, um, far);
       anyU = umin1(anyU);
-      r = (s1 | anyU) & ~s0 & 1u;
+      // s0, s1 and anyU are each 0 or 1, so this is one 3-input bit op
+      r = (s1 | anyU) & ~s0;
     }
     // FREE(t,v,v): v computed, not kept, no computed user after it. A node
     // other than t is computed only because it is kept (s1) or used (anyU),
@@ -682,7 +683,8 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
       const uint32_t far = __builtin_amdgcn_ubfe(L.fl[sl], bitpos(b0, r1, 2 + 2 * sl), 1);
       uint32_t later = and_or(sc.Rwin, lm, far);
       later = umin1(later);
-      const uint32_t fr = r & ~__builtin_amdgcn_ubfe(L.s1[sl], bitpos(b0, r1, 1 + 2 * sl), 1) & ~later & 1u;
+      // r and later are 0 or 1: no mask needed
+      const uint32_t fr = r & ~__builtin_amdgcn_ubfe(L.s1[sl], bitpos(b0, r1, 1 + 2 * sl), 1) & ~later;
       val = fma((double)fr, dMs, val);
     };
     // most nodes have one or two dependencies
