@@ -451,7 +451,7 @@ __global__ void __launch_bounds__(kWave) ckm_round_rows_kernel(const uint32_t* _
                                                                int32_t det_words, uint32_t key0, uint32_t key1,
                                                                uint32_t det0, int32_t kpad,
                                                                uint32_t* __restrict__ rows) {
-  const int r = blockIdx.y;
+  const int r = gridDim.y - 1 - blockIdx.y;  // long rows (high r) dispatched first: a shorter tail
   const uint32_t k = blockIdx.x * kWave + threadIdx.x;
   const bool det_lane = det0 && k == 0;
   cptr<uint32_t> qrow = as_const(q) + (size_t)r * ldq;
@@ -471,7 +471,7 @@ __global__ void __launch_bounds__(kWave) ckm_round_rows_kernel(const uint32_t* _
 __global__ void __launch_bounds__(kWave) ckm_threshold_rows_kernel(const uint32_t* __restrict__ q, int32_t ldq,
                                                                    const uint32_t* __restrict__ rank, int32_t K,
                                                                    int32_t kpad, uint32_t* __restrict__ rows) {
-  const int r = blockIdx.y;
+  const int r = gridDim.y - 1 - blockIdx.y;  // long rows (high r) dispatched first: a shorter tail
   const uint32_t k = blockIdx.x * kWave + threadIdx.x;
   const uint32_t rk = rank[k < (uint32_t)K ? k : (uint32_t)K - 1u];
   cptr<uint32_t> qrow = as_const(q) + (size_t)r * ldq;
@@ -490,7 +490,7 @@ __global__ void __launch_bounds__(256) ckm_user_rows_kernel(const uint32_t* __re
                                                             int32_t K, int32_t s_words, int32_t kpad,
                                                             uint32_t* __restrict__ rows) {
   extern __shared__ uint32_t tile[];
-  const int r = blockIdx.y;
+  const int r = gridDim.y - 1 - blockIdx.y;  // long rows (high r) dispatched first: a shorter tail
   const int nw = (r >> 5) + 1;
   const int k0 = blockIdx.x * kWave;
   const int cells = nw * kWave;
