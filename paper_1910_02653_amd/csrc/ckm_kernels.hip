@@ -477,7 +477,18 @@ __global__ void __launch_bounds__(kWave) ckm_threshold_rows_kernel(const uint32_
   cptr<uint32_t> qrow = as_const(q) + (size_t)r * ldq;
   uint32_t* dst = rows + row_base(r) * (size_t)kpad + k;
   const int nw = (r >> 5) + 1;
-  for (int w = 0; w < nw; ++w) dst[(size_t)w * kpad] = threshold_word<true>(qrow, w, r, rk);
+  for (int w = 0; w < nw; ++w) {
+    // the word's 32 keys at once: one wait instead of one per byte (keys on
+    // and above the diagonal are 0 and give 0 bits, so no entry is skipped;
+    // the key rows are ldq >= 32 * nw entries long)
+    uint32_t key[32];
+#pragma unroll
+    for (int j = 0; j < 32; ++j) key[j] = qrow[32 * w + j];
+    uint32_t word = 0;
+#pragma unroll
+    for (int b = 3; b >= 0; --b) word = append8_rank(word, rk, key + 8 * b);
+    dst[(size_t)w * kpad] = word;
+  }
 }
 
 // The caller's S matrices ([K][n][s_words] 32-bit words) into the kSrcRows
