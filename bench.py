@@ -30,6 +30,10 @@ argmin and the best S and R.
 `max_batch` times quantize + evaluate + the largest batch multiplier of
 every candidate (budget 3x the median activation peak, cost cap at the
 median cost) on the same workload.
+`pipelined` times the same steps over two work buffers, a step's thresholds
+and rounding on a second stream beside the previous step's evaluation (which
+leaves vector ALU slots free), timed by events around the whole loop only:
+per-step timing events on the main stream stop the two from overlapping.
 `feasible_budget` times the same step at the median-peak budget, where
 select also writes the best candidate's S and R rows.
 `execution_plan` times Algorithm 1's plan (with the memory after each
@@ -291,6 +295,50 @@ def time_feasible(g, w, steps, stream, d_s):
             "input": "the bench step at the median-peak budget %d B (best S and R rows written)" % budget}
 
 
+def time_pipelined(g, w, steps, stream, d_s):
+    """Consecutive steps overlapped: thresholds and rounding of step i+1 (on
+    a second stream, into the other of two work buffers) beside the
+    evaluation and selection of step i. Events order each buffer's reuse."""
+    import torch
+
+    from paper_1910_02653_amd import ckm
+
+    K = w.K
+    works = [g.alloc_work(K), g.alloc_work(K)]
+    out = g.alloc_outputs(K)
+    side = torch.cuda.Stream()              # default priority, like the main stream
+    rounded = [torch.cuda.Event(), torch.cuda.Event()]
+    released = [torch.cuda.Event(), torch.cuda.Event()]
+    for e in released:
+        e.record(stream)
+
+    def step(i):
+        b = i & 1
+        side.wait_event(released[b])        # the step two back is done with this buffer
+        g.quantize_async(d_s, works[b], side)
+        g.round_async(K, w.seed, 0, works[b], side)
+        rounded[b].record(side)
+        stream.wait_event(rounded[b])
+        g.evaluate_async(K, w.seed, ckm.F_ROUNDED, works[b], stream=stream)
+        g.select_async(K, w.seed, w.budget, 0, out, works[b], stream)
+        released[b].record(stream)
+
+    for i in range(10):
+        step(i)
+    torch.cuda.synchronize()
+    assert int(out["status"].item()) == ckm.OK
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(steps):
+        step(i)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    return {"value": K / (ms * 1e-3), "unit": "candidates/s", "ms_per_step": ms, "steps": steps,
+            "input": "the bench step, consecutive steps overlapped on two streams and two work buffers"}
+
+
 def time_plan(g, w, steps, stream, d_s):
     """Throughput of ckm_plan_async on one schedule of the workload: the best
     candidate at the median-peak budget (a budget some candidates meet)."""
@@ -349,6 +397,8 @@ def main():
                     help="timed calls of the threshold-family evaluation (0 = skip)")
     ap.add_argument("--plan-steps", type=int, default=20,
                     help="timed calls of the execution-plan generation (0 = skip)")
+    ap.add_argument("--pipe-steps", type=int, default=100,
+                    help="timed steps with consecutive steps overlapped (0 = skip)")
     ap.add_argument("--feasible-steps", type=int, default=20,
                     help="timed steps at the median-peak budget (0 = skip)")
     ap.add_argument("--batch-steps", type=int, default=20,
@@ -450,6 +500,8 @@ def main():
     }
     if args.host_steps > 0:
         result["host_round_trip"] = time_host_round_trip(g, w, K, args.host_steps)
+    if args.pipe_steps > 0:
+        result["pipelined"] = time_pipelined(g, w, args.pipe_steps, stream, d_s)
     if args.feasible_steps > 0:
         result["feasible_budget"] = time_feasible(g, w, args.feasible_steps, stream, d_s)
     if args.sched_steps > 0:
