@@ -133,7 +133,9 @@ ckm_status ckm_round_eval(const ckm_graph* g, const double* s_frac, int64_t ld, 
  * quantize -> evaluate -> select, on one work buffer. */
 
 /* Bytes of work buffer for K candidates on graph g. This includes, when the
- * S rows of all K candidates fit in 1 GiB, room for them (the row array):
+ * S rows of all K candidates fit in 8 GiB, room for them and for their R
+ * rows (the row arrays, twice the S rows' size; 8.3 GB at n = 4001,
+ * K = 4096):
  * the evaluate stage then streams each row from there instead of making it
  * twice (randomized rounding, threshold rounding) or reading it from each
  * candidate's own matrix (supplied schedules). A smaller buffer of at least

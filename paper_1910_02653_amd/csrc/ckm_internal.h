@@ -48,10 +48,12 @@ enum : int {
   kSrcRows = 3,       // randomized rounding done beforehand into the work buffer's row array
 };
 
-// The rounded-row array of the randomized path is used when it fits in this
-// many bytes (it holds K * n^2 / 64 words); larger problems round in the
-// evaluate kernel.
-constexpr size_t kRowsMaxBytes = (size_t)1 << 30;
+// The row arrays (S rows streamed by the evaluate kernel, R rows it keeps)
+// are used when the S rows fit in this many bytes (about K * n^2 / 16 bytes
+// each; 4.1 GB at n = 4001, K = 4096); larger problems, or work buffers sized
+// without them, make the S rows in the evaluate kernel and recompute the best
+// candidate's R.
+constexpr size_t kRowsMaxBytes = (size_t)8 << 30;
 
 // Host-side builder of the per-node records the evaluate kernel reads
 // (layout documented with NodeRec in ckm_kernels.hip). Writes n records.

@@ -290,23 +290,28 @@ def test_async_stages_and_split_invariance():
 
 
 def test_rounded_flag_without_row_array():
-    """n = 4001, K = 4096: the rounded rows would take 4.1 GB, so there is no
-    row array; ckm_round_async does nothing and evaluate with CKM_F_ROUNDED
-    rounds inside, with the same results as the one-call form."""
+    """n = 4001, K = 4096 on a work buffer without the row arrays:
+    ckm_round_async does nothing and evaluate with CKM_F_ROUNDED rounds
+    inside, with the same results for every candidate as the one-call form
+    on a buffer with the row arrays (4.1 GB of S rows, streamed)."""
     import torch
     w = wl.config(5)
     g = ckm.Graph.from_workload(w)
     try:
         work = g.alloc_work(w.K)
+        small = g.alloc_work(w.K, rows=False)
+        assert small.numel() < work.numel()
         d_s = torch.from_numpy(w.s_frac).cuda()
         budget = int(w.budget * 2)
         a = g.alloc_outputs(w.K)
         g.round_eval_async(d_s, w.K, w.seed, budget, 0, a, work)
+        torch.cuda.synchronize()
+        del work
         b = g.alloc_outputs(w.K)
-        g.quantize_async(d_s, work)
-        g.round_async(w.K, w.seed, 0, work)
-        g.evaluate_async(w.K, w.seed, ckm.F_ROUNDED, work)
-        g.select_async(w.K, w.seed, budget, 0, b, work)
+        g.quantize_async(d_s, small)
+        g.round_async(w.K, w.seed, 0, small)
+        g.evaluate_async(w.K, w.seed, ckm.F_ROUNDED, small)
+        g.select_async(w.K, w.seed, budget, 0, b, small)
         torch.cuda.synchronize()
         log("config 5 rounded flag")
         for key in ("peak", "cost", "feasible", "best_k"):
