@@ -1101,6 +1101,46 @@ __global__ void __launch_bounds__(256) ckm_argmin_kernel(int32_t nblocks, const 
   }
 }
 
+// Both steps in one block of 1024 threads, for K up to kSelectOneBlock: each
+// thread walks candidates tid, tid + 1024, ... (in increasing k, so among
+// equal (cost, peak) it keeps the smallest k), then the block's minimum.
+constexpr int kSelectOneBlock = 1 << 16;
+__global__ void __launch_bounds__(1024) ckm_select_kernel(int32_t K, const int64_t* __restrict__ tot_peak,
+                                                          const int64_t* __restrict__ tot_cost, int64_t budget,
+                                                          int64_t* __restrict__ peak, int64_t* __restrict__ cost,
+                                                          uint8_t* __restrict__ feasible, int32_t n,
+                                                          const int32_t* __restrict__ nan_row,
+                                                          int32_t* __restrict__ best_k,
+                                                          int32_t* __restrict__ status) {
+  __shared__ Best sb[1024];
+  __shared__ int any_nan;
+  if (threadIdx.x == 0) any_nan = 0;
+  Best b{0, 0, -1, 0};
+  for (int k = threadIdx.x; k < K; k += blockDim.x) {
+    const int64_t p = tot_peak[k], c = tot_cost[k];
+    peak[k] = p;
+    cost[k] = c;
+    const bool f = p <= budget;
+    feasible[k] = f ? 1 : 0;
+    const Best x{c, p, k, 0};
+    if (f && better(x, b)) b = x;
+  }
+  int nan = 0;
+  for (int r = threadIdx.x; r < n; r += blockDim.x) nan |= nan_row[r];
+  sb[threadIdx.x] = b;
+  __syncthreads();
+  if (nan) atomicOr(&any_nan, 1);
+  for (int off = blockDim.x / 2; off > 0; off >>= 1) {
+    if (threadIdx.x < off && better(sb[threadIdx.x + off], sb[threadIdx.x]))
+      sb[threadIdx.x] = sb[threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    best_k[0] = sb[0].k;
+    if (status) status[0] = any_nan ? (int32_t)CKM_E_INVALID_ARG : (int32_t)CKM_OK;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Largest batch multiplier per candidate (the maximum-batch experiment of
 // the evaluation): with node sizes B * M_i (M_in, M_param fixed) every U term
@@ -1178,6 +1218,8 @@ __global__ void __launch_bounds__(256) ckm_batch_argmax_kernel(int32_t nblocks, 
 // Best candidate's S rows: thread per (row r, 32-bit word w). Output rows
 // have row_words words; words with no node (32w >= n) are zero. rank: the
 // threshold family (q holds keys), else randomized or deterministic rounding.
+// With R_rows, the same threads also gather the best candidate's R rows
+// from the R rows the evaluate kernel kept (words above r/32 are zero).
 __global__ void __launch_bounds__(256) ckm_best_rows_kernel(const uint32_t* __restrict__ q,
                                                             const uint32_t* __restrict__ det,
                                                             int32_t n, int32_t ldq, int32_t det_words,
@@ -1185,11 +1227,18 @@ __global__ void __launch_bounds__(256) ckm_best_rows_kernel(const uint32_t* __re
                                                             uint32_t key1, uint32_t det0,
                                                             const uint32_t* __restrict__ rank,
                                                             const int32_t* __restrict__ best_k,
-                                                            uint32_t* __restrict__ S_rows) {
+                                                            uint32_t* __restrict__ S_rows,
+                                                            const uint32_t* __restrict__ rrows, int32_t kpad,
+                                                            uint32_t* __restrict__ R_rows) {
   const int r = blockIdx.y;
   const int w = blockIdx.x * blockDim.x + threadIdx.x;
   if (w >= row_words) return;
   const int bk = best_k[0];
+  if (R_rows) {
+    uint32_t rw = 0;
+    if (bk >= 0 && w <= (r >> 5)) rw = rrows[(row_base(r) + w) * (size_t)kpad + bk];
+    R_rows[(size_t)r * row_words + w] = rw;
+  }
   uint32_t word = 0;
   if (bk >= 0 && 32 * w < n) {
     if (rank)
@@ -1522,40 +1571,47 @@ hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_
                          uint8_t* d_feasible, int32_t* d_best_k, uint64_t* d_best_S,
                          uint64_t* d_best_R, int32_t* d_status, int src, const uint64_t* s_user,
                          char* work, hipStream_t stream) {
-  const int rb = L.reduce_blocks;
-  hipLaunchKernelGGL(ckm_reduce_kernel, dim3(rb), dim3(256), 0, stream, K,
-                     at<const int64_t>(work, L.part_peak_off), at<const int64_t>(work, L.part_cost_off),
-                     budget, d_peak, d_cost, d_feasible, at<Best>(work, L.best_off));
   // rounded candidates: NaN flags from the quantize or key stage; supplied S: none
-  hipLaunchKernelGGL(ckm_argmin_kernel, dim3(1), dim3(256), 0, stream, rb,
-                     at<const Best>(work, L.best_off), src == kSrcUser ? 0 : g.n,
-                     at<const int32_t>(work, L.nan_off), d_best_k, d_status);
-  // with the row arrays, the evaluate stage kept every candidate's R rows
-  const bool gather_R = d_best_R && L.rows_on;
-  if (gather_R) {
-    hipLaunchKernelGGL(ckm_best_rrows_kernel, dim3((L.row_words + 255) / 256, g.n), dim3(256), 0, stream,
-                       at<const uint32_t>(work, L.rrows_off), (int32_t)(groups_of(K) * kWave), L.row_words,
-                       d_best_k, reinterpret_cast<uint32_t*>(d_best_R));
-    d_best_R = nullptr;
+  const int32_t nan_rows = src == kSrcUser ? 0 : g.n;
+  if (K <= kSelectOneBlock) {
+    hipLaunchKernelGGL(ckm_select_kernel, dim3(1), dim3(1024), 0, stream, K,
+                       at<const int64_t>(work, L.part_peak_off), at<const int64_t>(work, L.part_cost_off), budget,
+                       d_peak, d_cost, d_feasible, nan_rows, at<const int32_t>(work, L.nan_off), d_best_k, d_status);
+  } else {
+    const int rb = L.reduce_blocks;
+    hipLaunchKernelGGL(ckm_reduce_kernel, dim3(rb), dim3(256), 0, stream, K,
+                       at<const int64_t>(work, L.part_peak_off), at<const int64_t>(work, L.part_cost_off),
+                       budget, d_peak, d_cost, d_feasible, at<Best>(work, L.best_off));
+    hipLaunchKernelGGL(ckm_argmin_kernel, dim3(1), dim3(256), 0, stream, rb,
+                       at<const Best>(work, L.best_off), nan_rows, at<const int32_t>(work, L.nan_off), d_best_k,
+                       d_status);
   }
+  // With the row arrays the evaluate stage kept every candidate's R rows, so
+  // the best R is a gather; otherwise Algorithm 2 runs again for it.
+  const bool gather_R = d_best_R && L.rows_on;
+  const int32_t kpad = (int32_t)(groups_of(K) * kWave);
+  const dim3 rows_grid((L.row_words + 255) / 256, g.n);
+  uint32_t* R_out = reinterpret_cast<uint32_t*>(d_best_R);
   if (src == kSrcUser) {
-    if (d_best_R) {
+    if (gather_R) {
+      hipLaunchKernelGGL(ckm_best_rrows_kernel, rows_grid, dim3(256), 0, stream,
+                         at<const uint32_t>(work, L.rrows_off), kpad, L.row_words, d_best_k, R_out);
+    } else if (d_best_R) {
       hipError_t e = launch_closure(g, L, d_best_k, reinterpret_cast<const uint32_t*>(s_user),
-                                    (size_t)g.n * L.row_words, reinterpret_cast<uint32_t*>(d_best_R), stream);
+                                    (size_t)g.n * L.row_words, R_out, stream);
       if (e != hipSuccess) return e;
     }
   } else if (d_best_S || d_best_R) {
+    // the S rows: output, and the closure's input when there is no gather
     uint32_t* srows = d_best_S ? reinterpret_cast<uint32_t*>(d_best_S) : at<uint32_t>(work, L.srows_off);
-    dim3 grid((L.row_words + 255) / 256, g.n);
-    hipLaunchKernelGGL(ckm_best_rows_kernel, grid, dim3(256), 0, stream,
+    hipLaunchKernelGGL(ckm_best_rows_kernel, rows_grid, dim3(256), 0, stream,
                        at<const uint32_t>(work, L.q_off), at<const uint32_t>(work, L.det_off), g.n,
                        L.ldq, L.det_words, L.row_words, (uint32_t)(seed & 0xFFFFFFFFu),
                        (uint32_t)(seed >> 32), (flags & CKM_F_DET0) ? 1u : 0u,
                        src == kSrcThreshold ? at<const uint32_t>(work, L.thr_rank_off) : nullptr, d_best_k,
-                       srows);
-    if (d_best_R) {
-      hipError_t e = launch_closure(g, L, d_best_k, static_cast<const uint32_t*>(srows), (size_t)0,
-                                    reinterpret_cast<uint32_t*>(d_best_R), stream);
+                       srows, at<const uint32_t>(work, L.rrows_off), kpad, gather_R ? R_out : nullptr);
+    if (d_best_R && !gather_R) {
+      hipError_t e = launch_closure(g, L, d_best_k, static_cast<const uint32_t*>(srows), (size_t)0, R_out, stream);
       if (e != hipSuccess) return e;
     }
   }

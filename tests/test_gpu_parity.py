@@ -128,6 +128,19 @@ def test_det0_candidate(cfg):
     check_full(w, got2, flags=ckm.F_DET0, budget=big)
 
 
+def test_many_candidates_two_stage_select():
+    """K = 70,001 (more than one select block handles: reduction in blocks,
+    then the argmin) on workload 1, every candidate against the oracle at a
+    budget about half of them meet."""
+    w = wl.config(1).replace(K=70001)
+    peak0 = gpu_round_eval(w, budget=2 ** 62)["peak"]
+    budget = int(np.median(peak0))
+    log("K=%d budget %d" % (w.K, budget))
+    got = gpu_round_eval(w, budget=budget)
+    check_full(w, got, budget=budget)
+    assert got["best_k"] >= 0
+
+
 def test_config4_transformer_full_parity():
     w = wl.config(4)
     log("config 4 n=%d K=%d" % (w.n, w.K))
