@@ -101,7 +101,7 @@ def test_config4_transformer_schedules():
 
 
 def test_config5_sampled():
-    """n = 4001 (two LDS rows): sampled candidates against the oracle."""
+    """n = 4001 (128-word register row): sampled candidates against the oracle."""
     w = wl.config(5)
     K = 70
     rows = wl.random_schedules(w.n, K, seed=505, density=0.1, kind="intervals")

@@ -113,7 +113,7 @@ def test_config4_transformer_grid():
 
 
 def test_config5_sampled():
-    """n = 4001 (two LDS rows): sampled thresholds against the oracle."""
+    """n = 4001 (128-word register row): sampled thresholds against the oracle."""
     w = wl.config(5)
     p = grid(96, 5)
     log("config 5 n=%d K=96" % w.n)
