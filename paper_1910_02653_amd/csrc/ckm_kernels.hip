@@ -6,8 +6,13 @@
 // stages. All lanes walk the same nodes in the same order, so graph data,
 // thresholds and loop bounds are wave-uniform and only the candidate's bits
 // and running sums differ per lane. Each lane keeps two bit rows (32-bit
-// words, bit i%32 of word i/32) in LDS, laid out [word][lane] so that a
-// wave-uniform word index touches 64 consecutive dwords: no bank conflicts.
+// words, bit i%32 of word i/32): S_t, which becomes R_t as the scan passes,
+// in LDS laid out [word][lane] so that a wave-uniform word index touches 64
+// consecutive dwords (no bank conflicts), and S_{t+1} in vector registers
+// (in LDS too for the largest graphs). S rows are rounded beforehand into a
+// row array in HBM, [row][word][candidate], and streamed; R rows go back to
+// a second such array for the best-candidate output. Without those arrays
+// the kernel makes its own S rows.
 //
 // Sums of sizes and costs run in binary64. The host admits only graphs whose
 // totals stay below 2^53, so every partial sum is an exactly represented
