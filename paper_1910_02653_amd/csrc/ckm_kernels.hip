@@ -223,10 +223,13 @@ struct NodeRec {
 };
 static_assert(sizeof(NodeRec) == kNodeRecBytes, "node record layout");
 static_assert(offsetof(NodeRec, mc) % 16 == 0 && offsetof(NodeRec, dm01) % 16 == 0, "16-byte loads");
-static_assert(offsetof(NodeRec, umask) == 16 && offsetof(NodeRec, refs0) == 20 && offsetof(NodeRec, refs1) == 24 &&
-                  offsetof(NodeRec, bits0) == 28 && offsetof(NodeRec, lm) == 32 && offsetof(NodeRec, refs2) == 48 &&
-                  offsetof(NodeRec, dM) == 56,
-              "dword indices used by RecRegs and the closure kernel");
+// Dword indices of the fields that move to scalar registers (v_readlane).
+constexpr int kDwUmask = 4, kDwRefs0 = 5, kDwRefs1 = 6, kDwBits0 = 7, kDwLm = 8, kDwRefs2 = 12, kDwDM = 14;
+static_assert(offsetof(NodeRec, umask) == 4 * kDwUmask && offsetof(NodeRec, refs0) == 4 * kDwRefs0 &&
+                  offsetof(NodeRec, refs1) == 4 * kDwRefs1 && offsetof(NodeRec, bits0) == 4 * kDwBits0 &&
+                  offsetof(NodeRec, lm) == 4 * kDwLm && offsetof(NodeRec, refs2) == 4 * kDwRefs2 &&
+                  offsetof(NodeRec, dM) == 4 * kDwDM,
+              "dword indices used by RecRegs, issue_reads and the closure kernel");
 constexpr uint32_t kRefsSlow = 1u << 11;   // refs1: node does not fit, use the CSR lists
 
 __device__ __forceinline__ double dbl(uint32_t lo, uint32_t hi) {
@@ -245,13 +248,13 @@ struct RecRegs {
   __device__ double M() const { return dbl(mc.x, mc.y); }
   __device__ double C() const { return dbl(mc.z, mc.w); }
   __device__ double dM01(int s) const { return s == 0 ? dbl(dm.x, dm.y) : dbl(dm.z, dm.w); }
-  __device__ uint32_t umask() const { return get(4); }
-  __device__ uint32_t refs0() const { return get(5); }
-  __device__ uint32_t refs1() const { return get(6); }
-  __device__ uint32_t bits0() const { return get(7); }
-  __device__ uint32_t lm(int s) const { return get(8 + s); }
-  __device__ uint32_t refs2() const { return get(12); }
-  __device__ double dM(int s) const { return dbl(get(14 + 2 * s), get(15 + 2 * s)); }
+  __device__ uint32_t umask() const { return get(kDwUmask); }
+  __device__ uint32_t refs0() const { return get(kDwRefs0); }
+  __device__ uint32_t refs1() const { return get(kDwRefs1); }
+  __device__ uint32_t bits0() const { return get(kDwBits0); }
+  __device__ uint32_t lm(int s) const { return get(kDwLm + s); }
+  __device__ uint32_t refs2() const { return get(kDwRefs2); }
+  __device__ double dM(int s) const { return dbl(get(kDwDM + 2 * s), get(kDwDM + 1 + 2 * s)); }
 };
 
 // Bit position k of a record (0: fu; 1 + 2s: s1 of slot s; 2 + 2s: fl of
@@ -269,20 +272,28 @@ __device__ __forceinline__ uint32_t word_at(uint32_t refs, int j) { return (refs
 // record count instead of faulting.
 constexpr int kBufWord3 = 0x00020000;
 
-// Loads node v's record into r: one dword per lane, plus the two fp64
-// groups in every lane. These are vector-memory loads, whose completion
-// counter is in order, so they can run nodes ahead of their use (a scalar
-// load would share its counter with LDS reads). As buffer loads with the
-// node's offset in a scalar register they need no per-node address
+// A node record is loaded in two parts: the lane's dword of it (the fields
+// that go to scalar registers; needed one node before the node itself, for
+// its LDS reads) and the two fp64 groups, the same 16 bytes in every lane
+// (needed when the node is evaluated). These are vector-memory loads, whose
+// completion counter is in order, so they can run nodes ahead of their use
+// (a scalar load would share its counter with LDS reads). As buffer loads
+// with the node's offset in a scalar register they need no per-node address
 // arithmetic in vector registers, which a global load of a uniform address
 // would (a zero or 64-bit address register rebuilt for each node).
-__device__ __forceinline__ void load_rec(RecRegs& r, __amdgpu_buffer_rsrc_t rs, int v) {
+struct RecF {
+  uint4 mc, dm;
+};
+__device__ __forceinline__ void load_rec_w(uint32_t& w, __amdgpu_buffer_rsrc_t rs, int v) {
+  const int so = __builtin_amdgcn_readfirstlane(v) * kNodeRecBytes;
+  w = __builtin_amdgcn_raw_buffer_load_b32(rs, (threadIdx.x & 63u) * 4u, so, 0);
+}
+__device__ __forceinline__ void load_rec_f(RecF& f, __amdgpu_buffer_rsrc_t rs, int v) {
   const int so = __builtin_amdgcn_readfirstlane(v) * kNodeRecBytes;
   const auto mc = __builtin_amdgcn_raw_buffer_load_b128(rs, 0, so + (int)offsetof(NodeRec, mc), 0);
   const auto dm = __builtin_amdgcn_raw_buffer_load_b128(rs, 0, so + (int)offsetof(NodeRec, dm01), 0);
-  r.mc = make_uint4(mc[0], mc[1], mc[2], mc[3]);
-  r.dm = make_uint4(dm[0], dm[1], dm[2], dm[3]);
-  r.w = __builtin_amdgcn_raw_buffer_load_b32(rs, (threadIdx.x & 63u) * 4u, so, 0);
+  f.mc = make_uint4(mc[0], mc[1], mc[2], mc[3]);
+  f.dm = make_uint4(dm[0], dm[1], dm[2], dm[3]);
 }
 
 struct EvalArgs {
@@ -590,24 +601,27 @@ struct Scan {
 
 // LDS words one node reads: the R word of v's user beyond the window, and
 // per dependency slot the R word of its user beyond the window and its
-// S_{t+1} word. Unused slots reference the "none" bit (node n).
+// S_{t+1} word, for the first kSlots slots (the others, if any, are read when
+// the node is evaluated). Unused slots reference the "none" bit (node n).
+template <int kSlots>
 struct LdsVals {
   uint32_t fu;
-  uint32_t fl[kRecDeps];
-  uint32_t s1[kRecDeps];
+  uint32_t fl[kSlots];
+  uint32_t s1[kSlots];
 };
 
 // Keeps a group of scalar values together: all of them are computed before
 // any use that follows (the v_readlane results then need no wait states).
 __device__ __forceinline__ void pin_s(uint32_t a, uint32_t b, uint32_t c) { asm volatile("" ::"s"(a), "s"(b), "s"(c)); }
 
-// Issues the reads for the node whose record is `rec`. They are issued one
-// node ahead of their use: the words they read are final by then (a user
-// more than 32 nodes above the node lies in a chunk above the current one,
-// already finished; S_{t+1} is not written during the stage).
-template <typename RowB>
-__device__ __forceinline__ void issue_reads(const RecRegs& rec, Row A, RowB& B, LdsVals& L) {
-  const uint32_t r0 = rec.refs0(), r1 = rec.refs1();
+// Issues the LDS and register-row reads of the node whose record dword
+// (this lane's) is w. They are issued one node ahead of their use: the words
+// they read are final by then (a user more than 32 nodes above the node lies
+// in a chunk above the current one, already finished; S_{t+1} is not written
+// during the stage).
+template <int kSlots, typename RowB>
+__device__ __forceinline__ void issue_reads(uint32_t w, Row A, RowB& B, LdsVals<kSlots>& L) {
+  const uint32_t r0 = __builtin_amdgcn_readlane(w, kDwRefs0), r1 = __builtin_amdgcn_readlane(w, kDwRefs1);
   const uint32_t fu = word_at(r0, 0), fl0 = word_at(r0, 1), s10 = word_at(r0, 2);
   const uint32_t fl1 = word_at(r0, 3), s11 = word_at(r1, 0);
   pin_s(fu, fl0, s10);
@@ -618,15 +632,15 @@ __device__ __forceinline__ void issue_reads(const RecRegs& rec, Row A, RowB& B, 
   L.fl[1] = A.at_word(fl1);
   L.s1[1] = B.at_word(s11);
   // slots 2 and 3 only for the few nodes that use them
-  if (__builtin_expect(((r1 >> 8) & 7u) > 2u, 0)) {
-    const uint32_t r2 = rec.refs2();
+  if (kSlots == 4 && __builtin_expect(((r1 >> 8) & 7u) > 2u, 0)) {
+    const uint32_t r2 = __builtin_amdgcn_readlane(w, kDwRefs2);
     const uint32_t fl2 = word_at(r2, 0), s12 = word_at(r2, 1), fl3 = word_at(r2, 2), s13 = word_at(r2, 3);
     pin_s(fl2, s12, fl3);
     pin_s(s13, s13, s13);
-    L.fl[2] = A.at_word(fl2);
-    L.s1[2] = B.at_word(s12);
-    L.fl[3] = A.at_word(fl3);
-    L.s1[3] = B.at_word(s13);
+    L.fl[kSlots - 2] = A.at_word(fl2);
+    L.s1[kSlots - 2] = B.at_word(s12);
+    L.fl[kSlots - 1] = A.at_word(fl3);
+    L.s1[kSlots - 1] = B.at_word(s13);
   }
 }
 
@@ -651,8 +665,8 @@ __device__ __forceinline__ double max_f64(double a, double b) {
 // S_{t+1}. Rows are zero beyond their last word, so a reference to a node
 // above t (or to node n, "none") reads 0. kFirst: v == t, which is always
 // computed and has no computed user in the stage.
-template <bool kFirst, typename RowB>
-__device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const RecRegs& rec, const LdsVals& L,
+template <bool kFirst, int kSlots, typename RowB>
+__device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const RecRegs& rec, const LdsVals<kSlots>& L,
                                           Scan& sc, Row A, RowB& B) {
   const int jj = v & 31;
   const uint32_t s0 = bit(sc.w0, jj);
@@ -686,29 +700,40 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
     // other than t is computed only because it is kept (s1) or used (anyU),
     // so only node t can be freed right after it is computed.
     if (kFirst) val = fma((double)(~s1 & 1u), Mv, val);
-    auto slot = [&](int sl) {
+    auto slot = [&](int sl, uint32_t flw, uint32_t s1w) {
       const uint32_t lm = rec.lm(sl);
       double dMs;
       if (sl < 2) {
         dMs = rec.dM01(sl);
       } else {
-        const uint32_t d_lo = rec.get(14 + 2 * sl), d_hi = rec.get(15 + 2 * sl);
+        const uint32_t d_lo = rec.get(kDwDM + 2 * sl), d_hi = rec.get(kDwDM + 1 + 2 * sl);
         pin_s(d_lo, d_hi, d_hi);
         dMs = dbl(d_lo, d_hi);
       }
-      const uint32_t far = __builtin_amdgcn_ubfe(L.fl[sl], bitpos(b0, r1, 2 + 2 * sl), 1);
+      const uint32_t far = __builtin_amdgcn_ubfe(flw, bitpos(b0, r1, 2 + 2 * sl), 1);
       uint32_t later = and_or(sc.Rwin, lm, far);
       later = umin1(later);
       // r and later are 0 or 1: no mask needed
-      const uint32_t fr = r & ~__builtin_amdgcn_ubfe(L.s1[sl], bitpos(b0, r1, 1 + 2 * sl), 1) & ~later;
+      const uint32_t fr = r & ~__builtin_amdgcn_ubfe(s1w, bitpos(b0, r1, 1 + 2 * sl), 1) & ~later;
       val = fma((double)fr, dMs, val);
     };
     // most nodes have one or two dependencies
-    if (__builtin_expect(nd >= 1, 1)) slot(0);
-    if (__builtin_expect(nd >= 2, 1)) slot(1);
+    if (__builtin_expect(nd >= 1, 1)) slot(0, L.fl[0], L.s1[0]);
+    if (__builtin_expect(nd >= 2, 1)) slot(1, L.fl[1], L.s1[1]);
     if (__builtin_expect(nd >= 3, 0)) {
-      slot(2);
-      if (nd >= 4) slot(3);
+      if (kSlots == 4) {
+        slot(2, L.fl[kSlots - 2], L.s1[kSlots - 2]);
+        if (nd >= 4) slot(3, L.fl[kSlots - 1], L.s1[kSlots - 1]);
+      } else {
+        // slots 2 and 3 (few nodes here): their words are read now, not pipelined
+        const uint32_t r2 = rec.refs2();
+        const uint32_t fl2 = A.at_word(word_at(r2, 0)), s12 = B.at_word(word_at(r2, 1));
+        slot(2, fl2, s12);
+        if (nd >= 4) {
+          const uint32_t fl3 = A.at_word(word_at(r2, 2)), s13 = B.at_word(word_at(r2, 3));
+          slot(3, fl3, s13);
+        }
+      }
     }
   } else {
     // nodes outside the record format: walk the CSR lists
@@ -761,23 +786,44 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rec_rsrc(const EvalArgs& a) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(a.recs), 0, a.n * kNodeRecBytes, kBufWord3);
 }
 
-// Waits for every load of a record buffer.
-__device__ __forceinline__ void settle(const RecRegs& r) {
-  asm volatile("" ::"v"(r.w), "v"(r.mc.x), "v"(r.mc.y), "v"(r.mc.z), "v"(r.mc.w), "v"(r.dm.x), "v"(r.dm.y),
-               "v"(r.dm.z), "v"(r.dm.w));
+__device__ __forceinline__ void settle_w(uint32_t w) { asm volatile("" ::"v"(w)); }
+__device__ __forceinline__ void settle_f(const RecF& f) {
+  asm volatile("" ::"v"(f.mc.x), "v"(f.mc.y), "v"(f.mc.z), "v"(f.mc.w), "v"(f.dm.x), "v"(f.dm.y), "v"(f.dm.z),
+               "v"(f.dm.w));
 }
 
-// One node of the scan, software-pipelined: the record of node v - 2 is
-// requested, the LDS words of node v - 1 are requested, then node v is
-// evaluated with the record and words requested one and two nodes earlier.
-// Record buffers rotate through (C, N, NN) so registers never move.
-template <int C, int N, int NN, bool kFirst, typename RowB>
-__device__ __forceinline__ void pipe_step(const EvalArgs& a, int t, int v, RecRegs (&rb)[3], LdsVals (&lb)[3],
-                                          Scan& sc, Row A, RowB& B) {
-  load_rec(rb[NN], rec_rsrc(a), max(v - 2, 0));
-  issue_reads(rb[N], A, B, lb[N]);
+// Pipeline shape per row storage: with S_{t+1} in 32 registers (n < 1024)
+// the kernel runs 5 waves per SIMD if it stays within 96 VGPRs, so the fp64
+// record group comes one node ahead (two buffers) and only dependency slots
+// 0-1 are pipelined; the wider variants run 1-2 waves per SIMD, where
+// latency matters more than registers: the fp64 group two nodes ahead (four
+// buffers) and all four slots pipelined.
+template <typename RowB> struct PipeShape { static constexpr int kFAhead = 2, kSlots = 4; };
+template <> struct PipeShape<RowReg> { static constexpr int kFAhead = 1, kSlots = 2; };
+
+// One node of the scan, software-pipelined: the record dword of node v - 2
+// and the fp64 record group of node v - kFAhead are requested, the LDS words
+// of node v - 1 are requested, then node v is evaluated. Record dwords and
+// fp64 groups rotate through four buffers (two for the groups one node
+// ahead), LDS words through two, so registers never move within a turn of
+// the 4-node unrolled loop.
+template <int CW, bool kFirst, typename RowB>
+__device__ __forceinline__ void pipe_step(const EvalArgs& a, int t, int v, uint32_t (&rw)[4], RecF (&rf)[4],
+                                          LdsVals<PipeShape<RowB>::kSlots> (&lb)[2], Scan& sc, Row A, RowB& B) {
+  constexpr int kFA = PipeShape<RowB>::kFAhead;
+  constexpr int NW = (CW + 1) & 3, FW = (CW + 2) & 3;
+  constexpr int CF = kFA == 1 ? (CW & 1) : CW;
+  constexpr int LF = kFA == 1 ? (CF ^ 1) : ((CW + 2) & 3);
+  constexpr int LC = CW & 1, LN = LC ^ 1;
+  load_rec_w(rw[FW], rec_rsrc(a), max(v - 2, 0));
+  load_rec_f(rf[LF], rec_rsrc(a), max(v - kFA, 0));
+  issue_reads(rw[NW], A, B, lb[LN]);
   asm volatile("" ::: "memory");  // keep the requests ahead of this node's work
-  scan_node<kFirst, RowB>(a, t, v, rb[C], lb[C], sc, A, B);
+  RecRegs rec;
+  rec.w = rw[CW];
+  rec.mc = rf[CF].mc;
+  rec.dm = rf[CF].dm;
+  scan_node<kFirst>(a, t, v, rec, lb[LC], sc, A, B);
 }
 
 // One stage t of one candidate (per lane): S_t in A, S_{t+1} in B on entry,
@@ -785,6 +831,7 @@ __device__ __forceinline__ void pipe_step(const EvalArgs& a, int t, int v, RecRe
 template <typename RowB>
 __device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, RowB& B, double& stage_peak,
                                            double& stage_cost) {
+  constexpr int kFA = PipeShape<RowB>::kFAhead;
   Scan sc;
   sc.U0 = a.base;
   sc.Y = 0.0;
@@ -793,30 +840,37 @@ __device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, RowB
   sc.Rwin = 0;
   sc.w0 = A.word(t >> 5);
   sc.w1 = B.word(t >> 5);
-  RecRegs rb[3];
-  LdsVals lb[3];
-  load_rec(rb[0], rec_rsrc(a), t);
-  load_rec(rb[1], rec_rsrc(a), max(t - 1, 0));
-  issue_reads(rb[0], A, B, lb[0]);
+  uint32_t rw[4];
+  RecF rf[4];
+  LdsVals<PipeShape<RowB>::kSlots> lb[2];
+  load_rec_w(rw[0], rec_rsrc(a), t);
+  load_rec_w(rw[1], rec_rsrc(a), max(t - 1, 0));
+  load_rec_f(rf[0], rec_rsrc(a), t);
+  if (kFA == 2) load_rec_f(rf[1], rec_rsrc(a), max(t - 1, 0));
+  issue_reads(rw[0], A, B, lb[0]);
   int v = t;
-  pipe_step<0, 1, 2, true>(a, t, v, rb, lb, sc, A, B);
-  // node t leaves part of its record unread; retire those loads here, once
-  // per stage, so the loop never waits for loads older than two nodes
-  settle(rb[0]);
-  // nodes t-1 .. 0 in groups of three (one turn of the buffer rotation),
-  // then the remainder
-  const int groups = __builtin_amdgcn_readfirstlane(t / 3);
+  pipe_step<0, true>(a, t, v, rw, rf, lb, sc, A, B);
+  const int groups = __builtin_amdgcn_readfirstlane(t / 4);
   for (int g = 0; g < groups; ++g) {
-    pipe_step<1, 2, 0, false>(a, t, --v, rb, lb, sc, A, B);
-    pipe_step<2, 0, 1, false>(a, t, --v, rb, lb, sc, A, B);
-    pipe_step<0, 1, 2, false>(a, t, --v, rb, lb, sc, A, B);
+    pipe_step<1, false>(a, t, --v, rw, rf, lb, sc, A, B);
+    pipe_step<2, false>(a, t, --v, rw, rf, lb, sc, A, B);
+    pipe_step<3, false>(a, t, --v, rw, rf, lb, sc, A, B);
+    pipe_step<0, false>(a, t, --v, rw, rf, lb, sc, A, B);
   }
-  if (v >= 1) pipe_step<1, 2, 0, false>(a, t, --v, rb, lb, sc, A, B);
-  if (v >= 1) pipe_step<2, 0, 1, false>(a, t, --v, rb, lb, sc, A, B);
+  if (v >= 1) pipe_step<1, false>(a, t, --v, rw, rf, lb, sc, A, B);
+  if (v >= 1) pipe_step<2, false>(a, t, --v, rw, rf, lb, sc, A, B);
+  if (v >= 1) pipe_step<3, false>(a, t, --v, rw, rf, lb, sc, A, B);
   // prefetches past node 0 are never read: retire them inside the stage
-  settle(rb[0]);
-  settle(rb[1]);
-  settle(rb[2]);
+  settle_w(rw[0]);
+  settle_w(rw[1]);
+  settle_w(rw[2]);
+  settle_w(rw[3]);
+  settle_f(rf[0]);
+  settle_f(rf[1]);
+  if (kFA == 2) {
+    settle_f(rf[2]);
+    settle_f(rf[3]);
+  }
   stage_peak = sc.U0 - sc.Y + sc.maxv;
   stage_cost = sc.cost;
 }
@@ -1314,18 +1368,18 @@ __device__ __forceinline__ uint32_t rl(uint32_t w, int i) { return __builtin_amd
 __device__ __forceinline__ void closure_chunk(const ClosureArgs& a, int c, int t, int tmax, const uint32_t (&rec)[kChunk],
                                               Row A, Row S0, Row S1, uint32_t& Rwin) {
   const uint32_t w0 = S0.word(c), w1 = S1.word(c);
-  uint32_t far_next = A.at_word(word_at(rl(rec[kChunk - 1], 5), 0));
+  uint32_t far_next = A.at_word(word_at(rl(rec[kChunk - 1], kDwRefs0), 0));
 #pragma unroll
   for (int jj = kChunk - 1; jj >= 0; --jj) {
     const int v = kChunk * c + jj;
     const uint32_t far_w = far_next;
-    if (jj > 0) far_next = A.at_word(word_at(rl(rec[jj - 1], 5), 0));
+    if (jj > 0) far_next = A.at_word(word_at(rl(rec[jj - 1], kDwRefs0), 0));
     uint32_t r = 0;
     if (v <= tmax) {
-      const uint32_t um = rl(rec[jj], 4), b0 = rl(rec[jj], 7);
+      const uint32_t um = rl(rec[jj], kDwUmask), b0 = rl(rec[jj], kDwBits0);
       pin_s(um, b0, b0);
       bool slow = false;
-      if (__builtin_expect((b0 >> 30) == 3u, 0)) slow = (rl(rec[jj], 6) & kRefsSlow) != 0u;
+      if (__builtin_expect((b0 >> 30) == 3u, 0)) slow = (rl(rec[jj], kDwRefs1) & kRefsSlow) != 0u;
       uint32_t anyU;
       if (__builtin_expect(!slow, 1)) {
         anyU = umin1(and_or(Rwin, um, __builtin_amdgcn_ubfe(far_w, b0, 1)));
