@@ -252,6 +252,39 @@ def test_max_nodes_chain():
     check_rows(w, got, got["best_k"])
 
 
+@pytest.mark.parametrize("n", [337, 1500, 2047])
+def test_in_kernel_rows_without_row_arrays(n):
+    """The rounding path on a work buffer without the row arrays: rows
+    rounded in the evaluate kernel (register rows of 32 and 64 words) and the
+    best R recomputed by Algorithm 2 in the closure kernel. Every output
+    equals the row-array path's, whose results the oracle checks; the best
+    candidate's rows are checked against the oracle here too."""
+    import torch
+    w = wl.config(3) if n == 337 else wl.random_dag(n, seed=n + 1, K=200, window=40, max_deg=3, max_size=1000,
+                                                    max_cost=1000, s_kind="uniform", budget_pct=55.0)
+    g = ckm.Graph.from_workload(w)
+    try:
+        K = w.K if n == 337 else 200
+        full = g.round_eval(w.s_frac, K, w.seed, 2 ** 62)
+        budget = int(np.median(full["peak"]))
+        want = g.round_eval(w.s_frac, K, w.seed, budget)
+        small = g.alloc_work(K, rows=False)
+        assert small.numel() < g.workspace_size(K)
+        out = g.alloc_outputs(K)
+        log("n=%d K=%d in-kernel rows" % (n, K))
+        g.round_eval_async(torch.from_numpy(w.s_frac).cuda(), K, w.seed, budget, 0, out, small)
+        torch.cuda.synchronize()
+        assert int(out["status"].item()) == ckm.OK
+        for key in ("peak", "cost", "feasible"):
+            assert np.array_equal(out[key].cpu().numpy(), want[key]), key
+        assert int(out["best_k"].item()) == want["best_k"] >= 0
+        assert np.array_equal(ckm.rows_to_numpy(out["best_S"]), want["best_S"])
+        assert np.array_equal(ckm.rows_to_numpy(out["best_R"]), want["best_R"])
+    finally:
+        g.close()
+    check_rows(w.replace(K=K), want, want["best_k"])
+
+
 def test_async_stages_and_split_invariance():
     """The staged async calls give the same bits for any stage split (a race
     or a split-boundary error would change them)."""
