@@ -82,7 +82,14 @@ enum {
  *   cost, bytes        int64 [n], >= 0
  *   m_input, m_param   M_in and M_param of eq. U_init, >= 0
  *   out                receives the handle
- * All arrays are host arrays, copied; the caller keeps ownership. */
+ * All arrays are host arrays, copied; the caller keeps ownership.
+ * Errors: CKM_E_GRAPH for a malformed CSR (dep_ptr[0] != 0, dep_ptr
+ * decreasing, more than n(n-1)/2 edges), an edge i -> j with i < 0 or
+ * i >= j, a duplicate edge, or Users that differ from the transpose of Deps;
+ * CKM_E_OVERFLOW when M_in + 2 M_param + sum(M) or sum(C) reaches 2^53, or
+ * n * sum(C) exceeds INT64_MAX; CKM_E_INVALID_ARG for NULL arrays or negative
+ * sizes and costs; CKM_E_NOMEM, CKM_E_DEVICE when allocation or upload
+ * fails. On error *out is NULL. */
 ckm_status ckm_graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
                             const int32_t* user_ptr, const int32_t* user_idx,
                             const int64_t* cost, const int64_t* bytes, int64_t m_input,

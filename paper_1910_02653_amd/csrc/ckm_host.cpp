@@ -217,10 +217,6 @@ int32_t max_splits_for(int32_t n, int32_t /*K*/) {
   return std::max<int32_t>(n, 1);
 }
 
-// Resident evaluate waves on the device: 256 CUs times the waves per CU.
-// With n < 1024 one row is in registers and the register file allows 16
-// waves per CU; otherwise the two LDS rows of a wave set the count.
-
 Plan plan_splits(int32_t n, int32_t splits) {
   Plan p;
   p.kind = 0;
@@ -312,12 +308,27 @@ const char* ckm_last_error(void) { return g_last_error.c_str(); }
 
 int32_t ckm_graph_num_nodes(const ckm_graph* g) { return g ? g->n : -1; }
 
+static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
+                               const int32_t* user_ptr, const int32_t* user_idx, const int64_t* cost,
+                               const int64_t* bytes, int64_t m_input, int64_t m_param, ckm_graph** out);
+
 ckm_status ckm_graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
                             const int32_t* user_ptr, const int32_t* user_idx,
                             const int64_t* cost, const int64_t* bytes, int64_t m_input,
                             int64_t m_param, ckm_graph** out) {
   if (!out) return fail(CKM_E_INVALID_ARG, "out is NULL");
   *out = nullptr;
+  // the host-side vectors are the only allocations here that throw
+  try {
+    return graph_create(n, dep_ptr, dep_idx, user_ptr, user_idx, cost, bytes, m_input, m_param, out);
+  } catch (const std::bad_alloc&) {
+    return fail(CKM_E_NOMEM, "out of host memory");
+  }
+}
+
+static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
+                               const int32_t* user_ptr, const int32_t* user_idx, const int64_t* cost,
+                               const int64_t* bytes, int64_t m_input, int64_t m_param, ckm_graph** out) {
   if (n < 1) return fail(CKM_E_INVALID_ARG, "n = %d < 1", n);
   if (n > CKM_MAX_NODES) return fail(CKM_E_UNSUPPORTED, "n = %d > %d", n, CKM_MAX_NODES);
   if (!dep_ptr || !cost || !bytes) return fail(CKM_E_INVALID_ARG, "NULL dep_ptr, cost or bytes");
@@ -327,6 +338,9 @@ ckm_status ckm_graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* de
   for (int32_t j = 0; j < n; ++j)
     if (dep_ptr[j + 1] < dep_ptr[j]) return fail(CKM_E_GRAPH, "dep_ptr decreases at %d", j);
   const int32_t E = dep_ptr[n];
+  // edges i -> j with i < j, no two alike: at most n (n - 1) / 2 of them
+  if ((int64_t)E > (int64_t)n * (n - 1) / 2)
+    return fail(CKM_E_GRAPH, "%d edges on %d nodes: some edge repeats or is not in topological order", E, n);
   if (E > 0 && !dep_idx) return fail(CKM_E_INVALID_ARG, "dep_idx is NULL with %d edges", E);
   if (m_input < 0 || m_param < 0) return fail(CKM_E_INVALID_ARG, "negative m_input or m_param");
 
@@ -397,17 +411,6 @@ ckm_status ckm_graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* de
       upos[a] = (int32_t)(std::upper_bound(b, e, j) - ui.data());
     }
 
-  ckm_graph* g = new (std::nothrow) ckm_graph();
-  if (!g) return fail(CKM_E_NOMEM, "host allocation failed");
-  g->n = n;
-  g->num_edges = E;
-  g->base = (double)(m_input + 2 * m_param);
-  hipError_t e = hipGetDevice(&g->device);
-  if (e != hipSuccess) {
-    delete g;
-    return fail_hip(e, "hipGetDevice");
-  }
-  g->eval_waves = ckm::eval_waves_per_cu(n);
   const size_t Ea = (size_t)std::max(E, 1);
   const size_t off_M = 0;
   const size_t off_C = align256(off_M + n * sizeof(double));
@@ -433,6 +436,18 @@ ckm_status ckm_graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* de
   if (E) memcpy(host.data() + off_uo, upos.data(), E * sizeof(int32_t));
   ckm::build_node_records(n, Md.data(), Cd.data(), dp.data(), di.data(), up.data(), ui.data(),
                           host.data() + off_rec);
+
+  ckm_graph* g = new (std::nothrow) ckm_graph();
+  if (!g) return fail(CKM_E_NOMEM, "host allocation failed");
+  g->n = n;
+  g->num_edges = E;
+  g->base = (double)(m_input + 2 * m_param);
+  hipError_t e = hipGetDevice(&g->device);
+  if (e != hipSuccess) {
+    delete g;
+    return fail_hip(e, "hipGetDevice");
+  }
+  g->eval_waves = ckm::eval_waves_per_cu(n);
   e = hipMalloc(&g->d_mem, total);
   if (e != hipSuccess) {
     delete g;
@@ -514,6 +529,7 @@ ckm_status ckm_quantize_async(const ckm_graph* g, const double* d_s_frac, int64_
   if (!d_s_frac) return fail(CKM_E_INVALID_ARG, "S* is NULL");
   if (ld < g->n) return fail(CKM_E_INVALID_ARG, "ld = %lld < n = %d", (long long)ld, g->n);
   DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
   hipError_t e = ckm::launch_quantize(*g, L, d_s_frac, ld, static_cast<char*>(d_work),
                                       static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CKM_OK : fail_hip(e, "quantize launch");
@@ -526,6 +542,7 @@ ckm_status ckm_round_async(const ckm_graph* g, int32_t K, uint64_t seed, uint32_
   if (st != CKM_OK) return st;
   if (flags & ~(uint32_t)CKM_F_DET0) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
   DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
   hipError_t e = ckm::launch_round_rows(*g, L, K, seed, flags, static_cast<char*>(d_work),
                                         static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CKM_OK : fail_hip(e, "round launch");
@@ -542,6 +559,7 @@ ckm_status ckm_evaluate_async(const ckm_graph* g, int32_t K, uint64_t seed, uint
   const ckm::Plan plan = stage_splits ? ckm::plan_splits(g->n, std::min(stage_splits, L.max_splits))
                                       : ckm::plan_auto(g->n, K, L.max_splits, g->eval_waves);
   DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
   hipError_t e = ckm::launch_evaluate(*g, L, K, seed, flags, plan, ckm::kSrcRound, nullptr,
                                       static_cast<char*>(d_work), static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CKM_OK : fail_hip(e, "evaluate launch");
@@ -560,6 +578,7 @@ ckm_status ckm_select_async(const ckm_graph* g, int32_t K, uint64_t seed, int64_
   if (!d_peak || !d_cost || !d_feasible || !d_best_k)
     return fail(CKM_E_INVALID_ARG, "NULL peak, cost, feasible or best_k");
   DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
   hipError_t e = ckm::launch_select(*g, L, K, seed, budget, flags, d_peak, d_cost, d_feasible,
                                     d_best_k, d_best_S, d_best_R, d_status, ckm::kSrcRound, nullptr,
                                     static_cast<char*>(d_work), static_cast<hipStream_t>(stream));
@@ -599,6 +618,7 @@ ckm_status ckm_eval_schedules_async(const ckm_graph* g, const uint64_t* d_S, int
     return fail(CKM_E_INVALID_ARG, "NULL peak, cost, feasible or best_k");
   const ckm::Plan plan = ckm::plan_auto(g->n, K, L.max_splits, g->eval_waves);
   DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
   hipError_t e = ckm::launch_evaluate(*g, L, K, 0, 0, plan, ckm::kSrcUser, d_S, static_cast<char*>(d_work),
                                       static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail_hip(e, "evaluate launch");
@@ -666,6 +686,7 @@ ckm_status ckm_threshold_eval_async(const ckm_graph* g, const double* d_s_frac, 
     return fail(CKM_E_INVALID_ARG, "NULL peak, cost, feasible or best_k");
   const ckm::Plan plan = ckm::plan_auto(g->n, K, L.max_splits, g->eval_waves);
   DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* work = static_cast<char*>(d_work);
   hipError_t e = ckm::launch_threshold_keys(*g, L, d_s_frac, ld, d_p, K, work, s);
@@ -743,6 +764,7 @@ ckm_status ckm_plan_async(const ckm_graph* g, const uint64_t* d_S, const uint64_
   if (flags & ~(uint32_t)CKM_PLAN_EARLY_FREE) return fail(CKM_E_INVALID_ARG, "unknown flags 0x%x", flags);
   if (capacity < 0) return fail(CKM_E_INVALID_ARG, "capacity = %lld < 0", (long long)capacity);
   DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
   hipError_t e = ckm::launch_plan(*g, L, d_S, d_R, flags, reinterpret_cast<int32_t*>(d_P), capacity, d_count,
                                   d_P ? d_mem : nullptr, d_status, static_cast<char*>(d_work),
                                   static_cast<hipStream_t>(stream));
@@ -818,6 +840,7 @@ ckm_status ckm_max_batch_async(const ckm_graph* g, int32_t K, int64_t budget, in
   if (cost_cap < 0) return fail(CKM_E_INVALID_ARG, "cost_cap = %lld < 0", (long long)cost_cap);
   if (!d_batch || !d_best_k) return fail(CKM_E_INVALID_ARG, "NULL batch or best_k");
   DeviceGuard dg(g->device);
+  if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
   hipError_t e = ckm::launch_max_batch(*g, L, K, budget, cost_cap, d_batch, d_best_k, d_best_batch, d_status,
                                        static_cast<char*>(d_work), static_cast<hipStream_t>(stream));
   return e == hipSuccess ? CKM_OK : fail_hip(e, "max batch launch");

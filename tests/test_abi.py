@@ -83,6 +83,21 @@ def test_graph_validation_errors(case, status):
     assert ckm.last_error()
 
 
+def test_edge_count_checked_before_the_edges_are_read():
+    """dep_ptr[n] above n(n-1)/2 is rejected before dep_idx (one entry here)
+    is read or anything is sized by it."""
+    n = 3
+    ptr = np.array([0, 0, 0, 2 ** 31 - 1], np.int32)
+    idx = np.zeros(1, np.int32)
+    ones = np.ones(n, np.int64)
+    h = C.c_void_p()
+    st = ckm.lib().ckm_graph_create(n, ptr.ctypes.data_as(C.c_void_p), idx.ctypes.data_as(C.c_void_p), None, None,
+                                    ones.ctypes.data_as(C.c_void_p), ones.ctypes.data_as(C.c_void_p), 0, 0,
+                                    C.byref(h))
+    assert st == ckm.E_GRAPH and not h.value
+    assert "edges" in ckm.last_error()
+
+
 def test_null_arguments_rejected():
     L = ckm.lib()
     h = C.c_void_p()
