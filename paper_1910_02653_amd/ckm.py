@@ -113,8 +113,50 @@ def _np_ptr(a):
     return None if a is None else a.ctypes.data_as(C.c_void_p)
 
 
-def _dev_ptr(t):
-    return None if t is None else C.c_void_p(t.data_ptr())
+
+def _host_s(s_frac, n: int) -> np.ndarray:
+    """S* as a C-contiguous float64 array with at least n rows and n columns
+    (the library reads n rows of stride shape[1])."""
+    s = np.ascontiguousarray(s_frac, dtype=np.float64)
+    if s.ndim != 2 or s.shape[0] < n or s.shape[1] < n:
+        raise ValueError("S* must be a 2-D array of at least [%d][%d], got shape %s" % (n, n, s.shape))
+    return s
+
+
+def _dev(t, name: str, dtype, numel: int = 0):
+    """Pointer of a contiguous device tensor of the given dtype holding at
+    least numel elements (the library cannot check sizes behind a pointer)."""
+    if t is None:
+        return None
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if t.dtype != dtype:
+        raise ValueError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if t.numel() < numel:
+        raise ValueError("%s holds %d elements, %d needed" % (name, t.numel(), numel))
+    return C.c_void_p(t.data_ptr())
+
+
+def _dev_s(t, n: int):
+    """(pointer, row stride) of a float64 device S* with at least n x n
+    entries and unit column stride."""
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.float64 or t.dim() != 2:
+        raise ValueError("S* must be a 2-D float64 device tensor")
+    if t.shape[0] < n or t.shape[1] < n or (n > 1 and t.stride(1) != 1) or t.stride(0) < n:
+        raise ValueError("S* must hold at least [%d][%d] entries in rows of unit column stride, got shape %s, "
+                         "strides %s" % (n, n, tuple(t.shape), t.stride()))
+    return C.c_void_p(t.data_ptr()), t.stride(0)
+
+
+def _work(work):
+    import torch
+    if not isinstance(work, torch.Tensor) or not work.is_cuda or not work.is_contiguous():
+        raise ValueError("work must be a contiguous device tensor")
+    return C.c_void_p(work.data_ptr()), work.numel() * work.element_size()
 
 
 def _stream_ptr(stream):
@@ -172,7 +214,7 @@ class Graph:
 
     # -- synchronous, host arrays -----------------------------------------
     def round_eval(self, s_frac, K: int, seed: int, budget: int, flags: int = 0, want_rows: bool = True):
-        s = np.ascontiguousarray(s_frac, dtype=np.float64)
+        s = _host_s(s_frac, self.n)
         peak = np.zeros(K, np.int64)
         cost = np.zeros(K, np.int64)
         feas = np.zeros(K, np.uint8)
@@ -186,7 +228,7 @@ class Graph:
 
     def threshold_eval(self, s_frac, p, budget: int, want_rows: bool = True):
         """One deterministic candidate per threshold p_k (ckm_threshold_eval)."""
-        s = np.ascontiguousarray(s_frac, dtype=np.float64)
+        s = _host_s(s_frac, self.n)
         pk = np.ascontiguousarray(p, dtype=np.float64).reshape(-1)
         K = pk.size
         peak = np.zeros(K, np.int64)
@@ -202,7 +244,7 @@ class Graph:
 
     def max_batch(self, s_frac, K: int, seed: int, budget: int, cost_cap: int, flags: int = 0):
         """Largest batch multiplier of each rounded candidate (ckm_max_batch)."""
-        s = np.ascontiguousarray(s_frac, dtype=np.float64)
+        s = _host_s(s_frac, self.n)
         batch = np.zeros(K, np.int64)
         bk = np.zeros(1, np.int32)
         bb = np.zeros(1, np.int64)
@@ -211,9 +253,12 @@ class Graph:
         return dict(batch=batch, best_k=int(bk[0]), best_batch=int(bb[0]))
 
     def max_batch_async(self, K, budget, cost_cap, d_batch, d_best_k, d_best_batch, d_status, work, stream=None):
-        _check(lib().ckm_max_batch_async(self._h, int(K), int(budget), int(cost_cap), _dev_ptr(d_batch),
-                                         _dev_ptr(d_best_k), _dev_ptr(d_best_batch), _dev_ptr(d_status),
-                                         _dev_ptr(work), work.numel() * work.element_size(), _stream_ptr(stream)))
+        import torch
+        wp, wb = _work(work)
+        _check(lib().ckm_max_batch_async(self._h, int(K), int(budget), int(cost_cap),
+                                         _dev(d_batch, "batch", torch.int64, K), _dev(d_best_k, "best_k", torch.int32, 1),
+                                         _dev(d_best_batch, "best_batch", torch.int64, 1),
+                                         _dev(d_status, "status", torch.int32, 1), wp, wb, _stream_ptr(stream)))
 
     def plan(self, S_rows, R_rows, early: bool = False, capacity=None, want_mem: bool = True):
         """Algorithm 1's execution plan of (S, R) bit rows (ckm_plan): statements
@@ -237,10 +282,15 @@ class Graph:
 
     def plan_async(self, d_S, d_R, early, d_P, capacity, d_count, d_mem, d_status, work, stream=None):
         """Device tensors: d_S, d_R int64 [n][W]; d_P int32 [capacity][4] or None."""
-        _check(lib().ckm_plan_async(self._h, _dev_ptr(d_S), _dev_ptr(d_R), PLAN_EARLY_FREE if early else 0,
-                                    _dev_ptr(d_P), int(capacity), _dev_ptr(d_count), _dev_ptr(d_mem),
-                                    _dev_ptr(d_status), _dev_ptr(work), work.numel() * work.element_size(),
-                                    _stream_ptr(stream)))
+        import torch
+        rows = self.n * self.W
+        cap = int(capacity) if d_P is not None else 0
+        wp, wb = _work(work)
+        _check(lib().ckm_plan_async(self._h, _dev(d_S, "S", torch.int64, rows), _dev(d_R, "R", torch.int64, rows),
+                                    PLAN_EARLY_FREE if early else 0, _dev(d_P, "P", torch.int32, 4 * cap),
+                                    int(capacity), _dev(d_count, "count", torch.int64, 1),
+                                    _dev(d_mem, "mem", torch.int64, cap), _dev(d_status, "status", torch.int32, 1),
+                                    wp, wb, _stream_ptr(stream)))
 
     def eval_schedules(self, S_rows, budget: int, want_rows: bool = True):
         """K given checkpoint matrices as uint64 bit rows [K][n][W] (ckm_eval_schedules)."""
@@ -258,50 +308,61 @@ class Graph:
         return dict(peak=peak, cost=cost, feasible=feas, best_k=int(bk[0]), best_R=bR)
 
     # -- asynchronous, torch device tensors ---------------------------------
+    def _out(self, out: dict, K: int):
+        """Pointers of the result tensors (see alloc_outputs) for K candidates."""
+        import torch
+        rows = self.n * self.W
+        return (_dev(out["peak"], "peak", torch.int64, K), _dev(out["cost"], "cost", torch.int64, K),
+                _dev(out["feasible"], "feasible", torch.uint8, K), _dev(out["best_k"], "best_k", torch.int32, 1),
+                _dev(out.get("best_S"), "best_S", torch.int64, rows), _dev(out.get("best_R"), "best_R", torch.int64, rows),
+                _dev(out.get("status"), "status", torch.int32, 1))
+
     def quantize_async(self, d_s_frac, work, stream=None):
-        _check(lib().ckm_quantize_async(self._h, _dev_ptr(d_s_frac), d_s_frac.stride(0), _dev_ptr(work),
-                                        work.numel() * work.element_size(), _stream_ptr(stream)))
+        sp, ld = _dev_s(d_s_frac, self.n)
+        wp, wb = _work(work)
+        _check(lib().ckm_quantize_async(self._h, sp, ld, wp, wb, _stream_ptr(stream)))
 
     def round_async(self, K, seed, flags, work, stream=None):
-        _check(lib().ckm_round_async(self._h, int(K), int(seed), int(flags), _dev_ptr(work),
-                                     work.numel() * work.element_size(), _stream_ptr(stream)))
+        wp, wb = _work(work)
+        _check(lib().ckm_round_async(self._h, int(K), int(seed), int(flags), wp, wb, _stream_ptr(stream)))
 
     def evaluate_async(self, K, seed, flags, work, stage_splits: int = 0, stream=None):
-        _check(lib().ckm_evaluate_async(self._h, int(K), int(seed), int(flags), int(stage_splits),
-                                        _dev_ptr(work), work.numel() * work.element_size(), _stream_ptr(stream)))
+        wp, wb = _work(work)
+        _check(lib().ckm_evaluate_async(self._h, int(K), int(seed), int(flags), int(stage_splits), wp, wb,
+                                        _stream_ptr(stream)))
 
     def select_async(self, K, seed, budget, flags, out: dict, work, stream=None):
-        _check(lib().ckm_select_async(self._h, int(K), int(seed), int(budget), int(flags), _dev_ptr(out["peak"]),
-                                      _dev_ptr(out["cost"]), _dev_ptr(out["feasible"]), _dev_ptr(out["best_k"]),
-                                      _dev_ptr(out.get("best_S")), _dev_ptr(out.get("best_R")),
-                                      _dev_ptr(out.get("status")), _dev_ptr(work),
-                                      work.numel() * work.element_size(), _stream_ptr(stream)))
+        peak, cost, feas, bk, bS, bR, st = self._out(out, K)
+        wp, wb = _work(work)
+        _check(lib().ckm_select_async(self._h, int(K), int(seed), int(budget), int(flags), peak, cost, feas, bk,
+                                      bS, bR, st, wp, wb, _stream_ptr(stream)))
 
     def round_eval_async(self, d_s_frac, K, seed, budget, flags, out: dict, work, stream=None):
-        _check(lib().ckm_round_eval_async(self._h, _dev_ptr(d_s_frac), d_s_frac.stride(0), int(K), int(seed),
-                                          int(budget), int(flags), _dev_ptr(out["peak"]), _dev_ptr(out["cost"]),
-                                          _dev_ptr(out["feasible"]), _dev_ptr(out["best_k"]),
-                                          _dev_ptr(out.get("best_S")), _dev_ptr(out.get("best_R")),
-                                          _dev_ptr(out.get("status")), _dev_ptr(work),
-                                          work.numel() * work.element_size(), _stream_ptr(stream)))
+        sp, ld = _dev_s(d_s_frac, self.n)
+        peak, cost, feas, bk, bS, bR, st = self._out(out, K)
+        wp, wb = _work(work)
+        _check(lib().ckm_round_eval_async(self._h, sp, ld, int(K), int(seed), int(budget), int(flags), peak, cost,
+                                          feas, bk, bS, bR, st, wp, wb, _stream_ptr(stream)))
 
     def eval_schedules_async(self, d_S, K, budget, out: dict, work, stream=None):
         """d_S: int64 device tensor holding K x n x W bit-row words."""
-        _check(lib().ckm_eval_schedules_async(self._h, _dev_ptr(d_S), int(K), int(budget), _dev_ptr(out["peak"]),
-                                              _dev_ptr(out["cost"]), _dev_ptr(out["feasible"]),
-                                              _dev_ptr(out["best_k"]), _dev_ptr(out.get("best_R")),
-                                              _dev_ptr(out.get("status")), _dev_ptr(work),
-                                              work.numel() * work.element_size(), _stream_ptr(stream)))
+        import torch
+        peak, cost, feas, bk, _, bR, st = self._out(out, K)
+        wp, wb = _work(work)
+        _check(lib().ckm_eval_schedules_async(self._h, _dev(d_S, "S", torch.int64, int(K) * self.n * self.W),
+                                              int(K), int(budget), peak, cost, feas, bk, bR, st, wp, wb,
+                                              _stream_ptr(stream)))
 
     def threshold_eval_async(self, d_s_frac, d_p, budget, out: dict, work, stream=None):
         """d_p: float64 device tensor of K thresholds."""
-        _check(lib().ckm_threshold_eval_async(self._h, _dev_ptr(d_s_frac), d_s_frac.stride(0), _dev_ptr(d_p),
-                                              int(d_p.numel()), int(budget), _dev_ptr(out["peak"]),
-                                              _dev_ptr(out["cost"]), _dev_ptr(out["feasible"]),
-                                              _dev_ptr(out["best_k"]), _dev_ptr(out.get("best_S")),
-                                              _dev_ptr(out.get("best_R")), _dev_ptr(out.get("status")),
-                                              _dev_ptr(work), work.numel() * work.element_size(),
-                                              _stream_ptr(stream)))
+        import torch
+        sp, ld = _dev_s(d_s_frac, self.n)
+        K = int(d_p.numel())
+        pp = _dev(d_p, "thresholds", torch.float64, K)
+        peak, cost, feas, bk, bS, bR, st = self._out(out, K)
+        wp, wb = _work(work)
+        _check(lib().ckm_threshold_eval_async(self._h, sp, ld, pp, K, int(budget), peak, cost, feas, bk, bS, bR, st,
+                                              wp, wb, _stream_ptr(stream)))
 
     def alloc_outputs(self, K: int, device="cuda", rows: bool = True) -> dict:
         """Device tensors for the async calls (torch: memory only)."""

@@ -126,3 +126,21 @@ def test_null_arguments_rejected():
     assert L.ckm_round_async(None, 4, 0, 0, None, 0, None) == ckm.E_INVALID_ARG
     assert L.ckm_graph_num_nodes(None) == -1
     L.ckm_graph_destroy(None)
+
+
+def test_binding_checks_arrays_before_the_library_reads_them():
+    """The binding passes bare pointers, so it checks shapes, dtypes and
+    devices itself: an S* with fewer than n rows or columns, host tensors
+    where device tensors belong, and short result tensors are refused."""
+    import torch
+    with pytest.raises(ValueError):
+        ckm._host_s(np.zeros((4, 5)), 5)          # 4 rows, n = 5
+    with pytest.raises(ValueError):
+        ckm._host_s(np.zeros(25), 5)              # not 2-D
+    assert ckm._host_s(np.zeros((5, 7), np.float32), 5).dtype == np.float64
+    with pytest.raises(ValueError):
+        ckm._dev_s(torch.zeros((5, 5), dtype=torch.float64), 5)   # host tensor
+    with pytest.raises(ValueError):
+        ckm._dev(torch.zeros(8, dtype=torch.int64), "peak", torch.int64, 8)
+    with pytest.raises(ValueError):
+        ckm._work(torch.zeros(64, dtype=torch.uint8))

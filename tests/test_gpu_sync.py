@@ -112,3 +112,36 @@ def test_concurrent_threads_one_graph():
                     same(r, want[job])
     finally:
         g.close()
+
+
+def test_binding_refuses_wrong_device_tensors():
+    """Wrong dtype, layout or size of a device argument is a ValueError from
+    the binding, raised before any launch."""
+    import torch
+    w = wl.config(2)
+    K = 64
+    g = ckm.Graph.from_workload(w)
+    try:
+        work = g.alloc_work(K)
+        out = g.alloc_outputs(K)
+        d_s = torch.from_numpy(w.s_frac).cuda()
+        with pytest.raises(ValueError):
+            g.quantize_async(d_s.float(), work)                  # float32 S*
+        with pytest.raises(ValueError):
+            g.quantize_async(d_s[:-1], work)                     # n - 1 rows
+        with pytest.raises(ValueError):
+            g.quantize_async(d_s.t(), work)                      # column stride n
+        short = dict(out, peak=out["peak"][:K - 1])
+        with pytest.raises(ValueError):
+            g.round_eval_async(d_s, K, w.seed, w.budget, 0, short, work)
+        bad = dict(out, best_k=out["best_k"].to(torch.int64))
+        with pytest.raises(ValueError):
+            g.round_eval_async(d_s, K, w.seed, w.budget, 0, bad, work)
+        # the correct call still runs
+        g.round_eval_async(d_s, K, w.seed, w.budget, 0, out, work)
+        torch.cuda.synchronize()
+        assert int(out["status"].item()) == ckm.OK
+        want = g.round_eval(w.s_frac, K, w.seed, w.budget)
+        assert np.array_equal(out["peak"].cpu().numpy(), want["peak"])
+    finally:
+        g.close()
