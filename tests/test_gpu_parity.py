@@ -200,9 +200,10 @@ def test_random_dag_sweep(n, K, kind):
     check_full(w, gpu_round_eval(w, budget=med), budget=med)
 
 
-@pytest.mark.parametrize("n", [1023, 1024, 1500, 2047, 2048, 3000])
+@pytest.mark.parametrize("n", [1023, 1024, 1500, 2047, 2048, 3000, 4095])
 def test_register_row_widths(n):
-    """Rows of 32, 64 and 128 words in registers (n < 1024, < 2048, < 4096):
+    """Rows of 32, 64 and 128 words in registers (n < 1024, < 2048, < 4096;
+    n = 4095 fills all 128 words):
     graphs on both sides of each boundary, sampled candidates against the
     oracle, the rest through the argmin and the best rows."""
     w = wl.random_dag(n, seed=n, K=70, window=40, max_deg=3, max_size=1000, max_cost=1000, s_kind="uniform",
@@ -252,10 +253,10 @@ def test_max_nodes_chain():
     check_rows(w, got, got["best_k"])
 
 
-@pytest.mark.parametrize("n", [337, 1500, 2047])
+@pytest.mark.parametrize("n", [337, 1500, 2047, 4095])
 def test_in_kernel_rows_without_row_arrays(n):
     """The rounding path on a work buffer without the row arrays: rows
-    rounded in the evaluate kernel (register rows of 32 and 64 words) and the
+    rounded in the evaluate kernel (register rows of 32, 64 and 128 words) and the
     best R recomputed by Algorithm 2 in the closure kernel. Every output
     equals the row-array path's, whose results the oracle checks; the best
     candidate's rows are checked against the oracle here too."""
