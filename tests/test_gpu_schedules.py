@@ -120,6 +120,28 @@ def test_config5_sampled():
     assert np.array_equal(got2["best_R"], ref.pack_rows(ref.solve_R(w, S)))
 
 
+def test_max_nodes_sampled():
+    """n = 4096, the largest graph (both rows in LDS, 128-word rows in the
+    transpose kernel): sampled candidates against the oracle."""
+    n, K = 4096, 70
+    w = wl.random_dag(n, seed=4096, K=K, window=40, max_deg=3, max_size=1000, max_cost=1000, s_kind="uniform",
+                      budget_pct=55.0)
+    rows = wl.random_schedules(n, K, seed=4097, density=0.2, kind="intervals")
+    log("n=%d K=%d" % (n, K))
+    got = gpu_eval(w, rows, 2 ** 62)
+    ks = [0, 1, 63, 64, 69]
+    orc = oracle_schedules(w, rows, ks)
+    for k in ks:
+        assert (int(got["peak"][k]), int(got["cost"][k])) == orc[k], k
+    budget = int(np.quantile(got["peak"], 0.5))
+    got2 = gpu_eval(w, rows, budget)
+    bk = lexi_best(got2["peak"], got2["cost"], budget)
+    assert got2["best_k"] == bk >= 0
+    assert (int(got2["peak"][bk]), int(got2["cost"][bk])) == oracle_schedules(w, rows, [bk])[bk]
+    S = np.tril(wl.unpack_schedules(rows[bk:bk + 1], w.n)[0], -1)
+    assert np.array_equal(got2["best_R"], ref.pack_rows(ref.solve_R(w, S)))
+
+
 def test_closed_forms_checkpoint_all_and_none():
     """Checkpoint-all (cost sum C, peak M_in + 2 M_param + sum M, R = I) next
     to the all-zero schedule, on a transformer-sized graph."""

@@ -130,6 +130,27 @@ def test_config5_sampled():
     check_rows(w, got2, p, bk)
 
 
+def test_max_nodes_sampled():
+    """n = 4096, the largest graph (both rows in LDS): sampled thresholds
+    against the oracle, best S and R included."""
+    n = 4096
+    w = wl.random_dag(n, seed=4098, K=80, window=40, max_deg=3, max_size=1000, max_cost=1000, s_kind="uniform",
+                      budget_pct=55.0)
+    p = grid(80, 6)
+    log("n=%d K=80" % n)
+    got = gpu_eval(w, p, 2 ** 62)
+    ks = [0, 1, 63, 64, 79]
+    orc = oracle_thresholds(w, p, ks)
+    for k in ks:
+        assert (int(got["peak"][k]), int(got["cost"][k])) == orc[k], k
+    budget = int(np.quantile(got["peak"], 0.5))
+    got2 = gpu_eval(w, p, budget)
+    bk = lexi_best(got2["peak"], got2["cost"], budget)
+    assert got2["best_k"] == bk >= 0
+    assert (int(got2["peak"][bk]), int(got2["cost"][bk])) == oracle_thresholds(w, p, [bk])[bk]
+    check_rows(w, got2, p, bk)
+
+
 def test_exact_ties_and_clamping():
     """S* on a 1/16 lattice (with values outside [0, 1]) and thresholds on
     the same lattice: every comparison at a tie must come out 'not greater'."""
