@@ -95,6 +95,15 @@ def test_config5_random_dag():
     check_plan(w, S, R)
 
 
+def test_max_nodes():
+    """n = 4096, the largest graph: 128-word columns in the R transpose."""
+    w = wl.random_dag(4096, seed=4099, K=4, window=40, max_deg=3, max_size=1000, max_cost=1000,
+                      s_kind="uniform", m_input=5, m_param=3)
+    S, R = oracle_schedule(w, 1)
+    log("n=%d" % w.n)
+    check_plan(w, S, R, junk=True, seed=4)
+
+
 SWEEP = [(1, 0), (2, 1), (3, 2), (31, 3), (32, 4), (33, 5), (63, 6), (64, 7), (65, 8), (127, 9), (129, 10),
          (200, 11), (300, 12)]
 
