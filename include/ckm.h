@@ -137,7 +137,9 @@ ckm_status ckm_round_eval(const ckm_graph* g, const double* s_frac, int64_t ld, 
  * stay alive until the stream has executed it. Work buffers are caller-owned
  * and sized by ckm_workspace_size; one work buffer must not be used by two
  * calls that may run concurrently. The three stages run in the order
- * quantize -> evaluate -> select, on one work buffer. */
+ * quantize -> evaluate -> select, on one work buffer. The library cannot
+ * check sizes behind a pointer: each array must hold the elements stated
+ * for it (work_bytes is checked against the layout). */
 
 /* Bytes of work buffer for K candidates on graph g. This includes, when the
  * S rows of all K candidates fit in 8 GiB, room for them and for their R
