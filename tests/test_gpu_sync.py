@@ -145,3 +145,41 @@ def test_binding_refuses_wrong_device_tensors():
         assert np.array_equal(out["peak"].cpu().numpy(), want["peak"])
     finally:
         g.close()
+
+
+def test_async_calls_from_threads_on_own_streams():
+    """Async calls on one graph from 4 threads, each with its own stream and
+    work buffer (calls only enqueue; the graph is shared read-only), give the
+    synchronous call's results."""
+    import torch
+    w = wl.config(3)
+    big = int(w.budget * 2.5)
+    jobs = [(K, seed) for K in (64, 300) for seed in (5, 6)]
+    want = {job: fresh(w, lambda g, job=job: g.round_eval(w.s_frac, job[0], job[1], big)) for job in jobs}
+    g = ckm.Graph.from_workload(w)
+    d_s = torch.from_numpy(w.s_frac).cuda()
+    torch.cuda.synchronize()
+
+    def run(job):
+        K, seed = job
+        stream = torch.cuda.Stream()
+        with torch.cuda.stream(stream):
+            work = g.alloc_work(K)
+            out = g.alloc_outputs(K)
+        g.round_eval_async(d_s, K, seed, big, 0, out, work, stream)
+        stream.synchronize()
+        return {k: v.cpu().numpy() for k, v in out.items()}
+
+    try:
+        log("%d async jobs on 4 threads" % len(jobs))
+        with ThreadPoolExecutor(4) as ex:
+            for _ in range(2):
+                for job, got in zip(jobs, ex.map(run, jobs)):
+                    assert int(got["status"][0]) == ckm.OK
+                    for key in ("peak", "cost", "feasible"):
+                        assert np.array_equal(got[key], want[job][key]), (job, key)
+                    assert int(got["best_k"][0]) == want[job]["best_k"]
+                    assert np.array_equal(got["best_S"].view(np.uint64), want[job]["best_S"])
+                    assert np.array_equal(got["best_R"].view(np.uint64), want[job]["best_R"])
+    finally:
+        g.close()
