@@ -230,7 +230,26 @@ static_assert(offsetof(NodeRec, umask) == 4 * kDwUmask && offsetof(NodeRec, refs
                   offsetof(NodeRec, lm) == 4 * kDwLm && offsetof(NodeRec, refs2) == 4 * kDwRefs2 &&
                   offsetof(NodeRec, dM) == 4 * kDwDM,
               "dword indices used by RecRegs, issue_reads and the closure kernel");
-constexpr uint32_t kRefsSlow = 1u << 11;   // refs1: node does not fit, use the CSR lists
+constexpr uint32_t kRefsSlow = 1u << 11;   // refs1: node does not fit the record format
+
+// A slow node (more than four dependencies, or more than one user beyond
+// v + 32, for v or for one of its dependencies) reads only umask, refs0,
+// refs1, bits0 and the fp64 groups of its record. The other dwords then hold
+// its lists in a second form:
+//   dword 32: far users of v (count) | dependencies (count) << 8 | kExtValid
+//   dwords 33-39: v's users beyond v + 32 (node numbers, two 16-bit fields
+//     per dword)
+//   dependency slot d at dwords ext_slot(d) ..+5: the dependency's users u
+//     with v < u <= v + 32 as a mask (bit u - v - 1); M of the dependency
+//     (binary64, two dwords); its node number | the count of its users beyond
+//     v + 32 << 16; those users (two dwords, two per dword)
+// A node beyond these counts walks the CSR lists (dword 32 without kExtValid).
+constexpr int kDwExt = 32, kExtFar = 14, kExtDeps = 6, kExtLate = 4;
+constexpr uint32_t kExtValid = 1u << 31;
+__host__ __device__ constexpr int ext_slot(int d) { return d < 4 ? 40 + 6 * d : 8 + 6 * (d - 4); }
+static_assert(ext_slot(3) + 6 <= 64 && ext_slot(5) + 6 <= 24 && kDwExt + 1 + kExtFar / 2 <= ext_slot(0),
+              "extended form inside the record, clear of the fields a slow node reads");
+static_assert(offsetof(NodeRec, mc) >= 24 * 4 && offsetof(NodeRec, dm01) + 16 <= 32 * 4, "fp64 groups at 24-31");
 
 __device__ __forceinline__ double dbl(uint32_t lo, uint32_t hi) {
   return __hiloint2double((int)hi, (int)lo);
@@ -735,8 +754,42 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
         }
       }
     }
+  } else if (const uint32_t h = rec.get(kDwExt); h & kExtValid) {
+    // outside the record format, inside its second form: the same tests with
+    // the far references listed there (each read from the R row; a node
+    // above t reads 0, as in the record format)
+    const uint32_t nfar = h & 0xFFu, nds = (h >> 8) & 0xFFu;
+    auto node16 = [&](int dw, uint32_t f) { return (rec.get(dw + (int)(f >> 1)) >> (16 * (f & 1u))) & 0xFFFFu; };
+    if (kFirst) {
+      anyU = 0;
+      r = 1;
+      val = fma((double)(~s1 & 1u), Mv, val);
+    } else {
+      uint32_t acc = sc.Rwin & um;
+      for (uint32_t f = 0; f < nfar; ++f) {
+        const uint32_t u = node16(kDwExt + 1, f);
+        acc |= bit(A.at_word(u >> 5), u & 31);
+      }
+      anyU = umin1(acc);
+      r = (s1 | anyU) & ~s0;
+    }
+    for (uint32_t d = 0; d < nds; ++d) {
+      const int b = ext_slot((int)d);
+      const uint32_t lm = rec.get(b);
+      const double dMs = dbl(rec.get(b + 1), rec.get(b + 2));
+      const uint32_t x = rec.get(b + 3);
+      const uint32_t i = x & 0xFFFFu, nl = x >> 16;
+      uint32_t later = sc.Rwin & lm;
+      for (uint32_t l = 0; l < nl; ++l) {
+        const uint32_t u = node16(b + 4, l);
+        later |= bit(A.at_word(u >> 5), u & 31);
+      }
+      later = umin1(later);
+      const uint32_t fr = r & ~bit(B.at_word(i >> 5), i & 31) & ~later & 1u;
+      val = fma((double)fr, dMs, val);
+    }
   } else {
-    // nodes outside the record format: walk the CSR lists
+    // nodes outside both formats: walk the CSR lists
     anyU = 0;
     const int ue = a.user_ptr[v + 1];
     for (int e = a.user_ptr[v]; e < ue; ++e) {
@@ -930,7 +983,8 @@ __device__ __forceinline__ void run_item(const EvalArgs& a, int t0, int t1, uint
 // are in LDS and swap roles. kSrc: where the S rows come from (kSrcRound,
 // kSrcUser, kSrcThreshold).
 template <int kRegW, int kSrc>
-__global__ void __launch_bounds__(kWave) ckm_eval_kernel(EvalArgs a) {
+__global__ void __launch_bounds__(kWave, kRegW == kRegRowWords ? 5 : 1)
+ckm_eval_kernel(EvalArgs a) {
   extern __shared__ uint32_t lds[];
   const int lane = threadIdx.x;
   const int group = blockIdx.x;
@@ -1678,6 +1732,46 @@ hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_
 }
 
 // ---------------------------------------------------------------------------
+// The second form of slow node v's lists (see kDwExt) into the record's
+// dwords, or false when v exceeds its counts.
+static bool build_ext_lists(int32_t v, const double* M, const int32_t* dep_ptr, const int32_t* dep_idx,
+                            const int32_t* user_ptr, const int32_t* user_idx, uint32_t dw[64]) {
+  auto put16 = [&](int at, int f, uint32_t node) { dw[at + f / 2] |= node << (16 * (f & 1)); };
+  int nfar = 0;
+  for (int32_t e = user_ptr[v]; e < user_ptr[v + 1]; ++e) {
+    const int u = user_idx[e];
+    if (u - v - 1 < 32) continue;
+    if (nfar == kExtFar) return false;
+    put16(kDwExt + 1, nfar++, (uint32_t)u);
+  }
+  const int nd = dep_ptr[v + 1] - dep_ptr[v];
+  if (nd > kExtDeps) return false;
+  for (int d = 0; d < nd; ++d) {
+    const int i = dep_idx[dep_ptr[v] + d];
+    const int b = ext_slot(d);
+    uint32_t lm = 0;
+    int nl = 0;
+    for (int32_t e = user_ptr[i]; e < user_ptr[i + 1]; ++e) {
+      const int u = user_idx[e];
+      if (u <= v) continue;
+      if (u - v - 1 < 32) {
+        lm |= 1u << (u - v - 1);
+      } else {
+        if (nl == kExtLate) return false;
+        put16(b + 4, nl++, (uint32_t)u);
+      }
+    }
+    uint64_t mbits;
+    memcpy(&mbits, &M[i], sizeof(mbits));
+    dw[b] = lm;
+    dw[b + 1] = (uint32_t)mbits;
+    dw[b + 2] = (uint32_t)(mbits >> 32);
+    dw[b + 3] = (uint32_t)i | (uint32_t)nl << 16;
+  }
+  dw[kDwExt] = (uint32_t)nfar | (uint32_t)nd << 8 | kExtValid;
+  return true;
+}
+
 void build_node_records(int32_t n, const double* M, const double* C, const int32_t* dep_ptr,
                         const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx,
                         void* out) {
@@ -1728,6 +1822,15 @@ void build_node_records(int32_t n, const double* M, const double* C, const int32
     r.mc[1] = r.C;
     r.dm01[0] = r.dM[0];
     r.dm01[1] = r.dM[1];
+    if (slow) {
+      // the slot fields are unused for a slow node: its lists go there
+      // (kept only if they fit; the fields a slow node reads are untouched)
+      uint32_t dw[64];
+      memcpy(dw, &r, sizeof(dw));
+      for (int k = 0; k < 64; ++k)
+        if ((k < 4 || k >= 8) && (k < 24 || k >= 32)) dw[k] = 0;
+      if (build_ext_lists(v, M, dep_ptr, dep_idx, user_ptr, user_idx, dw)) memcpy(&r, dw, sizeof(dw));
+    }
     recs[v] = r;
   }
 }
