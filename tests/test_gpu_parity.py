@@ -231,6 +231,43 @@ def test_dense_wide_graph():
     peak, _ = check_full(w, got)
 
 
+def boundary_graph():
+    """A 200-node graph whose slow nodes sit at the limits of the record's
+    second form (14 far users, 6 deps, 4 far later users per dep) and one
+    past each, next to a chain that keeps every node reachable."""
+    n = 200
+    deps = [set() if v == 0 else {v - 1} for v in range(n)]
+    deps[150] |= {0, 10, 20, 30, 40}            # 6 deps: second form
+    deps[160] |= {1, 11, 21, 31, 41, 51}        # 7 deps: CSR lists
+    for k in range(14):                         # node 5: 14 users beyond 5 + 32
+        deps[40 + 5 * k].add(5)
+    for k in range(15):                         # node 6: 15 of them
+        deps[41 + 5 * k].add(6)
+    deps[60].add(7)                             # dep 7 of node 60: 4 users beyond 60 + 32
+    for u in (100, 110, 120, 130):
+        deps[u].add(7)
+    deps[61].add(8)                             # dep 8 of node 61: 5 of them
+    for u in (101, 111, 121, 131, 141):
+        deps[u].add(8)
+    ptr, idx = wl.csr_from_deps([sorted(d) for d in deps])
+    rng = np.random.default_rng(200)
+    size = rng.integers(1, 1000, n).astype(np.int64)
+    cost = rng.integers(1, 1000, n).astype(np.int64)
+    return wl.Workload("form_limits", n, ptr, idx, cost, size, 7, 3, wl.s_frac_uniform(n, 21), 130, 21, 1 << 40)
+
+
+def test_slow_node_form_limits():
+    """Slow nodes at and one past each limit of the record's second form:
+    every candidate against the oracle, and the best rows at a budget where
+    some are feasible."""
+    w = boundary_graph()
+    log("form limits n=%d K=%d" % (w.n, w.K))
+    got = gpu_round_eval(w)
+    peak, _ = check_full(w, got)
+    med = int(np.median(peak))
+    check_full(w, gpu_round_eval(w, budget=med), budget=med)
+
+
 def test_max_nodes_chain():
     """n = 4096 (the largest graph): a chain with a mirrored backward pass."""
     F = 2047
