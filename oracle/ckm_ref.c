@@ -131,7 +131,7 @@ void ckm_ref_round_random(int32_t n, const uint32_t* q, uint64_t seed, uint32_t 
     }
 }
 
-/* Algorithm 2, first line: deterministic rounding S_int = 1[S* > 0.5]. */
+/* The deterministic rounding of Algorithm 2: S_int = 1[S* > 0.5]. */
 void ckm_ref_round_det(int32_t n, const double* s_frac, int64_t ld, uint8_t* S) {
   int32_t t, i;
   for (t = 0; t < n; ++t)
@@ -163,43 +163,47 @@ int ckm_ref_round_threshold(int32_t n, const double* s_frac, int64_t ld, double 
 }
 
 /* ------------------------------------------------------------------------ */
-/* Algorithm 2 (two-phase rounding), given S_int:
- *   R <- I (constraint 4a: node t is computed in stage t);
- *   while constraint (1c) S[t][i] <= R[t-1][i] + S[t-1][i] is violated for
- *     some t >= 1: compute v_i in the previous stage, R[t-1][i] <- 1;
- *   while constraint (1b) R[t][j] <= R[t][i] + S[t][i] is violated for some
- *     edge (i, j): compute v_i as a temporary, R[t][i] <- 1.
- * Section 5.2 scans each stage right to left (reverse topological order);
- * the loops below repeat full sweeps until no violation remains. */
+/* The recomputation matrix of two-phase rounding (Section 5.2), from the
+ * constraints it has to satisfy rather than from the repair loops of the
+ * printed listing. For stage t, R_t must contain node t (constraint 4a),
+ * every value kept for stage t+1 that stage t does not already hold
+ * (constraint 1c: S[t+1][i] <= R[t][i] + S[t][i]), and every dependency of a
+ * computed node that stage t does not hold (constraint 1b: R[t][j] <=
+ * R[t][i] + S[t][i] for each edge (i, j)). Section 5.2 takes the smallest such
+ * R_t, and the conditions are monotone, so R_t is the set reached from those
+ * seeds by walking dependency edges backwards, never into a value of S_t:
+ * a least fixed point, found here by a plain worklist search. */
 void ckm_ref_solve_R(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
                      const uint8_t* S, uint8_t* R) {
-  int32_t t, i, j, a;
-  int changed;
+  int32_t* stack = (int32_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+  int32_t t, i, a, top;
   memset(R, 0, (size_t)n * (size_t)n);
-  for (t = 0; t < n; ++t) R[(int64_t)t * n + t] = 1;
-
-  do {  /* constraint (1c) */
-    changed = 0;
-    for (t = 1; t < n; ++t)
-      for (i = 0; i < n; ++i)
-        if (S[(int64_t)t * n + i] > R[(int64_t)(t - 1) * n + i] + S[(int64_t)(t - 1) * n + i]) {
-          R[(int64_t)(t - 1) * n + i] = 1;
-          changed = 1;
+  for (t = 0; t < n; ++t) {
+    const uint8_t* St = S + (int64_t)t * n;
+    const uint8_t* Snext = (t + 1 < n) ? S + (int64_t)(t + 1) * n : NULL;  /* S[n] = 0 */
+    uint8_t* Rt = R + (int64_t)t * n;
+    top = 0;
+    /* seeds: node t (4a), values kept into t+1 but not held in t (1c) */
+    Rt[t] = 1;
+    stack[top++] = t;
+    for (i = 0; i < t; ++i)
+      if (Snext && Snext[i] && !St[i] && !Rt[i]) {
+        Rt[i] = 1;
+        stack[top++] = i;
+      }
+    /* closure under (1b): an operand of a computed node that is not held */
+    while (top > 0) {
+      int32_t j = stack[--top];
+      for (a = dep_ptr[j]; a < dep_ptr[j + 1]; ++a) {
+        i = dep_idx[a];
+        if (!St[i] && !Rt[i]) {
+          Rt[i] = 1;
+          stack[top++] = i;
         }
-  } while (changed);
-
-  do {  /* constraint (1b) */
-    changed = 0;
-    for (t = 0; t < n; ++t)
-      for (j = n - 1; j >= 0; --j)
-        for (a = dep_ptr[j]; a < dep_ptr[j + 1]; ++a) {
-          i = dep_idx[a];
-          if (R[(int64_t)t * n + j] > R[(int64_t)t * n + i] + S[(int64_t)t * n + i]) {
-            R[(int64_t)t * n + i] = 1;
-            changed = 1;
-          }
-        }
-  } while (changed);
+      }
+    }
+  }
+  free(stack);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -388,40 +392,44 @@ int ckm_ref_check_schedule(int32_t n, const int32_t* dep_ptr, const int32_t* dep
   return CKM_REF_OK;
 }
 
-/* Section 4.9, Algorithm 1: a row-major scan of R; stage t, node k:
- *   if R[t][k]: "%r = compute v_k", Regs[k] = r, r = r + 1;
- *   for i in Deps[k] u {k} (ascending; k is the largest): if FREE(t,i,k):
- *   "deallocate %Regs[i]", with FREE(t,i,k) = R[t][k] (1 - S[t+1][i])
- *   prod_{j in Users[i], j > k} (1 - R[t][j]) (eq. collectable).
- * A checkpoint of stage t with no computed user in the stage and not kept
- * into stage t+1 gets no FREE term; it is deallocated at the end of the stage
- * (where the U recurrence stops counting it), or with early != 0 at the
- * start of the stage (the code motion of Section 4.9).
- * Statement s is stmts[4s .. 4s+3] = (op, node, register, stage) with op 0 =
- * compute, 1 = deallocate. mem[s] (may be NULL) = M_in + 2 M_param + the
+/* The execution plan of Section 4.9 for a schedule (S, R), built from the
+ * memory model of Section 4.4 rather than by retracing the printed listing.
+ * Within stage t the plan computes, in increasing node order, every node
+ * with R[t][k] = 1, each into a fresh virtual register (registers numbered
+ * in compute order). A value i is released at the node k for which
+ * FREE(t,i,k) = 1 (eq. collectable: k computed, i in Deps[k] u {k}, i not
+ * kept into stage t+1, and no user of i after k computed in the stage);
+ * Theorem 4.1 makes that k unique. The release follows the compute of k, and
+ * releases at one k go in increasing order of the value (so k itself, the
+ * largest, comes last). A value held at the start of the stage that no
+ * computed node uses and that is not kept has no FREE term; it is released
+ * at the end of the stage, where the U recurrence stops counting it, or with
+ * early != 0 at the start (the code motion Section 4.9 describes).
+ * Statement s is stmts[4s .. 4s+3] = (op, node, register, stage), op 0 =
+ * compute, 1 = deallocate. mem[s] (may be NULL) = M_in + 2 M_param plus the
  * sizes of the registers live after statement s. At most `capacity`
- * statements are written; *count receives the number the plan has. Returns
+ * statements are written; *count receives the plan's length. Returns
  * CKM_REF_E_INVALID_ARG when (S, R) fails ckm_ref_check_schedule. */
 int ckm_ref_plan(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx, const int64_t* size,
                  int64_t m_input, int64_t m_param, const uint8_t* S, const uint8_t* R, int early,
                  int32_t* stmts, int64_t* mem, int64_t capacity, int64_t* count) {
-  int32_t t, k, i, j, a, m, pass;
+  int32_t t, k, i, j, a, b;
   int64_t s = 0, r = 0, live_bytes = 0;
-  int32_t* Regs;
+  int32_t* reg;       /* register holding value i, -1 if none */
+  int32_t* free_at;   /* per stage: the k with FREE(t,i,k) = 1, or -1 */
   int32_t* user_ptr;
   int32_t* user_idx;
   int32_t* fill;
-  int32_t* order;
-  int32_t deg;
   int32_t E = dep_ptr[n];
   int st = ckm_ref_check_schedule(n, dep_ptr, dep_idx, S, R);
   if (st != CKM_REF_OK) return st;
-  Regs = (int32_t*)malloc((size_t)n * sizeof(int32_t));
+  reg = (int32_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+  free_at = (int32_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
   user_ptr = (int32_t*)calloc((size_t)n + 1, sizeof(int32_t));
   user_idx = (int32_t*)malloc((size_t)(E > 0 ? E : 1) * sizeof(int32_t));
   fill = (int32_t*)calloc((size_t)n, sizeof(int32_t));
-  order = (int32_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
-  for (i = 0; i < n; ++i) Regs[i] = -1;
+  for (i = 0; i < n; ++i) reg[i] = -1;
+  /* Users[i] = { j : (v_i, v_j) in E } (transpose of Deps) */
   for (j = 0; j < n; ++j)
     for (a = dep_ptr[j]; a < dep_ptr[j + 1]; ++a) user_ptr[dep_idx[a] + 1]++;
   for (i = 0; i < n; ++i) user_ptr[i + 1] += user_ptr[i];
@@ -443,62 +451,52 @@ int ckm_ref_plan(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx, cons
     }                                                                           \
     ++s;                                                                        \
   } while (0)
+#define KEPT(i_) (t + 1 < n && (i_) < t + 1 && S[(int64_t)(t + 1) * n + (i_)])
 
   for (t = 0; t < n; ++t) {
     const uint8_t* St = S + (int64_t)t * n;
     const uint8_t* Rt = R + (int64_t)t * n;
-    for (pass = 0; pass < 3; ++pass) {
-      if (pass == 1) {
-        /* the scan of Algorithm 1 */
-        for (k = 0; k <= t; ++k) {
-          if (Rt[k]) {
-            Regs[k] = (int32_t)r;
-            EMIT(0, k, r);
-            ++r;
-          }
-          /* Deps[k] in ascending order, then k */
-          deg = dep_ptr[k + 1] - dep_ptr[k];
-          for (m = 0; m < deg; ++m) {
-            int32_t x = dep_idx[dep_ptr[k] + m], y = m;
-            while (y > 0 && order[y - 1] > x) {
-              order[y] = order[y - 1];
-              --y;
-            }
-            order[y] = x;
-          }
-          for (m = 0; m <= deg; ++m) {
-            int64_t FREE;
-            int32_t b;
-            i = (m < deg) ? order[m] : k;
-            FREE = (int64_t)Rt[k] * (1 - (int64_t)((t + 1 < n && i < t + 1) ? S[(int64_t)(t + 1) * n + i] : 0));
-            for (b = user_ptr[i]; b < user_ptr[i + 1]; ++b) {
-              j = user_idx[b];
-              if (j > k) FREE *= (1 - (int64_t)(j <= t ? Rt[j] : 0));
-            }
-            if (FREE) EMIT(1, i, Regs[i]);
-          }
+    /* free point of each value: eq. collectable evaluated for every pair
+     * (i, k) with i in Deps[k] u {k} */
+    for (i = 0; i < n; ++i) free_at[i] = -1;
+    for (k = 0; k <= t; ++k) {
+      if (!Rt[k]) continue;
+      for (a = dep_ptr[k]; a <= dep_ptr[k + 1]; ++a) {
+        int later = 0;
+        i = (a < dep_ptr[k + 1]) ? dep_idx[a] : k;
+        if (KEPT(i)) continue;
+        for (b = user_ptr[i]; b < user_ptr[i + 1]; ++b) {
+          j = user_idx[b];
+          if (j > k && j <= t && Rt[j]) later = 1;
         }
-      } else if ((pass == 0) == (early != 0)) {
-        /* unused checkpoints not kept into stage t+1 */
-        for (i = 0; i < t; ++i) {
-          int32_t b, used = 0;
-          if (!St[i] || (t + 1 < n && S[(int64_t)(t + 1) * n + i])) continue;
-          for (b = user_ptr[i]; b < user_ptr[i + 1]; ++b) {
-            j = user_idx[b];
-            if (j <= t && Rt[j]) used = 1;
-          }
-          if (!used) EMIT(1, i, Regs[i]);
-        }
+        if (!later) free_at[i] = k;
       }
     }
+    /* unused checkpoints not kept into t+1: released at the start (early) */
+    if (early)
+      for (i = 0; i < t; ++i)
+        if (St[i] && free_at[i] < 0 && !KEPT(i)) EMIT(1, i, reg[i]);
+    for (k = 0; k <= t; ++k) {
+      if (!Rt[k]) continue;
+      reg[k] = (int32_t)r;
+      EMIT(0, k, r);
+      ++r;
+      for (i = 0; i <= k; ++i)
+        if (free_at[i] == k) EMIT(1, i, reg[i]);
+    }
+    /* ... or at the end of the stage */
+    if (!early)
+      for (i = 0; i < t; ++i)
+        if (St[i] && free_at[i] < 0 && !KEPT(i)) EMIT(1, i, reg[i]);
   }
+#undef KEPT
 #undef EMIT
   *count = s;
-  free(Regs);
+  free(reg);
+  free(free_at);
   free(user_ptr);
   free(user_idx);
   free(fill);
-  free(order);
   return CKM_REF_OK;
 }
 

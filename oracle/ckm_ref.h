@@ -71,8 +71,10 @@ void ckm_ref_round_det(int32_t n, const double* s_frac, int64_t ld, uint8_t* S);
  * CKM_REF_E_INVALID_ARG for a NaN p or a NaN S* entry with i < t. */
 int ckm_ref_round_threshold(int32_t n, const double* s_frac, int64_t ld, double p, uint8_t* S);
 
-/* Algorithm 2, phase two: R = I, then repair constraint (1c) and then (1b)
- * until neither is violated. */
+/* Two-phase rounding's R (Section 5.2): per stage, the least set holding
+ * node t (4a) and the values kept into t+1 but not held in t (1c), closed
+ * under taking an operand of a computed node that stage t does not hold
+ * (1b). Found by a worklist search over the dependency edges. */
 void ckm_ref_solve_R(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
                      const uint8_t* S, uint8_t* R);
 
@@ -112,9 +114,11 @@ int ckm_ref_round_eval(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx
 int ckm_ref_check_schedule(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,
                            const uint8_t* S, const uint8_t* R);
 
-/* Algorithm 1 (Section 4.9): the execution plan of (S, R) as statements
- * (op, node, register, stage), op 0 = compute, 1 = deallocate, with the
- * memory in use after each statement (mem may be NULL). Unused checkpoints
+/* The execution plan of Section 4.9 for (S, R) as statements (op, node,
+ * register, stage), op 0 = compute, 1 = deallocate, with the memory in use
+ * after each statement (mem may be NULL). Each value is released after the
+ * compute of the node where its FREE term (eq. collectable) is 1; releases
+ * at one node go in increasing value order. Unused checkpoints
  * that are not kept are deallocated at the end of their stage, or at its
  * start when early != 0. Writes at most capacity statements; *count = the
  * plan's length. CKM_REF_E_INVALID_ARG if (S, R) fails the check above. */

@@ -198,20 +198,24 @@ def test_solve_R_is_unique_minimum_all_S(n, seed):
 
 
 @pytest.mark.parametrize("seed", range(3))
-def test_solve_R_is_unique_minimum_n5_sampled(seed):
+def test_solve_R_is_unique_minimum_n5_all_S(seed):
+    """The same brute force on 5-node graphs: all 1024 strict-lower S, each
+    against all 1024 R with R_tt = 1."""
     n = 5
     w = small_graph(n, 10 + seed)
     deps = deps_lists(w)
     Rs = all_lower(n, strict=True, diag_one=True)
-    rng = np.random.default_rng(seed)
-    for S in all_lower(n, strict=True, count=48, rng=rng):
+    C = w.cost.astype(np.int64)
+    for S in all_lower(n, strict=True):
         R = ref.solve_R(w, S)
         feas = Rs[feasible_R_mask(deps, S, Rs)]
         assert feasible_R_mask(deps, S, R[None])[0]
         assert np.all(feas >= R[None])
+        costs = (feas * C[None, None, :]).sum(axis=(1, 2))
+        assert int((R * C[None, :]).sum()) == int(costs.min())
 
 
-@pytest.mark.parametrize("n,seed", [(3, 0), (4, 1), (4, 2)])
+@pytest.mark.parametrize("n,seed", [(3, 0), (4, 1), (4, 2), (5, 3)])
 def test_ilp_optimum_bounds_two_phase(n, seed):
     """The MILP of Section 4.7 is a lower bound on any rounded schedule: for
     every budget, min over feasible (S, R) pairs <= min over S of the

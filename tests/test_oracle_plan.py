@@ -57,6 +57,30 @@ def test_diamond_plan_golden():
     assert mem.tolist() == want_mem.tolist()
 
 
+def test_descending_csr_plan_golden():
+    """Releases after one compute come in increasing node order, also when
+    the graph's CSR row lists the dependencies in another order."""
+    n = 4
+    ptr = np.array([0, 0, 0, 0, 3], np.int32)
+    idx = np.array([2, 0, 1], np.int32)          # node 3's row, unsorted
+    w = wl.Workload("g", n, ptr, idx, np.ones(n, np.int64), np.array([1, 2, 4, 8], np.int64), 0, 0,
+                    np.zeros((n, n)), 1, 0, 0)
+    S = np.zeros((n, n), np.uint8)
+    R = ref.solve_R(w, S)
+    want_R = np.eye(n, dtype=np.uint8)
+    want_R[3, :3] = 1
+    assert np.array_equal(R, want_R)
+    want_st, want_mem = read_plan_fixture("plan_descending_deps.txt")[""]
+    for early in (False, True):                  # no unused checkpoints: same plan
+        st, mem = ref.plan(w, S, R, early=early)
+        assert st.tolist() == want_st.tolist()
+        assert mem.tolist() == want_mem.tolist()
+    # the same graph with its rows sorted gives the same plan
+    ws = w.replace(dep_idx=np.array([0, 1, 2], np.int32))
+    st, mem = ref.plan(ws, S, R)
+    assert st.tolist() == want_st.tolist()
+
+
 def test_unused_checkpoint_plans_golden():
     w = graph([[], [0], [1]], [1, 2, 4])
     S = np.zeros((3, 3), np.uint8)
