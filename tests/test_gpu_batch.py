@@ -80,22 +80,28 @@ def test_configs(cfg, K):
 
 
 def test_config4_transformer_sampled():
+    """All K = 1024 candidates of the transformer workload: a spread of 24
+    against the oracle's search over its simulator, and the whole array
+    against the linear form of the GPU's own peaks and costs (which the
+    rounding-path tests check against the oracle for every candidate)."""
     w = wl.config(4)
-    K = 256
+    K = w.K
     peak, cost = peaks_costs(w, K)
     base = w.m_input + 2 * w.m_param
     budget = int(base + 2.5 * (np.median(peak) - base))
     cap = int(np.median(cost))
     log("config 4 K=%d" % K)
     got = gpu_max_batch(w, K, budget, cap)
-    ks = [0, 1, 63, 64, 127, 200, 255]
+    rng = np.random.default_rng(44)
+    ks = sorted(set([0, 1, 63, 64, 127, 200, 255, 511, 1023] + [int(k) for k in rng.integers(0, K, 15)]))
     orc = oracle_batches(w, ks, budget, cap)
     for k in ks:
         assert got["batch"][k] == orc[k][0], k
-    # the whole array against the linear form of the GPU's own peaks and
-    # costs (checked against the oracle in the rounding-path tests)
+    assert len({int(got["batch"][k]) for k in ks}) > 1      # the sample spans several multipliers
     lin = np.where((cost <= cap) & (peak <= budget), (budget - base) // np.maximum(peak - base, 1), 0)
     assert np.array_equal(got["batch"], lin)
+    bk = int(got["best_k"])
+    assert bk >= 0 and got["batch"][bk] == oracle_batches(w, [bk], budget, cap)[bk][0]
 
 
 @pytest.mark.parametrize("n,K", [(1, 1), (2, 5), (33, 64), (65, 70), (129, 33)])

@@ -159,28 +159,52 @@ def test_config4_sparse_sampled():
     check_full(w, got)
 
 
-def test_config5_random_dag_sampled():
-    """n = 4001, K = 4096: the GPU evaluates every candidate; the oracle checks
-    a spread of candidates (each is independent of the others)."""
+FIXTURE5 = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "workload5_oracle.npz")
+
+
+def test_config5_random_dag_all_candidates():
+    """n = 4001, K = 4096: every candidate's peak and cost against the
+    oracle's, stored by tests/golden/make_workload5_fixture.py (which calls
+    only the oracle); the argmin and the best candidate's S and R rows at two
+    budgets where some candidates are feasible, against the oracle run here."""
     w = wl.config(5)
+    fx = np.load(FIXTURE5)
+    assert int(fx["n"]) == w.n and int(fx["K"]) == w.K and int(fx["seed"]) == w.seed
+    peak, cost = fx["peak"], fx["cost"]
     log("config 5 n=%d K=%d" % (w.n, w.K))
     got = gpu_round_eval(w)
-    rng = np.random.default_rng(5)
-    ks = sorted(set([0, 1, 63, 64, 65, 127, 2047, 4031, 4095] + list(rng.integers(0, w.K, 23))))
-    orc = oracle_candidates(w, ks)
-    for k in ks:
-        assert (int(got["peak"][k]), int(got["cost"][k])) == orc[k], k
-    assert np.array_equal(got["feasible"], (got["peak"] <= w.budget).astype(np.uint8))
-    assert got["best_k"] == lexi_best(got["peak"], got["cost"], w.budget)
-    # a budget that admits some candidates: argmin and its rows
-    budget = int(np.quantile(got["peak"], 0.3))
-    got2 = gpu_round_eval(w, budget=budget)
-    assert np.array_equal(got2["peak"], got["peak"]) and np.array_equal(got2["cost"], got["cost"])
-    bk = lexi_best(got2["peak"], got2["cost"], budget)
-    assert got2["best_k"] == bk >= 0
-    orc_bk = oracle_candidates(w, [bk])[bk]
-    assert (int(got2["peak"][bk]), int(got2["cost"][bk])) == orc_bk
-    check_rows(w, got2, bk)
+    bad = np.nonzero((got["peak"] != peak) | (got["cost"] != cost))[0]
+    assert bad.size == 0, "mismatch at k=%s" % bad[:8]
+    assert np.array_equal(got["feasible"], (peak <= w.budget).astype(np.uint8))
+    assert got["best_k"] == lexi_best(peak, cost, w.budget)
+    for q in (0.3, 0.5):
+        budget = int(np.quantile(peak, q))
+        log("config 5 budget at the %.1f peak quantile" % q)
+        got2 = gpu_round_eval(w, budget=budget)
+        assert np.array_equal(got2["peak"], peak) and np.array_equal(got2["cost"], cost)
+        bk = lexi_best(peak, cost, budget)
+        assert got2["best_k"] == bk >= 0
+        check_rows(w, got2, bk)
+
+
+SEED64 = 0x89ABCDEF01234567       # both 32-bit halves of the Philox key nonzero
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_seed_with_high_word(cfg):
+    """A seed whose high 32 bits are nonzero (the second Philox key word):
+    every candidate, with and without the deterministic candidate 0."""
+    w = wl.config(cfg)
+    for flags in (0, ckm.F_DET0):
+        log("config %d seed 0x%x flags %d" % (cfg, SEED64, flags))
+        got = gpu_round_eval(w, seed=SEED64, flags=flags)
+        peak, _ = check_full(w, got, flags=flags, seed=SEED64)
+        med = int(np.median(peak))
+        got2 = gpu_round_eval(w, seed=SEED64, flags=flags, budget=med)
+        check_full(w, got2, flags=flags, budget=med, seed=SEED64)
+    # the high word changes the draws
+    assert not np.array_equal(gpu_round_eval(w, seed=SEED64)["peak"],
+                              gpu_round_eval(w, seed=SEED64 & 0xFFFFFFFF)["peak"])
 
 
 SWEEP = [(1, 3, "uniform"), (2, 5, "uniform"), (3, 4, "beta"), (5, 9, "binary"), (17, 64, "sparse"),
@@ -318,9 +342,15 @@ def test_in_kernel_rows_without_row_arrays(n):
         assert int(out["best_k"].item()) == want["best_k"] >= 0
         assert np.array_equal(ckm.rows_to_numpy(out["best_S"]), want["best_S"])
         assert np.array_equal(ckm.rows_to_numpy(out["best_R"]), want["best_R"])
+        direct = out["peak"].cpu().numpy(), out["cost"].cpu().numpy()
     finally:
         g.close()
     check_rows(w.replace(K=K), want, want["best_k"])
+    # the in-kernel path's own outputs against the oracle, candidate by candidate
+    ks = [0, 1, 63, 64, 65, 127, 128, K - 1]
+    orc = oracle_candidates(w, ks)
+    for k in ks:
+        assert (int(direct[0][k]), int(direct[1][k])) == orc[k], k
 
 
 def test_async_stages_and_split_invariance():
