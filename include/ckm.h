@@ -318,6 +318,27 @@ ckm_status ckm_plan_async(const ckm_graph* g, const uint64_t* d_S, const uint64_
                           ckm_stmt* d_P, int64_t capacity, int64_t* d_count, int64_t* d_mem, int32_t* d_status,
                           void* d_work, size_t work_bytes, void* stream);
 
+/* ---- no allocation -----------------------------------------------------
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.
+ * ckm_round_eval_noalloc is ckm_round_eval_async (same arguments, same
+ * results) with the caller's work buffer replaced by a static work area of
+ * CKM_NOALLOC_SCRATCH_BYTES on each device, held from the library's first
+ * use of the device until the process ends; its address is resolved when a
+ * graph is created on the device. The call allocates nothing (no hipMalloc,
+ * hipFree or other allocating routine) and only enqueues work on `stream`.
+ * A problem whose smallest work buffer (ckm_workspace_size_min) exceeds the
+ * area gives CKM_E_UNSUPPORTED; the row arrays are used when the full work
+ * buffer (ckm_workspace_size) fits in it. Every call on one device shares
+ * that device's area and the area keeps the last call's contents: calls
+ * that may overlap on one device (other streams, other threads) race, and
+ * the caller must serialize them. */
+#define CKM_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+ckm_status ckm_round_eval_noalloc(const ckm_graph* g, const double* d_s_frac, int64_t ld, int32_t K,
+                                  uint64_t seed, int64_t budget, uint32_t flags, int64_t* d_peak,
+                                  int64_t* d_cost, uint8_t* d_feasible, int32_t* d_best_k,
+                                  uint64_t* d_best_S, uint64_t* d_best_R, int32_t* d_status, void* stream);
+
 /* Thread-local text describing the calling thread's last non-OK status. */
 const char* ckm_last_error(void);
 

@@ -9,6 +9,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB_PATH = os.path.join(HERE, "libckm.so")
 SOURCES = [os.path.join(HERE, "csrc", "ckm_kernels.hip"), os.path.join(HERE, "csrc", "ckm_plan.hip"),
+           os.path.join(HERE, "csrc", "ckm_noalloc.hip"),
            os.path.join(HERE, "csrc", "ckm_host.cpp")]
 ARCH = "gfx950"
 

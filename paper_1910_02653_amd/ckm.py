@@ -28,8 +28,9 @@ EXPORTS = (
     "ckm_workspace_size", "ckm_workspace_size_min", "ckm_quantize_async", "ckm_round_async",
     "ckm_evaluate_async", "ckm_select_async", "ckm_round_eval_async", "ckm_eval_schedules", "ckm_eval_schedules_async", "ckm_threshold_eval",
     "ckm_threshold_eval_async", "ckm_plan", "ckm_plan_async", "ckm_max_batch",
-    "ckm_max_batch_async", "ckm_last_error",
+    "ckm_max_batch_async", "ckm_round_eval_noalloc", "ckm_last_error",
 )
+NOALLOC_SCRATCH_BYTES = 256 << 20
 PLAN_EARLY_FREE = 1
 OP_COMPUTE, OP_DEALLOCATE = 0, 1
 
@@ -78,6 +79,8 @@ def lib():
         L.ckm_select_async.restype = C.c_int
         L.ckm_round_eval_async.argtypes = [p, p, i64, i32, u64, i64, u32, p, p, p, p, p, p, p, p, sz, p]
         L.ckm_round_eval_async.restype = C.c_int
+        L.ckm_round_eval_noalloc.argtypes = [p, p, i64, i32, u64, i64, u32, p, p, p, p, p, p, p, p]
+        L.ckm_round_eval_noalloc.restype = C.c_int
         L.ckm_eval_schedules.argtypes = [p, p, i32, i64, p, p, p, p, p]
         L.ckm_eval_schedules.restype = C.c_int
         L.ckm_eval_schedules_async.argtypes = [p, p, i32, i64, p, p, p, p, p, p, p, sz, p]
@@ -343,6 +346,13 @@ class Graph:
         wp, wb = _work(work)
         _check(lib().ckm_round_eval_async(self._h, sp, ld, int(K), int(seed), int(budget), int(flags), peak, cost,
                                           feas, bk, bS, bR, st, wp, wb, _stream_ptr(stream)))
+
+    def round_eval_noalloc(self, d_s_frac, K, seed, budget, flags, out: dict, stream=None):
+        """ckm_round_eval_async on the library's static per-device work area."""
+        sp, ld = _dev_s(d_s_frac, self.n)
+        peak, cost, feas, bk, bS, bR, st = self._out(out, K)
+        _check(lib().ckm_round_eval_noalloc(self._h, sp, ld, int(K), int(seed), int(budget), int(flags), peak, cost,
+                                            feas, bk, bS, bR, st, _stream_ptr(stream)))
 
     def eval_schedules_async(self, d_S, K, budget, out: dict, work, stream=None):
         """d_S: int64 device tensor holding K x n x W bit-row words."""

@@ -53,6 +53,16 @@ struct DeviceGuard {
 
 namespace ckm {
 
+ckm_status set_error(ckm_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
 // Device memory, pinned host memory and a stream for the synchronous entry
 // points, kept on the graph so that repeated calls allocate nothing after the
 // first. The buffers grow to the largest call seen and are released with the
@@ -448,6 +458,12 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
     return fail_hip(e, "hipGetDevice");
   }
   g->eval_waves = ckm::eval_waves_per_cu(n);
+  // the work area of ckm_round_eval_noalloc on this device, resolved once
+  e = ckm::noalloc_setup(g->device);
+  if (e != hipSuccess) {
+    delete g;
+    return fail_hip(e, "resolving the no-allocation work area");
+  }
   e = hipMalloc(&g->d_mem, total);
   if (e != hipSuccess) {
     delete g;

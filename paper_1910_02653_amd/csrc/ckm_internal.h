@@ -90,6 +90,16 @@ struct Layout {
 
 Layout make_layout(int32_t n, int32_t K);
 
+// Records a thread-local error message (ckm_last_error) and returns st.
+ckm_status set_error(ckm_status st, const char* fmt, ...);
+
+// The static work area of ckm_round_eval_noalloc (ckm_noalloc.hip):
+// noalloc_setup resolves its address on `device`, which must be current
+// (graph creation calls it); noalloc_scratch returns the kept address, or
+// NULL when the device was never set up.
+hipError_t noalloc_setup(int device);
+void* noalloc_scratch(int device);
+
 // How the stages of one group of 64 candidates are cut into work items (one
 // wave each). Items are numbered in dispatch order, most expensive first, so
 // the cheap ones fill the end of the launch.
