@@ -32,10 +32,11 @@
  * ckm_last_error() gives a thread-local message for the last non-OK status
  * of the calling thread. On a non-OK return the outputs are unspecified.
  *
- * Exact-arithmetic range: the kernels accumulate sizes and costs in IEEE
- * binary64, which is exact for integers below 2^53. A graph whose
- * M_in + 2 M_param + sum(M) or sum(C) reaches 2^53, or whose n * sum(C)
- * exceeds INT64_MAX, is rejected with CKM_E_OVERFLOW.
+ * Exact-arithmetic range: every memory level and cost the method forms is
+ * at most M_in + 2 M_param + sum(M), or n * sum(C); a graph for which either
+ * exceeds INT64_MAX is rejected with CKM_E_OVERFLOW, and every other graph is
+ * evaluated exactly. (The kernels sum in IEEE binary64 while all sums stay
+ * below 2^53, where it is exact, and in int64 otherwise.)
  */
 #ifndef CKM_H
 #define CKM_H
@@ -53,7 +54,7 @@ typedef enum {
   CKM_OK = 0,
   CKM_E_INVALID_ARG = 1, /* bad argument: NULL, K < 1, ld < n, negative budget, NaN in S* */
   CKM_E_GRAPH = 2,       /* not topologically numbered, duplicate edge, users != transpose */
-  CKM_E_OVERFLOW = 3,    /* sizes or costs outside the exact-arithmetic range */
+  CKM_E_OVERFLOW = 3,    /* M_in + 2 M_param + sum(M) or n * sum(C) exceeds INT64_MAX */
   CKM_E_UNSUPPORTED = 4, /* n > CKM_MAX_NODES, K > CKM_MAX_CANDIDATES (CKM_MAX_THRESHOLDS) */
   CKM_E_NOMEM = 5,       /* host or device allocation failed */
   CKM_E_DEVICE = 6       /* a HIP runtime call failed (message has the HIP error) */
@@ -86,8 +87,8 @@ enum {
  * Errors: CKM_E_GRAPH for a malformed CSR (dep_ptr[0] != 0, dep_ptr
  * decreasing, more than n(n-1)/2 edges), an edge i -> j with i < 0 or
  * i >= j, a duplicate edge, or Users that differ from the transpose of Deps;
- * CKM_E_OVERFLOW when M_in + 2 M_param + sum(M) or sum(C) reaches 2^53, or
- * n * sum(C) exceeds INT64_MAX; CKM_E_INVALID_ARG for NULL arrays or negative
+ * CKM_E_OVERFLOW when M_in + 2 M_param + sum(M) or n * sum(C) exceeds
+ * INT64_MAX; CKM_E_INVALID_ARG for NULL arrays or negative
  * sizes and costs; CKM_E_NOMEM, CKM_E_DEVICE when allocation or upload
  * fails. On error *out is NULL. */
 ckm_status ckm_graph_create(int32_t n, const int32_t* dep_ptr, const int32_t* dep_idx,

@@ -368,24 +368,30 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
     }
     std::sort(di.begin() + dp[j], di.begin() + dp[j + 1]);
   }
-  // Sizes and costs: non-negative, totals inside the exact range.
+  // Sizes and costs: non-negative; M_in + 2 M_param + sum(M) and n sum(C)
+  // within int64 (every memory level and every cost the method forms is at
+  // most these).
   int64_t total_m = m_input, total_c = 0;
   auto add_checked = [](int64_t& acc, int64_t v) {
-    if (v > kExactLimit - 1 - acc) return false;
+    if (v > INT64_MAX - acc) return false;
     acc += v;
     return true;
   };
   if (!add_checked(total_m, m_param) || !add_checked(total_m, m_param))
-    return fail(CKM_E_OVERFLOW, "M_in + 2 M_param reaches 2^53");
+    return fail(CKM_E_OVERFLOW, "M_in + 2 M_param exceeds INT64_MAX");
   for (int32_t v = 0; v < n; ++v) {
     if (cost[v] < 0 || bytes[v] < 0)
       return fail(CKM_E_INVALID_ARG, "negative cost or size at node %d", v);
     if (!add_checked(total_m, bytes[v]))
-      return fail(CKM_E_OVERFLOW, "M_in + 2 M_param + sum(M) reaches 2^53");
-    if (!add_checked(total_c, cost[v])) return fail(CKM_E_OVERFLOW, "sum(C) reaches 2^53");
+      return fail(CKM_E_OVERFLOW, "M_in + 2 M_param + sum(M) exceeds INT64_MAX");
+    if (!add_checked(total_c, cost[v])) return fail(CKM_E_OVERFLOW, "sum(C) exceeds INT64_MAX");
   }
   if (total_c > 0 && (int64_t)n > INT64_MAX / total_c)
     return fail(CKM_E_OVERFLOW, "n * sum(C) exceeds INT64_MAX");
+  // binary64 sums are exact while every partial sum stays below 2^53: each
+  // stage's memory levels are at most M_in + 2 M_param + sum(M), its cost at
+  // most sum(C) (the stage costs are added in int64)
+  const bool wide = total_m >= kExactLimit || total_c >= kExactLimit;
 
   // Users = transpose(Deps), rows ascending.
   std::vector<int32_t> up(n + 1, 0), ui(E);
@@ -423,8 +429,8 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
 
   const size_t Ea = (size_t)std::max(E, 1);
   const size_t off_M = 0;
-  const size_t off_C = align256(off_M + n * sizeof(double));
-  const size_t off_up = align256(off_C + n * sizeof(double));
+  const size_t off_C = align256(off_M + n * sizeof(int64_t));
+  const size_t off_up = align256(off_C + n * sizeof(int64_t));
   const size_t off_ui = align256(off_up + (n + 1) * sizeof(int32_t));
   const size_t off_dp = align256(off_ui + Ea * sizeof(int32_t));
   const size_t off_di = align256(off_dp + (n + 1) * sizeof(int32_t));
@@ -432,32 +438,28 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
   const size_t off_rec = align256(off_uo + Ea * sizeof(int32_t));
   const size_t total = align256(off_rec + (size_t)n * ckm::kNodeRecBytes);
   std::vector<char> host(total, 0);
-  std::vector<double> Md(n), Cd(n);
-  for (int32_t v = 0; v < n; ++v) {
-    Md[v] = (double)bytes[v];
-    Cd[v] = (double)cost[v];
-  }
-  memcpy(host.data() + off_M, Md.data(), n * sizeof(double));
-  memcpy(host.data() + off_C, Cd.data(), n * sizeof(double));
+  memcpy(host.data() + off_M, bytes, n * sizeof(int64_t));
+  memcpy(host.data() + off_C, cost, n * sizeof(int64_t));
   memcpy(host.data() + off_up, up.data(), (n + 1) * sizeof(int32_t));
   if (E) memcpy(host.data() + off_ui, ui.data(), E * sizeof(int32_t));
   memcpy(host.data() + off_dp, dp.data(), (n + 1) * sizeof(int32_t));
   if (E) memcpy(host.data() + off_di, di.data(), E * sizeof(int32_t));
   if (E) memcpy(host.data() + off_uo, upos.data(), E * sizeof(int32_t));
-  ckm::build_node_records(n, Md.data(), Cd.data(), dp.data(), di.data(), up.data(), ui.data(),
+  ckm::build_node_records(n, bytes, cost, wide, dp.data(), di.data(), up.data(), ui.data(),
                           host.data() + off_rec);
 
   ckm_graph* g = new (std::nothrow) ckm_graph();
   if (!g) return fail(CKM_E_NOMEM, "host allocation failed");
   g->n = n;
   g->num_edges = E;
-  g->base = (double)(m_input + 2 * m_param);
+  g->base = m_input + 2 * m_param;
+  g->wide = wide;
   hipError_t e = hipGetDevice(&g->device);
   if (e != hipSuccess) {
     delete g;
     return fail_hip(e, "hipGetDevice");
   }
-  g->eval_waves = ckm::eval_waves_per_cu(n);
+  g->eval_waves = ckm::eval_waves_per_cu(n, wide);
   // the work area of ckm_round_eval_noalloc on this device, resolved once
   e = ckm::noalloc_setup(g->device);
   if (e != hipSuccess) {
@@ -477,8 +479,8 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
     return fail_hip(e, "hipMemcpy graph upload");
   }
   char* base = static_cast<char*>(g->d_mem);
-  g->d_M = reinterpret_cast<const double*>(base + off_M);
-  g->d_C = reinterpret_cast<const double*>(base + off_C);
+  g->d_M = reinterpret_cast<const int64_t*>(base + off_M);
+  g->d_C = reinterpret_cast<const int64_t*>(base + off_C);
   g->d_user_ptr = reinterpret_cast<const int32_t*>(base + off_up);
   g->d_user_idx = reinterpret_cast<const int32_t*>(base + off_ui);
   g->d_dep_ptr = reinterpret_cast<const int32_t*>(base + off_dp);

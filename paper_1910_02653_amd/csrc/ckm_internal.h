@@ -12,19 +12,22 @@ namespace ckm {
 struct SyncCache;  // buffers and stream of the synchronous entry points (ckm_host.cpp)
 }
 
-// Graph on the device. Node arrays hold sizes and costs as binary64 (exact:
-// the host rejects totals >= 2^53). Users rows are sorted ascending; for the
-// dep entry e = (i -> v) in v's deps row, dep_upos[e] is the index in
-// user_idx of the first user of i that is greater than v.
+// Graph on the device. Node arrays hold sizes and costs as int64. Users
+// rows are sorted ascending; for the dep entry e = (i -> v) in v's deps row,
+// dep_upos[e] is the index in user_idx of the first user of i that is
+// greater than v. The evaluate kernels sum sizes and costs in binary64 when
+// every sum they form stays below 2^53 (exact there), and in int64 otherwise
+// (`wide`); the node records carry the values in the chosen form.
 struct ckm_graph {
   int32_t n = 0;
   int32_t num_edges = 0;
   int device = 0;
-  double base = 0.0;          // M_in + 2 M_param (eq. U_init constant overhead)
+  int64_t base = 0;           // M_in + 2 M_param (eq. U_init constant overhead)
+  bool wide = false;          // sums reach 2^53: int64 arithmetic in the evaluate kernels
   int32_t eval_waves = 1;     // resident evaluate waves per CU for this n (work plan sizing)
   void* d_mem = nullptr;      // one allocation holding every array below
-  const double* d_M = nullptr;
-  const double* d_C = nullptr;
+  const int64_t* d_M = nullptr;
+  const int64_t* d_C = nullptr;
   const int32_t* d_user_ptr = nullptr;
   const int32_t* d_user_idx = nullptr;
   const int32_t* d_dep_ptr = nullptr;
@@ -57,7 +60,8 @@ constexpr size_t kRowsMaxBytes = (size_t)8 << 30;
 
 // Host-side builder of the per-node records the evaluate kernel reads
 // (layout documented with NodeRec in ckm_kernels.hip). Writes n records.
-void build_node_records(int32_t n, const double* M, const double* C, const int32_t* dep_ptr,
+// M, C: int64 sizes and costs; wide: store them as int64 (else as binary64).
+void build_node_records(int32_t n, const int64_t* M, const int64_t* C, bool wide, const int32_t* dep_ptr,
                         const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx,
                         void* out);
 
@@ -114,8 +118,8 @@ Plan plan_auto(int32_t n, int32_t K, int32_t max_items, int32_t waves_per_cu);
 Plan plan_splits(int32_t n, int32_t splits);
 
 // Resident evaluate waves per CU for a graph of n nodes (the runtime's
-// occupancy figure for the kernel variant and LDS size n selects).
-int32_t eval_waves_per_cu(int32_t n);
+// occupancy figure for the kernel variant and LDS size n and wide select).
+int32_t eval_waves_per_cu(int32_t n, bool wide);
 
 // Kernel launchers (defined in ckm_kernels.hip). They only enqueue work.
 hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,

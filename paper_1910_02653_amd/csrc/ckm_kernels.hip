@@ -205,7 +205,7 @@ __device__ __forceinline__ uint32_t threshold_word(QPtr qrow, int w, int r, uint
 // n, whose bit no row ever sets.
 constexpr int kRecDeps = 4;
 struct NodeRec {
-  double M, C;              // M_v, C_v
+  uint64_t M, C;            // M_v, C_v (binary64, or int64 for a wide graph)
   uint32_t umask;           // users u of v with u <= v + 32
   uint32_t refs0;           // word indices: fu | fl0 << 8 | s1_0 << 16 | fl1 << 24
   uint32_t refs1;           // s1_1 word | deps << 8 | slow << 11 | bit positions 6-8 at 12, 17, 22
@@ -214,11 +214,11 @@ struct NodeRec {
   uint32_t lm[kRecDeps];    // per slot: users u of the dep with v < u <= v + 32
   uint32_t refs2;           // word indices: fl2 | s1_2 << 8 | fl3 << 16 | s1_3 << 24
   uint32_t pad0;
-  double dM[kRecDeps];      // M of each dependency slot
+  uint64_t dM[kRecDeps];    // M of each dependency slot
   uint32_t pad1[2];
   // fp64 operands again, read by two wave-uniform 16-byte loads: M_v, C_v,
   // and the M of dependency slots 0 and 1
-  double mc[2], dm01[2];
+  uint64_t mc[2], dm01[2];
   uint32_t pad[32];         // one dword per lane of a 64-lane load
 };
 static_assert(sizeof(NodeRec) == kNodeRecBytes, "node record layout");
@@ -255,6 +255,45 @@ __device__ __forceinline__ double dbl(uint32_t lo, uint32_t hi) {
   return __hiloint2double((int)hi, (int)lo);
 }
 
+// max(a, b) for values that are never NaN, without the quieting step that
+// fmax adds on a loop-carried operand.
+__device__ __forceinline__ double max_f64(double a, double b) {
+  double d;
+  asm("v_max_f64 %0, %1, %2" : "=v"(d) : "v"(a), "v"(b));
+  return d;
+}
+
+// The sums of the scan: binary64, exact while every partial sum stays below
+// 2^53 (the host checks the graph's totals), or int64 for a wide graph. The
+// b01 arguments are 0 or 1. In int64 the stage peak U0 - Y + max is formed
+// with wrapping additions: its terms may leave the int64 range on the way,
+// the result (a memory level of the stage) does not.
+template <bool kWide> struct Ar;
+template <> struct Ar<false> {
+  using T = double;
+  static __device__ T of(uint32_t lo, uint32_t hi) { return dbl(lo, hi); }
+  static __device__ T of_i(int64_t x) { return (double)x; }
+  static __device__ T madd(T acc, uint32_t b01, T m) { return fma((double)b01, m, acc); }
+  static __device__ T msub(T acc, uint32_t b01, T m) { return fma(-(double)b01, m, acc); }
+  static __device__ T max(T a, T b) { return max_f64(a, b); }
+  static __device__ T lowest() { return -INFINITY; }
+  static __device__ T stage_peak(T U0, T Y, T m) { return U0 - Y + m; }
+  static __device__ T seg_max(T a, T b) { return fmax(a, b); }
+  static __device__ int64_t i64(T x) { return (int64_t)x; }
+};
+template <> struct Ar<true> {
+  using T = int64_t;
+  static __device__ T of(uint32_t lo, uint32_t hi) { return (int64_t)(((uint64_t)hi << 32) | lo); }
+  static __device__ T of_i(int64_t x) { return x; }
+  static __device__ T madd(T acc, uint32_t b01, T m) { return acc + (m & -(int64_t)b01); }
+  static __device__ T msub(T acc, uint32_t b01, T m) { return acc - (m & -(int64_t)b01); }
+  static __device__ T max(T a, T b) { return a > b ? a : b; }
+  static __device__ T lowest() { return INT64_MIN; }
+  static __device__ T stage_peak(T U0, T Y, T m) { return (int64_t)((uint64_t)U0 - (uint64_t)Y + (uint64_t)m); }
+  static __device__ T seg_max(T a, T b) { return a > b ? a : b; }
+  static __device__ int64_t i64(T x) { return x; }
+};
+
 
 // A node record spread over the lanes of one vector register: lane L holds
 // dword L. Fields are moved to scalar registers when used
@@ -264,16 +303,20 @@ struct RecRegs {
   uint32_t w;
   uint4 mc, dm;  // M_v, C_v and the M of slots 0-1, in every lane
   __device__ uint32_t get(int i) const { return __builtin_amdgcn_readlane(w, i); }
-  __device__ double M() const { return dbl(mc.x, mc.y); }
-  __device__ double C() const { return dbl(mc.z, mc.w); }
-  __device__ double dM01(int s) const { return s == 0 ? dbl(dm.x, dm.y) : dbl(dm.z, dm.w); }
+  template <bool W> __device__ typename Ar<W>::T M() const { return Ar<W>::of(mc.x, mc.y); }
+  template <bool W> __device__ typename Ar<W>::T C() const { return Ar<W>::of(mc.z, mc.w); }
+  template <bool W> __device__ typename Ar<W>::T dM01(int s) const {
+    return s == 0 ? Ar<W>::of(dm.x, dm.y) : Ar<W>::of(dm.z, dm.w);
+  }
   __device__ uint32_t umask() const { return get(kDwUmask); }
   __device__ uint32_t refs0() const { return get(kDwRefs0); }
   __device__ uint32_t refs1() const { return get(kDwRefs1); }
   __device__ uint32_t bits0() const { return get(kDwBits0); }
   __device__ uint32_t lm(int s) const { return get(kDwLm + s); }
   __device__ uint32_t refs2() const { return get(kDwRefs2); }
-  __device__ double dM(int s) const { return dbl(get(kDwDM + 2 * s), get(kDwDM + 1 + 2 * s)); }
+  template <bool W> __device__ typename Ar<W>::T dM(int s) const {
+    return Ar<W>::of(get(kDwDM + 2 * s), get(kDwDM + 1 + 2 * s));
+  }
 };
 
 // Bit position k of a record (0: fu; 1 + 2s: s1 of slot s; 2 + 2s: fl of
@@ -320,10 +363,10 @@ struct EvalArgs {
   int32_t items, kind, P, T0, R1, R2;   // work plan (see Plan)
   uint32_t key0, key1;
   uint32_t det0;                 // CKM_F_DET0 given
-  double base;                   // M_in + 2 M_param
+  int64_t base;                  // M_in + 2 M_param
   cptr<uint32_t> q;
   cptr<uint32_t> det;
-  cptr<double> M;
+  cptr<int64_t> M;
   cptr<int32_t> user_ptr;
   cptr<int32_t> user_idx;
   cptr<int32_t> dep_ptr;
@@ -612,8 +655,9 @@ __device__ __forceinline__ uint32_t r_bit(int u, int v, uint32_t Rwin, Row A) {
 }
 
 // Running state of the right-to-left scan of one stage (per lane).
+template <typename T>
 struct Scan {
-  double U0, Y, maxv, cost;
+  T U0, Y, maxv, cost;
   uint32_t Rwin;       // R bits of the 32 nodes above the current node
   uint32_t w0, w1;     // S_t and S_{t+1} words of the current chunk
 };
@@ -663,14 +707,6 @@ __device__ __forceinline__ void issue_reads(uint32_t w, Row A, RowB& B, LdsVals<
   }
 }
 
-// max(a, b) for values that are never NaN, without the quieting step that
-// fmax adds on a loop-carried operand.
-__device__ __forceinline__ double max_f64(double a, double b) {
-  double d;
-  asm("v_max_f64 %0, %1, %2" : "=v"(d) : "v"(a), "v"(b));
-  return d;
-}
-
 // One node v of stage t. Algorithm 2's repair runs right to left (reverse
 // topological order), so every user of v is decided before v: v is computed
 // iff it is node t (constraint 4a), or it is not checkpointed and is kept
@@ -684,20 +720,22 @@ __device__ __forceinline__ double max_f64(double a, double b) {
 // S_{t+1}. Rows are zero beyond their last word, so a reference to a node
 // above t (or to node n, "none") reads 0. kFirst: v == t, which is always
 // computed and has no computed user in the stage.
-template <bool kFirst, int kSlots, typename RowB>
+template <bool kWide, bool kFirst, int kSlots, typename RowB>
 __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const RecRegs& rec, const LdsVals<kSlots>& L,
-                                          Scan& sc, Row A, RowB& B) {
+                                          Scan<typename Ar<kWide>::T>& sc, Row A, RowB& B) {
+  using AR = Ar<kWide>;
+  using T = typename AR::T;
   const int jj = v & 31;
   const uint32_t s0 = bit(sc.w0, jj);
   const uint32_t s1 = bit(sc.w1, jj);
   // the node's scalar fields, read together
   const uint32_t um = rec.umask(), b0 = rec.bits0();
   pin_s(um, b0, b0);
-  const double Mv = rec.M();
-  const double Cv = rec.C();
+  const T Mv = rec.template M<kWide>();
+  const T Cv = rec.template C<kWide>();
   uint32_t anyU, r;
   // val = Y + freed_v, accumulated in place (exact integers: any order)
-  double val = sc.Y;
+  T val = sc.Y;
   // deps 0-2 from bits0; 3 means "read refs1" (3 or 4 deps, or a slow node)
   uint32_t nd = b0 >> 30, r1 = 0;
   if (__builtin_expect(nd == 3u, 0)) {
@@ -718,23 +756,23 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
     // FREE(t,v,v): v computed, not kept, no computed user after it. A node
     // other than t is computed only because it is kept (s1) or used (anyU),
     // so only node t can be freed right after it is computed.
-    if (kFirst) val = fma((double)(~s1 & 1u), Mv, val);
+    if (kFirst) val = AR::madd(val, ~s1 & 1u, Mv);
     auto slot = [&](int sl, uint32_t flw, uint32_t s1w) {
       const uint32_t lm = rec.lm(sl);
-      double dMs;
+      T dMs;
       if (sl < 2) {
-        dMs = rec.dM01(sl);
+        dMs = rec.template dM01<kWide>(sl);
       } else {
         const uint32_t d_lo = rec.get(kDwDM + 2 * sl), d_hi = rec.get(kDwDM + 1 + 2 * sl);
         pin_s(d_lo, d_hi, d_hi);
-        dMs = dbl(d_lo, d_hi);
+        dMs = AR::of(d_lo, d_hi);
       }
       const uint32_t far = __builtin_amdgcn_ubfe(flw, bitpos(b0, r1, 2 + 2 * sl), 1);
       uint32_t later = and_or(sc.Rwin, lm, far);
       later = umin1(later);
       // r and later are 0 or 1: no mask needed
       const uint32_t fr = r & ~__builtin_amdgcn_ubfe(s1w, bitpos(b0, r1, 1 + 2 * sl), 1) & ~later;
-      val = fma((double)fr, dMs, val);
+      val = AR::madd(val, fr, dMs);
     };
     // most nodes have one or two dependencies
     if (__builtin_expect(nd >= 1, 1)) slot(0, L.fl[0], L.s1[0]);
@@ -763,7 +801,7 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
     if (kFirst) {
       anyU = 0;
       r = 1;
-      val = fma((double)(~s1 & 1u), Mv, val);
+      val = AR::madd(val, ~s1 & 1u, Mv);
     } else {
       uint32_t acc = sc.Rwin & um;
       for (uint32_t f = 0; f < nfar; ++f) {
@@ -776,7 +814,7 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
     for (uint32_t d = 0; d < nds; ++d) {
       const int b = ext_slot((int)d);
       const uint32_t lm = rec.get(b);
-      const double dMs = dbl(rec.get(b + 1), rec.get(b + 2));
+      const T dMs = AR::of(rec.get(b + 1), rec.get(b + 2));
       const uint32_t x = rec.get(b + 3);
       const uint32_t i = x & 0xFFFFu, nl = x >> 16;
       uint32_t later = sc.Rwin & lm;
@@ -786,7 +824,7 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
       }
       later = umin1(later);
       const uint32_t fr = r & ~bit(B.at_word(i >> 5), i & 31) & ~later & 1u;
-      val = fma((double)fr, dMs, val);
+      val = AR::madd(val, fr, dMs);
     }
   } else {
     // nodes outside both formats: walk the CSR lists
@@ -798,7 +836,7 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
       anyU |= r_bit(u, v, sc.Rwin, A);
     }
     r = ((s1 | anyU) & ~s0 & 1u) | (uint32_t)kFirst;
-    val = fma((double)(r & ~s1 & ~anyU & 1u), Mv, val);
+    val = AR::madd(val, r & ~s1 & ~anyU & 1u, Mv);
     const int de = a.dep_ptr[v + 1];
     for (int e = a.dep_ptr[v]; e < de; ++e) {
       const int i = a.dep_idx[e];
@@ -810,18 +848,17 @@ __device__ __forceinline__ void scan_node(const EvalArgs& a, int t, int v, const
         later |= r_bit(u, v, sc.Rwin, A);
       }
       const uint32_t fr = r & ~bit(B.word(i >> 5), i & 31) & ~later & 1u;
-      val = fma((double)fr, a.M[i], val);
+      val = AR::madd(val, fr, AR::of_i(a.M[i]));
     }
   }
-  const double rd = (double)r;
-  sc.cost = fma(rd, Cv, sc.cost);
-  sc.U0 = fma((double)s0, Mv, sc.U0);
+  sc.cost = AR::madd(sc.cost, r, Cv);
+  sc.U0 = AR::madd(sc.U0, s0, Mv);
   // Keep both sums here: left free, the compiler sinks them to the end of
   // the unrolled loop, which keeps a fourth record buffer alive and adds
   // register copies to every iteration.
   asm volatile("" : "+v"(sc.cost), "+v"(sc.U0));
-  sc.maxv = max_f64(sc.maxv, val);
-  sc.Y = fma(-rd, Mv, val);
+  sc.maxv = AR::max(sc.maxv, val);
+  sc.Y = AR::msub(val, r, Mv);
   // slide the window down by one node: bit 0 becomes node v
   sc.Rwin = (sc.Rwin << 1) | r;
   if (__builtin_expect(jj == 0, 0)) {  // chunk finished: R_t replaces S_t, move to the next chunk
@@ -860,9 +897,10 @@ template <> struct PipeShape<RowReg> { static constexpr int kFAhead = 1, kSlots 
 // fp64 groups rotate through four buffers (two for the groups one node
 // ahead), LDS words through two, so registers never move within a turn of
 // the 4-node unrolled loop.
-template <int CW, bool kFirst, typename RowB>
+template <bool kWide, int CW, bool kFirst, typename RowB>
 __device__ __forceinline__ void pipe_step(const EvalArgs& a, int t, int v, uint32_t (&rw)[4], RecF (&rf)[4],
-                                          LdsVals<PipeShape<RowB>::kSlots> (&lb)[2], Scan& sc, Row A, RowB& B) {
+                                          LdsVals<PipeShape<RowB>::kSlots> (&lb)[2],
+                                          Scan<typename Ar<kWide>::T>& sc, Row A, RowB& B) {
   constexpr int kFA = PipeShape<RowB>::kFAhead;
   constexpr int NW = (CW + 1) & 3, FW = (CW + 2) & 3;
   constexpr int CF = kFA == 1 ? (CW & 1) : CW;
@@ -876,20 +914,21 @@ __device__ __forceinline__ void pipe_step(const EvalArgs& a, int t, int v, uint3
   rec.w = rw[CW];
   rec.mc = rf[CF].mc;
   rec.dm = rf[CF].dm;
-  scan_node<kFirst>(a, t, v, rec, lb[LC], sc, A, B);
+  scan_node<kWide, kFirst>(a, t, v, rec, lb[LC], sc, A, B);
 }
 
 // One stage t of one candidate (per lane): S_t in A, S_{t+1} in B on entry,
 // R_t in A on exit.
-template <typename RowB>
-__device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, RowB& B, double& stage_peak,
-                                           double& stage_cost) {
+template <bool kWide, typename RowB>
+__device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, RowB& B, typename Ar<kWide>::T& stage_peak,
+                                           typename Ar<kWide>::T& stage_cost) {
+  using AR = Ar<kWide>;
   constexpr int kFA = PipeShape<RowB>::kFAhead;
-  Scan sc;
-  sc.U0 = a.base;
-  sc.Y = 0.0;
-  sc.maxv = -INFINITY;
-  sc.cost = 0.0;
+  Scan<typename AR::T> sc;
+  sc.U0 = AR::of_i(a.base);
+  sc.Y = 0;
+  sc.maxv = AR::lowest();
+  sc.cost = 0;
   sc.Rwin = 0;
   sc.w0 = A.word(t >> 5);
   sc.w1 = B.word(t >> 5);
@@ -902,17 +941,17 @@ __device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, RowB
   if (kFA == 2) load_rec_f(rf[1], rec_rsrc(a), max(t - 1, 0));
   issue_reads(rw[0], A, B, lb[0]);
   int v = t;
-  pipe_step<0, true>(a, t, v, rw, rf, lb, sc, A, B);
+  pipe_step<kWide, 0, true>(a, t, v, rw, rf, lb, sc, A, B);
   const int groups = __builtin_amdgcn_readfirstlane(t / 4);
   for (int g = 0; g < groups; ++g) {
-    pipe_step<1, false>(a, t, --v, rw, rf, lb, sc, A, B);
-    pipe_step<2, false>(a, t, --v, rw, rf, lb, sc, A, B);
-    pipe_step<3, false>(a, t, --v, rw, rf, lb, sc, A, B);
-    pipe_step<0, false>(a, t, --v, rw, rf, lb, sc, A, B);
+    pipe_step<kWide, 1, false>(a, t, --v, rw, rf, lb, sc, A, B);
+    pipe_step<kWide, 2, false>(a, t, --v, rw, rf, lb, sc, A, B);
+    pipe_step<kWide, 3, false>(a, t, --v, rw, rf, lb, sc, A, B);
+    pipe_step<kWide, 0, false>(a, t, --v, rw, rf, lb, sc, A, B);
   }
-  if (v >= 1) pipe_step<1, false>(a, t, --v, rw, rf, lb, sc, A, B);
-  if (v >= 1) pipe_step<2, false>(a, t, --v, rw, rf, lb, sc, A, B);
-  if (v >= 1) pipe_step<3, false>(a, t, --v, rw, rf, lb, sc, A, B);
+  if (v >= 1) pipe_step<kWide, 1, false>(a, t, --v, rw, rf, lb, sc, A, B);
+  if (v >= 1) pipe_step<kWide, 2, false>(a, t, --v, rw, rf, lb, sc, A, B);
+  if (v >= 1) pipe_step<kWide, 3, false>(a, t, --v, rw, rf, lb, sc, A, B);
   // prefetches past node 0 are never read: retire them inside the stage
   settle_w(rw[0]);
   settle_w(rw[1]);
@@ -924,7 +963,7 @@ __device__ __forceinline__ void eval_stage(const EvalArgs& a, int t, Row A, RowB
     settle_f(rf[2]);
     settle_f(rf[3]);
   }
-  stage_peak = sc.U0 - sc.Y + sc.maxv;
+  stage_peak = AR::stage_peak(sc.U0, sc.Y, sc.maxv);
   stage_cost = sc.cost;
 }
 
@@ -957,17 +996,18 @@ __device__ __forceinline__ void next_stage(Row& A, RowRegV<kVecs>& B, int t) {
 }
 
 // The stages t0 .. t1-1 of one work item: fold each stage's peak and cost.
-template <int kSrc, typename RowB>
+template <bool kWide, int kSrc, typename RowB>
 __device__ __forceinline__ void run_item(const EvalArgs& a, int t0, int t1, uint32_t k, bool det_lane, uint32_t rk,
-                                         Row& A, RowB& B, double& seg_peak, int64_t& seg_cost) {
+                                         Row& A, RowB& B, typename Ar<kWide>::T& seg_peak, int64_t& seg_cost) {
+  using AR = Ar<kWide>;
   if (t0 >= t1) return;
   gen_row<kSrc>(a, t0, k, det_lane, rk, A);
   for (int t = t0; t < t1; ++t) {
     gen_row<kSrc>(a, t + 1, k, det_lane, rk, B);
-    double sp, sc;
-    eval_stage(a, t, A, B, sp, sc);
-    seg_peak = fmax(seg_peak, sp);
-    seg_cost += (int64_t)sc;
+    typename AR::T sp, sc;
+    eval_stage<kWide>(a, t, A, B, sp, sc);
+    seg_peak = AR::seg_max(seg_peak, sp);
+    seg_cost += AR::i64(sc);
     if (a.rrows) {  // R_t, now in A, kept for the best-candidate output
       uint32_t* dst = a.rrows + row_base(t) * (size_t)a.kpad + k;
       for (int w = 0; w <= (t >> 5); ++w) dst[(size_t)w * a.kpad] = A.word(w);
@@ -982,9 +1022,10 @@ __device__ __forceinline__ void run_item(const EvalArgs& a, int t0, int t1, uint
 // the end of each stage, which halves the LDS a wave needs; 0 when both rows
 // are in LDS and swap roles. kSrc: where the S rows come from (kSrcRound,
 // kSrcUser, kSrcThreshold).
-template <int kRegW, int kSrc>
+template <int kRegW, int kSrc, bool kWide = false>
 __global__ void __launch_bounds__(kWave, kRegW == kRegRowWords ? 5 : 1)
 ckm_eval_kernel(EvalArgs a) {
+  using AR = Ar<kWide>;
   extern __shared__ uint32_t lds[];
   const int lane = threadIdx.x;
   const int group = blockIdx.x;
@@ -1000,25 +1041,25 @@ ckm_eval_kernel(EvalArgs a) {
 
   int t0, t1;
   item_range(a, item, t0, t1);
-  double seg_peak = -INFINITY;
+  typename AR::T seg_peak = AR::lowest();
   int64_t seg_cost = 0;
   if constexpr (kRegW == 0) {
     Row B{wave_lds + (size_t)a.row_words * 256 + 4 * lane};
     for (int w = 0; w < a.row_words; ++w) B.word(w) = 0u;
-    run_item<kSrc>(a, t0, t1, k, det_lane, rk, A, B, seg_peak, seg_cost);
+    run_item<kWide, kSrc>(a, t0, t1, k, det_lane, rk, A, B, seg_peak, seg_cost);
   } else if constexpr (kRegW == kRegRowWords) {
     RowReg B;
     B.w = (u32x32)0u;
-    run_item<kSrc>(a, t0, t1, k, det_lane, rk, A, B, seg_peak, seg_cost);
+    run_item<kWide, kSrc>(a, t0, t1, k, det_lane, rk, A, B, seg_peak, seg_cost);
   } else {
     u32x32 b0 = (u32x32)0u, b1 = (u32x32)0u, b2 = (u32x32)0u, b3 = (u32x32)0u;
     RowRegV<kRegW / 32> B{b0, b1, b2, b3};
-    run_item<kSrc>(a, t0, t1, k, det_lane, rk, A, B, seg_peak, seg_cost);
+    run_item<kWide, kSrc>(a, t0, t1, k, det_lane, rk, A, B, seg_peak, seg_cost);
   }
   // fold the item's result into the candidate's totals: max of the stage
   // peaks, sum of the stage costs (exact integers, any order)
   if ((int)k < a.K && t0 < t1) {
-    atomicMax(reinterpret_cast<long long*>(a.part_peak) + k, (long long)seg_peak);
+    atomicMax(reinterpret_cast<long long*>(a.part_peak) + k, (long long)AR::i64(seg_peak));
     atomicAdd(reinterpret_cast<unsigned long long*>(a.part_cost) + k, (unsigned long long)seg_cost);
   }
   if (group == 0 && item == 0 && lane == 0) a.hdr[0] = a.items;
@@ -1539,7 +1580,15 @@ static void (*eval_kernel_w(int w))(EvalArgs) {
   }
 }
 
-static void (*eval_kernel_for(int32_t words, int src))(EvalArgs) {
+// Wide graphs (int64 sums) use the LDS-row variant only: they are rare, and
+// one variant per row source keeps the library small.
+static void (*eval_kernel_for(int32_t words, int src, bool wide))(EvalArgs) {
+  if (wide) {
+    if (src == kSrcRows) return ckm_eval_kernel<0, kSrcRows, true>;
+    if (src == kSrcUser) return ckm_eval_kernel<0, kSrcUser, true>;
+    if (src == kSrcThreshold) return ckm_eval_kernel<0, kSrcThreshold, true>;
+    return ckm_eval_kernel<0, kSrcRound, true>;
+  }
   const int w = reg_row_width(words);
   if (src == kSrcRows) return eval_kernel_w<kSrcRows>(w);
   if (src == kSrcUser) return eval_kernel_w<kSrcUser>(w);
@@ -1547,14 +1596,14 @@ static void (*eval_kernel_for(int32_t words, int src))(EvalArgs) {
   return eval_kernel_w<kSrcRound>(w);
 }
 
-static size_t eval_lds_bytes(int32_t words) {
-  return (reg_row_width(words) ? 1u : 2u) * (size_t)words * kWave * sizeof(uint32_t);
+static size_t eval_lds_bytes(int32_t words, bool wide) {
+  return (!wide && reg_row_width(words) ? 1u : 2u) * (size_t)words * kWave * sizeof(uint32_t);
 }
 
-int32_t eval_waves_per_cu(int32_t n) {
+int32_t eval_waves_per_cu(int32_t n, bool wide) {
   const int32_t words = (n >> 5) + 1;
-  const void* fn = (const void*)eval_kernel_for(words, kSrcRound);
-  const size_t lds = eval_lds_bytes(words);
+  const void* fn = (const void*)eval_kernel_for(words, kSrcRound, wide);
+  const size_t lds = eval_lds_bytes(words, wide);
   if (lds > 65536) (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   int blocks = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, fn, kWave, lds) != hipSuccess || blocks < 1) blocks = 1;
@@ -1633,8 +1682,8 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   a.part_cost = at<int64_t>(work, L.part_cost_off);
   a.hdr = at<int32_t>(work, L.hdr_off);
   const int groups = (K + kWave - 1) / kWave;
-  void (*fn)(EvalArgs) = eval_kernel_for(a.row_words, src);
-  const size_t lds_bytes = eval_lds_bytes(a.row_words);
+  void (*fn)(EvalArgs) = eval_kernel_for(a.row_words, src, g.wide);
+  const size_t lds_bytes = eval_lds_bytes(a.row_words, g.wide);
   if (lds_bytes > 65536) {
     hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
     if (e != hipSuccess) return e;
@@ -1672,7 +1721,7 @@ hipError_t launch_max_batch(const ckm_graph& g, const Layout& L, int32_t K, int6
                             char* work, hipStream_t stream) {
   const int rb = L.reduce_blocks;
   hipLaunchKernelGGL(ckm_batch_kernel, dim3(rb), dim3(256), 0, stream, K, at<const int64_t>(work, L.part_peak_off),
-                     at<const int64_t>(work, L.part_cost_off), (int64_t)g.base, budget, cost_cap, d_batch,
+                     at<const int64_t>(work, L.part_cost_off), g.base, budget, cost_cap, d_batch,
                      at<BestB>(work, L.bbest_off));
   hipLaunchKernelGGL(ckm_batch_argmax_kernel, dim3(1), dim3(256), 0, stream, rb, at<const BestB>(work, L.bbest_off),
                      g.n, at<const int32_t>(work, L.nan_off), d_best_k, d_best_batch, d_status);
@@ -1734,7 +1783,16 @@ hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_
 // ---------------------------------------------------------------------------
 // The second form of slow node v's lists (see kDwExt) into the record's
 // dwords, or false when v exceeds its counts.
-static bool build_ext_lists(int32_t v, const double* M, const int32_t* dep_ptr, const int32_t* dep_idx,
+// A size or cost in the record's form: binary64, or int64 for a wide graph.
+static uint64_t rec_value(int64_t x, bool wide) {
+  if (wide) return (uint64_t)x;
+  const double d = (double)x;
+  uint64_t bits;
+  memcpy(&bits, &d, sizeof(bits));
+  return bits;
+}
+
+static bool build_ext_lists(int32_t v, const int64_t* M, bool wide, const int32_t* dep_ptr, const int32_t* dep_idx,
                             const int32_t* user_ptr, const int32_t* user_idx, uint32_t dw[64]) {
   auto put16 = [&](int at, int f, uint32_t node) { dw[at + f / 2] |= node << (16 * (f & 1)); };
   int nfar = 0;
@@ -1761,8 +1819,7 @@ static bool build_ext_lists(int32_t v, const double* M, const int32_t* dep_ptr, 
         put16(b + 4, nl++, (uint32_t)u);
       }
     }
-    uint64_t mbits;
-    memcpy(&mbits, &M[i], sizeof(mbits));
+    const uint64_t mbits = rec_value(M[i], wide);
     dw[b] = lm;
     dw[b + 1] = (uint32_t)mbits;
     dw[b + 2] = (uint32_t)(mbits >> 32);
@@ -1772,15 +1829,15 @@ static bool build_ext_lists(int32_t v, const double* M, const int32_t* dep_ptr, 
   return true;
 }
 
-void build_node_records(int32_t n, const double* M, const double* C, const int32_t* dep_ptr,
+void build_node_records(int32_t n, const int64_t* M, const int64_t* C, bool wide, const int32_t* dep_ptr,
                         const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx,
                         void* out) {
   NodeRec* recs = static_cast<NodeRec*>(out);
   for (int32_t v = 0; v < n; ++v) {
     NodeRec r;
     memset(&r, 0, sizeof(r));
-    r.M = M[v];
-    r.C = C[v];
+    r.M = rec_value(M[v], wide);
+    r.C = rec_value(C[v], wide);
     // references, node n for "none": fu, then per slot s1 and fl
     int ref[1 + 2 * kRecDeps];
     for (int k = 0; k < 1 + 2 * kRecDeps; ++k) ref[k] = n;
@@ -1798,7 +1855,7 @@ void build_node_records(int32_t n, const double* M, const double* C, const int32
     for (int sl = 0; sl < nd && !slow; ++sl) {
       const int i = dep_idx[dep_ptr[v] + sl];
       ref[1 + 2 * sl] = i;
-      r.dM[sl] = M[i];
+      r.dM[sl] = rec_value(M[i], wide);
       int nlate = 0;
       for (int32_t e = user_ptr[i]; e < user_ptr[i + 1]; ++e) {
         const int u = user_idx[e];
@@ -1829,7 +1886,7 @@ void build_node_records(int32_t n, const double* M, const double* C, const int32
       memcpy(dw, &r, sizeof(dw));
       for (int k = 0; k < 64; ++k)
         if ((k < 4 || k >= 8) && (k < 24 || k >= 32)) dw[k] = 0;
-      if (build_ext_lists(v, M, dep_ptr, dep_idx, user_ptr, user_idx, dw)) memcpy(&r, dw, sizeof(dw));
+      if (build_ext_lists(v, M, wide, dep_ptr, dep_idx, user_ptr, user_idx, dw)) memcpy(&r, dw, sizeof(dw));
     }
     recs[v] = r;
   }

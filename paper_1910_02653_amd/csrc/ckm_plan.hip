@@ -56,24 +56,11 @@ __device__ __forceinline__ int64_t wave_sum_i64(int64_t x) {
   for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
   return x;
 }
-__device__ __forceinline__ double wave_sum_f64(double x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-  return x;
-}
 // Inclusive prefix sums over the lanes of the wave.
 __device__ __forceinline__ int64_t wave_scan_i64(int64_t x, int lane) {
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     const int64_t y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  return x;
-}
-__device__ __forceinline__ double wave_scan_f64(double x, int lane) {
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const double y = __shfl_up(x, o);
     if (lane >= o) x += y;
   }
   return x;
@@ -191,7 +178,7 @@ struct PlanArgs {
   int32_t n, rw;
   int32_t early;
   int32_t rtw;                       // words per column of RT: ceil(n / 32)
-  double base;                       // M_in + 2 M_param
+  int64_t base;                      // M_in + 2 M_param
   const uint32_t* S;
   const uint32_t* R;
   const uint32_t* RT;                // R transposed: bit s of RT[i] = R[s][i]
@@ -200,7 +187,7 @@ struct PlanArgs {
   const int32_t* dep_idx;
   const int32_t* user_ptr;
   const int32_t* user_idx;
-  const double* M;
+  const int64_t* M;
   const int64_t* off;
   const int64_t* rbase;
   const int32_t* go;
@@ -210,7 +197,7 @@ struct PlanArgs {
 };
 
 __device__ __forceinline__ void put_stmt(const PlanArgs& a, int64_t s, int op, int node, int64_t reg, int t,
-                                         double mem_after) {
+                                         int64_t mem_after) {
   // positions come from the count kernel's totals, which the scan checked
   // against the capacity; the guard keeps every store inside the buffers
   if (s < 0 || s >= a.capacity) return;
@@ -219,7 +206,7 @@ __device__ __forceinline__ void put_stmt(const PlanArgs& a, int64_t s, int op, i
   p[1] = node;
   p[2] = (int32_t)reg;
   p[3] = t;
-  if (a.mem) a.mem[s] = (int64_t)mem_after;
+  if (a.mem) a.mem[s] = mem_after;
 }
 
 // Register of value i live in stage t: computed in this stage, or else kept
@@ -266,18 +253,18 @@ constexpr int kMaxChunks = CKM_MAX_NODES / kPlanWave;
 //      totals;
 //   3. one wave: offsets of every 64-node group (positions and memory);
 //   4. every wave writes the statements of its groups.
-// Dynamic LDS: n doubles (memory change), then n + n int32 (free point,
+// Dynamic LDS: n int64 (memory change), then n + n int32 (free point,
 // statement count).
 template <int kEmitWaves>
 __global__ void __launch_bounds__(kEmitWaves * kPlanWave) ckm_plan_emit_kernel(PlanArgs a) {
   constexpr int kEmitThreads = kEmitWaves * kPlanWave;
-  extern __shared__ double dyn[];
+  extern __shared__ int64_t dyn[];
   __shared__ uint32_t st_l[kMaxNodesWords], rt_l[kMaxNodesWords], sn_l[kMaxNodesWords];
   __shared__ int32_t wpre[kMaxNodesWords];
   __shared__ int64_t ch_cnt[kMaxChunks], uc_cnt[kMaxChunks];
-  __shared__ double ch_mem[kMaxChunks], uc_mem[kMaxChunks];
-  __shared__ double kept_part[kEmitWaves];
-  double* cmem = dyn;
+  __shared__ int64_t ch_mem[kMaxChunks], uc_mem[kMaxChunks];
+  __shared__ int64_t kept_part[kEmitWaves];
+  int64_t* cmem = dyn;
   int32_t* fpt = reinterpret_cast<int32_t*>(dyn + a.n);
   int32_t* ccnt = fpt + a.n;
   const int t = a.n - 1 - (int)blockIdx.x;
@@ -304,11 +291,11 @@ __global__ void __launch_bounds__(kEmitWaves * kPlanWave) ckm_plan_emit_kernel(P
     }
   }
   // 1. free points; wave w owns the 64-node groups w, w + 4, ...
-  double kept_bytes = 0.0;
+  int64_t kept_bytes = 0;
   for (int c = wave; c < nc; c += kEmitWaves) {
     const int i = 64 * c + lane;
     int f = kFreeNone;
-    double mi = 0.0;
+    int64_t mi = 0;
     if (i <= t) {
       const uint32_t si = bit_of(st_l[i >> 5], i), ri = bit_of(rt_l[i >> 5], i);
       mi = a.M[i];
@@ -326,21 +313,21 @@ __global__ void __launch_bounds__(kEmitWaves * kPlanWave) ckm_plan_emit_kernel(P
       if (si) kept_bytes += mi;
     }
     const bool un = f == kFreeUnused;
-    const double su = wave_sum_f64(un ? -mi : 0.0);
+    const int64_t su = wave_sum_i64(un ? -mi : 0);
     const uint64_t um = __ballot(un);
     if (lane == 0) {
       uc_cnt[c] = __popcll(um);
       uc_mem[c] = su;
     }
   }
-  kept_bytes = wave_sum_f64(kept_bytes);
+  kept_bytes = wave_sum_i64(kept_bytes);
   if (lane == 0) kept_part[wave] = kept_bytes;
   __syncthreads();
   // 2. per node: statements and memory change
   for (int c = wave; c < nc; c += kEmitWaves) {
     const int k = 64 * c + lane;
     int64_t cn = 0;
-    double d = 0.0;
+    int64_t d = 0;
     if (k <= t) {
       if (bit_of(rt_l[k >> 5], k)) {
         cn = 1;
@@ -361,7 +348,7 @@ __global__ void __launch_bounds__(kEmitWaves * kPlanWave) ckm_plan_emit_kernel(P
       cmem[k] = d;
     }
     cn = wave_sum_i64(cn);
-    d = wave_sum_f64(d);
+    d = wave_sum_i64(d);
     if (lane == 0) {
       ch_cnt[c] = cn;
       ch_mem[c] = d;
@@ -370,18 +357,18 @@ __global__ void __launch_bounds__(kEmitWaves * kPlanWave) ckm_plan_emit_kernel(P
   __syncthreads();
   // 3. offsets of the groups (nc <= 64: one wave)
   if (wave == 0) {
-    double u0 = a.base;
+    int64_t u0 = a.base;
     for (int w = 0; w < kEmitWaves; ++w) u0 += kept_part[w];
     const bool in = lane < nc;
     const int64_t cn = in ? ch_cnt[lane] : 0, un = in ? uc_cnt[lane] : 0;
-    const double dm = in ? ch_mem[lane] : 0.0, um = in ? uc_mem[lane] : 0.0;
+    const int64_t dm = in ? ch_mem[lane] : 0, um = in ? uc_mem[lane] : 0;
     const int64_t cn_inc = wave_scan_i64(cn, lane), un_inc = wave_scan_i64(un, lane);
-    const double dm_inc = wave_scan_f64(dm, lane), um_inc = wave_scan_f64(um, lane);
+    const int64_t dm_inc = wave_scan_i64(dm, lane), um_inc = wave_scan_i64(um, lane);
     const int64_t node_total = __shfl(cn_inc, kPlanWave - 1), un_total = __shfl(un_inc, kPlanWave - 1);
-    const double node_mem = __shfl(dm_inc, kPlanWave - 1), un_mem = __shfl(um_inc, kPlanWave - 1);
+    const int64_t node_mem = __shfl(dm_inc, kPlanWave - 1), un_mem = __shfl(um_inc, kPlanWave - 1);
     const int64_t o = a.off[t];
     int64_t node_pos = o, un_pos = o + node_total;
-    double node_mb = u0, un_mb = u0 + node_mem;
+    int64_t node_mb = u0, un_mb = u0 + node_mem;
     if (a.early) {
       un_pos = o;
       un_mb = u0;
@@ -401,11 +388,11 @@ __global__ void __launch_bounds__(kEmitWaves * kPlanWave) ckm_plan_emit_kernel(P
     const int k = 64 * c + lane;
     const bool in = k <= t;
     const int64_t cn = in ? ccnt[k] : 0;
-    const double d = in ? cmem[k] : 0.0;
+    const int64_t d = in ? cmem[k] : 0;
     const int64_t cinc = wave_scan_i64(cn, lane);
-    const double dinc = wave_scan_f64(d, lane);
+    const int64_t dinc = wave_scan_i64(d, lane);
     int64_t s = ch_cnt[c] + cinc - cn;
-    double mu = ch_mem[c] + dinc - d;   // memory before node k's statements
+    int64_t mu = ch_mem[c] + dinc - d;   // memory before node k's statements
     if (cn) {
       if (bit_of(rt_l[k >> 5], k)) {
         mu += a.M[k];
@@ -428,8 +415,8 @@ __global__ void __launch_bounds__(kEmitWaves * kPlanWave) ckm_plan_emit_kernel(P
     const bool un = in && fpt[k] == kFreeUnused;
     const uint64_t um = __ballot(un);
     if (um) {
-      const double du = un ? -a.M[k] : 0.0;
-      const double uinc = wave_scan_f64(du, lane);
+      const int64_t du = un ? -a.M[k] : 0;
+      const int64_t uinc = wave_scan_i64(du, lane);
       if (un)
         put_stmt(a, uc_cnt[c] + __popcll(um & ((1ull << lane) - 1ull)), 1, k, reg_of(a, t, k, rt_l, wpre), t,
                  uc_mem[c] + uinc);
@@ -485,7 +472,7 @@ hipError_t launch_plan(const ckm_graph& g, const Layout& L, const uint64_t* d_S,
     a.P = d_P;
     a.mem = d_mem;
     a.capacity = capacity;
-    const size_t lds = (size_t)g.n * (sizeof(double) + 2 * sizeof(int32_t));
+    const size_t lds = (size_t)g.n * (sizeof(int64_t) + 2 * sizeof(int32_t));
     const bool wide = g.n > 1024;
     void (*fn)(PlanArgs) = wide ? ckm_plan_emit_kernel<16> : ckm_plan_emit_kernel<4>;
     hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

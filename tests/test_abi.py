@@ -71,16 +71,35 @@ def create(n, deps, cost=None, size=None, m_input=0, m_param=0, users=None):
     (dict(n=2, deps=[[], [0]], cost=[1, -1]), ckm.E_INVALID_ARG),
     (dict(n=2, deps=[[], [0]], size=[-5, 1]), ckm.E_INVALID_ARG),
     (dict(n=2, deps=[[], [0]], m_param=-1), ckm.E_INVALID_ARG),
-    (dict(n=2, deps=[[], [0]], size=[2 ** 52, 2 ** 52]), ckm.E_OVERFLOW),      # sum M reaches 2^53
-    (dict(n=2, deps=[[], [0]], size=[1, 1], m_param=2 ** 52), ckm.E_OVERFLOW),
-    (dict(n=2, deps=[[], [0]], cost=[2 ** 53 - 1, 1]), ckm.E_OVERFLOW),
+    (dict(n=2, deps=[[], [0]], size=[2 ** 62, 2 ** 62]), ckm.E_OVERFLOW),      # sum M past INT64_MAX
+    (dict(n=2, deps=[[], [0]], size=[2 ** 62 - 1, 2 ** 62 - 1], m_input=2), ckm.E_OVERFLOW),
+    (dict(n=2, deps=[[], [0]], size=[1, 1], m_param=2 ** 62), ckm.E_OVERFLOW),  # 2 M_param
+    (dict(n=2, deps=[[], [0]], cost=[2 ** 63 - 1, 1]), ckm.E_OVERFLOW),        # sum C
     (dict(n=4096, deps=[[]] * 4096, cost=[2 ** 52] + [0] * 4095), ckm.E_OVERFLOW),  # n * sum C
+    (dict(n=7, deps=[[]] * 7, cost=[(2 ** 63 - 1) // 7 + 1] + [0] * 6), ckm.E_OVERFLOW),
 ])
 def test_graph_validation_errors(case, status):
     st, h = create(**case)
     assert st == status, ckm.last_error()
     assert not h.value
     assert ckm.last_error()
+
+
+@pytest.mark.parametrize("case", [
+    dict(n=2, deps=[[], [0]], size=[2 ** 62 - 1, 2 ** 62 - 1], m_input=1),    # M_in + sum M = INT64_MAX
+    dict(n=2, deps=[[], [0]], size=[1, 2 ** 62], m_param=2 ** 61 - 1),       # 2 M_param counted twice
+    dict(n=1, deps=[[]], cost=[2 ** 63 - 1]),                                # n sum C = INT64_MAX
+    dict(n=7, deps=[[]] * 7, cost=[(2 ** 63 - 1) // 7] + [0] * 6),
+    dict(n=3, deps=[[], [0], [1]], size=[2 ** 55, 3, 2 ** 53 + 1], cost=[2 ** 58, 1, 2 ** 53]),
+])
+def test_graph_totals_up_to_int64_max_accepted(case):
+    """Only totals beyond INT64_MAX are refused: a graph at the limit passes
+    validation (here it then needs a device, which a CPU-only host lacks)."""
+    st, h = create(**case)
+    assert st != ckm.E_OVERFLOW, ckm.last_error()
+    assert st in (ckm.OK, ckm.E_DEVICE), ckm.last_error()
+    if h.value:
+        ckm.lib().ckm_graph_destroy(h)
 
 
 def test_edge_count_checked_before_the_edges_are_read():

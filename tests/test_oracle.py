@@ -262,6 +262,28 @@ def test_simulate_matches_live_set_model(n, seed, kind):
         assert sim["max_frees"] <= 1          # Theorem 4.1
 
 
+def test_simulate_exact_above_2_53():
+    """Sizes near 2^56, odd: the oracle's int64 memory and cost equal the
+    live-set model's (Python integers, exact at any size), where binary64
+    sums would round."""
+    w = wl.random_dag(40, 9, s_kind="uniform", max_size=1000, max_cost=1000)
+    rng = np.random.default_rng(9)
+    w = w.replace(size=(w.size.astype(np.int64) << 46) + (rng.integers(1, 1 << 20, w.n) | 1),
+                  cost=(w.cost.astype(np.int64) << 42) + (rng.integers(1, 1 << 20, w.n) | 1),
+                  m_input=(1 << 50) + 1, m_param=(1 << 51) + 3)
+    assert int(w.size.sum()) > 2 ** 55 and int(w.cost.sum()) > 2 ** 55
+    assert ref.validate_graph(w.n, w.dep_ptr, w.dep_idx, w.cost, w.size, w.m_input, w.m_param) == ref.OK
+    q = ref.quantize(w.s_frac)
+    for k in range(3):
+        S = ref.round_random(q, 9, k)
+        R = ref.solve_R(w, S)
+        sim = ref.simulate(w, S, R)
+        peak, stage_peaks, ends = live_set_memory(w, S, R)
+        assert sim["peak"] == peak and list(sim["stage_peak"]) == stage_peaks and list(sim["U_end"]) == ends
+        assert sim["cost"] == sum(int(w.cost[i]) for t in range(w.n) for i in range(w.n) if R[t][i])
+        assert float(sim["peak"]) == float(sim["peak"] + 1)   # past binary64's integer range
+
+
 @pytest.mark.parametrize("cfg", [1, 2, 3])
 def test_schedule_invariants_on_workloads(cfg):
     """(4a) R_tt = 1; (4b)/(4c) triangularity; (1b) operands resident;
