@@ -300,11 +300,15 @@ Layout make_layout(int32_t n, int32_t K) {
   // stage makes its S rows itself and select recomputes the best R)
   const size_t kpad = (size_t)((K + kWave - 1) / kWave) * kWave;
   const size_t full = (size_t)(n >> 5), rem = (size_t)(n & 31);
-  const size_t rows_bytes = kpad * (32 * full * (full + 1) / 2 + rem * (full + 1)) * sizeof(uint32_t);
+  const size_t rrows_bytes = kpad * (32 * full * (full + 1) / 2 + rem * (full + 1)) * sizeof(uint32_t);
+  // the S rows are in this layout, or (the mask path) as one 64-bit word per
+  // group of 64 candidates and node: room for the larger of the two
+  const size_t mask_bytes = (kpad / kWave) * ckm::mask_rows_words(n) * sizeof(uint64_t);
+  const size_t rows_bytes = std::max(rrows_bytes, mask_bytes);
   L.rows_on = rows_bytes <= ckm::kRowsMaxBytes;
   L.rows_off = off;
   L.rrows_off = align256(off + rows_bytes);
-  L.total_rows = L.rows_on ? align256(L.rrows_off + rows_bytes) : off;
+  L.total_rows = L.rows_on ? align256(L.rrows_off + rrows_bytes) : off;
   return L;
 }
 
@@ -436,8 +440,17 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
   const size_t off_di = align256(off_dp + (n + 1) * sizeof(int32_t));
   const size_t off_uo = align256(off_di + Ea * sizeof(int32_t));
   const size_t off_rec = align256(off_uo + Ea * sizeof(int32_t));
-  const size_t total = align256(off_rec + (size_t)n * ckm::kNodeRecBytes);
+  const size_t off_mrec = align256(off_rec + (size_t)n * ckm::kNodeRecBytes);
+  // the mask path's records, when the graph fits their format
+  std::vector<char> mrecs;
+  if (!wide && n <= ckm::kMaskPathMaxNodes) {
+    mrecs.resize((size_t)ckm::mask_records_bytes(n));
+    if (!ckm::build_mask_records(n, bytes, cost, dp.data(), di.data(), up.data(), ui.data(), mrecs.data()))
+      mrecs.clear();
+  }
+  const size_t total = align256(off_mrec + mrecs.size());
   std::vector<char> host(total, 0);
+  if (!mrecs.empty()) memcpy(host.data() + off_mrec, mrecs.data(), mrecs.size());
   memcpy(host.data() + off_M, bytes, n * sizeof(int64_t));
   memcpy(host.data() + off_C, cost, n * sizeof(int64_t));
   memcpy(host.data() + off_up, up.data(), (n + 1) * sizeof(int32_t));
@@ -487,6 +500,7 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
   g->d_dep_idx = reinterpret_cast<const int32_t*>(base + off_di);
   g->d_dep_upos = reinterpret_cast<const int32_t*>(base + off_uo);
   g->d_recs = base + off_rec;
+  g->d_mrecs = mrecs.empty() ? nullptr : base + off_mrec;
   g->sync = new (std::nothrow) ckm::SyncCache;
   if (!g->sync) {
     (void)hipFree(g->d_mem);

@@ -34,6 +34,7 @@ struct ckm_graph {
   const int32_t* d_dep_idx = nullptr;
   const int32_t* d_dep_upos = nullptr;
   const void* d_recs = nullptr;  // n node records of ckm::kNodeRecBytes (see ckm_kernels.hip)
+  const void* d_mrecs = nullptr; // mask-path records (mask_records_bytes) when the graph fits them, else NULL
   ckm::SyncCache* sync = nullptr;  // reused by the synchronous calls; freed with the graph
 };
 
@@ -64,6 +65,18 @@ constexpr size_t kRowsMaxBytes = (size_t)8 << 30;
 void build_node_records(int32_t n, const int64_t* M, const int64_t* C, bool wide, const int32_t* dep_ptr,
                         const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx,
                         void* out);
+
+// Records of the mask path (see ckm_kernels.hip), mask_records_bytes(n)
+// of them; false when some node exceeds their format (more than four
+// dependencies, more than one user more than 32 nodes above it, or a
+// dependency with more than one such later user): the graph then takes the
+// other kernels.
+constexpr int kMaskPathMaxNodes = 1023;   // R row of up to 32 words in registers
+int32_t mask_records_bytes(int32_t n);
+bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int32_t* dep_ptr,
+                        const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx, void* out);
+// Words of one candidate group's mask rows (rows 0 .. n).
+size_t mask_rows_words(int32_t n);
 
 // Work-buffer layout for (n, K). Offsets are bytes from the buffer start,
 // each 256-byte aligned.

@@ -398,7 +398,8 @@ __device__ __forceinline__ int split_begin(int m, int parts, int s) {
 }
 
 // Stages [t0, t1) of work item `item` (numbered most expensive first).
-__device__ __forceinline__ void item_range(const EvalArgs& a, int item, int& t0, int& t1) {
+template <typename Args>
+__device__ __forceinline__ void item_range(const Args& a, int item, int& t0, int& t1) {
   if (a.kind == 0) {
     const int s = a.items - 1 - item;
     t0 = split_begin(a.n, a.items, s);
@@ -1540,6 +1541,336 @@ __global__ void __launch_bounds__(kWave) ckm_best_closure_kernel(ClosureArgs a) 
     for (int w = 0; w < a.row_words; ++w) Rout[w] = w <= (t >> 5) ? A.word(w) : 0u;
 }
 
+// ---------------------------------------------------------------------------
+// Mask path. A group's 64 candidates share one 64-bit word per (stage row,
+// node): bit j is candidate 64g + j. With the rows in that form, the repair
+// of Algorithm 2 and the FREE tests of eq. collectable become scalar-unit
+// operations on whole words (one instruction decides a node for all 64
+// candidates), and the vector unit keeps only the sums, each a masked
+// binary64 update selected by such a word. A node's record and its S words
+// come through the scalar cache; the R bits of the nodes above it stay in
+// each lane's window register and register row, as in the kernel above.
+//
+// Mask rows of a group: row t holds 8 (t/8 + 1) words (nodes 0 .. t rounded
+// up to whole blocks of 8; words for nodes >= t are zero); row n, after the
+// last stage, is all zero.
+__host__ __device__ __forceinline__ size_t mrow_off(int t) {
+  const size_t q = (size_t)(t >> 3), r = (size_t)(t & 7);
+  return 8 * ((size_t)t + 4 * q * (q ? q - 1 : 0) + q * r);
+}
+
+// Mask record of node v, 8 dwords (one scalar load); slots 2-3 of a node
+// with three or four dependencies are in record np + v, np = the padded
+// node count (see below).
+//   0: users u of v with u <= v + 32 (bit u - v - 1)
+//   1: ctrl: far user of v present << 3 | slots 2-3 present << 4 | its word
+//      << 8 | its bit << 16
+//   slot s (words 2 + 2s, 3 + 2s; slots 2-3 at 2(s-2) of record np + v):
+//      lm: users u of the dependency with v < u <= v + 32 (bit u - v - 1)
+//      ref: dependency node | far later user present << 25 | its word << 13
+//           | its bit << 20
+//      An absent slot 0 or 1 is all zero: it frees nothing, its size being 0.
+//   6: for node v-1, the byte offsets in a mask row of the S_{t+1} words of
+//      its slot 0 and 1 dependencies (low and high half; 0 for an absent
+//      slot), fetched one node ahead
+//   7: the byte offset of record v-1 (0 for node 0, whose loads for "node
+//      -1" repeat its own and are not used). The loads for node v-1 take
+//      their addresses from here, so that they cannot be issued before node
+//      v's record has arrived: scalar loads complete out of order, and a
+//      wait for that record would wait for them as well.
+// Node v's binary64 operands (M_v, C_v, M of slots 0-3) are 64 bytes of a
+// second array, read by vector-memory loads into every lane. Blocks of four
+// nodes are aligned (nodes 4c .. 4c+3). A stage's scan starts at the top of
+// its node's block; the nodes above t there (and past n - 1, for which the
+// records are padded with empty ones up to np = round_up(n, 4) + 4) compute
+// nothing and hold nothing, so they leave every sum unchanged.
+constexpr uint32_t kMFarU = 1u << 3, kMRare = 1u << 4;
+constexpr uint32_t kMRefFar = 1u << 25;
+constexpr int kMRecDwords = 8;
+constexpr int kMValBytes = 64;
+__host__ __device__ __forceinline__ int mask_padded_nodes(int n) { return ((n + 3) & ~3) + 4; }
+
+typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
+
+struct MaskArgs {
+  int32_t n, K, items, kind, P, T0, R1, R2;   // work plan (see Plan)
+  int32_t np;                                 // padded node count of the records
+  double base;                                // M_in + 2 M_param
+  size_t mgroup;                              // words of one group's mask rows
+  cptr<uint64_t> mrows;                       // S masks, group-major
+  cptr<u32x8> mrecs;                          // 2 np records
+  const uint4* __restrict__ mvals;            // np x 64 bytes of binary64 operands
+  uint32_t* __restrict__ rrows;               // R rows out (row array layout), or NULL
+  int32_t kpad;
+  int64_t* __restrict__ part_peak;
+  int64_t* __restrict__ part_cost;
+  int32_t* __restrict__ hdr;
+};
+
+__device__ __forceinline__ uint64_t mpair(const u32x8& b, int p) {
+  return (uint64_t)b[2 * p] | ((uint64_t)b[2 * p + 1] << 32);
+}
+__device__ __forceinline__ bool lane_of(uint64_t m) { return __builtin_amdgcn_inverse_ballot_w64(m); }
+__device__ __forceinline__ uint64_t mask_of(bool b) { return __builtin_amdgcn_ballot_w64(b); }
+// acc + [lane's bit of m] * x, one masked binary64 update
+__device__ __forceinline__ double madd_m(double acc, uint64_t m, double x) {
+  return fma(lane_of(m) ? 1.0 : 0.0, x, acc);
+}
+// Scalar loads at a 32-bit byte offset from a base (one instruction, the
+// offset in a register).
+template <typename T>
+__device__ __forceinline__ T sload(cptr<uint64_t> base, uint32_t off) {
+  return *(const __attribute__((address_space(4))) T*)((const __attribute__((address_space(4))) char*)base + off);
+}
+template <typename T>
+__device__ __forceinline__ T sload(cptr<u32x8> base, uint32_t off) {
+  return *(const __attribute__((address_space(4))) T*)((const __attribute__((address_space(4))) char*)base + off);
+}
+__device__ __forceinline__ u32x8 load_blk(cptr<uint64_t> row, int c) {
+  return *(const __attribute__((address_space(4))) u32x8*)(row + 4 * c);
+}
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t mval_rsrc(const MaskArgs& a) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(a.mvals), 0, a.np * kMValBytes, kBufWord3);
+}
+// 16 bytes at byte offset off + kOff of the operands, in every lane
+template <int kOff>
+__device__ __forceinline__ uint4 load_mval(__amdgpu_buffer_rsrc_t rs, uint32_t off) {
+  const auto x = __builtin_amdgcn_raw_buffer_load_b128(rs, kOff, (int)off, 0);
+  return make_uint4(x[0], x[1], x[2], x[3]);
+}
+
+struct MScan {
+  double U0, Y, maxv, cost;
+  uint32_t Rwin;   // R bits of nodes v+1 .. v+32 (bit d <-> node v + 1 + d)
+};
+
+// A bit of the register row of R words (a node more than 32 above the one
+// being decided: its word is complete).
+__device__ __forceinline__ uint32_t rrow_bit(const u32x32& Rrow, uint32_t word, uint32_t pos) {
+  return (Rrow[word] >> pos) & 1u;
+}
+
+// One dependency slot of node v: the dependency's value is released after
+// v (FREE(t,i,v) = 1) on the candidates that compute v, do not keep the
+// value into stage t+1 and compute none of its later users in stage t.
+__device__ __forceinline__ double mask_slot(double val, uint64_t R, uint32_t lm, uint32_t ref, double Mi,
+                                            uint64_t s1i, uint32_t Rwin, const u32x32& Rrow) {
+  uint32_t y = Rwin & lm;
+  if (ref & kMRefFar) y |= rrow_bit(Rrow, (ref >> 13) & 127u, (ref >> 20) & 31u);
+  const uint64_t later = mask_of(y != 0u);
+  const uint64_t fr = R & ~(s1i | later);
+  return madd_m(val, fr, Mi);
+}
+
+// What node v needs besides its block: its record, the S_{t+1} words of its
+// slot 0 and 1 dependencies and its binary64 operands (M_v, C_v | M of slots
+// 0, 1), all requested one node ahead.
+struct MNode {
+  u32x8 rec;
+  uint64_t d0, d1;
+  uint4 mc, dm;
+};
+
+// Node v of stage t for the 64 candidates of a group: S0, S1 are the words
+// of S_t[v] and S_{t+1}[v]. Algorithm 2: v is computed if it is node t
+// (constraint 4a), or it is not held and is kept into t+1 (1c) or used by a
+// computed node (1b). kTop: v is in the block of node t, and may be t; below
+// that block, v < t. Released right after its own compute (eq. collectable
+// with i = v): a computed node that is neither kept nor used, which only
+// node t can be.
+template <bool kTop>
+__device__ __forceinline__ void mask_node(const MaskArgs& a, int t, int v, const MNode& nd, uint64_t S0, uint64_t S1,
+                                          cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow) {
+  const u32x8& rec = nd.rec;
+  const uint32_t ctrl = rec[1];
+  const double Mv = dbl(nd.mc.x, nd.mc.y), Cv = dbl(nd.mc.z, nd.mc.w);
+  uint32_t x = sc.Rwin & rec[0];
+  if (ctrl & kMFarU) x |= rrow_bit(Rrow, (ctrl >> 8) & 127u, (ctrl >> 16) & 31u);
+  const uint64_t x1 = S1 | mask_of(x != 0u);
+  uint64_t R = x1 & ~S0;
+  double val = sc.Y;
+  if (kTop && v == t) {
+    R = ~0ull;
+    val = madd_m(val, ~x1, Mv);
+  }
+  val = mask_slot(val, R, rec[2], rec[3], dbl(nd.dm.x, nd.dm.y), nd.d0, sc.Rwin, Rrow);
+  val = mask_slot(val, R, rec[4], rec[5], dbl(nd.dm.z, nd.dm.w), nd.d1, sc.Rwin, Rrow);
+  if (__builtin_expect((ctrl & kMRare) != 0u, 0)) {
+    const u32x8 r2 = a.mrecs[a.np + v];
+    const uint4 m23 = load_mval<32>(mval_rsrc(a), (uint32_t)v * kMValBytes);
+    const uint32_t ns = r2[4];
+    val = mask_slot(val, R, r2[0], r2[1], dbl(m23.x, m23.y), s1row[r2[1] & 0x1FFFu], sc.Rwin, Rrow);
+    if (ns >= 4) val = mask_slot(val, R, r2[2], r2[3], dbl(m23.z, m23.w), s1row[r2[3] & 0x1FFFu], sc.Rwin, Rrow);
+  }
+  // suffix form of the U recurrence (see scan_node): val = Y + freed_v
+  sc.maxv = max_f64(sc.maxv, val);
+  const bool rb = lane_of(R);
+  const double sel = rb ? 1.0 : 0.0;
+  sc.Y = fma(-sel, Mv, val);
+  sc.cost = fma(sel, Cv, sc.cost);
+  sc.U0 = madd_m(sc.U0, S0, Mv);
+  sc.Rwin = sc.Rwin + sc.Rwin + (rb ? 1u : 0u);
+}
+
+// After node v with v % 32 == 0: the R bits of nodes v .. v+31 are complete,
+// one word of R_t, kept in the register row (and stored for the output).
+__device__ __forceinline__ void mask_flush(const MaskArgs& a, int v, const MScan& sc, u32x32& Rrow, uint32_t* rrow_t) {
+  if ((v & 31) == 0) {
+    Rrow[v >> 5] = sc.Rwin;
+    if (rrow_t) rrow_t[(size_t)(v >> 5) * a.kpad] = sc.Rwin;
+  }
+}
+
+// The loads node v-1 needs, issued while node v is decided: its record and
+// operands, and the dependency words node v's record lists for it.
+__device__ __forceinline__ MNode mask_fetch(const MaskArgs& a, const u32x8& rec_v, cptr<uint64_t> s1row) {
+  const uint32_t roff = rec_v[7], f = rec_v[6];
+  MNode nx;
+  nx.rec = sload<u32x8>(a.mrecs, roff);
+  nx.d0 = sload<uint64_t>(s1row, f & 0xFFFFu);
+  nx.d1 = sload<uint64_t>(s1row, f >> 16);
+  const auto rs = mval_rsrc(a);
+  nx.mc = load_mval<0>(rs, roff * 2u);
+  nx.dm = load_mval<16>(rs, roff * 2u);
+  return nx;
+}
+
+// Node v at position P of its block (P = v & 3), with the next node's loads
+// issued first; at P = 0 they include the next block's words. The loads
+// alternate between two buffers by position (node v's in buf[P & 1], node
+// v-1's into the other), so nothing moves from one to the other.
+template <int P, bool kTop>
+__device__ __forceinline__ void mask_step(const MaskArgs& a, int t, int v, MNode (&buf)[2], u32x8& B0, u32x8& B1,
+                                          cptr<uint64_t> s0row, cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow,
+                                          uint32_t* rrow_t) {
+  constexpr int kCur = P & 1, kNext = kCur ^ 1;
+  const uint64_t S0 = mpair(B0, P), S1 = mpair(B1, P);
+  const u32x8& rec = buf[kCur].rec;
+  buf[kNext] = mask_fetch(a, rec, s1row);
+  if (P == 0) {
+    // block c-1 starts (c - 1) * 32 bytes into a row: record v-1's byte
+    // offset is (4c - 1) * 32, so (rec[7] >> 2) & ~31 (0 for c = 0)
+    const uint32_t boff = (rec[7] >> 2) & ~31u;
+    B0 = sload<u32x8>(s0row, boff);
+    B1 = sload<u32x8>(s1row, boff);
+  }
+  mask_node<kTop>(a, t, v, buf[kCur], S0, S1, s1row, sc, Rrow);
+  if (P == 0) mask_flush(a, v, sc, Rrow, rrow_t);
+}
+
+template <bool kTop>
+__device__ __forceinline__ void mask_block(const MaskArgs& a, int t, int c, MNode (&buf)[2], u32x8& B0, u32x8& B1,
+                                           cptr<uint64_t> s0row, cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow,
+                                           uint32_t* rrow_t) {
+  mask_step<3, kTop>(a, t, 4 * c + 3, buf, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
+  mask_step<2, kTop>(a, t, 4 * c + 2, buf, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
+  mask_step<1, kTop>(a, t, 4 * c + 1, buf, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
+  mask_step<0, kTop>(a, t, 4 * c, buf, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
+}
+
+// One wave per work item: the 64 candidates of group blockIdx.x over the
+// stages of item blockIdx.y. Graphs up to 1023 nodes (R row in 32 registers),
+// none of whose nodes exceed the record (at most four dependencies, one user
+// more than 32 nodes above the node, one such later user per dependency).
+// Each node's loads are issued one node ahead, in one batch, so that a node
+// waits once, for loads that had a whole node's work to arrive.
+__global__ void __launch_bounds__(kWave) ckm_mask_eval_kernel(MaskArgs a) {
+  const int lane = threadIdx.x;
+  const int group = blockIdx.x;
+  const int item = blockIdx.y;
+  const uint32_t k = (uint32_t)(group * kWave + lane);
+  int t0, t1;
+  item_range(a, item, t0, t1);
+  const cptr<uint64_t> rows = a.mrows + (size_t)group * a.mgroup;
+  u32x32 Rrow = (u32x32)0u;
+  double seg_peak = -INFINITY;
+  int64_t seg_cost = 0;
+  for (int t = t0; t < t1; ++t) {
+    const cptr<uint64_t> s0row = rows + mrow_off(t);
+    const cptr<uint64_t> s1row = rows + mrow_off(t + 1);
+    uint32_t* rrow_t = a.rrows ? a.rrows + row_base(t) * (size_t)a.kpad + k : nullptr;
+    MScan sc;
+    sc.U0 = (double)a.base;
+    sc.Y = 0.0;
+    sc.maxv = -INFINITY;
+    sc.cost = 0.0;
+    sc.Rwin = 0u;
+    // the scan starts at the top of t's block: node v0 = 4c + 3, whose loads
+    // record v0 + 1 names
+    const int c = t >> 2;
+    MNode buf[2];
+    const u32x8 top = a.mrecs[4 * c + 4];
+    buf[1] = mask_fetch(a, top, s1row);
+    u32x8 B0 = load_blk(s0row, c), B1 = load_blk(s1row, c);
+    mask_block<true>(a, t, c, buf, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
+    for (int cc = c - 1; cc >= 0; --cc) mask_block<false>(a, t, cc, buf, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
+    seg_peak = fmax(seg_peak, sc.U0 - sc.Y + sc.maxv);
+    seg_cost += (int64_t)sc.cost;
+  }
+  if ((int)k < a.K && t0 < t1) {
+    atomicMax(reinterpret_cast<long long*>(a.part_peak) + k, (long long)seg_peak);
+    atomicAdd(reinterpret_cast<unsigned long long*>(a.part_cost) + k, (unsigned long long)seg_cost);
+  }
+  if (group == 0 && item == 0 && lane == 0) a.hdr[0] = a.items;
+}
+
+// Lane L of v takes the wave-uniform x (v_writelane_b32 with the lane as an
+// inline constant).
+template <int L>
+__device__ __forceinline__ uint32_t write_lane(uint32_t v, uint32_t x) {
+  asm("v_writelane_b32 %0, %1, %2" : "+v"(v) : "s"(x), "i"(L));
+  return v;
+}
+// Lanes 2j and 2j+1 take the low and high halves of m[j], j >= J.
+template <int J>
+__device__ __forceinline__ uint32_t put_masks(uint32_t v, const uint64_t (&m)[8]) {
+  v = write_lane<2 * J>(v, (uint32_t)m[J]);
+  v = write_lane<2 * J + 1>(v, (uint32_t)(m[J] >> 32));
+  if constexpr (J + 1 < 8) v = put_masks<J + 1>(v, m);
+  return v;
+}
+
+// Randomized rounding into mask rows: block (group, row r), lane = candidate.
+// Word i of row r is the group's 64 decisions [u_{k,r,i} < q[r][i]] (the
+// same draws as round_word); candidate 0 takes the deterministic bits under
+// CKM_F_DET0. A block of 8 nodes shares one Philox output per lane.
+__global__ void __launch_bounds__(kWave) ckm_round_masks_kernel(const uint32_t* __restrict__ q,
+                                                                const uint32_t* __restrict__ det, int32_t n,
+                                                                int32_t ldq, int32_t det_words, uint32_t key0,
+                                                                uint32_t key1, uint32_t det0, size_t mgroup,
+                                                                uint64_t* __restrict__ mrows) {
+  const int lane = threadIdx.x;
+  const int group = blockIdx.x;
+  const int r = blockIdx.y;   // 0 .. n (row n: zero)
+  const uint32_t k = (uint32_t)(group * kWave + lane);
+  uint32_t* dst = reinterpret_cast<uint32_t*>(mrows + (size_t)group * mgroup + mrow_off(r));
+  const int nblk = (r >> 3) + 1;
+  const cptr<uint32_t> qrow = as_const(q + (size_t)(r < n ? r : 0) * ldq);
+  const cptr<uint32_t> drow = as_const(det + (size_t)(r < n ? r : 0) * det_words);
+  for (int b = 0; b < nblk; ++b) {
+    uint64_t m[8];
+    if (8 * b >= r) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) m[j] = 0ull;
+    } else {
+      uint32_t x[4];
+      philox4x32_10((uint32_t)b, (uint32_t)r, k, 0u, key0, key1, x);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t u = (x[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+        m[j] = mask_of(u < qrow[8 * b + j]);
+      }
+      if (det0 && group == 0) {
+        const uint32_t dw = drow[b >> 2] >> (8 * (b & 3));
+#pragma unroll
+        for (int j = 0; j < 8; ++j) m[j] = (m[j] & ~1ull) | ((dw >> j) & 1u);
+      }
+    }
+    const uint32_t out = put_masks<0>(0u, m);
+    if (lane < 16) dst[16 * b + lane] = out;   // words 8b .. 8b+7 of the row
+  }
+}
+
 template <typename T>
 T* at(char* work, size_t off) { return reinterpret_cast<T*>(work + off); }
 
@@ -1612,9 +1943,20 @@ int32_t eval_waves_per_cu(int32_t n, bool wide) {
 
 static unsigned groups_of(int32_t K) { return (unsigned)((K + kWave - 1) / kWave); }
 
+static bool use_mask_path(const ckm_graph& g, const Layout& L) { return L.rows_on && g.d_mrecs != nullptr; }
+
+size_t mask_rows_words(int32_t n) { return mrow_off(n + 1); }
+
 hipError_t launch_round_rows(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed, uint32_t flags,
                              char* work, hipStream_t stream) {
   if (!L.rows_on) return hipSuccess;
+  if (use_mask_path(g, L)) {
+    hipLaunchKernelGGL(ckm_round_masks_kernel, dim3(groups_of(K), g.n + 1), dim3(kWave), 0, stream,
+                       at<const uint32_t>(work, L.q_off), at<const uint32_t>(work, L.det_off), g.n, L.ldq,
+                       L.det_words, (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32),
+                       (flags & CKM_F_DET0) ? 1u : 0u, mask_rows_words(g.n), at<uint64_t>(work, L.rows_off));
+    return hipGetLastError();
+  }
   const int32_t kpad = ((K + kWave - 1) / kWave) * kWave;
   hipLaunchKernelGGL(ckm_round_rows_kernel, dim3((K + kWave - 1) / kWave, g.n), dim3(kWave), 0, stream,
                      at<const uint32_t>(work, L.q_off), at<const uint32_t>(work, L.det_off), L.ldq, L.det_words,
@@ -1635,6 +1977,7 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   a.rows = at<const uint32_t>(work, L.rows_off);
   a.rrows = L.rows_on ? at<uint32_t>(work, L.rrows_off) : nullptr;
   a.kpad = ((K + kWave - 1) / kWave) * kWave;
+  const bool mask_path = src == kSrcRound && use_mask_path(g, L);
   if (src == kSrcRound && L.rows_on) {
     // every row rounded once (here, or by an earlier launch_round_rows), then streamed
     if (!(flags & CKM_F_ROUNDED)) {
@@ -1655,6 +1998,33 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
     hipLaunchKernelGGL(ckm_user_rows_kernel, dim3(groups_of(K), g.n), dim3(256), tile, stream, a.s_user, g.n, K,
                        a.s_words, a.kpad, at<uint32_t>(work, L.rows_off));
     src = kSrcRows;
+  }
+  if (mask_path) {
+    MaskArgs m;
+    m.n = g.n;
+    m.K = K;
+    m.items = plan.items;
+    m.kind = plan.kind;
+    m.P = plan.P;
+    m.T0 = plan.T0;
+    m.R1 = plan.R1;
+    m.R2 = plan.R2;
+    m.base = (double)g.base;
+    m.mgroup = mask_rows_words(g.n);
+    m.mrows = as_const(at<const uint64_t>(work, L.rows_off));
+    m.np = mask_padded_nodes(g.n);
+    m.mrecs = (cptr<u32x8>)(g.d_mrecs);
+    m.mvals = reinterpret_cast<const uint4*>(static_cast<const char*>(g.d_mrecs) +
+                                             (size_t)2 * m.np * kMRecDwords * sizeof(uint32_t));
+    m.rrows = at<uint32_t>(work, L.rrows_off);
+    m.kpad = a.kpad;
+    m.part_peak = at<int64_t>(work, L.part_peak_off);
+    m.part_cost = at<int64_t>(work, L.part_cost_off);
+    m.hdr = at<int32_t>(work, L.hdr_off);
+    hipLaunchKernelGGL(ckm_eval_init_kernel, dim3((K + 255) / 256), dim3(256), 0, stream, K, m.part_peak,
+                       m.part_cost);
+    hipLaunchKernelGGL(ckm_mask_eval_kernel, dim3((K + kWave - 1) / kWave, plan.items), dim3(kWave), 0, stream, m);
+    return hipGetLastError();
   }
   a.items = plan.items;
   a.kind = plan.kind;
@@ -1827,6 +2197,75 @@ static bool build_ext_lists(int32_t v, const int64_t* M, bool wide, const int32_
   }
   dw[kDwExt] = (uint32_t)nfar | (uint32_t)nd << 8 | kExtValid;
   return true;
+}
+
+int32_t mask_records_bytes(int32_t n) {
+  return mask_padded_nodes(n) * (2 * kMRecDwords * (int32_t)sizeof(uint32_t) + kMValBytes);
+}
+
+bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int32_t* dep_ptr,
+                        const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx, void* out) {
+  const int32_t np = mask_padded_nodes(n);
+  uint32_t* recs = static_cast<uint32_t*>(out);
+  double* vals = reinterpret_cast<double*>(recs + (size_t)2 * np * kMRecDwords);
+  memset(out, 0, (size_t)mask_records_bytes(n));
+  for (int32_t v = 0; v < n; ++v) {
+    uint32_t* r = recs + (size_t)v * kMRecDwords;
+    uint32_t* r2 = recs + (size_t)(np + v) * kMRecDwords;
+    double* val = vals + (size_t)v * (kMValBytes / sizeof(double));
+    uint32_t ctrl = 0;
+    int nfar = 0;
+    for (int32_t e = user_ptr[v]; e < user_ptr[v + 1]; ++e) {
+      const int u = user_idx[e];
+      if (u - v - 1 < 32) {
+        r[0] |= 1u << (u - v - 1);
+      } else {
+        if (nfar++) return false;
+        ctrl |= kMFarU | (uint32_t)(u >> 5) << 8 | (uint32_t)(u & 31) << 16;
+      }
+    }
+    const int nd = dep_ptr[v + 1] - dep_ptr[v];
+    if (nd > 4) return false;
+    if (nd > 2) {
+      ctrl |= kMRare;
+      r2[4] = (uint32_t)nd;
+    }
+    val[0] = (double)M[v];
+    val[1] = (double)C[v];
+    for (int sl = 0; sl < nd; ++sl) {
+      const int i = dep_idx[dep_ptr[v] + sl];
+      uint32_t* w = sl < 2 ? r + 2 + 2 * sl : r2 + 2 * (sl - 2);
+      uint32_t ref = (uint32_t)i;
+      int nlate = 0;
+      for (int32_t e = user_ptr[i]; e < user_ptr[i + 1]; ++e) {
+        const int u = user_idx[e];
+        if (u <= v) continue;
+        if (u - v - 1 < 32) {
+          w[0] |= 1u << (u - v - 1);
+        } else {
+          if (nlate++) return false;
+          ref |= kMRefFar | (uint32_t)(u >> 5) << 13 | (uint32_t)(u & 31) << 20;
+        }
+      }
+      w[1] = ref;
+      val[2 + sl] = (double)M[i];
+    }
+    r[1] = ctrl;
+  }
+  // fetch lists: record v (padded ones included) names the S_{t+1} words of
+  // node v-1's slots 0 and 1, and where record v-1 is
+  for (int32_t v = 1; v < np; ++v) {
+    const int32_t u = v - 1;
+    uint32_t f = 0;
+    if (u < n) {
+      const int nd = dep_ptr[u + 1] - dep_ptr[u];
+      if (nd >= 1) f |= (uint32_t)dep_idx[dep_ptr[u]] * 8u;
+      if (nd >= 2) f |= (uint32_t)dep_idx[dep_ptr[u] + 1] * 8u << 16;
+    }
+    recs[(size_t)v * kMRecDwords + 6] = f;
+    recs[(size_t)v * kMRecDwords + 7] = (uint32_t)u * (uint32_t)(kMRecDwords * sizeof(uint32_t));
+  }
+  return true;   // record 0 keeps fetch list 0 and word 7 = 0
 }
 
 void build_node_records(int32_t n, const int64_t* M, const int64_t* C, bool wide, const int32_t* dep_ptr,
