@@ -1559,47 +1559,50 @@ __host__ __device__ __forceinline__ size_t mrow_off(int t) {
   return 8 * ((size_t)t + 4 * q * (q ? q - 1 : 0) + q * r);
 }
 
-// Mask record of node v, 8 dwords (one scalar load); slots 2-3 of a node
-// with three or four dependencies are in record np + v, np = the padded
-// node count (see below).
+// Node v's data, 128 bytes at 128 v:
+//   [0, 32)   record, 8 dwords (one scalar load)
+//   [32, 96)  binary64 operands M_v, C_v and M of dependency slots 0-3,
+//             read by vector-memory loads into every lane
+//   [96, 128) slots 2-3 (nodes with three or four dependencies): lm, ref of
+//             slot 2, of slot 3, dependency count, byte offsets in a mask
+//             row of the S_{t+1} words of the slot 2 and 3 dependencies
+// A far reference names a node u more than 32 above v as u << 16 | (u & 31)
+// (none: 0xFFFF << 16). Its R bit matters only when u <= t, i.e. when the
+// field is below (t + 1) << 16: a node above t computes nothing in stage t.
+// Record words:
 //   0: users u of v with u <= v + 32 (bit u - v - 1)
-//   1: ctrl: far user of v present << 3 | slots 2-3 present << 4 | its word
-//      << 8 | its bit << 16
-//   slot s (words 2 + 2s, 3 + 2s; slots 2-3 at 2(s-2) of record np + v):
+//   1: ctrl: far reference to the user of v more than 32 above it | slots
+//      2-3 present << 8
+//   slot s (words 2 + 2s, 3 + 2s):
 //      lm: users u of the dependency with v < u <= v + 32 (bit u - v - 1)
-//      ref: dependency node | far later user present << 25 | its word << 13
-//           | its bit << 20
-//      An absent slot 0 or 1 is all zero: it frees nothing, its size being 0.
+//      ref: far reference to the dependency's later user
+//      An absent slot has lm = 0 and no far reference: it frees nothing, its
+//      size being 0.
 //   6: for node v-1, the byte offsets in a mask row of the S_{t+1} words of
 //      its slot 0 and 1 dependencies (low and high half; 0 for an absent
 //      slot), fetched one node ahead
-//   7: the byte offset of record v-1 (0 for node 0, whose loads for "node
-//      -1" repeat its own and are not used). The loads for node v-1 take
-//      their addresses from here, so that they cannot be issued before node
-//      v's record has arrived: scalar loads complete out of order, and a
-//      wait for that record would wait for them as well.
-// Node v's binary64 operands (M_v, C_v, M of slots 0-3) are 64 bytes of a
-// second array, read by vector-memory loads into every lane. Blocks of four
-// nodes are aligned (nodes 4c .. 4c+3). A stage's scan starts at the top of
-// its node's block; the nodes above t there (and past n - 1, for which the
-// records are padded with empty ones up to np = round_up(n, 4) + 4) compute
-// nothing and hold nothing, so they leave every sum unchanged.
-constexpr uint32_t kMFarU = 1u << 3, kMRare = 1u << 4;
-constexpr uint32_t kMRefFar = 1u << 25;
-constexpr int kMRecDwords = 8;
-constexpr int kMValBytes = 64;
+//   7: 128 (v - 1), where node v-1's data starts (0 for node 0, whose loads
+//      for "node -1" repeat its own and are not used). The loads for node
+//      v-1 take their addresses from here, so that they cannot be issued
+//      before node v's record has arrived: scalar loads complete out of
+//      order, and a wait for that record would wait for them as well.
+// Blocks of four nodes are aligned (nodes 4c .. 4c+3). A stage's scan
+// starts at the top of its node's block; the nodes above t there (and past
+// n - 1, whose data is padded with empty nodes up to np = round_up(n, 4) +
+// 4) compute nothing and hold nothing, so they leave every sum unchanged.
+constexpr uint32_t kMNoFar = 0xFFFFu << 16, kMRare = 1u << 8;
+constexpr int kMNodeBytes = 128;
 __host__ __device__ __forceinline__ int mask_padded_nodes(int n) { return ((n + 3) & ~3) + 4; }
 
 typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
 
 struct MaskArgs {
   int32_t n, K, items, kind, P, T0, R1, R2;   // work plan (see Plan)
-  int32_t np;                                 // padded node count of the records
+  int32_t np;                                 // padded node count of the node data
   double base;                                // M_in + 2 M_param
   size_t mgroup;                              // words of one group's mask rows
   cptr<uint64_t> mrows;                       // S masks, group-major
-  cptr<u32x8> mrecs;                          // 2 np records
-  const uint4* __restrict__ mvals;            // np x 64 bytes of binary64 operands
+  cptr<u32x8> mnodes;                         // np x 128 bytes of node data
   uint32_t* __restrict__ rrows;               // R rows out (row array layout), or NULL
   int32_t kpad;
   int64_t* __restrict__ part_peak;
@@ -1616,23 +1619,17 @@ __device__ __forceinline__ uint64_t mask_of(bool b) { return __builtin_amdgcn_ba
 __device__ __forceinline__ double madd_m(double acc, uint64_t m, double x) {
   return fma(lane_of(m) ? 1.0 : 0.0, x, acc);
 }
-// Scalar loads at a 32-bit byte offset from a base (one instruction, the
+// A scalar load at a 32-bit byte offset from a base (one instruction, the
 // offset in a register).
-template <typename T>
-__device__ __forceinline__ T sload(cptr<uint64_t> base, uint32_t off) {
+template <typename T, typename B>
+__device__ __forceinline__ T sload(cptr<B> base, uint32_t off) {
   return *(const __attribute__((address_space(4))) T*)((const __attribute__((address_space(4))) char*)base + off);
 }
-template <typename T>
-__device__ __forceinline__ T sload(cptr<u32x8> base, uint32_t off) {
-  return *(const __attribute__((address_space(4))) T*)((const __attribute__((address_space(4))) char*)base + off);
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t mnode_rsrc(const MaskArgs& a) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<u32x8*>((const u32x8*)a.mnodes), 0, a.np * kMNodeBytes,
+                                           kBufWord3);
 }
-__device__ __forceinline__ u32x8 load_blk(cptr<uint64_t> row, int c) {
-  return *(const __attribute__((address_space(4))) u32x8*)(row + 4 * c);
-}
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t mval_rsrc(const MaskArgs& a) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(a.mvals), 0, a.np * kMValBytes, kBufWord3);
-}
-// 16 bytes at byte offset off + kOff of the operands, in every lane
+// 16 bytes at byte offset off + kOff of the node data, in every lane
 template <int kOff>
 __device__ __forceinline__ uint4 load_mval(__amdgpu_buffer_rsrc_t rs, uint32_t off) {
   const auto x = __builtin_amdgcn_raw_buffer_load_b128(rs, kOff, (int)off, 0);
@@ -1644,19 +1641,23 @@ struct MScan {
   uint32_t Rwin;   // R bits of nodes v+1 .. v+32 (bit d <-> node v + 1 + d)
 };
 
-// A bit of the register row of R words (a node more than 32 above the one
-// being decided: its word is complete).
-__device__ __forceinline__ uint32_t rrow_bit(const u32x32& Rrow, uint32_t word, uint32_t pos) {
-  return (Rrow[word] >> pos) & 1u;
+// The R bit of the far node that field f names (more than 32 above the node
+// being decided: its word of the register row is complete). A shift uses the
+// low five bits of its count by itself. Only for u <= t; the empty asm keeps
+// the compiler from hoisting the indexed register read out of that branch
+// (the word index is clamped to the row all the same).
+__device__ __forceinline__ uint32_t far_bit(const u32x32& Rrow, uint32_t f) {
+  asm volatile("");
+  return (Rrow[(f >> 21) & 31u] >> (f & 31u)) & 1u;
 }
 
 // One dependency slot of node v: the dependency's value is released after
 // v (FREE(t,i,v) = 1) on the candidates that compute v, do not keep the
 // value into stage t+1 and compute none of its later users in stage t.
 __device__ __forceinline__ double mask_slot(double val, uint64_t R, uint32_t lm, uint32_t ref, double Mi,
-                                            uint64_t s1i, uint32_t Rwin, const u32x32& Rrow) {
+                                            uint64_t s1i, uint32_t Rwin, const u32x32& Rrow, uint32_t tlim) {
   uint32_t y = Rwin & lm;
-  if (ref & kMRefFar) y |= rrow_bit(Rrow, (ref >> 13) & 127u, (ref >> 20) & 31u);
+  if (__builtin_expect(ref < tlim, 0)) y |= far_bit(Rrow, ref);
   const uint64_t later = mask_of(y != 0u);
   const uint64_t fr = R & ~(s1i | later);
   return madd_m(val, fr, Mi);
@@ -1675,32 +1676,41 @@ struct MNode {
 // of S_t[v] and S_{t+1}[v]. Algorithm 2: v is computed if it is node t
 // (constraint 4a), or it is not held and is kept into t+1 (1c) or used by a
 // computed node (1b). kTop: v is in the block of node t, and may be t; below
-// that block, v < t. Released right after its own compute (eq. collectable
-// with i = v): a computed node that is neither kept nor used, which only
-// node t can be.
+// that block, v < t and the scan has passed at least one node. Released
+// right after its own compute (eq. collectable with i = v): a computed node
+// that is neither kept nor used, which only node t can be.
 template <bool kTop>
 __device__ __forceinline__ void mask_node(const MaskArgs& a, int t, int v, const MNode& nd, uint64_t S0, uint64_t S1,
                                           cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow) {
   const u32x8& rec = nd.rec;
   const uint32_t ctrl = rec[1];
+  const uint32_t tlim = (uint32_t)(t + 1) << 16;
   const double Mv = dbl(nd.mc.x, nd.mc.y), Cv = dbl(nd.mc.z, nd.mc.w);
   uint32_t x = sc.Rwin & rec[0];
-  if (ctrl & kMFarU) x |= rrow_bit(Rrow, (ctrl >> 8) & 127u, (ctrl >> 16) & 31u);
+  if (__builtin_expect(ctrl < tlim, 0)) x |= far_bit(Rrow, ctrl);
   const uint64_t x1 = S1 | mask_of(x != 0u);
   uint64_t R = x1 & ~S0;
+  sc.U0 = madd_m(sc.U0, S0, Mv);
+  if (!kTop && R == 0ull) {
+    // no candidate computes v: nothing is released after it, and the sums
+    // stay (maxv already covers Y, the running value only falling since)
+    sc.Rwin = sc.Rwin + sc.Rwin;
+    return;
+  }
   double val = sc.Y;
   if (kTop && v == t) {
     R = ~0ull;
     val = madd_m(val, ~x1, Mv);
   }
-  val = mask_slot(val, R, rec[2], rec[3], dbl(nd.dm.x, nd.dm.y), nd.d0, sc.Rwin, Rrow);
-  val = mask_slot(val, R, rec[4], rec[5], dbl(nd.dm.z, nd.dm.w), nd.d1, sc.Rwin, Rrow);
+  val = mask_slot(val, R, rec[2], rec[3], dbl(nd.dm.x, nd.dm.y), nd.d0, sc.Rwin, Rrow, tlim);
+  val = mask_slot(val, R, rec[4], rec[5], dbl(nd.dm.z, nd.dm.w), nd.d1, sc.Rwin, Rrow, tlim);
   if (__builtin_expect((ctrl & kMRare) != 0u, 0)) {
-    const u32x8 r2 = a.mrecs[a.np + v];
-    const uint4 m23 = load_mval<32>(mval_rsrc(a), (uint32_t)v * kMValBytes);
-    const uint32_t ns = r2[4];
-    val = mask_slot(val, R, r2[0], r2[1], dbl(m23.x, m23.y), s1row[r2[1] & 0x1FFFu], sc.Rwin, Rrow);
-    if (ns >= 4) val = mask_slot(val, R, r2[2], r2[3], dbl(m23.z, m23.w), s1row[r2[3] & 0x1FFFu], sc.Rwin, Rrow);
+    const uint32_t off = (uint32_t)v * kMNodeBytes;
+    const u32x8 r2 = sload<u32x8>(a.mnodes, off + 96);
+    const uint4 m23 = load_mval<64>(mnode_rsrc(a), off);
+    val = mask_slot(val, R, r2[0], r2[1], dbl(m23.x, m23.y), sload<uint64_t>(s1row, r2[5]), sc.Rwin, Rrow, tlim);
+    if (r2[4] >= 4)
+      val = mask_slot(val, R, r2[2], r2[3], dbl(m23.z, m23.w), sload<uint64_t>(s1row, r2[6]), sc.Rwin, Rrow, tlim);
   }
   // suffix form of the U recurrence (see scan_node): val = Y + freed_v
   sc.maxv = max_f64(sc.maxv, val);
@@ -1708,64 +1718,61 @@ __device__ __forceinline__ void mask_node(const MaskArgs& a, int t, int v, const
   const double sel = rb ? 1.0 : 0.0;
   sc.Y = fma(-sel, Mv, val);
   sc.cost = fma(sel, Cv, sc.cost);
-  sc.U0 = madd_m(sc.U0, S0, Mv);
   sc.Rwin = sc.Rwin + sc.Rwin + (rb ? 1u : 0u);
-}
-
-// After node v with v % 32 == 0: the R bits of nodes v .. v+31 are complete,
-// one word of R_t, kept in the register row (and stored for the output).
-__device__ __forceinline__ void mask_flush(const MaskArgs& a, int v, const MScan& sc, u32x32& Rrow, uint32_t* rrow_t) {
-  if ((v & 31) == 0) {
-    Rrow[v >> 5] = sc.Rwin;
-    if (rrow_t) rrow_t[(size_t)(v >> 5) * a.kpad] = sc.Rwin;
-  }
 }
 
 // The loads node v-1 needs, issued while node v is decided: its record and
 // operands, and the dependency words node v's record lists for it.
 __device__ __forceinline__ MNode mask_fetch(const MaskArgs& a, const u32x8& rec_v, cptr<uint64_t> s1row) {
-  const uint32_t roff = rec_v[7], f = rec_v[6];
+  const uint32_t off = rec_v[7], f = rec_v[6];
   MNode nx;
-  nx.rec = sload<u32x8>(a.mrecs, roff);
+  nx.rec = sload<u32x8>(a.mnodes, off);
   nx.d0 = sload<uint64_t>(s1row, f & 0xFFFFu);
   nx.d1 = sload<uint64_t>(s1row, f >> 16);
-  const auto rs = mval_rsrc(a);
-  nx.mc = load_mval<0>(rs, roff * 2u);
-  nx.dm = load_mval<16>(rs, roff * 2u);
+  const auto rs = mnode_rsrc(a);
+  nx.mc = load_mval<32>(rs, off);
+  nx.dm = load_mval<48>(rs, off);
   return nx;
 }
 
 // Node v at position P of its block (P = v & 3), with the next node's loads
-// issued first; at P = 0 they include the next block's words. The loads
-// alternate between two buffers by position (node v's in buf[P & 1], node
-// v-1's into the other), so nothing moves from one to the other.
+// issued first; at P = 0 they include the next block's words, into Bn0 and
+// Bn1 (the current block is in B0, B1). The loads alternate between two
+// buffers by position (node v's in buf[P & 1], node v-1's into the other),
+// so nothing moves from one to the other.
 template <int P, bool kTop>
-__device__ __forceinline__ void mask_step(const MaskArgs& a, int t, int v, MNode (&buf)[2], u32x8& B0, u32x8& B1,
-                                          cptr<uint64_t> s0row, cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow,
-                                          uint32_t* rrow_t) {
+__device__ __forceinline__ void mask_step(const MaskArgs& a, int t, int v, MNode (&buf)[2], const u32x8& B0,
+                                          const u32x8& B1, u32x8& Bn0, u32x8& Bn1, cptr<uint64_t> s0row,
+                                          cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow, uint32_t* rrow_t) {
   constexpr int kCur = P & 1, kNext = kCur ^ 1;
   const uint64_t S0 = mpair(B0, P), S1 = mpair(B1, P);
   const u32x8& rec = buf[kCur].rec;
   buf[kNext] = mask_fetch(a, rec, s1row);
   if (P == 0) {
-    // block c-1 starts (c - 1) * 32 bytes into a row: record v-1's byte
-    // offset is (4c - 1) * 32, so (rec[7] >> 2) & ~31 (0 for c = 0)
-    const uint32_t boff = (rec[7] >> 2) & ~31u;
-    B0 = sload<u32x8>(s0row, boff);
-    B1 = sload<u32x8>(s1row, boff);
+    // block c-1 starts 32 (c - 1) bytes into a row; rec[7] = 128 (4c - 1),
+    // so (rec[7] >> 4) & ~31 (0 for c = 0)
+    const uint32_t boff = (rec[7] >> 4) & ~31u;
+    Bn0 = sload<u32x8>(s0row, boff);
+    Bn1 = sload<u32x8>(s1row, boff);
   }
   mask_node<kTop>(a, t, v, buf[kCur], S0, S1, s1row, sc, Rrow);
-  if (P == 0) mask_flush(a, v, sc, Rrow, rrow_t);
+  if (P == 0 && (v & 31) == 0) {
+    // the R bits of nodes v .. v+31 are complete: one word of R_t, kept in
+    // the register row (and stored for the output)
+    Rrow[v >> 5] = sc.Rwin;
+    if (rrow_t) rrow_t[(size_t)(v >> 5) * a.kpad] = sc.Rwin;
+  }
 }
 
+// Block c (nodes 4c+3 down to 4c) from B0, B1; block c-1 loaded into Bn0, Bn1.
 template <bool kTop>
-__device__ __forceinline__ void mask_block(const MaskArgs& a, int t, int c, MNode (&buf)[2], u32x8& B0, u32x8& B1,
-                                           cptr<uint64_t> s0row, cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow,
-                                           uint32_t* rrow_t) {
-  mask_step<3, kTop>(a, t, 4 * c + 3, buf, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
-  mask_step<2, kTop>(a, t, 4 * c + 2, buf, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
-  mask_step<1, kTop>(a, t, 4 * c + 1, buf, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
-  mask_step<0, kTop>(a, t, 4 * c, buf, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
+__device__ __forceinline__ void mask_block(const MaskArgs& a, int t, int c, MNode (&buf)[2], const u32x8& B0,
+                                           const u32x8& B1, u32x8& Bn0, u32x8& Bn1, cptr<uint64_t> s0row,
+                                           cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow, uint32_t* rrow_t) {
+  mask_step<3, kTop>(a, t, 4 * c + 3, buf, B0, B1, Bn0, Bn1, s0row, s1row, sc, Rrow, rrow_t);
+  mask_step<2, kTop>(a, t, 4 * c + 2, buf, B0, B1, Bn0, Bn1, s0row, s1row, sc, Rrow, rrow_t);
+  mask_step<1, kTop>(a, t, 4 * c + 1, buf, B0, B1, Bn0, Bn1, s0row, s1row, sc, Rrow, rrow_t);
+  mask_step<0, kTop>(a, t, 4 * c, buf, B0, B1, Bn0, Bn1, s0row, s1row, sc, Rrow, rrow_t);
 }
 
 // One wave per work item: the 64 candidates of group blockIdx.x over the
@@ -1795,15 +1802,21 @@ __global__ void __launch_bounds__(kWave) ckm_mask_eval_kernel(MaskArgs a) {
     sc.maxv = -INFINITY;
     sc.cost = 0.0;
     sc.Rwin = 0u;
-    // the scan starts at the top of t's block: node v0 = 4c + 3, whose loads
-    // record v0 + 1 names
+    // the scan starts at the top of t's block: node 4c + 3, whose loads node
+    // 4c + 4's record names
     const int c = t >> 2;
     MNode buf[2];
-    const u32x8 top = a.mrecs[4 * c + 4];
+    const u32x8 top = a.mnodes[(size_t)(4 * c + 4) * (kMNodeBytes / 32)];
     buf[1] = mask_fetch(a, top, s1row);
-    u32x8 B0 = load_blk(s0row, c), B1 = load_blk(s1row, c);
-    mask_block<true>(a, t, c, buf, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
-    for (int cc = c - 1; cc >= 0; --cc) mask_block<false>(a, t, cc, buf, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
+    const u32x8 T0 = sload<u32x8>(s0row, 32u * c), T1 = sload<u32x8>(s1row, 32u * c);
+    u32x8 A0, A1, B0, B1;
+    mask_block<true>(a, t, c, buf, T0, T1, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
+    int cc = c - 1;
+    for (; cc >= 1; cc -= 2) {
+      mask_block<false>(a, t, cc, buf, B0, B1, A0, A1, s0row, s1row, sc, Rrow, rrow_t);
+      mask_block<false>(a, t, cc - 1, buf, A0, A1, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
+    }
+    if (cc == 0) mask_block<false>(a, t, 0, buf, B0, B1, A0, A1, s0row, s1row, sc, Rrow, rrow_t);
     seg_peak = fmax(seg_peak, sc.U0 - sc.Y + sc.maxv);
     seg_cost += (int64_t)sc.cost;
   }
@@ -1830,20 +1843,16 @@ __device__ __forceinline__ uint32_t put_masks(uint32_t v, const uint64_t (&m)[8]
   return v;
 }
 
-// Randomized rounding into mask rows: block (group, row r), lane = candidate.
-// Word i of row r is the group's 64 decisions [u_{k,r,i} < q[r][i]] (the
-// same draws as round_word); candidate 0 takes the deterministic bits under
+// Randomized rounding into mask row r of a group, lane = candidate. Word i
+// of the row is the group's 64 decisions [u_{k,r,i} < q[r][i]] (the same
+// draws as round_word); candidate 0 takes the deterministic bits under
 // CKM_F_DET0. A block of 8 nodes shares one Philox output per lane.
-__global__ void __launch_bounds__(kWave) ckm_round_masks_kernel(const uint32_t* __restrict__ q,
-                                                                const uint32_t* __restrict__ det, int32_t n,
-                                                                int32_t ldq, int32_t det_words, uint32_t key0,
-                                                                uint32_t key1, uint32_t det0, size_t mgroup,
-                                                                uint64_t* __restrict__ mrows) {
+__device__ __forceinline__ void round_mask_row(const uint32_t* __restrict__ q, const uint32_t* __restrict__ det,
+                                               int32_t n, int32_t ldq, int32_t det_words, uint32_t key0,
+                                               uint32_t key1, uint32_t det0, int group, int r, uint64_t* row) {
   const int lane = threadIdx.x;
-  const int group = blockIdx.x;
-  const int r = blockIdx.y;   // 0 .. n (row n: zero)
   const uint32_t k = (uint32_t)(group * kWave + lane);
-  uint32_t* dst = reinterpret_cast<uint32_t*>(mrows + (size_t)group * mgroup + mrow_off(r));
+  uint32_t* dst = reinterpret_cast<uint32_t*>(row);
   const int nblk = (r >> 3) + 1;
   const cptr<uint32_t> qrow = as_const(q + (size_t)(r < n ? r : 0) * ldq);
   const cptr<uint32_t> drow = as_const(det + (size_t)(r < n ? r : 0) * det_words);
@@ -1869,6 +1878,20 @@ __global__ void __launch_bounds__(kWave) ckm_round_masks_kernel(const uint32_t* 
     const uint32_t out = put_masks<0>(0u, m);
     if (lane < 16) dst[16 * b + lane] = out;   // words 8b .. 8b+7 of the row
   }
+}
+
+// Block (group, y) makes rows y and n - y of the group (rows 0 .. n; row n
+// is zero), so that every block has about the same number of node blocks.
+__global__ void __launch_bounds__(kWave) ckm_round_masks_kernel(const uint32_t* __restrict__ q,
+                                                                const uint32_t* __restrict__ det, int32_t n,
+                                                                int32_t ldq, int32_t det_words, uint32_t key0,
+                                                                uint32_t key1, uint32_t det0, size_t mgroup,
+                                                                uint64_t* __restrict__ mrows) {
+  const int group = blockIdx.x;
+  const int y = blockIdx.y;
+  uint64_t* rows = mrows + (size_t)group * mgroup;
+  round_mask_row(q, det, n, ldq, det_words, key0, key1, det0, group, n - y, rows + mrow_off(n - y));
+  if (y != n - y) round_mask_row(q, det, n, ldq, det_words, key0, key1, det0, group, y, rows + mrow_off(y));
 }
 
 template <typename T>
@@ -1951,7 +1974,7 @@ hipError_t launch_round_rows(const ckm_graph& g, const Layout& L, int32_t K, uin
                              char* work, hipStream_t stream) {
   if (!L.rows_on) return hipSuccess;
   if (use_mask_path(g, L)) {
-    hipLaunchKernelGGL(ckm_round_masks_kernel, dim3(groups_of(K), g.n + 1), dim3(kWave), 0, stream,
+    hipLaunchKernelGGL(ckm_round_masks_kernel, dim3(groups_of(K), g.n / 2 + 1), dim3(kWave), 0, stream,
                        at<const uint32_t>(work, L.q_off), at<const uint32_t>(work, L.det_off), g.n, L.ldq,
                        L.det_words, (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32),
                        (flags & CKM_F_DET0) ? 1u : 0u, mask_rows_words(g.n), at<uint64_t>(work, L.rows_off));
@@ -2013,9 +2036,7 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
     m.mgroup = mask_rows_words(g.n);
     m.mrows = as_const(at<const uint64_t>(work, L.rows_off));
     m.np = mask_padded_nodes(g.n);
-    m.mrecs = (cptr<u32x8>)(g.d_mrecs);
-    m.mvals = reinterpret_cast<const uint4*>(static_cast<const char*>(g.d_mrecs) +
-                                             (size_t)2 * m.np * kMRecDwords * sizeof(uint32_t));
+    m.mnodes = (cptr<u32x8>)(g.d_mrecs);
     m.rrows = at<uint32_t>(work, L.rrows_off);
     m.kpad = a.kpad;
     m.part_peak = at<int64_t>(work, L.part_peak_off);
@@ -2199,21 +2220,24 @@ static bool build_ext_lists(int32_t v, const int64_t* M, bool wide, const int32_
   return true;
 }
 
-int32_t mask_records_bytes(int32_t n) {
-  return mask_padded_nodes(n) * (2 * kMRecDwords * (int32_t)sizeof(uint32_t) + kMValBytes);
-}
+int32_t mask_records_bytes(int32_t n) { return mask_padded_nodes(n) * kMNodeBytes; }
 
 bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int32_t* dep_ptr,
                         const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx, void* out) {
   const int32_t np = mask_padded_nodes(n);
-  uint32_t* recs = static_cast<uint32_t*>(out);
-  double* vals = reinterpret_cast<double*>(recs + (size_t)2 * np * kMRecDwords);
+  char* base = static_cast<char*>(out);
   memset(out, 0, (size_t)mask_records_bytes(n));
+  auto far = [](int u) { return (uint32_t)u << 16 | (uint32_t)(u & 31); };
+  for (int32_t v = 0; v < np; ++v) {   // no far references, padded nodes included
+    uint32_t* r = reinterpret_cast<uint32_t*>(base + (size_t)v * kMNodeBytes);
+    r[1] = r[3] = r[5] = r[24 + 1] = r[24 + 3] = kMNoFar;
+  }
   for (int32_t v = 0; v < n; ++v) {
-    uint32_t* r = recs + (size_t)v * kMRecDwords;
-    uint32_t* r2 = recs + (size_t)(np + v) * kMRecDwords;
-    double* val = vals + (size_t)v * (kMValBytes / sizeof(double));
-    uint32_t ctrl = 0;
+    char* node = base + (size_t)v * kMNodeBytes;
+    uint32_t* r = reinterpret_cast<uint32_t*>(node);
+    double* val = reinterpret_cast<double*>(node + 32);
+    uint32_t* r2 = reinterpret_cast<uint32_t*>(node + 96);
+    uint32_t ctrl = kMNoFar;   // stays, or names the one far user
     int nfar = 0;
     for (int32_t e = user_ptr[v]; e < user_ptr[v + 1]; ++e) {
       const int u = user_idx[e];
@@ -2221,7 +2245,7 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
         r[0] |= 1u << (u - v - 1);
       } else {
         if (nfar++) return false;
-        ctrl |= kMFarU | (uint32_t)(u >> 5) << 8 | (uint32_t)(u & 31) << 16;
+        ctrl = far(u);
       }
     }
     const int nd = dep_ptr[v + 1] - dep_ptr[v];
@@ -2235,7 +2259,8 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
     for (int sl = 0; sl < nd; ++sl) {
       const int i = dep_idx[dep_ptr[v] + sl];
       uint32_t* w = sl < 2 ? r + 2 + 2 * sl : r2 + 2 * (sl - 2);
-      uint32_t ref = (uint32_t)i;
+      if (sl >= 2) r2[5 + (sl - 2)] = (uint32_t)i * 8u;
+      uint32_t ref = kMNoFar;
       int nlate = 0;
       for (int32_t e = user_ptr[i]; e < user_ptr[i + 1]; ++e) {
         const int u = user_idx[e];
@@ -2244,7 +2269,7 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
           w[0] |= 1u << (u - v - 1);
         } else {
           if (nlate++) return false;
-          ref |= kMRefFar | (uint32_t)(u >> 5) << 13 | (uint32_t)(u & 31) << 20;
+          ref = far(u);
         }
       }
       w[1] = ref;
@@ -2253,7 +2278,7 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
     r[1] = ctrl;
   }
   // fetch lists: record v (padded ones included) names the S_{t+1} words of
-  // node v-1's slots 0 and 1, and where record v-1 is
+  // node v-1's slots 0 and 1, and where node v-1's data is
   for (int32_t v = 1; v < np; ++v) {
     const int32_t u = v - 1;
     uint32_t f = 0;
@@ -2262,10 +2287,11 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
       if (nd >= 1) f |= (uint32_t)dep_idx[dep_ptr[u]] * 8u;
       if (nd >= 2) f |= (uint32_t)dep_idx[dep_ptr[u] + 1] * 8u << 16;
     }
-    recs[(size_t)v * kMRecDwords + 6] = f;
-    recs[(size_t)v * kMRecDwords + 7] = (uint32_t)u * (uint32_t)(kMRecDwords * sizeof(uint32_t));
+    uint32_t* r = reinterpret_cast<uint32_t*>(base + (size_t)v * kMNodeBytes);
+    r[6] = f;
+    r[7] = (uint32_t)u * (uint32_t)kMNodeBytes;
   }
-  return true;   // record 0 keeps fetch list 0 and word 7 = 0
+  return true;   // node 0 keeps fetch list 0 and word 7 = 0
 }
 
 void build_node_records(int32_t n, const int64_t* M, const int64_t* C, bool wide, const int32_t* dep_ptr,
