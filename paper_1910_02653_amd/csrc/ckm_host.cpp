@@ -448,9 +448,21 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
     if (!ckm::build_mask_records(n, bytes, cost, dp.data(), di.data(), up.data(), ui.data(), mrecs.data()))
       mrecs.clear();
   }
-  const size_t total = align256(off_mrec + mrecs.size());
+  // else the seen path's node data, when the graph fits it
+  std::vector<char> snodes;
+  std::vector<uint32_t> sover;
+  int32_t seen_words = 0;
+  if (mrecs.empty() && !wide &&
+      !ckm::build_seen_records(n, bytes, cost, dp.data(), di.data(), up.data(), ui.data(), snodes, sover,
+                               seen_words))
+    snodes.clear();
+  const size_t off_snode = align256(off_mrec + mrecs.size());
+  const size_t off_sover = align256(off_snode + snodes.size());
+  const size_t total = align256(off_sover + sover.size() * sizeof(uint32_t));
   std::vector<char> host(total, 0);
   if (!mrecs.empty()) memcpy(host.data() + off_mrec, mrecs.data(), mrecs.size());
+  if (!snodes.empty()) memcpy(host.data() + off_snode, snodes.data(), snodes.size());
+  if (!sover.empty()) memcpy(host.data() + off_sover, sover.data(), sover.size() * sizeof(uint32_t));
   memcpy(host.data() + off_M, bytes, n * sizeof(int64_t));
   memcpy(host.data() + off_C, cost, n * sizeof(int64_t));
   memcpy(host.data() + off_up, up.data(), (n + 1) * sizeof(int32_t));
@@ -472,7 +484,9 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
     delete g;
     return fail_hip(e, "hipGetDevice");
   }
-  g->eval_waves = ckm::eval_waves_per_cu(n, wide);
+  g->eval_waves = !mrecs.empty()    ? ckm::mask_waves_per_cu()
+                  : !snodes.empty() ? ckm::seen_waves_per_cu(seen_words)
+                                    : ckm::eval_waves_per_cu(n, wide);
   // the work area of ckm_round_eval_noalloc on this device, resolved once
   e = ckm::noalloc_setup(g->device);
   if (e != hipSuccess) {
@@ -501,6 +515,9 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
   g->d_dep_upos = reinterpret_cast<const int32_t*>(base + off_uo);
   g->d_recs = base + off_rec;
   g->d_mrecs = mrecs.empty() ? nullptr : base + off_mrec;
+  g->d_snodes = snodes.empty() ? nullptr : base + off_snode;
+  g->d_sover = snodes.empty() || sover.empty() ? nullptr : base + off_sover;
+  g->seen_words = seen_words;
   g->sync = new (std::nothrow) ckm::SyncCache;
   if (!g->sync) {
     (void)hipFree(g->d_mem);

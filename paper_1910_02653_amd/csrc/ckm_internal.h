@@ -5,6 +5,7 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <vector>
 
 #include "ckm.h"
 
@@ -35,6 +36,9 @@ struct ckm_graph {
   const int32_t* d_dep_upos = nullptr;
   const void* d_recs = nullptr;  // n node records of ckm::kNodeRecBytes (see ckm_kernels.hip)
   const void* d_mrecs = nullptr; // mask-path records (mask_records_bytes) when the graph fits them, else NULL
+  const void* d_snodes = nullptr; // else the seen path's node data, when the graph fits it
+  const void* d_sover = nullptr;  // and its overflow entries (NULL when there are none)
+  int32_t seen_words = 0;         // seen bits per lane / 32 on the seen path
   ckm::SyncCache* sync = nullptr;  // reused by the synchronous calls; freed with the graph
 };
 
@@ -77,6 +81,16 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
                         const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx, void* out);
 // Words of one candidate group's mask rows (rows 0 .. n).
 size_t mask_rows_words(int32_t n);
+// Node data of the seen path (see ckm_kernels.hip) for graphs of up to
+// kSeenMaxNodes nodes: (n + 1) x 128 bytes, the overflow entries (8 dwords
+// each) and the seen words per lane; false when n is too large.
+constexpr int32_t kSeenMaxNodes = 4096;
+bool build_seen_records(int32_t n, const int64_t* M, const int64_t* C, const int32_t* dep_ptr,
+                        const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx,
+                        std::vector<char>& nodes, std::vector<uint32_t>& over, int32_t& seen_words);
+// Resident waves per CU of the mask and seen evaluate kernels.
+int32_t mask_waves_per_cu();
+int32_t seen_waves_per_cu(int32_t seen_words);
 
 // Work-buffer layout for (n, K). Offsets are bytes from the buffer start,
 // each 256-byte aligned.

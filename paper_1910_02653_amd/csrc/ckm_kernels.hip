@@ -1894,6 +1894,241 @@ __global__ void __launch_bounds__(kWave) ckm_round_masks_kernel(const uint32_t* 
   if (y != n - y) round_mask_row(q, det, n, ldq, det_words, key0, key1, det0, group, y, rows + mrow_off(y));
 }
 
+// ---------------------------------------------------------------------------
+// Seen path: the mask path for graphs of up to 4096 nodes with any number of
+// users and dependencies per node. What a node needs from users more than 32
+// nodes above it goes through a per-lane "seen" bit of the used node: when a
+// far user u of node x (u > x + 32) is decided, it ORs R_t[u] into x's seen
+// bit. When the scan reaches x, the bit holds R_t of x's far users (all above
+// it), and when a user v of x looks for users of x computed after v, the bit
+// holds those of x's far users above v (a far user within 32 above v is also
+// in v's R window). Near users stay in the window, as in the mask path. The
+// seen bits are numbered over the nodes that have a far user: W words per
+// lane in LDS (word w of lane j at byte 256 w + 4 j), cleared at each stage.
+//
+// Node v's data, 128 bytes at 128 v (v = 0 .. n; node n has only the fetch
+// block for node n-1):
+//   [0, 64)   record, 16 dwords (one scalar load):
+//     0  users u of v with u <= v + 32 (bit u - v - 1)
+//     1  v's seen bit (0 when v has no far user)
+//     2  slots 2-3 present (bit 0) | overflow list present (bit 1) | its
+//        length << 8
+//     3  seen writes of slots 0 (low half) and 1 (high half): the LDS byte
+//        offset of the dependency's seen word | kSWrite when v is a far user
+//        of the dependency
+//     4, 5  slot 0: lm (users u of the dependency with v < u <= v + 32, bit
+//           u - v - 1), the dependency's seen bit (0: it has no far user)
+//     6, 7  slot 1
+//     8  first overflow entry (dependencies beyond the fourth)
+//     fetch block, for node v-1 (all zero for v = 0):
+//     9  byte offsets in a mask row of the S_{t+1} words of v-1's slot 0 and
+//        1 dependencies (low, high half) | kSExtNext: v-1 has slots 2-3
+//     10 the same for slots 2 and 3
+//     11 128 (v - 1)
+//     12 LDS byte offsets of v-1's seen word | of its slot 0 dependency's << 16
+//     13 slot 1 | slot 2 << 16
+//     14 slot 3
+//     15 seen writes of slots 2 and 3 (as word 3)
+//   [64, 112) binary64 M_v, C_v, M of slots 0-3
+//   [112, 128) slots 2 and 3: lm, seen bit each
+// An absent slot has lm = 0, no seen bit and size 0: it frees nothing.
+// Overflow entries, 32 bytes: lm, seen bit, seen write (as word 3), byte
+// offset of the S_{t+1} word, LDS byte offset of the seen word, M (binary64).
+// All loads for node v-1 take their addresses from node v's record, so they
+// are issued after it has arrived, one batch per node.
+constexpr int kSNodeBytes = 128;
+constexpr uint32_t kSExt = 1u, kSOver = 2u, kSWrite = 0x8000u, kSExtNext = 0x8000u;
+
+typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+struct SeenArgs {
+  int32_t n, K, items, kind, P, T0, R1, R2;   // work plan (see Plan)
+  int32_t np;                                 // node data entries: n + 1
+  int32_t seen_words;                         // W
+  double base;                                // M_in + 2 M_param
+  size_t mgroup;                              // words of one group's mask rows
+  cptr<uint64_t> mrows;                       // S masks, group-major
+  cptr<u32x16> snodes;                        // np x 128 bytes of node data
+  cptr<u32x8> over;                           // overflow entries
+  uint32_t* __restrict__ rrows;               // R rows out (row array layout)
+  int32_t kpad;
+  int64_t* __restrict__ part_peak;
+  int64_t* __restrict__ part_cost;
+  int32_t* __restrict__ hdr;
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t snode_rsrc(const SeenArgs& a) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<u32x16*>((const u32x16*)a.snodes), 0, a.np * kSNodeBytes,
+                                           kBufWord3);
+}
+// The lane's word at LDS byte offset off (off wave-uniform, a multiple of 256).
+__device__ __forceinline__ uint32_t seen_read(char* lds_lane, uint32_t off) {
+  return *reinterpret_cast<const uint32_t*>(lds_lane + off);
+}
+__device__ __forceinline__ void seen_or(char* lds_lane, uint32_t off, uint32_t bits) {
+  atomicOr(reinterpret_cast<uint32_t*>(lds_lane + off), bits);
+}
+
+// What node v needs, all requested while node v+1 is decided.
+struct SNode {
+  u32x16 rec;
+  uint64_t S0, S1;          // S_t[v], S_{t+1}[v]
+  uint64_t d0, d1, d2, d3;  // S_{t+1} words of the slot 0-3 dependencies
+  u32x4 ext;                // slots 2-3
+  uint32_t has_ext;
+  uint4 mc, dm, dm2;        // M_v, C_v | M of slots 0, 1 | M of slots 2, 3
+  uint32_t sv, s0, s1, s2, s3;   // seen words of v and of the slot dependencies
+};
+
+__device__ __forceinline__ SNode seen_fetch(const SeenArgs& a, const u32x16& rec_v, cptr<uint64_t> s0row,
+                                            cptr<uint64_t> s1row, char* lds_lane) {
+  const uint32_t off = rec_v[11], f01 = rec_v[9];
+  SNode nx;
+  nx.rec = sload<u32x16>(a.snodes, off);
+  nx.S0 = sload<uint64_t>(s0row, off >> 4);   // 8 (v - 1)
+  nx.S1 = sload<uint64_t>(s1row, off >> 4);
+  nx.d0 = sload<uint64_t>(s1row, f01 & 0x7FFFu);
+  nx.d1 = sload<uint64_t>(s1row, f01 >> 16);
+  const auto rs = snode_rsrc(a);
+  nx.mc = load_mval<64>(rs, off);
+  nx.dm = load_mval<80>(rs, off);
+  nx.sv = seen_read(lds_lane, rec_v[12] & 0xFFFFu);
+  nx.s0 = seen_read(lds_lane, rec_v[12] >> 16);
+  nx.s1 = seen_read(lds_lane, rec_v[13] & 0xFFFFu);
+  nx.has_ext = f01 & kSExtNext;
+  if (nx.has_ext) {
+    const uint32_t f23 = rec_v[10];
+    nx.d2 = sload<uint64_t>(s1row, f23 & 0xFFFFu);
+    nx.d3 = sload<uint64_t>(s1row, f23 >> 16);
+    nx.ext = sload<u32x4>(a.snodes, off + 112);
+    nx.dm2 = load_mval<96>(rs, off);
+    nx.s2 = seen_read(lds_lane, rec_v[13] >> 16);
+    nx.s3 = seen_read(lds_lane, rec_v[14]);
+  }
+  return nx;
+}
+
+struct SScan {
+  double U0, Y, maxv, cost;
+  uint32_t Rwin;   // R bits of nodes v+1 .. v+32 (bit d <-> node v + 1 + d)
+};
+
+// One dependency slot of node v (see mask_slot): later users of the
+// dependency are those in v's R window (lm) and those its seen bit holds.
+// Then, when v is a far user of the dependency, R_t[v] goes into its bit.
+__device__ __forceinline__ double seen_slot(double val, uint64_t R, bool rb, uint32_t lm, uint32_t bit, uint32_t sw,
+                                            uint64_t s1i, double Mi, uint32_t Rwin, uint32_t wr, char* lds_lane) {
+  const uint32_t y = (Rwin & lm) | (sw & bit);
+  const uint64_t later = mask_of(y != 0u);
+  const uint64_t fr = R & ~(s1i | later);
+  val = madd_m(val, fr, Mi);
+  if (wr & kSWrite) seen_or(lds_lane, wr & 0x7FFFu, rb ? bit : 0u);
+  return val;
+}
+
+// Node v of stage t (see mask_node). kTop: v = t.
+template <bool kTop>
+__device__ __forceinline__ void seen_node(const SeenArgs& a, const SNode& nd, cptr<uint64_t> s1row, SScan& sc,
+                                          char* lds_lane) {
+  const u32x16& r = nd.rec;
+  const double Mv = dbl(nd.mc.x, nd.mc.y), Cv = dbl(nd.mc.z, nd.mc.w);
+  const uint32_t x = (sc.Rwin & r[0]) | (nd.sv & r[1]);
+  const uint64_t x1 = nd.S1 | mask_of(x != 0u);
+  uint64_t R = x1 & ~nd.S0;
+  sc.U0 = madd_m(sc.U0, nd.S0, Mv);
+  if (!kTop && R == 0ull) {
+    // no candidate computes v (see mask_node)
+    sc.Rwin = sc.Rwin + sc.Rwin;
+    return;
+  }
+  double val = sc.Y;
+  if (kTop) {
+    R = ~0ull;
+    val = madd_m(val, ~x1, Mv);
+  }
+  const bool rb = lane_of(R);
+  val = seen_slot(val, R, rb, r[4], r[5], nd.s0, nd.d0, dbl(nd.dm.x, nd.dm.y), sc.Rwin, r[3] & 0xFFFFu, lds_lane);
+  val = seen_slot(val, R, rb, r[6], r[7], nd.s1, nd.d1, dbl(nd.dm.z, nd.dm.w), sc.Rwin, r[3] >> 16, lds_lane);
+  if (nd.has_ext) {
+    val = seen_slot(val, R, rb, nd.ext[0], nd.ext[1], nd.s2, nd.d2, dbl(nd.dm2.x, nd.dm2.y), sc.Rwin,
+                    r[15] & 0xFFFFu, lds_lane);
+    val = seen_slot(val, R, rb, nd.ext[2], nd.ext[3], nd.s3, nd.d3, dbl(nd.dm2.z, nd.dm2.w), sc.Rwin, r[15] >> 16,
+                    lds_lane);
+  }
+  if (__builtin_expect((r[2] & kSOver) != 0u, 0)) {
+    // dependencies beyond the fourth, one entry at a time
+    const uint32_t cnt = r[2] >> 8;
+    for (uint32_t c = 0, e = r[8]; c < cnt; ++c, ++e) {
+      const u32x8 en = a.over[e];
+      const uint64_t s1i = sload<uint64_t>(s1row, en[3]);
+      const uint32_t sw = seen_read(lds_lane, en[4]);
+      val = seen_slot(val, R, rb, en[0], en[1], sw, s1i, dbl(en[5], en[6]), sc.Rwin, en[2], lds_lane);
+    }
+  }
+  // suffix form of the U recurrence (see scan_node): val = Y + freed_v
+  sc.maxv = max_f64(sc.maxv, val);
+  const double sel = rb ? 1.0 : 0.0;
+  sc.Y = fma(-sel, Mv, val);
+  sc.cost = fma(sel, Cv, sc.cost);
+  sc.Rwin = sc.Rwin + sc.Rwin + (rb ? 1u : 0u);
+}
+
+// Node v from buf[P] (P: its parity in the scan), node v-1's loads into
+// buf[P ^ 1] first.
+template <int P, bool kTop>
+__device__ __forceinline__ void seen_step(const SeenArgs& a, int v, SNode (&buf)[2], cptr<uint64_t> s0row,
+                                          cptr<uint64_t> s1row, SScan& sc, char* lds_lane, uint32_t* rrow_t) {
+  buf[P ^ 1] = seen_fetch(a, buf[P].rec, s0row, s1row, lds_lane);
+  seen_node<kTop>(a, buf[P], s1row, sc, lds_lane);
+  if ((v & 31) == 0) rrow_t[(size_t)(v >> 5) * a.kpad] = sc.Rwin;   // R of nodes v .. v+31
+}
+
+// One wave per work item: the 64 candidates of group blockIdx.x over the
+// stages of item blockIdx.y; the scan of stage t runs from node t down.
+__global__ void __launch_bounds__(kWave) ckm_seen_eval_kernel(SeenArgs a) {
+  extern __shared__ uint32_t seen_lds[];
+  const int lane = threadIdx.x;
+  const int group = blockIdx.x;
+  const int item = blockIdx.y;
+  const uint32_t k = (uint32_t)(group * kWave + lane);
+  char* lds_lane = reinterpret_cast<char*>(seen_lds) + 4 * lane;
+  int t0, t1;
+  item_range(a, item, t0, t1);
+  const cptr<uint64_t> rows = a.mrows + (size_t)group * a.mgroup;
+  double seg_peak = -INFINITY;
+  int64_t seg_cost = 0;
+  for (int t = t0; t < t1; ++t) {
+    for (int w = 0; w < a.seen_words; ++w) *reinterpret_cast<uint32_t*>(lds_lane + 256 * w) = 0u;
+    const cptr<uint64_t> s0row = rows + mrow_off(t);
+    const cptr<uint64_t> s1row = rows + mrow_off(t + 1);
+    uint32_t* rrow_t = a.rrows + row_base(t) * (size_t)a.kpad + k;
+    SScan sc;
+    sc.U0 = (double)a.base;
+    sc.Y = 0.0;
+    sc.maxv = -INFINITY;
+    sc.cost = 0.0;
+    sc.Rwin = 0u;
+    SNode buf[2];
+    const u32x16 top = a.snodes[(size_t)(t + 1) * (kSNodeBytes / 64)];   // its fetch block: node t
+    buf[1] = seen_fetch(a, top, s0row, s1row, lds_lane);
+    seen_step<1, true>(a, t, buf, s0row, s1row, sc, lds_lane, rrow_t);
+    int v = t - 1;
+    for (; v >= 1; v -= 2) {
+      seen_step<0, false>(a, v, buf, s0row, s1row, sc, lds_lane, rrow_t);
+      seen_step<1, false>(a, v - 1, buf, s0row, s1row, sc, lds_lane, rrow_t);
+    }
+    if (v == 0) seen_step<0, false>(a, 0, buf, s0row, s1row, sc, lds_lane, rrow_t);
+    seg_peak = fmax(seg_peak, sc.U0 - sc.Y + sc.maxv);
+    seg_cost += (int64_t)sc.cost;
+  }
+  if ((int)k < a.K && t0 < t1) {
+    atomicMax(reinterpret_cast<long long*>(a.part_peak) + k, (long long)seg_peak);
+    atomicAdd(reinterpret_cast<unsigned long long*>(a.part_cost) + k, (unsigned long long)seg_cost);
+  }
+  if (group == 0 && item == 0 && lane == 0) a.hdr[0] = a.items;
+}
+
 template <typename T>
 T* at(char* work, size_t off) { return reinterpret_cast<T*>(work + off); }
 
@@ -1966,7 +2201,27 @@ int32_t eval_waves_per_cu(int32_t n, bool wide) {
 
 static unsigned groups_of(int32_t K) { return (unsigned)((K + kWave - 1) / kWave); }
 
-static bool use_mask_path(const ckm_graph& g, const Layout& L) { return L.rows_on && g.d_mrecs != nullptr; }
+static bool use_mask_path(const ckm_graph& g, const Layout& L) {
+  return L.rows_on && (g.d_mrecs != nullptr || g.d_snodes != nullptr);
+}
+
+int32_t mask_waves_per_cu() {
+  int blocks = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, (const void*)ckm_mask_eval_kernel, kWave, 0) !=
+          hipSuccess ||
+      blocks < 1)
+    blocks = 1;
+  return blocks;
+}
+
+int32_t seen_waves_per_cu(int32_t seen_words) {
+  int blocks = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, (const void*)ckm_seen_eval_kernel, kWave,
+                                                   (size_t)seen_words * 256) != hipSuccess ||
+      blocks < 1)
+    blocks = 1;
+  return blocks;
+}
 
 size_t mask_rows_words(int32_t n) { return mrow_off(n + 1); }
 
@@ -2021,6 +2276,34 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
     hipLaunchKernelGGL(ckm_user_rows_kernel, dim3(groups_of(K), g.n), dim3(256), tile, stream, a.s_user, g.n, K,
                        a.s_words, a.kpad, at<uint32_t>(work, L.rows_off));
     src = kSrcRows;
+  }
+  if (mask_path && g.d_snodes) {
+    SeenArgs m;
+    m.n = g.n;
+    m.K = K;
+    m.items = plan.items;
+    m.kind = plan.kind;
+    m.P = plan.P;
+    m.T0 = plan.T0;
+    m.R1 = plan.R1;
+    m.R2 = plan.R2;
+    m.np = g.n + 1;
+    m.seen_words = g.seen_words;
+    m.base = (double)g.base;
+    m.mgroup = mask_rows_words(g.n);
+    m.mrows = as_const(at<const uint64_t>(work, L.rows_off));
+    m.snodes = (cptr<u32x16>)(g.d_snodes);
+    m.over = (cptr<u32x8>)(g.d_sover);
+    m.rrows = at<uint32_t>(work, L.rrows_off);
+    m.kpad = a.kpad;
+    m.part_peak = at<int64_t>(work, L.part_peak_off);
+    m.part_cost = at<int64_t>(work, L.part_cost_off);
+    m.hdr = at<int32_t>(work, L.hdr_off);
+    hipLaunchKernelGGL(ckm_eval_init_kernel, dim3((K + 255) / 256), dim3(256), 0, stream, K, m.part_peak,
+                       m.part_cost);
+    hipLaunchKernelGGL(ckm_seen_eval_kernel, dim3((K + kWave - 1) / kWave, plan.items), dim3(kWave),
+                       (size_t)g.seen_words * 256, stream, m);
+    return hipGetLastError();
   }
   if (mask_path) {
     MaskArgs m;
@@ -2292,6 +2575,95 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
     r[7] = (uint32_t)u * (uint32_t)kMNodeBytes;
   }
   return true;   // node 0 keeps fetch list 0 and word 7 = 0
+}
+
+bool build_seen_records(int32_t n, const int64_t* M, const int64_t* C, const int32_t* dep_ptr,
+                        const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx,
+                        std::vector<char>& nodes, std::vector<uint32_t>& over, int32_t& seen_words) {
+  if (n < 1 || n > kSeenMaxNodes) return false;
+  // seen bits: the nodes with a user more than 32 above them, in order
+  std::vector<int32_t> slot(n, -1);
+  int32_t ns = 0;
+  for (int32_t x = 0; x < n; ++x)
+    for (int32_t e = user_ptr[x]; e < user_ptr[x + 1]; ++e)
+      if (user_idx[e] - x - 1 >= 32) {
+        slot[x] = ns++;
+        break;
+      }
+  seen_words = std::max<int32_t>(1, (ns + 31) / 32);
+  auto soff = [&](int32_t x) { return slot[x] < 0 ? 0u : (uint32_t)(slot[x] >> 5) * 256u; };
+  auto sbit = [&](int32_t x) { return slot[x] < 0 ? 0u : 1u << (slot[x] & 31); };
+  const int32_t np = n + 1;
+  nodes.assign((size_t)np * kSNodeBytes, 0);
+  over.clear();
+  for (int32_t v = 0; v < n; ++v) {
+    char* node = nodes.data() + (size_t)v * kSNodeBytes;
+    uint32_t* r = reinterpret_cast<uint32_t*>(node);
+    double* val = reinterpret_cast<double*>(node + 64);
+    uint32_t* ext = reinterpret_cast<uint32_t*>(node + 112);
+    for (int32_t e = user_ptr[v]; e < user_ptr[v + 1]; ++e) {
+      const int32_t u = user_idx[e];
+      if (u - v - 1 < 32) r[0] |= 1u << (u - v - 1);
+    }
+    r[1] = sbit(v);
+    val[0] = (double)M[v];
+    val[1] = (double)C[v];
+    const int32_t nd = dep_ptr[v + 1] - dep_ptr[v];
+    uint32_t flags = nd > 2 ? kSExt : 0u;
+    if (nd > 4) {
+      flags |= kSOver | (uint32_t)(nd - 4) << 8;
+      r[8] = (uint32_t)(over.size() / 8);
+    }
+    r[2] = flags;
+    for (int32_t sl = 0; sl < nd; ++sl) {
+      const int32_t i = dep_idx[dep_ptr[v] + sl];
+      uint32_t lm = 0;
+      for (int32_t e = user_ptr[i]; e < user_ptr[i + 1]; ++e) {
+        const int32_t u = user_idx[e];
+        if (u > v && u - v - 1 < 32) lm |= 1u << (u - v - 1);
+      }
+      const uint32_t wr = v - i - 1 >= 32 ? (soff(i) | kSWrite) : 0u;
+      if (sl < 2) {
+        r[4 + 2 * sl] = lm;
+        r[5 + 2 * sl] = sbit(i);
+        r[3] |= wr << (16 * sl);
+        val[2 + sl] = (double)M[i];
+      } else if (sl < 4) {
+        ext[2 * (sl - 2)] = lm;
+        ext[2 * (sl - 2) + 1] = sbit(i);
+        r[15] |= wr << (16 * (sl - 2));
+        val[2 + sl] = (double)M[i];
+      } else {
+        const double mi = (double)M[i];
+        uint32_t mw[2];
+        memcpy(mw, &mi, sizeof(mw));
+        const uint32_t en[8] = {lm, sbit(i), wr, (uint32_t)i * 8u, soff(i), mw[0], mw[1], 0u};
+        over.insert(over.end(), en, en + 8);
+      }
+    }
+  }
+  // fetch blocks: node v's record describes node v-1's loads
+  for (int32_t v = 1; v < np; ++v) {
+    const int32_t u = v - 1;
+    const int32_t nd = dep_ptr[u + 1] - dep_ptr[u];
+    auto dep = [&](int32_t sl) { return dep_idx[dep_ptr[u] + sl]; };
+    uint32_t* r = reinterpret_cast<uint32_t*>(nodes.data() + (size_t)v * kSNodeBytes);
+    uint32_t f01 = 0, f23 = 0;
+    if (nd >= 1) f01 |= (uint32_t)dep(0) * 8u;
+    if (nd >= 2) f01 |= (uint32_t)dep(1) * 8u << 16;
+    if (nd >= 3) {
+      f01 |= kSExtNext;
+      f23 |= (uint32_t)dep(2) * 8u;
+    }
+    if (nd >= 4) f23 |= (uint32_t)dep(3) * 8u << 16;
+    r[9] = f01;
+    r[10] = f23;
+    r[11] = (uint32_t)u * (uint32_t)kSNodeBytes;
+    r[12] = soff(u) | (nd >= 1 ? soff(dep(0)) : 0u) << 16;
+    r[13] = (nd >= 2 ? soff(dep(1)) : 0u) | (nd >= 3 ? soff(dep(2)) : 0u) << 16;
+    r[14] = nd >= 4 ? soff(dep(3)) : 0u;
+  }
+  return true;
 }
 
 void build_node_records(int32_t n, const int64_t* M, const int64_t* C, bool wide, const int32_t* dep_ptr,
