@@ -16,8 +16,12 @@ written once and read once: 4 * n * ceil(n/64) * 8 bytes per candidate.
 actually bounds it: VALU instructions per launch (committed rocprofv3
 counters of the current kernel source, else null) x 64 lanes / the launch
 time, against 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz.
+`roofline_step` prices the whole timed step with the same bytes.
 `cpu_baseline` times the CPU oracle on a bounded sample of the same
-workload, on every host thread (candidates split across them) and on one.
+workload (about 15 s of wall time, whole passes over the candidates), on the host threads a one-GPU job is
+granted (16, or fewer when the affinity set is smaller; candidates split
+across them) and on one thread, with the CPU model, the machine's logical
+CPU count and the affinity set recorded.
 `hbm_copy` is the bandwidth a plain device copy reaches on the same GPU, the
 achievable line beside the 8 TB/s peak. `host_round_trip` times the
 synchronous call that takes S* from host memory and returns host results
@@ -79,45 +83,85 @@ def measured_counters():
     return d
 
 
-def host_threads() -> int:
-    """CPU threads for the oracle: this process's CPU set, at most 16."""
+# Host threads granted to one GPU's job on the GPU machines this runs on.
+HOST_THREADS_PER_GPU = 16
+
+
+def host_info():
+    """CPU model, logical CPUs of the machine, CPUs this process may run on."""
+    model = "unknown"
     try:
-        n = len(os.sched_getaffinity(0))
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        affinity = len(os.sched_getaffinity(0))
     except AttributeError:
-        n = os.cpu_count() or 1
-    return max(1, min(16, n))
+        affinity = os.cpu_count() or 1
+    return {"cpu_model": model, "nproc": os.cpu_count() or 1, "affinity_cpus": affinity}
 
 
-def cpu_baseline(w, sample: int, single: int):
+def host_threads() -> int:
+    """Oracle threads: the CPUs of this process's affinity set, at most the
+    16 host threads a one-GPU job is granted (more would contend with other
+    jobs on the same host, whatever the affinity set shows)."""
+    return max(1, min(HOST_THREADS_PER_GPU, host_info()["affinity_cpus"]))
+
+
+def cpu_baseline(w, sample: int, single: int, target_s: float = 15.0):
     """The oracle on candidates 0 .. sample-1 of the workload, split by
-    candidate over every host thread (each thread runs the unmodified oracle
+    candidate over the oracle threads (each thread runs the unmodified oracle
     on its own candidates; candidates are independent), and on candidates
-    0 .. single-1 in one thread."""
+    0 .. single-1 in one thread. Each run takes whole passes over its
+    candidates until about target_s seconds (the multi-thread run) or a third
+    of that (the single thread) have passed, at least one pass."""
     from concurrent.futures import ThreadPoolExecutor
 
     from oracle import ref
     q = ref.quantize(w.s_frac)
     threads = host_threads()
 
-    def run(ks):
-        for k in ks:
-            ref.eval_candidate(w, k, q=q)
+    def passes(ks, seconds):
+        """Whole passes over ks until `seconds` have passed: candidates done."""
+        done = 0
+        end = time.perf_counter() + seconds
+        while True:
+            for k in ks:
+                ref.eval_candidate(w, k, q=q)
+            done += len(ks)
+            if time.perf_counter() >= end:
+                return done
 
     t = time.perf_counter()
-    run(range(single))
+    ref.eval_candidate(w, 0, q=q)
+    one = time.perf_counter() - t
+    # fewer candidates where one pass over them would take much longer
+    single = max(1, min(single, int(target_s / 3 / one)))
+    sample = max(threads, min(sample, int(target_s * threads / one)))
+    t = time.perf_counter()
+    n1 = passes(range(single), target_s / 3)
     dt1 = time.perf_counter() - t
     chunks = [range(i, sample, threads) for i in range(threads)]
     t = time.perf_counter()
     with ThreadPoolExecutor(threads) as ex:
-        list(ex.map(run, chunks))
+        done = sum(ex.map(lambda ks: passes(ks, target_s), chunks))
     dt = time.perf_counter() - t
-    return {"value": sample / dt, "unit": "candidates/s", "cores": threads, "kind": "oracle",
-            "sample": "candidates 0-%d of the same %d-candidate transformer workload (n=%d): "
-                      "rounding + Algorithm 2 repair + literal U/FREE simulation per candidate, "
+    info = host_info()
+    return {"value": done / dt, "unit": "candidates/s", "cores": threads, "kind": "oracle",
+            "stage_evals_per_s": done * w.n / dt,
+            "sample": "%d candidate evaluations over candidates 0-%d of the same %d-candidate workload "
+                      "(%s, n=%d): rounding + Algorithm 2 repair + literal U/FREE simulation per candidate, "
                       "%d threads (candidates split across them), %.1f s wall"
-                      % (sample - 1, w.K, w.n, threads, dt),
-            "single_thread": {"value": single / dt1, "unit": "candidates/s", "cores": 1,
-                              "sample": "candidates 0-%d, %.1f s" % (single - 1, dt1)}}
+                      % (done, sample - 1, w.K, w.name, w.n, threads, dt),
+            "host": dict(info, threads_used=threads,
+                         thread_cap="at most %d: the host threads a one-GPU job is granted" % HOST_THREADS_PER_GPU),
+            "single_thread": {"value": n1 / dt1, "unit": "candidates/s", "cores": 1,
+                              "sample": "%d candidate evaluations over candidates 0-%d, %.1f s"
+                                        % (n1, single - 1, dt1)}}
 
 
 def copy_bandwidth(stream, nbytes: int = 1 << 30, reps: int = 10):
@@ -497,6 +541,9 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic},
+        "roofline_step": {"bound": "hbm", "achieved": K * b_cand / (ms_step * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+                          "unit": "GB/s", "frac": K * b_cand / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                          "note": "the same algorithmic bytes over the whole timed step"},
         "roofline_alu": ({"bound": "alu", "achieved": valu * 64 / (eval_avg_ms * 1e-3) / 1e12,
                           "peak": ALU_PEAK_TOPS, "unit": "T lane-ops/s",
                           "frac": valu * 64 / (eval_avg_ms * 1e-3) / 1e12 / ALU_PEAK_TOPS,
