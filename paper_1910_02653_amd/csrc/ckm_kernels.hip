@@ -1827,12 +1827,13 @@ __global__ void __launch_bounds__(kWave) ckm_mask_eval_kernel(MaskArgs a) {
   if (group == 0 && item == 0 && lane == 0) a.hdr[0] = a.items;
 }
 
-// Lane L of v takes the wave-uniform x (v_writelane_b32 with the lane as an
-// inline constant).
+// v_writelane_b32 through its compiler intrinsic, so that the compiler sees
+// the instruction and its hazards (this compiler has no builtin for it).
+__device__ int amdgcn_writelane(int x, int lane, int v) __asm("llvm.amdgcn.writelane.i32");
+// Lane L of v takes the wave-uniform x.
 template <int L>
 __device__ __forceinline__ uint32_t write_lane(uint32_t v, uint32_t x) {
-  asm("v_writelane_b32 %0, %1, %2" : "+v"(v) : "s"(x), "i"(L));
-  return v;
+  return (uint32_t)amdgcn_writelane((int)x, L, (int)v);
 }
 // Lanes 2j and 2j+1 take the low and high halves of m[j], j >= J.
 template <int J>
