@@ -1,0 +1,103 @@
+"""Parity of the seen path with the oracle: graphs the mask records cannot
+hold (more than 1023 nodes, more than four dependencies of a node, more than
+one user more than 32 nodes above a node or a dependency), so their rounding
+path evaluates with far relations kept as per-lane seen bits in LDS.
+
+Hand-built and seeded graphs put the path's limits to work: a node with 120
+far users, a dependency with dozens of far later users, a node with 60
+dependencies (the overflow list), slots 2-3, and seen rows of 1 to 127 words.
+Small graphs are compared over every candidate; large ones on sampled
+candidates, the argmin and the best rows.
+"""
+import numpy as np
+import pytest
+
+from paper_1910_02653_amd import workloads as wl
+from test_gpu_parity import check_full, check_rows, gpu_round_eval, lexi_best, log, oracle_candidates
+
+pytestmark = pytest.mark.gpu
+
+
+def workload(name, deps, seed, K, m_in=5, m_param=3):
+    n = len(deps)
+    ptr, idx = wl.csr_from_deps([sorted(d) for d in deps])
+    rng = np.random.default_rng(seed)
+    size = rng.integers(1, 1000, n).astype(np.int64)
+    cost = rng.integers(1, 1000, n).astype(np.int64)
+    return wl.Workload(name, n, ptr, idx, cost, size, m_in, m_param, wl.s_frac_uniform(n, seed), K, seed, 1 << 40)
+
+
+def hub_graph():
+    """300 nodes on a chain, plus: node 5 used by 121 nodes from 40 up (far
+    users of one node); node 10 used by 251 .. 299, so node 250's slot for it
+    sees up to 48 far later users; node 250 with 3 dependencies (slots 2-3)
+    and node 290 with 60 (the overflow list)."""
+    n = 300
+    deps = [set() if v == 0 else {v - 1} for v in range(n)]
+    for u in range(40, 281, 2):
+        deps[u].add(5)
+    deps[250] |= {10, 11}
+    for u in range(251, 300):
+        deps[u].add(10)
+    deps[290] |= set(range(0, 240, 4))
+    return workload("hub", deps, seed=300, K=70)
+
+
+def test_hub_graph_all_candidates():
+    w = hub_graph()
+    log("seen path: hub graph n=%d K=%d" % (w.n, w.K))
+    peak, _ = check_full(w, gpu_round_eval(w))
+    med = int(np.median(peak))
+    check_full(w, gpu_round_eval(w, budget=med), budget=med)
+
+
+def test_fan_in_fan_out_all_candidates():
+    """A random DAG with up to 12 dependencies per node and users anywhere above."""
+    w = wl.random_dag(200, seed=17, K=96, max_deg=12, window=200, max_size=1000, max_cost=1000,
+                      s_kind="uniform", budget_pct=60.0)
+    log("seen path: fan-in/out n=%d K=%d" % (w.n, w.K))
+    peak, _ = check_full(w, gpu_round_eval(w))
+    med = int(np.median(peak))
+    check_full(w, gpu_round_eval(w, budget=med), budget=med)
+
+
+def sampled(w, ks=(0, 1, 33, 63, 64, 69)):
+    got = gpu_round_eval(w)
+    orc = oracle_candidates(w, list(ks))
+    for k in ks:
+        assert (int(got["peak"][k]), int(got["cost"][k])) == orc[k], k
+    budget = int(np.median(got["peak"]))
+    got2 = gpu_round_eval(w, budget=budget)
+    assert np.array_equal(got2["peak"], got["peak"]) and np.array_equal(got2["cost"], got["cost"])
+    bk = lexi_best(got2["peak"], got2["cost"], budget)
+    assert got2["best_k"] == bk >= 0
+    assert (int(got2["peak"][bk]), int(got2["cost"][bk])) == oracle_candidates(w, [bk])[bk]
+    check_rows(w, got2, bk)
+
+
+def test_mirrored_training_graph():
+    """A random forward DAG of 750 ops (1-3 predecessors within 16) with its
+    mirrored backward pass: n = 1501, every forward op far-used by its
+    gradient."""
+    rng = np.random.default_rng(1501)
+    F = 750
+    fwd = [[]] + [sorted(set(rng.integers(max(0, v - 16), v, rng.integers(1, 4)).tolist())) for v in range(1, F)]
+    deps, size, cost, _ = wl.mirror_training_graph(fwd, rng.integers(1, 1 << 20, F), rng.integers(1, 5000, F), 4, 7)
+    ptr, idx = wl.csr_from_deps(deps)
+    n = len(deps)
+    w = wl.Workload("mirror1501", n, ptr, idx, np.asarray(cost, np.int64), np.asarray(size, np.int64), 1 << 20,
+                    1 << 19, wl.s_frac_uniform(n, 5), 70, 5, 1 << 40)
+    log("seen path: mirrored n=%d" % n)
+    sampled(w)
+
+
+def test_seen_row_of_127_words():
+    """n = 4096 (the largest graph), every node used 40 nodes above it: 4056
+    seen bits, 127 words per lane."""
+    n = 4096
+    deps = [set() if v == 0 else {v - 1} for v in range(n)]
+    for v in range(40, n):
+        deps[v].add(v - 40)
+    w = workload("skip40", deps, seed=4096, K=70)
+    log("seen path: n=%d, 127 seen words" % n)
+    sampled(w, ks=(0, 63, 69))
