@@ -1560,12 +1560,11 @@ __host__ __device__ __forceinline__ size_t mrow_off(int t) {
 }
 
 // Node v's data, 128 bytes at 128 v:
-//   [0, 32)   record, 8 dwords (one scalar load)
-//   [32, 96)  binary64 operands M_v, C_v and M of dependency slots 0-3,
-//             read by vector-memory loads into every lane
-//   [96, 128) slots 2-3 (nodes with three or four dependencies): lm, ref of
+//   [0, 64)   record, 16 dwords (one scalar load)
+//   [64, 96)  slots 2-3 (nodes with three or four dependencies): lm, ref of
 //             slot 2, of slot 3, dependency count, byte offsets in a mask
 //             row of the S_{t+1} words of the slot 2 and 3 dependencies
+//   [96, 112) binary64 M of slots 2 and 3
 // A far reference names a node u more than 32 above v as u << 16 | (u & 31)
 // (none: 0xFFFF << 16). Its R bit matters only when u <= t, i.e. when the
 // field is below (t + 1) << 16: a node above t computes nothing in stage t.
@@ -1586,15 +1585,19 @@ __host__ __device__ __forceinline__ size_t mrow_off(int t) {
 //      v-1 take their addresses from here, so that they cannot be issued
 //      before node v's record has arrived: scalar loads complete out of
 //      order, and a wait for that record would wait for them as well.
-// Blocks of four nodes are aligned (nodes 4c .. 4c+3). A stage's scan
-// starts at the top of its node's block; the nodes above t there (and past
-// n - 1, whose data is padded with empty nodes up to np = round_up(n, 4) +
-// 4) compute nothing and hold nothing, so they leave every sum unchanged.
+//   8-15: binary64 M_v, C_v, M of slots 0 and 1, used from scalar registers
+//      (the vector registers they would take are worth a wave per SIMD)
+// Pairs of nodes are aligned (nodes 2c, 2c+1). A stage's scan starts at the
+// top of its node's pair; a node above t there (or past n - 1, whose data is
+// padded with empty nodes up to np = round_up(n, 4) + 4) computes nothing
+// and holds nothing, so it leaves every sum unchanged.
 constexpr uint32_t kMNoFar = 0xFFFFu << 16, kMRare = 1u << 8;
 constexpr int kMNodeBytes = 128;
 __host__ __device__ __forceinline__ int mask_padded_nodes(int n) { return ((n + 3) & ~3) + 4; }
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
 
 struct MaskArgs {
   int32_t n, K, items, kind, P, T0, R1, R2;   // work plan (see Plan)
@@ -1602,7 +1605,7 @@ struct MaskArgs {
   double base;                                // M_in + 2 M_param
   size_t mgroup;                              // words of one group's mask rows
   cptr<uint64_t> mrows;                       // S masks, group-major
-  cptr<u32x8> mnodes;                         // np x 128 bytes of node data
+  cptr<u32x16> mnodes;                        // np x 128 bytes of node data
   uint32_t* __restrict__ rrows;               // R rows out (row array layout), or NULL
   int32_t kpad;
   int64_t* __restrict__ part_peak;
@@ -1624,10 +1627,6 @@ __device__ __forceinline__ double madd_m(double acc, uint64_t m, double x) {
 template <typename T, typename B>
 __device__ __forceinline__ T sload(cptr<B> base, uint32_t off) {
   return *(const __attribute__((address_space(4))) T*)((const __attribute__((address_space(4))) char*)base + off);
-}
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t mnode_rsrc(const MaskArgs& a) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<u32x8*>((const u32x8*)a.mnodes), 0, a.np * kMNodeBytes,
-                                           kBufWord3);
 }
 // 16 bytes at byte offset off + kOff of the node data, in every lane
 template <int kOff>
@@ -1667,9 +1666,8 @@ __device__ __forceinline__ double mask_slot(double val, uint64_t R, uint32_t lm,
 // slot 0 and 1 dependencies and its binary64 operands (M_v, C_v | M of slots
 // 0, 1), all requested one node ahead.
 struct MNode {
-  u32x8 rec;
+  u32x16 rec;
   uint64_t d0, d1;
-  uint4 mc, dm;
 };
 
 // Node v of stage t for the 64 candidates of a group: S0, S1 are the words
@@ -1682,10 +1680,10 @@ struct MNode {
 template <bool kTop>
 __device__ __forceinline__ void mask_node(const MaskArgs& a, int t, int v, const MNode& nd, uint64_t S0, uint64_t S1,
                                           cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow) {
-  const u32x8& rec = nd.rec;
+  const u32x16& rec = nd.rec;
   const uint32_t ctrl = rec[1];
   const uint32_t tlim = (uint32_t)(t + 1) << 16;
-  const double Mv = dbl(nd.mc.x, nd.mc.y), Cv = dbl(nd.mc.z, nd.mc.w);
+  const double Mv = dbl(rec[8], rec[9]), Cv = dbl(rec[10], rec[11]);
   uint32_t x = sc.Rwin & rec[0];
   if (__builtin_expect(ctrl < tlim, 0)) x |= far_bit(Rrow, ctrl);
   const uint64_t x1 = S1 | mask_of(x != 0u);
@@ -1702,15 +1700,15 @@ __device__ __forceinline__ void mask_node(const MaskArgs& a, int t, int v, const
     R = ~0ull;
     val = madd_m(val, ~x1, Mv);
   }
-  val = mask_slot(val, R, rec[2], rec[3], dbl(nd.dm.x, nd.dm.y), nd.d0, sc.Rwin, Rrow, tlim);
-  val = mask_slot(val, R, rec[4], rec[5], dbl(nd.dm.z, nd.dm.w), nd.d1, sc.Rwin, Rrow, tlim);
+  val = mask_slot(val, R, rec[2], rec[3], dbl(rec[12], rec[13]), nd.d0, sc.Rwin, Rrow, tlim);
+  val = mask_slot(val, R, rec[4], rec[5], dbl(rec[14], rec[15]), nd.d1, sc.Rwin, Rrow, tlim);
   if (__builtin_expect((ctrl & kMRare) != 0u, 0)) {
     const uint32_t off = (uint32_t)v * kMNodeBytes;
-    const u32x8 r2 = sload<u32x8>(a.mnodes, off + 96);
-    const uint4 m23 = load_mval<64>(mnode_rsrc(a), off);
-    val = mask_slot(val, R, r2[0], r2[1], dbl(m23.x, m23.y), sload<uint64_t>(s1row, r2[5]), sc.Rwin, Rrow, tlim);
+    const u32x8 r2 = sload<u32x8>(a.mnodes, off + 64);
+    const u32x4 m23 = sload<u32x4>(a.mnodes, off + 96);
+    val = mask_slot(val, R, r2[0], r2[1], dbl(m23[0], m23[1]), sload<uint64_t>(s1row, r2[5]), sc.Rwin, Rrow, tlim);
     if (r2[4] >= 4)
-      val = mask_slot(val, R, r2[2], r2[3], dbl(m23.z, m23.w), sload<uint64_t>(s1row, r2[6]), sc.Rwin, Rrow, tlim);
+      val = mask_slot(val, R, r2[2], r2[3], dbl(m23[2], m23[3]), sload<uint64_t>(s1row, r2[6]), sc.Rwin, Rrow, tlim);
   }
   // suffix form of the U recurrence (see scan_node): val = Y + freed_v
   sc.maxv = max_f64(sc.maxv, val);
@@ -1721,39 +1719,37 @@ __device__ __forceinline__ void mask_node(const MaskArgs& a, int t, int v, const
   sc.Rwin = sc.Rwin + sc.Rwin + (rb ? 1u : 0u);
 }
 
-// The loads node v-1 needs, issued while node v is decided: its record and
-// operands, and the dependency words node v's record lists for it.
-__device__ __forceinline__ MNode mask_fetch(const MaskArgs& a, const u32x8& rec_v, cptr<uint64_t> s1row) {
+// The loads node v-1 needs, issued while node v is decided: its record (with
+// its operands), and the dependency words node v's record lists for it.
+__device__ __forceinline__ MNode mask_fetch(const MaskArgs& a, const u32x16& rec_v, cptr<uint64_t> s1row) {
   const uint32_t off = rec_v[7], f = rec_v[6];
   MNode nx;
-  nx.rec = sload<u32x8>(a.mnodes, off);
+  nx.rec = sload<u32x16>(a.mnodes, off);
   nx.d0 = sload<uint64_t>(s1row, f & 0xFFFFu);
   nx.d1 = sload<uint64_t>(s1row, f >> 16);
-  const auto rs = mnode_rsrc(a);
-  nx.mc = load_mval<32>(rs, off);
-  nx.dm = load_mval<48>(rs, off);
   return nx;
 }
 
-// Node v at position P of its block (P = v & 3), with the next node's loads
-// issued first; at P = 0 they include the next block's words, into Bn0 and
-// Bn1 (the current block is in B0, B1). The loads alternate between two
-// buffers by position (node v's in buf[P & 1], node v-1's into the other),
-// so nothing moves from one to the other.
+// Node v at position P of its pair (P = v & 1), with the next node's loads
+// issued first; at P = 0 they include the next pair's words, into Bn0 and
+// Bn1 (the current pair is in B0, B1). The loads alternate between two
+// buffers by position (node v's in buf[P], node v-1's into the other), so
+// nothing moves from one to the other.
 template <int P, bool kTop>
-__device__ __forceinline__ void mask_step(const MaskArgs& a, int t, int v, MNode (&buf)[2], const u32x8& B0,
-                                          const u32x8& B1, u32x8& Bn0, u32x8& Bn1, cptr<uint64_t> s0row,
+__device__ __forceinline__ void mask_step(const MaskArgs& a, int t, int v, MNode (&buf)[2], const u32x4& B0,
+                                          const u32x4& B1, u32x4& Bn0, u32x4& Bn1, cptr<uint64_t> s0row,
                                           cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow, uint32_t* rrow_t) {
-  constexpr int kCur = P & 1, kNext = kCur ^ 1;
-  const uint64_t S0 = mpair(B0, P), S1 = mpair(B1, P);
-  const u32x8& rec = buf[kCur].rec;
+  constexpr int kCur = P, kNext = P ^ 1;
+  const uint64_t S0 = (uint64_t)B0[2 * P] | (uint64_t)B0[2 * P + 1] << 32;
+  const uint64_t S1 = (uint64_t)B1[2 * P] | (uint64_t)B1[2 * P + 1] << 32;
+  const u32x16& rec = buf[kCur].rec;
   buf[kNext] = mask_fetch(a, rec, s1row);
   if (P == 0) {
-    // block c-1 starts 32 (c - 1) bytes into a row; rec[7] = 128 (4c - 1),
-    // so (rec[7] >> 4) & ~31 (0 for c = 0)
-    const uint32_t boff = (rec[7] >> 4) & ~31u;
-    Bn0 = sload<u32x8>(s0row, boff);
-    Bn1 = sload<u32x8>(s1row, boff);
+    // pair c-1 starts 16 (c - 1) bytes into a row; rec[7] = 128 (2c - 1),
+    // so (rec[7] >> 4) & ~15 (0 for c = 0)
+    const uint32_t boff = (rec[7] >> 4) & ~15u;
+    Bn0 = sload<u32x4>(s0row, boff);
+    Bn1 = sload<u32x4>(s1row, boff);
   }
   mask_node<kTop>(a, t, v, buf[kCur], S0, S1, s1row, sc, Rrow);
   if (P == 0 && (v & 31) == 0) {
@@ -1764,15 +1760,13 @@ __device__ __forceinline__ void mask_step(const MaskArgs& a, int t, int v, MNode
   }
 }
 
-// Block c (nodes 4c+3 down to 4c) from B0, B1; block c-1 loaded into Bn0, Bn1.
+// Pair c (nodes 2c+1, 2c) from B0, B1; pair c-1 loaded into Bn0, Bn1.
 template <bool kTop>
-__device__ __forceinline__ void mask_block(const MaskArgs& a, int t, int c, MNode (&buf)[2], const u32x8& B0,
-                                           const u32x8& B1, u32x8& Bn0, u32x8& Bn1, cptr<uint64_t> s0row,
+__device__ __forceinline__ void mask_block(const MaskArgs& a, int t, int c, MNode (&buf)[2], const u32x4& B0,
+                                           const u32x4& B1, u32x4& Bn0, u32x4& Bn1, cptr<uint64_t> s0row,
                                            cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow, uint32_t* rrow_t) {
-  mask_step<3, kTop>(a, t, 4 * c + 3, buf, B0, B1, Bn0, Bn1, s0row, s1row, sc, Rrow, rrow_t);
-  mask_step<2, kTop>(a, t, 4 * c + 2, buf, B0, B1, Bn0, Bn1, s0row, s1row, sc, Rrow, rrow_t);
-  mask_step<1, kTop>(a, t, 4 * c + 1, buf, B0, B1, Bn0, Bn1, s0row, s1row, sc, Rrow, rrow_t);
-  mask_step<0, kTop>(a, t, 4 * c, buf, B0, B1, Bn0, Bn1, s0row, s1row, sc, Rrow, rrow_t);
+  mask_step<1, kTop>(a, t, 2 * c + 1, buf, B0, B1, Bn0, Bn1, s0row, s1row, sc, Rrow, rrow_t);
+  mask_step<0, kTop>(a, t, 2 * c, buf, B0, B1, Bn0, Bn1, s0row, s1row, sc, Rrow, rrow_t);
 }
 
 // One wave per work item: the 64 candidates of group blockIdx.x over the
@@ -1802,14 +1796,14 @@ __global__ void __launch_bounds__(kWave) ckm_mask_eval_kernel(MaskArgs a) {
     sc.maxv = -INFINITY;
     sc.cost = 0.0;
     sc.Rwin = 0u;
-    // the scan starts at the top of t's block: node 4c + 3, whose loads node
-    // 4c + 4's record names
-    const int c = t >> 2;
+    // the scan starts at the top of t's pair: node 2c + 1, whose loads node
+    // 2c + 2's record names
+    const int c = t >> 1;
     MNode buf[2];
-    const u32x8 top = a.mnodes[(size_t)(4 * c + 4) * (kMNodeBytes / 32)];
+    const u32x16 top = a.mnodes[(size_t)(2 * c + 2) * (kMNodeBytes / 64)];
     buf[1] = mask_fetch(a, top, s1row);
-    const u32x8 T0 = sload<u32x8>(s0row, 32u * c), T1 = sload<u32x8>(s1row, 32u * c);
-    u32x8 A0, A1, B0, B1;
+    const u32x4 T0 = sload<u32x4>(s0row, 16u * c), T1 = sload<u32x4>(s1row, 16u * c);
+    u32x4 A0, A1, B0, B1;
     mask_block<true>(a, t, c, buf, T0, T1, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
     int cc = c - 1;
     for (; cc >= 1; cc -= 2) {
@@ -1939,9 +1933,6 @@ __global__ void __launch_bounds__(kWave) ckm_round_masks_kernel(const uint32_t* 
 // are issued after it has arrived, one batch per node.
 constexpr int kSNodeBytes = 128;
 constexpr uint32_t kSExt = 1u, kSOver = 2u, kSWrite = 0x8000u, kSExtNext = 0x8000u;
-
-typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 struct SeenArgs {
   int32_t n, K, items, kind, P, T0, R1, R2;   // work plan (see Plan)
@@ -2320,7 +2311,7 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
     m.mgroup = mask_rows_words(g.n);
     m.mrows = as_const(at<const uint64_t>(work, L.rows_off));
     m.np = mask_padded_nodes(g.n);
-    m.mnodes = (cptr<u32x8>)(g.d_mrecs);
+    m.mnodes = (cptr<u32x16>)(g.d_mrecs);
     m.rrows = at<uint32_t>(work, L.rrows_off);
     m.kpad = a.kpad;
     m.part_peak = at<int64_t>(work, L.part_peak_off);
@@ -2512,15 +2503,16 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
   char* base = static_cast<char*>(out);
   memset(out, 0, (size_t)mask_records_bytes(n));
   auto far = [](int u) { return (uint32_t)u << 16 | (uint32_t)(u & 31); };
+  auto put = [](uint32_t* w, double x) { memcpy(w, &x, sizeof(x)); };
   for (int32_t v = 0; v < np; ++v) {   // no far references, padded nodes included
     uint32_t* r = reinterpret_cast<uint32_t*>(base + (size_t)v * kMNodeBytes);
-    r[1] = r[3] = r[5] = r[24 + 1] = r[24 + 3] = kMNoFar;
+    r[1] = r[3] = r[5] = r[16 + 1] = r[16 + 3] = kMNoFar;
   }
   for (int32_t v = 0; v < n; ++v) {
     char* node = base + (size_t)v * kMNodeBytes;
     uint32_t* r = reinterpret_cast<uint32_t*>(node);
-    double* val = reinterpret_cast<double*>(node + 32);
-    uint32_t* r2 = reinterpret_cast<uint32_t*>(node + 96);
+    uint32_t* r2 = reinterpret_cast<uint32_t*>(node + 64);
+    uint32_t* m23 = reinterpret_cast<uint32_t*>(node + 96);
     uint32_t ctrl = kMNoFar;   // stays, or names the one far user
     int nfar = 0;
     for (int32_t e = user_ptr[v]; e < user_ptr[v + 1]; ++e) {
@@ -2538,8 +2530,8 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
       ctrl |= kMRare;
       r2[4] = (uint32_t)nd;
     }
-    val[0] = (double)M[v];
-    val[1] = (double)C[v];
+    put(r + 8, (double)M[v]);
+    put(r + 10, (double)C[v]);
     for (int sl = 0; sl < nd; ++sl) {
       const int i = dep_idx[dep_ptr[v] + sl];
       uint32_t* w = sl < 2 ? r + 2 + 2 * sl : r2 + 2 * (sl - 2);
@@ -2557,7 +2549,7 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
         }
       }
       w[1] = ref;
-      val[2 + sl] = (double)M[i];
+      put(sl < 2 ? r + 12 + 2 * sl : m23 + 2 * (sl - 2), (double)M[i]);
     }
     r[1] = ctrl;
   }
