@@ -1838,6 +1838,25 @@ __device__ __forceinline__ uint32_t put_masks(uint32_t v, const uint64_t (&m)[8]
   return v;
 }
 
+// The 8 entries of block b of a row of thresholds (q or keys), read into
+// every lane by vector loads: they complete in order, so the next block's
+// can be requested while this one is in use (scalar loads complete out of
+// order, and waiting for one waits for all).
+struct Q8 {
+  uint4 lo, hi;
+  __device__ uint32_t operator[](int j) const {
+    const uint4& h = j < 4 ? lo : hi;
+    const int i = j & 3;
+    return i == 0 ? h.x : i == 1 ? h.y : i == 2 ? h.z : h.w;
+  }
+};
+__device__ __forceinline__ Q8 load_q8(__amdgpu_buffer_rsrc_t rs, uint32_t row_bytes, int b) {
+  Q8 x;
+  x.lo = load_mval<0>(rs, row_bytes + 32u * (uint32_t)b);
+  x.hi = load_mval<16>(rs, row_bytes + 32u * (uint32_t)b);
+  return x;
+}
+
 // Randomized rounding into mask row r of a group, lane = candidate. Word i
 // of the row is the group's 64 decisions [u_{k,r,i} < q[r][i]] (the same
 // draws as round_word); candidate 0 takes the deterministic bits under
@@ -1849,9 +1868,13 @@ __device__ __forceinline__ void round_mask_row(const uint32_t* __restrict__ q, c
   const uint32_t k = (uint32_t)(group * kWave + lane);
   uint32_t* dst = reinterpret_cast<uint32_t*>(row);
   const int nblk = (r >> 3) + 1;
-  const cptr<uint32_t> qrow = as_const(q + (size_t)(r < n ? r : 0) * ldq);
+  const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(q), 0, n * ldq * 4, kBufWord3);
+  const uint32_t row_bytes = (uint32_t)(r < n ? r : 0) * (uint32_t)ldq * 4u;
   const cptr<uint32_t> drow = as_const(det + (size_t)(r < n ? r : 0) * det_words);
+  Q8 qn = load_q8(rs, row_bytes, 0);
   for (int b = 0; b < nblk; ++b) {
+    const Q8 qb = qn;
+    if (b + 1 < nblk) qn = load_q8(rs, row_bytes, b + 1);
     uint64_t m[8];
     if (8 * b >= r) {
 #pragma unroll
@@ -1862,7 +1885,7 @@ __device__ __forceinline__ void round_mask_row(const uint32_t* __restrict__ q, c
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const uint32_t u = (x[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-        m[j] = mask_of(u < qrow[8 * b + j]);
+        m[j] = mask_of(u < qb[j]);
       }
       if (det0 && group == 0) {
         const uint32_t dw = drow[b >> 2] >> (8 * (b & 3));
@@ -2121,6 +2144,92 @@ __global__ void __launch_bounds__(kWave) ckm_seen_eval_kernel(SeenArgs a) {
   if (group == 0 && item == 0 && lane == 0) a.hdr[0] = a.items;
 }
 
+// Threshold candidates into mask rows (block (group, y): rows y and n - y):
+// word i of row r is the group's 64 decisions [rank_k < key[r][i]], the
+// threshold test of threshold_word. Keys on and above the diagonal are 0.
+__global__ void __launch_bounds__(kWave) ckm_threshold_masks_kernel(const uint32_t* __restrict__ key, int32_t ldq,
+                                                                    const uint32_t* __restrict__ rank, int32_t K,
+                                                                    int32_t n, size_t mgroup,
+                                                                    uint64_t* __restrict__ mrows) {
+  const int lane = threadIdx.x;
+  const int group = blockIdx.x;
+  const uint32_t k = (uint32_t)(group * kWave + lane);
+  const uint32_t rk = rank[k < (uint32_t)K ? k : (uint32_t)K - 1u];
+  uint64_t* rows = mrows + (size_t)group * mgroup;
+  const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(key), 0, n * ldq * 4, kBufWord3);
+  const int y = blockIdx.y;
+  for (int h = 0; h < 2; ++h) {
+    const int r = h == 0 ? n - y : y;
+    if (h == 1 && r == n - y) break;
+    uint32_t* dst = reinterpret_cast<uint32_t*>(rows + mrow_off(r));
+    const int lim = r < n ? r : 0;   // row n (after the last stage) is empty
+    const uint32_t row_bytes = (uint32_t)lim * (uint32_t)ldq * 4u;
+    const int nblk = (r >> 3) + 1;
+    Q8 kn = load_q8(rs, row_bytes, 0);
+    for (int b = 0; b < nblk; ++b) {
+      const Q8 kb = kn;
+      if (b + 1 < nblk) kn = load_q8(rs, row_bytes, b + 1);
+      uint64_t m[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) m[j] = 8 * b + j < lim ? mask_of(rk < kb[j]) : 0ull;
+      const uint32_t out = put_masks<0>(0u, m);
+      if (lane < 16) dst[16 * b + lane] = out;
+    }
+  }
+}
+
+// Caller-supplied checkpoint matrices into mask rows (block (group, y): rows
+// y and n - y): word i of row r is bit i of row r of each of the group's 64
+// matrices ([K][n][s_words] 32-bit words), for i < r only (bits on and above
+// the diagonal are not part of S). Lanes past K repeat candidate K-1. Each
+// lane reads its matrix row 16 bytes (128 nodes) at a time, the next chunk
+// requested before the current one is turned into masks.
+__device__ __forceinline__ uint4 user_chunk(const uint32_t* row, int c, int lim) {
+  // chunk c: words 4c .. 4c+3; only words with a node below lim are read
+  uint4 x = make_uint4(0u, 0u, 0u, 0u);
+  if (128 * c < lim) x.x = row[4 * c];
+  if (128 * c + 32 < lim) x.y = row[4 * c + 1];
+  if (128 * c + 64 < lim) x.z = row[4 * c + 2];
+  if (128 * c + 96 < lim) x.w = row[4 * c + 3];
+  return x;
+}
+
+__global__ void __launch_bounds__(kWave) ckm_user_masks_kernel(const uint32_t* __restrict__ s_user, int32_t n,
+                                                               int32_t K, int32_t s_words, size_t mgroup,
+                                                               uint64_t* __restrict__ mrows) {
+  const int lane = threadIdx.x;
+  const int group = blockIdx.x;
+  const uint32_t k = (uint32_t)(group * kWave + lane);
+  const uint32_t kk = k < (uint32_t)K ? k : (uint32_t)K - 1u;
+  uint64_t* rows = mrows + (size_t)group * mgroup;
+  const int y = blockIdx.y;
+  for (int h = 0; h < 2; ++h) {
+    const int r = h == 0 ? n - y : y;
+    if (h == 1 && r == n - y) break;
+    uint32_t* dst = reinterpret_cast<uint32_t*>(rows + mrow_off(r));
+    const int lim = r < n ? r : 0;   // row n (after the last stage) is empty
+    const uint32_t* src = s_user + ((size_t)kk * n + lim) * s_words;
+    const int nblk = (r >> 3) + 1;
+    uint4 cur = user_chunk(src, 0, lim);
+    for (int c = 0; 16 * c < nblk; ++c) {
+      const uint4 nxt = user_chunk(src, c + 1, lim);
+      const uint32_t w4[4] = {cur.x, cur.y, cur.z, cur.w};
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int b = 16 * c + q;
+        if (b >= nblk) break;
+        const uint32_t byte = w4[q >> 2] >> (8 * (q & 3));
+        uint64_t m[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) m[j] = 8 * b + j < lim ? mask_of(((byte >> j) & 1u) != 0u) : 0ull;
+        const uint32_t out = put_masks<0>(0u, m);
+        if (lane < 16) dst[16 * b + lane] = out;
+      }
+      cur = nxt;
+    }
+  }
+}
+
 template <typename T>
 T* at(char* work, size_t off) { return reinterpret_cast<T*>(work + off); }
 
@@ -2247,8 +2356,19 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
   a.rows = at<const uint32_t>(work, L.rows_off);
   a.rrows = L.rows_on ? at<uint32_t>(work, L.rrows_off) : nullptr;
   a.kpad = ((K + kWave - 1) / kWave) * kWave;
-  const bool mask_path = src == kSrcRound && use_mask_path(g, L);
-  if (src == kSrcRound && L.rows_on) {
+  const bool mask_path = use_mask_path(g, L);
+  if (mask_path && src == kSrcThreshold) {
+    // threshold candidates made once into mask rows
+    hipLaunchKernelGGL(ckm_threshold_masks_kernel, dim3(groups_of(K), g.n / 2 + 1), dim3(kWave), 0, stream,
+                       at<const uint32_t>(work, L.q_off), L.ldq, at<const uint32_t>(work, L.thr_rank_off), K, g.n,
+                       mask_rows_words(g.n), at<uint64_t>(work, L.rows_off));
+    src = kSrcRows;
+  } else if (mask_path && src == kSrcUser) {
+    // the caller's matrices gathered once into mask rows
+    hipLaunchKernelGGL(ckm_user_masks_kernel, dim3(groups_of(K), g.n / 2 + 1), dim3(kWave), 0, stream, a.s_user,
+                       g.n, K, a.s_words, mask_rows_words(g.n), at<uint64_t>(work, L.rows_off));
+    src = kSrcRows;
+  } else if (src == kSrcRound && L.rows_on) {
     // every row rounded once (here, or by an earlier launch_round_rows), then streamed
     if (!(flags & CKM_F_ROUNDED)) {
       hipError_t e = launch_round_rows(g, L, K, seed, flags, work, stream);
