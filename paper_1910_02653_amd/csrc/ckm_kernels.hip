@@ -2146,7 +2146,8 @@ __global__ void __launch_bounds__(kWave) ckm_seen_eval_kernel(SeenArgs a) {
 
 // Threshold candidates into mask rows (block (group, y): rows y and n - y):
 // word i of row r is the group's 64 decisions [rank_k < key[r][i]], the
-// threshold test of threshold_word. Keys on and above the diagonal are 0.
+// threshold test of threshold_word. Keys on and above the diagonal are 0, so
+// are their words (row n reads row 0, all of whose keys are 0).
 __global__ void __launch_bounds__(kWave) ckm_threshold_masks_kernel(const uint32_t* __restrict__ key, int32_t ldq,
                                                                     const uint32_t* __restrict__ rank, int32_t K,
                                                                     int32_t n, size_t mgroup,
@@ -2171,7 +2172,7 @@ __global__ void __launch_bounds__(kWave) ckm_threshold_masks_kernel(const uint32
       if (b + 1 < nblk) kn = load_q8(rs, row_bytes, b + 1);
       uint64_t m[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) m[j] = 8 * b + j < lim ? mask_of(rk < kb[j]) : 0ull;
+      for (int j = 0; j < 8; ++j) m[j] = mask_of(rk < kb[j]);   // keys at and above lim are 0
       const uint32_t out = put_masks<0>(0u, m);
       if (lane < 16) dst[16 * b + lane] = out;
     }
@@ -2218,10 +2219,13 @@ __global__ void __launch_bounds__(kWave) ckm_user_masks_kernel(const uint32_t* _
       for (int q = 0; q < 16; ++q) {
         const int b = 16 * c + q;
         if (b >= nblk) break;
-        const uint32_t byte = w4[q >> 2] >> (8 * (q & 3));
+        // the block's bits of nodes below lim only
+        const int below = lim - 8 * b;
+        const uint32_t keep = below >= 8 ? 0xFFu : below <= 0 ? 0u : (1u << below) - 1u;
+        const uint32_t byte = (w4[q >> 2] >> (8 * (q & 3))) & keep;
         uint64_t m[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) m[j] = 8 * b + j < lim ? mask_of(((byte >> j) & 1u) != 0u) : 0ull;
+        for (int j = 0; j < 8; ++j) m[j] = mask_of(((byte >> j) & 1u) != 0u);
         const uint32_t out = put_masks<0>(0u, m);
         if (lane < 16) dst[16 * b + lane] = out;
       }
