@@ -524,6 +524,19 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
     delete g;
     return fail(CKM_E_NOMEM, "out of host memory");
   }
+  // the side stream of the overlapped launches (seen-path graphs only)
+  if (g->d_snodes) {
+    g->fork = new (std::nothrow) ckm::Fork;
+    e = g->fork ? ckm::fork_create(*g->fork) : hipErrorOutOfMemory;
+    if (e != hipSuccess) {
+      delete g->fork;
+      g->sync->release();
+      delete g->sync;
+      (void)hipFree(g->d_mem);
+      delete g;
+      return fail_hip(e, "side stream");
+    }
+  }
   *out = g;
   return CKM_OK;
 }
@@ -531,6 +544,10 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
 void ckm_graph_destroy(ckm_graph* g) {
   if (!g) return;
   DeviceGuard dg(g->device);
+  if (g->fork) {
+    ckm::fork_destroy(*g->fork);
+    delete g->fork;
+  }
   if (g->sync) {
     g->sync->release();
     delete g->sync;
@@ -597,8 +614,8 @@ ckm_status ckm_round_async(const ckm_graph* g, int32_t K, uint64_t seed, uint32_
   return e == hipSuccess ? CKM_OK : fail_hip(e, "round launch");
 }
 
-ckm_status ckm_evaluate_async(const ckm_graph* g, int32_t K, uint64_t seed, uint32_t flags,
-                              int32_t stage_splits, void* d_work, size_t work_bytes, void* stream) {
+static ckm_status evaluate_impl(const ckm_graph* g, int32_t K, uint64_t seed, uint32_t flags,
+                                int32_t stage_splits, void* d_work, size_t work_bytes, void* stream, bool overlap) {
   Layout L;
   ckm_status st = check_work(g, K, d_work, work_bytes, &L);
   if (st != CKM_OK) return st;
@@ -610,8 +627,13 @@ ckm_status ckm_evaluate_async(const ckm_graph* g, int32_t K, uint64_t seed, uint
   DeviceGuard dg(g->device);
   if (!dg.ok) return fail(CKM_E_DEVICE, "cannot select the graph's device %d", g->device);
   hipError_t e = ckm::launch_evaluate(*g, L, K, seed, flags, plan, ckm::kSrcRound, nullptr,
-                                      static_cast<char*>(d_work), static_cast<hipStream_t>(stream));
+                                      static_cast<char*>(d_work), static_cast<hipStream_t>(stream), overlap);
   return e == hipSuccess ? CKM_OK : fail_hip(e, "evaluate launch");
+}
+
+ckm_status ckm_evaluate_async(const ckm_graph* g, int32_t K, uint64_t seed, uint32_t flags,
+                              int32_t stage_splits, void* d_work, size_t work_bytes, void* stream) {
+  return evaluate_impl(g, K, seed, flags, stage_splits, d_work, work_bytes, stream, true);
 }
 
 ckm_status ckm_select_async(const ckm_graph* g, int32_t K, uint64_t seed, int64_t budget,
@@ -639,6 +661,16 @@ ckm_status ckm_round_eval_async(const ckm_graph* g, const double* d_s_frac, int6
                                 int64_t* d_cost, uint8_t* d_feasible, int32_t* d_best_k,
                                 uint64_t* d_best_S, uint64_t* d_best_R, int32_t* d_status,
                                 void* d_work, size_t work_bytes, void* stream) {
+  return ckm::round_eval(g, d_s_frac, ld, K, seed, budget, flags, d_peak, d_cost, d_feasible, d_best_k, d_best_S,
+                         d_best_R, d_status, d_work, work_bytes, stream, true);
+}
+
+}  // extern "C"
+
+ckm_status ckm::round_eval(const ckm_graph* g, const double* d_s_frac, int64_t ld, int32_t K, uint64_t seed,
+                           int64_t budget, uint32_t flags, int64_t* d_peak, int64_t* d_cost, uint8_t* d_feasible,
+                           int32_t* d_best_k, uint64_t* d_best_S, uint64_t* d_best_R, int32_t* d_status,
+                           void* d_work, size_t work_bytes, void* stream, bool overlap) {
   Layout L;
   ckm_status st = check_work(g, K, d_work, work_bytes, &L);
   if (st != CKM_OK) return st;
@@ -648,11 +680,13 @@ ckm_status ckm_round_eval_async(const ckm_graph* g, const double* d_s_frac, int6
     return fail(CKM_E_INVALID_ARG, "NULL peak, cost, feasible or best_k");
   st = ckm_quantize_async(g, d_s_frac, ld, d_work, work_bytes, stream);
   if (st != CKM_OK) return st;
-  st = ckm_evaluate_async(g, K, seed, flags, 0, d_work, work_bytes, stream);
+  st = evaluate_impl(g, K, seed, flags, 0, d_work, work_bytes, stream, overlap);
   if (st != CKM_OK) return st;
   return ckm_select_async(g, K, seed, budget, flags, d_peak, d_cost, d_feasible, d_best_k,
                           d_best_S, d_best_R, d_status, d_work, work_bytes, stream);
 }
+
+extern "C" {
 
 ckm_status ckm_eval_schedules_async(const ckm_graph* g, const uint64_t* d_S, int32_t K, int64_t budget,
                                     int64_t* d_peak, int64_t* d_cost, uint8_t* d_feasible,

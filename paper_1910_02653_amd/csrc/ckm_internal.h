@@ -5,12 +5,14 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <mutex>
 #include <vector>
 
 #include "ckm.h"
 
 namespace ckm {
 struct SyncCache;  // buffers and stream of the synchronous entry points (ckm_host.cpp)
+struct Fork;       // second stream of the overlapped producer/evaluate launches
 }
 
 // Graph on the device. Node arrays hold sizes and costs as int64. Users
@@ -40,6 +42,7 @@ struct ckm_graph {
   const void* d_sover = nullptr;  // and its overflow entries (NULL when there are none)
   int32_t seen_words = 0;         // seen bits per lane / 32 on the seen path
   ckm::SyncCache* sync = nullptr;  // reused by the synchronous calls; freed with the graph
+  ckm::Fork* fork = nullptr;       // NULL: every launch on the caller's stream
 };
 
 namespace ckm {
@@ -148,6 +151,25 @@ Plan plan_splits(int32_t n, int32_t splits);
 // occupancy figure for the kernel variant and LDS size n and wide select).
 int32_t eval_waves_per_cu(int32_t n, bool wide);
 
+// A second stream and two events, made with a seen-path graph on its device,
+// over which launch_evaluate splits its candidate groups in two chunks: the
+// second chunk's producer and evaluate run beside the first chunk's evaluate.
+// The mutex keeps one call's record/wait sequence on the events whole.
+struct Fork {
+  std::mutex mu;
+  hipStream_t side = nullptr;
+  hipEvent_t forked = nullptr, joined = nullptr;
+};
+hipError_t fork_create(Fork& f);
+void fork_destroy(Fork& f);
+
+// ckm_round_eval_async, with the overlapped launch on or off (off for the
+// entry point that creates and allocates nothing).
+ckm_status round_eval(const ckm_graph* g, const double* d_s_frac, int64_t ld, int32_t K, uint64_t seed,
+                      int64_t budget, uint32_t flags, int64_t* d_peak, int64_t* d_cost, uint8_t* d_feasible,
+                      int32_t* d_best_k, uint64_t* d_best_S, uint64_t* d_best_R, int32_t* d_status, void* d_work,
+                      size_t work_bytes, void* stream, bool overlap);
+
 // Kernel launchers (defined in ckm_kernels.hip). They only enqueue work.
 hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,
                            char* work, hipStream_t stream);
@@ -155,6 +177,9 @@ hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_
 // buffer's row array (nothing when L.rows_on is false).
 hipError_t launch_round_rows(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed, uint32_t flags,
                              char* work, hipStream_t stream);
+// The same for candidate groups g0 .. g0 + gn - 1 (64 candidates each).
+hipError_t launch_round_rows(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed, uint32_t flags,
+                             int32_t g0, int32_t gn, char* work, hipStream_t stream);
 // Threshold family: ranks of the K thresholds, their sorted copy, and the
 // keys of S* in place of the quantized thresholds q.
 hipError_t launch_threshold_keys(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,
@@ -173,9 +198,12 @@ hipError_t launch_max_batch(const ckm_graph& g, const Layout& L, int32_t K, int6
 // array when L.rows_on, rounding it first unless flags has CKM_F_ROUNDED).
 // s_user: for kSrcUser, K
 // caller-supplied S matrices ([K][n][row_words] 32-bit words).
+// With overlap, the candidate groups are split over the caller's stream and
+// g.fork's (when the graph has one and K is large enough); the caller's
+// stream waits for the other before it returns, as after one launch.
 hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
                            uint32_t flags, const Plan& plan, int src, const uint64_t* s_user, char* work,
-                           hipStream_t stream);
+                           hipStream_t stream, bool overlap = true);
 hipError_t launch_select(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
                          int64_t budget, uint32_t flags, int64_t* d_peak,
                          int64_t* d_cost, uint8_t* d_feasible, int32_t* d_best_k,

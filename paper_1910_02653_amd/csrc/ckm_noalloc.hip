@@ -65,6 +65,7 @@ extern "C" ckm_status ckm_round_eval_noalloc(const ckm_graph* g, const double* d
   // The area is passed as an ordinary work buffer of its full size: the row
   // arrays are used when they fit in it, and every stage initializes what it
   // reads, so nothing carried over from an earlier call is read.
-  return ckm_round_eval_async(g, d_s_frac, ld, K, seed, budget, flags, d_peak, d_cost, d_feasible, d_best_k,
-                              d_best_S, d_best_R, d_status, work, CKM_NOALLOC_SCRATCH_BYTES, stream);
+  // Every launch goes on the caller's stream (no side stream).
+  return ckm::round_eval(g, d_s_frac, ld, K, seed, budget, flags, d_peak, d_cost, d_feasible, d_best_k, d_best_S,
+                         d_best_R, d_status, work, CKM_NOALLOC_SCRATCH_BYTES, stream, false);
 }

@@ -7,13 +7,18 @@ Hand-built and seeded graphs put the path's limits to work: a node with 120
 far users, a dependency with dozens of far later users, a node with 60
 dependencies (the overflow list), slots 2-3, and seen rows of 1 to 127 words.
 Small graphs are compared over every candidate; large ones on sampled
-candidates, the argmin and the best rows.
+candidates, the argmin and the best rows. With eight or more candidate groups
+the library overlaps the producer of the later groups' mask rows with the
+evaluate of the first quarter (a second stream); the K = 520 cases run that
+launch for all three sources.
 """
 import numpy as np
 import pytest
 
 from paper_1910_02653_amd import workloads as wl
 from test_gpu_parity import check_full, check_rows, gpu_round_eval, lexi_best, log, oracle_candidates
+import test_gpu_schedules as sched
+import test_gpu_threshold as thr
 
 pytestmark = pytest.mark.gpu
 
@@ -101,3 +106,36 @@ def test_seen_row_of_127_words():
     w = workload("skip40", deps, seed=4096, K=70)
     log("seen path: n=%d, 127 seen words" % n)
     sampled(w, ks=(0, 63, 69))
+
+
+def fan_graph(K):
+    return wl.random_dag(200, seed=17, K=K, max_deg=12, window=200, max_size=1000, max_cost=1000,
+                         s_kind="uniform", budget_pct=60.0)
+
+
+def test_overlapped_rounding_all_candidates():
+    """K = 520 (9 groups: the first two rounded and evaluated on the caller's
+    stream, the other 7 on the side stream): every candidate at two budgets."""
+    w = fan_graph(520)
+    log("seen path, overlapped: rounding n=%d K=%d" % (w.n, w.K))
+    peak, _ = check_full(w, gpu_round_eval(w))
+    med = int(np.median(peak))
+    check_full(w, gpu_round_eval(w, budget=med), budget=med)
+
+
+def test_overlapped_thresholds_all_candidates():
+    w = fan_graph(520)
+    p = thr.grid(520, 9)
+    log("seen path, overlapped: thresholds n=%d K=520" % w.n)
+    peak, _ = thr.check(w, p, thr.gpu_eval(w, p, w.budget), w.budget)
+    med = int(np.median(peak))
+    thr.check(w, p, thr.gpu_eval(w, p, med), med)
+
+
+def test_overlapped_schedules_all_candidates():
+    w = fan_graph(520)
+    rows = wl.random_schedules(w.n, 520, seed=520, density=0.3, kind="intervals")
+    log("seen path, overlapped: supplied schedules n=%d K=520" % w.n)
+    peak, _ = sched.check(w, rows, sched.gpu_eval(w, rows, w.budget), w.budget)
+    med = int(np.median(peak))
+    sched.check(w, rows, sched.gpu_eval(w, rows, med), med)
