@@ -385,6 +385,50 @@ def time_pipelined(g, w, steps, stream, d_s):
             "input": "the bench step, consecutive steps overlapped on two streams and two work buffers"}
 
 
+def time_graph(g, w, steps, d_s):
+    """The bench step captured once into a HIP graph (torch.cuda.CUDAGraph
+    over the library's launches) and replayed: the same kernels without the
+    host's per-launch work. Every replay repeats the whole step."""
+    import torch
+
+    from paper_1910_02653_amd import ckm
+
+    K = w.K
+    work = g.alloc_work(K)
+    out = g.alloc_outputs(K)
+
+    def step():
+        g.quantize_async(d_s, work)
+        g.evaluate_async(K, w.seed, 0, work)
+        g.select_async(K, w.seed, w.budget, 0, out, work)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    cg = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(cg):
+        step()
+    torch.cuda.synchronize()
+    for _ in range(10):
+        cg.replay()
+    torch.cuda.synchronize()
+    assert int(out["status"].item()) == ckm.OK
+    stream = torch.cuda.current_stream()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(steps):
+        cg.replay()
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    return {"value": K / (ms * 1e-3), "unit": "candidates/s", "ms_per_step": ms, "steps": steps,
+            "input": "the bench step captured once into a HIP graph, replayed"}
+
+
 def time_plan(g, w, steps, stream, d_s):
     """Throughput of ckm_plan_async on one schedule of the workload: the best
     candidate at the median-peak budget (a budget some candidates meet)."""
@@ -443,6 +487,8 @@ def main():
                     help="timed calls of the threshold-family evaluation (0 = skip)")
     ap.add_argument("--plan-steps", type=int, default=20,
                     help="timed calls of the execution-plan generation (0 = skip)")
+    ap.add_argument("--graph-steps", type=int, default=100,
+                    help="replays of the step captured into a HIP graph (0 = skip)")
     ap.add_argument("--pipe-steps", type=int, default=100,
                     help="timed steps with consecutive steps overlapped (0 = skip)")
     ap.add_argument("--feasible-steps", type=int, default=20,
@@ -570,6 +616,8 @@ def main():
     }
     if args.host_steps > 0:
         result["host_round_trip"] = time_host_round_trip(g, w, K, args.host_steps)
+    if args.graph_steps > 0:
+        result["graph_replay"] = time_graph(g, w, args.graph_steps, d_s)
     if args.pipe_steps > 0:
         result["pipelined"] = time_pipelined(g, w, args.pipe_steps, stream, d_s)
     if args.feasible_steps > 0:

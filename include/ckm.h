@@ -140,7 +140,16 @@ ckm_status ckm_round_eval(const ckm_graph* g, const double* s_frac, int64_t ld, 
  * calls that may run concurrently. The three stages run in the order
  * quantize -> evaluate -> select, on one work buffer. The library cannot
  * check sizes behind a pointer: each array must hold the elements stated
- * for it (work_bytes is checked against the layout). */
+ * for it (work_bytes is checked against the layout).
+ *
+ * The calls enqueue kernel launches only (no allocation, memset, copy or
+ * synchronization), so a sequence of them can be captured into a HIP graph
+ * on `stream` and replayed; scalar arguments (K, seed, budget, flags) are
+ * fixed at capture. On a graph whose evaluate LDS holds to a few waves per
+ * CU (the seen path of large graphs), an evaluate with 8 or more groups of
+ * 64 candidates runs the later groups on the graph's second stream, forked
+ * from `stream` and joined back to it by events before the call's work on
+ * `stream` ends; a capture takes that fork and join in as dependencies. */
 
 /* Bytes of work buffer for K candidates on graph g. This includes, when the
  * S rows of all K candidates fit in 8 GiB, room for them and for their R

@@ -524,8 +524,9 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
     delete g;
     return fail(CKM_E_NOMEM, "out of host memory");
   }
-  // the side stream of the overlapped launches (seen-path graphs only)
-  if (g->d_snodes) {
+  // the side stream of the overlapped launches (seen-path graphs whose
+  // evaluate LDS holds to a few waves per SIMD)
+  if (g->d_snodes && g->eval_waves <= ckm::kForkMaxWaves) {
     g->fork = new (std::nothrow) ckm::Fork;
     e = g->fork ? ckm::fork_create(*g->fork) : hipErrorOutOfMemory;
     if (e != hipSuccess) {

@@ -160,6 +160,9 @@ struct Fork {
   hipStream_t side = nullptr;
   hipEvent_t forked = nullptr, joined = nullptr;
 };
+// Seen-path evaluates resident at no more than this many waves per CU (held
+// there by their LDS) get the overlapped launch and so the second stream.
+constexpr int32_t kForkMaxWaves = 16;
 hipError_t fork_create(Fork& f);
 void fork_destroy(Fork& f);
 

@@ -2355,15 +2355,18 @@ hipError_t launch_round_rows(const ckm_graph& g, const Layout& L, int32_t K, uin
   return hipGetLastError();
 }
 
-// Overlapped launches (seen path only). The first quarter of the candidate
-// groups has its mask rows made alone; the other groups' producer then runs
-// beside the first quarter's evaluate, and their evaluate follows on the side
-// stream. The producers are VALU-bound and the seen kernel leaves VALU slots
-// free while it waits for loads: at n = 4001, K = 4096 the step drops from
-// 100.2 to 96.8 ms (halves: 98.6, eighths: 97.7). The mask kernel does not
-// gain: its longest stages are its critical path, and the second chunk's
-// start behind its producer costs more than the overlap saves (n = 1009,
-// K = 1024: 0.611 ms alone, 0.68 to 0.73 ms split).
+// Overlapped launches (seen path, when LDS holds its evaluate to at most
+// kForkMaxWaves waves per CU). The first quarter of the candidate groups has
+// its mask rows made alone; the other groups' producer then runs beside the
+// first quarter's evaluate, and their evaluate follows on the side stream.
+// The producers are VALU-bound, and an evaluate that LDS keeps at a few waves
+// per SIMD leaves them registers and VALU slots: at n = 4001, K = 4096 (16 KiB
+// of seen bits per wave, 10 waves per CU) the step drops from 100.2 to
+// 96.8 ms (halves: 98.6, eighths: 97.7). An evaluate that its registers
+// keep at 6 waves per SIMD leaves no room, and the second chunk's longest
+// stages then start behind its producer: n = 1009, K = 1024 on the mask
+// kernel takes 0.68 to 0.73 ms split against 0.611, n = 337, K = 512 on the
+// seen kernel 0.156 against 0.106.
 static int32_t fork_first_groups(int32_t groups) { return groups / 4 > 0 ? groups / 4 : 1; }
 constexpr int32_t kForkMinGroups = 8;
 
@@ -2471,7 +2474,7 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
                        at<int64_t>(work, L.part_peak_off), at<int64_t>(work, L.part_cost_off));
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (!(overlap && produce && g.fork && g.d_snodes && G >= kForkMinGroups)) {
+    if (!(overlap && produce && g.fork && g.d_snodes && g.eval_waves <= kForkMaxWaves && G >= kForkMinGroups)) {
       if (produce) e = launch_mask_producer(g, L, K, seed, flags, src, s_user, 0, G, work, stream);
       if (e == hipSuccess) e = launch_mask_eval(g, L, K, plan, 0, G, work, stream);
       return e;

@@ -8,9 +8,10 @@ far users, a dependency with dozens of far later users, a node with 60
 dependencies (the overflow list), slots 2-3, and seen rows of 1 to 127 words.
 Small graphs are compared over every candidate; large ones on sampled
 candidates, the argmin and the best rows. With eight or more candidate groups
-the library overlaps the producer of the later groups' mask rows with the
-evaluate of the first quarter (a second stream); the K = 520 cases run that
-launch for all three sources.
+on a graph whose seen bits hold the evaluate to a few waves per CU, the
+library overlaps the producer of the later groups' mask rows with the
+evaluate of the first quarter (a second stream); the K = 520 cases on such a
+graph run that launch for all three sources.
 """
 import numpy as np
 import pytest
@@ -108,15 +109,21 @@ def test_seen_row_of_127_words():
     sampled(w, ks=(0, 63, 69))
 
 
-def fan_graph(K):
-    return wl.random_dag(200, seed=17, K=K, max_deg=12, window=200, max_size=1000, max_cost=1000,
-                         s_kind="uniform", budget_pct=60.0)
+def lds_bound_graph(K):
+    """n = 1400, every node used by the next and by the node 40 above it:
+    1360 seen bits, 43 words per lane (11 KiB of LDS per wave, 14 waves per
+    CU), so the evaluate takes the overlapped launch."""
+    n = 1400
+    deps = [set() if v == 0 else {v - 1} for v in range(n)]
+    for v in range(40, n):
+        deps[v].add(v - 40)
+    return workload("skip40_1400", deps, seed=1400, K=K)
 
 
 def test_overlapped_rounding_all_candidates():
     """K = 520 (9 groups: the first two rounded and evaluated on the caller's
     stream, the other 7 on the side stream): every candidate at two budgets."""
-    w = fan_graph(520)
+    w = lds_bound_graph(520)
     log("seen path, overlapped: rounding n=%d K=%d" % (w.n, w.K))
     peak, _ = check_full(w, gpu_round_eval(w))
     med = int(np.median(peak))
@@ -124,7 +131,7 @@ def test_overlapped_rounding_all_candidates():
 
 
 def test_overlapped_thresholds_all_candidates():
-    w = fan_graph(520)
+    w = lds_bound_graph(520)
     p = thr.grid(520, 9)
     log("seen path, overlapped: thresholds n=%d K=520" % w.n)
     peak, _ = thr.check(w, p, thr.gpu_eval(w, p, w.budget), w.budget)
@@ -133,7 +140,7 @@ def test_overlapped_thresholds_all_candidates():
 
 
 def test_overlapped_schedules_all_candidates():
-    w = fan_graph(520)
+    w = lds_bound_graph(520)
     rows = wl.random_schedules(w.n, 520, seed=520, density=0.3, kind="intervals")
     log("seen path, overlapped: supplied schedules n=%d K=520" % w.n)
     peak, _ = sched.check(w, rows, sched.gpu_eval(w, rows, w.budget), w.budget)
