@@ -180,9 +180,10 @@ hipError_t launch_quantize(const ckm_graph& g, const Layout& L, const double* d_
 // buffer's row array (nothing when L.rows_on is false).
 hipError_t launch_round_rows(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed, uint32_t flags,
                              char* work, hipStream_t stream);
-// The same for candidate groups g0 .. g0 + gn - 1 (64 candidates each).
+// The same for candidate groups g0 .. g0 + gn - 1 (64 candidates each);
+// clear: on the mask path, also reset those candidates' evaluate totals.
 hipError_t launch_round_rows(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed, uint32_t flags,
-                             int32_t g0, int32_t gn, char* work, hipStream_t stream);
+                             int32_t g0, int32_t gn, bool clear, char* work, hipStream_t stream);
 // Threshold family: ranks of the K thresholds, their sorted copy, and the
 // keys of S* in place of the quantized thresholds q.
 hipError_t launch_threshold_keys(const ckm_graph& g, const Layout& L, const double* d_s, int64_t ld,

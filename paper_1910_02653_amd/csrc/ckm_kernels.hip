@@ -1076,6 +1076,21 @@ __global__ void __launch_bounds__(256) ckm_eval_init_kernel(int32_t K, int64_t* 
   }
 }
 
+// The same for the 64 candidates of one group, done by the mask producers'
+// blocks of y = 0 in place of a launch of its own (peak NULL: nothing).
+struct Totals {
+  int64_t* __restrict__ peak;
+  int64_t* __restrict__ cost;
+  int32_t K;
+};
+__device__ __forceinline__ void clear_totals(const Totals& tot, int group) {
+  const int k = group * kWave + (int)threadIdx.x;
+  if (tot.peak && blockIdx.y == 0 && k < tot.K) {
+    tot.peak[k] = INT64_MIN;
+    tot.cost[k] = 0;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Thresholds: one block per row r; q[r][i] = floor(clamp(S*, 0, 1) * 2^16) for
 // i < r (Section 5.1), the deterministic bits 1[S* > 0.5] of Algorithm 2, and
@@ -1905,9 +1920,11 @@ __global__ void __launch_bounds__(kWave) ckm_round_masks_kernel(const uint32_t* 
                                                                 const uint32_t* __restrict__ det, int32_t n,
                                                                 int32_t ldq, int32_t det_words, uint32_t key0,
                                                                 uint32_t key1, uint32_t det0, size_t mgroup,
-                                                                uint64_t* __restrict__ mrows, int32_t g0) {
+                                                                uint64_t* __restrict__ mrows, int32_t g0,
+                                                                Totals tot) {
   const int group = blockIdx.x + g0;
   const int y = blockIdx.y;
+  clear_totals(tot, group);
   uint64_t* rows = mrows + (size_t)group * mgroup;
   round_mask_row(q, det, n, ldq, det_words, key0, key1, det0, group, n - y, rows + mrow_off(n - y));
   if (y != n - y) round_mask_row(q, det, n, ldq, det_words, key0, key1, det0, group, y, rows + mrow_off(y));
@@ -2153,9 +2170,11 @@ __global__ void __launch_bounds__(kWave) ckm_seen_eval_kernel(SeenArgs a) {
 __global__ void __launch_bounds__(kWave) ckm_threshold_masks_kernel(const uint32_t* __restrict__ key, int32_t ldq,
                                                                     const uint32_t* __restrict__ rank, int32_t K,
                                                                     int32_t n, size_t mgroup,
-                                                                    uint64_t* __restrict__ mrows, int32_t g0) {
+                                                                    uint64_t* __restrict__ mrows, int32_t g0,
+                                                                    Totals tot) {
   const int lane = threadIdx.x;
   const int group = blockIdx.x + g0;
+  clear_totals(tot, group);
   const uint32_t k = (uint32_t)(group * kWave + lane);
   const uint32_t rk = rank[k < (uint32_t)K ? k : (uint32_t)K - 1u];
   uint64_t* rows = mrows + (size_t)group * mgroup;
@@ -2199,9 +2218,11 @@ __device__ __forceinline__ uint4 user_chunk(const uint32_t* row, int c, int lim)
 
 __global__ void __launch_bounds__(kWave) ckm_user_masks_kernel(const uint32_t* __restrict__ s_user, int32_t n,
                                                                int32_t K, int32_t s_words, size_t mgroup,
-                                                               uint64_t* __restrict__ mrows, int32_t g0) {
+                                                               uint64_t* __restrict__ mrows, int32_t g0,
+                                                               Totals tot) {
   const int lane = threadIdx.x;
   const int group = blockIdx.x + g0;
+  clear_totals(tot, group);
   const uint32_t k = (uint32_t)(group * kWave + lane);
   const uint32_t kk = k < (uint32_t)K ? k : (uint32_t)K - 1u;
   uint64_t* rows = mrows + (size_t)group * mgroup;
@@ -2334,17 +2355,19 @@ size_t mask_rows_words(int32_t n) { return mrow_off(n + 1); }
 
 hipError_t launch_round_rows(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed, uint32_t flags,
                              char* work, hipStream_t stream) {
-  return launch_round_rows(g, L, K, seed, flags, 0, (int32_t)groups_of(K), work, stream);
+  return launch_round_rows(g, L, K, seed, flags, 0, (int32_t)groups_of(K), false, work, stream);
 }
 
 hipError_t launch_round_rows(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed, uint32_t flags,
-                             int32_t g0, int32_t gn, char* work, hipStream_t stream) {
+                             int32_t g0, int32_t gn, bool clear, char* work, hipStream_t stream) {
   if (!L.rows_on || gn <= 0) return hipSuccess;
   if (use_mask_path(g, L)) {
+    const Totals tot{clear ? at<int64_t>(work, L.part_peak_off) : nullptr, at<int64_t>(work, L.part_cost_off), K};
     hipLaunchKernelGGL(ckm_round_masks_kernel, dim3(gn, g.n / 2 + 1), dim3(kWave), 0, stream,
                        at<const uint32_t>(work, L.q_off), at<const uint32_t>(work, L.det_off), g.n, L.ldq,
                        L.det_words, (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32),
-                       (flags & CKM_F_DET0) ? 1u : 0u, mask_rows_words(g.n), at<uint64_t>(work, L.rows_off), g0);
+                       (flags & CKM_F_DET0) ? 1u : 0u, mask_rows_words(g.n), at<uint64_t>(work, L.rows_off), g0,
+                       tot);
     return hipGetLastError();
   }
   const int32_t kpad = ((K + kWave - 1) / kWave) * kWave;
@@ -2379,6 +2402,7 @@ hipError_t fork_create(Fork& f) {
 }
 
 void fork_destroy(Fork& f) {
+  if (f.side) (void)hipStreamSynchronize(f.side);   // nothing of the graph's still running there
   if (f.forked) (void)hipEventDestroy(f.forked);
   if (f.joined) (void)hipEventDestroy(f.joined);
   if (f.side) (void)hipStreamDestroy(f.side);
@@ -2387,21 +2411,23 @@ void fork_destroy(Fork& f) {
 }
 
 // The mask rows of groups g0 .. g0 + gn - 1 from source src (kSrcRound,
-// kSrcThreshold or kSrcUser).
+// kSrcThreshold or kSrcUser); their candidates' totals are cleared on the
+// way (the evaluate that follows accumulates into them).
 static hipError_t launch_mask_producer(const ckm_graph& g, const Layout& L, int32_t K, uint64_t seed,
                                        uint32_t flags, int src, const uint64_t* s_user, int32_t g0, int32_t gn,
                                        char* work, hipStream_t stream) {
   if (gn <= 0) return hipSuccess;
+  const Totals tot{at<int64_t>(work, L.part_peak_off), at<int64_t>(work, L.part_cost_off), K};
   if (src == kSrcThreshold) {
     hipLaunchKernelGGL(ckm_threshold_masks_kernel, dim3(gn, g.n / 2 + 1), dim3(kWave), 0, stream,
                        at<const uint32_t>(work, L.q_off), L.ldq, at<const uint32_t>(work, L.thr_rank_off), K, g.n,
-                       mask_rows_words(g.n), at<uint64_t>(work, L.rows_off), g0);
+                       mask_rows_words(g.n), at<uint64_t>(work, L.rows_off), g0, tot);
   } else if (src == kSrcUser) {
     hipLaunchKernelGGL(ckm_user_masks_kernel, dim3(gn, g.n / 2 + 1), dim3(kWave), 0, stream,
                        reinterpret_cast<const uint32_t*>(s_user), g.n, K, L.row_words, mask_rows_words(g.n),
-                       at<uint64_t>(work, L.rows_off), g0);
+                       at<uint64_t>(work, L.rows_off), g0, tot);
   } else {
-    return launch_round_rows(g, L, K, seed, flags, g0, gn, work, stream);
+    return launch_round_rows(g, L, K, seed, flags, g0, gn, true, work, stream);
   }
   return hipGetLastError();
 }
@@ -2470,10 +2496,14 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
     // beforehand), then the evaluate, chunk by chunk
     const bool produce = !(src == kSrcRound && (flags & CKM_F_ROUNDED));
     const int32_t G = (int32_t)groups_of(K);
-    hipLaunchKernelGGL(ckm_eval_init_kernel, dim3((K + 255) / 256), dim3(256), 0, stream, K,
-                       at<int64_t>(work, L.part_peak_off), at<int64_t>(work, L.part_cost_off));
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    hipError_t e = hipSuccess;
+    if (!produce) {
+      // no producer to clear the totals on the way
+      hipLaunchKernelGGL(ckm_eval_init_kernel, dim3((K + 255) / 256), dim3(256), 0, stream, K,
+                         at<int64_t>(work, L.part_peak_off), at<int64_t>(work, L.part_cost_off));
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
     if (!(overlap && produce && g.fork && g.d_snodes && g.eval_waves <= kForkMaxWaves && G >= kForkMinGroups)) {
       if (produce) e = launch_mask_producer(g, L, K, seed, flags, src, s_user, 0, G, work, stream);
       if (e == hipSuccess) e = launch_mask_eval(g, L, K, plan, 0, G, work, stream);
