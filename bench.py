@@ -114,6 +114,12 @@ def host_threads() -> int:
     return max(1, min(HOST_THREADS_PER_GPU, host_info()["affinity_cpus"]))
 
 
+def progress(msg):
+    """One line on stderr as each part of the run ends (the JSON line alone
+    goes to stdout)."""
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
 def cpu_baseline(w, sample: int, single: int, target_s: float = 15.0):
     """The oracle on candidates 0 .. sample-1 of the workload, split by
     candidate over the oracle threads (each thread runs the unmodified oracle
@@ -614,24 +620,23 @@ def main():
                      "evaluate_frac": achieved / copy_gbs},
         "wall_s": wall,
     }
-    if args.host_steps > 0:
-        result["host_round_trip"] = time_host_round_trip(g, w, K, args.host_steps)
-    if args.graph_steps > 0:
-        result["graph_replay"] = time_graph(g, w, args.graph_steps, d_s)
-    if args.pipe_steps > 0:
-        result["pipelined"] = time_pipelined(g, w, args.pipe_steps, stream, d_s)
-    if args.feasible_steps > 0:
-        result["feasible_budget"] = time_feasible(g, w, args.feasible_steps, stream, d_s)
-    if args.sched_steps > 0:
-        result["supplied_schedules"] = time_schedules(g, w, K, args.sched_steps, stream)
-    if args.batch_steps > 0:
-        result["max_batch"] = time_max_batch(g, w, args.batch_steps, stream, d_s)
-    if args.plan_steps > 0:
-        result["execution_plan"] = time_plan(g, w, args.plan_steps, stream, d_s)
-    if args.thr_steps > 0:
-        result["threshold_family"] = time_thresholds(g, w, K, args.thr_steps, stream, d_s)
-    if args.cpu_sample > 0:
-        result["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, K), min(args.cpu_single, K))
+    progress("timed steps: %.4f ms per step" % ms_step)
+    legs = [
+        ("host_round_trip", args.host_steps, lambda: time_host_round_trip(g, w, K, args.host_steps)),
+        ("graph_replay", args.graph_steps, lambda: time_graph(g, w, args.graph_steps, d_s)),
+        ("pipelined", args.pipe_steps, lambda: time_pipelined(g, w, args.pipe_steps, stream, d_s)),
+        ("feasible_budget", args.feasible_steps, lambda: time_feasible(g, w, args.feasible_steps, stream, d_s)),
+        ("supplied_schedules", args.sched_steps, lambda: time_schedules(g, w, K, args.sched_steps, stream)),
+        ("max_batch", args.batch_steps, lambda: time_max_batch(g, w, args.batch_steps, stream, d_s)),
+        ("execution_plan", args.plan_steps, lambda: time_plan(g, w, args.plan_steps, stream, d_s)),
+        ("threshold_family", args.thr_steps, lambda: time_thresholds(g, w, K, args.thr_steps, stream, d_s)),
+        ("cpu_baseline", args.cpu_sample,
+         lambda: cpu_baseline(w, min(args.cpu_sample, K), min(args.cpu_single, K))),
+    ]
+    for name, count, run in legs:
+        if count > 0:
+            result[name] = run()
+            progress("%s done" % name)
     print(json.dumps(result), flush=True)
     g.close()
 
