@@ -1877,6 +1877,86 @@ __device__ __forceinline__ Q8 load_q8(__amdgpu_buffer_rsrc_t rs, uint32_t row_by
 // of the row is the group's 64 decisions [u_{k,r,i} < q[r][i]] (the same
 // draws as round_word); candidate 0 takes the deterministic bits under
 // CKM_F_DET0. A block of 8 nodes shares one Philox output per lane.
+// Philox4x32-10 of counter (b, r, k, 0), the counter of block b of row r for
+// candidate k, split by what each part depends on. Round 0 multiplies b
+// (wave-uniform) and k (per lane, the same for every block of the row);
+// round 1 multiplies round 0's two results again. So the per-lane products
+// of rounds 0 and 1 are made once per row (PhiloxRow), the per-block products
+// are scalar, and a block costs each lane two XORs of round 1 and rounds 2-9.
+struct PhiloxRow {
+  uint32_t lo_k;          // lo(M1 k): round 0's counter word 1
+  uint32_t hi_n, lo_n;    // M0 n0, n0 = hi(M1 k) ^ r ^ key0: round 1's product of word 0
+};
+__device__ __forceinline__ PhiloxRow philox_row(uint32_t r, uint32_t k, uint32_t key0) {
+  const uint64_t a = (uint64_t)kPhiloxM1 * k;
+  const uint32_t n0 = (uint32_t)(a >> 32) ^ (r ^ key0);
+  const uint64_t p = (uint64_t)kPhiloxM0 * n0;
+  return {(uint32_t)a, (uint32_t)(p >> 32), (uint32_t)p};
+}
+__device__ __forceinline__ void philox_block(const PhiloxRow& pr, uint32_t b, uint32_t key0, uint32_t key1,
+                                             uint32_t x[4]) {
+  // round 0: words 2, 3 from the block index alone
+  const uint64_t pb = (uint64_t)kPhiloxM0 * b;
+  const uint32_t w2 = (uint32_t)(pb >> 32) ^ key1, w3 = (uint32_t)pb;
+  // round 1: word 2's product is uniform, word 0's was made per row
+  uint32_t k0 = key0 + kPhiloxW0, k1 = key1 + kPhiloxW1;
+  const uint64_t pu = (uint64_t)kPhiloxM1 * w2;
+  uint32_t c0 = pr.lo_k ^ ((uint32_t)(pu >> 32) ^ k0);
+  uint32_t c1 = (uint32_t)pu;
+  uint32_t c2 = pr.hi_n ^ (w3 ^ k1);
+  uint32_t c3 = pr.lo_n;
+  // round 2: word 1 is still uniform
+  k0 += kPhiloxW0;
+  k1 += kPhiloxW1;
+  {
+    const uint64_t p0 = (uint64_t)kPhiloxM0 * c0;
+    const uint64_t p1 = (uint64_t)kPhiloxM1 * c2;
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ (c1 ^ k0);
+    const uint32_t n2 = xor3((uint32_t)(p0 >> 32), c3, k1);
+    c0 = n0; c1 = (uint32_t)p1; c2 = n2; c3 = (uint32_t)p0;
+  }
+#pragma unroll
+  for (int rr = 3; rr < 10; ++rr) {
+    k0 += kPhiloxW0;
+    k1 += kPhiloxW1;
+    const uint64_t p0 = (uint64_t)kPhiloxM0 * c0;
+    const uint64_t p1 = (uint64_t)kPhiloxM1 * c2;
+    const uint32_t n0 = xor3((uint32_t)(p1 >> 32), c1, k0);
+    const uint32_t n2 = xor3((uint32_t)(p0 >> 32), c3, k1);
+    c0 = n0; c1 = (uint32_t)p1; c2 = n2; c3 = (uint32_t)p0;
+  }
+  x[0] = c0; x[1] = c1; x[2] = c2; x[3] = c3;
+}
+
+// Block b of row r (8 nodes) for the 64 candidates of a group, thresholds
+// qb: one Philox output per lane, 8 compares whose lane masks are the words,
+// one 64-byte store.
+__device__ __forceinline__ void round_mask_block(const PhiloxRow& pr, const Q8& qb, int b, int r, uint32_t k,
+                                                 uint32_t key0, uint32_t key1, bool det_here,
+                                                 cptr<uint32_t> drow, uint32_t* dst) {
+  uint64_t m[8];
+  if (8 * b >= r) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) m[j] = 0ull;
+  } else {
+    uint32_t x[4];
+    philox_block(pr, (uint32_t)b, key0, key1, x);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t u = (x[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+      m[j] = mask_of(u < qb[j]);
+    }
+    if (det_here) {
+      const uint32_t dw = drow[b >> 2] >> (8 * (b & 3));
+#pragma unroll
+      for (int j = 0; j < 8; ++j) m[j] = (m[j] & ~1ull) | ((dw >> j) & 1u);
+    }
+  }
+  // lanes 16-63 of out are never stored, so out starts from any value
+  const uint32_t out = put_masks<0>(k, m);
+  if (threadIdx.x < 16) dst[16 * b + threadIdx.x] = out;   // words 8b .. 8b+7 of the row
+}
+
 __device__ __forceinline__ void round_mask_row(const uint32_t* __restrict__ q, const uint32_t* __restrict__ det,
                                                int32_t n, int32_t ldq, int32_t det_words, uint32_t key0,
                                                uint32_t key1, uint32_t det0, int group, int r, uint64_t* row) {
@@ -1887,30 +1967,17 @@ __device__ __forceinline__ void round_mask_row(const uint32_t* __restrict__ q, c
   const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(q), 0, n * ldq * 4, kBufWord3);
   const uint32_t row_bytes = (uint32_t)(r < n ? r : 0) * (uint32_t)ldq * 4u;
   const cptr<uint32_t> drow = as_const(det + (size_t)(r < n ? r : 0) * det_words);
-  Q8 qn = load_q8(rs, row_bytes, 0);
-  for (int b = 0; b < nblk; ++b) {
-    const Q8 qb = qn;
-    if (b + 1 < nblk) qn = load_q8(rs, row_bytes, b + 1);
-    uint64_t m[8];
-    if (8 * b >= r) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) m[j] = 0ull;
-    } else {
-      uint32_t x[4];
-      philox4x32_10((uint32_t)b, (uint32_t)r, k, 0u, key0, key1, x);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t u = (x[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-        m[j] = mask_of(u < qb[j]);
-      }
-      if (det0 && group == 0) {
-        const uint32_t dw = drow[b >> 2] >> (8 * (b & 3));
-#pragma unroll
-        for (int j = 0; j < 8; ++j) m[j] = (m[j] & ~1ull) | ((dw >> j) & 1u);
-      }
-    }
-    const uint32_t out = put_masks<0>(0u, m);
-    if (lane < 16) dst[16 * b + lane] = out;   // words 8b .. 8b+7 of the row
+  const PhiloxRow pr = philox_row((uint32_t)r, k, key0);
+  const bool det_here = det0 && group == 0;
+  // two threshold buffers by block parity, each block's requested one block
+  // ahead (vector loads complete in order)
+  Q8 qa = load_q8(rs, row_bytes, 0), qb;
+  for (int b = 0; b < nblk; b += 2) {
+    if (b + 1 < nblk) qb = load_q8(rs, row_bytes, b + 1);
+    round_mask_block(pr, qa, b, r, k, key0, key1, det_here, drow, dst);
+    if (b + 1 >= nblk) break;
+    if (b + 2 < nblk) qa = load_q8(rs, row_bytes, b + 2);
+    round_mask_block(pr, qb, b + 1, r, k, key0, key1, det_here, drow, dst);
   }
 }
 
