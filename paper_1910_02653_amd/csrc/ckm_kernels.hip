@@ -1867,9 +1867,12 @@ struct Q8 {
   }
 };
 __device__ __forceinline__ Q8 load_q8(__amdgpu_buffer_rsrc_t rs, uint32_t row_bytes, int b) {
+  // the offset is wave-uniform; stating it keeps it a scalar operand where
+  // the compiler cannot prove it (else it loops over the lanes' values)
+  const uint32_t off = __builtin_amdgcn_readfirstlane(row_bytes + 32u * (uint32_t)b);
   Q8 x;
-  x.lo = load_mval<0>(rs, row_bytes + 32u * (uint32_t)b);
-  x.hi = load_mval<16>(rs, row_bytes + 32u * (uint32_t)b);
+  x.lo = load_mval<0>(rs, off);
+  x.hi = load_mval<16>(rs, off);
   return x;
 }
 
@@ -2234,6 +2237,17 @@ __global__ void __launch_bounds__(kWave) ckm_seen_eval_kernel(SeenArgs a) {
 // word i of row r is the group's 64 decisions [rank_k < key[r][i]], the
 // threshold test of threshold_word. Keys on and above the diagonal are 0, so
 // are their words (row n reads row 0, all of whose keys are 0).
+// Block b (8 nodes) of a threshold row: word i is the lane mask of
+// [rank_k < key_i] (keys at and above the diagonal are 0).
+__device__ __forceinline__ void threshold_mask_block(const Q8& kb, uint32_t rk, uint32_t k, int b, uint32_t* dst) {
+  uint64_t m[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) m[j] = mask_of(rk < kb[j]);
+  // lanes 16-63 of out are never stored, so out starts from any value
+  const uint32_t out = put_masks<0>(k, m);
+  if (threadIdx.x < 16) dst[16 * b + threadIdx.x] = out;
+}
+
 __global__ void __launch_bounds__(kWave) ckm_threshold_masks_kernel(const uint32_t* __restrict__ key, int32_t ldq,
                                                                     const uint32_t* __restrict__ rank, int32_t K,
                                                                     int32_t n, size_t mgroup,
@@ -2248,21 +2262,22 @@ __global__ void __launch_bounds__(kWave) ckm_threshold_masks_kernel(const uint32
   const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(key), 0, n * ldq * 4, kBufWord3);
   const int y = blockIdx.y;
   for (int h = 0; h < 2; ++h) {
-    const int r = h == 0 ? n - y : y;
+    // the row is wave-uniform; stating it keeps the block loop scalar
+    const int r = __builtin_amdgcn_readfirstlane(h == 0 ? n - y : y);
     if (h == 1 && r == n - y) break;
     uint32_t* dst = reinterpret_cast<uint32_t*>(rows + mrow_off(r));
     const int lim = r < n ? r : 0;   // row n (after the last stage) is empty
     const uint32_t row_bytes = (uint32_t)lim * (uint32_t)ldq * 4u;
     const int nblk = (r >> 3) + 1;
-    Q8 kn = load_q8(rs, row_bytes, 0);
-    for (int b = 0; b < nblk; ++b) {
-      const Q8 kb = kn;
-      if (b + 1 < nblk) kn = load_q8(rs, row_bytes, b + 1);
-      uint64_t m[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) m[j] = mask_of(rk < kb[j]);   // keys at and above lim are 0
-      const uint32_t out = put_masks<0>(0u, m);
-      if (lane < 16) dst[16 * b + lane] = out;
+    // two key buffers by block parity, each block's requested one block ahead
+    const uint32_t rb = row_bytes;
+    Q8 ka = load_q8(rs, rb, 0), kb;
+    for (int b = 0; b < nblk; b += 2) {
+      if (b + 1 < nblk) kb = load_q8(rs, rb, b + 1);
+      threshold_mask_block(ka, rk, k, b, dst);
+      if (b + 1 >= nblk) break;
+      if (b + 2 < nblk) ka = load_q8(rs, rb, b + 2);
+      threshold_mask_block(kb, rk, k, b + 1, dst);
     }
   }
 }
@@ -2295,7 +2310,8 @@ __global__ void __launch_bounds__(kWave) ckm_user_masks_kernel(const uint32_t* _
   uint64_t* rows = mrows + (size_t)group * mgroup;
   const int y = blockIdx.y;
   for (int h = 0; h < 2; ++h) {
-    const int r = h == 0 ? n - y : y;
+    // the row is wave-uniform; stating it keeps the block loop scalar
+    const int r = __builtin_amdgcn_readfirstlane(h == 0 ? n - y : y);
     if (h == 1 && r == n - y) break;
     uint32_t* dst = reinterpret_cast<uint32_t*>(rows + mrow_off(r));
     const int lim = r < n ? r : 0;   // row n (after the last stage) is empty
@@ -2316,7 +2332,7 @@ __global__ void __launch_bounds__(kWave) ckm_user_masks_kernel(const uint32_t* _
         uint64_t m[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) m[j] = mask_of(((byte >> j) & 1u) != 0u);
-        const uint32_t out = put_masks<0>(0u, m);
+        const uint32_t out = put_masks<0>(k, m);   // lanes 16-63 are not stored
         if (lane < 16) dst[16 * b + lane] = out;
       }
       cur = nxt;
