@@ -145,6 +145,7 @@ struct Plan {
   int32_t items = 1, kind = 0, P = 0, T0 = 0, R1 = 0, R2 = 0;
 };
 Plan plan_auto(int32_t n, int32_t K, int32_t max_items, int32_t waves_per_cu);
+Plan plan_stages(int32_t n, int32_t max_items);
 Plan plan_splits(int32_t n, int32_t splits);
 
 // Resident evaluate waves per CU for a graph of n nodes (the runtime's
