@@ -1595,11 +1595,10 @@ __host__ __device__ __forceinline__ size_t mrow_off(int t) {
 //   6: for node v-1, the byte offsets in a mask row of the S_{t+1} words of
 //      its slot 0 and 1 dependencies (low and high half; 0 for an absent
 //      slot), fetched one node ahead
-//   7: 128 (v - 1), where node v-1's data starts (0 for node 0, whose loads
-//      for "node -1" repeat its own and are not used). The loads for node
-//      v-1 take their addresses from here, so that they cannot be issued
-//      before node v's record has arrived: scalar loads complete out of
-//      order, and a wait for that record would wait for them as well.
+//   7: the gate, the least of the node's three far references (words 1, 3
+//      and 5), or 0 when the node has more than two dependencies: when it is
+//      at or above the stage's limit (t + 1) << 16, the node is decided in a
+//      form without far lookups or rare slots.
 //   8-15: binary64 M_v, C_v, M of slots 0 and 1, used from scalar registers
 //      (the vector registers they would take are worth a wave per SIMD)
 // Pairs of nodes are aligned (nodes 2c, 2c+1). A stage's scan starts at the
@@ -1669,10 +1668,11 @@ __device__ __forceinline__ uint32_t far_bit(const u32x32& Rrow, uint32_t f) {
 // One dependency slot of node v: the dependency's value is released after
 // v (FREE(t,i,v) = 1) on the candidates that compute v, do not keep the
 // value into stage t+1 and compute none of its later users in stage t.
+template <bool kFar>
 __device__ __forceinline__ double mask_slot(double val, uint64_t R, uint32_t lm, uint32_t ref, double Mi,
                                             uint64_t s1i, uint32_t Rwin, const u32x32& Rrow, uint32_t tlim) {
   uint32_t y = Rwin & lm;
-  if (__builtin_expect(ref < tlim, 0)) y |= far_bit(Rrow, ref);
+  if (kFar && __builtin_expect(ref < tlim, 0)) y |= far_bit(Rrow, ref);
   const uint64_t later = mask_of(y != 0u);
   const uint64_t fr = R & ~(s1i | later);
   return madd_m(val, fr, Mi);
@@ -1693,15 +1693,18 @@ struct MNode {
 // that block, v < t and the scan has passed at least one node. Released
 // right after its own compute (eq. collectable with i = v): a computed node
 // that is neither kept nor used, which only node t can be.
-template <bool kTop>
-__device__ __forceinline__ void mask_node(const MaskArgs& a, int t, int v, const MNode& nd, uint64_t S0, uint64_t S1,
-                                          cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow) {
+// kSlow: the general form, for a node whose gate (record word 7: the least
+// of its three far references, 0 with more than two dependencies) is below
+// the stage's limit; the fast form has no far lookup and no rare slots.
+template <bool kTop, bool kSlow>
+__device__ __forceinline__ void mask_node_as(const MaskArgs& a, int t, int v, const MNode& nd, uint64_t S0,
+                                             uint64_t S1, cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow,
+                                             uint32_t tlim) {
   const u32x16& rec = nd.rec;
   const uint32_t ctrl = rec[1];
-  const uint32_t tlim = (uint32_t)(t + 1) << 16;
   const double Mv = dbl(rec[8], rec[9]), Cv = dbl(rec[10], rec[11]);
   uint32_t x = sc.Rwin & rec[0];
-  if (__builtin_expect(ctrl < tlim, 0)) x |= far_bit(Rrow, ctrl);
+  if (kSlow && __builtin_expect(ctrl < tlim, 0)) x |= far_bit(Rrow, ctrl);
   const uint64_t x1 = S1 | mask_of(x != 0u);
   uint64_t R = x1 & ~S0;
   sc.U0 = madd_m(sc.U0, S0, Mv);
@@ -1716,15 +1719,17 @@ __device__ __forceinline__ void mask_node(const MaskArgs& a, int t, int v, const
     R = ~0ull;
     val = madd_m(val, ~x1, Mv);
   }
-  val = mask_slot(val, R, rec[2], rec[3], dbl(rec[12], rec[13]), nd.d0, sc.Rwin, Rrow, tlim);
-  val = mask_slot(val, R, rec[4], rec[5], dbl(rec[14], rec[15]), nd.d1, sc.Rwin, Rrow, tlim);
-  if (__builtin_expect((ctrl & kMRare) != 0u, 0)) {
+  val = mask_slot<kSlow>(val, R, rec[2], rec[3], dbl(rec[12], rec[13]), nd.d0, sc.Rwin, Rrow, tlim);
+  val = mask_slot<kSlow>(val, R, rec[4], rec[5], dbl(rec[14], rec[15]), nd.d1, sc.Rwin, Rrow, tlim);
+  if (kSlow && __builtin_expect((ctrl & kMRare) != 0u, 0)) {
     const uint32_t off = (uint32_t)v * kMNodeBytes;
     const u32x8 r2 = sload<u32x8>(a.mnodes, off + 64);
     const u32x4 m23 = sload<u32x4>(a.mnodes, off + 96);
-    val = mask_slot(val, R, r2[0], r2[1], dbl(m23[0], m23[1]), sload<uint64_t>(s1row, r2[5]), sc.Rwin, Rrow, tlim);
+    val = mask_slot<true>(val, R, r2[0], r2[1], dbl(m23[0], m23[1]), sload<uint64_t>(s1row, r2[5]), sc.Rwin, Rrow,
+                          tlim);
     if (r2[4] >= 4)
-      val = mask_slot(val, R, r2[2], r2[3], dbl(m23[2], m23[3]), sload<uint64_t>(s1row, r2[6]), sc.Rwin, Rrow, tlim);
+      val = mask_slot<true>(val, R, r2[2], r2[3], dbl(m23[2], m23[3]), sload<uint64_t>(s1row, r2[6]), sc.Rwin,
+                            Rrow, tlim);
   }
   // suffix form of the U recurrence (see scan_node): val = Y + freed_v
   sc.maxv = max_f64(sc.maxv, val);
@@ -1735,10 +1740,30 @@ __device__ __forceinline__ void mask_node(const MaskArgs& a, int t, int v, const
   sc.Rwin = sc.Rwin + sc.Rwin + (rb ? 1u : 0u);
 }
 
+template <bool kTop>
+__device__ __forceinline__ void mask_node(const MaskArgs& a, int t, int v, const MNode& nd, uint64_t S0, uint64_t S1,
+                                          cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow) {
+  const uint32_t tlim = (uint32_t)(t + 1) << 16;
+  if (__builtin_expect(nd.rec[7] < tlim, 0))
+    mask_node_as<kTop, true>(a, t, v, nd, S0, S1, s1row, sc, Rrow, tlim);
+  else
+    mask_node_as<kTop, false>(a, t, v, nd, S0, S1, s1row, sc, Rrow, tlim);
+}
+
+// x, made to depend on a word of a record that a wait delivers, so that the
+// loads it addresses are issued after that wait: scalar loads complete out
+// of order, and a wait for the record would wait for them as well.
+__device__ __forceinline__ uint32_t after_record(uint32_t x, uint32_t word) {
+  asm("" : "+s"(x) : "s"(word));
+  return x;
+}
+
 // The loads node v-1 needs, issued while node v is decided: its record (with
-// its operands), and the dependency words node v's record lists for it.
-__device__ __forceinline__ MNode mask_fetch(const MaskArgs& a, const u32x16& rec_v, cptr<uint64_t> s1row) {
-  const uint32_t off = rec_v[7], f = rec_v[6];
+// its operands) at byte off, and the dependency words node v's record lists
+// for it.
+__device__ __forceinline__ MNode mask_fetch(const MaskArgs& a, const u32x16& rec_v, cptr<uint64_t> s1row,
+                                            uint32_t off) {
+  const uint32_t f = rec_v[6];
   MNode nx;
   nx.rec = sload<u32x16>(a.mnodes, off);
   nx.d0 = sload<uint64_t>(s1row, f & 0xFFFFu);
@@ -1759,11 +1784,11 @@ __device__ __forceinline__ void mask_step(const MaskArgs& a, int t, int v, MNode
   const uint64_t S0 = (uint64_t)B0[2 * P] | (uint64_t)B0[2 * P + 1] << 32;
   const uint64_t S1 = (uint64_t)B1[2 * P] | (uint64_t)B1[2 * P + 1] << 32;
   const u32x16& rec = buf[kCur].rec;
-  buf[kNext] = mask_fetch(a, rec, s1row);
+  // node v-1's data (node 0 fetches its own again: nothing is left to load)
+  buf[kNext] = mask_fetch(a, rec, s1row, after_record(v >= 1 ? (uint32_t)(v - 1) * kMNodeBytes : 0u, rec[6]));
   if (P == 0) {
-    // pair c-1 starts 16 (c - 1) bytes into a row; rec[7] = 128 (2c - 1),
-    // so (rec[7] >> 4) & ~15 (0 for c = 0)
-    const uint32_t boff = (rec[7] >> 4) & ~15u;
+    // pair c-1 (v = 2c) starts 16 (c - 1) bytes into a row (0 for c = 0)
+    const uint32_t boff = after_record(v >= 2 ? 8u * (uint32_t)v - 16u : 0u, rec[6]);
     Bn0 = sload<u32x4>(s0row, boff);
     Bn1 = sload<u32x4>(s1row, boff);
   }
@@ -1817,7 +1842,7 @@ __global__ void __launch_bounds__(kWave) ckm_mask_eval_kernel(MaskArgs a) {
     const int c = t >> 1;
     MNode buf[2];
     const u32x16 top = a.mnodes[(size_t)(2 * c + 2) * (kMNodeBytes / 64)];
-    buf[1] = mask_fetch(a, top, s1row);
+    buf[1] = mask_fetch(a, top, s1row, (uint32_t)(2 * c + 1) * kMNodeBytes);
     const u32x4 T0 = sload<u32x4>(s0row, 16u * c), T1 = sload<u32x4>(s1row, 16u * c);
     u32x4 A0, A1, B0, B1;
     mask_block<true>(a, t, c, buf, T0, T1, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
@@ -2821,7 +2846,7 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
   auto put = [](uint32_t* w, double x) { memcpy(w, &x, sizeof(x)); };
   for (int32_t v = 0; v < np; ++v) {   // no far references, padded nodes included
     uint32_t* r = reinterpret_cast<uint32_t*>(base + (size_t)v * kMNodeBytes);
-    r[1] = r[3] = r[5] = r[16 + 1] = r[16 + 3] = kMNoFar;
+    r[1] = r[3] = r[5] = r[7] = r[16 + 1] = r[16 + 3] = kMNoFar;
   }
   for (int32_t v = 0; v < n; ++v) {
     char* node = base + (size_t)v * kMNodeBytes;
@@ -2867,9 +2892,11 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
       put(sl < 2 ? r + 12 + 2 * sl : m23 + 2 * (sl - 2), (double)M[i]);
     }
     r[1] = ctrl;
+    // the gate: below the stage's limit when a far reference may apply
+    r[7] = (ctrl & kMRare) ? 0u : std::min(ctrl, std::min(r[3], r[5]));
   }
   // fetch lists: record v (padded ones included) names the S_{t+1} words of
-  // node v-1's slots 0 and 1, and where node v-1's data is
+  // node v-1's slots 0 and 1
   for (int32_t v = 1; v < np; ++v) {
     const int32_t u = v - 1;
     uint32_t f = 0;
@@ -2880,9 +2907,8 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
     }
     uint32_t* r = reinterpret_cast<uint32_t*>(base + (size_t)v * kMNodeBytes);
     r[6] = f;
-    r[7] = (uint32_t)u * (uint32_t)kMNodeBytes;
   }
-  return true;   // node 0 keeps fetch list 0 and word 7 = 0
+  return true;   // node 0 keeps fetch list 0
 }
 
 bool build_seen_records(int32_t n, const int64_t* M, const int64_t* C, const int32_t* dep_ptr,
