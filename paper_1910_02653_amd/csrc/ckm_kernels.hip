@@ -2492,8 +2492,8 @@ hipError_t launch_round_rows(const ckm_graph& g, const Layout& L, int32_t K, uin
 // first quarter's evaluate, and their evaluate follows on the side stream.
 // The producers are VALU-bound, and an evaluate that LDS keeps at a few waves
 // per SIMD leaves them registers and VALU slots: at n = 4001, K = 4096 (16 KiB
-// of seen bits per wave, 10 waves per CU) the step drops from 100.2 to
-// 96.8 ms (halves: 98.6, eighths: 97.7). An evaluate that its registers
+// of seen bits per wave, 10 waves per CU) the step drops from 95.3 to
+// 91.7 ms (halves: 93.7, eighths: 91.3). An evaluate that its registers
 // keep at 6 waves per SIMD leaves no room, and the second chunk's longest
 // stages then start behind its producer: n = 1009, K = 1024 on the mask
 // kernel takes 0.68 to 0.73 ms split against 0.611, n = 337, K = 512 on the
