@@ -183,3 +183,52 @@ def test_async_calls_from_threads_on_own_streams():
                     assert np.array_equal(got["best_R"].view(np.uint64), want[job]["best_R"])
     finally:
         g.close()
+
+
+def test_async_threads_on_one_overlapped_graph():
+    """The same from 4 threads on a graph whose evaluate takes the overlapped
+    launch (the graph's second stream, shared by the calls, and its two
+    events): every result equals the call that stays on one stream (the
+    entry point that allocates nothing), and sampled candidates the oracle."""
+    import torch
+    from test_gpu_seen import lds_bound_graph
+    w = lds_bound_graph(520)
+    big = 1 << 40
+    jobs = [(K, seed) for K in (520, 600) for seed in (5, 6)]
+
+    def single_stream(g, K, seed):
+        d = torch.from_numpy(w.s_frac).cuda()
+        out = g.alloc_outputs(K)
+        g.round_eval_noalloc(d, K, seed, big, 0, out)
+        torch.cuda.synchronize()
+        return {k: v.cpu().numpy() for k, v in out.items()}
+
+    want = {job: fresh(w, lambda g, job=job: single_stream(g, *job)) for job in jobs}
+    for (K, seed), res in want.items():
+        ks = [0, 63, 64, K - 1]
+        orc = {k: ref.eval_candidate(w.replace(seed=seed), k) for k in ks}
+        for k in ks:
+            assert (int(res["peak"][k]), int(res["cost"][k])) == orc[k], (K, seed, k)
+    g = ckm.Graph.from_workload(w)
+    d_s = torch.from_numpy(w.s_frac).cuda()
+    torch.cuda.synchronize()
+
+    def run(job):
+        K, seed = job
+        stream = torch.cuda.Stream()
+        with torch.cuda.stream(stream):
+            work = g.alloc_work(K)
+            out = g.alloc_outputs(K)
+        g.round_eval_async(d_s, K, seed, big, 0, out, work, stream)
+        stream.synchronize()
+        return {k: v.cpu().numpy() for k, v in out.items()}
+
+    try:
+        log("%d overlapped async jobs on 4 threads" % len(jobs))
+        with ThreadPoolExecutor(4) as ex:
+            for _ in range(2):
+                for job, got in zip(jobs, ex.map(run, jobs)):
+                    for key in ("status", "peak", "cost", "feasible", "best_k", "best_S", "best_R"):
+                        assert np.array_equal(got[key], want[job][key]), (job, key)
+    finally:
+        g.close()
