@@ -2009,8 +2009,11 @@ __device__ __forceinline__ void round_mask_row(const uint32_t* __restrict__ q, c
   }
 }
 
-// Block (group, y) makes rows y and n - y of the group (rows 0 .. n; row n
-// is zero), so that every block has about the same number of node blocks.
+// Block (group, y) makes row n - y of the group (rows 0 .. n; row n is
+// zero). Blocks start in order of y, so the longest rows start first and the
+// last to start are the shortest: the launch ends with little left on any
+// SIMD. (Equal pairs of rows y and n - y per block ended with most SIMDs
+// running one wave, the youngest, which the issue order serves last.)
 __global__ void __launch_bounds__(kWave) ckm_round_masks_kernel(const uint32_t* __restrict__ q,
                                                                 const uint32_t* __restrict__ det, int32_t n,
                                                                 int32_t ldq, int32_t det_words, uint32_t key0,
@@ -2022,7 +2025,6 @@ __global__ void __launch_bounds__(kWave) ckm_round_masks_kernel(const uint32_t* 
   clear_totals(tot, group);
   uint64_t* rows = mrows + (size_t)group * mgroup;
   round_mask_row(q, det, n, ldq, det_words, key0, key1, det0, group, n - y, rows + mrow_off(n - y));
-  if (y != n - y) round_mask_row(q, det, n, ldq, det_words, key0, key1, det0, group, y, rows + mrow_off(y));
 }
 
 // ---------------------------------------------------------------------------
@@ -2258,7 +2260,7 @@ __global__ void __launch_bounds__(kWave) ckm_seen_eval_kernel(SeenArgs a) {
   if (group == 0 && item == 0 && lane == 0) a.hdr[0] = a.items;
 }
 
-// Threshold candidates into mask rows (block (group, y): rows y and n - y):
+// Threshold candidates into mask rows (block (group, y): row n - y):
 // word i of row r is the group's 64 decisions [rank_k < key[r][i]], the
 // threshold test of threshold_word. Keys on and above the diagonal are 0, so
 // are their words (row n reads row 0, all of whose keys are 0).
@@ -2285,30 +2287,26 @@ __global__ void __launch_bounds__(kWave) ckm_threshold_masks_kernel(const uint32
   const uint32_t rk = rank[k < (uint32_t)K ? k : (uint32_t)K - 1u];
   uint64_t* rows = mrows + (size_t)group * mgroup;
   const auto rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(key), 0, n * ldq * 4, kBufWord3);
-  const int y = blockIdx.y;
-  for (int h = 0; h < 2; ++h) {
-    // the row is wave-uniform; stating it keeps the block loop scalar
-    const int r = __builtin_amdgcn_readfirstlane(h == 0 ? n - y : y);
-    if (h == 1 && r == n - y) break;
-    uint32_t* dst = reinterpret_cast<uint32_t*>(rows + mrow_off(r));
-    const int lim = r < n ? r : 0;   // row n (after the last stage) is empty
-    const uint32_t row_bytes = (uint32_t)lim * (uint32_t)ldq * 4u;
-    const int nblk = (r >> 3) + 1;
-    // two key buffers by block parity, each block's requested one block ahead
-    const uint32_t rb = row_bytes;
-    Q8 ka = load_q8(rs, rb, 0), kb;
-    for (int b = 0; b < nblk; b += 2) {
-      if (b + 1 < nblk) kb = load_q8(rs, rb, b + 1);
-      threshold_mask_block(ka, rk, k, b, dst);
-      if (b + 1 >= nblk) break;
-      if (b + 2 < nblk) ka = load_q8(rs, rb, b + 2);
-      threshold_mask_block(kb, rk, k, b + 1, dst);
-    }
+  // row n - y (longest first, as in ckm_round_masks_kernel); the row is
+  // wave-uniform, and stating it keeps the block loop scalar
+  const int r = __builtin_amdgcn_readfirstlane(n - (int)blockIdx.y);
+  uint32_t* dst = reinterpret_cast<uint32_t*>(rows + mrow_off(r));
+  const int lim = r < n ? r : 0;   // row n (after the last stage) is empty
+  const uint32_t rb = (uint32_t)lim * (uint32_t)ldq * 4u;
+  const int nblk = (r >> 3) + 1;
+  // two key buffers by block parity, each block's requested one block ahead
+  Q8 ka = load_q8(rs, rb, 0), kb;
+  for (int b = 0; b < nblk; b += 2) {
+    if (b + 1 < nblk) kb = load_q8(rs, rb, b + 1);
+    threshold_mask_block(ka, rk, k, b, dst);
+    if (b + 1 >= nblk) break;
+    if (b + 2 < nblk) ka = load_q8(rs, rb, b + 2);
+    threshold_mask_block(kb, rk, k, b + 1, dst);
   }
 }
 
-// Caller-supplied checkpoint matrices into mask rows (block (group, y): rows
-// y and n - y): word i of row r is bit i of row r of each of the group's 64
+// Caller-supplied checkpoint matrices into mask rows (block (group, y): row
+// n - y): word i of row r is bit i of row r of each of the group's 64
 // matrices ([K][n][s_words] 32-bit words), for i < r only (bits on and above
 // the diagonal are not part of S). Lanes past K repeat candidate K-1. Each
 // lane reads its matrix row 16 bytes (128 nodes) at a time, the next chunk
@@ -2333,35 +2331,32 @@ __global__ void __launch_bounds__(kWave) ckm_user_masks_kernel(const uint32_t* _
   const uint32_t k = (uint32_t)(group * kWave + lane);
   const uint32_t kk = k < (uint32_t)K ? k : (uint32_t)K - 1u;
   uint64_t* rows = mrows + (size_t)group * mgroup;
-  const int y = blockIdx.y;
-  for (int h = 0; h < 2; ++h) {
-    // the row is wave-uniform; stating it keeps the block loop scalar
-    const int r = __builtin_amdgcn_readfirstlane(h == 0 ? n - y : y);
-    if (h == 1 && r == n - y) break;
-    uint32_t* dst = reinterpret_cast<uint32_t*>(rows + mrow_off(r));
-    const int lim = r < n ? r : 0;   // row n (after the last stage) is empty
-    const uint32_t* src = s_user + ((size_t)kk * n + lim) * s_words;
-    const int nblk = (r >> 3) + 1;
-    uint4 cur = user_chunk(src, 0, lim);
-    for (int c = 0; 16 * c < nblk; ++c) {
-      const uint4 nxt = user_chunk(src, c + 1, lim);
-      const uint32_t w4[4] = {cur.x, cur.y, cur.z, cur.w};
+  // row n - y (longest first, as in ckm_round_masks_kernel); the row is
+  // wave-uniform, and stating it keeps the block loop scalar
+  const int r = __builtin_amdgcn_readfirstlane(n - (int)blockIdx.y);
+  uint32_t* dst = reinterpret_cast<uint32_t*>(rows + mrow_off(r));
+  const int lim = r < n ? r : 0;   // row n (after the last stage) is empty
+  const uint32_t* src = s_user + ((size_t)kk * n + lim) * s_words;
+  const int nblk = (r >> 3) + 1;
+  uint4 cur = user_chunk(src, 0, lim);
+  for (int c = 0; 16 * c < nblk; ++c) {
+    const uint4 nxt = user_chunk(src, c + 1, lim);
+    const uint32_t w4[4] = {cur.x, cur.y, cur.z, cur.w};
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int b = 16 * c + q;
-        if (b >= nblk) break;
-        // the block's bits of nodes below lim only
-        const int below = lim - 8 * b;
-        const uint32_t keep = below >= 8 ? 0xFFu : below <= 0 ? 0u : (1u << below) - 1u;
-        const uint32_t byte = (w4[q >> 2] >> (8 * (q & 3))) & keep;
-        uint64_t m[8];
+    for (int q = 0; q < 16; ++q) {
+      const int b = 16 * c + q;
+      if (b >= nblk) break;
+      // the block's bits of nodes below lim only
+      const int below = lim - 8 * b;
+      const uint32_t keep = below >= 8 ? 0xFFu : below <= 0 ? 0u : (1u << below) - 1u;
+      const uint32_t byte = (w4[q >> 2] >> (8 * (q & 3))) & keep;
+      uint64_t m[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) m[j] = mask_of(((byte >> j) & 1u) != 0u);
-        const uint32_t out = put_masks<0>(k, m);   // lanes 16-63 are not stored
-        if (lane < 16) dst[16 * b + lane] = out;
-      }
-      cur = nxt;
+      for (int j = 0; j < 8; ++j) m[j] = mask_of(((byte >> j) & 1u) != 0u);
+      const uint32_t out = put_masks<0>(k, m);   // lanes 16-63 are not stored
+      if (lane < 16) dst[16 * b + lane] = out;
     }
+    cur = nxt;
   }
 }
 
@@ -2471,7 +2466,7 @@ hipError_t launch_round_rows(const ckm_graph& g, const Layout& L, int32_t K, uin
   if (!L.rows_on || gn <= 0) return hipSuccess;
   if (use_mask_path(g, L)) {
     const Totals tot{clear ? at<int64_t>(work, L.part_peak_off) : nullptr, at<int64_t>(work, L.part_cost_off), K};
-    hipLaunchKernelGGL(ckm_round_masks_kernel, dim3(gn, g.n / 2 + 1), dim3(kWave), 0, stream,
+    hipLaunchKernelGGL(ckm_round_masks_kernel, dim3(gn, g.n + 1), dim3(kWave), 0, stream,
                        at<const uint32_t>(work, L.q_off), at<const uint32_t>(work, L.det_off), g.n, L.ldq,
                        L.det_words, (uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32),
                        (flags & CKM_F_DET0) ? 1u : 0u, mask_rows_words(g.n), at<uint64_t>(work, L.rows_off), g0,
@@ -2527,11 +2522,11 @@ static hipError_t launch_mask_producer(const ckm_graph& g, const Layout& L, int3
   if (gn <= 0) return hipSuccess;
   const Totals tot{at<int64_t>(work, L.part_peak_off), at<int64_t>(work, L.part_cost_off), K};
   if (src == kSrcThreshold) {
-    hipLaunchKernelGGL(ckm_threshold_masks_kernel, dim3(gn, g.n / 2 + 1), dim3(kWave), 0, stream,
+    hipLaunchKernelGGL(ckm_threshold_masks_kernel, dim3(gn, g.n + 1), dim3(kWave), 0, stream,
                        at<const uint32_t>(work, L.q_off), L.ldq, at<const uint32_t>(work, L.thr_rank_off), K, g.n,
                        mask_rows_words(g.n), at<uint64_t>(work, L.rows_off), g0, tot);
   } else if (src == kSrcUser) {
-    hipLaunchKernelGGL(ckm_user_masks_kernel, dim3(gn, g.n / 2 + 1), dim3(kWave), 0, stream,
+    hipLaunchKernelGGL(ckm_user_masks_kernel, dim3(gn, g.n + 1), dim3(kWave), 0, stream,
                        reinterpret_cast<const uint32_t*>(s_user), g.n, K, L.row_words, mask_rows_words(g.n),
                        at<uint64_t>(work, L.rows_off), g0, tot);
   } else {
