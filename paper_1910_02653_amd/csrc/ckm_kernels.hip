@@ -1,22 +1,27 @@
 // HIP kernels for gfx950: batched rounding, Algorithm 2 repair, memory
 // simulation, reduction and argmin of Checkmate candidate schedules.
 //
-// Work decomposition of the dominant kernel (ckm_eval_kernel): one wave of 64
-// lanes owns 64 candidates (lane = candidate) and a contiguous range of
-// stages. All lanes walk the same nodes in the same order, so graph data,
-// thresholds and loop bounds are wave-uniform and only the candidate's bits
-// and running sums differ per lane. Each lane keeps two bit rows (32-bit
-// words, bit i%32 of word i/32): S_t, which becomes R_t as the scan passes,
-// in LDS laid out [word][lane] so that a wave-uniform word index touches 64
-// consecutive dwords (no bank conflicts), and S_{t+1} in vector registers
-// (in LDS too for the largest graphs). S rows are rounded beforehand into a
-// row array in HBM, [row][word][candidate], and streamed; R rows go back to
-// a second such array for the best-candidate output. Without those arrays
-// the kernel makes its own S rows.
+// Work decomposition: one wave of 64 lanes owns 64 candidates (lane =
+// candidate) and one work item of stages. All lanes walk the same nodes in
+// the same order, so graph data and loop bounds are wave-uniform and only the
+// candidates' bits and running sums differ per lane. Three evaluate kernels
+// share that shape:
+// - ckm_mask_eval_kernel and ckm_seen_eval_kernel (graphs up to 4096 nodes
+//   with the row arrays in the work buffer): S is rounded beforehand into
+//   mask rows, one 64-bit word per (row, node) whose bit j is candidate j of
+//   the group, so the repair and the FREE tests are 64-bit scalar operations
+//   for the whole group and only the binary64 sums run per lane;
+// - ckm_eval_kernel (the rest: larger or wide graphs, no row arrays): each
+//   lane keeps its own bit rows (32-bit words, bit i%32 of word i/32): S_t,
+//   which becomes R_t as the scan passes, in LDS laid out [word][lane] so that
+//   a wave-uniform word index touches 64 consecutive dwords, and S_{t+1} in
+//   vector registers (in LDS too for the largest graphs). S rows come from a
+//   row array in HBM, [row][word][candidate], or are made in the kernel.
 //
-// Sums of sizes and costs run in binary64. The host admits only graphs whose
-// totals stay below 2^53, so every partial sum is an exactly represented
-// integer and the result is identical to int64 arithmetic in any order.
+// Sums of sizes and costs run in binary64 while the graph's totals stay below
+// 2^53, so every partial sum is an exactly represented integer and the result
+// is identical to int64 arithmetic in any order; a graph whose totals reach
+// 2^53 (a wide graph) is summed in int64 by ckm_eval_kernel.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -1696,7 +1701,7 @@ struct MNode {
 // kSlow: the general form, for a node whose gate (record word 7: the least
 // of its three far references, 0 with more than two dependencies) is below
 // the stage's limit; the fast form has no far lookup and no rare slots.
-template <bool kTop, bool kSlow>
+template <bool kTop, bool kSlow, bool kSkip>
 __device__ __forceinline__ void mask_node_as(const MaskArgs& a, int t, int v, const MNode& nd, uint64_t S0,
                                              uint64_t S1, cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow,
                                              uint32_t tlim) {
@@ -1708,9 +1713,17 @@ __device__ __forceinline__ void mask_node_as(const MaskArgs& a, int t, int v, co
   const uint64_t x1 = S1 | mask_of(x != 0u);
   uint64_t R = x1 & ~S0;
   sc.U0 = madd_m(sc.U0, S0, Mv);
-  if (!kTop && R == 0ull) {
-    // no candidate computes v: nothing is released after it, and the sums
-    // stay (maxv already covers Y, the running value only falling since)
+  // A lane that does not compute v frees nothing after it, and its val = Y
+  // changes neither maxv (which already covers Y: the running value has only
+  // fallen since the last computed node) nor Y. kSkip: a node that no
+  // candidate of the group computes returns here. Without it such nodes take
+  // the general path, which is faster for randomized rounding (19 % of the
+  // visits on the transformer workload: 0.455 against 0.458 ms; the seen
+  // kernel at n = 4001, K = 4096: 87.2 against 88.0 ms), while the threshold
+  // family, whose groups hold neighbouring thresholds, has many more of them
+  // and gains from the skip on those two graphs (0.557 against 0.570 ms and
+  // 85.2 against 90.3 ms per call).
+  if (kSkip && !kTop && R == 0ull) {
     sc.Rwin = sc.Rwin + sc.Rwin;
     return;
   }
@@ -1740,14 +1753,14 @@ __device__ __forceinline__ void mask_node_as(const MaskArgs& a, int t, int v, co
   sc.Rwin = sc.Rwin + sc.Rwin + (rb ? 1u : 0u);
 }
 
-template <bool kTop>
+template <bool kTop, bool kSkip>
 __device__ __forceinline__ void mask_node(const MaskArgs& a, int t, int v, const MNode& nd, uint64_t S0, uint64_t S1,
                                           cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow) {
   const uint32_t tlim = (uint32_t)(t + 1) << 16;
   if (__builtin_expect(nd.rec[7] < tlim, 0))
-    mask_node_as<kTop, true>(a, t, v, nd, S0, S1, s1row, sc, Rrow, tlim);
+    mask_node_as<kTop, true, kSkip>(a, t, v, nd, S0, S1, s1row, sc, Rrow, tlim);
   else
-    mask_node_as<kTop, false>(a, t, v, nd, S0, S1, s1row, sc, Rrow, tlim);
+    mask_node_as<kTop, false, kSkip>(a, t, v, nd, S0, S1, s1row, sc, Rrow, tlim);
 }
 
 // x, made to depend on a word of a record that a wait delivers, so that the
@@ -1776,7 +1789,7 @@ __device__ __forceinline__ MNode mask_fetch(const MaskArgs& a, const u32x16& rec
 // Bn1 (the current pair is in B0, B1). The loads alternate between two
 // buffers by position (node v's in buf[P], node v-1's into the other), so
 // nothing moves from one to the other.
-template <int P, bool kTop>
+template <int P, bool kTop, bool kSkip>
 __device__ __forceinline__ void mask_step(const MaskArgs& a, int t, int v, MNode (&buf)[2], const u32x4& B0,
                                           const u32x4& B1, u32x4& Bn0, u32x4& Bn1, cptr<uint64_t> s0row,
                                           cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow, uint32_t* rrow_t) {
@@ -1792,7 +1805,7 @@ __device__ __forceinline__ void mask_step(const MaskArgs& a, int t, int v, MNode
     Bn0 = sload<u32x4>(s0row, boff);
     Bn1 = sload<u32x4>(s1row, boff);
   }
-  mask_node<kTop>(a, t, v, buf[kCur], S0, S1, s1row, sc, Rrow);
+  mask_node<kTop, kSkip>(a, t, v, buf[kCur], S0, S1, s1row, sc, Rrow);
   if (P == 0 && (v & 31) == 0) {
     // the R bits of nodes v .. v+31 are complete: one word of R_t, kept in
     // the register row (and stored for the output)
@@ -1802,12 +1815,12 @@ __device__ __forceinline__ void mask_step(const MaskArgs& a, int t, int v, MNode
 }
 
 // Pair c (nodes 2c+1, 2c) from B0, B1; pair c-1 loaded into Bn0, Bn1.
-template <bool kTop>
+template <bool kTop, bool kSkip>
 __device__ __forceinline__ void mask_block(const MaskArgs& a, int t, int c, MNode (&buf)[2], const u32x4& B0,
                                            const u32x4& B1, u32x4& Bn0, u32x4& Bn1, cptr<uint64_t> s0row,
                                            cptr<uint64_t> s1row, MScan& sc, u32x32& Rrow, uint32_t* rrow_t) {
-  mask_step<1, kTop>(a, t, 2 * c + 1, buf, B0, B1, Bn0, Bn1, s0row, s1row, sc, Rrow, rrow_t);
-  mask_step<0, kTop>(a, t, 2 * c, buf, B0, B1, Bn0, Bn1, s0row, s1row, sc, Rrow, rrow_t);
+  mask_step<1, kTop, kSkip>(a, t, 2 * c + 1, buf, B0, B1, Bn0, Bn1, s0row, s1row, sc, Rrow, rrow_t);
+  mask_step<0, kTop, kSkip>(a, t, 2 * c, buf, B0, B1, Bn0, Bn1, s0row, s1row, sc, Rrow, rrow_t);
 }
 
 // One wave per work item: the 64 candidates of group blockIdx.x over the
@@ -1816,6 +1829,7 @@ __device__ __forceinline__ void mask_block(const MaskArgs& a, int t, int c, MNod
 // more than 32 nodes above the node, one such later user per dependency).
 // Each node's loads are issued one node ahead, in one batch, so that a node
 // waits once, for loads that had a whole node's work to arrive.
+template <bool kSkip>
 __global__ void __launch_bounds__(kWave) ckm_mask_eval_kernel(MaskArgs a) {
   const int lane = threadIdx.x;
   const int group = blockIdx.x + a.g0;
@@ -1845,13 +1859,13 @@ __global__ void __launch_bounds__(kWave) ckm_mask_eval_kernel(MaskArgs a) {
     buf[1] = mask_fetch(a, top, s1row, (uint32_t)(2 * c + 1) * kMNodeBytes);
     const u32x4 T0 = sload<u32x4>(s0row, 16u * c), T1 = sload<u32x4>(s1row, 16u * c);
     u32x4 A0, A1, B0, B1;
-    mask_block<true>(a, t, c, buf, T0, T1, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
+    mask_block<true, kSkip>(a, t, c, buf, T0, T1, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
     int cc = c - 1;
     for (; cc >= 1; cc -= 2) {
-      mask_block<false>(a, t, cc, buf, B0, B1, A0, A1, s0row, s1row, sc, Rrow, rrow_t);
-      mask_block<false>(a, t, cc - 1, buf, A0, A1, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
+      mask_block<false, kSkip>(a, t, cc, buf, B0, B1, A0, A1, s0row, s1row, sc, Rrow, rrow_t);
+      mask_block<false, kSkip>(a, t, cc - 1, buf, A0, A1, B0, B1, s0row, s1row, sc, Rrow, rrow_t);
     }
-    if (cc == 0) mask_block<false>(a, t, 0, buf, B0, B1, A0, A1, s0row, s1row, sc, Rrow, rrow_t);
+    if (cc == 0) mask_block<false, kSkip>(a, t, 0, buf, B0, B1, A0, A1, s0row, s1row, sc, Rrow, rrow_t);
     seg_peak = fmax(seg_peak, sc.U0 - sc.Y + sc.maxv);
     seg_cost += (int64_t)sc.cost;
   }
@@ -2158,8 +2172,8 @@ __device__ __forceinline__ double seen_slot(double val, uint64_t R, bool rb, uin
   return val;
 }
 
-// Node v of stage t (see mask_node). kTop: v = t.
-template <bool kTop>
+// Node v of stage t (see mask_node and mask_node_as). kTop: v = t.
+template <bool kTop, bool kSkip>
 __device__ __forceinline__ void seen_node(const SeenArgs& a, const SNode& nd, cptr<uint64_t> s1row, SScan& sc,
                                           char* lds_lane) {
   const u32x16& r = nd.rec;
@@ -2168,9 +2182,8 @@ __device__ __forceinline__ void seen_node(const SeenArgs& a, const SNode& nd, cp
   const uint64_t x1 = nd.S1 | mask_of(x != 0u);
   uint64_t R = x1 & ~nd.S0;
   sc.U0 = madd_m(sc.U0, nd.S0, Mv);
-  if (!kTop && R == 0ull) {
-    // no candidate computes v (see mask_node)
-    sc.Rwin = sc.Rwin + sc.Rwin;
+  if (kSkip && !kTop && R == 0ull) {
+    sc.Rwin = sc.Rwin + sc.Rwin;   // no candidate computes v (see mask_node_as)
     return;
   }
   double val = sc.Y;
@@ -2207,16 +2220,17 @@ __device__ __forceinline__ void seen_node(const SeenArgs& a, const SNode& nd, cp
 
 // Node v from buf[P] (P: its parity in the scan), node v-1's loads into
 // buf[P ^ 1] first.
-template <int P, bool kTop>
+template <int P, bool kTop, bool kSkip>
 __device__ __forceinline__ void seen_step(const SeenArgs& a, int v, SNode (&buf)[2], cptr<uint64_t> s0row,
                                           cptr<uint64_t> s1row, SScan& sc, char* lds_lane, uint32_t* rrow_t) {
   buf[P ^ 1] = seen_fetch(a, buf[P].rec, s0row, s1row, lds_lane);
-  seen_node<kTop>(a, buf[P], s1row, sc, lds_lane);
+  seen_node<kTop, kSkip>(a, buf[P], s1row, sc, lds_lane);
   if ((v & 31) == 0) rrow_t[(size_t)(v >> 5) * a.kpad] = sc.Rwin;   // R of nodes v .. v+31
 }
 
 // One wave per work item: the 64 candidates of group blockIdx.x over the
 // stages of item blockIdx.y; the scan of stage t runs from node t down.
+template <bool kSkip>
 __global__ void __launch_bounds__(kWave) ckm_seen_eval_kernel(SeenArgs a) {
   extern __shared__ uint32_t seen_lds[];
   const int lane = threadIdx.x;
@@ -2243,13 +2257,13 @@ __global__ void __launch_bounds__(kWave) ckm_seen_eval_kernel(SeenArgs a) {
     SNode buf[2];
     const u32x16 top = a.snodes[(size_t)(t + 1) * (kSNodeBytes / 64)];   // its fetch block: node t
     buf[1] = seen_fetch(a, top, s0row, s1row, lds_lane);
-    seen_step<1, true>(a, t, buf, s0row, s1row, sc, lds_lane, rrow_t);
+    seen_step<1, true, kSkip>(a, t, buf, s0row, s1row, sc, lds_lane, rrow_t);
     int v = t - 1;
     for (; v >= 1; v -= 2) {
-      seen_step<0, false>(a, v, buf, s0row, s1row, sc, lds_lane, rrow_t);
-      seen_step<1, false>(a, v - 1, buf, s0row, s1row, sc, lds_lane, rrow_t);
+      seen_step<0, false, kSkip>(a, v, buf, s0row, s1row, sc, lds_lane, rrow_t);
+      seen_step<1, false, kSkip>(a, v - 1, buf, s0row, s1row, sc, lds_lane, rrow_t);
     }
-    if (v == 0) seen_step<0, false>(a, 0, buf, s0row, s1row, sc, lds_lane, rrow_t);
+    if (v == 0) seen_step<0, false, kSkip>(a, 0, buf, s0row, s1row, sc, lds_lane, rrow_t);
     seg_peak = fmax(seg_peak, sc.U0 - sc.Y + sc.maxv);
     seg_cost += (int64_t)sc.cost;
   }
@@ -2438,7 +2452,7 @@ static bool use_mask_path(const ckm_graph& g, const Layout& L) {
 
 int32_t mask_waves_per_cu() {
   int blocks = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, (const void*)ckm_mask_eval_kernel, kWave, 0) !=
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, (const void*)ckm_mask_eval_kernel<false>, kWave, 0) !=
           hipSuccess ||
       blocks < 1)
     blocks = 1;
@@ -2447,7 +2461,7 @@ int32_t mask_waves_per_cu() {
 
 int32_t seen_waves_per_cu(int32_t seen_words) {
   int blocks = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, (const void*)ckm_seen_eval_kernel, kWave,
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, (const void*)ckm_seen_eval_kernel<false>, kWave,
                                                    (size_t)seen_words * 256) != hipSuccess ||
       blocks < 1)
     blocks = 1;
@@ -2536,9 +2550,13 @@ static hipError_t launch_mask_producer(const ckm_graph& g, const Layout& L, int3
 }
 
 // The mask-path evaluate (seen kernel or mask kernel) of groups g0 .. g0 + gn - 1.
-static hipError_t launch_mask_eval(const ckm_graph& g, const Layout& L, int32_t K, const Plan& plan,
+// The evaluate of groups g0 .. g0 + gn - 1 on the mask rows. Rows of the
+// threshold family or of supplied schedules take the kernels that skip a
+// node no candidate of the group computes (see mask_node_as).
+static hipError_t launch_mask_eval(const ckm_graph& g, const Layout& L, int32_t K, const Plan& plan, int src,
                                    int32_t g0, int32_t gn, char* work, hipStream_t stream) {
   if (gn <= 0) return hipSuccess;
+  const bool skip = src != kSrcRound;
   const int32_t kpad = ((K + kWave - 1) / kWave) * kWave;
   if (g.d_snodes) {
     SeenArgs m;
@@ -2563,8 +2581,12 @@ static hipError_t launch_mask_eval(const ckm_graph& g, const Layout& L, int32_t 
     m.part_cost = at<int64_t>(work, L.part_cost_off);
     m.hdr = at<int32_t>(work, L.hdr_off);
     m.g0 = g0;
-    hipLaunchKernelGGL(ckm_seen_eval_kernel, dim3(gn, plan.items), dim3(kWave), (size_t)g.seen_words * 256,
-                       stream, m);
+    if (skip)
+      hipLaunchKernelGGL(ckm_seen_eval_kernel<true>, dim3(gn, plan.items), dim3(kWave),
+                         (size_t)g.seen_words * 256, stream, m);
+    else
+      hipLaunchKernelGGL(ckm_seen_eval_kernel<false>, dim3(gn, plan.items), dim3(kWave),
+                         (size_t)g.seen_words * 256, stream, m);
     return hipGetLastError();
   }
   MaskArgs m;
@@ -2587,7 +2609,10 @@ static hipError_t launch_mask_eval(const ckm_graph& g, const Layout& L, int32_t 
   m.part_cost = at<int64_t>(work, L.part_cost_off);
   m.hdr = at<int32_t>(work, L.hdr_off);
   m.g0 = g0;
-  hipLaunchKernelGGL(ckm_mask_eval_kernel, dim3(gn, plan.items), dim3(kWave), 0, stream, m);
+  if (skip)
+    hipLaunchKernelGGL(ckm_mask_eval_kernel<true>, dim3(gn, plan.items), dim3(kWave), 0, stream, m);
+  else
+    hipLaunchKernelGGL(ckm_mask_eval_kernel<false>, dim3(gn, plan.items), dim3(kWave), 0, stream, m);
   return hipGetLastError();
 }
 
@@ -2609,7 +2634,7 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
     }
     if (!(overlap && produce && g.fork && g.d_snodes && g.eval_waves <= kForkMaxWaves && G >= kForkMinGroups)) {
       if (produce) e = launch_mask_producer(g, L, K, seed, flags, src, s_user, 0, G, work, stream);
-      if (e == hipSuccess) e = launch_mask_eval(g, L, K, plan, 0, G, work, stream);
+      if (e == hipSuccess) e = launch_mask_eval(g, L, K, plan, src, 0, G, work, stream);
       return e;
     }
     const int32_t ga = fork_first_groups(G);
@@ -2619,11 +2644,11 @@ hipError_t launch_evaluate(const ckm_graph& g, const Layout& L, int32_t K, uint6
     e = hipEventRecord(g.fork->forked, stream);
     if (e == hipSuccess) e = hipStreamWaitEvent(g.fork->side, g.fork->forked, 0);
     if (e == hipSuccess) e = launch_mask_producer(g, L, K, seed, flags, src, s_user, ga, G - ga, work, g.fork->side);
-    if (e == hipSuccess) e = launch_mask_eval(g, L, K, plan, ga, G - ga, work, g.fork->side);
+    if (e == hipSuccess) e = launch_mask_eval(g, L, K, plan, src, ga, G - ga, work, g.fork->side);
     if (e == hipSuccess) e = hipEventRecord(g.fork->joined, g.fork->side);
     // the first chunk's evaluate is enqueued whatever happened above, and the
     // caller's stream always waits for what the side stream was given
-    hipError_t e2 = launch_mask_eval(g, L, K, plan, 0, ga, work, stream);
+    hipError_t e2 = launch_mask_eval(g, L, K, plan, src, 0, ga, work, stream);
     hipError_t e3 = hipStreamWaitEvent(stream, g.fork->joined, 0);
     return e != hipSuccess ? e : e2 != hipSuccess ? e2 : e3;
   }
