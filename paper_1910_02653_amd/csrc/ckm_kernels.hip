@@ -1597,13 +1597,16 @@ __host__ __device__ __forceinline__ size_t mrow_off(int t) {
 //      ref: far reference to the dependency's later user
 //      An absent slot has lm = 0 and no far reference: it frees nothing, its
 //      size being 0.
-//   6: for node v-1, the byte offsets in a mask row of the S_{t+1} words of
-//      its slot 0 and 1 dependencies (low and high half; 0 for an absent
-//      slot), fetched one node ahead
-//   7: the gate, the least of the node's three far references (words 1, 3
-//      and 5), or 0 when the node has more than two dependencies: when it is
-//      at or above the stage's limit (t + 1) << 16, the node is decided in a
-//      form without far lookups or rare slots.
+//   6: for node v-1, the byte offset in a mask row of the S_{t+1} word of
+//      its slot 0 dependency (0 for an absent slot), fetched one node ahead
+//   7: high half: the gate, the high half of the least of the node's three
+//      far references (words 1, 3 and 5), or 0 when the node has more than
+//      two dependencies: when the word is at or above the stage's limit
+//      (t + 1) << 16, the node is decided in a form without far lookups or
+//      rare slots (the limit's low half is 0, so the low half of the word
+//      never decides). Low half: for node v-1, the byte offset of its slot 1
+//      dependency's S_{t+1} word, as word 6. (Both offsets in word 6 cost a
+//      shift and a mask per node.)
 //   8-15: binary64 M_v, C_v, M of slots 0 and 1, used from scalar registers
 //      (the vector registers they would take are worth a wave per SIMD)
 // Pairs of nodes are aligned (nodes 2c, 2c+1). A stage's scan starts at the
@@ -1776,11 +1779,10 @@ __device__ __forceinline__ uint32_t after_record(uint32_t x, uint32_t word) {
 // for it.
 __device__ __forceinline__ MNode mask_fetch(const MaskArgs& a, const u32x16& rec_v, cptr<uint64_t> s1row,
                                             uint32_t off) {
-  const uint32_t f = rec_v[6];
   MNode nx;
   nx.rec = sload<u32x16>(a.mnodes, off);
-  nx.d0 = sload<uint64_t>(s1row, f & 0xFFFFu);
-  nx.d1 = sload<uint64_t>(s1row, f >> 16);
+  nx.d0 = sload<uint64_t>(s1row, rec_v[6]);
+  nx.d1 = sload<uint64_t>(s1row, rec_v[7] & 0xFFFFu);
   return nx;
 }
 
@@ -2917,21 +2919,23 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
       put(sl < 2 ? r + 12 + 2 * sl : m23 + 2 * (sl - 2), (double)M[i]);
     }
     r[1] = ctrl;
-    // the gate: below the stage's limit when a far reference may apply
-    r[7] = (ctrl & kMRare) ? 0u : std::min(ctrl, std::min(r[3], r[5]));
+    // the gate: below the stage's limit when a far reference may apply (the
+    // low half takes node v-1's slot 1 offset below)
+    r[7] = (ctrl & kMRare) ? 0u : std::min(ctrl, std::min(r[3], r[5])) & 0xFFFF0000u;
   }
   // fetch lists: record v (padded ones included) names the S_{t+1} words of
-  // node v-1's slots 0 and 1
+  // node v-1's slots 0 (word 6) and 1 (low half of word 7)
   for (int32_t v = 1; v < np; ++v) {
     const int32_t u = v - 1;
-    uint32_t f = 0;
+    uint32_t f0 = 0, f1 = 0;
     if (u < n) {
       const int nd = dep_ptr[u + 1] - dep_ptr[u];
-      if (nd >= 1) f |= (uint32_t)dep_idx[dep_ptr[u]] * 8u;
-      if (nd >= 2) f |= (uint32_t)dep_idx[dep_ptr[u] + 1] * 8u << 16;
+      if (nd >= 1) f0 = (uint32_t)dep_idx[dep_ptr[u]] * 8u;
+      if (nd >= 2) f1 = (uint32_t)dep_idx[dep_ptr[u] + 1] * 8u;
     }
     uint32_t* r = reinterpret_cast<uint32_t*>(base + (size_t)v * kMNodeBytes);
-    r[6] = f;
+    r[6] = f0;
+    r[7] = (r[7] & 0xFFFF0000u) | f1;
   }
   return true;   // node 0 keeps fetch list 0
 }
