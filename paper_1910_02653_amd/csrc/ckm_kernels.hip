@@ -1107,6 +1107,7 @@ __global__ void __launch_bounds__(256) ckm_quantize_kernel(const double* __restr
                                                            int32_t* __restrict__ nan_row) {
   __shared__ int any_nan;
   const int r = blockIdx.x;
+  if (r >= n) return;   // the grid has one block per row
   if (threadIdx.x == 0) any_nan = 0;
   __syncthreads();
   int my_nan = 0;
@@ -1171,6 +1172,7 @@ __global__ void __launch_bounds__(256) ckm_threshold_key_kernel(const double* __
                                                                 int32_t* __restrict__ nan_row) {
   __shared__ int any_nan;
   const int r = blockIdx.x;
+  if (r >= n) return;   // the grid has one block per row
   if (threadIdx.x == 0) any_nan = 0;
   __syncthreads();
   int my_nan = 0;
@@ -1243,7 +1245,7 @@ __global__ void __launch_bounds__(256) ckm_reduce_kernel(int32_t K, const int64_
   sb[threadIdx.x] = b;
   __syncthreads();
   for (int off = blockDim.x / 2; off > 0; off >>= 1) {
-    if (threadIdx.x < off && better(sb[threadIdx.x + off], sb[threadIdx.x]))
+    if ((int)threadIdx.x < off && better(sb[threadIdx.x + off], sb[threadIdx.x]))
       sb[threadIdx.x] = sb[threadIdx.x + off];
     __syncthreads();
   }
@@ -1266,7 +1268,7 @@ __global__ void __launch_bounds__(256) ckm_argmin_kernel(int32_t nblocks, const 
   __syncthreads();
   if (nan) atomicOr(&any_nan, 1);
   for (int off = blockDim.x / 2; off > 0; off >>= 1) {
-    if (threadIdx.x < off && better(sb[threadIdx.x + off], sb[threadIdx.x]))
+    if ((int)threadIdx.x < off && better(sb[threadIdx.x + off], sb[threadIdx.x]))
       sb[threadIdx.x] = sb[threadIdx.x + off];
     __syncthreads();
   }
@@ -1306,7 +1308,7 @@ __global__ void __launch_bounds__(1024) ckm_select_kernel(int32_t K, const int64
   __syncthreads();
   if (nan) atomicOr(&any_nan, 1);
   for (int off = blockDim.x / 2; off > 0; off >>= 1) {
-    if (threadIdx.x < off && better(sb[threadIdx.x + off], sb[threadIdx.x]))
+    if ((int)threadIdx.x < off && better(sb[threadIdx.x + off], sb[threadIdx.x]))
       sb[threadIdx.x] = sb[threadIdx.x + off];
     __syncthreads();
   }
@@ -1356,7 +1358,7 @@ __global__ void __launch_bounds__(256) ckm_batch_kernel(int32_t K, const int64_t
   sb[threadIdx.x] = b;
   __syncthreads();
   for (int off = blockDim.x / 2; off > 0; off >>= 1) {
-    if (threadIdx.x < off && better_b(sb[threadIdx.x + off], sb[threadIdx.x])) sb[threadIdx.x] = sb[threadIdx.x + off];
+    if ((int)threadIdx.x < off && better_b(sb[threadIdx.x + off], sb[threadIdx.x])) sb[threadIdx.x] = sb[threadIdx.x + off];
     __syncthreads();
   }
   if (threadIdx.x == 0) block_best[blockIdx.x] = sb[0];
@@ -1379,7 +1381,7 @@ __global__ void __launch_bounds__(256) ckm_batch_argmax_kernel(int32_t nblocks, 
   __syncthreads();
   if (nan) atomicOr(&any_nan, 1);
   for (int off = blockDim.x / 2; off > 0; off >>= 1) {
-    if (threadIdx.x < off && better_b(sb[threadIdx.x + off], sb[threadIdx.x])) sb[threadIdx.x] = sb[threadIdx.x + off];
+    if ((int)threadIdx.x < off && better_b(sb[threadIdx.x + off], sb[threadIdx.x])) sb[threadIdx.x] = sb[threadIdx.x + off];
     __syncthreads();
   }
   if (threadIdx.x == 0) {
@@ -1636,9 +1638,6 @@ struct MaskArgs {
   int32_t g0;                                 // group of blockIdx.x = 0
 };
 
-__device__ __forceinline__ uint64_t mpair(const u32x8& b, int p) {
-  return (uint64_t)b[2 * p] | ((uint64_t)b[2 * p + 1] << 32);
-}
 __device__ __forceinline__ bool lane_of(uint64_t m) { return __builtin_amdgcn_inverse_ballot_w64(m); }
 __device__ __forceinline__ uint64_t mask_of(bool b) { return __builtin_amdgcn_ballot_w64(b); }
 // acc + [lane's bit of m] * x, one masked binary64 update
@@ -1883,9 +1882,13 @@ __global__ void __launch_bounds__(kWave) ckm_mask_eval_kernel(MaskArgs a) {
   if (group == 0 && item == 0 && lane == 0) a.hdr[0] = a.items;
 }
 
+}  // namespace
 // v_writelane_b32 through its compiler intrinsic, so that the compiler sees
-// the instruction and its hazards (this compiler has no builtin for it).
+// the instruction and its hazards (this compiler has no builtin for it). The
+// declaration binds a name to the intrinsic, so it stays outside the unnamed
+// namespace: there it would name an internal function that is never defined.
 __device__ int amdgcn_writelane(int x, int lane, int v) __asm("llvm.amdgcn.writelane.i32");
+namespace {
 // Lane L of v takes the wave-uniform x.
 template <int L>
 __device__ __forceinline__ uint32_t write_lane(uint32_t v, uint32_t x) {
