@@ -14,10 +14,11 @@ Prints one JSON line. `value` is candidate schedules evaluated per second.
 `roofline` prices the dominant kernel (the evaluate kernel) against HBM
 bandwidth with the algorithmic bytes of bit-packed S and R rows, each
 written once and read once: 4 * n * ceil(n/64) * 8 bytes per candidate.
-`roofline_alu` prices the same launch against the vector ALU issue rate that
-actually bounds it: VALU instructions per launch (committed rocprofv3
-counters of the current kernel source, else null) x 64 lanes / the launch
-time, against 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz.
+`roofline_alu` prices the same launch against the vector ALU issue rate:
+VALU instructions per launch (committed rocprofv3 counters of the current
+kernel source, else null) x 64 lanes / the launch time, against 256 CUs x 4
+SIMDs x 16 lanes x 2.4 GHz. (The kernel's own limit is its scalar issue and
+the round trip of each node's loads; the vector unit is about 70 % busy.)
 `roofline_step` prices the whole timed step with the same bytes.
 `cpu_baseline` times the CPU oracle on a bounded sample of the same
 workload (about 15 s of wall time, whole passes over the candidates), on the host threads a one-GPU job is
@@ -27,7 +28,8 @@ CPU count and the affinity set recorded.
 `hbm_copy` is the bandwidth a plain device copy reaches on the same GPU, the
 achievable line beside the 8 TB/s peak. `host_round_trip` times the
 synchronous call that takes S* from host memory and returns host results
-(PCIe transfers and the call's own work-buffer allocation included). `supplied_schedules` times the batch evaluation of K given integral
+(PCIe transfers and the call's own copies included; its buffers stay on
+the graph between calls). `supplied_schedules` times the batch evaluation of K given integral
 checkpoint matrices (banded, 30 % of values kept) on the same graph: Algorithm
 2 repair, simulation, argmin and the best R, with the matrices resident in HBM.
 `threshold_family` times K deterministic candidates [clamp(S*) > p_k] on an
