@@ -39,8 +39,9 @@ argmin and the best S and R.
 every candidate (budget 3x the median activation peak, cost cap at the
 median cost) on the same workload.
 `pipelined` times the same steps over two work buffers, a step's thresholds
-and rounding on a second stream beside the previous step's evaluation (which
-leaves vector ALU slots free), timed by events around the whole loop only:
+and rounding on a second stream beside the previous step's evaluation (whose
+tail, and the small kernels, leave room for it), timed by events around the
+whole loop only:
 per-step timing events on the main stream stop the two from overlapping.
 `feasible_budget` times the same step at the median-peak budget, where
 select also writes the best candidate's S and R rows.
