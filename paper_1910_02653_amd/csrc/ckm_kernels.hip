@@ -2060,8 +2060,13 @@ __global__ void __launch_bounds__(kWave) ckm_round_masks_kernel(const uint32_t* 
 // it), and when a user v of x looks for users of x computed after v, the bit
 // holds those of x's far users above v (a far user within 32 above v is also
 // in v's R window). Near users stay in the window, as in the mask path. The
-// seen bits are numbered over the nodes that have a far user: W words per
-// lane in LDS (word w of lane j at byte 256 w + 4 j), cleared at each stage.
+// seen bits are numbered over the nodes that have a far user, in order of
+// their first far user: W words per lane in LDS (word w of lane j at byte
+// 256 w + 4 j), cleared at each stage. Stage t writes only bits of nodes
+// whose first far user is at most t, a prefix of that order, so the stages
+// below a split point need only the first words: they run in a launch of
+// their own with that much LDS (more waves per CU), where every read past
+// those words lands on one more word that stays zero.
 //
 // Node v's data, 128 bytes at 128 v (v = 0 .. n; node n has only the fetch
 // block for node n-1):
@@ -2094,12 +2099,16 @@ __global__ void __launch_bounds__(kWave) ckm_round_masks_kernel(const uint32_t* 
 // All loads for node v-1 take their addresses from node v's record, so they
 // are issued after it has arrived, one batch per node.
 constexpr int kSNodeBytes = 128;
+// Graphs with fewer seen words run every stage in one launch.
+constexpr int32_t kSeenSplitMinWords = 16;
 constexpr uint32_t kSExt = 1u, kSOver = 2u, kSWrite = 0x8000u, kSExtNext = 0x8000u;
 
 struct SeenArgs {
   int32_t n, K, items, kind, P, T0, R1, R2;   // work plan (see Plan)
   int32_t np;                                 // node data entries: n + 1
-  int32_t seen_words;                         // W
+  int32_t seen_words;                         // LDS words per lane of this launch
+  uint32_t seen_lim;                          // byte offset of its last word: reads clamp to it
+  int32_t item0;                              // work item of blockIdx.y = 0
   double base;                                // M_in + 2 M_param
   size_t mgroup;                              // words of one group's mask rows
   cptr<uint64_t> mrows;                       // S masks, group-major
@@ -2118,8 +2127,8 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t snode_rsrc(const SeenArgs& a) 
                                            kBufWord3);
 }
 // The lane's word at LDS byte offset off (off wave-uniform, a multiple of 256).
-__device__ __forceinline__ uint32_t seen_read(char* lds_lane, uint32_t off) {
-  return *reinterpret_cast<const uint32_t*>(lds_lane + off);
+__device__ __forceinline__ uint32_t seen_read(const SeenArgs& a, char* lds_lane, uint32_t off) {
+  return *reinterpret_cast<const uint32_t*>(lds_lane + min(off, a.seen_lim));
 }
 __device__ __forceinline__ void seen_or(char* lds_lane, uint32_t off, uint32_t bits) {
   atomicOr(reinterpret_cast<uint32_t*>(lds_lane + off), bits);
@@ -2148,9 +2157,9 @@ __device__ __forceinline__ SNode seen_fetch(const SeenArgs& a, const u32x16& rec
   const auto rs = snode_rsrc(a);
   nx.mc = load_mval<64>(rs, off);
   nx.dm = load_mval<80>(rs, off);
-  nx.sv = seen_read(lds_lane, rec_v[12] & 0xFFFFu);
-  nx.s0 = seen_read(lds_lane, rec_v[12] >> 16);
-  nx.s1 = seen_read(lds_lane, rec_v[13] & 0xFFFFu);
+  nx.sv = seen_read(a, lds_lane, rec_v[12] & 0xFFFFu);
+  nx.s0 = seen_read(a, lds_lane, rec_v[12] >> 16);
+  nx.s1 = seen_read(a, lds_lane, rec_v[13] & 0xFFFFu);
   nx.has_ext = f01 & kSExtNext;
   if (nx.has_ext) {
     const uint32_t f23 = rec_v[10];
@@ -2158,8 +2167,8 @@ __device__ __forceinline__ SNode seen_fetch(const SeenArgs& a, const u32x16& rec
     nx.d3 = sload<uint64_t>(s1row, f23 >> 16);
     nx.ext = sload<u32x4>(a.snodes, off + 112);
     nx.dm2 = load_mval<96>(rs, off);
-    nx.s2 = seen_read(lds_lane, rec_v[13] >> 16);
-    nx.s3 = seen_read(lds_lane, rec_v[14]);
+    nx.s2 = seen_read(a, lds_lane, rec_v[13] >> 16);
+    nx.s3 = seen_read(a, lds_lane, rec_v[14]);
   }
   return nx;
 }
@@ -2216,7 +2225,7 @@ __device__ __forceinline__ void seen_node(const SeenArgs& a, const SNode& nd, cp
     for (uint32_t c = 0, e = r[8]; c < cnt; ++c, ++e) {
       const u32x8 en = a.over[e];
       const uint64_t s1i = sload<uint64_t>(s1row, en[3]);
-      const uint32_t sw = seen_read(lds_lane, en[4]);
+      const uint32_t sw = seen_read(a, lds_lane, en[4]);
       val = seen_slot(val, R, rb, en[0], en[1], sw, s1i, dbl(en[5], en[6]), sc.Rwin, en[2], lds_lane);
     }
   }
@@ -2245,7 +2254,7 @@ __global__ void __launch_bounds__(kWave) ckm_seen_eval_kernel(SeenArgs a) {
   extern __shared__ uint32_t seen_lds[];
   const int lane = threadIdx.x;
   const int group = blockIdx.x + a.g0;
-  const int item = blockIdx.y;
+  const int item = blockIdx.y + a.item0;
   const uint32_t k = (uint32_t)(group * kWave + lane);
   char* lds_lane = reinterpret_cast<char*>(seen_lds) + 4 * lane;
   int t0, t1;
@@ -2579,7 +2588,6 @@ static hipError_t launch_mask_eval(const ckm_graph& g, const Layout& L, int32_t 
     m.R1 = plan.R1;
     m.R2 = plan.R2;
     m.np = g.n + 1;
-    m.seen_words = g.seen_words;
     m.base = (double)g.base;
     m.mgroup = mask_rows_words(g.n);
     m.mrows = as_const(at<const uint64_t>(work, L.rows_off));
@@ -2591,13 +2599,29 @@ static hipError_t launch_mask_eval(const ckm_graph& g, const Layout& L, int32_t 
     m.part_cost = at<int64_t>(work, L.part_cost_off);
     m.hdr = at<int32_t>(work, L.hdr_off);
     m.g0 = g0;
-    if (skip)
-      hipLaunchKernelGGL(ckm_seen_eval_kernel<true>, dim3(gn, plan.items), dim3(kWave),
-                         (size_t)g.seen_words * 256, stream, m);
-    else
-      hipLaunchKernelGGL(ckm_seen_eval_kernel<false>, dim3(gn, plan.items), dim3(kWave),
-                         (size_t)g.seen_words * 256, stream, m);
-    return hipGetLastError();
+    // items [i0, i0 + ni) with `words` LDS words per lane, reads clamped to
+    // the last of them
+    auto launch = [&](int32_t i0, int32_t ni, int32_t words) {
+      m.item0 = i0;
+      m.seen_words = words;
+      m.seen_lim = (uint32_t)(words - 1) * 256u;
+      if (skip)
+        hipLaunchKernelGGL(ckm_seen_eval_kernel<true>, dim3(gn, ni), dim3(kWave), (size_t)words * 256, stream, m);
+      else
+        hipLaunchKernelGGL(ckm_seen_eval_kernel<false>, dim3(gn, ni), dim3(kWave), (size_t)words * 256, stream, m);
+      return hipGetLastError();
+    };
+    // The single-stage items of the stages at or above the split point come
+    // first (items are numbered from stage n-1 down); the rest, stages below
+    // it, touch only the first seen_low_words words, plus one that stays zero.
+    const int32_t t_s = g.seen_split_t;
+    if (t_s > 0 && plan.kind == 1 && plan.P == 1 && t_s >= plan.T0 && t_s < g.n) {
+      const int32_t na = g.n - t_s;
+      hipError_t e = launch(0, na, g.seen_words);
+      if (e == hipSuccess) e = launch(na, plan.items - na, g.seen_low_words + 1);
+      return e;
+    }
+    return launch(0, plan.items, g.seen_words);
   }
   MaskArgs m;
   m.n = g.n;
@@ -2945,18 +2969,33 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
 
 bool build_seen_records(int32_t n, const int64_t* M, const int64_t* C, const int32_t* dep_ptr,
                         const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx,
-                        std::vector<char>& nodes, std::vector<uint32_t>& over, int32_t& seen_words) {
+                        std::vector<char>& nodes, std::vector<uint32_t>& over, int32_t& seen_words,
+                        int32_t& split_t, int32_t& low_words) {
   if (n < 1 || n > kSeenMaxNodes) return false;
-  // seen bits: the nodes with a user more than 32 above them, in order
-  std::vector<int32_t> slot(n, -1);
-  int32_t ns = 0;
-  for (int32_t x = 0; x < n; ++x)
+  // seen bits: the nodes with a user more than 32 above them, in order of
+  // their first such user (then of the node)
+  std::vector<int32_t> first(n, INT32_MAX);
+  std::vector<int32_t> order;
+  for (int32_t x = 0; x < n; ++x) {
     for (int32_t e = user_ptr[x]; e < user_ptr[x + 1]; ++e)
-      if (user_idx[e] - x - 1 >= 32) {
-        slot[x] = ns++;
-        break;
-      }
+      if (user_idx[e] - x - 1 >= 32) first[x] = std::min(first[x], user_idx[e]);
+    if (first[x] != INT32_MAX) order.push_back(x);
+  }
+  std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) { return first[x] < first[y]; });
+  std::vector<int32_t> slot(n, -1);
+  const int32_t ns = (int32_t)order.size();
+  for (int32_t i = 0; i < ns; ++i) slot[order[i]] = i;
   seen_words = std::max<int32_t>(1, (ns + 31) / 32);
+  // stages t < split_t write only bits of nodes whose first far user is
+  // below split_t: the first 32 low_words bits when split_t is the first far
+  // user of bit 32 low_words. Half the words, where that is worth a launch.
+  split_t = 0;
+  low_words = 0;
+  if (seen_words >= kSeenSplitMinWords) {
+    const int32_t lw = seen_words / 2;
+    split_t = first[order[32 * lw]];
+    low_words = lw;
+  }
   auto soff = [&](int32_t x) { return slot[x] < 0 ? 0u : (uint32_t)(slot[x] >> 5) * 256u; };
   auto sbit = [&](int32_t x) { return slot[x] < 0 ? 0u : 1u << (slot[x] & 31); };
   const int32_t np = n + 1;
