@@ -476,10 +476,10 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
   // else the seen path's node data, when the graph fits it
   std::vector<char> snodes;
   std::vector<uint32_t> sover;
-  int32_t seen_words = 0, seen_split_t = 0, seen_low_words = 0;
+  int32_t seen_words = 0, seen_tiers = 0, seen_tier_t[2] = {0, 0}, seen_tier_w[2] = {0, 0};
   if (mrecs.empty() && !wide &&
       !ckm::build_seen_records(n, bytes, cost, dp.data(), di.data(), up.data(), ui.data(), snodes, sover,
-                               seen_words, seen_split_t, seen_low_words))
+                               seen_words, seen_tier_t, seen_tier_w, seen_tiers))
     snodes.clear();
   const size_t off_snode = align256(off_mrec + mrecs.size());
   const size_t off_sover = align256(off_snode + snodes.size());
@@ -543,8 +543,11 @@ static ckm_status graph_create(int32_t n, const int32_t* dep_ptr, const int32_t*
   g->d_snodes = snodes.empty() ? nullptr : base + off_snode;
   g->d_sover = snodes.empty() || sover.empty() ? nullptr : base + off_sover;
   g->seen_words = seen_words;
-  g->seen_split_t = seen_split_t;
-  g->seen_low_words = seen_low_words;
+  g->seen_tiers = seen_tiers;
+  for (int i = 0; i < 2; ++i) {
+    g->seen_tier_t[i] = seen_tier_t[i];
+    g->seen_tier_w[i] = seen_tier_w[i];
+  }
   g->sync = new (std::nothrow) ckm::SyncCache;
   if (!g->sync) {
     (void)hipFree(g->d_mem);

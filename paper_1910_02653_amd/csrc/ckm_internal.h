@@ -41,8 +41,11 @@ struct ckm_graph {
   const void* d_snodes = nullptr; // else the seen path's node data, when the graph fits it
   const void* d_sover = nullptr;  // and its overflow entries (NULL when there are none)
   int32_t seen_words = 0;         // seen bits per lane / 32 on the seen path
-  int32_t seen_split_t = 0;       // stages below it touch only the first seen_low_words words (0: no split)
-  int32_t seen_low_words = 0;
+  // seen-path launches by stage: the stages below seen_tier_t[i] touch only
+  // the first seen_tier_w[i] words (seen_tiers of them, split stages falling)
+  int32_t seen_tiers = 0;
+  int32_t seen_tier_t[2] = {0, 0};
+  int32_t seen_tier_w[2] = {0, 0};
   ckm::SyncCache* sync = nullptr;  // reused by the synchronous calls; freed with the graph
   ckm::Fork* fork = nullptr;       // NULL: every launch on the caller's stream
 };
@@ -88,14 +91,14 @@ bool build_mask_records(int32_t n, const int64_t* M, const int64_t* C, const int
 size_t mask_rows_words(int32_t n);
 // Node data of the seen path (see ckm_kernels.hip) for graphs of up to
 // kSeenMaxNodes nodes: (n + 1) x 128 bytes, the overflow entries (8 dwords
-// each) and the seen words per lane; false when n is too large. split_t and
-// low_words: the stages below split_t touch only the first low_words seen
-// words (split_t = 0 when a split would not pay).
+// each) and the seen words per lane; false when n is too large. tier_t and
+// tier_w (ntiers entries, at most 2): the stages below tier_t[i] touch only
+// the first tier_w[i] seen words (no tiers where they would not pay).
 constexpr int32_t kSeenMaxNodes = 4096;
 bool build_seen_records(int32_t n, const int64_t* M, const int64_t* C, const int32_t* dep_ptr,
                         const int32_t* dep_idx, const int32_t* user_ptr, const int32_t* user_idx,
                         std::vector<char>& nodes, std::vector<uint32_t>& over, int32_t& seen_words,
-                        int32_t& split_t, int32_t& low_words);
+                        int32_t tier_t[2], int32_t tier_w[2], int32_t& ntiers);
 // Resident waves per CU of the mask and seen evaluate kernels.
 int32_t mask_waves_per_cu();
 int32_t seen_waves_per_cu(int32_t seen_words);
