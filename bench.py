@@ -88,7 +88,7 @@ def measured_counters():
     return d
 
 
-# Host threads granted to one GPU's job on the GPU machines this runs on.
+# Host threads a one-GPU job is granted on the machines it runs on.
 HOST_THREADS_PER_GPU = 16
 
 
@@ -506,7 +506,7 @@ def main():
                     help="timed calls of the largest-batch search (0 = skip)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
               "(candidates would shard across GPUs with one small all-gather; not built)", file=sys.stderr)
         sys.exit(2)
 
